@@ -1,0 +1,317 @@
+/*
+ * CPU ORACLE for the LSM-GNN feature-gather cache -- TEST INFRASTRUCTURE ONLY.
+ * Plain sequential C; every step follows the definition in the order the
+ * paper's design section gives it (citations per function).  No blocking, no
+ * parallelism, no shared code with the GPU library.
+ *
+ * Readings of points the paper leaves open (each is listed in the design notes
+ * of the repository):
+ *   - requests are deduplicated and served in ascending node-ID order;
+ *   - the output holds one row per unique ID, ascending, plus an inverse index;
+ *   - set(x) = fastrange(high 32 bits of SplitMix64(x), S): the output of a
+ *     SplitMix64 generator seeded with x, reduced with Lemire's multiply-shift;
+ *   - reuse "dynamic value" is read as the distance d from the current gather to
+ *     the next announced use; d <= T is the kept "near" level, T < d <= L the
+ *     "far" level; T defaults to max(1, floor(L/8));
+ *   - the dynamic information is exact at every gather (refresh period 1);
+ *   - "recently inserted" = inserted during the current gather;
+ *   - ties at equal level and equal static score go to the lowest way index,
+ *     and empty ways are always filled first, lowest index first;
+ *   - the victim buffer is one FIFO ring of V entries that overwrites its
+ *     oldest entry; lines in the far or near level are enqueued, others are
+ *     dropped; a victim hit removes the entry and refills the line through the
+ *     normal fill path; V > 0 turns on the swapped (PVP) level order.
+ */
+#include "oracle.h"
+
+#include <stdlib.h>
+#include <string.h>
+
+#define EMPTY 0xffffffffu
+
+/* dynamic classes of a resident line */
+enum { CLS_N = 0, CLS_F = 1, CLS_R = 2, CLS_C = 3 };
+
+typedef struct {
+  int64_t *ids; /* sorted, unique */
+  uint64_t n;
+} ann_list;
+
+struct orc_cache {
+  uint64_t num_nodes, num_sets, victim_rows;
+  uint32_t row_bytes, ways, lookahead, near_thr;
+  const unsigned char *store;
+  uint32_t *stat;    /* static score per node (copied) */
+  uint32_t *tag;     /* [num_sets][ways] */
+  int64_t *ins;      /* [num_sets][ways] gather index at insertion */
+  uint32_t *vtag;    /* [victim_rows] */
+  int64_t *where;    /* [num_nodes] ring slot holding the node, or -1 */
+  uint64_t tail;     /* total enqueues ever */
+  ann_list *ann;     /* announced batches, index j */
+  uint64_t n_ann, cap_ann;
+  uint64_t t;        /* completed gathers */
+  orc_counts last, total;
+};
+
+/* SplitMix64 (Steele, Lea, Flood 2014): first output of the generator whose
+   state is x, then Lemire's fastrange on its high 32 bits. */
+uint64_t orc_set_of(uint64_t x, uint64_t num_sets) {
+  uint64_t z = x + 0x9e3779b97f4a7c15ULL;
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;
+  z = z ^ (z >> 31);
+  return ((z >> 32) * num_sets) >> 32;
+}
+
+static int cmp_i64(const void *a, const void *b) {
+  int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
+  return (x > y) - (x < y);
+}
+
+/* sorted unique copy of ids */
+static int64_t *sorted_unique(const int64_t *ids, uint64_t n, uint64_t *m) {
+  int64_t *u = (int64_t *)malloc((n ? n : 1) * sizeof(int64_t));
+  if (!u) return NULL;
+  memcpy(u, ids, n * sizeof(int64_t));
+  qsort(u, n, sizeof(int64_t), cmp_i64);
+  uint64_t w = 0;
+  for (uint64_t i = 0; i < n; ++i)
+    if (w == 0 || u[w - 1] != u[i]) u[w++] = u[i];
+  *m = w;
+  return u;
+}
+
+static int contains(const ann_list *l, int64_t x) {
+  return l->n && bsearch(&x, l->ids, l->n, sizeof(int64_t), cmp_i64) != NULL;
+}
+
+int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const uint32_t *static_score,
+               uint64_t num_sets, uint32_t ways, uint64_t victim_rows, uint32_t lookahead,
+               uint32_t near_threshold, orc_cache **out) {
+  if (!out || !static_score) return ORC_E_INVAL;
+  *out = NULL;
+  if (num_nodes == 0 || num_nodes > 0xffffffffULL || row_bytes == 0 || row_bytes % 16 != 0 ||
+      num_sets == 0 || num_sets > 0xffffffffULL || ways == 0 || lookahead > 31)
+    return ORC_E_INVAL;
+  orc_cache *c = (orc_cache *)calloc(1, sizeof(orc_cache));
+  if (!c) return ORC_E_NOMEM;
+  c->num_nodes = num_nodes;
+  c->num_sets = num_sets;
+  c->victim_rows = victim_rows;
+  c->row_bytes = row_bytes;
+  c->ways = ways;
+  c->lookahead = lookahead;
+  /* Sec. 4.2: the default threshold is one eighth of the window; at least 1 */
+  c->near_thr = near_threshold ? near_threshold : (lookahead / 8 > 1 ? lookahead / 8 : 1);
+  c->store = (const unsigned char *)store;
+  c->stat = (uint32_t *)malloc(num_nodes * sizeof(uint32_t));
+  c->tag = (uint32_t *)malloc(num_sets * ways * sizeof(uint32_t));
+  c->ins = (int64_t *)malloc(num_sets * ways * sizeof(int64_t));
+  c->vtag = (uint32_t *)malloc((victim_rows ? victim_rows : 1) * sizeof(uint32_t));
+  c->where = (int64_t *)malloc(num_nodes * sizeof(int64_t));
+  if (!c->stat || !c->tag || !c->ins || !c->vtag || !c->where) { orc_destroy(c); return ORC_E_NOMEM; }
+  memcpy(c->stat, static_score, num_nodes * sizeof(uint32_t));
+  for (uint64_t i = 0; i < num_sets * ways; ++i) { c->tag[i] = EMPTY; c->ins[i] = -1; }
+  for (uint64_t k = 0; k < victim_rows; ++k) c->vtag[k] = EMPTY;
+  for (uint64_t v = 0; v < num_nodes; ++v) c->where[v] = -1;
+  *out = c;
+  return ORC_OK;
+}
+
+void orc_destroy(orc_cache *c) {
+  if (!c) return;
+  for (uint64_t j = 0; j < c->n_ann; ++j) free(c->ann[j].ids);
+  free(c->ann);
+  free(c->stat); free(c->tag); free(c->ins); free(c->vtag); free(c->where);
+  free(c);
+}
+
+uint32_t orc_near_threshold(const orc_cache *c) { return c->near_thr; }
+
+/* Window buffering (Sec. 4, overview; Sec. 4.2): the k-th call announces the
+   sampled list of minibatch k.  At most L minibatches beyond the current one
+   may be known ahead. */
+int orc_advance(orc_cache *c, const int64_t *ids, uint64_t n) {
+  if (!c || (n && !ids)) return ORC_E_INVAL;
+  uint64_t j = c->n_ann;
+  if (j > c->t + c->lookahead) return ORC_E_WINDOW;
+  for (uint64_t i = 0; i < n; ++i)
+    if (ids[i] < 0 || (uint64_t)ids[i] >= c->num_nodes) return ORC_E_RANGE;
+  if (c->n_ann == c->cap_ann) {
+    uint64_t nc = c->cap_ann ? 2 * c->cap_ann : 64;
+    ann_list *na = (ann_list *)realloc(c->ann, nc * sizeof(ann_list));
+    if (!na) return ORC_E_NOMEM;
+    c->ann = na;
+    c->cap_ann = nc;
+  }
+  ann_list l = {NULL, 0};
+  if (j > c->t) { /* a list for a minibatch already being served is never consulted */
+    l.ids = sorted_unique(ids, n, &l.n);
+    if (!l.ids) return ORC_E_NOMEM;
+  }
+  c->ann[c->n_ann++] = l;
+  return ORC_OK;
+}
+
+/* Dynamic information (Sec. 4.2): the class of the line in way w of set s while
+   gather t is served.  Lines inserted during gather t have no reuse
+   information yet ("recently inserted").  Otherwise the announced lists of the
+   next L minibatches are scanned for the line's node: none -> no reuse; the
+   nearest use at distance d <= T -> near; T < d <= L -> far. */
+static int line_class(const orc_cache *c, uint64_t s, uint32_t w) {
+  uint64_t i = s * c->ways + w;
+  if (c->ins[i] == (int64_t)c->t) return CLS_R;
+  for (uint64_t d = 1; d <= c->lookahead; ++d) {
+    uint64_t j = c->t + d;
+    if (j < c->n_ann && contains(&c->ann[j], (int64_t)c->tag[i]))
+      return d <= c->near_thr ? CLS_C : CLS_F;
+  }
+  return CLS_N;
+}
+
+/* Eviction priority, lowest level evicted first.  Hybrid order (Sec. 4.2):
+   no reuse < far < recently inserted < near.  With the victim buffer enabled the
+   two lowest levels swap (Sec. 4.3.2): far < no reuse < recent < near. */
+static int level_of(const orc_cache *c, int cls) {
+  if (c->victim_rows > 0) {
+    switch (cls) {
+      case CLS_F: return 0;
+      case CLS_N: return 1;
+      case CLS_R: return 2;
+      default: return 3;
+    }
+  }
+  switch (cls) {
+    case CLS_N: return 0;
+    case CLS_F: return 1;
+    case CLS_R: return 2;
+    default: return 3;
+  }
+}
+
+static void ring_put(orc_cache *c, uint64_t k, uint32_t v) {
+  if (c->vtag[k] != EMPTY) c->where[c->vtag[k]] = -1;
+  c->vtag[k] = v;
+  if (v != EMPTY) c->where[v] = (int64_t)k;
+}
+
+/* Feature aggregation of one minibatch through the cache (Sec. 4 overview,
+   Sec. 4.2, Sec. 4.3.1). */
+int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t *uniq_out, int64_t *inv,
+               uint8_t *outcome, uint64_t *n_unique) {
+  if (!c || (n && !ids)) return ORC_E_INVAL;
+  for (uint64_t i = 0; i < n; ++i)
+    if (ids[i] < 0 || (uint64_t)ids[i] >= c->num_nodes) return ORC_E_RANGE;
+
+  uint64_t U = 0;
+  int64_t *uniq = sorted_unique(ids, n, &U);
+  if (!uniq) return ORC_E_NOMEM;
+  orc_counts st;
+  memset(&st, 0, sizeof st);
+  st.batch = c->t;
+  st.requests = n;
+  st.unique = U;
+
+  for (uint64_t u = 0; u < U; ++u) {
+    uint32_t x = (uint32_t)uniq[u];
+    uint64_t s = orc_set_of(x, c->num_sets);
+    uint32_t *tag = c->tag + s * c->ways;
+    int64_t *ins = c->ins + s * c->ways;
+    int hit = 0;
+    for (uint32_t w = 0; w < c->ways; ++w)
+      if (tag[w] == x) hit = 1;
+    if (hit) {
+      ++st.hits;
+      if (outcome) outcome[u] = ORC_HIT;
+    } else {
+      /* the victim buffer is probed for the line before storage (Sec. 4.3) */
+      if (c->victim_rows && c->where[x] >= 0) {
+        ++st.victim_hits;
+        ring_put(c, (uint64_t)c->where[x], EMPTY);
+        if (outcome) outcome[u] = ORC_VICTIM_HIT;
+      } else {
+        ++st.misses;
+        if (outcome) outcome[u] = ORC_MISS;
+      }
+      /* choose the way: an empty way first, else the lowest level, then the
+         lowest static score, then the lowest way index (Sec. 4.2) */
+      uint32_t pick = c->ways;
+      for (uint32_t w = 0; w < c->ways && pick == c->ways; ++w)
+        if (tag[w] == EMPTY) pick = w;
+      if (pick == c->ways) {
+        int best_lvl = 99;
+        uint32_t best_stat = 0;
+        for (uint32_t w = 0; w < c->ways; ++w) {
+          int lvl = level_of(c, line_class(c, s, w));
+          uint32_t sv = c->stat[tag[w]];
+          if (lvl < best_lvl || (lvl == best_lvl && sv < best_stat)) {
+            best_lvl = lvl;
+            best_stat = sv;
+            pick = w;
+          }
+        }
+        /* evict: a line with reuse information goes to the victim buffer,
+           others are discarded (Sec. 4.3.1) */
+        uint32_t z = tag[pick];
+        int cls = line_class(c, s, pick);
+        ++st.evictions;
+        if (c->victim_rows && (cls == CLS_F || cls == CLS_C)) {
+          ring_put(c, c->tail % c->victim_rows, z);
+          ++c->tail;
+          ++st.enqueued;
+        } else {
+          ++st.dropped;
+        }
+      }
+      tag[pick] = x;
+      ins[pick] = (int64_t)c->t;
+    }
+    /* every served row is the stored row of its node, whatever path served it */
+    if (out && c->store)
+      memcpy((unsigned char *)out + u * c->row_bytes, c->store + (uint64_t)x * c->row_bytes, c->row_bytes);
+  }
+
+  if (uniq_out) memcpy(uniq_out, uniq, U * sizeof(int64_t));
+  if (inv)
+    for (uint64_t i = 0; i < n; ++i) {
+      int64_t *p = (int64_t *)bsearch(&ids[i], uniq, U, sizeof(int64_t), cmp_i64);
+      inv[i] = p - uniq;
+    }
+  free(uniq);
+  if (n_unique) *n_unique = U;
+
+  /* lists of minibatches up to t are never consulted again */
+  if (c->t < c->n_ann) {
+    free(c->ann[c->t].ids);
+    c->ann[c->t].ids = NULL;
+    c->ann[c->t].n = 0;
+  }
+  c->last = st;
+  c->total.batch = st.batch + 1;
+  c->total.requests += st.requests;
+  c->total.unique += st.unique;
+  c->total.hits += st.hits;
+  c->total.victim_hits += st.victim_hits;
+  c->total.misses += st.misses;
+  c->total.evictions += st.evictions;
+  c->total.enqueued += st.enqueued;
+  c->total.dropped += st.dropped;
+  ++c->t;
+  return ORC_OK;
+}
+
+int orc_stats(const orc_cache *c, orc_counts *last, orc_counts *total) {
+  if (!c) return ORC_E_INVAL;
+  if (last) *last = c->last;
+  if (total) *total = c->total;
+  return ORC_OK;
+}
+
+int orc_export_state(const orc_cache *c, uint32_t *tags, uint32_t *ring_tags, uint64_t *ring_tail, uint64_t *t) {
+  if (!c) return ORC_E_INVAL;
+  if (tags) memcpy(tags, c->tag, c->num_sets * c->ways * sizeof(uint32_t));
+  if (ring_tags && c->victim_rows) memcpy(ring_tags, c->vtag, c->victim_rows * sizeof(uint32_t));
+  if (ring_tail) *ring_tail = c->tail;
+  if (t) *t = c->t;
+  return ORC_OK;
+}

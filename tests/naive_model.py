@@ -1,0 +1,93 @@
+"""A deliberately naive brute-force model of the cache policy, used only to
+cross-check the C oracle on tiny inputs.
+
+It is written from the rules of the paper (arXiv 2407.15264, Sec. 4.2 levels and
+static tie-break, Sec. 4.3.1 victim-buffer enqueue, Sec. 4.3.2 level swap) with
+different data structures from the oracle: Python lists of (node, inserted_at)
+pairs per set, the victim ring as a plain list searched linearly, the window as
+the list of announced Python sets scanned at every class query, and victim
+selection by sorting all candidates.  The set-index function is injected.
+"""
+from __future__ import annotations
+
+NEAR, FAR, RECENT, NONE = "near", "far", "recent", "none"
+
+
+class NaiveCache:
+    def __init__(self, num_nodes, num_sets, ways, victim_rows, lookahead, static, set_of,
+                 near_threshold=0):
+        self.N, self.S, self.W, self.V, self.L = num_nodes, num_sets, ways, victim_rows, lookahead
+        self.T = near_threshold or max(1, lookahead // 8)
+        self.static = list(static)
+        self.set_of = set_of
+        self.sets = [[None] * ways for _ in range(num_sets)]  # (node, inserted_at) | None
+        self.ring = [None] * victim_rows
+        self.tail = 0
+        self.announced = []
+        self.t = 0
+
+    def advance(self, ids):
+        if len(self.announced) > self.t + self.L:
+            return "E_WINDOW"
+        if any(not (0 <= x < self.N) for x in ids):
+            return "E_RANGE"
+        self.announced.append(set(int(x) for x in ids))
+        return "OK"
+
+    def _class(self, entry):
+        node, at = entry
+        if at == self.t:
+            return RECENT
+        for d in range(1, self.L + 1):
+            j = self.t + d
+            if j < len(self.announced) and node in self.announced[j]:
+                return NEAR if d <= self.T else FAR
+        return NONE
+
+    def _level(self, cls):
+        order = [FAR, NONE, RECENT, NEAR] if self.V > 0 else [NONE, FAR, RECENT, NEAR]
+        return order.index(cls)
+
+    def gather(self, ids):
+        if any(not (0 <= x < self.N) for x in ids):
+            return "E_RANGE", None
+        uniq = sorted(set(int(x) for x in ids))
+        st = dict(hits=0, victim_hits=0, misses=0, evictions=0, enqueued=0, dropped=0)
+        outcome = []
+        for x in uniq:
+            ways = self.sets[self.set_of(x)]
+            if any(e is not None and e[0] == x for e in ways):
+                st["hits"] += 1
+                outcome.append("H")
+                continue
+            if x in self.ring:
+                self.ring[self.ring.index(x)] = None
+                st["victim_hits"] += 1
+                outcome.append("V")
+            else:
+                st["misses"] += 1
+                outcome.append("M")
+            empties = [w for w, e in enumerate(ways) if e is None]
+            if empties:
+                w = empties[0]
+            else:
+                cands = sorted((self._level(self._class(e)), self.static[e[0]], w)
+                               for w, e in enumerate(ways))
+                w = cands[0][2]
+                cls = self._class(ways[w])
+                st["evictions"] += 1
+                if self.V > 0 and cls in (FAR, NEAR):
+                    self.ring[self.tail % self.V] = ways[w][0]
+                    self.tail += 1
+                    st["enqueued"] += 1
+                else:
+                    st["dropped"] += 1
+            ways[w] = (x, self.t)
+        self.t += 1
+        return "OK", dict(uniq=uniq, outcome="".join(outcome), **st)
+
+    def tags(self):
+        return [[-1 if e is None else e[0] for e in s] for s in self.sets]
+
+    def ring_tags(self):
+        return [-1 if r is None else r for r in self.ring]

@@ -1,0 +1,326 @@
+"""Pins for the CPU oracle (no GPU).
+
+The oracle is the definition the GPU library is held to, so it is pinned here to
+things other than itself: published SplitMix64 outputs, hand-derived scenarios
+(tests/golden/scenarios.yaml), closed-form special cases, library routines
+(numpy unique), invariants that follow from the rules, an optimal-policy upper
+bound (Belady MIN with bypass), and a naive brute-force model on tiny inputs.
+"""
+import itertools
+import os
+
+import numpy as np
+import pytest
+import yaml
+
+from oracle.oracle import HIT, MISS, VICTIM_HIT, Oracle, OracleError, set_of
+from paper_2407_15264_amd import workload as W
+from tests.naive_model import NaiveCache
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+GAMMA = 0x9E3779B97F4A7C15
+EMPTY = 0xFFFFFFFF
+CODE = {HIT: "H", VICTIM_HIT: "V", MISS: "M"}
+
+
+def _published_splitmix():
+    vals = []
+    with open(os.path.join(GOLDEN, "splitmix64_seed1234567.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                vals.append(int(line))
+    return vals
+
+
+def test_set_index_matches_published_splitmix64_outputs():
+    # set(x) is fastrange(hi32(first SplitMix64 output of state x)).  The k-th
+    # output of the stream seeded with s is the first output of state s + k*gamma.
+    vals = _published_splitmix()
+    assert len(vals) == 5
+    for k, v in enumerate(vals):
+        x = (1234567 + k * GAMMA) % (1 << 64)
+        for S in (1, 2, 13107, 262144, 6291456, (1 << 32) - 1):
+            assert set_of(x, S) == ((v >> 32) * S) >> 32
+    assert W.splitmix_at(1234567, 0) == vals[0]  # the generators use the same stream
+
+
+def test_set_index_is_uniform_enough():
+    S = 2048
+    counts = np.bincount([set_of(x, S) for x in range(1 << 15)], minlength=S)
+    assert counts.min() >= 3 and counts.max() <= 40  # mean 16
+
+
+# --------------------------------------------------------------- scenarios
+def _load_scenarios():
+    with open(os.path.join(GOLDEN, "scenarios.yaml")) as f:
+        return yaml.safe_load(f)
+
+
+def _static_array(spec, n):
+    a = np.full(n, spec.get("default", 0), np.uint32)
+    for k, v in spec.items():
+        if k != "default":
+            a[int(k)] = v
+    return a
+
+
+@pytest.mark.parametrize("name", sorted(_load_scenarios().keys()))
+def test_golden_scenario(name):
+    sc = _load_scenarios()[name]
+    n = sc["num_nodes"]
+    o = Oracle(n, 16, _static_array(sc["static"], n), sc["num_sets"], sc["victim_rows"],
+               sc["lookahead"], ways=sc["ways"])
+    for op in sc["ops"]:
+        if op[0] == "advance":
+            o.advance(np.array(op[1], np.int64))
+            continue
+        r = o.gather(np.array(op[1], np.int64), rows=False)
+        exp = op[2]
+        if "outcome" in exp:
+            assert "".join(CODE[c] for c in r["outcome"]) == exp["outcome"]
+        for key in ("hits", "victim_hits", "misses", "evictions", "enqueued", "dropped"):
+            if key in exp:
+                assert r["stats"][key] == exp[key], key
+        st = o.export_state()
+        if "tags" in exp:
+            tags = [[-1 if t == EMPTY else int(t) for t in row] for row in st["tags"]]
+            assert tags == exp["tags"]
+        if "ring" in exp:
+            assert [-1 if t == EMPTY else int(t) for t in st["ring_tags"]] == exp["ring"]
+        if "tail" in exp:
+            assert st["ring_tail"] == exp["tail"]
+
+
+# ----------------------------------------------------------- special cases
+def test_single_set_small_universe_misses_are_first_touches():
+    rng = np.random.default_rng(1)
+    n = 8
+    o = Oracle(n, 16, rng.integers(0, 5, n), 1, 4, 2)
+    seen = set()
+    for b in range(12):
+        ids = rng.integers(0, n, rng.integers(0, 10))
+        r = o.gather(ids, rows=False)
+        first = set(np.unique(ids).tolist()) - seen
+        assert r["stats"]["misses"] == len(first)
+        assert r["stats"]["hits"] == np.unique(ids).size - len(first)
+        assert r["stats"]["evictions"] == 0 and r["stats"]["victim_hits"] == 0
+        seen |= first
+
+
+@pytest.mark.parametrize("k", [1, 3, 8])
+def test_no_window_reduces_to_static_order(k):
+    # L = 0: no line has reuse information, so within a batch the policy evicts
+    # the lowest-static line that was not inserted in this batch (Sec. 4.2).
+    rng = np.random.default_rng(k)
+    stat = rng.permutation(np.arange(100, 116)).astype(np.uint32)
+    stat[16 - 8:] = 1  # new IDs 8..15
+    o = Oracle(16, 16, stat, 1, 0, 0)
+    o.gather(np.arange(8))
+    o.gather(np.arange(8, 8 + k))
+    tags = set(o.export_state()["tags"][0].tolist())
+    survivors = sorted(range(8), key=lambda x: stat[x])[k:]
+    assert tags == set(survivors) | set(range(8, 8 + k))
+
+
+# --------------------------------------------------------------- invariants
+def _check_invariants(o, ids, r, store=None):
+    st = r["stats"]
+    uniq, inv = np.unique(ids, return_inverse=True)
+    assert np.array_equal(r["uniq"], uniq)
+    assert np.array_equal(r["inv"], inv.reshape(-1))
+    assert st["hits"] + st["victim_hits"] + st["misses"] == st["unique"] == uniq.size
+    assert st["evictions"] == st["enqueued"] + st["dropped"]
+    assert np.count_nonzero(r["outcome"] == HIT) == st["hits"]
+    assert np.count_nonzero(r["outcome"] == VICTIM_HIT) == st["victim_hits"]
+    s = o.export_state()
+    tags = s["tags"]
+    live = tags[tags != EMPTY]
+    assert np.unique(live).size == live.size, "duplicate resident tag"
+    for si in range(tags.shape[0]):
+        for t in tags[si]:
+            if t != EMPTY:
+                assert set_of(int(t), o.num_sets) == si
+    ring = s["ring_tags"][s["ring_tags"] != EMPTY]
+    assert np.unique(ring).size == ring.size
+    assert not (set(ring.tolist()) & set(live.tolist())), "a line is in the cache and the ring"
+    _, tot = o.stats()
+    assert s["ring_tail"] == tot["enqueued"]
+    assert live.size == tot["victim_hits"] + tot["misses"] - tot["evictions"]
+    if store is not None:
+        assert np.array_equal(r["out"], store.view(np.uint8).reshape(store.shape[0], -1)[uniq])
+
+
+def _drive(o, batches, L, announce=None, check=None):
+    announce = batches if announce is None else announce
+    for j in range(min(L + 1, len(announce))):
+        o.advance(announce[j])
+    res = []
+    for b, ids in enumerate(batches):
+        r = o.gather(ids, rows=check is not None and check.get("rows", False))
+        if check is not None:
+            _check_invariants(o, ids, r, check.get("store"))
+        res.append(r)
+        if b + L + 1 < len(announce):
+            o.advance(announce[b + L + 1])
+    return res
+
+
+def test_invariants_on_small_rmat_stream():
+    cfg = W.CONFIGS[1]
+    wl = W.Workload(cfg)
+    store = W.features(cfg.num_nodes, cfg.dim)
+    o = Oracle(cfg.num_nodes, cfg.row_bytes, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows,
+               cfg.cache.lookahead, store=store)
+    res = _drive(o, [wl.batch(b) for b in range(wl.num_batches)], cfg.cache.lookahead,
+                 check=dict(rows=True, store=store))
+    _, tot = o.stats()
+    assert tot["victim_hits"] > 0 and tot["enqueued"] > 0 and tot["hits"] > 0
+    assert len(res) == cfg.batches
+
+
+def test_features_are_standard_normal():
+    x = W.features(4096, 128).astype(np.float64)
+    assert abs(x.mean()) < 0.01 and abs(x.std() - 1) < 0.01
+    assert np.array_equal(x, W.features(4096, 128).astype(np.float64))
+
+
+# ------------------------------------------------------------- Belady bound
+def _belady_hits(seq, ways):
+    """Optimal hits for one fully associative set of `ways` lines with bypass
+    allowed (Belady's MIN): on a miss with a full set, drop whichever of the
+    residents and the newcomer is next used farthest in the future."""
+    hits, cache = 0, set()
+    for i, x in enumerate(seq):
+        if x in cache:
+            hits += 1
+            continue
+        if len(cache) < ways:
+            cache.add(x)
+            continue
+
+        def nxt(y):
+            for j in range(i + 1, len(seq)):
+                if seq[j] == y:
+                    return j
+            return len(seq) + 1
+        far = max(list(cache) + [x], key=nxt)
+        if far != x:
+            cache.remove(far)
+            cache.add(x)
+    return hits
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_hits_never_exceed_belady(seed):
+    rng = np.random.default_rng(seed)
+    n, S, ways_ = 40, 3, 8
+    batches = [rng.integers(0, n, rng.integers(5, 30)) for _ in range(15)]
+    o = Oracle(n, 16, rng.integers(0, 4, n), S, int(rng.integers(0, 6)), 3)
+    res = _drive(o, batches, 3)
+    per_set = {s: [] for s in range(S)}
+    for ids in batches:
+        for x in np.unique(ids):
+            per_set[set_of(int(x), S)].append(int(x))
+    bound = sum(_belady_hits(seq, ways_) for seq in per_set.values())
+    assert sum(r["stats"]["hits"] for r in res) <= bound
+
+
+# ------------------------------------------------------- naive brute force
+def _naive_run(n, S, ways, V, L, T, stat, batches, announce):
+    m = NaiveCache(n, S, ways, V, L, stat, lambda x: set_of(x, S), T)
+    out = []
+    for j in range(min(L + 1, len(announce))):
+        assert m.advance(announce[j]) == "OK"
+    for b, ids in enumerate(batches):
+        _, r = m.gather(ids)
+        out.append(r)
+        if b + L + 1 < len(announce):
+            assert m.advance(announce[b + L + 1]) == "OK"
+    return m, out
+
+
+def _compare(n, S, ways, V, L, T, stat, batches, announce):
+    m, exp = _naive_run(n, S, ways, V, L, T, stat, batches, announce)
+    o = Oracle(n, 16, stat, S, V, L, near_threshold=T, ways=ways)
+    got = _drive(o, batches, L, announce)
+    for e, g in zip(exp, got):
+        assert "".join(CODE[c] for c in g["outcome"]) == e["outcome"]
+        for k in ("hits", "victim_hits", "misses", "evictions", "enqueued", "dropped"):
+            assert g["stats"][k] == e[k], k
+    st = o.export_state()
+    assert [[-1 if t == EMPTY else int(t) for t in row] for row in st["tags"]] == m.tags()
+    assert [-1 if t == EMPTY else int(t) for t in st["ring_tags"]] == m.ring_tags()
+    assert st["ring_tail"] == m.tail
+
+
+def test_exhaustive_tiny_universe_against_naive_model():
+    n = 3
+    subsets = [np.array(c, np.int64) for r in range(n + 1) for c in itertools.combinations(range(n), r)]
+    stat = np.array([2, 1, 2], np.uint32)
+    count = 0
+    for V in (0, 1):
+        for L in (1, 2):
+            for seq in itertools.product(range(len(subsets)), repeat=4):
+                batches = [subsets[i] for i in seq]
+                _compare(n, 1, 2, V, L, 0, stat, batches, batches)
+                count += 1
+    assert count == 4 * len(subsets) ** 4
+
+
+@pytest.mark.parametrize("seed", range(300))
+def test_random_small_against_naive_model(seed):
+    rng = np.random.default_rng(1000 + seed)
+    n = int(rng.integers(2, 14))
+    S = int(rng.integers(1, 4))
+    ways = int(rng.integers(1, 4))
+    V = int(rng.choice([0, 1, 2, 3, 5]))
+    L = int(rng.choice([0, 1, 2, 3, 5, 9]))
+    T = int(rng.choice([0, 0, 1, 2]))
+    stat = rng.integers(0, 4, n).astype(np.uint32)
+    nb = int(rng.integers(1, 8))
+    batches = [rng.integers(0, n, rng.integers(0, 8)) for _ in range(nb)]
+    # announced lists differ from the served ones half of the time
+    if rng.random() < 0.5:
+        announce = [rng.integers(0, n, rng.integers(0, 8)) for _ in range(nb + L)]
+    else:
+        announce = batches
+    _compare(n, S, ways, V, L, T, stat, batches, announce)
+
+
+# ------------------------------------------------------------------- errors
+def test_errors_leave_state_unchanged():
+    o = Oracle(10, 16, np.ones(10, np.uint32), 2, 2, 1)
+    o.advance(np.array([1, 2]))
+    o.advance(np.array([3]))
+    with pytest.raises(OracleError) as e:
+        o.advance(np.array([4]))
+    assert e.value.status == "E_WINDOW"
+    o.gather(np.array([1, 2, 5]))
+    before = o.export_state()
+    with pytest.raises(OracleError) as e:
+        o.gather(np.array([1, 10]))
+    assert e.value.status == "E_RANGE"
+    with pytest.raises(OracleError) as e:
+        o.gather(np.array([-1]))
+    assert e.value.status == "E_RANGE"
+    with pytest.raises(OracleError) as e:
+        o.advance(np.array([11]))
+    assert e.value.status == "E_RANGE"
+    after = o.export_state()
+    assert after["t"] == before["t"]
+    assert np.array_equal(after["tags"], before["tags"])
+    r = o.gather(np.array([], np.int64))
+    assert r["stats"]["unique"] == 0 and r["stats"]["requests"] == 0
+    assert o.export_state()["t"] == before["t"] + 1
+
+
+@pytest.mark.parametrize("kw", [dict(num_nodes=0), dict(row_bytes=8), dict(num_sets=0),
+                                dict(lookahead=32), dict(num_nodes=1 << 33)])
+def test_bad_config_rejected(kw):
+    args = dict(num_nodes=10, row_bytes=16, num_sets=2, victim_rows=2, lookahead=1)
+    args.update(kw)
+    with pytest.raises(OracleError) as e:
+        Oracle(args["num_nodes"], args["row_bytes"], np.ones(max(1, min(args["num_nodes"], 64)), np.uint32),
+               args["num_sets"], args["victim_rows"], args["lookahead"])
+    assert e.value.status == "E_INVAL"
