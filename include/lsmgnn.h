@@ -1,0 +1,161 @@
+/*
+ * lsmgnn.h -- C ABI of the MI355X (gfx950) feature-gather cache.
+ *
+ * The library serves the per-minibatch node-feature gather of storage-based GNN
+ * training through a GPU-resident, 8-way set-associative software cache in HBM,
+ * with the hybrid eviction policy and the victim buffer of LSM-GNN (Kim et al.,
+ * arXiv 2407.15264):
+ *   - the software cache holding recently used feature rows, with misses served
+ *     from the backing feature store (Sec. 4, system design overview);
+ *   - the window of sampled-node lists of upcoming minibatches that supplies
+ *     the dynamic (next-reuse) information (Sec. 4 overview, Sec. 4.2);
+ *   - the hybrid eviction policy: four levels from the dynamic information, the
+ *     lowest static score evicted first within a level (Sec. 4.2);
+ *   - the victim buffer in host memory that keeps evicted lines carrying reuse
+ *     information, with the two lowest levels swapped when it is enabled
+ *     (Sec. 4.3.1, 4.3.2).
+ * Storage (SSDs in the paper) is a host-resident, pinned backing feature table.
+ *
+ * Semantics, fixed where the paper is silent:
+ *   - a gather deduplicates its IDs and serves them in ascending ID order; the
+ *     output holds one row per unique ID, ascending, plus an inverse index;
+ *   - set(x) = ((hi32(splitmix64(x)) * num_sets) >> 32), where splitmix64(x) is
+ *     the first output of a SplitMix64 generator with state x;
+ *   - a line's class while gather t runs: "recent" if inserted during gather t;
+ *     otherwise with d the distance to its next announced use in (t, t+L]:
+ *     none -> "no reuse", d <= T -> "near", T < d <= L -> "far";
+ *   - eviction: an empty way first (lowest index); else the minimum of
+ *     (level, static score, way) with levels far < none < recent < near when the
+ *     victim ring is on (V > 0) and none < far < recent < near when it is off;
+ *   - an evicted line of class far or near enters the victim ring (a FIFO of V
+ *     entries that overwrites its oldest entry); others are dropped;
+ *   - a request missing in the cache but present in the ring is a victim hit:
+ *     the entry is removed and the line is refilled like any miss.
+ * Every gathered row is bit-identical to the backing-store row of its node.
+ *
+ * Threading: one cache object must not be used from two threads at once.
+ * Calls are stream-ordered on the stream passed in (a hipStream_t as void*,
+ * NULL = the null stream) and return once their status is known; gather and
+ * advance synchronise that stream before returning.
+ */
+#ifndef LSMGNN_H
+#define LSMGNN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct lsmgnn_cache lsmgnn_cache; /* opaque, owned by the library */
+
+typedef enum {
+  LSMGNN_OK = 0,
+  LSMGNN_E_INVAL = 1,  /* bad argument or configuration */
+  LSMGNN_E_RANGE = 2,  /* a node ID outside [0, num_nodes) */
+  LSMGNN_E_WINDOW = 3, /* advance would announce a minibatch beyond t + L */
+  LSMGNN_E_NOMEM = 4,  /* device or pinned host allocation failed */
+  LSMGNN_E_DEVICE = 5, /* a HIP runtime call failed */
+  LSMGNN_E_STATE = 6   /* the object is unusable after an earlier device error */
+} lsmgnn_status;
+
+/* per-unique-ID outcome codes written by lsmgnn_gather */
+enum { LSMGNN_HIT = 0, LSMGNN_VICTIM_HIT = 1, LSMGNN_MISS = 2 };
+
+typedef struct {
+  uint64_t num_nodes;   /* IDs are int64 in [0, num_nodes); 1 <= num_nodes <= 2^32 - 1 */
+  uint64_t row_bytes;   /* bytes per feature row; a positive multiple of 16 */
+  uint64_t num_sets;    /* S >= 1 sets of 8 ways; S * 8 * row_bytes bytes of HBM */
+  uint64_t victim_rows; /* V rows of pinned host victim ring; 0 disables it */
+  uint64_t max_batch;   /* largest n accepted by gather and advance (>= 1) */
+  uint32_t lookahead;   /* L in [0, 31]: minibatches announced ahead */
+  uint32_t near_threshold; /* T; 0 selects max(1, L / 8) (one eighth of the window) */
+  int32_t device;       /* HIP device ordinal */
+  uint32_t flags;       /* reserved, must be 0 */
+  /* Backing store: num_nodes * row_bytes bytes of PINNED host memory (from
+     lsmgnn_host_alloc, hipHostMalloc or a pinned torch tensor), row v at
+     offset v * row_bytes.  Borrowed: the caller keeps it alive and unchanged
+     while the cache exists; the library only reads it. */
+  const void *host_store;
+  /* Static score per node (host, num_nodes entries); copied at create. */
+  const uint32_t *static_score;
+} lsmgnn_config;
+
+typedef struct {
+  uint64_t batch;       /* gather index t of the last gather (total: gathers done) */
+  uint64_t requests;    /* raw IDs */
+  uint64_t unique;      /* unique IDs = hits + victim_hits + misses */
+  uint64_t hits;        /* served from the HBM cache */
+  uint64_t victim_hits; /* served from the victim ring */
+  uint64_t misses;      /* served from the backing store */
+  uint64_t evictions;   /* = enqueued + dropped */
+  uint64_t enqueued;    /* evicted lines written to the victim ring */
+  uint64_t dropped;     /* evicted lines discarded */
+} lsmgnn_counts;
+
+/* Accumulated device time of the data-movement kernels (filled only while
+   profiling is on; see lsmgnn_set_profiling).  Bytes are algorithmic: rows
+   moved times row_bytes, per direction. */
+typedef struct {
+  double hbm_copy_ms;   uint64_t hbm_copy_launches;   uint64_t hbm_copy_rows;   /* cache -> out */
+  double host_fetch_ms; uint64_t host_fetch_launches; uint64_t host_fetch_rows; /* store/ring -> out */
+  double enqueue_ms;    uint64_t enqueue_launches;    uint64_t enqueue_rows;    /* cache -> ring */
+  double fill_ms;       uint64_t fill_launches;       uint64_t fill_rows;       /* out -> cache */
+  double gather_ms;     uint64_t gathers;             /* whole gather, first to last kernel */
+} lsmgnn_profile;
+
+/* Create a cache on cfg->device.  Allocates the HBM cache (S*8 rows), its
+   metadata, per-node window/static/ring-index arrays (about 16 bytes per node),
+   scratch sized for max_batch, and the pinned victim ring (V rows).  On
+   failure *out is NULL and nothing stays allocated. */
+lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out);
+void lsmgnn_cache_destroy(lsmgnn_cache *c);
+
+/* Announce the sampled-node list of the next minibatch (the k-th call announces
+   minibatch k).  ids: device pointer to n int64 IDs (duplicates allowed).
+   E_WINDOW if k > t + L (t = gathers done); E_RANGE if an ID is out of range;
+   E_INVAL if n > max_batch.  An announcement for k <= t is accepted and unused.
+   On error nothing changes.  Synchronises `stream`. */
+lsmgnn_status lsmgnn_advance(lsmgnn_cache *c, const int64_t *ids, uint64_t n, void *stream);
+
+/* Gather one minibatch (gather index t, then t += 1).
+     ids        device, n int64 node IDs (duplicates allowed)
+     out        device, >= n * row_bytes bytes; row u = feature row of unique_ids[u]
+     unique_ids device, >= n int64; ascending unique IDs
+     inverse    device, n int64 or NULL; unique_ids[inverse[i]] == ids[i]
+     outcome    device, >= n uint8 or NULL; LSMGNN_HIT / _VICTIM_HIT / _MISS per unique ID
+     n_unique   host; number of unique IDs
+   E_RANGE (nothing changes) if an ID is out of range; E_INVAL if n > max_batch
+   or a required pointer is NULL.  Synchronises `stream`. */
+lsmgnn_status lsmgnn_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, void *out,
+                            int64_t *unique_ids, int64_t *inverse, uint8_t *outcome,
+                            uint64_t *n_unique, void *stream);
+
+/* Counters of the last gather and totals over all gathers (either may be NULL). */
+lsmgnn_status lsmgnn_stats(const lsmgnn_cache *c, lsmgnn_counts *last, lsmgnn_counts *total);
+
+/* Copy the policy state to host memory (each pointer may be NULL):
+   tags num_sets*8 uint32 (0xFFFFFFFF = empty way), ring_tags victim_rows uint32
+   (0xFFFFFFFF = empty entry), ring_tail = entries ever enqueued, t = gathers done. */
+lsmgnn_status lsmgnn_export_state(const lsmgnn_cache *c, uint32_t *tags, uint32_t *ring_tags,
+                                  uint64_t *ring_tail, uint64_t *t);
+
+/* Turn per-kernel event timing of the data-movement kernels on (1) or off (0);
+   turning it on clears the accumulated profile. */
+lsmgnn_status lsmgnn_set_profiling(lsmgnn_cache *c, int on);
+lsmgnn_status lsmgnn_get_profile(const lsmgnn_cache *c, lsmgnn_profile *out);
+
+/* Pinned, device-mapped host memory for a backing store (exact size, unlike
+   caching allocators that round up).  Free with lsmgnn_host_free. */
+lsmgnn_status lsmgnn_host_alloc(uint64_t bytes, void **ptr);
+void lsmgnn_host_free(void *ptr);
+
+/* Set index the cache uses for node x (host-side helper, for tests). */
+uint64_t lsmgnn_set_of(uint64_t x, uint64_t num_sets);
+
+const char *lsmgnn_strerror(lsmgnn_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LSMGNN_H */

@@ -1,0 +1,245 @@
+"""Python binding of the MI355X feature-gather cache (C ABI in include/lsmgnn.h).
+
+Argument marshalling only: every step of a gather runs in the gfx950 kernels of
+liblsmgnn.so.  PyTorch supplies device memory (tensors) and the stream.  There
+is no CPU fallback: if the library is missing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblsmgnn.so")
+
+OK, E_INVAL, E_RANGE, E_WINDOW, E_NOMEM, E_DEVICE, E_STATE = range(7)
+STATUS_NAMES = {0: "OK", 1: "E_INVAL", 2: "E_RANGE", 3: "E_WINDOW", 4: "E_NOMEM", 5: "E_DEVICE", 6: "E_STATE"}
+HIT, VICTIM_HIT, MISS = 0, 1, 2
+EMPTY = 0xFFFFFFFF
+COUNT_FIELDS = ("batch", "requests", "unique", "hits", "victim_hits", "misses", "evictions", "enqueued",
+                "dropped")
+
+
+class LsmgnnError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        self.status = STATUS_NAMES.get(code, str(code))
+        msg = lib().lsmgnn_strerror(code).decode() if _lib is not None else self.status
+        super().__init__(f"{where}: {self.status} ({msg})")
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("num_nodes", ctypes.c_uint64), ("row_bytes", ctypes.c_uint64), ("num_sets", ctypes.c_uint64),
+                ("victim_rows", ctypes.c_uint64), ("max_batch", ctypes.c_uint64), ("lookahead", ctypes.c_uint32),
+                ("near_threshold", ctypes.c_uint32), ("device", ctypes.c_int32), ("flags", ctypes.c_uint32),
+                ("host_store", ctypes.c_void_p), ("static_score", ctypes.c_void_p)]
+
+
+class Counts(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_uint64) for f in COUNT_FIELDS]
+
+
+class Profile(ctypes.Structure):
+    _fields_ = [("hbm_copy_ms", ctypes.c_double), ("hbm_copy_launches", ctypes.c_uint64),
+                ("hbm_copy_rows", ctypes.c_uint64),
+                ("host_fetch_ms", ctypes.c_double), ("host_fetch_launches", ctypes.c_uint64),
+                ("host_fetch_rows", ctypes.c_uint64),
+                ("enqueue_ms", ctypes.c_double), ("enqueue_launches", ctypes.c_uint64),
+                ("enqueue_rows", ctypes.c_uint64),
+                ("fill_ms", ctypes.c_double), ("fill_launches", ctypes.c_uint64), ("fill_rows", ctypes.c_uint64),
+                ("gather_ms", ctypes.c_double), ("gathers", ctypes.c_uint64)]
+
+
+_lib = None
+
+
+def lib():
+    """Load liblsmgnn.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(hipcc --offload-arch=gfx950); there is no fallback path")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, u64, i32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int
+        L.lsmgnn_cache_create.restype = i32
+        L.lsmgnn_cache_create.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(vp)]
+        L.lsmgnn_cache_destroy.restype = None
+        L.lsmgnn_cache_destroy.argtypes = [vp]
+        L.lsmgnn_advance.restype = i32
+        L.lsmgnn_advance.argtypes = [vp, vp, u64, vp]
+        L.lsmgnn_gather.restype = i32
+        L.lsmgnn_gather.argtypes = [vp, vp, u64, vp, vp, vp, vp, ctypes.POINTER(u64), vp]
+        L.lsmgnn_stats.restype = i32
+        L.lsmgnn_stats.argtypes = [vp, ctypes.POINTER(Counts), ctypes.POINTER(Counts)]
+        L.lsmgnn_export_state.restype = i32
+        L.lsmgnn_export_state.argtypes = [vp, vp, vp, ctypes.POINTER(u64), ctypes.POINTER(u64)]
+        L.lsmgnn_set_profiling.restype = i32
+        L.lsmgnn_set_profiling.argtypes = [vp, i32]
+        L.lsmgnn_get_profile.restype = i32
+        L.lsmgnn_get_profile.argtypes = [vp, ctypes.POINTER(Profile)]
+        L.lsmgnn_host_alloc.restype = i32
+        L.lsmgnn_host_alloc.argtypes = [u64, ctypes.POINTER(vp)]
+        L.lsmgnn_host_free.restype = None
+        L.lsmgnn_host_free.argtypes = [vp]
+        L.lsmgnn_set_of.restype = u64
+        L.lsmgnn_set_of.argtypes = [u64, u64]
+        L.lsmgnn_strerror.restype = ctypes.c_char_p
+        L.lsmgnn_strerror.argtypes = [i32]
+        _lib = L
+    return _lib
+
+
+def _check(rc: int, where: str):
+    if rc != OK:
+        raise LsmgnnError(rc, where)
+
+
+def set_of(x: int, num_sets: int) -> int:
+    return int(lib().lsmgnn_set_of(int(x), int(num_sets)))
+
+
+class PinnedBuffer:
+    """Exact-size pinned, device-mapped host memory (lsmgnn_host_alloc)."""
+
+    def __init__(self, nbytes: int):
+        p = ctypes.c_void_p()
+        _check(lib().lsmgnn_host_alloc(int(nbytes), ctypes.byref(p)), "lsmgnn_host_alloc")
+        self.ptr = p.value
+        self.nbytes = int(nbytes)
+
+    def numpy(self, dtype=np.uint8, shape=None) -> np.ndarray:
+        raw = (ctypes.c_uint8 * self.nbytes).from_address(self.ptr)
+        a = np.frombuffer(raw, dtype=np.uint8).view(dtype)
+        return a if shape is None else a.reshape(shape)
+
+    def close(self):
+        if getattr(self, "ptr", None):
+            lib().lsmgnn_host_free(self.ptr)
+            self.ptr = None
+
+    __del__ = close
+
+
+def _stream_handle(stream, device):
+    import torch
+    s = torch.cuda.current_stream(device) if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev_ptr(t, dtype, name):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous {dtype} tensor")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+@dataclasses.dataclass
+class GatherResult:
+    n_unique: int
+    out: "object"        # torch uint8 view (n_unique, row_bytes) of the caller's buffer
+    unique: "object"     # torch int64 (n_unique,)
+    inverse: "object"    # torch int64 (n,) or None
+    outcome: "object"    # torch uint8 (n_unique,) or None
+
+
+class FeatureCache:
+    """GPU feature-gather cache on one device.
+
+    host_store: address of pinned host memory holding num_nodes * row_bytes
+    bytes (PinnedBuffer.ptr, or a pinned torch tensor's data_ptr()); it must
+    outlive the cache.  static_score: num_nodes unsigned scores."""
+
+    def __init__(self, num_nodes, row_bytes, host_store, static_score, num_sets, victim_rows, lookahead,
+                 max_batch, near_threshold=0, device=0):
+        import torch
+        self.device = torch.device("cuda", device)
+        self.num_nodes, self.row_bytes = int(num_nodes), int(row_bytes)
+        self.num_sets, self.victim_rows = int(num_sets), int(victim_rows)
+        self.lookahead, self.max_batch = int(lookahead), int(max_batch)
+        if isinstance(host_store, PinnedBuffer):
+            host_store = host_store.ptr
+        elif isinstance(host_store, torch.Tensor):
+            host_store = host_store.data_ptr()
+        stat = np.ascontiguousarray(np.asarray(static_score), dtype=np.uint32)
+        cfg = Config(self.num_nodes, self.row_bytes, self.num_sets, self.victim_rows, self.max_batch,
+                     self.lookahead, int(near_threshold), int(device), 0, ctypes.c_void_p(int(host_store)),
+                     ctypes.c_void_p(stat.ctypes.data))
+        h = ctypes.c_void_p()
+        _check(lib().lsmgnn_cache_create(ctypes.byref(cfg), ctypes.byref(h)), "lsmgnn_cache_create")
+        self._h = h
+        self._scratch = {}
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().lsmgnn_cache_destroy(self._h)
+            self._h = None
+
+    __del__ = close
+
+    def _buf(self, name, n, dtype):
+        import torch
+        b = self._scratch.get(name)
+        if b is None or b.numel() < n:
+            b = torch.empty(max(n, 1), dtype=dtype, device=self.device)
+            self._scratch[name] = b
+        return b
+
+    def advance(self, ids, stream=None):
+        import torch
+        n = ids.numel()
+        p = _dev_ptr(ids, torch.int64, "ids") if n else None
+        _check(lib().lsmgnn_advance(self._h, p, n, _stream_handle(stream, self.device)), "lsmgnn_advance")
+
+    def gather(self, ids, out=None, unique=None, inverse=True, outcome=False, stream=None) -> GatherResult:
+        """Gather one minibatch.  `out` (uint8, >= n*row_bytes bytes) and
+        `unique` (int64, >= n) may be passed to reuse caller buffers;
+        `inverse`/`outcome` may be True (allocate), a tensor, or False/None."""
+        import torch
+        n = ids.numel()
+        if out is None:
+            out = self._buf("out", n * self.row_bytes, torch.uint8)
+        if unique is None:
+            unique = self._buf("unique", n, torch.int64)
+        inv_t = self._buf("inverse", n, torch.int64) if inverse is True else (inverse or None)
+        oc_t = self._buf("outcome", n, torch.uint8) if outcome is True else (outcome or None)
+        if out.numel() * out.element_size() < n * self.row_bytes or unique.numel() < n:
+            raise ValueError("out/unique buffers too small")
+        nu = ctypes.c_uint64()
+        rc = lib().lsmgnn_gather(
+            self._h, _dev_ptr(ids, torch.int64, "ids") if n else None, n,
+            ctypes.c_void_p(out.data_ptr()), _dev_ptr(unique, torch.int64, "unique"),
+            _dev_ptr(inv_t, torch.int64, "inverse") if inv_t is not None else None,
+            _dev_ptr(oc_t, torch.uint8, "outcome") if oc_t is not None else None,
+            ctypes.byref(nu), _stream_handle(stream, self.device))
+        _check(rc, "lsmgnn_gather")
+        U = nu.value
+        flat = out.view(torch.uint8).reshape(-1)
+        return GatherResult(U, flat[: U * self.row_bytes].view(U, self.row_bytes), unique[:U],
+                            inv_t[:n] if inv_t is not None else None, oc_t[:U] if oc_t is not None else None)
+
+    def stats(self):
+        last, total = Counts(), Counts()
+        _check(lib().lsmgnn_stats(self._h, ctypes.byref(last), ctypes.byref(total)), "lsmgnn_stats")
+        return ({f: getattr(last, f) for f in COUNT_FIELDS}, {f: getattr(total, f) for f in COUNT_FIELDS})
+
+    def export_state(self):
+        tags = np.empty(self.num_sets * 8, np.uint32)
+        ring = np.empty(max(self.victim_rows, 1), np.uint32)
+        tail, t = ctypes.c_uint64(), ctypes.c_uint64()
+        _check(lib().lsmgnn_export_state(self._h, tags.ctypes.data, ring.ctypes.data, ctypes.byref(tail),
+                                         ctypes.byref(t)), "lsmgnn_export_state")
+        return dict(tags=tags.reshape(self.num_sets, 8), ring_tags=ring[: self.victim_rows],
+                    ring_tail=tail.value, t=t.value)
+
+    def set_profiling(self, on: bool):
+        _check(lib().lsmgnn_set_profiling(self._h, 1 if on else 0), "lsmgnn_set_profiling")
+
+    def profile(self) -> dict:
+        p = Profile()
+        _check(lib().lsmgnn_get_profile(self._h, ctypes.byref(p)), "lsmgnn_get_profile")
+        return {f: getattr(p, f) for f, _ in Profile._fields_}

@@ -1,0 +1,131 @@
+"""Side-by-side driver: the GPU library (through its C ABI) and the CPU oracle
+consume the same seeded request stream and are compared after every gather.
+
+Compared per gather: the ascending unique IDs, the inverse index, the outcome
+of every unique ID (hit / victim hit / miss), all counters, and the gathered
+rows (bit-exact).  Compared at the end: every cache tag, every ring tag, the
+ring tail and the gather count.  Integer work, so everything must match
+exactly.
+"""
+from __future__ import annotations
+
+import sys
+import time
+
+import numpy as np
+
+from oracle.oracle import Oracle
+from paper_2407_15264_amd import lsmgnn
+from paper_2407_15264_amd import workload as W
+
+COUNT_KEYS = ("batch", "requests", "unique", "hits", "victim_hits", "misses", "evictions", "enqueued", "dropped")
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+class Store:
+    """A pinned host feature table (num_nodes x row_bytes)."""
+
+    def __init__(self, num_nodes, dim, elt_bytes=4, seed=0, fill=None):
+        self.num_nodes, self.row_bytes = num_nodes, dim * elt_bytes
+        self.buf = lsmgnn.PinnedBuffer(num_nodes * self.row_bytes)
+        self.np = self.buf.numpy(np.uint8, (num_nodes, self.row_bytes))
+        if fill is None:
+            W.fill_features(self.buf.ptr, dim, elt_bytes, 0, num_nodes, seed)
+        else:
+            self.np[:] = fill
+
+    @classmethod
+    def random_bytes(cls, num_nodes, row_bytes, seed=0):
+        rng = np.random.default_rng(seed)
+        s = cls.__new__(cls)
+        s.num_nodes, s.row_bytes = num_nodes, row_bytes
+        s.buf = lsmgnn.PinnedBuffer(num_nodes * row_bytes)
+        s.np = s.buf.numpy(np.uint8, (num_nodes, row_bytes))
+        s.np[:] = rng.integers(0, 256, (num_nodes, row_bytes), dtype=np.uint8)
+        return s
+
+
+def compare_state(cache, orc, where=""):
+    g, o = cache.export_state(), orc.export_state()
+    if not np.array_equal(g["tags"], o["tags"]):
+        bad = np.argwhere(g["tags"] != o["tags"])[:5]
+        raise AssertionError(f"{where}: cache tags differ at {bad.tolist()}: gpu {g['tags'][tuple(bad[0])]} "
+                             f"oracle {o['tags'][tuple(bad[0])]}")
+    if not np.array_equal(g["ring_tags"], o["ring_tags"]):
+        bad = np.flatnonzero(g["ring_tags"] != o["ring_tags"])[:5]
+        raise AssertionError(f"{where}: ring tags differ at {bad.tolist()}")
+    assert g["ring_tail"] == o["ring_tail"], (where, g["ring_tail"], o["ring_tail"])
+    assert g["t"] == o["t"], (where, g["t"], o["t"])
+
+
+def run_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, announce=None,
+               near_threshold=0, rows="all", max_batch=None, device=0, state_every=0, label="parity",
+               store_gpu=None):
+    """rows: 'all' -> compare every gathered row with the oracle's; an int k ->
+    compare with the oracle on every k-th gather and, on every gather, with the
+    backing-store rows indexed on the GPU (store_gpu, a device copy)."""
+    import torch
+    dev = torch.device("cuda", device)
+    announce = batches if announce is None else announce
+    mb = max_batch or max(1, max((len(b) for b in list(batches) + list(announce)), default=1))
+    L = lookahead
+    cache = lsmgnn.FeatureCache(store.num_nodes, store.row_bytes, store.buf, static, num_sets, victim_rows, L, mb,
+                                near_threshold=near_threshold, device=device)
+    orc = Oracle(store.num_nodes, store.row_bytes, static, num_sets, victim_rows, L,
+                 near_threshold=near_threshold, store=store.np)
+    dev_ann = [torch.as_tensor(np.asarray(a, np.int64)).to(dev) for a in announce]
+    dev_bat = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in batches]
+    for j in range(min(L + 1, len(announce))):
+        cache.advance(dev_ann[j])
+        orc.advance(announce[j])
+    t0 = time.time()
+    for b, ids in enumerate(batches):
+        where = f"{label} gather {b}"
+        r = cache.gather(dev_bat[b], inverse=True, outcome=True)
+        full_rows = rows == "all" or (isinstance(rows, int) and b % rows == 0)
+        o = orc.gather(np.asarray(ids, np.int64), rows=full_rows)
+        U = r.n_unique
+        assert U == o["uniq"].size, (where, U, o["uniq"].size)
+        uq = r.unique.cpu().numpy()
+        if not np.array_equal(uq, o["uniq"]):
+            raise AssertionError(f"{where}: unique IDs differ")
+        if not np.array_equal(r.inverse.cpu().numpy(), o["inv"]):
+            raise AssertionError(f"{where}: inverse differs")
+        oc = r.outcome.cpu().numpy()
+        if not np.array_equal(oc, o["outcome"]):
+            bad = np.flatnonzero(oc != o["outcome"])[:5]
+            raise AssertionError(f"{where}: outcome differs at unique idx {bad.tolist()} "
+                                 f"(ids {o['uniq'][bad].tolist()}): gpu {oc[bad].tolist()} "
+                                 f"oracle {o['outcome'][bad].tolist()}")
+        last, _ = cache.stats()
+        for k in COUNT_KEYS:
+            if last[k] != o["stats"][k]:
+                raise AssertionError(f"{where}: counter {k}: gpu {last[k]} oracle {o['stats'][k]}")
+        if full_rows:
+            if not np.array_equal(r.out.cpu().numpy(), o["out"]):
+                bad = np.flatnonzero((r.out.cpu().numpy() != o["out"]).any(axis=1))[:5]
+                raise AssertionError(f"{where}: gathered rows differ at unique idx {bad.tolist()} "
+                                     f"outcomes {oc[bad].tolist()}")
+        elif store_gpu is not None:
+            ref = store_gpu.index_select(0, r.unique)
+            if not torch.equal(r.out, ref):
+                raise AssertionError(f"{where}: gathered rows differ from the backing store")
+        if state_every and (b + 1) % state_every == 0:
+            compare_state(cache, orc, where)
+        if b + L + 1 < len(announce):
+            cache.advance(dev_ann[b + L + 1])
+            orc.advance(announce[b + L + 1])
+    compare_state(cache, orc, f"{label} end")
+    tot = cache.stats()[1]
+    cache.close()
+    orc.close()
+    return dict(total=tot, seconds=time.time() - t0)
+
+
+def config_stream(cfg, batches=None):
+    wl = W.Workload(cfg, batches)
+    return wl, [wl.batch(b) for b in range(wl.num_batches)]

@@ -1,0 +1,233 @@
+"""GPU <-> oracle parity through the C ABI (needs an MI355X).
+
+Every case drives the GPU library and the CPU oracle with the same seeded
+stream and requires identical unique IDs, inverse, per-ID outcomes, counters,
+rows (bit-exact) and final cache/ring state.  Cases: the two smaller workload
+shapes end to end, randomized small caches, adversarial streams (one set,
+duplicates, single IDs, ragged ID ranges, empty batches, batches larger than
+the cache, L = 0, V = 0 and 1, n = max_batch), error paths that must leave the
+state unchanged, determinism, and provenance (hits come from HBM, misses from
+the backing store).
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from paper_2407_15264_amd import lsmgnn  # noqa: E402
+from paper_2407_15264_amd import workload as W  # noqa: E402
+from tests.parity_driver import Store, compare_state, config_stream, log, run_parity  # noqa: E402
+from oracle.oracle import Oracle  # noqa: E402
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lsmgnn.lib()
+
+
+def test_workload_rmat14_full_parity():
+    cfg = W.CONFIGS[1]
+    log(f"case: {cfg.name}, all {cfg.batches} gathers, all rows")
+    wl, batches = config_stream(cfg)
+    store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
+    res = run_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead, batches,
+                     rows="all", state_every=5, label=cfg.name)
+    tot = res["total"]
+    assert tot["victim_hits"] > 0 and tot["enqueued"] > 0
+
+
+@pytest.mark.timeout(600)
+def test_workload_rmat20_parity():
+    cfg = W.CONFIGS[2]
+    log(f"case: {cfg.name}, all {cfg.batches} gathers; rows vs oracle every 20th gather, "
+        f"vs the backing store on the GPU for every gather")
+    wl, batches = config_stream(cfg)
+    store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
+    store_gpu = torch.from_numpy(store.np).to("cuda")
+    res = run_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead, batches,
+                     rows=20, state_every=50, label=cfg.name, store_gpu=store_gpu)
+    tot = res["total"]
+    log(f"  {cfg.name}: {tot}")
+    assert tot["victim_hits"] > 0 and tot["hits"] > 0
+
+
+def _random_case(seed):
+    rng = np.random.default_rng(5000 + seed)
+    n = int(rng.choice([1, 7, 33, 100, 1000, 5000, 70001]))
+    S = int(rng.choice([1, 2, 3, 5, 16, 61, 400]))
+    V = int(rng.choice([0, 1, 2, 7, 64, 1000]))
+    L = int(rng.choice([0, 1, 2, 4, 8, 16, 31]))
+    T = int(rng.choice([0, 0, 1, 2, 3]))
+    rb = int(rng.choice([16, 48, 64, 512]))
+    nb = int(rng.integers(1, 12))
+    bmax = int(rng.choice([1, 5, 40, 300, 3000]))
+    stat = rng.integers(0, rng.choice([1, 3, 1000]), n).astype(np.uint32)
+    batches = [rng.integers(0, n, rng.integers(0, bmax + 1)) for _ in range(nb)]
+    if rng.random() < 0.5:
+        announce = [rng.integers(0, n, rng.integers(0, bmax + 1)) for _ in range(nb + L)]
+    else:
+        announce = batches
+    return n, S, V, L, T, rb, stat, batches, announce
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_small_caches(seed):
+    n, S, V, L, T, rb, stat, batches, announce = _random_case(seed)
+    log(f"case: random seed {seed}: N={n} S={S} V={V} L={L} T={T} R={rb} batches={len(batches)}")
+    store = Store.random_bytes(n, rb, seed)
+    run_parity(store, stat, S, V, L, batches, announce, near_threshold=T, rows="all", label=f"random{seed}")
+
+
+def _adversarial():
+    rng = np.random.default_rng(7)
+    cases = {}
+    # every request maps to one set
+    cases["one_set"] = dict(n=64, S=1, V=8, L=3, batches=[rng.integers(0, 64, 30) for _ in range(10)])
+    # heavy duplication
+    cases["duplicates"] = dict(n=1000, S=4, V=4, L=2,
+                               batches=[np.repeat(rng.integers(0, 1000, 3), 1000) for _ in range(6)])
+    cases["single_ids"] = dict(n=50, S=2, V=2, L=2, batches=[np.array([i % 7]) for i in range(20)])
+    # top of the ID range and a ragged bitmap tail
+    top = (1 << 20) + 37
+    cases["id_top"] = dict(n=top, S=64, V=16, L=2,
+                           batches=[np.array([top - 1, top - 2, 0, top - 33, top - 1] * 3)
+                                    for _ in range(4)] + [rng.integers(top - 3000, top, 2000)])
+    cases["no_window"] = dict(n=3000, S=16, V=64, L=0, batches=[rng.integers(0, 3000, 500) for _ in range(8)])
+    cases["no_ring"] = dict(n=3000, S=16, V=0, L=4, batches=[rng.integers(0, 3000, 500) for _ in range(8)])
+    cases["ring_of_one"] = dict(n=300, S=4, V=1, L=4, batches=[rng.integers(0, 300, 80) for _ in range(12)])
+    cases["batch_exceeds_cache"] = dict(n=100000, S=4, V=100, L=3,
+                                        batches=[rng.integers(0, 100000, 5000) for _ in range(6)])
+    cases["empty_batches"] = dict(n=500, S=8, V=8, L=2,
+                                  batches=[np.array([], np.int64), rng.integers(0, 500, 100), np.array([], np.int64),
+                                           rng.integers(0, 500, 100), rng.integers(0, 500, 100)])
+    cases["single_node"] = dict(n=1, S=1, V=1, L=1, batches=[np.zeros(5, np.int64), np.zeros(1, np.int64)] * 3)
+    cases["big_batch"] = dict(n=1 << 22, S=4096, V=20000, L=4,
+                              batches=[rng.integers(0, 1 << 22, 1 << 20) for _ in range(3)])
+    return cases
+
+
+@pytest.mark.parametrize("name", sorted(_adversarial().keys()))
+def test_adversarial_streams(name):
+    c = _adversarial()[name]
+    log(f"case: adversarial {name}: N={c['n']} S={c['S']} V={c['V']} L={c['L']}")
+    rb = 64 if c["n"] < (1 << 21) else 16
+    store = Store.random_bytes(c["n"], rb, 1)
+    stat = np.random.default_rng(3).integers(0, 5, c["n"]).astype(np.uint32)
+    mb = max(1, max(len(b) for b in c["batches"]))
+    run_parity(store, stat, c["S"], c["V"], c["L"], c["batches"], rows="all", max_batch=mb, label=name)
+
+
+def test_errors_leave_state_unchanged():
+    log("case: error paths")
+    n, S, V, L = 200, 4, 8, 1
+    store = Store.random_bytes(n, 32, 2)
+    stat = np.arange(n, dtype=np.uint32) % 5
+    cache = lsmgnn.FeatureCache(n, 32, store.buf, stat, S, V, L, 64)
+    orc = Oracle(n, 32, stat, S, V, L, store=store.np)
+    dev = lambda a: torch.as_tensor(np.asarray(a, np.int64)).cuda()  # noqa: E731
+    a0, a1 = np.arange(0, 40), np.arange(20, 60)
+    for a in (a0, a1):
+        cache.advance(dev(a))
+        orc.advance(a)
+    with pytest.raises(lsmgnn.LsmgnnError) as e:
+        cache.advance(dev([1]))
+    assert e.value.status == "E_WINDOW"
+    r = cache.gather(dev(a0), outcome=True)
+    orc.gather(a0)
+    before = cache.export_state()
+    for bad in ([0, 200], [-1, 3], [199, 1 << 40]):
+        with pytest.raises(lsmgnn.LsmgnnError) as e:
+            cache.gather(dev(bad))
+        assert e.value.status == "E_RANGE"
+        with pytest.raises(lsmgnn.LsmgnnError) as e:
+            cache.advance(dev(bad))
+        assert e.value.status == "E_RANGE"
+    with pytest.raises(lsmgnn.LsmgnnError) as e:
+        cache.gather(dev(np.zeros(65)))
+    assert e.value.status == "E_INVAL"
+    after = cache.export_state()
+    assert after["t"] == before["t"] and np.array_equal(after["tags"], before["tags"])
+    assert np.array_equal(after["ring_tags"], before["ring_tags"])
+    # the stream continues exactly like the oracle's after the rejected calls
+    cache.advance(dev(a1))
+    orc.advance(a1)
+    r = cache.gather(dev(a1), outcome=True)
+    o = orc.gather(a1)
+    assert np.array_equal(r.outcome.cpu().numpy(), o["outcome"])
+    assert np.array_equal(r.out.cpu().numpy(), o["out"])
+    compare_state(cache, orc, "after errors")
+    r = cache.gather(dev([]))
+    assert r.n_unique == 0 and cache.stats()[0]["unique"] == 0
+    cache.close()
+
+
+def test_bad_configs_rejected():
+    store = Store.random_bytes(16, 16, 0)
+    stat = np.ones(16, np.uint32)
+    base = dict(num_nodes=16, row_bytes=16, host_store=store.buf, static_score=stat, num_sets=2, victim_rows=2,
+                lookahead=1, max_batch=8)
+    for bad in (dict(num_sets=0), dict(row_bytes=24), dict(lookahead=32), dict(max_batch=0), dict(num_nodes=0)):
+        kw = dict(base, **bad)
+        with pytest.raises(lsmgnn.LsmgnnError) as e:
+            lsmgnn.FeatureCache(**kw)
+        assert e.value.status == "E_INVAL", bad
+    pageable = np.zeros(16 * 16, np.uint8)
+    with pytest.raises(lsmgnn.LsmgnnError) as e:
+        lsmgnn.FeatureCache(**dict(base, host_store=pageable.ctypes.data))
+    assert e.value.status == "E_INVAL"
+
+
+def test_deterministic_state():
+    cfg = W.CONFIGS[1]
+    wl, batches = config_stream(cfg)
+    store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes)
+    states = []
+    for rep in range(2):
+        log(f"case: determinism run {rep}")
+        c = lsmgnn.FeatureCache(cfg.num_nodes, cfg.row_bytes, store.buf, wl.static, cfg.cache.num_sets,
+                                cfg.cache.victim_rows, cfg.cache.lookahead, wl.max_batch)
+        dev = [torch.as_tensor(b).cuda() for b in batches]
+        for j in range(cfg.cache.lookahead + 1):
+            c.advance(dev[j])
+        for b in range(len(batches)):
+            c.gather(dev[b])
+            if b + cfg.cache.lookahead + 1 < len(batches):
+                c.advance(dev[b + cfg.cache.lookahead + 1])
+        states.append(c.export_state())
+        c.close()
+    assert np.array_equal(states[0]["tags"], states[1]["tags"])
+    assert np.array_equal(states[0]["ring_tags"], states[1]["ring_tags"])
+
+
+def test_provenance_hits_from_hbm_misses_from_store():
+    """After warm-up, overwrite the backing-store rows of every resident line
+    with a sentinel: hits must still return the original bytes (served from
+    HBM), while misses of non-resident nodes return the sentinel (served from
+    the store)."""
+    log("case: provenance")
+    n, S, rb = 4096, 64, 64
+    store = Store.random_bytes(n, rb, 11)
+    orig = store.np.copy()
+    stat = np.ones(n, np.uint32)
+    cache = lsmgnn.FeatureCache(n, rb, store.buf, stat, S, 0, 0, 1024)
+    warm = np.arange(0, 4096, 9)
+    cache.gather(torch.as_tensor(warm).cuda())
+    tags = cache.export_state()["tags"]
+    resident = tags[tags != lsmgnn.EMPTY].astype(np.int64)
+    absent = np.setdiff1d(np.arange(n), resident)[:200]
+    store.np[resident] = 0xAB
+    store.np[absent] = 0xCD
+    # hits alone (a hit changes nothing, so every probed line stays resident)
+    r = cache.gather(torch.as_tensor(resident[:300]).cuda(), outcome=True)
+    uq = r.unique.cpu().numpy()
+    assert (r.outcome.cpu().numpy() == lsmgnn.HIT).all()
+    assert np.array_equal(r.out.cpu().numpy(), orig[uq])
+    # then misses alone
+    r = cache.gather(torch.as_tensor(absent).cuda(), outcome=True)
+    assert (r.outcome.cpu().numpy() == lsmgnn.MISS).all()
+    assert (r.out.cpu().numpy() == 0xCD).all()
+    cache.close()

@@ -1,0 +1,79 @@
+"""CPU-side checks of the HIP library (no GPU needed): it loads, exports every
+entry point its header declares, rejects bad configurations before touching a
+device, and its host set-index helper agrees with the oracle's."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle.oracle import set_of as oracle_set_of
+from paper_2407_15264_amd import lsmgnn
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lsmgnn.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(lsmgnn.LIB_PATH):
+        from paper_2407_15264_amd import build
+        build.build_hip()
+    return lsmgnn.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lsmgnn_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("lsmgnn_cache_create", "lsmgnn_cache_destroy", "lsmgnn_gather", "lsmgnn_advance",
+                     "lsmgnn_stats", "lsmgnn_export_state"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    raw = ctypes.CDLL(lsmgnn.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(raw, name), name
+
+
+def test_strerror(L):
+    for code in range(7):
+        assert L.lsmgnn_strerror(code)
+    assert b"range" in L.lsmgnn_strerror(lsmgnn.E_RANGE)
+
+
+def test_set_index_helper_matches_oracle(L):
+    rng = np.random.default_rng(0)
+    for x in rng.integers(0, 1 << 32, 200):
+        for S in (1, 7, 2048, 13107, 6291456):
+            assert lsmgnn.set_of(int(x), S) == oracle_set_of(int(x), S)
+
+
+@pytest.mark.parametrize("bad", [dict(num_sets=0), dict(row_bytes=24), dict(lookahead=32), dict(max_batch=0),
+                                 dict(num_nodes=0), dict(num_nodes=1 << 32), dict(flags=1)])
+def test_bad_config_rejected_before_device(L, bad):
+    stat = np.ones(16, np.uint32)
+    store = np.zeros(16 * 16, np.uint8)
+    kw = dict(num_nodes=16, row_bytes=16, num_sets=2, victim_rows=2, max_batch=8, lookahead=1, near_threshold=0,
+              device=0, flags=0)
+    kw.update(bad)
+    cfg = lsmgnn.Config(kw["num_nodes"], kw["row_bytes"], kw["num_sets"], kw["victim_rows"], kw["max_batch"],
+                        kw["lookahead"], kw["near_threshold"], kw["device"], kw["flags"],
+                        ctypes.c_void_p(store.ctypes.data), ctypes.c_void_p(stat.ctypes.data))
+    h = ctypes.c_void_p()
+    assert L.lsmgnn_cache_create(ctypes.byref(cfg), ctypes.byref(h)) == lsmgnn.E_INVAL
+    assert not h.value
+
+
+def test_null_arguments(L):
+    h = ctypes.c_void_p()
+    assert L.lsmgnn_cache_create(None, ctypes.byref(h)) == lsmgnn.E_INVAL
+    assert L.lsmgnn_gather(None, None, 0, None, None, None, None, None, None) == lsmgnn.E_INVAL
+    assert L.lsmgnn_advance(None, None, 0, None) == lsmgnn.E_INVAL
+    assert L.lsmgnn_stats(None, None, None) == lsmgnn.E_INVAL
