@@ -1,0 +1,221 @@
+#!/usr/bin/env python3
+"""Benchmark of the per-minibatch feature gather through the MI355X cache.
+
+One step = one pass of the whole hot path over one minibatch: lsmgnn_gather on
+the minibatch's raw request IDs (dedup, set walk with hybrid eviction, victim
+ring, hit/miss/victim-hit row movement, fills) followed by lsmgnn_advance of the
+minibatch L+1 ahead.  All request streams are on the GPU and the feature table
+is in pinned host memory before the timed region starts.
+
+Default workload: R-MAT graph with 2^20 nodes and 2^24 edges (a, b, c, d =
+0.57, 0.19, 0.19, 0.05), fp32 x 256 features (1 GiB pinned host store), GraphSAGE
+sampling of 1024 seeds per minibatch with fanout (15, 10, 5), an 8-way cache
+holding 10% of the nodes, a victim ring of 5% of the nodes, lookahead 4.
+
+Prints one JSON line.  `value` is gathered feature bytes (unique rows x row
+bytes) per second over the timed steps; `roofline` rates the dominant data
+kernel against its bound, timed with HIP events on the gather's stream.
+"""
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "gathered feature GB/s per minibatch stream (% HBM/host-link roofline) + hit rate"
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
+PCIE5_X16_PEAK_GBPS = 64.0      # host link, published per direction
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def measure_ceilings(torch, lsmgnn, store_ptr, nbytes):
+    """Host-link and HBM ceilings in this run: pinned H2D DMA, zero-copy reads
+    and writes by the 128-bit copy kernel, and a device-to-device copy."""
+    dev = torch.device("cuda", 0)
+    nbytes = min(nbytes, 1 << 30) // 16 * 16
+    d0 = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    d1 = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    pinned = torch.empty(nbytes, dtype=torch.uint8).pin_memory()
+    res = {}
+
+    def best(fn, reps=5):
+        ts = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            ts.append(time.perf_counter() - t0)
+        return min(ts)
+
+    res["dma_h2d_GBps"] = nbytes / best(lambda: d0.copy_(pinned, non_blocking=True)) / 1e9
+    res["dma_d2h_GBps"] = nbytes / best(lambda: pinned.copy_(d0, non_blocking=True)) / 1e9
+    res["zero_copy_read_GBps"] = nbytes / best(lambda: lsmgnn.copy_bytes(d0.data_ptr(), store_ptr, nbytes)) / 1e9
+    res["zero_copy_write_GBps"] = nbytes / best(
+        lambda: lsmgnn.copy_bytes(pinned.data_ptr(), d0.data_ptr(), nbytes)) / 1e9
+    res["hbm_copy_GBps"] = 2 * nbytes / best(lambda: lsmgnn.copy_bytes(d1.data_ptr(), d0.data_ptr(), nbytes)) / 1e9
+    res["bytes"] = nbytes
+    del d0, d1, pinned
+    return res
+
+
+def cpu_baseline(cfg, wl, store_np, budget_s):
+    """The CPU oracle (single-threaded C) on the same stream from gather 0,
+    stopped after about budget_s seconds."""
+    from oracle.oracle import Oracle
+    L = cfg.cache.lookahead
+    o = Oracle(cfg.num_nodes, cfg.row_bytes, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, L,
+               store=store_np)
+    for j in range(L + 1):
+        o.advance(wl.batch(j))
+    t0 = time.perf_counter()
+    done, rows = 0, 0
+    while done < wl.num_batches - L - 1 and time.perf_counter() - t0 < budget_s:
+        r = o.gather(wl.batch(done), rows=True)
+        o.advance(wl.batch(done + L + 1))
+        rows += r["uniq"].size
+        done += 1
+    dt = time.perf_counter() - t0
+    o.close()
+    return {"value": rows * cfg.row_bytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"gathers 0..{done - 1} of the same stream ({done} minibatches, {rows} unique rows, "
+                      f"{dt:.1f} s), rows copied with memcpy from the host store",
+            "rows_per_s": rows / dt, "seconds_per_minibatch": dt / max(done, 1),
+            "cpu": platform.processor() or platform.machine()}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=180)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=2, help="workload shape (1, 2, 3 or 5)")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU: this build has no multi-GPU path (asked for --gpus "
+              f"{args.gpus}). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2407_15264_amd import lsmgnn
+    from paper_2407_15264_amd import workload as W
+
+    lsmgnn.lib()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    cfg = W.CONFIGS[args.config]
+    L = cfg.cache.lookahead
+    nb = max(cfg.batches, args.warmup + args.steps + L + 1)
+    t0 = time.perf_counter()
+    wl = W.Workload(cfg, nb)
+    log(f"[bench] workload {cfg.name}: {nb} minibatches generated in {time.perf_counter() - t0:.1f}s "
+        f"(mean {np.diff(wl.offsets).mean():.0f} requests)")
+    store = lsmgnn.PinnedBuffer(cfg.num_nodes * cfg.row_bytes)
+    W.fill_features(store.ptr, cfg.dim, cfg.elt_bytes, 0, cfg.num_nodes, cfg.seed)
+    store_np = store.numpy(np.uint8, (cfg.num_nodes, cfg.row_bytes))
+    log(f"[bench] pinned store {cfg.num_nodes * cfg.row_bytes / 2**30:.2f} GiB filled")
+
+    ceil = measure_ceilings(torch, lsmgnn, store.ptr, cfg.num_nodes * cfg.row_bytes)
+    log(f"[bench] ceilings: {json.dumps({k: round(v, 1) for k, v in ceil.items()})}")
+
+    dev = torch.device("cuda", 0)
+    batches = [torch.as_tensor(wl.batch(b)).to(dev) for b in range(nb)]
+    mb = wl.max_batch
+    cache = lsmgnn.FeatureCache(cfg.num_nodes, cfg.row_bytes, store, wl.static, cfg.cache.num_sets,
+                                cfg.cache.victim_rows, L, mb, near_threshold=cfg.cache.near_threshold)
+    out = torch.empty(mb * cfg.row_bytes, dtype=torch.uint8, device=dev)
+    uniq = torch.empty(mb, dtype=torch.int64, device=dev)
+    inv = torch.empty(mb, dtype=torch.int64, device=dev)
+    for j in range(L + 1):
+        cache.advance(batches[j])
+
+    def step(b):
+        r = cache.gather(batches[b], out=out, unique=uniq, inverse=inv)
+        cache.advance(batches[b + L + 1])
+        return r.n_unique
+
+    for b in range(args.warmup):
+        step(b)
+    _, tot0 = cache.stats()
+    cache.set_profiling(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    rows = 0
+    for b in range(args.warmup, args.warmup + args.steps):
+        rows += step(b)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    prof = cache.profile()
+    cache.set_profiling(False)
+    _, tot1 = cache.stats()
+    d = {k: tot1[k] - tot0[k] for k in tot1}
+    R = cfg.row_bytes
+    gbps = rows * R / dt / 1e9
+
+    # per-kernel rates from HIP events on the gather stream
+    kern = {}
+    for name, rows_k, ms, per_row, bound in (
+            ("hbm_copy", prof["hbm_copy_rows"], prof["hbm_copy_ms"], 2 * R, "hbm"),
+            ("host_fetch", prof["host_fetch_rows"], prof["host_fetch_ms"], R, "host_link"),
+            ("enqueue", prof["enqueue_rows"], prof["enqueue_ms"], R, "host_link"),
+            ("fill", prof["fill_rows"], prof["fill_ms"], 2 * R, "hbm")):
+        launches = max(prof[name + "_launches"], 1)
+        kern[name] = dict(ms_total=ms, launches=launches, rows=rows_k, avg_us=1e3 * ms / launches,
+                          bytes_per_launch=rows_k * per_row / launches,
+                          GBps=(rows_k * per_row / (ms / 1e3) / 1e9) if ms > 0 else 0.0, bound=bound)
+    dom = max(kern, key=lambda k: kern[k]["ms_total"])
+    kd = kern[dom]
+    link_peak = max(ceil["dma_h2d_GBps"], ceil["zero_copy_read_GBps"])
+    if kd["bound"] == "hbm":
+        roof = {"bound": "hbm", "achieved": kd["GBps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": kd["GBps"] / HBM_PEAK_GBPS, "traffic": None}
+    else:
+        peak = link_peak if dom == "host_fetch" else max(ceil["dma_d2h_GBps"], ceil["zero_copy_write_GBps"])
+        roof = {"bound": "host_link", "achieved": kd["GBps"], "peak": peak, "unit": "GB/s",
+                "frac": kd["GBps"] / peak, "traffic": None,
+                "peak_source": "measured in this run (best of pinned DMA and zero-copy kernel)",
+                "frac_of_published_pcie5_x16": kd["GBps"] / PCIE5_X16_PEAK_GBPS}
+    roof.update(kernel=dom, avg_launch_us=kd["avg_us"], bytes_per_launch=kd["bytes_per_launch"])
+    hb = kern["hbm_copy"]
+    roof_hbm = {"bound": "hbm", "kernel": "hbm_copy (hit rows cache->out)", "achieved": hb["GBps"],
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": hb["GBps"] / HBM_PEAK_GBPS,
+                "frac_of_measured_d2d": hb["GBps"] / ceil["hbm_copy_GBps"], "avg_launch_us": hb["avg_us"],
+                "bytes_per_launch": hb["bytes_per_launch"]}
+
+    res = {
+        "metric": METRIC, "value": gbps, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": 1e3 * dt / args.steps, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
+        "config": dict(cfg.describe(), feature_dtype=cfg.feature_dtype, minibatches_timed=args.steps,
+                       first_timed_minibatch=args.warmup),
+        "rows_per_s": rows / dt,
+        "hit_rate": d["hits"] / max(d["unique"], 1),
+        "victim_hit_rate": d["victim_hits"] / max(d["unique"], 1),
+        "miss_rate": d["misses"] / max(d["unique"], 1),
+        "unique_per_minibatch": d["unique"] / args.steps,
+        "requests_per_minibatch": d["requests"] / args.steps,
+        "roofline": roof,
+        "roofline_hbm": roof_hbm,
+        "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}
+                    for k, v in kern.items()},
+        "gather_ms_events": prof["gather_ms"] / max(prof["gathers"], 1),
+        "ceilings": ceil,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(cfg, wl, store_np, args.cpu_budget)
+        res["cpu_baseline"]["gpu_over_cpu"] = gbps / res["cpu_baseline"]["value"]
+    cache.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

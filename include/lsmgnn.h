@@ -150,6 +150,13 @@ lsmgnn_status lsmgnn_get_profile(const lsmgnn_cache *c, lsmgnn_profile *out);
 lsmgnn_status lsmgnn_host_alloc(uint64_t bytes, void **ptr);
 void lsmgnn_host_free(void *ptr);
 
+/* Calibration copy: bytes (a multiple of 16) from src to dst, both 16-byte
+   aligned, each either device memory or pinned host memory, with the same
+   128-bit access pattern as the gather's row copies.  Used to measure the
+   host-link and HBM ceilings the gather is compared against.  Synchronises
+   `stream`. */
+lsmgnn_status lsmgnn_copy_bytes(void *dst, const void *src, uint64_t bytes, void *stream);
+
 /* Set index the cache uses for node x (host-side helper, for tests). */
 uint64_t lsmgnn_set_of(uint64_t x, uint64_t num_sets);
 

@@ -41,29 +41,6 @@ __host__ __device__ __forceinline__ uint32_t set_index(uint64_t x, uint64_t S) {
 
 uint64_t set_of_host(uint64_t x, uint64_t num_sets) { return set_index(x, num_sets); }
 
-__device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
-  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-}
-
-// Wave-aggregated append: every lane of the wave must call this.  Returns the
-// list index for lanes with pred set (one atomic per wave).
-__device__ __forceinline__ uint32_t wave_append(bool pred, uint32_t *counter) {
-  const uint64_t m = __ballot(pred);
-  uint32_t base = 0;
-  if (m) {
-    const int leader = __ffsll((unsigned long long)m) - 1;
-    if ((int)__lane_id() == leader) base = atomicAdd(counter, (uint32_t)__popcll(m));
-    base = __shfl(base, leader);
-  }
-  return base + lanes_below(m);
-}
-
-__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-
 // Block-wide exclusive scan of one value per thread (kBlock threads).
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t &total) {
   __shared__ uint32_t wsum[kBlock / 64];
@@ -100,45 +77,135 @@ static inline unsigned grid_for(uint64_t work, uint64_t per_block, unsigned cap)
   if (b > cap) b = cap;
   return (unsigned)b;
 }
-constexpr unsigned kMaxGrid = 8192;
 
-// ------------------------------------------------------------------- begin
-__global__ void k_begin(Counters *cn) {
-  uint32_t *p = reinterpret_cast<uint32_t *>(cn);
-  for (unsigned i = threadIdx.x; i < sizeof(Counters) / 4; i += blockDim.x) p[i] = 0;
-}
-
-void launch_begin(Counters *cn, hipStream_t s) { hipLaunchKernelGGL(k_begin, dim3(1), dim3(64), 0, s, cn); }
-
-// ---------------------------------------------------------------- validate
-__global__ void k_validate(const int64_t *ids, uint32_t n, uint64_t N, Counters *cn) {
-  bool bad = false;
-  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
-    const int64_t x = ids[i];
-    bad |= (x < 0) | ((uint64_t)x >= N);
+// ------------------------------------------------------------------ finish
+// Last kernel of every call: add up the per-block partial counts, publish all
+// counters to pinned host memory and zero the device counters for the next
+// call (they start zeroed at create).
+__global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host, const uint32_t *part,
+                                                   StatGrids grids) {
+  __shared__ uint32_t sums[kNumStat];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  for (int st = wid; st < kNumStat; st += kBlock / 64) {  // one wave per counter
+    uint32_t v = 0;
+    for (uint32_t b = lane; b < grids.g[st]; b += 64) v += part[st * kMaxGrid + b];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    if (lane == 0) sums[st] = v;
   }
-  if (__ballot(bad) && __lane_id() == 0) atomicOr(&cn->err, 1u);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    Counters c = *cn;
+    c.hits = sums[kStHits];
+    c.fills = sums[kStFills];
+    c.evictions = sums[kStEvictions];
+    c.enqueued = sums[kStEnqueued];
+    c.dropped = sums[kStDropped];
+    c.n_fill = sums[kStFinal];
+    c.victim_hits = sums[kStVictimHits];
+    c.misses = sums[kStMisses];
+    c.n_hbm = sums[kStHbm];
+    c.n_host = sums[kStHost];
+    c.n_enq_copy = sums[kStEnqCopy];
+    *host = c;
+    *cn = Counters{};
+  }
 }
 
-void launch_validate(const int64_t *ids, uint64_t n, uint64_t N, Counters *cn, hipStream_t s) {
-  hipLaunchKernelGGL(k_validate, dim3(grid_for(n, kBlock, kMaxGrid)), dim3(kBlock), 0, s, ids, (uint32_t)n, N, cn);
+void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, const StatGrids &grids,
+                   hipStream_t s) {
+  hipLaunchKernelGGL(k_finish, dim3(1), dim3(kBlock), 0, s, cn, host, stat_part, grids);
+}
+
+// ------------------------------------------------------------- LDS combine
+// Per-block open-addressing table in LDS that ORs bit patterns per 32-bit key.
+// Hub nodes occur thousands of times per batch; combining them in LDS turns
+// those occurrences into one global atomic per block.  A block inserts at
+// most kCombineItems keys into kCombineSlots slots, so probing always ends.
+constexpr int kCombinePerThread = 4;
+constexpr int kCombineItems = kBlock * kCombinePerThread;
+constexpr int kCombineSlots = 2 * kCombineItems;
+
+struct LdsCombine {
+  uint32_t key[kCombineSlots];
+  uint32_t val[kCombineSlots];
+};
+
+__device__ __forceinline__ void combine_init(LdsCombine &t) {
+  for (int i = threadIdx.x; i < kCombineSlots; i += kBlock) {
+    t.key[i] = kEmpty;
+    t.val[i] = 0;
+  }
+  __syncthreads();
+}
+
+__device__ __forceinline__ void combine_or(LdsCombine &t, uint32_t key, uint32_t bits) {
+  uint32_t h = (key * 0x9e3779b1u) >> (32 - 11);  // log2(kCombineSlots) == 11
+  static_assert(kCombineSlots == 2048, "hash width");
+  for (;;) {
+    const uint32_t old = atomicCAS(&t.key[h], kEmpty, key);
+    if (old == kEmpty || old == key) {
+      atomicOr(&t.val[h], bits);
+      return;
+    }
+    h = (h + 1) & (kCombineSlots - 1);
+  }
 }
 
 // ------------------------------------------------------------------- dedup
-__global__ void k_mark(const int64_t *ids, uint32_t n, uint32_t *bitmap, const Counters *cn) {
-  if (cn->err) return;
-  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
-    const uint32_t x = (uint32_t)ids[i];
-    atomicOr(&bitmap[x >> 5], 1u << (x & 31u));
+// Validate and mark.  Out-of-range IDs set Counters::err; valid ones are still
+// marked, and the compaction kernel then clears the bitmap instead of
+// compacting it, so a rejected batch leaves no trace.  The same kernel clears
+// the window bit of the minibatch being gathered: that list is never consulted
+// again, whether or not this call succeeds.
+__global__ __launch_bounds__(kBlock) void k_mark(const int64_t *ids, uint32_t n, uint64_t N, uint32_t *bitmap,
+                                                 const int64_t *clear_ids, uint32_t clear_n, uint32_t clear_bit,
+                                                 uint32_t *mask, Counters *cn) {
+  __shared__ LdsCombine tab;
+  const uint32_t base = blockIdx.x * kCombineItems;
+  bool bad = false;
+  if (base < n) {
+    combine_init(tab);
+    for (int k = 0; k < kCombinePerThread; ++k) {
+      const uint32_t i = base + k * kBlock + threadIdx.x;
+      if (i < n) {
+        const int64_t xi = ids[i];
+        if (xi < 0 || (uint64_t)xi >= N) {
+          bad = true;
+        } else {
+          const uint32_t x = (uint32_t)xi;
+          combine_or(tab, x >> 5, 1u << (x & 31u));
+        }
+      }
+    }
+    __syncthreads();
+    for (int h = threadIdx.x; h < kCombineSlots; h += kBlock) {
+      const uint32_t w = tab.key[h];
+      if (w != kEmpty) atomicOr(&bitmap[w], tab.val[h]);
+    }
+  }
+  if (__ballot(bad) && __lane_id() == 0) atomicOr(&cn->err, 1u);
+  if (base < clear_n) {
+    __syncthreads();
+    combine_init(tab);
+    for (int k = 0; k < kCombinePerThread; ++k) {
+      const uint32_t i = base + k * kBlock + threadIdx.x;
+      if (i < clear_n) combine_or(tab, (uint32_t)clear_ids[i], 1u);
+    }
+    __syncthreads();
+    const uint32_t cb = 1u << clear_bit;
+    for (int h = threadIdx.x; h < kCombineSlots; h += kBlock) {
+      const uint32_t x = tab.key[h];
+      if (x != kEmpty) atomicAnd(&mask[x], ~cb);
+    }
   }
 }
 
 __device__ __forceinline__ void load_words(const uint32_t *bitmap, uint32_t (&w)[kWordsPerThread]) {
-  const u32x4 *p = reinterpret_cast<const u32x4 *>(bitmap + (size_t)blockIdx.x * kChunkWords +
-                                                    threadIdx.x * kWordsPerThread);
-  const u32x4 a = p[0], b = p[1];
+  static_assert(kWordsPerThread == 4, "one 128-bit load per thread");
+  const u32x4 a = *reinterpret_cast<const u32x4 *>(bitmap + (size_t)blockIdx.x * kChunkWords +
+                                                   threadIdx.x * kWordsPerThread);
   w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
-  w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
 }
 
 __global__ __launch_bounds__(kBlock) void k_chunk_popc(const uint32_t *bitmap, uint32_t *chunk_sums,
@@ -167,12 +234,18 @@ __global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uin
   if (threadIdx.x == 0) cn->n_unique = carry;
 }
 
-__global__ __launch_bounds__(kBlock) void k_compact(const uint32_t *bitmap, const uint32_t *chunk_off,
+__global__ __launch_bounds__(kBlock) void k_compact(uint32_t *bitmap, const uint32_t *chunk_off,
                                                     uint32_t *word_rank, uint32_t *uniq, int64_t *uniq_out,
                                                     const Counters *cn) {
-  if (cn->err) return;
   uint32_t w[kWordsPerThread];
   load_words(bitmap, w);
+  const size_t w0 = (size_t)blockIdx.x * kChunkWords + threadIdx.x * kWordsPerThread;
+  if (cn->err) {  // rejected batch: undo the marks
+#pragma unroll
+    for (int k = 0; k < kWordsPerThread; ++k)
+      if (w[k]) bitmap[w0 + k] = 0;
+    return;
+  }
   uint32_t c = 0;
 #pragma unroll
   for (int k = 0; k < kWordsPerThread; ++k) c += __popc(w[k]);
@@ -180,7 +253,6 @@ __global__ __launch_bounds__(kBlock) void k_compact(const uint32_t *bitmap, cons
   const uint32_t ex = block_exclusive_scan(c, tot);
   if (tot == 0) return;
   uint32_t pos = chunk_off[blockIdx.x] + ex;
-  const size_t w0 = (size_t)blockIdx.x * kChunkWords + threadIdx.x * kWordsPerThread;
 #pragma unroll
   for (int k = 0; k < kWordsPerThread; ++k) {
     uint32_t word = w[k];
@@ -198,52 +270,69 @@ __global__ __launch_bounds__(kBlock) void k_compact(const uint32_t *bitmap, cons
   }
 }
 
-__global__ void k_inverse(const int64_t *ids, uint32_t n, const uint32_t *bitmap, const uint32_t *word_rank,
-                          int64_t *inv, const Counters *cn) {
-  if (cn->err) return;
-  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
-    const uint32_t x = (uint32_t)ids[i];
-    const uint32_t wi = x >> 5, b = x & 31u;
-    inv[i] = (int64_t)(word_rank[wi] + __popc(bitmap[wi] & ((1u << b) - 1u)));
-  }
-}
-
-void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, Scratch &sc, int64_t *unique_out,
-                  int64_t *inverse, Counters *cn, hipStream_t s) {
-  const unsigned g = grid_for(n, kBlock, kMaxGrid);
-  hipLaunchKernelGGL(k_mark, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, d.bitmap, cn);
+void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, const int64_t *clear_ids, uint64_t clear_n,
+                  uint32_t clear_bit, Scratch &sc, int64_t *unique_out, Counters *cn, hipStream_t s) {
+  const uint64_t items = n > clear_n ? n : clear_n;
+  const unsigned g = (unsigned)((items + kCombineItems - 1) / kCombineItems);
+  hipLaunchKernelGGL(k_mark, dim3(g ? g : 1), dim3(kBlock), 0, s, ids, (uint32_t)n, d.N, d.bitmap, clear_ids,
+                     (uint32_t)clear_n, clear_bit, d.mask, cn);
   hipLaunchKernelGGL(k_chunk_popc, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.bitmap, d.chunk_sums, cn);
   hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, s, d.chunk_sums, (uint32_t)d.nchunks, cn);
   hipLaunchKernelGGL(k_compact, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.bitmap, d.chunk_sums,
                      d.word_rank, sc.uniq, unique_out, cn);
-  if (inverse)
-    hipLaunchKernelGGL(k_inverse, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, d.bitmap, d.word_rank, inverse,
-                       cn);
 }
 
 // ------------------------------------------------------------ group by set
-__global__ __launch_bounds__(kBlock) void k_claim(const DevState d, Scratch sc, Counters *cn) {
+// Every thread of the block must call this; returns the list index for
+// threads with pred set (one atomic per block).
+__device__ __forceinline__ uint32_t block_append(bool pred, uint32_t *counter) {
+  __shared__ uint32_t base;
+  uint32_t tot;
+  const uint32_t ex = block_exclusive_scan(pred ? 1u : 0u, tot);
+  if (threadIdx.x == 0 && tot) base = atomicAdd(counter, tot);
+  __syncthreads();
+  const uint32_t r = base + ex;
+  __syncthreads();
+  return r;
+}
+
+// Sum of a per-thread counter over the block, stored as this block's partial.
+__device__ __forceinline__ void block_count(uint32_t v, uint32_t *part, int slot) {
+  const uint32_t tot = block_sum(v);
+  if (threadIdx.x == 0) part[slot * kMaxGrid + blockIdx.x] = tot;
+}
+
+// Inverse index of every request (rank = unique IDs before its bitmap word +
+// set bits below it in the word), then per-set counts of the unique IDs.
+__global__ __launch_bounds__(kBlock) void k_inverse_claim(const DevState d, Scratch sc, const int64_t *ids,
+                                                          uint32_t n, int64_t *inv, Counters *cn) {
   if (cn->err) return;
+  if (inv) {
+    for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
+      const uint32_t x = (uint32_t)ids[i];
+      const uint32_t wi = x >> 5, b = x & 31u;
+      inv[i] = (int64_t)(d.word_rank[wi] + __popc(d.bitmap[wi] & ((1u << b) - 1u)));
+    }
+  }
   const uint32_t U = cn->n_unique;
-  const uint32_t lane = threadIdx.x & 63u;
-  for (uint32_t base = blockIdx.x * kBlock + (threadIdx.x - lane); base < U; base += gridDim.x * kBlock) {
-    const uint32_t u = base + lane;
+  for (uint32_t base = blockIdx.x * kBlock; base < U; base += gridDim.x * kBlock) {
+    const uint32_t u = base + threadIdx.x;
     bool claim = false;
     uint32_t s = 0;
     if (u < U) {
       const uint32_t x = sc.uniq[u];
       s = set_index(x, d.S);
       sc.uset[u] = s;
-      sc.ustat[u] = d.stat[x];
       const uint32_t old = atomicAdd(&d.set_count[s], 1u);
       sc.arrival[u] = old;
       claim = (old == 0);
       sc.flags[u] = 0;
       sc.dead[u] = 0;
       sc.this_q[u] = 0;
-      d.bitmap[x >> 5] = 0;  // every marked word holds only IDs of this batch
+      sc.fill_dst[u] = 0;
+      d.uidx[x] = u;
     }
-    const uint32_t i = wave_append(claim, &cn->n_touched);
+    const uint32_t i = block_append(claim, &cn->n_touched);
     if (claim) {
       sc.touched[i] = s;
       d.set_idx[s] = i;
@@ -274,6 +363,8 @@ __global__ void k_place(const DevState d, Scratch sc, const Counters *cn) {
     sc.seg[sc.seg_off[d.set_idx[sc.uset[u]]] + sc.arrival[u]] = u;
 }
 
+// Rank of u among the IDs of its set (all smaller unique indices come first);
+// lays out (u, ID, static score) contiguously per set for the walk.
 __global__ void k_rank(const DevState d, Scratch sc, const Counters *cn) {
   if (cn->err) return;
   const uint32_t U = cn->n_unique;
@@ -284,13 +375,18 @@ __global__ void k_rank(const DevState d, Scratch sc, const Counters *cn) {
     uint32_t r = 0;
     if (k > 1)
       for (uint32_t j = 0; j < k; ++j) r += sc.seg[off + j] < u ? 1u : 0u;
-    sc.sorted[off + r] = u;
+    const uint32_t x = sc.uniq[u];
+    sc.seg_u[off + r] = u;
+    sc.seg_x[off + r] = x;
+    sc.seg_st[off + r] = d.stat[x];
+    d.bitmap[x >> 5] = 0;  // the bitmap's last reader (the inverse) is done
   }
 }
 
-void launch_group_by_set(const DevState &d, uint64_t n, Scratch &sc, Counters *cn, hipStream_t s) {
+void launch_group_by_set(const DevState &d, const int64_t *ids, uint64_t n, int64_t *inverse, Scratch &sc,
+                         Counters *cn, hipStream_t s) {
   const unsigned g = grid_for(n, kBlock, kMaxGrid);
-  hipLaunchKernelGGL(k_claim, dim3(g), dim3(kBlock), 0, s, d, sc, cn);
+  hipLaunchKernelGGL(k_inverse_claim, dim3(g), dim3(kBlock), 0, s, d, sc, ids, (uint32_t)n, inverse, cn);
   hipLaunchKernelGGL(k_seg_alloc, dim3(g), dim3(kBlock), 0, s, d, sc, cn);
   hipLaunchKernelGGL(k_place, dim3(g), dim3(kBlock), 0, s, d, sc, cn);
   hipLaunchKernelGGL(k_rank, dim3(g), dim3(kBlock), 0, s, d, sc, cn);
@@ -312,135 +408,130 @@ __device__ __forceinline__ uint32_t level_of(uint32_t cls, bool ring_on) {
   return (ring_on && cls <= kClsFar) ? (cls ^ 1u) : cls;
 }
 
-template <typename T>
-__device__ __forceinline__ T pick_of(const T (&a)[kWays], int w) {
-  T r = a[0];
+// Minimum of a 64-bit key over the 8 lanes of a set's lane group.
+__device__ __forceinline__ uint64_t group_min(uint64_t v) {
 #pragma unroll
-  for (int q = 1; q < (int)kWays; ++q)
-    if (q == w) r = a[q];
-  return r;
+  for (int o = 1; o < (int)kWays; o <<= 1) {
+    const uint32_t lo = __shfl_xor((uint32_t)v, o, kWays);
+    const uint32_t hi = __shfl_xor((uint32_t)(v >> 32), o, kWays);
+    const uint64_t w = ((uint64_t)hi << 32) | lo;
+    v = w < v ? w : v;
+  }
+  return v;
 }
 
+// One set per group of 8 lanes, lane w owning way w.  The group walks the
+// set's IDs in ascending order (the per-set order of the definition); each
+// step is a ballot for the tag probe, a ballot for an empty way, and on a full
+// set a 3-step shuffle minimum of (level, static score, way).
 __global__ __launch_bounds__(kBlock) void k_set_walk(const DevState d, Scratch sc, uint32_t t, Counters *cn) {
   if (cn->err) return;
   const uint32_t Tn = cn->n_touched;
   const bool ring_on = d.V > 0;
   const uint32_t recent_lvl = level_of(kClsRecent, ring_on);
-  uint32_t c_hit = 0, c_fill = 0, c_evict = 0, c_enq = 0, c_drop = 0;
-  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < Tn; i += gridDim.x * kBlock) {
+  const uint32_t lane = threadIdx.x & 63u;
+  const uint32_t w = lane & (kWays - 1);   // the way this lane owns
+  const uint32_t gsh = lane & ~(kWays - 1);  // first lane of the group in the wave
+  const bool lead = w == 0;
+  uint32_t c_hit = 0, c_fill = 0, c_evict = 0, c_enq = 0, c_drop = 0, c_final = 0;
+  const uint32_t groups = gridDim.x * (kBlock / kWays);
+  for (uint32_t i = blockIdx.x * (kBlock / kWays) + (threadIdx.x / kWays); i < Tn; i += groups) {
     const uint32_t s = sc.touched[i];
     const uint32_t off = sc.seg_off[i];
     const uint32_t k = d.set_count[s];
-    d.set_count[s] = 0;
-    u32x4 *rp = reinterpret_cast<u32x4 *>(d.sets + s);
-    const u32x4 t0 = rp[0], t1 = rp[1], s0 = rp[2], s1 = rp[3], i0 = rp[4], i1 = rp[5];
-    uint32_t tag[kWays] = {t0.x, t0.y, t0.z, t0.w, t1.x, t1.y, t1.z, t1.w};
-    uint32_t st[kWays] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-    uint32_t ins[kWays] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
-    uint32_t cls[kWays], lvl[kWays];
-    int32_t last[kWays];
-#pragma unroll
-    for (int w = 0; w < (int)kWays; ++w) { cls[w] = kClsNone; lvl[w] = 0; last[w] = -1; }
-    uint32_t known = 0;  // ways whose class for this gather is known
+    SetRec *rec = d.sets + s;
+    uint32_t tag = rec->tag[w], st = rec->stat[w], ins = rec->ins[w];
+    uint32_t cls = kClsNone, lvl = 0;
+    bool known = false;  // class of this way for this gather computed
+    int32_t last = -1;   // unique index of this way's last fill
     bool dirty = false;
+    uint32_t pu = 0, px = 0, ps = 0;  // entry (j & ~7) + w of the segment, loaded 8 at a time
     for (uint32_t j = 0; j < k; ++j) {
-      const uint32_t u = sc.sorted[off + j];
-      const uint32_t x = sc.uniq[u];
-      int hw = -1;
-#pragma unroll
-      for (int w = 0; w < (int)kWays; ++w)
-        if (tag[w] == x) hw = w;
-      if (hw >= 0) {
-        sc.kind[u] = kKindHit;
-        sc.slot[u] = s * kWays + (uint32_t)hw;
-        ++c_hit;
+      if ((j & (kWays - 1)) == 0 && j + w < k) {
+        pu = sc.seg_u[off + j + w];
+        px = sc.seg_x[off + j + w];
+        ps = sc.seg_st[off + j + w];
+      }
+      const int src = (int)(j & (kWays - 1));
+      const uint32_t u = __shfl(pu, src, kWays);
+      const uint32_t x = __shfl(px, src, kWays);
+      const uint32_t xs = __shfl(ps, src, kWays);
+      const uint32_t hitm = (uint32_t)(__ballot(tag == x) >> gsh) & 0xffu;
+      if (hitm) {
+        if (lead) {
+          sc.kind[u] = kKindHit;
+          sc.slot[u] = s * kWays + (uint32_t)__builtin_ctz(hitm);
+          ++c_hit;
+        }
         continue;
       }
-      ++c_fill;
       dirty = true;
-      int pick = -1;
-#pragma unroll
-      for (int w = (int)kWays - 1; w >= 0; --w)
-        if (tag[w] == kEmpty) pick = w;
-      uint32_t z = kEmpty;
+      const uint32_t emptym = (uint32_t)(__ballot(tag == kEmpty) >> gsh) & 0xffu;
+      uint32_t pick, z = kEmpty;
       uint8_t f = 0;
-      if (pick < 0) {
-        // classes of batch-start residents, computed once per gather
-#pragma unroll
-        for (int w = 0; w < (int)kWays; ++w) {
-          if (!((known >> w) & 1u)) {
-            const uint32_t c = (ins[w] == t) ? kClsRecent : class_from_bits(d.mask[tag[w]], t, d.L, d.T);
-            cls[w] = c;
-            lvl[w] = level_of(c, ring_on);
+      if (emptym) {
+        pick = (uint32_t)__builtin_ctz(emptym);
+      } else {
+        if (!known) {  // batch-start resident: class from its announced-use bits
+          cls = (ins == t) ? kClsRecent : class_from_bits(d.mask[tag], t, d.L, d.T);
+          lvl = level_of(cls, ring_on);
+          known = true;
+        }
+        const uint64_t key = ((uint64_t)lvl << 35) | ((uint64_t)st << 3) | w;
+        pick = (uint32_t)(group_min(key) & 7u);
+        z = __shfl(tag, (int)pick, kWays);
+        const uint32_t pc = __shfl(cls, (int)pick, kWays);
+        if (lead) {
+          ++c_evict;
+          if (ring_on && (pc == kClsFar || pc == kClsNear)) {
+            f = kFlagEnqueue;
+            ++c_enq;
+          } else {
+            ++c_drop;
           }
         }
-        known = (1u << kWays) - 1u;
-        pick = 0;
-        uint32_t bl = lvl[0], bs = st[0];
-#pragma unroll
-        for (int w = 1; w < (int)kWays; ++w) {
-          if (lvl[w] < bl || (lvl[w] == bl && st[w] < bs)) {
-            pick = w;
-            bl = lvl[w];
-            bs = st[w];
-          }
-        }
-        z = pick_of(tag, pick);
-        const uint32_t pc = pick_of(cls, pick);
-        ++c_evict;
-        if (ring_on && (pc == kClsFar || pc == kClsNear)) {
-          f = kFlagEnqueue;
-          ++c_enq;
-        } else {
-          ++c_drop;
-        }
       }
-      sc.kind[u] = kKindFill;
-      sc.slot[u] = s * kWays + (uint32_t)pick;
-      sc.evicted[u] = z;
-      sc.flags[u] = f;
-      const uint32_t nst = sc.ustat[u];
-#pragma unroll
-      for (int w = 0; w < (int)kWays; ++w) {
-        if (w == pick) {
-          tag[w] = x;
-          st[w] = nst;
-          ins[w] = t;
-          cls[w] = kClsRecent;
-          lvl[w] = recent_lvl;
-          last[w] = (int32_t)u;
-        }
+      if (lead) {
+        ++c_fill;
+        sc.kind[u] = kKindFill;
+        sc.slot[u] = s * kWays + pick;
+        sc.evicted[u] = z;
+        sc.flags[u] = f;
       }
-      known |= 1u << pick;
+      if (w == pick) {
+        tag = x;
+        st = xs;
+        ins = t;
+        cls = kClsRecent;
+        lvl = recent_lvl;
+        known = true;
+        last = (int32_t)u;
+      }
     }
-#pragma unroll
-    for (int w = 0; w < (int)kWays; ++w)
-      if (last[w] >= 0) sc.flags[last[w]] |= kFlagFinal;
+    if (last >= 0) {  // the way's final occupant refills the cache row
+      sc.fill_dst[last] = s * kWays + w + 1;
+      ++c_final;
+    }
     if (dirty) {
-      rp[0] = u32x4{tag[0], tag[1], tag[2], tag[3]};
-      rp[1] = u32x4{tag[4], tag[5], tag[6], tag[7]};
-      rp[2] = u32x4{st[0], st[1], st[2], st[3]};
-      rp[3] = u32x4{st[4], st[5], st[6], st[7]};
-      rp[4] = u32x4{ins[0], ins[1], ins[2], ins[3]};
-      rp[5] = u32x4{ins[4], ins[5], ins[6], ins[7]};
+      rec->tag[w] = tag;
+      rec->stat[w] = st;
+      rec->ins[w] = ins;
     }
+    if (lead) d.set_count[s] = 0;
   }
-  c_hit = wave_sum(c_hit);
-  c_fill = wave_sum(c_fill);
-  c_evict = wave_sum(c_evict);
-  c_enq = wave_sum(c_enq);
-  c_drop = wave_sum(c_drop);
-  if (__lane_id() == 0) {
-    if (c_hit) atomicAdd(&cn->hits, c_hit);
-    if (c_fill) atomicAdd(&cn->fills, c_fill);
-    if (c_evict) atomicAdd(&cn->evictions, c_evict);
-    if (c_enq) atomicAdd(&cn->enqueued, c_enq);
-    if (c_drop) atomicAdd(&cn->dropped, c_drop);
-  }
+  block_count(c_hit, sc.stat_part, kStHits);
+  block_count(c_fill, sc.stat_part, kStFills);
+  block_count(c_evict, sc.stat_part, kStEvictions);
+  block_count(c_enq, sc.stat_part, kStEnqueued);
+  block_count(c_drop, sc.stat_part, kStDropped);
+  block_count(c_final, sc.stat_part, kStFinal);
 }
 
-void launch_set_walk(const DevState &d, uint64_t n, uint32_t t, Scratch &sc, Counters *cn, hipStream_t s) {
-  hipLaunchKernelGGL(k_set_walk, dim3(grid_for(n, kBlock, kMaxGrid)), dim3(kBlock), 0, s, d, sc, t, cn);
+void launch_set_walk(const DevState &d, uint64_t n, uint32_t t, Scratch &sc, Counters *cn, StatGrids &grids,
+                     hipStream_t s) {
+  const unsigned g = grid_for(n * kWays, kBlock, 1024);
+  hipLaunchKernelGGL(k_set_walk, dim3(g), dim3(kBlock), 0, s, d, sc, t, cn);
+  for (int st = kStHits; st <= kStFinal; ++st) grids.g[st] = g;
 }
 
 // ---------------------------------------------------------- ring sequences
@@ -475,8 +566,11 @@ __global__ __launch_bounds__(kBlock) void k_scan_top(uint32_t *part, Counters *c
   if (threadIdx.x == 0) cn->enq_total = carry;
 }
 
-__global__ __launch_bounds__(kBlock) void k_scan_final(const uint8_t *flags, const uint32_t *part,
-                                                       uint32_t *enq_before, const Counters *cn) {
+// Exclusive scan of the enqueue flags in ascending-ID order gives each
+// enqueue its ring sequence number.  An enqueued line requested later in the
+// same batch is told where its entry went.
+__global__ __launch_bounds__(kBlock) void k_scan_final(const DevState d, Scratch sc, uint64_t tail0,
+                                                       const Counters *cn) {
   if (cn->err) return;
   const uint32_t U = cn->n_unique;
   const uint32_t nb = (U + kScanChunk - 1) / kScanChunk;
@@ -486,173 +580,188 @@ __global__ __launch_bounds__(kBlock) void k_scan_final(const uint8_t *flags, con
     uint32_t c = 0;
 #pragma unroll
     for (int k = 0; k < kScanPerThread; ++k) {
-      f[k] = (base + k < U) ? (flags[base + k] & kFlagEnqueue) : 0u;
+      f[k] = (base + k < U) ? (sc.flags[base + k] & kFlagEnqueue) : 0u;
       c += f[k];
     }
     uint32_t tot;
-    uint32_t run = part[b] + block_exclusive_scan(c, tot);
+    uint32_t run = sc.scan_part[b] + block_exclusive_scan(c, tot);
 #pragma unroll
     for (int k = 0; k < kScanPerThread; ++k) {
-      if (base + k < U) enq_before[base + k] = run;
+      const uint32_t u = base + k;
+      if (u < U) {
+        sc.enq_before[u] = run;
+        if (f[k]) {
+          const uint32_t z = sc.evicted[u];
+          const uint32_t v = d.uidx[z];  // stale unless z is requested in this batch
+          if (v < U && v > u && sc.uniq[v] == z) {
+            sc.this_q[v] = tail0 + run + 1;
+            sc.this_enq[v] = u;
+          }
+        }
+      }
       run += f[k];
     }
   }
 }
 
-// For each enqueue of this batch whose line is requested later in the same
-// batch, tell that line where its entry went.
-__global__ void k_enq_map(Scratch sc, uint64_t tail0, const Counters *cn) {
-  if (cn->err) return;
-  const uint32_t U = cn->n_unique;
-  for (uint32_t u = blockIdx.x * kBlock + threadIdx.x; u < U; u += gridDim.x * kBlock) {
-    if (sc.kind[u] != kKindFill || !(sc.flags[u] & kFlagEnqueue)) continue;
-    const uint32_t z = sc.evicted[u];
-    uint32_t lo = 0, hi = U;
-    while (lo < hi) {
-      const uint32_t mid = (lo + hi) >> 1;
-      if (sc.uniq[mid] < z) lo = mid + 1; else hi = mid;
-    }
-    if (lo < U && lo > u && sc.uniq[lo] == z) {
-      sc.this_q[lo] = tail0 + sc.enq_before[u] + 1;
-      sc.this_enq[lo] = u;
-    }
-  }
-}
-
+// Victim-ring probe of every fill and the row source of every unique ID.
 __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc, uint64_t tail0, uint8_t *outcome,
                                                     Counters *cn) {
   if (cn->err) return;
   const uint32_t U = cn->n_unique;
   const uint64_t tail_end = tail0 + cn->enq_total;
-  const uint32_t lane = threadIdx.x & 63u;
-  uint32_t c_vhit = 0, c_miss = 0;
-  for (uint32_t base = blockIdx.x * kBlock + (threadIdx.x - lane); base < U; base += gridDim.x * kBlock) {
-    const uint32_t u = base + lane;
-    bool to_hbm = false, to_host = false, to_fill = false;
-    uint64_t hbm_src = 0, host_src = 0;
-    if (u < U) {
-      const uint8_t kind = sc.kind[u];
-      uint8_t oc = 0;  // LSMGNN_HIT
-      if (kind == kKindHit) {
-        to_hbm = true;
-        hbm_src = sc.slot[u];
-      } else {
-        const uint32_t x = sc.uniq[u];
-        uint64_t q = 0;
-        bool valid = false, same_batch = false;
-        const uint64_t tq = sc.this_q[u];
-        if (tq) {
-          q = tq - 1;
-          valid = true;
-          same_batch = true;
-        } else if (d.V) {
-          const uint64_t vp = d.vpos[x];
-          if (vp) {
-            q = vp - 1;
-            valid = d.ring_tag[q % d.V] == x;
-          }
+  uint32_t c_vhit = 0, c_miss = 0, c_hbm = 0, c_host = 0;
+  for (uint32_t u = blockIdx.x * kBlock + threadIdx.x; u < U; u += gridDim.x * kBlock) {
+    const uint8_t kind = sc.kind[u];
+    uint8_t oc = 0;  // LSMGNN_HIT
+    uint64_t code;
+    if (kind == kKindHit) {
+      code = kSrcHbm | sc.slot[u];
+      ++c_hbm;
+    } else {
+      const uint32_t x = sc.uniq[u];
+      uint64_t q = 0;
+      bool valid = false, same_batch = false;
+      const uint64_t tq = sc.this_q[u];
+      if (tq) {
+        q = tq - 1;
+        valid = true;
+        same_batch = true;
+      } else if (d.V) {
+        const uint64_t vp = d.vpos[x];
+        if (vp) {
+          q = vp - 1;
+          valid = d.ring_tag[q % d.V] == x;
         }
-        const bool live = valid && q + d.V >= tail0 + sc.enq_before[u];
-        if (live) {
-          ++c_vhit;
-          oc = 1;  // LSMGNN_VICTIM_HIT
-          if (same_batch) {
-            // evicted earlier in this batch: its row is still in the cache
-            // slot the evicting fill took, which no copy has overwritten yet
-            const uint32_t e = sc.this_enq[u];
-            to_hbm = true;
-            hbm_src = sc.slot[e];
-            sc.dead[e] = 1;
-          } else {
-            to_host = true;
-            host_src = kSrcRing | (q % d.V);
-            // no entry of this batch reuses the slot: remove the entry now
-            if (q + d.V >= tail_end) d.ring_tag[q % d.V] = kEmpty;
-          }
-        } else {
-          ++c_miss;
-          oc = 2;  // LSMGNN_MISS
-          to_host = true;
-          host_src = x;
-        }
-        to_fill = (sc.flags[u] & kFlagFinal) != 0;
       }
-      if (outcome) outcome[u] = oc;
+      const bool live = valid && q + d.V >= tail0 + sc.enq_before[u];
+      if (live) {
+        ++c_vhit;
+        oc = 1;  // LSMGNN_VICTIM_HIT
+        if (same_batch) {
+          // evicted earlier in this batch: its row is still in the cache slot
+          // the evicting fill took, which no copy has overwritten yet
+          const uint32_t e = sc.this_enq[u];
+          code = kSrcHbm | sc.slot[e];
+          sc.dead[e] = 1;
+          ++c_hbm;
+        } else if (q + d.V >= tail_end) {
+          // no enqueue of this batch reuses the slot: read the ring row and
+          // remove the entry now
+          code = kSrcRing | (q % d.V);
+          d.ring_tag[q % d.V] = kEmpty;
+          ++c_host;
+        } else {
+          // the slot is rewritten by an enqueue of this batch, which runs
+          // concurrently with the host fetch: take the identical bytes from
+          // the backing store instead
+          code = kSrcStore | x;
+          ++c_host;
+        }
+      } else {
+        ++c_miss;
+        oc = 2;  // LSMGNN_MISS
+        code = kSrcStore | x;
+        ++c_host;
+      }
     }
-    const uint32_t ih = wave_append(to_hbm, &cn->n_hbm);
-    if (to_hbm) { sc.hbm_a[ih] = u; sc.hbm_b[ih] = hbm_src; }
-    const uint32_t io = wave_append(to_host, &cn->n_host);
-    if (to_host) { sc.host_a[io] = u; sc.host_b[io] = host_src; }
-    const uint32_t iff = wave_append(to_fill, &cn->n_fill);
-    if (to_fill) { sc.fill_a[iff] = sc.slot[u]; sc.fill_b[iff] = u; }
+    sc.src[u] = code;
+    if (outcome) outcome[u] = oc;
   }
-  c_vhit = wave_sum(c_vhit);
-  c_miss = wave_sum(c_miss);
-  if (__lane_id() == 0) {
-    if (c_vhit) atomicAdd(&cn->victim_hits, c_vhit);
-    if (c_miss) atomicAdd(&cn->misses, c_miss);
-  }
+  block_count(c_vhit, sc.stat_part, kStVictimHits);
+  block_count(c_miss, sc.stat_part, kStMisses);
+  block_count(c_hbm, sc.stat_part, kStHbm);
+  block_count(c_host, sc.stat_part, kStHost);
 }
 
-// Ring bookkeeping for this batch's enqueues; queue the row copies of the
+// Ring bookkeeping for this batch's enqueues; marks the row copies of the
 // entries that are still in the ring at the end of the batch.
 __global__ __launch_bounds__(kBlock) void k_enq_finalize(const DevState d, Scratch sc, uint64_t tail0,
                                                          Counters *cn) {
   if (cn->err) return;
   const uint32_t U = cn->n_unique;
   const uint64_t tail_end = tail0 + cn->enq_total;
-  const uint32_t lane = threadIdx.x & 63u;
-  for (uint32_t base = blockIdx.x * kBlock + (threadIdx.x - lane); base < U; base += gridDim.x * kBlock) {
-    const uint32_t u = base + lane;
-    bool copy = false;
-    uint64_t ring_slot = 0;
-    if (u < U && sc.kind[u] == kKindFill && (sc.flags[u] & kFlagEnqueue)) {
+  uint32_t c_copy = 0;
+  for (uint32_t u = blockIdx.x * kBlock + threadIdx.x; u < U; u += gridDim.x * kBlock) {
+    uint64_t dst = 0;
+    if (sc.kind[u] == kKindFill && (sc.flags[u] & kFlagEnqueue)) {
       const uint64_t q = tail0 + sc.enq_before[u];
       const uint32_t z = sc.evicted[u];
       d.vpos[z] = q + 1;
       if (q + d.V >= tail_end) {
-        ring_slot = q % d.V;
         if (sc.dead[u]) {
-          d.ring_tag[ring_slot] = kEmpty;
+          d.ring_tag[q % d.V] = kEmpty;
         } else {
-          d.ring_tag[ring_slot] = z;
-          copy = true;
+          d.ring_tag[q % d.V] = z;
+          dst = (q % d.V) + 1;
+          ++c_copy;
         }
       }
     }
-    const uint32_t ie = wave_append(copy, &cn->n_enq_copy);
-    if (copy) { sc.enq_a[ie] = sc.slot[u]; sc.enq_b[ie] = ring_slot; }
+    sc.ring_dst[u] = dst;
   }
+  block_count(c_copy, sc.stat_part, kStEnqCopy);
 }
 
 void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t tail0, Scratch &sc, uint8_t *outcome,
-                         Counters *cn, hipStream_t s) {
+                         Counters *cn, StatGrids &grids, hipStream_t s) {
   const unsigned g = grid_for(n, kBlock, kMaxGrid);
   const unsigned gs = grid_for(n, kScanChunk, kMaxGrid);
   if (d.V) {
     hipLaunchKernelGGL(k_scan_partial, dim3(gs), dim3(kBlock), 0, s, sc.flags, sc.scan_part, cn);
     hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kBlock), 0, s, sc.scan_part, cn);
-    hipLaunchKernelGGL(k_scan_final, dim3(gs), dim3(kBlock), 0, s, sc.flags, sc.scan_part, sc.enq_before, cn);
-    hipLaunchKernelGGL(k_enq_map, dim3(g), dim3(kBlock), 0, s, sc, tail0, cn);
+    hipLaunchKernelGGL(k_scan_final, dim3(gs), dim3(kBlock), 0, s, d, sc, tail0, cn);
   }
   hipLaunchKernelGGL(k_resolve, dim3(g), dim3(kBlock), 0, s, d, sc, tail0, outcome, cn);
-  if (d.V) hipLaunchKernelGGL(k_enq_finalize, dim3(g), dim3(kBlock), 0, s, d, sc, tail0, cn);
+  for (int st = kStVictimHits; st <= kStHost; ++st) grids.g[st] = g;
+  if (d.V) {
+    hipLaunchKernelGGL(k_enq_finalize, dim3(g), dim3(kBlock), 0, s, d, sc, tail0, cn);
+    grids.g[kStEnqCopy] = g;
+  }
 }
 
 // -------------------------------------------------------------- row copies
-// Work item w = (entry e, 16-byte vector v) with consecutive lanes on
-// consecutive vectors of one row, so each wave moves whole rows with 128-bit
-// accesses; every lane keeps kUnroll vectors in flight before storing.
+// Work item w = (unique index e, 16-byte vector v): consecutive lanes take
+// consecutive vectors of one row, so a wave moves whole rows with 128-bit
+// accesses, and each lane keeps kUnroll vectors in flight before storing.
+// Each mode reads the per-unique descriptor and skips rows it does not own.
 constexpr int kUnroll = 4;
 
+template <CopyMode M>
+__device__ __forceinline__ bool row_ends(const DevState &d, const Scratch &sc, uint8_t *out, uint32_t e,
+                                         const uint8_t *&src, uint8_t *&dst) {
+  const uint64_t R = d.R;
+  if constexpr (M == CopyMode::kHbmToOut) {
+    const uint64_t code = sc.src[e];
+    if ((code & ~kSrcIndex) != kSrcHbm) return false;
+    src = d.rows + (code & kSrcIndex) * R;
+    dst = out + (uint64_t)e * R;
+  } else if constexpr (M == CopyMode::kHostToOut) {
+    const uint64_t code = sc.src[e];
+    const uint64_t place = code & ~kSrcIndex;
+    if (place == kSrcHbm) return false;
+    src = (place == kSrcRing ? d.ring_rows : d.store) + (code & kSrcIndex) * R;
+    dst = out + (uint64_t)e * R;
+  } else if constexpr (M == CopyMode::kCacheToRing) {
+    const uint64_t rd = sc.ring_dst[e];
+    if (!rd) return false;
+    src = d.rows + (uint64_t)sc.slot[e] * R;
+    dst = d.ring_rows + (rd - 1) * R;
+  } else {
+    const uint32_t fd = sc.fill_dst[e];
+    if (!fd) return false;
+    src = out + (uint64_t)e * R;
+    dst = d.rows + (uint64_t)(fd - 1) * R;
+  }
+  return true;
+}
+
 template <CopyMode M, bool kPow2>
-__global__ __launch_bounds__(kBlock) void k_copy(const DevState d, const uint32_t *a, const uint64_t *b,
-                                                 const uint32_t *count, uint8_t *out, uint32_t nvec,
+__global__ __launch_bounds__(kBlock) void k_copy(const DevState d, Scratch sc, uint8_t *out, uint32_t nvec,
                                                  uint32_t vshift, const Counters *cn) {
   if (cn->err) return;
-  const uint64_t total = (uint64_t)(*count) * nvec;
+  const uint64_t total = (uint64_t)cn->n_unique * nvec;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-  const uint64_t R = d.R;
   for (uint64_t w0 = (uint64_t)blockIdx.x * kBlock + threadIdx.x; w0 < total; w0 += stride * kUnroll) {
     u32x4 v[kUnroll];
     uint8_t *dst[kUnroll];
@@ -665,22 +774,10 @@ __global__ __launch_bounds__(kBlock) void k_copy(const DevState d, const uint32_
         const uint64_t byte = (w - (uint64_t)e * nvec) * 16u;
         const uint8_t *src;
         uint8_t *dp;
-        if constexpr (M == CopyMode::kHbmToOut) {
-          src = d.rows + b[e] * R;
-          dp = out + (uint64_t)a[e] * R;
-        } else if constexpr (M == CopyMode::kHostToOut) {
-          const uint64_t code = b[e];
-          src = (code & kSrcRing) ? d.ring_rows + (code & ~kSrcRing) * R : d.store + code * R;
-          dp = out + (uint64_t)a[e] * R;
-        } else if constexpr (M == CopyMode::kCacheToRing) {
-          src = d.rows + (uint64_t)a[e] * R;
-          dp = d.ring_rows + b[e] * R;
-        } else {
-          src = out + b[e] * R;
-          dp = d.rows + (uint64_t)a[e] * R;
+        if (row_ends<M>(d, sc, out, e, src, dp)) {
+          v[k] = *reinterpret_cast<const u32x4 *>(src + byte);
+          dst[k] = dp + byte;
         }
-        v[k] = *reinterpret_cast<const u32x4 *>(src + byte);
-        dst[k] = dp + byte;
       }
     }
 #pragma unroll
@@ -689,57 +786,124 @@ __global__ __launch_bounds__(kBlock) void k_copy(const DevState d, const uint32_
   }
 }
 
+// Grid caps.  The host-link kernels need only a few hundred KB in flight to
+// cover PCIe latency; small grids leave wave slots for the kernels that run
+// beside them (hit copy, enqueue copy).
+#ifndef LSM_HOST_GRID
+#define LSM_HOST_GRID 256
+#endif
+#ifndef LSM_ENQ_GRID
+#define LSM_ENQ_GRID 256
+#endif
+#ifndef LSM_HBM_GRID
+#define LSM_HBM_GRID 2048
+#endif
+
 template <CopyMode M>
-static void launch_copy_mode(const DevState &d, uint64_t max_rows, const uint32_t *a, const uint64_t *b,
-                             const uint32_t *count, uint8_t *out, const Counters *cn, hipStream_t s) {
+static void launch_copy_mode(const DevState &d, uint64_t max_rows, const Scratch &sc, uint8_t *out,
+                             const Counters *cn, hipStream_t s) {
   const uint32_t nvec = (uint32_t)(d.R / 16);
   const bool pow2 = (nvec & (nvec - 1)) == 0;
   const uint32_t vshift = pow2 ? (uint32_t)__builtin_ctz(nvec) : 0u;
-  const unsigned g = grid_for(max_rows * nvec, (uint64_t)kBlock * kUnroll, 4096);
+  const unsigned cap = M == CopyMode::kHostToOut ? LSM_HOST_GRID
+                       : M == CopyMode::kCacheToRing ? LSM_ENQ_GRID : LSM_HBM_GRID;
+  const unsigned g = grid_for(max_rows * nvec, (uint64_t)kBlock * kUnroll, cap);
   if (pow2)
-    hipLaunchKernelGGL((k_copy<M, true>), dim3(g), dim3(kBlock), 0, s, d, a, b, count, out, nvec, vshift, cn);
+    hipLaunchKernelGGL((k_copy<M, true>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift, cn);
   else
-    hipLaunchKernelGGL((k_copy<M, false>), dim3(g), dim3(kBlock), 0, s, d, a, b, count, out, nvec, vshift, cn);
+    hipLaunchKernelGGL((k_copy<M, false>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift, cn);
 }
 
-void launch_copy(CopyMode mode, const DevState &d, uint64_t max_rows, const uint32_t *a, const uint64_t *b,
-                 const uint32_t *count, uint8_t *out, Counters *cn, hipStream_t s) {
+void launch_copy(CopyMode mode, const DevState &d, uint64_t max_rows, const Scratch &sc, uint8_t *out,
+                 const Counters *cn, hipStream_t s) {
   switch (mode) {
-    case CopyMode::kHbmToOut: launch_copy_mode<CopyMode::kHbmToOut>(d, max_rows, a, b, count, out, cn, s); break;
-    case CopyMode::kHostToOut: launch_copy_mode<CopyMode::kHostToOut>(d, max_rows, a, b, count, out, cn, s); break;
-    case CopyMode::kCacheToRing: launch_copy_mode<CopyMode::kCacheToRing>(d, max_rows, a, b, count, out, cn, s); break;
-    case CopyMode::kOutToCache: launch_copy_mode<CopyMode::kOutToCache>(d, max_rows, a, b, count, out, cn, s); break;
+    case CopyMode::kHbmToOut: launch_copy_mode<CopyMode::kHbmToOut>(d, max_rows, sc, out, cn, s); break;
+    case CopyMode::kHostToOut: launch_copy_mode<CopyMode::kHostToOut>(d, max_rows, sc, out, cn, s); break;
+    case CopyMode::kCacheToRing: launch_copy_mode<CopyMode::kCacheToRing>(d, max_rows, sc, out, cn, s); break;
+    case CopyMode::kOutToCache: launch_copy_mode<CopyMode::kOutToCache>(d, max_rows, sc, out, cn, s); break;
   }
+}
+
+// ------------------------------------------------------------ calibration
+// Plain contiguous copy with the same 128-bit access pattern and unrolling as
+// the row copies; used to measure the host-link and HBM ceilings and to scale
+// hardware byte counters against a copy of known size.
+__global__ __launch_bounds__(kBlock) void k_copy_plain(const u32x4 *src, u32x4 *dst, uint64_t nvec) {
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  for (uint64_t w0 = (uint64_t)blockIdx.x * kBlock + threadIdx.x; w0 < nvec; w0 += stride * kUnroll) {
+    u32x4 v[kUnroll];
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      const uint64_t w = w0 + k * stride;
+      if (w < nvec) v[k] = src[w];
+    }
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      const uint64_t w = w0 + k * stride;
+      if (w < nvec) dst[w] = v[k];
+    }
+  }
+}
+
+void launch_copy_plain(const void *src, void *dst, uint64_t bytes, hipStream_t s) {
+  const uint64_t nvec = bytes / 16;
+  hipLaunchKernelGGL(k_copy_plain, dim3(grid_for(nvec, (uint64_t)kBlock * kUnroll, 4096)), dim3(kBlock), 0, s,
+                     static_cast<const u32x4 *>(src), static_cast<u32x4 *>(dst), nvec);
 }
 
 // ------------------------------------------------------------------ window
-__global__ void k_window_set(const int64_t *ids, uint32_t n, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
-                             const Counters *cn) {
-  if (cn->err) return;
+// Announce: validate the IDs and, when the list is recorded, copy it into its
+// window slot and set the minibatch's bit for every ID (combined per block in
+// LDS, so repeated IDs cost one global atomic per block).
+__global__ __launch_bounds__(kBlock) void k_window_set(const int64_t *ids, uint32_t n, uint64_t N, uint32_t bit,
+                                                       uint32_t *mask, int64_t *slot_ids, int record,
+                                                       Counters *cn) {
+  __shared__ LdsCombine tab;
+  const uint32_t base = blockIdx.x * kCombineItems;
+  bool bad = false;
+  if (record) combine_init(tab);
+  for (int k = 0; k < kCombinePerThread; ++k) {
+    const uint32_t i = base + k * kBlock + threadIdx.x;
+    if (i < n) {
+      const int64_t x = ids[i];
+      if (x < 0 || (uint64_t)x >= N) {
+        bad = true;
+      } else if (record) {
+        slot_ids[i] = x;
+        combine_or(tab, (uint32_t)x, 1u);
+      }
+    }
+  }
+  if (record) {
+    __syncthreads();
+    const uint32_t b = 1u << bit;
+    for (int h = threadIdx.x; h < kCombineSlots; h += kBlock) {
+      const uint32_t x = tab.key[h];
+      if (x != kEmpty) atomicOr(&mask[x], b);
+    }
+  }
+  if (__ballot(bad) && __lane_id() == 0) atomicOr(&cn->err, 1u);
+}
+
+// After a rejected announcement: clear the bit again (it was clear before,
+// since the minibatch that last used this bit position has been gathered).
+__global__ void k_window_rollback(const int64_t *ids, uint32_t n, uint64_t N, uint32_t bit, uint32_t *mask,
+                                  const Counters *cn) {
+  if (!cn->err) return;
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
     const int64_t x = ids[i];
-    slot_ids[i] = x;
-    atomicOr(&mask[x], 1u << bit);
+    if (x >= 0 && (uint64_t)x < N) atomicAnd(&mask[x], ~(1u << bit));
   }
 }
 
-__global__ void k_window_clear(const int64_t *slot_ids, uint32_t n, uint32_t bit, uint32_t *mask,
-                               const Counters *cn) {
-  if (cn->err) return;
-  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock)
-    atomicAnd(&mask[slot_ids[i]], ~(1u << bit));
-}
-
-void launch_window_set(const int64_t *ids, uint64_t n, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
-                       Counters *cn, hipStream_t s) {
-  hipLaunchKernelGGL(k_window_set, dim3(grid_for(n, kBlock, kMaxGrid)), dim3(kBlock), 0, s, ids, (uint32_t)n, bit,
-                     mask, slot_ids, cn);
-}
-
-void launch_window_clear(const int64_t *slot_ids, uint64_t n, uint32_t bit, uint32_t *mask, Counters *cn,
-                         hipStream_t s) {
-  hipLaunchKernelGGL(k_window_clear, dim3(grid_for(n, kBlock, kMaxGrid)), dim3(kBlock), 0, s, slot_ids,
-                     (uint32_t)n, bit, mask, cn);
+void launch_window_set(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
+                       bool record, Counters *cn, hipStream_t s) {
+  const unsigned g = (unsigned)((n + kCombineItems - 1) / kCombineItems);
+  hipLaunchKernelGGL(k_window_set, dim3(g ? g : 1), dim3(kBlock), 0, s, ids, (uint32_t)n, N, bit, mask, slot_ids,
+                     record ? 1 : 0, cn);
+  if (record)
+    hipLaunchKernelGGL(k_window_rollback, dim3(grid_for(n, kBlock, kMaxGrid)), dim3(kBlock), 0, s, ids,
+                       (uint32_t)n, N, bit, mask, cn);
 }
 
 }  // namespace lsm

@@ -10,7 +10,7 @@ namespace lsm {
 constexpr uint32_t kWays = 8;
 constexpr uint32_t kEmpty = 0xffffffffu;
 constexpr int kBlock = 256;          // threads per block for every kernel
-constexpr int kWordsPerThread = 8;   // dedup bitmap words per thread
+constexpr int kWordsPerThread = 4;   // dedup bitmap words per thread
 constexpr int kChunkWords = kBlock * kWordsPerThread;  // bitmap words per block
 constexpr int kScanPerThread = 8;    // flags per thread in the enqueue scan
 constexpr int kScanChunk = kBlock * kScanPerThread;
@@ -20,9 +20,12 @@ enum : uint32_t { kClsNone = 0, kClsFar = 1, kClsRecent = 2, kClsNear = 3 };
 // per-unique kinds from the set walk
 enum : uint8_t { kKindHit = 0, kKindFill = 1 };
 // per-unique flags
-enum : uint8_t { kFlagEnqueue = 1, kFlagFinal = 2 };
-// host-fetch source code: bit 63 set = victim-ring row, else backing-store row
-constexpr uint64_t kSrcRing = 1ull << 63;
+enum : uint8_t { kFlagEnqueue = 1 };
+// per-unique row source: top two bits select the place, the rest index it
+constexpr uint64_t kSrcHbm = 0ull << 62;    // cache slot in HBM
+constexpr uint64_t kSrcStore = 1ull << 62;  // backing-store row (pinned host)
+constexpr uint64_t kSrcRing = 2ull << 62;   // victim-ring row (pinned host)
+constexpr uint64_t kSrcIndex = (1ull << 62) - 1;
 
 // One set = one 128-byte record (one L2 line): the 8 resident node IDs, their
 // static scores and the gather index at which each was inserted.
@@ -34,14 +37,29 @@ struct alignas(128) SetRec {
 };
 static_assert(sizeof(SetRec) == 128, "set record must be one 128-byte line");
 
-// Device counters of one call; zeroed by the first kernel of each call.
+// Per-block partial counts: each block of a counting kernel stores its sums
+// with plain stores and the last kernel of the call adds them up (no atomics
+// on one shared line, which serialize across the GPU).
+enum StatSlot : int {
+  kStHits, kStFills, kStEvictions, kStEnqueued, kStDropped, kStFinal,  // set walk
+  kStVictimHits, kStMisses, kStHbm, kStHost,                           // resolve
+  kStEnqCopy,                                                          // enqueue finalize
+  kNumStat
+};
+constexpr unsigned kMaxGrid = 8192;  // grid cap of every grid-stride kernel
+struct StatGrids {
+  uint32_t g[kNumStat];  // blocks that wrote each slot in this call (0 = none)
+};
+
+// Device counters of one call; zero at create, published and re-zeroed by the
+// last kernel of every call.
 struct Counters {
   uint32_t err;         // nonzero once any ID was out of range
   uint32_t n_unique;
   uint32_t n_touched;   // distinct sets touched by the batch
   uint32_t seg_cursor;
   uint32_t hits, fills, evictions, enqueued, dropped, victim_hits, misses;
-  uint32_t n_hbm, n_host, n_enq_copy, n_fill;
+  uint32_t n_hbm, n_host, n_enq_copy, n_fill;  // rows per data kernel
   uint32_t enq_total;
   uint32_t pad[16];
 };
@@ -50,26 +68,26 @@ struct Counters {
 struct Scratch {
   uint32_t *uniq;       // ascending unique IDs
   uint32_t *uset;       // set of uniq[u]
-  uint32_t *ustat;      // static score of uniq[u]
   uint32_t *arrival;    // arrival order of u within its set
   uint32_t *touched;    // touched set list (arbitrary order)
   uint32_t *seg_off;    // segment offset of touched[i]
   uint32_t *seg;        // u grouped by set, arrival order
-  uint32_t *sorted;     // u grouped by set, ascending within the set
+  uint32_t *seg_u;      // u grouped by set, ascending within the set
+  uint32_t *seg_x;      // uniq[seg_u[.]]
+  uint32_t *seg_st;     // static score of seg_x[.]
   uint8_t *kind;
   uint8_t *flags;
   uint8_t *dead;        // enqueue entry whose line was victim-hit in the same batch
   uint32_t *slot;       // cache slot (set*8+way) hit or filled by u
   uint32_t *evicted;    // node evicted by u's fill, or kEmpty
   uint32_t *enq_before; // enqueues by unique IDs below u in this batch
-  uint32_t *scan_part;  // ceil(max_batch / kScanChunk) + 1 partial sums
+  uint32_t *scan_part;  // ceil(max_batch / kScanChunk) + 2 partial sums
   uint64_t *this_q;     // 1 + ring sequence of u's own enqueue in this batch, or 0
   uint32_t *this_enq;   // the unique index that enqueued u in this batch
-  // work lists: (a, b) pairs
-  uint32_t *hbm_a; uint64_t *hbm_b;    // out row u  <- cache slot
-  uint32_t *host_a; uint64_t *host_b;  // out row u  <- store row / ring row
-  uint32_t *enq_a; uint64_t *enq_b;    // cache slot -> ring row
-  uint32_t *fill_a; uint64_t *fill_b;  // cache slot <- out row u
+  uint64_t *src;        // row source of out row u (kSrc* code)
+  uint64_t *ring_dst;   // 1 + ring slot that receives the row u evicted, or 0
+  uint32_t *fill_dst;   // 1 + cache slot that out row u refills (the way's final fill), or 0
+  uint32_t *stat_part;  // [kNumStat][kMaxGrid] per-block partial counts
 };
 
 struct DevState {
@@ -86,6 +104,8 @@ struct DevState {
   uint32_t *chunk_sums;  // [nchunks]
   uint32_t *set_count;   // [S] (all zero between calls)
   uint32_t *set_idx;     // [S]
+  uint32_t *uidx;        // [N] unique index of the node in the current batch
+                         //     (meaningful only where uniq[uidx[x]] == x)
   uint64_t N, R, S, V;
   uint64_t nchunks;
   uint32_t L, T;
@@ -94,20 +114,21 @@ struct DevState {
 enum class CopyMode { kHbmToOut, kHostToOut, kCacheToRing, kOutToCache };
 
 // ----- launchers (gather_kernels.hip) -----
-void launch_begin(Counters *cn, hipStream_t s);
-void launch_validate(const int64_t *ids, uint64_t n, uint64_t N, Counters *cn, hipStream_t s);
-void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, Scratch &sc, int64_t *unique_out,
-                  int64_t *inverse, Counters *cn, hipStream_t s);
-void launch_group_by_set(const DevState &d, uint64_t n, Scratch &sc, Counters *cn, hipStream_t s);
-void launch_set_walk(const DevState &d, uint64_t n, uint32_t t, Scratch &sc, Counters *cn, hipStream_t s);
-void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t tail0, Scratch &sc, uint8_t *outcome,
+void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, const StatGrids &grids,
+                   hipStream_t s);
+void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, const int64_t *clear_ids, uint64_t clear_n,
+                  uint32_t clear_bit, Scratch &sc, int64_t *unique_out, Counters *cn, hipStream_t s);
+void launch_group_by_set(const DevState &d, const int64_t *ids, uint64_t n, int64_t *inverse, Scratch &sc,
                          Counters *cn, hipStream_t s);
-void launch_copy(CopyMode mode, const DevState &d, uint64_t max_rows, const uint32_t *a, const uint64_t *b,
-                 const uint32_t *count, uint8_t *out, Counters *cn, hipStream_t s);
-void launch_window_set(const int64_t *ids, uint64_t n, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
-                       Counters *cn, hipStream_t s);
-void launch_window_clear(const int64_t *slot_ids, uint64_t n, uint32_t bit, uint32_t *mask, Counters *cn,
-                         hipStream_t s);
+void launch_set_walk(const DevState &d, uint64_t n, uint32_t t, Scratch &sc, Counters *cn, StatGrids &grids,
+                     hipStream_t s);
+void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t tail0, Scratch &sc, uint8_t *outcome,
+                         Counters *cn, StatGrids &grids, hipStream_t s);
+void launch_copy(CopyMode mode, const DevState &d, uint64_t max_rows, const Scratch &sc, uint8_t *out,
+                 const Counters *cn, hipStream_t s);
+void launch_window_set(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
+                       bool record, Counters *cn, hipStream_t s);
+void launch_copy_plain(const void *src, void *dst, uint64_t bytes, hipStream_t s);
 
 // host twin of the device set-index function
 uint64_t set_of_host(uint64_t x, uint64_t num_sets);

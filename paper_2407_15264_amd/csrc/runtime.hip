@@ -47,12 +47,15 @@ struct lsmgnn_cache {
   int64_t win_batch[kMaxSlots];
   uint64_t win_len[kMaxSlots];
   Counters *cn = nullptr;       // device
-  Counters *cn_host = nullptr;  // pinned host mirror
+  Counters *cn_host = nullptr;  // pinned host mirror, written by the last kernel of each call
+  Counters *cn_host_dev = nullptr;
   uint64_t t = 0, n_adv = 0, tail = 0;
   lsmgnn_counts last{}, total{};
   bool broken = false;
   std::vector<void *> dev_allocs;
   void *ring_host = nullptr;
+  hipStream_t side = nullptr;           // host-fetch stream (default priority)
+  hipEvent_t ev_meta = nullptr, ev_host = nullptr;
   int prof = 0;
   hipEvent_t ev[kNumEv] = {};
   lsmgnn_profile acc{};
@@ -67,6 +70,9 @@ void release(lsmgnn_cache *c) {
   if (c->cn_host) (void)hipHostFree(c->cn_host);
   for (auto &e : c->ev)
     if (e) (void)hipEventDestroy(e);
+  if (c->ev_meta) (void)hipEventDestroy(c->ev_meta);
+  if (c->ev_host) (void)hipEventDestroy(c->ev_host);
+  if (c->side) (void)hipStreamDestroy(c->side);
 }
 
 template <typename T>
@@ -173,22 +179,25 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   bool ok = dev_alloc(c, &d.sets, S) && dev_alloc(c, &d.rows, S * lsm::kWays * R) && dev_alloc(c, &d.mask, N) &&
             dev_alloc(c, &d.stat, N) && dev_alloc(c, &d.bitmap, bitmap_words) &&
             dev_alloc(c, &d.word_rank, bitmap_words) && dev_alloc(c, &d.chunk_sums, d.nchunks) &&
-            dev_alloc(c, &d.set_count, S) && dev_alloc(c, &d.set_idx, S) &&
+            dev_alloc(c, &d.set_count, S) && dev_alloc(c, &d.set_idx, S) && dev_alloc(c, &d.uidx, N) &&
             (V == 0 || (dev_alloc(c, &d.vpos, N) && dev_alloc(c, &d.ring_tag, V))) &&
             dev_alloc(c, &c->win_ids, (uint64_t)(d.L + 1) * B) && dev_alloc(c, &c->cn, 1) &&
-            dev_alloc(c, &sc.uniq, B) && dev_alloc(c, &sc.uset, B) && dev_alloc(c, &sc.ustat, B) &&
-            dev_alloc(c, &sc.arrival, B) && dev_alloc(c, &sc.touched, B) && dev_alloc(c, &sc.seg_off, B) &&
-            dev_alloc(c, &sc.seg, B) && dev_alloc(c, &sc.sorted, B) && dev_alloc(c, &sc.kind, B) &&
-            dev_alloc(c, &sc.flags, B) && dev_alloc(c, &sc.dead, B) && dev_alloc(c, &sc.slot, B) &&
-            dev_alloc(c, &sc.evicted, B) && dev_alloc(c, &sc.enq_before, B) &&
+            dev_alloc(c, &sc.uniq, B) && dev_alloc(c, &sc.uset, B) && dev_alloc(c, &sc.arrival, B) &&
+            dev_alloc(c, &sc.touched, B) && dev_alloc(c, &sc.seg_off, B) && dev_alloc(c, &sc.seg, B) &&
+            dev_alloc(c, &sc.seg_u, B) && dev_alloc(c, &sc.seg_x, B) && dev_alloc(c, &sc.seg_st, B) &&
+            dev_alloc(c, &sc.kind, B) && dev_alloc(c, &sc.flags, B) && dev_alloc(c, &sc.dead, B) &&
+            dev_alloc(c, &sc.slot, B) && dev_alloc(c, &sc.evicted, B) && dev_alloc(c, &sc.enq_before, B) &&
             dev_alloc(c, &sc.scan_part, B / lsm::kScanChunk + 2) && dev_alloc(c, &sc.this_q, B) &&
-            dev_alloc(c, &sc.this_enq, B) && dev_alloc(c, &sc.hbm_a, B) && dev_alloc(c, &sc.hbm_b, B) &&
-            dev_alloc(c, &sc.host_a, B) && dev_alloc(c, &sc.host_b, B) && dev_alloc(c, &sc.enq_a, B) &&
-            dev_alloc(c, &sc.enq_b, B) && dev_alloc(c, &sc.fill_a, B) && dev_alloc(c, &sc.fill_b, B);
-  if (ok && hipHostMalloc(reinterpret_cast<void **>(&c->cn_host), sizeof(Counters), hipHostMallocDefault) !=
+            dev_alloc(c, &sc.this_enq, B) && dev_alloc(c, &sc.src, B) && dev_alloc(c, &sc.ring_dst, B) &&
+            dev_alloc(c, &sc.fill_dst, B) && dev_alloc(c, &sc.stat_part, (uint64_t)lsm::kNumStat * lsm::kMaxGrid);
+  if (ok && hipHostMalloc(reinterpret_cast<void **>(&c->cn_host), sizeof(Counters), hipHostMallocMapped) !=
                 hipSuccess) {
     (void)hipGetLastError();
     c->cn_host = nullptr;
+    ok = false;
+  }
+  if (ok && hipHostGetDevicePointer(reinterpret_cast<void **>(&c->cn_host_dev), c->cn_host, 0) != hipSuccess) {
+    (void)hipGetLastError();
     ok = false;
   }
   if (ok && V) {
@@ -212,10 +221,13 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   }
   for (auto &e : c->ev)
     if (hipEventCreate(&e) != hipSuccess) ok = false;
+  ok = ok && hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) == hipSuccess &&
+       hipEventCreateWithFlags(&c->ev_meta, hipEventDisableTiming) == hipSuccess &&
+       hipEventCreateWithFlags(&c->ev_host, hipEventDisableTiming) == hipSuccess;
   // initial state: all ways empty, nothing announced, ring empty
   ok = ok && hipMemset(d.sets, 0xff, S * sizeof(lsm::SetRec)) == hipSuccess &&
        hipMemset(d.mask, 0, N * 4) == hipSuccess && hipMemset(d.bitmap, 0, bitmap_words * 4) == hipSuccess &&
-       hipMemset(d.set_count, 0, S * 4) == hipSuccess &&
+       hipMemset(d.set_count, 0, S * 4) == hipSuccess && hipMemset(c->cn, 0, sizeof(Counters)) == hipSuccess &&
        hipMemcpy(d.stat, cfg->static_score, N * 4, hipMemcpyHostToDevice) == hipSuccess &&
        (V == 0 || (hipMemset(d.vpos, 0, N * 8) == hipSuccess && hipMemset(d.ring_tag, 0xff, V * 4) == hipSuccess)) &&
        hipDeviceSynchronize() == hipSuccess;
@@ -250,13 +262,11 @@ lsmgnn_status lsmgnn_advance(lsmgnn_cache *c, const int64_t *ids, uint64_t n, vo
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool record = j > c->t && c->d.L > 0 && n > 0;  // lists for j <= t are never consulted
   const int slot = (int)(j % (c->d.L + 1));
-  lsm::launch_begin(c->cn, s);
-  if (n) lsm::launch_validate(ids, n, c->d.N, c->cn, s);
-  if (record)
-    lsm::launch_window_set(ids, n, (uint32_t)(j & 31u), c->d.mask, c->win_ids + (uint64_t)slot * c->max_batch,
-                           c->cn, s);
-  if (hipMemcpyAsync(c->cn_host, c->cn, sizeof(Counters), hipMemcpyDeviceToHost, s) != hipSuccess ||
-      hipStreamSynchronize(s) != hipSuccess) {
+  if (n)
+    lsm::launch_window_set(ids, n, c->d.N, (uint32_t)(j & 31u), c->d.mask,
+                           c->win_ids + (uint64_t)slot * c->max_batch, record, c->cn, s);
+  lsm::launch_finish(c->cn, c->cn_host_dev, c->sc.stat_part, lsm::StatGrids{}, s);
+  if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) {
     (void)hipGetLastError();
     return fail_device(c);
   }
@@ -290,42 +300,47 @@ lsmgnn_status lsmgnn_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, voi
   };
   uint8_t *outp = static_cast<uint8_t *>(out);
 
-  rec(kEvAll0);
-  lsm::launch_begin(c->cn, s);
-  if (n) {
-    lsm::launch_validate(ids, n, d.N, c->cn, s);
-    lsm::launch_dedup(d, ids, n, sc, unique_ids, inverse, c->cn, s);
-    lsm::launch_group_by_set(d, n, sc, c->cn, s);
-    lsm::launch_set_walk(d, n, t, sc, c->cn, s);
-    lsm::launch_ring_resolve(d, n, c->tail, sc, outcome, c->cn, s);
-    // Data movement.  Every read of a batch-start row precedes every write to
-    // the same place: cache rows are read by the hit copy and the enqueue copy
-    // before fills overwrite them; ring rows are read by victim hits before
-    // this batch's enqueues overwrite them.
-    rec(kEvHbm0);
-    lsm::launch_copy(CopyMode::kHbmToOut, d, n, sc.hbm_a, sc.hbm_b, &c->cn->n_hbm, outp, c->cn, s);
-    rec(kEvHbm1);
-    rec(kEvHost0);
-    lsm::launch_copy(CopyMode::kHostToOut, d, n, sc.host_a, sc.host_b, &c->cn->n_host, outp, c->cn, s);
-    rec(kEvHost1);
-    if (d.V) {
-      rec(kEvEnq0);
-      lsm::launch_copy(CopyMode::kCacheToRing, d, n, sc.enq_a, sc.enq_b, &c->cn->n_enq_copy, outp, c->cn, s);
-      rec(kEvEnq1);
-    }
-    rec(kEvFill0);
-    lsm::launch_copy(CopyMode::kOutToCache, d, n, sc.fill_a, sc.fill_b, &c->cn->n_fill, outp, c->cn, s);
-    rec(kEvFill1);
-  }
+  // the window list of the minibatch being gathered is cleared by the first
+  // kernel (it is never consulted again)
   const int slot = (int)(c->t % (d.L + 1));
   const bool clear = d.L > 0 && c->win_batch[slot] == (int64_t)c->t;
-  if (clear)
-    lsm::launch_window_clear(c->win_ids + (uint64_t)slot * c->max_batch, c->win_len[slot], (uint32_t)(c->t & 31u),
-                             d.mask, c->cn, s);
+  const int64_t *clear_ids = clear ? c->win_ids + (uint64_t)slot * c->max_batch : nullptr;
+  const uint64_t clear_n = clear ? c->win_len[slot] : 0;
+
+  lsm::StatGrids grids{};
+  rec(kEvAll0);
+  if (n || clear_n) lsm::launch_dedup(d, ids, n, clear_ids, clear_n, (uint32_t)(c->t & 31u), sc, unique_ids, c->cn, s);
+  if (n) {
+    lsm::launch_group_by_set(d, ids, n, inverse, sc, c->cn, s);
+    lsm::launch_set_walk(d, n, t, sc, c->cn, grids, s);
+    lsm::launch_ring_resolve(d, n, c->tail, sc, outcome, c->cn, grids, s);
+    // Data movement.  Every read of a batch-start row precedes every write to
+    // the same place: cache rows are read by the hit copy and the enqueue copy
+    // before fills overwrite them.  The host fetch (PCIe ingress) runs on the
+    // side stream concurrently with the hit copy and the enqueue copy (PCIe
+    // egress); it never reads a ring slot an enqueue of this batch rewrites.
+    (void)hipEventRecord(c->ev_meta, s);
+    (void)hipStreamWaitEvent(c->side, c->ev_meta, 0);
+    if (prof) (void)hipEventRecord(c->ev[kEvHost0], c->side);
+    lsm::launch_copy(CopyMode::kHostToOut, d, n, sc, outp, c->cn, c->side);
+    if (prof) (void)hipEventRecord(c->ev[kEvHost1], c->side);
+    (void)hipEventRecord(c->ev_host, c->side);
+    if (d.V) {
+      rec(kEvEnq0);
+      lsm::launch_copy(CopyMode::kCacheToRing, d, n, sc, outp, c->cn, s);
+      rec(kEvEnq1);
+    }
+    rec(kEvHbm0);
+    lsm::launch_copy(CopyMode::kHbmToOut, d, n, sc, outp, c->cn, s);
+    rec(kEvHbm1);
+    (void)hipStreamWaitEvent(s, c->ev_host, 0);
+    rec(kEvFill0);
+    lsm::launch_copy(CopyMode::kOutToCache, d, n, sc, outp, c->cn, s);
+    rec(kEvFill1);
+  }
+  lsm::launch_finish(c->cn, c->cn_host_dev, sc.stat_part, grids, s);
   rec(kEvAll1);
-  if (hipGetLastError() != hipSuccess ||
-      hipMemcpyAsync(c->cn_host, c->cn, sizeof(Counters), hipMemcpyDeviceToHost, s) != hipSuccess ||
-      hipStreamSynchronize(s) != hipSuccess) {
+  if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) {
     (void)hipGetLastError();
     return fail_device(c);
   }
@@ -420,6 +435,40 @@ lsmgnn_status lsmgnn_export_state(const lsmgnn_cache *c, uint32_t *tags, uint32_
   }
   if (ring_tail) *ring_tail = c->tail;
   if (t) *t = c->t;
+  return LSMGNN_OK;
+}
+
+lsmgnn_status lsmgnn_copy_bytes(void *dst, const void *src, uint64_t bytes, void *stream) {
+  if (!dst || !src || bytes % 16 != 0 || (reinterpret_cast<uintptr_t>(dst) & 15u) ||
+      (reinterpret_cast<uintptr_t>(src) & 15u))
+    return LSMGNN_E_INVAL;
+  if (bytes == 0) return LSMGNN_OK;
+  // pinned host memory is addressed through its device mapping
+  auto dev_view = [](const void *p) -> const void * {
+    hipPointerAttribute_t a{};
+    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    if (a.type == hipMemoryTypeHost) {
+      void *dp = nullptr;
+      if (hipHostGetDevicePointer(&dp, const_cast<void *>(p), 0) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+      }
+      return dp;
+    }
+    return (a.type == hipMemoryTypeDevice) ? p : nullptr;
+  };
+  const void *s_dev = dev_view(src);
+  void *d_dev = const_cast<void *>(dev_view(dst));
+  if (!s_dev || !d_dev) return LSMGNN_E_INVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  lsm::launch_copy_plain(s_dev, d_dev, bytes, s);
+  if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) {
+    (void)hipGetLastError();
+    return LSMGNN_E_DEVICE;
+  }
   return LSMGNN_OK;
 }
 

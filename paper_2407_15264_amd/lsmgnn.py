@@ -86,6 +86,8 @@ def lib():
         L.lsmgnn_host_free.argtypes = [vp]
         L.lsmgnn_set_of.restype = u64
         L.lsmgnn_set_of.argtypes = [u64, u64]
+        L.lsmgnn_copy_bytes.restype = i32
+        L.lsmgnn_copy_bytes.argtypes = [vp, vp, u64, vp]
         L.lsmgnn_strerror.restype = ctypes.c_char_p
         L.lsmgnn_strerror.argtypes = [i32]
         _lib = L
@@ -99,6 +101,12 @@ def _check(rc: int, where: str):
 
 def set_of(x: int, num_sets: int) -> int:
     return int(lib().lsmgnn_set_of(int(x), int(num_sets)))
+
+
+def copy_bytes(dst_ptr: int, src_ptr: int, nbytes: int, stream=None, device=0):
+    """Calibration copy (device or pinned host pointers), synchronous."""
+    _check(lib().lsmgnn_copy_bytes(ctypes.c_void_p(dst_ptr), ctypes.c_void_p(src_ptr), int(nbytes),
+                                   _stream_handle(stream, device)), "lsmgnn_copy_bytes")
 
 
 class PinnedBuffer:
@@ -205,8 +213,15 @@ class FeatureCache:
             out = self._buf("out", n * self.row_bytes, torch.uint8)
         if unique is None:
             unique = self._buf("unique", n, torch.int64)
-        inv_t = self._buf("inverse", n, torch.int64) if inverse is True else (inverse or None)
-        oc_t = self._buf("outcome", n, torch.uint8) if outcome is True else (outcome or None)
+        def pick(arg, name, dtype):
+            if isinstance(arg, torch.Tensor):
+                if arg.numel() < n:
+                    raise ValueError(f"{name} buffer too small")
+                return arg
+            return self._buf(name, n, dtype) if arg else None
+
+        inv_t = pick(inverse, "inverse", torch.int64)
+        oc_t = pick(outcome, "outcome", torch.uint8)
         if out.numel() * out.element_size() < n * self.row_bytes or unique.numel() < n:
             raise ValueError("out/unique buffers too small")
         nu = ctypes.c_uint64()
