@@ -17,6 +17,7 @@ bytes) per second over the timed steps; `roofline` rates the dominant data
 kernel against its bound, timed with HIP events on the gather's stream.
 """
 import argparse
+import hashlib
 import json
 import os
 import platform
@@ -33,6 +34,31 @@ PCIE5_X16_PEAK_GBPS = 64.0      # host link, published per direction
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+def copy_kernels_hash():
+    src = open(os.path.join(ROOT, "paper_2407_15264_amd", "csrc", "gather_kernels.hip")).read()
+    a = src.index("// -------------------------------------------------------------- row copies")
+    b = src.index("// ------------------------------------------------------------ calibration")
+    return hashlib.sha256(src[a:b].encode()).hexdigest()
+
+
+def recorded_traffic(workload, kernel):
+    """HBM/link bytes per launch of `kernel` from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE passes, each scaled by its reading for a copy of
+    known size; None when absent or when the row-copy kernels have changed
+    since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"counters_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("copy_kernels_source_sha256") != copy_kernels_hash() or kernel not in rec["kernels"]:
+        return None
+    k, cal = rec["kernels"][kernel], rec["calibration"]
+    fetch = k["fetch_kib"] * 1024 * cal["fetch_scale"]
+    write = k["write_kib"] * 1024 * cal["write_scale"]
+    return {"bytes": fetch + write, "fetch_bytes": fetch, "write_bytes": write,
+            "source": os.path.relpath(path, ROOT)}
 
 
 def measure_ceilings(torch, lsmgnn, store_ptr, nbytes):
@@ -185,11 +211,19 @@ def main():
                 "peak_source": "measured in this run (best of pinned DMA and zero-copy kernel)",
                 "frac_of_published_pcie5_x16": kd["GBps"] / PCIE5_X16_PEAK_GBPS}
     roof.update(kernel=dom, avg_launch_us=kd["avg_us"], bytes_per_launch=kd["bytes_per_launch"])
+    tr = recorded_traffic(cfg.name, dom)
+    if tr is not None:
+        # algorithmic bytes of the launch on both sides of the copy (read + write)
+        alg = kd["bytes_per_launch"] * (1 if kd["bound"] == "hbm" else 2)
+        roof["traffic"] = tr["bytes"]
+        roof["traffic_detail"] = dict(tr, algorithmic_read_plus_write=alg, ratio=tr["bytes"] / alg)
     hb = kern["hbm_copy"]
+    trh = recorded_traffic(cfg.name, "hbm_copy")
     roof_hbm = {"bound": "hbm", "kernel": "hbm_copy (hit rows cache->out)", "achieved": hb["GBps"],
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": hb["GBps"] / HBM_PEAK_GBPS,
                 "frac_of_measured_d2d": hb["GBps"] / ceil["hbm_copy_GBps"], "avg_launch_us": hb["avg_us"],
-                "bytes_per_launch": hb["bytes_per_launch"]}
+                "bytes_per_launch": hb["bytes_per_launch"],
+                "traffic": None if trh is None else trh["bytes"]}
 
     res = {
         "metric": METRIC, "value": gbps, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,

@@ -84,14 +84,30 @@ static inline unsigned grid_for(uint64_t work, uint64_t per_block, unsigned cap)
 // call (they start zeroed at create).
 __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host, const uint32_t *part,
                                                    StatGrids grids) {
+  __shared__ uint32_t red[kNumStat][kBlock / 64];
   __shared__ uint32_t sums[kNumStat];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  for (int st = wid; st < kNumStat; st += kBlock / 64) {  // one wave per counter
+#pragma unroll
+  for (int st = 0; st < kNumStat; ++st) {
     uint32_t v = 0;
-    for (uint32_t b = lane; b < grids.g[st]; b += 64) v += part[st * kMaxGrid + b];
+    // four independent loads per pass keep the partials' reads in flight
+    for (uint32_t b = threadIdx.x; b < grids.g[st]; b += 4 * kBlock) {
+      uint32_t a0 = part[st * kMaxGrid + b];
+      uint32_t a1 = b + kBlock < grids.g[st] ? part[st * kMaxGrid + b + kBlock] : 0u;
+      uint32_t a2 = b + 2 * kBlock < grids.g[st] ? part[st * kMaxGrid + b + 2 * kBlock] : 0u;
+      uint32_t a3 = b + 3 * kBlock < grids.g[st] ? part[st * kMaxGrid + b + 3 * kBlock] : 0u;
+      v += a0 + a1 + a2 + a3;
+    }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    if (lane == 0) sums[st] = v;
+    if (lane == 0) red[st][wid] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x < kNumStat) {
+    uint32_t v = 0;
+#pragma unroll
+    for (int w = 0; w < kBlock / 64; ++w) v += red[threadIdx.x][w];
+    sums[threadIdx.x] = v;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
