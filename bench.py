@@ -125,6 +125,8 @@ def main():
     ap.add_argument("--config", type=int, default=2, help="workload shape (1, 2, 3 or 5)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sync", action="store_true",
+                    help="blocking lsmgnn_gather per minibatch instead of the pipelined lsmgnn_gather_async")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU: this build has no multi-GPU path (asked for --gpus "
@@ -158,19 +160,29 @@ def main():
     mb = wl.max_batch
     cache = lsmgnn.FeatureCache(cfg.num_nodes, cfg.row_bytes, store, wl.static, cfg.cache.num_sets,
                                 cfg.cache.victim_rows, L, mb, near_threshold=cfg.cache.near_threshold)
-    out = torch.empty(mb * cfg.row_bytes, dtype=torch.uint8, device=dev)
-    uniq = torch.empty(mb, dtype=torch.int64, device=dev)
-    inv = torch.empty(mb, dtype=torch.int64, device=dev)
+    # three output sets rotate: at most two gathers are in flight
+    bufs = [(torch.empty(mb * cfg.row_bytes, dtype=torch.uint8, device=dev),
+             torch.empty(mb, dtype=torch.int64, device=dev),
+             torch.empty(mb, dtype=torch.int64, device=dev)) for _ in range(3)]
     for j in range(L + 1):
         cache.advance(batches[j])
+    tickets = {}
 
     def step(b):
-        r = cache.gather(batches[b], out=out, unique=uniq, inverse=inv)
+        out, uniq, inv = bufs[b % 3]
+        if args.sync:
+            r = cache.gather(batches[b], out=out, unique=uniq, inverse=inv)
+        else:
+            tickets[b], r = cache.gather_async(batches[b], out, uniq, inverse=inv)
         cache.advance(batches[b + L + 1])
+        if not args.sync and b - 1 in tickets:
+            cache.wait(tickets.pop(b - 1))  # a consumer of minibatch b-1 would run after this
         return r.n_unique
 
     for b in range(args.warmup):
         step(b)
+    for b in list(tickets):
+        cache.wait(tickets.pop(b))
     _, tot0 = cache.stats()
     cache.set_profiling(True)
     torch.cuda.synchronize()
@@ -178,6 +190,8 @@ def main():
     rows = 0
     for b in range(args.warmup, args.warmup + args.steps):
         rows += step(b)
+    for b in list(tickets):
+        cache.wait(tickets.pop(b))
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     prof = cache.profile()
@@ -230,7 +244,8 @@ def main():
         "warmup": args.warmup, "ms_per_step": 1e3 * dt / args.steps, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
         "config": dict(cfg.describe(), feature_dtype=cfg.feature_dtype, minibatches_timed=args.steps,
-                       first_timed_minibatch=args.warmup),
+                       first_timed_minibatch=args.warmup,
+                       api="lsmgnn_gather" if args.sync else "lsmgnn_gather_async (two minibatches in flight)"),
         "rows_per_s": rows / dt,
         "hit_rate": d["hits"] / max(d["unique"], 1),
         "victim_hit_rate": d["victim_hits"] / max(d["unique"], 1),

@@ -34,9 +34,10 @@
  * Every gathered row is bit-identical to the backing-store row of its node.
  *
  * Threading: one cache object must not be used from two threads at once.
- * Calls are stream-ordered on the stream passed in (a hipStream_t as void*,
- * NULL = the null stream) and return once their status is known; gather and
- * advance synchronise that stream before returning.
+ * Streams: a hipStream_t passed as void* (NULL = the null stream).  Each call
+ * first waits for the work already queued on that stream; lsmgnn_gather and
+ * lsmgnn_advance return once their work is complete, lsmgnn_gather_async once
+ * its unique count is known (see there).
  */
 #ifndef LSMGNN_H
 #define LSMGNN_H
@@ -131,19 +132,40 @@ lsmgnn_status lsmgnn_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, voi
                             int64_t *unique_ids, int64_t *inverse, uint8_t *outcome,
                             uint64_t *n_unique, void *stream);
 
-/* Counters of the last gather and totals over all gathers (either may be NULL). */
-lsmgnn_status lsmgnn_stats(const lsmgnn_cache *c, lsmgnn_counts *last, lsmgnn_counts *total);
+/* Pipelined gather, for loops that overlap consecutive minibatches.  Same
+   arguments, semantics and errors as lsmgnn_gather, but it returns as soon as
+   *n_unique is known, with *ticket identifying the gather.  The gather's
+   outputs (out, unique_ids, inverse, outcome) are complete once the caller has
+   called lsmgnn_gather_wait(c, ticket, s) and then synchronised s (or run work
+   on s after it).  Until then the caller must not read, reuse or free those
+   buffers.  The metadata of the next gather runs while this one still moves
+   rows; at most two gathers are in flight and later calls wait for the
+   oldest.  Waits for the work already queued on `stream` before reading ids. */
+lsmgnn_status lsmgnn_gather_async(lsmgnn_cache *c, const int64_t *ids, uint64_t n, void *out,
+                                  int64_t *unique_ids, int64_t *inverse, uint8_t *outcome,
+                                  uint64_t *n_unique, uint64_t *ticket, void *stream);
+
+/* Make `stream` wait (on the device, without blocking the host) until the
+   gather `ticket` has completed.  E_INVAL for a ticket never issued. */
+lsmgnn_status lsmgnn_gather_wait(lsmgnn_cache *c, uint64_t ticket, void *stream);
+
+/* Block the host until every queued gather and announcement has completed. */
+lsmgnn_status lsmgnn_sync(lsmgnn_cache *c);
+
+/* Counters of the last completed gather and totals over all gathers (either
+   may be NULL).  Waits for queued gathers first. */
+lsmgnn_status lsmgnn_stats(lsmgnn_cache *c, lsmgnn_counts *last, lsmgnn_counts *total);
 
 /* Copy the policy state to host memory (each pointer may be NULL):
    tags num_sets*8 uint32 (0xFFFFFFFF = empty way), ring_tags victim_rows uint32
    (0xFFFFFFFF = empty entry), ring_tail = entries ever enqueued, t = gathers done. */
-lsmgnn_status lsmgnn_export_state(const lsmgnn_cache *c, uint32_t *tags, uint32_t *ring_tags,
+lsmgnn_status lsmgnn_export_state(lsmgnn_cache *c, uint32_t *tags, uint32_t *ring_tags,
                                   uint64_t *ring_tail, uint64_t *t);
 
 /* Turn per-kernel event timing of the data-movement kernels on (1) or off (0);
    turning it on clears the accumulated profile. */
 lsmgnn_status lsmgnn_set_profiling(lsmgnn_cache *c, int on);
-lsmgnn_status lsmgnn_get_profile(const lsmgnn_cache *c, lsmgnn_profile *out);
+lsmgnn_status lsmgnn_get_profile(lsmgnn_cache *c, lsmgnn_profile *out);
 
 /* Pinned, device-mapped host memory for a backing store (exact size, unlike
    caching allocators that round up).  Free with lsmgnn_host_free. */

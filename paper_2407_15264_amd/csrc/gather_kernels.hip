@@ -6,9 +6,9 @@
 // synchronises once at the end.  Each kernel reads Counters::err first and does
 // nothing once an out-of-range ID was seen, so an invalid batch changes no state.
 //
-//   dedup       bitmap over node IDs: mark, per-chunk popcount, chunk scan,
-//               ascending compaction (ballot-free: one thread per 8 words),
-//               inverse index by rank = prefix + popcount below the bit
+//   dedup       byte map over node IDs marked with plain stores, per-chunk
+//               popcount, chunk scan, ascending compaction that records each
+//               node's unique index; the inverse index is one lookup
 //   group       per-set counts with atomics, segment allocation, placement and
 //               ranking so each touched set sees its IDs in ascending order
 //   set walk    one lane per touched set walks its IDs in ascending order over
@@ -133,102 +133,54 @@ void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, cons
   hipLaunchKernelGGL(k_finish, dim3(1), dim3(kBlock), 0, s, cn, host, stat_part, grids);
 }
 
-// ------------------------------------------------------------- LDS combine
-// Per-block open-addressing table in LDS that ORs bit patterns per 32-bit key.
-// Hub nodes occur thousands of times per batch; combining them in LDS turns
-// those occurrences into one global atomic per block.  A block inserts at
-// most kCombineItems keys into kCombineSlots slots, so probing always ends.
-constexpr int kCombinePerThread = 4;
-constexpr int kCombineItems = kBlock * kCombinePerThread;
-constexpr int kCombineSlots = 2 * kCombineItems;
-
-struct LdsCombine {
-  uint32_t key[kCombineSlots];
-  uint32_t val[kCombineSlots];
-};
-
-__device__ __forceinline__ void combine_init(LdsCombine &t) {
-  for (int i = threadIdx.x; i < kCombineSlots; i += kBlock) {
-    t.key[i] = kEmpty;
-    t.val[i] = 0;
-  }
-  __syncthreads();
-}
-
-__device__ __forceinline__ void combine_or(LdsCombine &t, uint32_t key, uint32_t bits) {
-  uint32_t h = (key * 0x9e3779b1u) >> (32 - 11);  // log2(kCombineSlots) == 11
-  static_assert(kCombineSlots == 2048, "hash width");
-  for (;;) {
-    const uint32_t old = atomicCAS(&t.key[h], kEmpty, key);
-    if (old == kEmpty || old == key) {
-      atomicOr(&t.val[h], bits);
-      return;
-    }
-    h = (h + 1) & (kCombineSlots - 1);
-  }
-}
-
 // ------------------------------------------------------------------- dedup
+// A byte per node marks the batch's requests.  Plain byte stores need no
+// atomics: every writer of a byte writes the same value, and bytes of
+// different nodes never interfere.  (Device-scope atomics serialize on hot
+// addresses and queue behind host-link traffic on this GPU.)
+//
 // Validate and mark.  Out-of-range IDs set Counters::err; valid ones are still
-// marked, and the compaction kernel then clears the bitmap instead of
-// compacting it, so a rejected batch leaves no trace.  The same kernel clears
-// the window bit of the minibatch being gathered: that list is never consulted
-// again, whether or not this call succeeds.
-__global__ __launch_bounds__(kBlock) void k_mark(const int64_t *ids, uint32_t n, uint64_t N, uint32_t *bitmap,
-                                                 const int64_t *clear_ids, uint32_t clear_n, uint32_t clear_bit,
-                                                 uint32_t *mask, Counters *cn) {
-  __shared__ LdsCombine tab;
-  const uint32_t base = blockIdx.x * kCombineItems;
+// marked, and the compaction kernel then clears the map instead of compacting
+// it, so a rejected batch leaves no trace.  The same kernel clears the window
+// bit of the minibatch being gathered: that list is never consulted again,
+// whether or not this call succeeds.  Only that bit of a node's window word
+// changes in this kernel, so a plain read-modify-write is exact.
+__global__ void k_mark(const int64_t *ids, uint32_t n, uint64_t N, uint8_t *present, const int64_t *clear_ids,
+                       uint32_t clear_n, uint32_t clear_bit, uint32_t *mask, Counters *cn) {
   bool bad = false;
-  if (base < n) {
-    combine_init(tab);
-    for (int k = 0; k < kCombinePerThread; ++k) {
-      const uint32_t i = base + k * kBlock + threadIdx.x;
-      if (i < n) {
-        const int64_t xi = ids[i];
-        if (xi < 0 || (uint64_t)xi >= N) {
-          bad = true;
-        } else {
-          const uint32_t x = (uint32_t)xi;
-          combine_or(tab, x >> 5, 1u << (x & 31u));
-        }
-      }
-    }
-    __syncthreads();
-    for (int h = threadIdx.x; h < kCombineSlots; h += kBlock) {
-      const uint32_t w = tab.key[h];
-      if (w != kEmpty) atomicOr(&bitmap[w], tab.val[h]);
-    }
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
+    const int64_t x = ids[i];
+    if (x < 0 || (uint64_t)x >= N)
+      bad = true;
+    else
+      present[x] = 1;
   }
   if (__ballot(bad) && __lane_id() == 0) atomicOr(&cn->err, 1u);
-  if (base < clear_n) {
-    __syncthreads();
-    combine_init(tab);
-    for (int k = 0; k < kCombinePerThread; ++k) {
-      const uint32_t i = base + k * kBlock + threadIdx.x;
-      if (i < clear_n) combine_or(tab, (uint32_t)clear_ids[i], 1u);
-    }
-    __syncthreads();
-    const uint32_t cb = 1u << clear_bit;
-    for (int h = threadIdx.x; h < kCombineSlots; h += kBlock) {
-      const uint32_t x = tab.key[h];
-      if (x != kEmpty) atomicAnd(&mask[x], ~cb);
-    }
+  const uint32_t cb = 1u << clear_bit;
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < clear_n; i += gridDim.x * kBlock) {
+    const int64_t x = clear_ids[i];
+    const uint32_t m = mask[x];
+    if (m & cb) mask[x] = m & ~cb;
   }
 }
 
-__device__ __forceinline__ void load_words(const uint32_t *bitmap, uint32_t (&w)[kWordsPerThread]) {
-  static_assert(kWordsPerThread == 4, "one 128-bit load per thread");
-  const u32x4 a = *reinterpret_cast<const u32x4 *>(bitmap + (size_t)blockIdx.x * kChunkWords +
-                                                   threadIdx.x * kWordsPerThread);
-  w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
+// Each thread owns kBytesPerThread consecutive bytes of the map (four 128-bit
+// loads); marked bytes hold exactly 1, so a popcount of a word counts them.
+__device__ __forceinline__ void load_bytes(const uint8_t *present, uint32_t (&w)[kWordsPerThread]) {
+  const u32x4 *p = reinterpret_cast<const u32x4 *>(present + (size_t)blockIdx.x * kChunkBytes +
+                                                    threadIdx.x * kBytesPerThread);
+#pragma unroll
+  for (int k = 0; k < kWordsPerThread / 4; ++k) {
+    const u32x4 a = p[k];
+    w[4 * k] = a.x; w[4 * k + 1] = a.y; w[4 * k + 2] = a.z; w[4 * k + 3] = a.w;
+  }
 }
 
-__global__ __launch_bounds__(kBlock) void k_chunk_popc(const uint32_t *bitmap, uint32_t *chunk_sums,
+__global__ __launch_bounds__(kBlock) void k_chunk_popc(const uint8_t *present, uint32_t *chunk_sums,
                                                        const Counters *cn) {
   if (cn->err) return;
   uint32_t w[kWordsPerThread];
-  load_words(bitmap, w);
+  load_bytes(present, w);
   uint32_t c = 0;
 #pragma unroll
   for (int k = 0; k < kWordsPerThread; ++k) c += __popc(w[k]);
@@ -236,8 +188,13 @@ __global__ __launch_bounds__(kBlock) void k_chunk_popc(const uint32_t *bitmap, u
   if (threadIdx.x == 0) chunk_sums[blockIdx.x] = tot;
 }
 
-__global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uint32_t nchunks, Counters *cn) {
-  if (cn->err) return;
+__global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uint32_t nchunks, Counters *cn,
+                                                       DedupResult *dd) {
+  const uint32_t err = cn->err;
+  if (err) {
+    if (threadIdx.x == 0) *dd = DedupResult{err, 0, {0, 0}};
+    return;
+  }
   uint32_t carry = 0;
   for (uint32_t base = 0; base < nchunks; base += kBlock) {
     const uint32_t i = base + threadIdx.x;
@@ -247,19 +204,21 @@ __global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uin
     if (i < nchunks) chunk_sums[i] = carry + ex;
     carry += tot;
   }
-  if (threadIdx.x == 0) cn->n_unique = carry;
+  if (threadIdx.x == 0) {
+    cn->n_unique = carry;
+    *dd = DedupResult{0, carry, {0, 0}};
+  }
 }
 
-__global__ __launch_bounds__(kBlock) void k_compact(uint32_t *bitmap, const uint32_t *chunk_off,
-                                                    uint32_t *word_rank, uint32_t *uniq, int64_t *uniq_out,
-                                                    const Counters *cn) {
+__global__ __launch_bounds__(kBlock) void k_compact(uint8_t *present, const uint32_t *chunk_off, uint32_t *uidx,
+                                                    uint32_t *uniq, int64_t *uniq_out, const Counters *cn) {
   uint32_t w[kWordsPerThread];
-  load_words(bitmap, w);
-  const size_t w0 = (size_t)blockIdx.x * kChunkWords + threadIdx.x * kWordsPerThread;
+  load_bytes(present, w);
+  const size_t b0 = (size_t)blockIdx.x * kChunkBytes + threadIdx.x * kBytesPerThread;
   if (cn->err) {  // rejected batch: undo the marks
 #pragma unroll
     for (int k = 0; k < kWordsPerThread; ++k)
-      if (w[k]) bitmap[w0 + k] = 0;
+      if (w[k]) reinterpret_cast<uint32_t *>(present + b0)[k] = 0;
     return;
   }
   uint32_t c = 0;
@@ -272,30 +231,27 @@ __global__ __launch_bounds__(kBlock) void k_compact(uint32_t *bitmap, const uint
 #pragma unroll
   for (int k = 0; k < kWordsPerThread; ++k) {
     uint32_t word = w[k];
-    if (word) {
-      word_rank[w0 + k] = pos;
-      const uint32_t idbase = (uint32_t)((w0 + k) * 32u);
-      while (word) {
-        const uint32_t x = idbase + (uint32_t)__builtin_ctz(word);
-        uniq[pos] = x;
-        uniq_out[pos] = (int64_t)x;
-        ++pos;
-        word &= word - 1u;
-      }
+    while (word) {  // marked bytes ascending: bit 8*j is set for byte j
+      const uint32_t x = (uint32_t)(b0 + 4 * k + (__builtin_ctz(word) >> 3));
+      uniq[pos] = x;
+      uniq_out[pos] = (int64_t)x;
+      uidx[x] = pos;
+      ++pos;
+      word &= word - 1u;
     }
   }
 }
 
 void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, const int64_t *clear_ids, uint64_t clear_n,
-                  uint32_t clear_bit, Scratch &sc, int64_t *unique_out, Counters *cn, hipStream_t s) {
-  const uint64_t items = n > clear_n ? n : clear_n;
-  const unsigned g = (unsigned)((items + kCombineItems - 1) / kCombineItems);
-  hipLaunchKernelGGL(k_mark, dim3(g ? g : 1), dim3(kBlock), 0, s, ids, (uint32_t)n, d.N, d.bitmap, clear_ids,
+                  uint32_t clear_bit, Scratch &sc, int64_t *unique_out, Counters *cn, DedupResult *dd,
+                  hipStream_t s) {
+  const unsigned g = grid_for(n > clear_n ? n : clear_n, kBlock, kMaxGrid);
+  hipLaunchKernelGGL(k_mark, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, d.N, d.present, clear_ids,
                      (uint32_t)clear_n, clear_bit, d.mask, cn);
-  hipLaunchKernelGGL(k_chunk_popc, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.bitmap, d.chunk_sums, cn);
-  hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, s, d.chunk_sums, (uint32_t)d.nchunks, cn);
-  hipLaunchKernelGGL(k_compact, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.bitmap, d.chunk_sums,
-                     d.word_rank, sc.uniq, unique_out, cn);
+  hipLaunchKernelGGL(k_chunk_popc, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.present, d.chunk_sums, cn);
+  hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, s, d.chunk_sums, (uint32_t)d.nchunks, cn, dd);
+  hipLaunchKernelGGL(k_compact, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.present, d.chunk_sums, d.uidx,
+                     sc.uniq, unique_out, cn);
 }
 
 // ------------------------------------------------------------ group by set
@@ -318,16 +274,14 @@ __device__ __forceinline__ void block_count(uint32_t v, uint32_t *part, int slot
   if (threadIdx.x == 0) part[slot * kMaxGrid + blockIdx.x] = tot;
 }
 
-// Inverse index of every request (rank = unique IDs before its bitmap word +
-// set bits below it in the word), then per-set counts of the unique IDs.
+// Inverse index of every request (the compaction recorded each node's unique
+// index), then per-set counts of the unique IDs.
 __global__ __launch_bounds__(kBlock) void k_inverse_claim(const DevState d, Scratch sc, const int64_t *ids,
                                                           uint32_t n, int64_t *inv, Counters *cn) {
   if (cn->err) return;
   if (inv) {
     for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
-      const uint32_t x = (uint32_t)ids[i];
-      const uint32_t wi = x >> 5, b = x & 31u;
-      inv[i] = (int64_t)(d.word_rank[wi] + __popc(d.bitmap[wi] & ((1u << b) - 1u)));
+      inv[i] = (int64_t)d.uidx[ids[i]];
     }
   }
   const uint32_t U = cn->n_unique;
@@ -346,7 +300,7 @@ __global__ __launch_bounds__(kBlock) void k_inverse_claim(const DevState d, Scra
       sc.dead[u] = 0;
       sc.this_q[u] = 0;
       sc.fill_dst[u] = 0;
-      d.uidx[x] = u;
+      d.present[x] = 0;  // the map's last reader (the compaction) is done
     }
     const uint32_t i = block_append(claim, &cn->n_touched);
     if (claim) {
@@ -395,7 +349,6 @@ __global__ void k_rank(const DevState d, Scratch sc, const Counters *cn) {
     sc.seg_u[off + r] = u;
     sc.seg_x[off + r] = x;
     sc.seg_st[off + r] = d.stat[x];
-    d.bitmap[x >> 5] = 0;  // the bitmap's last reader (the inverse) is done
   }
 }
 
@@ -773,10 +726,9 @@ __device__ __forceinline__ bool row_ends(const DevState &d, const Scratch &sc, u
 }
 
 template <CopyMode M, bool kPow2>
-__global__ __launch_bounds__(kBlock) void k_copy(const DevState d, Scratch sc, uint8_t *out, uint32_t nvec,
-                                                 uint32_t vshift, const Counters *cn) {
-  if (cn->err) return;
-  const uint64_t total = (uint64_t)cn->n_unique * nvec;
+__global__ __launch_bounds__(kBlock) void k_copy(const DevState d, Scratch sc, uint8_t *out, uint32_t n_unique,
+                                                 uint32_t nvec, uint32_t vshift) {
+  const uint64_t total = (uint64_t)n_unique * nvec;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
   for (uint64_t w0 = (uint64_t)blockIdx.x * kBlock + threadIdx.x; w0 < total; w0 += stride * kUnroll) {
     u32x4 v[kUnroll];
@@ -816,27 +768,27 @@ __global__ __launch_bounds__(kBlock) void k_copy(const DevState d, Scratch sc, u
 #endif
 
 template <CopyMode M>
-static void launch_copy_mode(const DevState &d, uint64_t max_rows, const Scratch &sc, uint8_t *out,
-                             const Counters *cn, hipStream_t s) {
+static void launch_copy_mode(const DevState &d, uint32_t n_unique, const Scratch &sc, uint8_t *out,
+                             hipStream_t s) {
   const uint32_t nvec = (uint32_t)(d.R / 16);
   const bool pow2 = (nvec & (nvec - 1)) == 0;
   const uint32_t vshift = pow2 ? (uint32_t)__builtin_ctz(nvec) : 0u;
   const unsigned cap = M == CopyMode::kHostToOut ? LSM_HOST_GRID
                        : M == CopyMode::kCacheToRing ? LSM_ENQ_GRID : LSM_HBM_GRID;
-  const unsigned g = grid_for(max_rows * nvec, (uint64_t)kBlock * kUnroll, cap);
+  const unsigned g = grid_for((uint64_t)n_unique * nvec, (uint64_t)kBlock * kUnroll, cap);
   if (pow2)
-    hipLaunchKernelGGL((k_copy<M, true>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift, cn);
+    hipLaunchKernelGGL((k_copy<M, true>), dim3(g), dim3(kBlock), 0, s, d, sc, out, n_unique, nvec, vshift);
   else
-    hipLaunchKernelGGL((k_copy<M, false>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift, cn);
+    hipLaunchKernelGGL((k_copy<M, false>), dim3(g), dim3(kBlock), 0, s, d, sc, out, n_unique, nvec, vshift);
 }
 
-void launch_copy(CopyMode mode, const DevState &d, uint64_t max_rows, const Scratch &sc, uint8_t *out,
-                 const Counters *cn, hipStream_t s) {
+void launch_copy(CopyMode mode, const DevState &d, uint32_t n_unique, const Scratch &sc, uint8_t *out,
+                 hipStream_t s) {
   switch (mode) {
-    case CopyMode::kHbmToOut: launch_copy_mode<CopyMode::kHbmToOut>(d, max_rows, sc, out, cn, s); break;
-    case CopyMode::kHostToOut: launch_copy_mode<CopyMode::kHostToOut>(d, max_rows, sc, out, cn, s); break;
-    case CopyMode::kCacheToRing: launch_copy_mode<CopyMode::kCacheToRing>(d, max_rows, sc, out, cn, s); break;
-    case CopyMode::kOutToCache: launch_copy_mode<CopyMode::kOutToCache>(d, max_rows, sc, out, cn, s); break;
+    case CopyMode::kHbmToOut: launch_copy_mode<CopyMode::kHbmToOut>(d, n_unique, sc, out, s); break;
+    case CopyMode::kHostToOut: launch_copy_mode<CopyMode::kHostToOut>(d, n_unique, sc, out, s); break;
+    case CopyMode::kCacheToRing: launch_copy_mode<CopyMode::kCacheToRing>(d, n_unique, sc, out, s); break;
+    case CopyMode::kOutToCache: launch_copy_mode<CopyMode::kOutToCache>(d, n_unique, sc, out, s); break;
   }
 }
 
@@ -869,33 +821,21 @@ void launch_copy_plain(const void *src, void *dst, uint64_t bytes, hipStream_t s
 
 // ------------------------------------------------------------------ window
 // Announce: validate the IDs and, when the list is recorded, copy it into its
-// window slot and set the minibatch's bit for every ID (combined per block in
-// LDS, so repeated IDs cost one global atomic per block).
-__global__ __launch_bounds__(kBlock) void k_window_set(const int64_t *ids, uint32_t n, uint64_t N, uint32_t bit,
-                                                       uint32_t *mask, int64_t *slot_ids, int record,
-                                                       Counters *cn) {
-  __shared__ LdsCombine tab;
-  const uint32_t base = blockIdx.x * kCombineItems;
+// window slot and set the minibatch's bit for every ID.  Only that bit of a
+// node's window word changes in this kernel (duplicates write the same value),
+// so a plain read-modify-write is exact.
+__global__ void k_window_set(const int64_t *ids, uint32_t n, uint64_t N, uint32_t bit, uint32_t *mask,
+                             int64_t *slot_ids, int record, Counters *cn) {
   bool bad = false;
-  if (record) combine_init(tab);
-  for (int k = 0; k < kCombinePerThread; ++k) {
-    const uint32_t i = base + k * kBlock + threadIdx.x;
-    if (i < n) {
-      const int64_t x = ids[i];
-      if (x < 0 || (uint64_t)x >= N) {
-        bad = true;
-      } else if (record) {
-        slot_ids[i] = x;
-        combine_or(tab, (uint32_t)x, 1u);
-      }
-    }
-  }
-  if (record) {
-    __syncthreads();
-    const uint32_t b = 1u << bit;
-    for (int h = threadIdx.x; h < kCombineSlots; h += kBlock) {
-      const uint32_t x = tab.key[h];
-      if (x != kEmpty) atomicOr(&mask[x], b);
+  const uint32_t b = 1u << bit;
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
+    const int64_t x = ids[i];
+    if (x < 0 || (uint64_t)x >= N) {
+      bad = true;
+    } else if (record) {
+      slot_ids[i] = x;
+      const uint32_t m = mask[x];
+      if (!(m & b)) mask[x] = m | b;
     }
   }
   if (__ballot(bad) && __lane_id() == 0) atomicOr(&cn->err, 1u);
@@ -908,18 +848,19 @@ __global__ void k_window_rollback(const int64_t *ids, uint32_t n, uint64_t N, ui
   if (!cn->err) return;
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
     const int64_t x = ids[i];
-    if (x >= 0 && (uint64_t)x < N) atomicAnd(&mask[x], ~(1u << bit));
+    if (x >= 0 && (uint64_t)x < N) {
+      const uint32_t m = mask[x];
+      if (m & (1u << bit)) mask[x] = m & ~(1u << bit);
+    }
   }
 }
 
 void launch_window_set(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
                        bool record, Counters *cn, hipStream_t s) {
-  const unsigned g = (unsigned)((n + kCombineItems - 1) / kCombineItems);
-  hipLaunchKernelGGL(k_window_set, dim3(g ? g : 1), dim3(kBlock), 0, s, ids, (uint32_t)n, N, bit, mask, slot_ids,
+  const unsigned g = grid_for(n, kBlock, kMaxGrid);
+  hipLaunchKernelGGL(k_window_set, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, N, bit, mask, slot_ids,
                      record ? 1 : 0, cn);
-  if (record)
-    hipLaunchKernelGGL(k_window_rollback, dim3(grid_for(n, kBlock, kMaxGrid)), dim3(kBlock), 0, s, ids,
-                       (uint32_t)n, N, bit, mask, cn);
+  if (record) hipLaunchKernelGGL(k_window_rollback, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, N, bit, mask, cn);
 }
 
 }  // namespace lsm

@@ -10,8 +10,9 @@ namespace lsm {
 constexpr uint32_t kWays = 8;
 constexpr uint32_t kEmpty = 0xffffffffu;
 constexpr int kBlock = 256;          // threads per block for every kernel
-constexpr int kWordsPerThread = 4;   // dedup bitmap words per thread
-constexpr int kChunkWords = kBlock * kWordsPerThread;  // bitmap words per block
+constexpr int kBytesPerThread = 64;  // dedup map bytes per thread
+constexpr int kWordsPerThread = kBytesPerThread / 4;
+constexpr int kChunkBytes = kBlock * kBytesPerThread;  // dedup map bytes per block
 constexpr int kScanPerThread = 8;    // flags per thread in the enqueue scan
 constexpr int kScanChunk = kBlock * kScanPerThread;
 
@@ -64,7 +65,18 @@ struct Counters {
   uint32_t pad[16];
 };
 
+// Dedup result of a gather, written to pinned host memory by the chunk scan:
+// the host waits for it before it launches the rest of the gather.
+struct DedupResult {
+  uint32_t err;
+  uint32_t n_unique;
+  uint32_t pad[2];
+};
+
 // Per-call scratch, every array sized for max_batch entries unless noted.
+// slot, src, ring_dst and fill_dst are read by the row copies of a gather while
+// the next gather's metadata kernels run, so the runtime keeps two of them and
+// alternates by gather parity.
 struct Scratch {
   uint32_t *uniq;       // ascending unique IDs
   uint32_t *uset;       // set of uniq[u]
@@ -99,8 +111,7 @@ struct DevState {
   uint32_t *ring_tag;    // [V]
   uint8_t *ring_rows;    // [V][R] pinned host, device-visible address
   const uint8_t *store;  // [N][R] pinned host, device-visible address
-  uint32_t *bitmap;      // [nchunks * kChunkWords] dedup bitmap (all zero between calls)
-  uint32_t *word_rank;   // [same] unique IDs before each nonzero word
+  uint8_t *present;      // [nchunks * kChunkBytes] dedup byte map (all zero between calls)
   uint32_t *chunk_sums;  // [nchunks]
   uint32_t *set_count;   // [S] (all zero between calls)
   uint32_t *set_idx;     // [S]
@@ -117,15 +128,16 @@ enum class CopyMode { kHbmToOut, kHostToOut, kCacheToRing, kOutToCache };
 void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, const StatGrids &grids,
                    hipStream_t s);
 void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, const int64_t *clear_ids, uint64_t clear_n,
-                  uint32_t clear_bit, Scratch &sc, int64_t *unique_out, Counters *cn, hipStream_t s);
+                  uint32_t clear_bit, Scratch &sc, int64_t *unique_out, Counters *cn, DedupResult *dd,
+                  hipStream_t s);
 void launch_group_by_set(const DevState &d, const int64_t *ids, uint64_t n, int64_t *inverse, Scratch &sc,
                          Counters *cn, hipStream_t s);
 void launch_set_walk(const DevState &d, uint64_t n, uint32_t t, Scratch &sc, Counters *cn, StatGrids &grids,
                      hipStream_t s);
 void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t tail0, Scratch &sc, uint8_t *outcome,
                          Counters *cn, StatGrids &grids, hipStream_t s);
-void launch_copy(CopyMode mode, const DevState &d, uint64_t max_rows, const Scratch &sc, uint8_t *out,
-                 const Counters *cn, hipStream_t s);
+void launch_copy(CopyMode mode, const DevState &d, uint32_t n_unique, const Scratch &sc, uint8_t *out,
+                 hipStream_t s);
 void launch_window_set(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
                        bool record, Counters *cn, hipStream_t s);
 void launch_copy_plain(const void *src, void *dst, uint64_t bytes, hipStream_t s);

@@ -2,7 +2,24 @@
 //
 // Owns every allocation (HBM cache and metadata, per-node arrays, scratch,
 // pinned victim ring), validates arguments before anything changes, and
-// launches the gfx950 pipeline of gather_kernels.hip on the caller's stream.
+// launches the gfx950 kernels of gather_kernels.hip.
+//
+// Streams.  A gather runs on three internal streams, all at default priority:
+//   meta  - dedup, set grouping, set walk, ring resolution, counters
+//   host  - the host fetch (misses and victim hits, PCIe ingress)
+//   data  - the enqueue copy (PCIe egress), the hit copy, the fills
+// The metadata of gather t+1 depends only on the metadata of gather t, so it
+// can run while gather t still moves rows.  The data kernels of a gather read
+// four per-unique arrays (slot, src, ring_dst, fill_dst) that its metadata
+// wrote; two copies of them alternate by gather parity, so gather t's
+// metadata first waits for gather t-2's data.  Other cross-gather hazards:
+//   - ring rows: gather t's host fetch waits for gather t-1's enqueue copy;
+//     gather t's enqueue copy follows gather t-1's fill on the data stream,
+//     and that fill waited for gather t-1's host fetch;
+//   - cache rows: gather t's hit and enqueue copies follow gather t-1's fill
+//     on the same stream.
+// Every call first makes the meta stream wait for the work already queued on
+// the caller's stream (the IDs and the output buffers).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -16,6 +33,7 @@
 
 using lsm::Counters;
 using lsm::CopyMode;
+using lsm::DedupResult;
 using lsm::DevState;
 using lsm::Scratch;
 
@@ -36,28 +54,44 @@ struct DeviceGuard {
 
 enum { kEvHbm0, kEvHbm1, kEvEnq0, kEvEnq1, kEvHost0, kEvHost1, kEvFill0, kEvFill1, kEvAll0, kEvAll1, kNumEv };
 
+// One gather in flight; two of these alternate by gather parity.
+struct Flight {
+  Scratch sc{};                // metadata scratch (shared) + this parity's per-unique arrays
+  Counters *hc = nullptr;      // pinned: counters published by the gather's last metadata kernel
+  Counters *hc_dev = nullptr;
+  hipEvent_t meta_done = nullptr, finish_done = nullptr, enq_done = nullptr, host_done = nullptr,
+             data_done = nullptr;
+  hipEvent_t pe[kNumEv] = {};  // profiling
+  bool used = false;           // events of this slot have been recorded at least once
+  bool stats_pending = false;  // counters not yet added to the totals
+  bool prof_pending = false;   // profiling events not yet read
+  bool ring = false;
+  uint64_t t = 0, requests = 0;
+};
+
 }  // namespace
 
 struct lsmgnn_cache {
   int device = 0;
   DevState d{};
-  Scratch sc{};
   uint64_t max_batch = 0;
   int64_t *win_ids = nullptr;  // (L+1) slots of max_batch IDs
   int64_t win_batch[kMaxSlots];
   uint64_t win_len[kMaxSlots];
-  Counters *cn = nullptr;       // device
-  Counters *cn_host = nullptr;  // pinned host mirror, written by the last kernel of each call
-  Counters *cn_host_dev = nullptr;
-  uint64_t t = 0, n_adv = 0, tail = 0;
+  Counters *cn = nullptr;      // counters of the metadata kernels (meta stream only)
+  Counters *cn_adv = nullptr;  // counters of announcements
+  Counters *hc_adv = nullptr, *hc_adv_dev = nullptr;
+  DedupResult *dd = nullptr, *dd_dev = nullptr;
+  Flight fl[2];
+  hipStream_t meta = nullptr, host = nullptr, data = nullptr;
+  hipEvent_t ev_in = nullptr, ev_dedup = nullptr, ev_adv = nullptr;
+  uint64_t t = 0;  // gathers issued
+  uint64_t n_adv = 0, tail = 0;
   lsmgnn_counts last{}, total{};
   bool broken = false;
   std::vector<void *> dev_allocs;
-  void *ring_host = nullptr;
-  hipStream_t side = nullptr;           // host-fetch stream (default priority)
-  hipEvent_t ev_meta = nullptr, ev_host = nullptr;
+  std::vector<void *> host_allocs;
   int prof = 0;
-  hipEvent_t ev[kNumEv] = {};
   lsmgnn_profile acc{};
 };
 
@@ -66,13 +100,18 @@ namespace {
 void release(lsmgnn_cache *c) {
   for (void *p : c->dev_allocs) (void)hipFree(p);
   c->dev_allocs.clear();
-  if (c->ring_host) (void)hipHostFree(c->ring_host);
-  if (c->cn_host) (void)hipHostFree(c->cn_host);
-  for (auto &e : c->ev)
+  for (void *p : c->host_allocs) (void)hipHostFree(p);
+  c->host_allocs.clear();
+  for (Flight &f : c->fl) {
+    for (hipEvent_t e : {f.meta_done, f.finish_done, f.enq_done, f.host_done, f.data_done})
+      if (e) (void)hipEventDestroy(e);
+    for (hipEvent_t e : f.pe)
+      if (e) (void)hipEventDestroy(e);
+  }
+  for (hipEvent_t e : {c->ev_in, c->ev_dedup, c->ev_adv})
     if (e) (void)hipEventDestroy(e);
-  if (c->ev_meta) (void)hipEventDestroy(c->ev_meta);
-  if (c->ev_host) (void)hipEventDestroy(c->ev_host);
-  if (c->side) (void)hipStreamDestroy(c->side);
+  for (hipStream_t s : {c->meta, c->host, c->data})
+    if (s) (void)hipStreamDestroy(s);
 }
 
 template <typename T>
@@ -87,9 +126,209 @@ bool dev_alloc(lsmgnn_cache *c, T **p, uint64_t count) {
   return true;
 }
 
+// Pinned, device-mapped host memory; *dev receives its device-side address.
+template <typename T>
+bool host_alloc(lsmgnn_cache *c, T **p, T **dev, uint64_t bytes, bool zero) {
+  void *q = nullptr, *qd = nullptr;
+  if (hipHostMalloc(&q, bytes, hipHostMallocMapped | hipHostMallocPortable) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  c->host_allocs.push_back(q);
+  if (hipHostGetDevicePointer(&qd, q, 0) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  if (zero) std::memset(q, 0, bytes);
+  *p = static_cast<T *>(q);
+  *dev = static_cast<T *>(qd);
+  return true;
+}
+
 lsmgnn_status fail_device(lsmgnn_cache *c) {
+  (void)hipGetLastError();
   c->broken = true;
   return LSMGNN_E_DEVICE;
+}
+
+// Add a finished gather's counters to the totals (its counter kernel must be
+// complete).  Gathers are accounted in issue order.
+void harvest_stats(lsmgnn_cache *c, Flight &f) {
+  if (!f.stats_pending) return;
+  const Counters &h = *f.hc;
+  lsmgnn_counts st{};
+  st.batch = f.t;
+  st.requests = f.requests;
+  st.unique = h.n_unique;
+  st.hits = h.hits;
+  st.victim_hits = h.victim_hits;
+  st.misses = h.misses;
+  st.evictions = h.evictions;
+  st.enqueued = h.enqueued;
+  st.dropped = h.dropped;
+  c->last = st;
+  c->total.batch = f.t + 1;
+  c->total.requests += st.requests;
+  c->total.unique += st.unique;
+  c->total.hits += st.hits;
+  c->total.victim_hits += st.victim_hits;
+  c->total.misses += st.misses;
+  c->total.evictions += st.evictions;
+  c->total.enqueued += st.enqueued;
+  c->total.dropped += st.dropped;
+  c->tail += h.enq_total;
+  f.stats_pending = false;
+}
+
+// Read a finished gather's kernel timings (its rows must have moved).
+void harvest_profile(lsmgnn_cache *c, Flight &f) {
+  if (!f.prof_pending) return;
+  auto el = [&](int a, int b) {
+    float v = 0;
+    return hipEventElapsedTime(&v, f.pe[a], f.pe[b]) == hipSuccess ? (double)v : 0.0;
+  };
+  const Counters &h = *f.hc;
+  c->acc.gather_ms += el(kEvAll0, kEvAll1);
+  c->acc.gathers += 1;
+  if (f.requests) {
+    c->acc.hbm_copy_ms += el(kEvHbm0, kEvHbm1);
+    c->acc.hbm_copy_launches += 1;
+    c->acc.hbm_copy_rows += h.n_hbm;
+    if (f.ring) {
+      c->acc.enqueue_ms += el(kEvEnq0, kEvEnq1);
+      c->acc.enqueue_launches += 1;
+      c->acc.enqueue_rows += h.n_enq_copy;
+    }
+    c->acc.host_fetch_ms += el(kEvHost0, kEvHost1);
+    c->acc.host_fetch_launches += 1;
+    c->acc.host_fetch_rows += h.n_host;
+    c->acc.fill_ms += el(kEvFill0, kEvFill1);
+    c->acc.fill_launches += 1;
+    c->acc.fill_rows += h.n_fill;
+  }
+  (void)hipGetLastError();
+  f.prof_pending = false;
+}
+
+// Wait for every queued kernel, then account everything in issue order.
+lsmgnn_status sync_all(lsmgnn_cache *c) {
+  for (hipStream_t s : {c->meta, c->host, c->data})
+    if (hipStreamSynchronize(s) != hipSuccess) return fail_device(c);
+  Flight &older = c->fl[c->t & 1], &newer = c->fl[(c->t + 1) & 1];
+  harvest_stats(c, older);
+  harvest_stats(c, newer);
+  harvest_profile(c, older);
+  harvest_profile(c, newer);
+  return LSMGNN_OK;
+}
+
+// Queue one gather.  Returns once its unique count is known; its row movement
+// may still be running on the host and data streams.
+lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t *unique_ids,
+                           int64_t *inverse, uint8_t *outcome, uint64_t *n_unique, hipStream_t s, Flight **used) {
+  DevState &d = c->d;
+  const uint64_t t = c->t;
+  Flight &f = c->fl[t & 1];
+  Flight &pf = c->fl[(t + 1) & 1];  // gather t-1
+  const bool prof = c->prof != 0;
+  auto rec = [&](int e, hipStream_t st) {
+    if (prof) (void)hipEventRecord(f.pe[e], st);
+  };
+  uint8_t *outp = static_cast<uint8_t *>(out);
+
+  // inputs are ready once the caller's queued work is; this parity's arrays
+  // are free once gather t-2's rows have moved
+  if (hipEventRecord(c->ev_in, s) != hipSuccess) return fail_device(c);
+  (void)hipStreamWaitEvent(c->meta, c->ev_in, 0);
+  if (f.used) (void)hipStreamWaitEvent(c->meta, f.data_done, 0);
+
+  // the window list of the minibatch being gathered is never consulted again:
+  // the first kernel clears its bits
+  const int slot = (int)(t % (d.L + 1));
+  const bool clear = d.L > 0 && c->win_batch[slot] == (int64_t)t;
+  const int64_t *clear_ids = clear ? c->win_ids + (uint64_t)slot * c->max_batch : nullptr;
+  const uint64_t clear_n = clear ? c->win_len[slot] : 0;
+
+  rec(kEvAll0, c->meta);
+  const bool dedup = n || clear_n;
+  if (dedup)
+    lsm::launch_dedup(d, ids, n, clear_ids, clear_n, (uint32_t)(t & 31u), f.sc, unique_ids, c->cn, c->dd_dev,
+                      c->meta);
+  if (hipEventRecord(c->ev_dedup, c->meta) != hipSuccess || hipGetLastError() != hipSuccess ||
+      hipEventSynchronize(c->ev_dedup) != hipSuccess)
+    return fail_device(c);
+  // the meta stream is in order: gather t-1's counters are published, and
+  // gather t-2's rows have moved
+  harvest_stats(c, pf);
+  harvest_profile(c, f);
+  const uint32_t err = dedup ? c->dd->err : 0u;
+  const uint32_t U = dedup ? c->dd->n_unique : 0u;
+  if (err) {
+    // rejected: the marks are already undone; re-zero the counters (the
+    // announcement mirror receives them and nobody reads it now)
+    lsm::launch_finish(c->cn, c->hc_adv_dev, f.sc.stat_part, lsm::StatGrids{}, c->meta);
+    if (hipGetLastError() != hipSuccess || hipStreamSynchronize(c->meta) != hipSuccess) return fail_device(c);
+    return LSMGNN_E_RANGE;
+  }
+
+  f.used = true;
+  f.t = t;
+  f.requests = n;
+  f.ring = d.V > 0;
+  lsm::StatGrids grids{};
+  if (n) {
+    lsm::launch_group_by_set(d, ids, n, inverse, f.sc, c->cn, c->meta);
+    lsm::launch_set_walk(d, n, (uint32_t)t, f.sc, c->cn, grids, c->meta);
+    lsm::launch_ring_resolve(d, n, c->tail, f.sc, outcome, c->cn, grids, c->meta);
+  }
+  (void)hipEventRecord(f.meta_done, c->meta);
+  lsm::launch_finish(c->cn, f.hc_dev, f.sc.stat_part, grids, c->meta);
+  (void)hipEventRecord(f.finish_done, c->meta);
+  f.stats_pending = true;
+
+  // host fetch (PCIe ingress) beside the enqueue copy (PCIe egress) and the
+  // hit copy; fills after both
+  (void)hipStreamWaitEvent(c->host, f.meta_done, 0);
+  if (pf.used) (void)hipStreamWaitEvent(c->host, pf.enq_done, 0);
+  rec(kEvHost0, c->host);
+  if (n) lsm::launch_copy(CopyMode::kHostToOut, d, U, f.sc, outp, c->host);
+  rec(kEvHost1, c->host);
+  (void)hipEventRecord(f.host_done, c->host);
+
+  (void)hipStreamWaitEvent(c->data, f.meta_done, 0);
+  rec(kEvEnq0, c->data);
+  if (n && d.V) lsm::launch_copy(CopyMode::kCacheToRing, d, U, f.sc, outp, c->data);
+  rec(kEvEnq1, c->data);
+  (void)hipEventRecord(f.enq_done, c->data);
+  rec(kEvHbm0, c->data);
+  if (n) lsm::launch_copy(CopyMode::kHbmToOut, d, U, f.sc, outp, c->data);
+  rec(kEvHbm1, c->data);
+  (void)hipStreamWaitEvent(c->data, f.host_done, 0);
+  rec(kEvFill0, c->data);
+  if (n) lsm::launch_copy(CopyMode::kOutToCache, d, U, f.sc, outp, c->data);
+  rec(kEvFill1, c->data);
+  rec(kEvAll1, c->data);
+  (void)hipEventRecord(f.data_done, c->data);
+  f.prof_pending = prof;
+  if (hipGetLastError() != hipSuccess) return fail_device(c);
+
+  if (clear) c->win_batch[slot] = -1;
+  c->t = t + 1;
+  *n_unique = U;
+  if (used) *used = &f;
+  return LSMGNN_OK;
+}
+
+lsmgnn_status check_gather_args(const lsmgnn_cache *c, const int64_t *ids, uint64_t n, const void *out,
+                                const int64_t *unique_ids, const int64_t *inverse, const uint64_t *n_unique) {
+  if (!c) return LSMGNN_E_INVAL;
+  if (c->broken) return LSMGNN_E_STATE;
+  if (!n_unique || n > c->max_batch || (n && (!ids || !out || !unique_ids))) return LSMGNN_E_INVAL;
+  // rows move as 16-byte vectors; ID arrays as 8-byte words
+  if ((reinterpret_cast<uintptr_t>(out) & 15u) || (reinterpret_cast<uintptr_t>(ids) & 7u) ||
+      (reinterpret_cast<uintptr_t>(unique_ids) & 7u) || (reinterpret_cast<uintptr_t>(inverse) & 7u))
+    return LSMGNN_E_INVAL;
+  return LSMGNN_OK;
 }
 
 }  // namespace
@@ -170,64 +409,55 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   d.L = cfg->lookahead;
   d.T = cfg->near_threshold ? cfg->near_threshold : (cfg->lookahead / 8 > 1 ? cfg->lookahead / 8 : 1);
   d.store = static_cast<const uint8_t *>(store_dev);
-  const uint64_t nwords = (N + 31) / 32;
-  d.nchunks = (nwords + lsm::kChunkWords - 1) / lsm::kChunkWords;
-  const uint64_t bitmap_words = d.nchunks * lsm::kChunkWords;
+  d.nchunks = (N + lsm::kChunkBytes - 1) / lsm::kChunkBytes;
+  const uint64_t map_bytes = d.nchunks * lsm::kChunkBytes;
   const uint64_t B = cfg->max_batch;
-  Scratch &sc = c->sc;
+  Scratch sc{};
 
   bool ok = dev_alloc(c, &d.sets, S) && dev_alloc(c, &d.rows, S * lsm::kWays * R) && dev_alloc(c, &d.mask, N) &&
-            dev_alloc(c, &d.stat, N) && dev_alloc(c, &d.bitmap, bitmap_words) &&
-            dev_alloc(c, &d.word_rank, bitmap_words) && dev_alloc(c, &d.chunk_sums, d.nchunks) &&
+            dev_alloc(c, &d.stat, N) && dev_alloc(c, &d.present, map_bytes) &&
+            dev_alloc(c, &d.chunk_sums, d.nchunks) &&
             dev_alloc(c, &d.set_count, S) && dev_alloc(c, &d.set_idx, S) && dev_alloc(c, &d.uidx, N) &&
             (V == 0 || (dev_alloc(c, &d.vpos, N) && dev_alloc(c, &d.ring_tag, V))) &&
             dev_alloc(c, &c->win_ids, (uint64_t)(d.L + 1) * B) && dev_alloc(c, &c->cn, 1) &&
-            dev_alloc(c, &sc.uniq, B) && dev_alloc(c, &sc.uset, B) && dev_alloc(c, &sc.arrival, B) &&
-            dev_alloc(c, &sc.touched, B) && dev_alloc(c, &sc.seg_off, B) && dev_alloc(c, &sc.seg, B) &&
-            dev_alloc(c, &sc.seg_u, B) && dev_alloc(c, &sc.seg_x, B) && dev_alloc(c, &sc.seg_st, B) &&
-            dev_alloc(c, &sc.kind, B) && dev_alloc(c, &sc.flags, B) && dev_alloc(c, &sc.dead, B) &&
-            dev_alloc(c, &sc.slot, B) && dev_alloc(c, &sc.evicted, B) && dev_alloc(c, &sc.enq_before, B) &&
+            dev_alloc(c, &c->cn_adv, 1) && dev_alloc(c, &sc.uniq, B) && dev_alloc(c, &sc.uset, B) &&
+            dev_alloc(c, &sc.arrival, B) && dev_alloc(c, &sc.touched, B) && dev_alloc(c, &sc.seg_off, B) &&
+            dev_alloc(c, &sc.seg, B) && dev_alloc(c, &sc.seg_u, B) && dev_alloc(c, &sc.seg_x, B) &&
+            dev_alloc(c, &sc.seg_st, B) && dev_alloc(c, &sc.kind, B) && dev_alloc(c, &sc.flags, B) &&
+            dev_alloc(c, &sc.dead, B) && dev_alloc(c, &sc.evicted, B) && dev_alloc(c, &sc.enq_before, B) &&
             dev_alloc(c, &sc.scan_part, B / lsm::kScanChunk + 2) && dev_alloc(c, &sc.this_q, B) &&
-            dev_alloc(c, &sc.this_enq, B) && dev_alloc(c, &sc.src, B) && dev_alloc(c, &sc.ring_dst, B) &&
-            dev_alloc(c, &sc.fill_dst, B) && dev_alloc(c, &sc.stat_part, (uint64_t)lsm::kNumStat * lsm::kMaxGrid);
-  if (ok && hipHostMalloc(reinterpret_cast<void **>(&c->cn_host), sizeof(Counters), hipHostMallocMapped) !=
-                hipSuccess) {
-    (void)hipGetLastError();
-    c->cn_host = nullptr;
-    ok = false;
-  }
-  if (ok && hipHostGetDevicePointer(reinterpret_cast<void **>(&c->cn_host_dev), c->cn_host, 0) != hipSuccess) {
-    (void)hipGetLastError();
-    ok = false;
+            dev_alloc(c, &sc.this_enq, B) &&
+            dev_alloc(c, &sc.stat_part, (uint64_t)lsm::kNumStat * lsm::kMaxGrid) &&
+            host_alloc(c, &c->dd, &c->dd_dev, sizeof(DedupResult), true) &&
+            host_alloc(c, &c->hc_adv, &c->hc_adv_dev, sizeof(Counters), true);
+  for (Flight &f : c->fl) {
+    f.sc = sc;
+    ok = ok && dev_alloc(c, &f.sc.slot, B) && dev_alloc(c, &f.sc.src, B) && dev_alloc(c, &f.sc.ring_dst, B) &&
+         dev_alloc(c, &f.sc.fill_dst, B) && host_alloc(c, &f.hc, &f.hc_dev, sizeof(Counters), true);
   }
   if (ok && V) {
-    if (hipHostMalloc(&c->ring_host, V * R, hipHostMallocMapped | hipHostMallocPortable) != hipSuccess) {
-      (void)hipGetLastError();
-      c->ring_host = nullptr;
-      ok = false;
-    } else {
-      void *rd = nullptr;
-      if (hipHostGetDevicePointer(&rd, c->ring_host, 0) != hipSuccess) {
-        (void)hipGetLastError();
-        ok = false;
-      }
-      d.ring_rows = static_cast<uint8_t *>(rd);
-    }
+    uint8_t *ring_host = nullptr;
+    ok = host_alloc(c, &ring_host, &d.ring_rows, V * R, false);
   }
   if (!ok) {
     release(c);
     delete c;
     return LSMGNN_E_NOMEM;
   }
-  for (auto &e : c->ev)
-    if (hipEventCreate(&e) != hipSuccess) ok = false;
-  ok = ok && hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) == hipSuccess &&
-       hipEventCreateWithFlags(&c->ev_meta, hipEventDisableTiming) == hipSuccess &&
-       hipEventCreateWithFlags(&c->ev_host, hipEventDisableTiming) == hipSuccess;
-  // initial state: all ways empty, nothing announced, ring empty
+  for (hipStream_t *s : {&c->meta, &c->host, &c->data})
+    ok = ok && hipStreamCreateWithFlags(s, hipStreamNonBlocking) == hipSuccess;
+  for (hipEvent_t *e : {&c->ev_in, &c->ev_dedup, &c->ev_adv})
+    ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
+  for (Flight &f : c->fl) {
+    for (hipEvent_t *e : {&f.meta_done, &f.finish_done, &f.enq_done, &f.host_done, &f.data_done})
+      ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
+    for (hipEvent_t &e : f.pe) ok = ok && hipEventCreate(&e) == hipSuccess;
+  }
+  // initial state: all ways empty, nothing announced, ring empty, counters zero
   ok = ok && hipMemset(d.sets, 0xff, S * sizeof(lsm::SetRec)) == hipSuccess &&
-       hipMemset(d.mask, 0, N * 4) == hipSuccess && hipMemset(d.bitmap, 0, bitmap_words * 4) == hipSuccess &&
+       hipMemset(d.mask, 0, N * 4) == hipSuccess && hipMemset(d.present, 0, map_bytes) == hipSuccess &&
        hipMemset(d.set_count, 0, S * 4) == hipSuccess && hipMemset(c->cn, 0, sizeof(Counters)) == hipSuccess &&
+       hipMemset(c->cn_adv, 0, sizeof(Counters)) == hipSuccess &&
        hipMemcpy(d.stat, cfg->static_score, N * 4, hipMemcpyHostToDevice) == hipSuccess &&
        (V == 0 || (hipMemset(d.vpos, 0, N * 8) == hipSuccess && hipMemset(d.ring_tag, 0xff, V * 4) == hipSuccess)) &&
        hipDeviceSynchronize() == hipSuccess;
@@ -245,7 +475,8 @@ void lsmgnn_cache_destroy(lsmgnn_cache *c) {
   if (!c) return;
   {
     DeviceGuard guard(c->device);
-    (void)hipDeviceSynchronize();
+    for (hipStream_t s : {c->meta, c->host, c->data})
+      if (s) (void)hipStreamSynchronize(s);
     release(c);
   }
   delete c;
@@ -262,15 +493,16 @@ lsmgnn_status lsmgnn_advance(lsmgnn_cache *c, const int64_t *ids, uint64_t n, vo
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool record = j > c->t && c->d.L > 0 && n > 0;  // lists for j <= t are never consulted
   const int slot = (int)(j % (c->d.L + 1));
+  if (hipEventRecord(c->ev_in, s) != hipSuccess) return fail_device(c);
+  (void)hipStreamWaitEvent(c->meta, c->ev_in, 0);
   if (n)
     lsm::launch_window_set(ids, n, c->d.N, (uint32_t)(j & 31u), c->d.mask,
-                           c->win_ids + (uint64_t)slot * c->max_batch, record, c->cn, s);
-  lsm::launch_finish(c->cn, c->cn_host_dev, c->sc.stat_part, lsm::StatGrids{}, s);
-  if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) {
-    (void)hipGetLastError();
+                           c->win_ids + (uint64_t)slot * c->max_batch, record, c->cn_adv, c->meta);
+  lsm::launch_finish(c->cn_adv, c->hc_adv_dev, c->fl[0].sc.stat_part, lsm::StatGrids{}, c->meta);
+  if (hipEventRecord(c->ev_adv, c->meta) != hipSuccess || hipGetLastError() != hipSuccess ||
+      hipEventSynchronize(c->ev_adv) != hipSuccess)
     return fail_device(c);
-  }
-  if (c->cn_host->err) return LSMGNN_E_RANGE;
+  if (c->hc_adv->err) return LSMGNN_E_RANGE;
   if (record) {
     c->win_batch[slot] = (int64_t)j;
     c->win_len[slot] = n;
@@ -281,137 +513,69 @@ lsmgnn_status lsmgnn_advance(lsmgnn_cache *c, const int64_t *ids, uint64_t n, vo
 
 lsmgnn_status lsmgnn_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t *unique_ids,
                             int64_t *inverse, uint8_t *outcome, uint64_t *n_unique, void *stream) {
-  if (!c) return LSMGNN_E_INVAL;
-  if (c->broken) return LSMGNN_E_STATE;
-  if (!n_unique || n > c->max_batch || (n && (!ids || !out || !unique_ids))) return LSMGNN_E_INVAL;
-  // rows move as 16-byte vectors; ID arrays as 8-byte words
-  if ((reinterpret_cast<uintptr_t>(out) & 15u) || (reinterpret_cast<uintptr_t>(ids) & 7u) ||
-      (reinterpret_cast<uintptr_t>(unique_ids) & 7u) || (reinterpret_cast<uintptr_t>(inverse) & 7u))
-    return LSMGNN_E_INVAL;
+  lsmgnn_status st = check_gather_args(c, ids, n, out, unique_ids, inverse, n_unique);
+  if (st != LSMGNN_OK) return st;
   DeviceGuard guard(c->device);
   if (!guard.ok) return LSMGNN_E_DEVICE;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  DevState &d = c->d;
-  Scratch &sc = c->sc;
-  const uint32_t t = (uint32_t)c->t;
-  const bool prof = c->prof != 0;
-  auto rec = [&](int e) {
-    if (prof) (void)hipEventRecord(c->ev[e], s);
-  };
-  uint8_t *outp = static_cast<uint8_t *>(out);
-
-  // the window list of the minibatch being gathered is cleared by the first
-  // kernel (it is never consulted again)
-  const int slot = (int)(c->t % (d.L + 1));
-  const bool clear = d.L > 0 && c->win_batch[slot] == (int64_t)c->t;
-  const int64_t *clear_ids = clear ? c->win_ids + (uint64_t)slot * c->max_batch : nullptr;
-  const uint64_t clear_n = clear ? c->win_len[slot] : 0;
-
-  lsm::StatGrids grids{};
-  rec(kEvAll0);
-  if (n || clear_n) lsm::launch_dedup(d, ids, n, clear_ids, clear_n, (uint32_t)(c->t & 31u), sc, unique_ids, c->cn, s);
-  if (n) {
-    lsm::launch_group_by_set(d, ids, n, inverse, sc, c->cn, s);
-    lsm::launch_set_walk(d, n, t, sc, c->cn, grids, s);
-    lsm::launch_ring_resolve(d, n, c->tail, sc, outcome, c->cn, grids, s);
-    // Data movement.  Every read of a batch-start row precedes every write to
-    // the same place: cache rows are read by the hit copy and the enqueue copy
-    // before fills overwrite them.  The host fetch (PCIe ingress) runs on the
-    // side stream concurrently with the hit copy and the enqueue copy (PCIe
-    // egress); it never reads a ring slot an enqueue of this batch rewrites.
-    (void)hipEventRecord(c->ev_meta, s);
-    (void)hipStreamWaitEvent(c->side, c->ev_meta, 0);
-    if (prof) (void)hipEventRecord(c->ev[kEvHost0], c->side);
-    lsm::launch_copy(CopyMode::kHostToOut, d, n, sc, outp, c->cn, c->side);
-    if (prof) (void)hipEventRecord(c->ev[kEvHost1], c->side);
-    (void)hipEventRecord(c->ev_host, c->side);
-    if (d.V) {
-      rec(kEvEnq0);
-      lsm::launch_copy(CopyMode::kCacheToRing, d, n, sc, outp, c->cn, s);
-      rec(kEvEnq1);
-    }
-    rec(kEvHbm0);
-    lsm::launch_copy(CopyMode::kHbmToOut, d, n, sc, outp, c->cn, s);
-    rec(kEvHbm1);
-    (void)hipStreamWaitEvent(s, c->ev_host, 0);
-    rec(kEvFill0);
-    lsm::launch_copy(CopyMode::kOutToCache, d, n, sc, outp, c->cn, s);
-    rec(kEvFill1);
-  }
-  lsm::launch_finish(c->cn, c->cn_host_dev, sc.stat_part, grids, s);
-  rec(kEvAll1);
-  if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) {
-    (void)hipGetLastError();
+  Flight *f = nullptr;
+  st = issue_gather(c, ids, n, out, unique_ids, inverse, outcome, n_unique, s, &f);
+  if (st != LSMGNN_OK) return st;
+  if (hipStreamWaitEvent(s, f->data_done, 0) != hipSuccess || hipEventSynchronize(f->finish_done) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
     return fail_device(c);
-  }
-  const Counters &h = *c->cn_host;
-  if (h.err) return LSMGNN_E_RANGE;
-
-  if (prof) {
-    float ms = 0;
-    auto el = [&](int a, int b) {
-      float v = 0;
-      return hipEventElapsedTime(&v, c->ev[a], c->ev[b]) == hipSuccess ? (double)v : 0.0;
-    };
-    c->acc.gather_ms += el(kEvAll0, kEvAll1);
-    c->acc.gathers += 1;
-    if (n) {
-      c->acc.hbm_copy_ms += el(kEvHbm0, kEvHbm1);
-      c->acc.hbm_copy_launches += 1;
-      c->acc.hbm_copy_rows += h.n_hbm;
-      if (d.V) {
-        c->acc.enqueue_ms += el(kEvEnq0, kEvEnq1);
-        c->acc.enqueue_launches += 1;
-        c->acc.enqueue_rows += h.n_enq_copy;
-      }
-      c->acc.host_fetch_ms += el(kEvHost0, kEvHost1);
-      c->acc.host_fetch_launches += 1;
-      c->acc.host_fetch_rows += h.n_host;
-      c->acc.fill_ms += el(kEvFill0, kEvFill1);
-      c->acc.fill_launches += 1;
-      c->acc.fill_rows += h.n_fill;
-    }
-    (void)ms;
-  }
-
-  *n_unique = h.n_unique;
-  lsmgnn_counts st{};
-  st.batch = c->t;
-  st.requests = n;
-  st.unique = h.n_unique;
-  st.hits = h.hits;
-  st.victim_hits = h.victim_hits;
-  st.misses = h.misses;
-  st.evictions = h.evictions;
-  st.enqueued = h.enqueued;
-  st.dropped = h.dropped;
-  c->last = st;
-  c->total.batch = c->t + 1;
-  c->total.requests += st.requests;
-  c->total.unique += st.unique;
-  c->total.hits += st.hits;
-  c->total.victim_hits += st.victim_hits;
-  c->total.misses += st.misses;
-  c->total.evictions += st.evictions;
-  c->total.enqueued += st.enqueued;
-  c->total.dropped += st.dropped;
-  c->tail += h.enq_total;
-  if (clear) c->win_batch[slot] = -1;
-  c->t += 1;
+  harvest_stats(c, *f);
+  harvest_profile(c, *f);
   return LSMGNN_OK;
 }
 
-lsmgnn_status lsmgnn_stats(const lsmgnn_cache *c, lsmgnn_counts *last, lsmgnn_counts *total) {
+lsmgnn_status lsmgnn_gather_async(lsmgnn_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t *unique_ids,
+                                  int64_t *inverse, uint8_t *outcome, uint64_t *n_unique, uint64_t *ticket,
+                                  void *stream) {
+  lsmgnn_status st = check_gather_args(c, ids, n, out, unique_ids, inverse, n_unique);
+  if (st != LSMGNN_OK) return st;
+  if (!ticket) return LSMGNN_E_INVAL;
+  DeviceGuard guard(c->device);
+  if (!guard.ok) return LSMGNN_E_DEVICE;
+  const uint64_t t = c->t;
+  st = issue_gather(c, ids, n, out, unique_ids, inverse, outcome, n_unique, static_cast<hipStream_t>(stream),
+                    nullptr);
+  if (st == LSMGNN_OK) *ticket = t;
+  return st;
+}
+
+lsmgnn_status lsmgnn_gather_wait(lsmgnn_cache *c, uint64_t ticket, void *stream) {
   if (!c) return LSMGNN_E_INVAL;
+  if (c->broken) return LSMGNN_E_STATE;
+  if (ticket >= c->t) return LSMGNN_E_INVAL;
+  DeviceGuard guard(c->device);
+  if (!guard.ok) return LSMGNN_E_DEVICE;
+  // the slot may hold a later gather by now: waiting for that one is conservative
+  if (hipStreamWaitEvent(static_cast<hipStream_t>(stream), c->fl[ticket & 1].data_done, 0) != hipSuccess)
+    return fail_device(c);
+  return LSMGNN_OK;
+}
+
+lsmgnn_status lsmgnn_sync(lsmgnn_cache *c) {
+  if (!c) return LSMGNN_E_INVAL;
+  if (c->broken) return LSMGNN_E_STATE;
+  DeviceGuard guard(c->device);
+  if (!guard.ok) return LSMGNN_E_DEVICE;
+  return sync_all(c);
+}
+
+lsmgnn_status lsmgnn_stats(lsmgnn_cache *c, lsmgnn_counts *last, lsmgnn_counts *total) {
+  lsmgnn_status st = lsmgnn_sync(c);
+  if (st != LSMGNN_OK) return st;
   if (last) *last = c->last;
   if (total) *total = c->total;
   return LSMGNN_OK;
 }
 
-lsmgnn_status lsmgnn_export_state(const lsmgnn_cache *c, uint32_t *tags, uint32_t *ring_tags, uint64_t *ring_tail,
+lsmgnn_status lsmgnn_export_state(lsmgnn_cache *c, uint32_t *tags, uint32_t *ring_tags, uint64_t *ring_tail,
                                   uint64_t *t) {
-  if (!c) return LSMGNN_E_INVAL;
-  if (c->broken) return LSMGNN_E_STATE;
+  lsmgnn_status st = lsmgnn_sync(c);
+  if (st != LSMGNN_OK) return st;
   DeviceGuard guard(c->device);
   if (!guard.ok) return LSMGNN_E_DEVICE;
   if (tags) {
@@ -473,14 +637,17 @@ lsmgnn_status lsmgnn_copy_bytes(void *dst, const void *src, uint64_t bytes, void
 }
 
 lsmgnn_status lsmgnn_set_profiling(lsmgnn_cache *c, int on) {
-  if (!c) return LSMGNN_E_INVAL;
+  lsmgnn_status st = lsmgnn_sync(c);
+  if (st != LSMGNN_OK) return st;
   c->prof = on ? 1 : 0;
   if (on) c->acc = lsmgnn_profile{};
   return LSMGNN_OK;
 }
 
-lsmgnn_status lsmgnn_get_profile(const lsmgnn_cache *c, lsmgnn_profile *out) {
-  if (!c || !out) return LSMGNN_E_INVAL;
+lsmgnn_status lsmgnn_get_profile(lsmgnn_cache *c, lsmgnn_profile *out) {
+  if (!out) return LSMGNN_E_INVAL;
+  lsmgnn_status st = lsmgnn_sync(c);
+  if (st != LSMGNN_OK) return st;
   *out = c->acc;
   return LSMGNN_OK;
 }

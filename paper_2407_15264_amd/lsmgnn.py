@@ -7,7 +7,6 @@ is no CPU fallback: if the library is missing this module raises.
 from __future__ import annotations
 
 import ctypes
-import dataclasses
 import os
 
 import numpy as np
@@ -72,6 +71,12 @@ def lib():
         L.lsmgnn_advance.argtypes = [vp, vp, u64, vp]
         L.lsmgnn_gather.restype = i32
         L.lsmgnn_gather.argtypes = [vp, vp, u64, vp, vp, vp, vp, ctypes.POINTER(u64), vp]
+        L.lsmgnn_gather_async.restype = i32
+        L.lsmgnn_gather_async.argtypes = [vp, vp, u64, vp, vp, vp, vp, ctypes.POINTER(u64), ctypes.POINTER(u64), vp]
+        L.lsmgnn_gather_wait.restype = i32
+        L.lsmgnn_gather_wait.argtypes = [vp, u64, vp]
+        L.lsmgnn_sync.restype = i32
+        L.lsmgnn_sync.argtypes = [vp]
         L.lsmgnn_stats.restype = i32
         L.lsmgnn_stats.argtypes = [vp, ctypes.POINTER(Counts), ctypes.POINTER(Counts)]
         L.lsmgnn_export_state.restype = i32
@@ -146,13 +151,35 @@ def _dev_ptr(t, dtype, name):
     return ctypes.c_void_p(t.data_ptr())
 
 
-@dataclasses.dataclass
 class GatherResult:
-    n_unique: int
-    out: "object"        # torch uint8 view (n_unique, row_bytes) of the caller's buffer
-    unique: "object"     # torch int64 (n_unique,)
-    inverse: "object"    # torch int64 (n,) or None
-    outcome: "object"    # torch uint8 (n_unique,) or None
+    """Outputs of one gather as views of the caller's buffers (built on first
+    access, so the hot loop pays nothing for them):
+    out (n_unique, row_bytes) uint8, unique (n_unique,) int64, inverse (n,)
+    int64 or None, outcome (n_unique,) uint8 or None."""
+
+    __slots__ = ("n_unique", "n", "row_bytes", "_out", "_unique", "_inverse", "_outcome")
+
+    def __init__(self, n_unique, n, row_bytes, out, unique, inverse, outcome):
+        self.n_unique, self.n, self.row_bytes = n_unique, n, row_bytes
+        self._out, self._unique, self._inverse, self._outcome = out, unique, inverse, outcome
+
+    @property
+    def out(self):
+        import torch
+        U = self.n_unique
+        return self._out.view(torch.uint8).reshape(-1)[: U * self.row_bytes].view(U, self.row_bytes)
+
+    @property
+    def unique(self):
+        return self._unique[: self.n_unique]
+
+    @property
+    def inverse(self):
+        return None if self._inverse is None else self._inverse[: self.n]
+
+    @property
+    def outcome(self):
+        return None if self._outcome is None else self._outcome[: self.n_unique]
 
 
 class FeatureCache:
@@ -203,16 +230,14 @@ class FeatureCache:
         p = _dev_ptr(ids, torch.int64, "ids") if n else None
         _check(lib().lsmgnn_advance(self._h, p, n, _stream_handle(stream, self.device)), "lsmgnn_advance")
 
-    def gather(self, ids, out=None, unique=None, inverse=True, outcome=False, stream=None) -> GatherResult:
-        """Gather one minibatch.  `out` (uint8, >= n*row_bytes bytes) and
-        `unique` (int64, >= n) may be passed to reuse caller buffers;
-        `inverse`/`outcome` may be True (allocate), a tensor, or False/None."""
+    def _gather_args(self, ids, out, unique, inverse, outcome):
         import torch
         n = ids.numel()
         if out is None:
             out = self._buf("out", n * self.row_bytes, torch.uint8)
         if unique is None:
             unique = self._buf("unique", n, torch.int64)
+
         def pick(arg, name, dtype):
             if isinstance(arg, torch.Tensor):
                 if arg.numel() < n:
@@ -224,18 +249,42 @@ class FeatureCache:
         oc_t = pick(outcome, "outcome", torch.uint8)
         if out.numel() * out.element_size() < n * self.row_bytes or unique.numel() < n:
             raise ValueError("out/unique buffers too small")
+        args = (self._h, _dev_ptr(ids, torch.int64, "ids") if n else None, n,
+                ctypes.c_void_p(out.data_ptr()), _dev_ptr(unique, torch.int64, "unique"),
+                _dev_ptr(inv_t, torch.int64, "inverse") if inv_t is not None else None,
+                _dev_ptr(oc_t, torch.uint8, "outcome") if oc_t is not None else None)
+        return n, out, unique, inv_t, oc_t, args
+
+    def _result(self, U, n, out, unique, inv_t, oc_t):
+        return GatherResult(U, n, self.row_bytes, out, unique, inv_t, oc_t)
+
+    def gather(self, ids, out=None, unique=None, inverse=True, outcome=False, stream=None) -> GatherResult:
+        """Gather one minibatch (returns when everything is complete).  `out`
+        (uint8, >= n*row_bytes bytes) and `unique` (int64, >= n) may be passed
+        to reuse caller buffers; `inverse`/`outcome` may be True (allocate), a
+        tensor, or False/None."""
+        n, out, unique, inv_t, oc_t, args = self._gather_args(ids, out, unique, inverse, outcome)
         nu = ctypes.c_uint64()
-        rc = lib().lsmgnn_gather(
-            self._h, _dev_ptr(ids, torch.int64, "ids") if n else None, n,
-            ctypes.c_void_p(out.data_ptr()), _dev_ptr(unique, torch.int64, "unique"),
-            _dev_ptr(inv_t, torch.int64, "inverse") if inv_t is not None else None,
-            _dev_ptr(oc_t, torch.uint8, "outcome") if oc_t is not None else None,
-            ctypes.byref(nu), _stream_handle(stream, self.device))
-        _check(rc, "lsmgnn_gather")
-        U = nu.value
-        flat = out.view(torch.uint8).reshape(-1)
-        return GatherResult(U, flat[: U * self.row_bytes].view(U, self.row_bytes), unique[:U],
-                            inv_t[:n] if inv_t is not None else None, oc_t[:U] if oc_t is not None else None)
+        _check(lib().lsmgnn_gather(*args, ctypes.byref(nu), _stream_handle(stream, self.device)), "lsmgnn_gather")
+        return self._result(nu.value, n, out, unique, inv_t, oc_t)
+
+    def gather_async(self, ids, out, unique, inverse=None, outcome=None, stream=None):
+        """Pipelined gather: returns (ticket, GatherResult) once the unique
+        count is known.  The buffers must be caller-owned tensors (not reused
+        until wait(ticket) and a synchronisation of the stream)."""
+        n, out, unique, inv_t, oc_t, args = self._gather_args(ids, out, unique, inverse, outcome)
+        nu, tk = ctypes.c_uint64(), ctypes.c_uint64()
+        _check(lib().lsmgnn_gather_async(*args, ctypes.byref(nu), ctypes.byref(tk),
+                                         _stream_handle(stream, self.device)), "lsmgnn_gather_async")
+        return tk.value, self._result(nu.value, n, out, unique, inv_t, oc_t)
+
+    def wait(self, ticket, stream=None):
+        """Make `stream` wait (on the device) for gather `ticket`."""
+        _check(lib().lsmgnn_gather_wait(self._h, int(ticket), _stream_handle(stream, self.device)),
+               "lsmgnn_gather_wait")
+
+    def sync(self):
+        _check(lib().lsmgnn_sync(self._h), "lsmgnn_sync")
 
     def stats(self):
         last, total = Counts(), Counts()

@@ -231,3 +231,77 @@ def test_provenance_hits_from_hbm_misses_from_store():
     assert (r.outcome.cpu().numpy() == lsmgnn.MISS).all()
     assert (r.out.cpu().numpy() == 0xCD).all()
     cache.close()
+
+
+def _run_async_parity(store, static, S, V, L, batches, label):
+    """Pipelined gathers (two in flight) with rotating output buffers; each
+    gather's outputs are compared with the oracle once it has been waited for."""
+    dev = torch.device("cuda", 0)
+    mb = max(1, max(len(b) for b in batches))
+    cache = lsmgnn.FeatureCache(store.num_nodes, store.row_bytes, store.buf, static, S, V, L, mb)
+    orc = Oracle(store.num_nodes, store.row_bytes, static, S, V, L, store=store.np)
+    db = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in batches]
+    bufs = [(torch.empty(mb * store.row_bytes, dtype=torch.uint8, device=dev),
+             torch.empty(mb, dtype=torch.int64, device=dev), torch.empty(mb, dtype=torch.int64, device=dev),
+             torch.empty(mb, dtype=torch.uint8, device=dev)) for _ in range(3)]
+    for j in range(min(L + 1, len(batches))):
+        cache.advance(db[j])
+        orc.advance(batches[j])
+    pending = []
+
+    def check(ticket, r, b):
+        cache.wait(ticket)
+        torch.cuda.current_stream().synchronize()
+        o = orc.gather(np.asarray(batches[b], np.int64))
+        where = f"{label} async gather {b}"
+        assert r.n_unique == o["uniq"].size, where
+        assert np.array_equal(r.unique.cpu().numpy(), o["uniq"]), where
+        assert np.array_equal(r.inverse.cpu().numpy(), o["inv"]), where
+        assert np.array_equal(r.outcome.cpu().numpy(), o["outcome"]), where
+        assert np.array_equal(r.out.cpu().numpy(), o["out"]), where
+        if b + L + 1 < len(batches):
+            orc.advance(batches[b + L + 1])
+
+    for b in range(len(batches)):
+        out, uq, inv, oc = bufs[b % 3]
+        ticket, r = cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc)
+        pending.append((ticket, r, b))
+        if b + L + 1 < len(batches):
+            cache.advance(db[b + L + 1])
+        if len(pending) == 2:
+            check(*pending.pop(0))
+    for p in pending:
+        check(*p)
+    tot_gpu = cache.stats()[1]
+    tot_orc = orc.stats()[1]
+    for k in ("batch", "requests", "unique", "hits", "victim_hits", "misses", "evictions", "enqueued", "dropped"):
+        assert tot_gpu[k] == tot_orc[k], (label, k, tot_gpu[k], tot_orc[k])
+    compare_state(cache, orc, f"{label} async end")
+    cache.close()
+
+
+def test_async_pipeline_rmat14():
+    cfg = W.CONFIGS[1]
+    log(f"case: pipelined gathers, {cfg.name}")
+    wl, batches = config_stream(cfg)
+    store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
+    _run_async_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead, batches,
+                      cfg.name)
+
+
+@pytest.mark.timeout(600)
+def test_async_pipeline_rmat20_first_60():
+    cfg = W.CONFIGS[2]
+    log(f"case: pipelined gathers, {cfg.name}, first 60 minibatches")
+    wl, batches = config_stream(cfg, 60)
+    store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
+    _run_async_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead, batches,
+                      cfg.name)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_async_pipeline_random(seed):
+    n, S, V, L, T, rb, stat, batches, announce = _random_case(100 + seed)
+    log(f"case: pipelined random seed {seed}: N={n} S={S} V={V} L={L}")
+    store = Store.random_bytes(n, rb, seed)
+    _run_async_parity(store, stat, S, V, L, batches, f"async-random{seed}")
