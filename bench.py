@@ -1,11 +1,13 @@
 #!/usr/bin/env python3
 """Benchmark of the per-minibatch feature gather through the MI355X cache.
 
-One step = one pass of the whole hot path over one minibatch: lsmgnn_gather on
-the minibatch's raw request IDs (dedup, set walk with hybrid eviction, victim
-ring, hit/miss/victim-hit row movement, fills) followed by lsmgnn_advance of the
-minibatch L+1 ahead.  All request streams are on the GPU and the feature table
-is in pinned host memory before the timed region starts.
+One step = one pass of the whole hot path over one minibatch: a gather of the
+minibatch's raw request IDs (dedup, set walk with hybrid eviction, victim ring,
+hit/miss/victim-hit row movement, fills) and the announcement of the minibatch
+L+1 ahead.  By default both go through one lsmgnn_gather_async call with two
+minibatches in flight; --sync uses lsmgnn_gather then lsmgnn_advance.  All
+request streams are on the GPU and the feature table is in pinned host memory
+before the timed region starts.
 
 Default workload: R-MAT graph with 2^20 nodes and 2^24 edges (a, b, c, d =
 0.57, 0.19, 0.19, 0.05), fp32 x 256 features (1 GiB pinned host store), GraphSAGE
@@ -172,9 +174,9 @@ def main():
         out, uniq, inv = bufs[b % 3]
         if args.sync:
             r = cache.gather(batches[b], out=out, unique=uniq, inverse=inv)
-        else:
-            tickets[b], r = cache.gather_async(batches[b], out, uniq, inverse=inv)
-        cache.advance(batches[b + L + 1])
+            cache.advance(batches[b + L + 1])
+        else:  # gather minibatch b and announce minibatch b+L+1 in one call
+            tickets[b], r = cache.gather_async(batches[b], out, uniq, inverse=inv, announce=batches[b + L + 1])
         if not args.sync and b - 1 in tickets:
             cache.wait(tickets.pop(b - 1))  # a consumer of minibatch b-1 would run after this
         return r.n_unique
@@ -245,7 +247,8 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
         "config": dict(cfg.describe(), feature_dtype=cfg.feature_dtype, minibatches_timed=args.steps,
                        first_timed_minibatch=args.warmup,
-                       api="lsmgnn_gather" if args.sync else "lsmgnn_gather_async (two minibatches in flight)"),
+                       api=("lsmgnn_gather + lsmgnn_advance" if args.sync
+                            else "lsmgnn_gather_async with announcement (two minibatches in flight)")),
         "rows_per_s": rows / dt,
         "hit_rate": d["hits"] / max(d["unique"], 1),
         "victim_hit_rate": d["victim_hits"] / max(d["unique"], 1),

@@ -132,18 +132,28 @@ lsmgnn_status lsmgnn_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, voi
                             int64_t *unique_ids, int64_t *inverse, uint8_t *outcome,
                             uint64_t *n_unique, void *stream);
 
-/* Pipelined gather, for loops that overlap consecutive minibatches.  Same
-   arguments, semantics and errors as lsmgnn_gather, but it returns as soon as
-   *n_unique is known, with *ticket identifying the gather.  The gather's
-   outputs (out, unique_ids, inverse, outcome) are complete once the caller has
-   called lsmgnn_gather_wait(c, ticket, s) and then synchronised s (or run work
-   on s after it).  Until then the caller must not read, reuse or free those
-   buffers.  The metadata of the next gather runs while this one still moves
-   rows; at most two gathers are in flight and later calls wait for the
-   oldest.  Waits for the work already queued on `stream` before reading ids. */
-lsmgnn_status lsmgnn_gather_async(lsmgnn_cache *c, const int64_t *ids, uint64_t n, void *out,
-                                  int64_t *unique_ids, int64_t *inverse, uint8_t *outcome,
-                                  uint64_t *n_unique, uint64_t *ticket, void *stream);
+/* Pipelined gather, for loops that overlap consecutive minibatches (the
+   sampler running ahead of training, Sec. 4.3.2).  Gathers ids like
+   lsmgnn_gather and then, if next_ids is not NULL, announces the next_n IDs at
+   next_ids (device int64) like lsmgnn_advance: the call is equivalent to that
+   pair of calls, but checks both ID lists with one wait for the dedup result.
+   next_ids == NULL announces nothing (next_n must be 0); an empty minibatch is
+   announced with any non-NULL next_ids and next_n == 0 (nothing is read).
+   Returns as soon as *n_unique is known, with *ticket identifying the gather.
+   The gather's outputs (out, unique_ids, inverse, outcome) are complete once
+   the caller has called lsmgnn_gather_wait(c, ticket, s) and then synchronised
+   s (or run work on s after it).  Until then the caller must not read, reuse
+   or free those buffers, nor change ids or next_ids.  The metadata of the next
+   gather runs while this one still moves rows; at most two gathers are in
+   flight and later calls wait for the oldest.  Waits for the work already
+   queued on `stream` before reading ids.
+   Errors: E_WINDOW if the announcement would be beyond the window once this
+   gather is done (k > t + 1 + L); E_RANGE if an ID of either list is out of
+   range; E_INVAL as for lsmgnn_gather, or if next_n > max_batch.  On any
+   error neither the gather nor the announcement happens. */
+lsmgnn_status lsmgnn_gather_async(lsmgnn_cache *c, const int64_t *ids, uint64_t n, const int64_t *next_ids,
+                                  uint64_t next_n, void *out, int64_t *unique_ids, int64_t *inverse,
+                                  uint8_t *outcome, uint64_t *n_unique, uint64_t *ticket, void *stream);
 
 /* Make `stream` wait (on the device, without blocking the host) until the
    gather `ticket` has completed.  E_INVAL for a ticket never issued. */

@@ -1,9 +1,10 @@
 // gfx950 kernels of the feature-gather cache (LSM-GNN, arXiv 2407.15264).
 //
 // One gather runs as a short pipeline of stream-ordered kernels.  Every count
-// that depends on the batch (unique IDs, touched sets, work-list lengths) stays
-// in device memory, so the host launches the whole pipeline without waiting and
-// synchronises once at the end.  Each kernel reads Counters::err first and does
+// that depends on the batch (unique IDs, touched sets, work-list lengths, the
+// ring tail) stays in device memory, so the host queues the whole pipeline
+// before it learns anything about the batch.  Each kernel reads the error flag
+// first (Counters::err, or the gather's gate in the row copies) and does
 // nothing once an out-of-range ID was seen, so an invalid batch changes no state.
 //
 //   dedup       byte map over node IDs marked with plain stores, per-chunk
@@ -20,8 +21,10 @@
 //               an entry with sequence q is still in the ring at x's turn iff
 //               q + V >= tail0 + (enqueues before x)  (Sec. 4.3.1)
 //   data        row copies with 128-bit loads/stores: hits HBM->out, misses
-//               and victim hits pinned host->out, enqueues HBM->pinned ring,
-//               then fills out->HBM for each way's final occupant
+//               and victim hits pinned host->out (a dense list, small grid),
+//               enqueued rows HBM->staging in ring order (a DMA engine then
+//               writes them to the pinned ring), then fills out->HBM for each
+//               way's final occupant
 #include "internal.h"
 
 namespace lsm {
@@ -80,10 +83,11 @@ static inline unsigned grid_for(uint64_t work, uint64_t per_block, unsigned cap)
 
 // ------------------------------------------------------------------ finish
 // Last kernel of every call: add up the per-block partial counts, publish all
-// counters to pinned host memory and zero the device counters for the next
-// call (they start zeroed at create).
+// counters to pinned host memory, advance the ring tail by the call's enqueues
+// (keeping the previous tail) and zero the device counters for the next call
+// (they start zeroed at create).
 __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host, const uint32_t *part,
-                                                   StatGrids grids) {
+                                                   StatGrids grids, uint64_t *tail) {
   __shared__ uint32_t red[kNumStat][kBlock / 64];
   __shared__ uint32_t sums[kNumStat];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -124,13 +128,17 @@ __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host,
     c.n_host = sums[kStHost];
     c.n_enq_copy = sums[kStEnqCopy];
     *host = c;
+    if (tail && !c.err) {  // a rejected gather leaves both tails alone
+      tail[1] = tail[0];
+      tail[0] += c.enq_total;
+    }
     *cn = Counters{};
   }
 }
 
 void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, const StatGrids &grids,
-                   hipStream_t s) {
-  hipLaunchKernelGGL(k_finish, dim3(1), dim3(kBlock), 0, s, cn, host, stat_part, grids);
+                   uint64_t *tail, hipStream_t s) {
+  hipLaunchKernelGGL(k_finish, dim3(1), dim3(kBlock), 0, s, cn, host, stat_part, grids, tail);
 }
 
 // ------------------------------------------------------------------- dedup
@@ -141,12 +149,15 @@ void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, cons
 //
 // Validate and mark.  Out-of-range IDs set Counters::err; valid ones are still
 // marked, and the compaction kernel then clears the map instead of compacting
-// it, so a rejected batch leaves no trace.  The same kernel clears the window
-// bit of the minibatch being gathered: that list is never consulted again,
-// whether or not this call succeeds.  Only that bit of a node's window word
-// changes in this kernel, so a plain read-modify-write is exact.
-__global__ void k_mark(const int64_t *ids, uint32_t n, uint64_t N, uint8_t *present, const int64_t *clear_ids,
-                       uint32_t clear_n, uint32_t clear_bit, uint32_t *mask, Counters *cn) {
+// it, so a rejected batch leaves no trace.  The list announced with the gather
+// (if any) is validated here too; its bits are set only after the gather has
+// been accepted.  The same kernel clears the window bit of the minibatch being
+// gathered: that list is never consulted again, whether or not this call
+// succeeds.  Only that bit of a node's window word changes in this kernel, so a
+// plain read-modify-write is exact.
+__global__ void k_mark(const int64_t *ids, uint32_t n, const int64_t *ann_ids, uint32_t ann_n, uint64_t N,
+                       uint8_t *present, const int64_t *clear_ids, uint32_t clear_n, uint32_t clear_bit,
+                       uint32_t *mask, Counters *cn) {
   bool bad = false;
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
     const int64_t x = ids[i];
@@ -154,6 +165,10 @@ __global__ void k_mark(const int64_t *ids, uint32_t n, uint64_t N, uint8_t *pres
       bad = true;
     else
       present[x] = 1;
+  }
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ann_n; i += gridDim.x * kBlock) {
+    const int64_t x = ann_ids[i];
+    bad |= x < 0 || (uint64_t)x >= N;
   }
   if (__ballot(bad) && __lane_id() == 0) atomicOr(&cn->err, 1u);
   const uint32_t cb = 1u << clear_bit;
@@ -189,10 +204,13 @@ __global__ __launch_bounds__(kBlock) void k_chunk_popc(const uint8_t *present, u
 }
 
 __global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uint32_t nchunks, Counters *cn,
-                                                       DedupResult *dd) {
+                                                       DedupResult *dd, DedupResult *gate) {
   const uint32_t err = cn->err;
   if (err) {
-    if (threadIdx.x == 0) *dd = DedupResult{err, 0, {0, 0}};
+    if (threadIdx.x == 0) {
+      *gate = DedupResult{err, 0, 0, 0};
+      *dd = DedupResult{err, 0, 0, 0};
+    }
     return;
   }
   uint32_t carry = 0;
@@ -206,7 +224,8 @@ __global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uin
   }
   if (threadIdx.x == 0) {
     cn->n_unique = carry;
-    *dd = DedupResult{0, carry, {0, 0}};
+    *gate = DedupResult{0, carry, 0, 0};
+    *dd = DedupResult{0, carry, 0, 0};
   }
 }
 
@@ -242,14 +261,17 @@ __global__ __launch_bounds__(kBlock) void k_compact(uint8_t *present, const uint
   }
 }
 
-void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, const int64_t *clear_ids, uint64_t clear_n,
-                  uint32_t clear_bit, Scratch &sc, int64_t *unique_out, Counters *cn, DedupResult *dd,
-                  hipStream_t s) {
-  const unsigned g = grid_for(n > clear_n ? n : clear_n, kBlock, kMaxGrid);
-  hipLaunchKernelGGL(k_mark, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, d.N, d.present, clear_ids,
-                     (uint32_t)clear_n, clear_bit, d.mask, cn);
+void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, const int64_t *ann_ids, uint64_t ann_n,
+                  const int64_t *clear_ids, uint64_t clear_n, uint32_t clear_bit, Scratch &sc, int64_t *unique_out,
+                  Counters *cn, DedupResult *dd, hipStream_t s) {
+  uint64_t work = n > clear_n ? n : clear_n;
+  work = work > ann_n ? work : ann_n;
+  const unsigned g = grid_for(work, kBlock, kMaxGrid);
+  hipLaunchKernelGGL(k_mark, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, ann_ids, (uint32_t)ann_n, d.N,
+                     d.present, clear_ids, (uint32_t)clear_n, clear_bit, d.mask, cn);
   hipLaunchKernelGGL(k_chunk_popc, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.present, d.chunk_sums, cn);
-  hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, s, d.chunk_sums, (uint32_t)d.nchunks, cn, dd);
+  hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, s, d.chunk_sums, (uint32_t)d.nchunks, cn, dd,
+                     sc.gate);
   hipLaunchKernelGGL(k_compact, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.present, d.chunk_sums, d.uidx,
                      sc.uniq, unique_out, cn);
 }
@@ -538,10 +560,10 @@ __global__ __launch_bounds__(kBlock) void k_scan_top(uint32_t *part, Counters *c
 // Exclusive scan of the enqueue flags in ascending-ID order gives each
 // enqueue its ring sequence number.  An enqueued line requested later in the
 // same batch is told where its entry went.
-__global__ __launch_bounds__(kBlock) void k_scan_final(const DevState d, Scratch sc, uint64_t tail0,
-                                                       const Counters *cn) {
+__global__ __launch_bounds__(kBlock) void k_scan_final(const DevState d, Scratch sc, const Counters *cn) {
   if (cn->err) return;
   const uint32_t U = cn->n_unique;
+  const uint64_t tail0 = d.tail[0];
   const uint32_t nb = (U + kScanChunk - 1) / kScanChunk;
   for (uint32_t b = blockIdx.x; b < nb; b += gridDim.x) {
     const uint32_t base = b * kScanChunk + threadIdx.x * kScanPerThread;
@@ -573,69 +595,80 @@ __global__ __launch_bounds__(kBlock) void k_scan_final(const DevState d, Scratch
   }
 }
 
-// Victim-ring probe of every fill and the row source of every unique ID.
-__global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc, uint64_t tail0, uint8_t *outcome,
-                                                    Counters *cn) {
+// Victim-ring probe of every fill and the row source of every unique ID; the
+// unique indices whose rows come from pinned host memory form the host-fetch
+// list (in arbitrary order).
+__global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc, uint8_t *outcome, Counters *cn) {
   if (cn->err) return;
   const uint32_t U = cn->n_unique;
+  const uint64_t tail0 = d.tail[0], tail_prev = d.tail[1];
   const uint64_t tail_end = tail0 + cn->enq_total;
   uint32_t c_vhit = 0, c_miss = 0, c_hbm = 0, c_host = 0;
-  for (uint32_t u = blockIdx.x * kBlock + threadIdx.x; u < U; u += gridDim.x * kBlock) {
-    const uint8_t kind = sc.kind[u];
-    uint8_t oc = 0;  // LSMGNN_HIT
-    uint64_t code;
-    if (kind == kKindHit) {
-      code = kSrcHbm | sc.slot[u];
-      ++c_hbm;
-    } else {
-      const uint32_t x = sc.uniq[u];
-      uint64_t q = 0;
-      bool valid = false, same_batch = false;
-      const uint64_t tq = sc.this_q[u];
-      if (tq) {
-        q = tq - 1;
-        valid = true;
-        same_batch = true;
-      } else if (d.V) {
-        const uint64_t vp = d.vpos[x];
-        if (vp) {
-          q = vp - 1;
-          valid = d.ring_tag[q % d.V] == x;
+  for (uint32_t base = blockIdx.x * kBlock; base < U; base += gridDim.x * kBlock) {
+    const uint32_t u = base + threadIdx.x;
+    bool from_host = false;
+    if (u < U) {
+      const uint8_t kind = sc.kind[u];
+      uint8_t oc = 0;  // LSMGNN_HIT
+      uint64_t code;
+      if (kind == kKindHit) {
+        code = kSrcHbm | sc.slot[u];
+        ++c_hbm;
+      } else {
+        const uint32_t x = sc.uniq[u];
+        uint64_t q = 0;
+        bool valid = false, same_batch = false;
+        const uint64_t tq = sc.this_q[u];
+        if (tq) {
+          q = tq - 1;
+          valid = true;
+          same_batch = true;
+        } else if (d.V) {
+          const uint64_t vp = d.vpos[x];
+          if (vp) {
+            q = vp - 1;
+            valid = d.ring_tag[q % d.V] == x;
+          }
         }
-      }
-      const bool live = valid && q + d.V >= tail0 + sc.enq_before[u];
-      if (live) {
-        ++c_vhit;
-        oc = 1;  // LSMGNN_VICTIM_HIT
-        if (same_batch) {
-          // evicted earlier in this batch: its row is still in the cache slot
-          // the evicting fill took, which no copy has overwritten yet
-          const uint32_t e = sc.this_enq[u];
-          code = kSrcHbm | sc.slot[e];
-          sc.dead[e] = 1;
-          ++c_hbm;
-        } else if (q + d.V >= tail_end) {
-          // no enqueue of this batch reuses the slot: read the ring row and
-          // remove the entry now
-          code = kSrcRing | (q % d.V);
-          d.ring_tag[q % d.V] = kEmpty;
-          ++c_host;
+        const bool live = valid && q + d.V >= tail0 + sc.enq_before[u];
+        if (live) {
+          ++c_vhit;
+          oc = 1;  // LSMGNN_VICTIM_HIT
+          if (same_batch) {
+            // evicted earlier in this batch: its row is still in the cache slot
+            // the evicting fill took, which no copy has overwritten yet
+            const uint32_t e = sc.this_enq[u];
+            code = kSrcHbm | sc.slot[e];
+            sc.dead[e] = 1;
+            ++c_hbm;
+          } else if (q + d.V >= tail_end) {
+            // no enqueue of this batch reuses the slot: remove the entry now.
+            // An entry of the previous gather may still be on its way to the
+            // ring (its DMA runs beside this gather), so its row is taken from
+            // the backing store, which holds identical bytes.
+            d.ring_tag[q % d.V] = kEmpty;
+            code = q >= tail_prev ? (kSrcStore | x) : (kSrcRing | (q % d.V));
+            ++c_host;
+          } else {
+            // the slot is rewritten by an enqueue of this batch, which runs
+            // concurrently with the host fetch: take the identical bytes from
+            // the backing store instead
+            code = kSrcStore | x;
+            ++c_host;
+          }
         } else {
-          // the slot is rewritten by an enqueue of this batch, which runs
-          // concurrently with the host fetch: take the identical bytes from
-          // the backing store instead
+          ++c_miss;
+          oc = 2;  // LSMGNN_MISS
           code = kSrcStore | x;
           ++c_host;
         }
-      } else {
-        ++c_miss;
-        oc = 2;  // LSMGNN_MISS
-        code = kSrcStore | x;
-        ++c_host;
       }
+      sc.src[u] = code;
+      from_host = (code & ~kSrcIndex) != kSrcHbm;
+      if (outcome) outcome[u] = oc;
     }
-    sc.src[u] = code;
-    if (outcome) outcome[u] = oc;
+    const uint32_t i = block_append(from_host, &sc.gate->n_host);
+    if (from_host) sc.host_list[i] = u;
   }
   block_count(c_vhit, sc.stat_part, kStVictimHits);
   block_count(c_miss, sc.stat_part, kStMisses);
@@ -644,12 +677,17 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
 }
 
 // Ring bookkeeping for this batch's enqueues; marks the row copies of the
-// entries that are still in the ring at the end of the batch.
-__global__ __launch_bounds__(kBlock) void k_enq_finalize(const DevState d, Scratch sc, uint64_t tail0,
-                                                         Counters *cn) {
+// entries that are still in the ring at the end of the batch.  Those entries
+// have the sequence numbers [q_lo, tail_end), q_lo = tail_end - min(E, V) for E
+// enqueues, and their rows are staged in that order (entries removed again in
+// this batch leave a hole that nothing reads).
+__global__ __launch_bounds__(kBlock) void k_enq_finalize(const DevState d, Scratch sc, Counters *cn) {
   if (cn->err) return;
   const uint32_t U = cn->n_unique;
-  const uint64_t tail_end = tail0 + cn->enq_total;
+  const uint64_t tail0 = d.tail[0];
+  const uint64_t E = cn->enq_total;
+  const uint64_t tail_end = tail0 + E;
+  const uint64_t q_lo = tail_end - (E < d.V ? E : d.V);
   uint32_t c_copy = 0;
   for (uint32_t u = blockIdx.x * kBlock + threadIdx.x; u < U; u += gridDim.x * kBlock) {
     uint64_t dst = 0;
@@ -662,7 +700,7 @@ __global__ __launch_bounds__(kBlock) void k_enq_finalize(const DevState d, Scrat
           d.ring_tag[q % d.V] = kEmpty;
         } else {
           d.ring_tag[q % d.V] = z;
-          dst = (q % d.V) + 1;
+          dst = (q - q_lo) + 1;
           ++c_copy;
         }
       }
@@ -672,19 +710,19 @@ __global__ __launch_bounds__(kBlock) void k_enq_finalize(const DevState d, Scrat
   block_count(c_copy, sc.stat_part, kStEnqCopy);
 }
 
-void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t tail0, Scratch &sc, uint8_t *outcome,
-                         Counters *cn, StatGrids &grids, hipStream_t s) {
+void launch_ring_resolve(const DevState &d, uint64_t n, Scratch &sc, uint8_t *outcome, Counters *cn,
+                         StatGrids &grids, hipStream_t s) {
   const unsigned g = grid_for(n, kBlock, kMaxGrid);
   const unsigned gs = grid_for(n, kScanChunk, kMaxGrid);
   if (d.V) {
     hipLaunchKernelGGL(k_scan_partial, dim3(gs), dim3(kBlock), 0, s, sc.flags, sc.scan_part, cn);
     hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kBlock), 0, s, sc.scan_part, cn);
-    hipLaunchKernelGGL(k_scan_final, dim3(gs), dim3(kBlock), 0, s, d, sc, tail0, cn);
+    hipLaunchKernelGGL(k_scan_final, dim3(gs), dim3(kBlock), 0, s, d, sc, cn);
   }
-  hipLaunchKernelGGL(k_resolve, dim3(g), dim3(kBlock), 0, s, d, sc, tail0, outcome, cn);
+  hipLaunchKernelGGL(k_resolve, dim3(g), dim3(kBlock), 0, s, d, sc, outcome, cn);
   for (int st = kStVictimHits; st <= kStHost; ++st) grids.g[st] = g;
   if (d.V) {
-    hipLaunchKernelGGL(k_enq_finalize, dim3(g), dim3(kBlock), 0, s, d, sc, tail0, cn);
+    hipLaunchKernelGGL(k_enq_finalize, dim3(g), dim3(kBlock), 0, s, d, sc, cn);
     grids.g[kStEnqCopy] = g;
   }
 }
@@ -693,7 +731,9 @@ void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t tail0, Scratch 
 // Work item w = (unique index e, 16-byte vector v): consecutive lanes take
 // consecutive vectors of one row, so a wave moves whole rows with 128-bit
 // accesses, and each lane keeps kUnroll vectors in flight before storing.
-// Each mode reads the per-unique descriptor and skips rows it does not own.
+// The HBM-side modes read the per-unique descriptor and skip rows they do not
+// own; the host fetch walks the dense host-fetch list instead.  Counts come
+// from the gather's gate; a rejected gather moves nothing.
 constexpr int kUnroll = 4;
 
 template <CopyMode M>
@@ -705,17 +745,11 @@ __device__ __forceinline__ bool row_ends(const DevState &d, const Scratch &sc, u
     if ((code & ~kSrcIndex) != kSrcHbm) return false;
     src = d.rows + (code & kSrcIndex) * R;
     dst = out + (uint64_t)e * R;
-  } else if constexpr (M == CopyMode::kHostToOut) {
-    const uint64_t code = sc.src[e];
-    const uint64_t place = code & ~kSrcIndex;
-    if (place == kSrcHbm) return false;
-    src = (place == kSrcRing ? d.ring_rows : d.store) + (code & kSrcIndex) * R;
-    dst = out + (uint64_t)e * R;
-  } else if constexpr (M == CopyMode::kCacheToRing) {
+  } else if constexpr (M == CopyMode::kCacheToStage) {
     const uint64_t rd = sc.ring_dst[e];
     if (!rd) return false;
     src = d.rows + (uint64_t)sc.slot[e] * R;
-    dst = d.ring_rows + (rd - 1) * R;
+    dst = sc.staging + (rd - 1) * R;
   } else {
     const uint32_t fd = sc.fill_dst[e];
     if (!fd) return false;
@@ -726,9 +760,11 @@ __device__ __forceinline__ bool row_ends(const DevState &d, const Scratch &sc, u
 }
 
 template <CopyMode M, bool kPow2>
-__global__ __launch_bounds__(kBlock) void k_copy(const DevState d, Scratch sc, uint8_t *out, uint32_t n_unique,
-                                                 uint32_t nvec, uint32_t vshift) {
-  const uint64_t total = (uint64_t)n_unique * nvec;
+__global__ __launch_bounds__(kBlock) void k_copy(const DevState d, Scratch sc, uint8_t *out, uint32_t nvec,
+                                                 uint32_t vshift) {
+  const DedupResult g = *sc.gate;
+  if (g.err) return;
+  const uint64_t total = (uint64_t)g.n_unique * nvec;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
   for (uint64_t w0 = (uint64_t)blockIdx.x * kBlock + threadIdx.x; w0 < total; w0 += stride * kUnroll) {
     u32x4 v[kUnroll];
@@ -754,41 +790,76 @@ __global__ __launch_bounds__(kBlock) void k_copy(const DevState d, Scratch sc, u
   }
 }
 
-// Grid caps.  The host-link kernels need only a few hundred KB in flight to
-// cover PCIe latency; small grids leave wave slots for the kernels that run
-// beside them (hit copy, enqueue copy).
+// Host fetch: item w = (host-list entry i, 16-byte vector v).  The list entry
+// and its source code are the same for all lanes of a row (broadcast loads).
+template <bool kPow2>
+__global__ __launch_bounds__(kBlock) void k_host_fetch(const DevState d, Scratch sc, uint8_t *out, uint32_t nvec,
+                                                       uint32_t vshift) {
+  const DedupResult g = *sc.gate;
+  if (g.err) return;
+  const uint64_t R = d.R;
+  const uint64_t total = (uint64_t)g.n_host * nvec;
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  for (uint64_t w0 = (uint64_t)blockIdx.x * kBlock + threadIdx.x; w0 < total; w0 += stride * kUnroll) {
+    u32x4 v[kUnroll];
+    uint8_t *dst[kUnroll];
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      const uint64_t w = w0 + k * stride;
+      dst[k] = nullptr;
+      if (w < total) {
+        const uint32_t i = kPow2 ? (uint32_t)(w >> vshift) : (uint32_t)(w / nvec);
+        const uint64_t byte = (w - (uint64_t)i * nvec) * 16u;
+        const uint32_t e = sc.host_list[i];
+        const uint64_t code = sc.src[e];
+        const uint8_t *src = ((code & ~kSrcIndex) == kSrcRing ? d.ring_rows : d.store) + (code & kSrcIndex) * R;
+        v[k] = *reinterpret_cast<const u32x4 *>(src + byte);
+        dst[k] = out + (uint64_t)e * R + byte;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k)
+      if (dst[k]) *reinterpret_cast<u32x4 *>(dst[k]) = v[k];
+  }
+}
+
+// Grid caps.  Every outstanding host-link read queues in front of the memory
+// requests of the kernels that run beside it (the next gather's metadata, the
+// hit copy, the fills), so the host fetch keeps only a few hundred KB in
+// flight: enough to cover the link's latency, not more.
 #ifndef LSM_HOST_GRID
-#define LSM_HOST_GRID 256
-#endif
-#ifndef LSM_ENQ_GRID
-#define LSM_ENQ_GRID 256
+#define LSM_HOST_GRID 32
 #endif
 #ifndef LSM_HBM_GRID
 #define LSM_HBM_GRID 2048
 #endif
 
 template <CopyMode M>
-static void launch_copy_mode(const DevState &d, uint32_t n_unique, const Scratch &sc, uint8_t *out,
-                             hipStream_t s) {
+static void launch_copy_mode(const DevState &d, uint64_t n, const Scratch &sc, uint8_t *out, hipStream_t s) {
   const uint32_t nvec = (uint32_t)(d.R / 16);
   const bool pow2 = (nvec & (nvec - 1)) == 0;
   const uint32_t vshift = pow2 ? (uint32_t)__builtin_ctz(nvec) : 0u;
-  const unsigned cap = M == CopyMode::kHostToOut ? LSM_HOST_GRID
-                       : M == CopyMode::kCacheToRing ? LSM_ENQ_GRID : LSM_HBM_GRID;
-  const unsigned g = grid_for((uint64_t)n_unique * nvec, (uint64_t)kBlock * kUnroll, cap);
+  if constexpr (M == CopyMode::kHostToOut) {
+    const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kUnroll, LSM_HOST_GRID);
+    if (pow2)
+      hipLaunchKernelGGL((k_host_fetch<true>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift);
+    else
+      hipLaunchKernelGGL((k_host_fetch<false>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift);
+    return;
+  }
+  const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kUnroll, LSM_HBM_GRID);
   if (pow2)
-    hipLaunchKernelGGL((k_copy<M, true>), dim3(g), dim3(kBlock), 0, s, d, sc, out, n_unique, nvec, vshift);
+    hipLaunchKernelGGL((k_copy<M, true>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift);
   else
-    hipLaunchKernelGGL((k_copy<M, false>), dim3(g), dim3(kBlock), 0, s, d, sc, out, n_unique, nvec, vshift);
+    hipLaunchKernelGGL((k_copy<M, false>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift);
 }
 
-void launch_copy(CopyMode mode, const DevState &d, uint32_t n_unique, const Scratch &sc, uint8_t *out,
-                 hipStream_t s) {
+void launch_copy(CopyMode mode, const DevState &d, uint64_t n, const Scratch &sc, uint8_t *out, hipStream_t s) {
   switch (mode) {
-    case CopyMode::kHbmToOut: launch_copy_mode<CopyMode::kHbmToOut>(d, n_unique, sc, out, s); break;
-    case CopyMode::kHostToOut: launch_copy_mode<CopyMode::kHostToOut>(d, n_unique, sc, out, s); break;
-    case CopyMode::kCacheToRing: launch_copy_mode<CopyMode::kCacheToRing>(d, n_unique, sc, out, s); break;
-    case CopyMode::kOutToCache: launch_copy_mode<CopyMode::kOutToCache>(d, n_unique, sc, out, s); break;
+    case CopyMode::kHbmToOut: launch_copy_mode<CopyMode::kHbmToOut>(d, n, sc, out, s); break;
+    case CopyMode::kHostToOut: launch_copy_mode<CopyMode::kHostToOut>(d, n, sc, out, s); break;
+    case CopyMode::kCacheToStage: launch_copy_mode<CopyMode::kCacheToStage>(d, n, sc, out, s); break;
+    case CopyMode::kOutToCache: launch_copy_mode<CopyMode::kOutToCache>(d, n, sc, out, s); break;
   }
 }
 
@@ -841,11 +912,10 @@ __global__ void k_window_set(const int64_t *ids, uint32_t n, uint64_t N, uint32_
   if (__ballot(bad) && __lane_id() == 0) atomicOr(&cn->err, 1u);
 }
 
-// After a rejected announcement: clear the bit again (it was clear before,
-// since the minibatch that last used this bit position has been gathered).
-__global__ void k_window_rollback(const int64_t *ids, uint32_t n, uint64_t N, uint32_t bit, uint32_t *mask,
-                                  const Counters *cn) {
-  if (!cn->err) return;
+// After a rejected announcement (the host launches it only then): clear the
+// bit again (it was clear before, since the minibatch that last used this bit
+// position has been gathered).
+__global__ void k_window_rollback(const int64_t *ids, uint32_t n, uint64_t N, uint32_t bit, uint32_t *mask) {
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
     const int64_t x = ids[i];
     if (x >= 0 && (uint64_t)x < N) {
@@ -860,7 +930,34 @@ void launch_window_set(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit,
   const unsigned g = grid_for(n, kBlock, kMaxGrid);
   hipLaunchKernelGGL(k_window_set, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, N, bit, mask, slot_ids,
                      record ? 1 : 0, cn);
-  if (record) hipLaunchKernelGGL(k_window_rollback, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, N, bit, mask, cn);
+}
+
+void launch_window_rollback(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask,
+                            hipStream_t s) {
+  const unsigned g = grid_for(n, kBlock, kMaxGrid);
+  hipLaunchKernelGGL(k_window_rollback, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, N, bit, mask);
+}
+
+// Announcement made together with a gather: the gather's mark kernel has
+// validated the IDs, and its gate says whether the call was accepted.  Records
+// the list in its window slot and sets the minibatch's bit for every ID (only
+// that bit changes in this kernel, so a plain read-modify-write is exact).
+__global__ void k_announce(const int64_t *ids, uint32_t n, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
+                           const DedupResult *gate) {
+  if (gate->err) return;
+  const uint32_t b = 1u << bit;
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
+    const int64_t x = ids[i];
+    slot_ids[i] = x;
+    const uint32_t m = mask[x];
+    if (!(m & b)) mask[x] = m | b;
+  }
+}
+
+void launch_announce(const int64_t *ids, uint64_t n, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
+                     const Scratch &sc, hipStream_t s) {
+  const unsigned g = grid_for(n, kBlock, kMaxGrid);
+  hipLaunchKernelGGL(k_announce, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, bit, mask, slot_ids, sc.gate);
 }
 
 }  // namespace lsm

@@ -65,18 +65,22 @@ struct Counters {
   uint32_t pad[16];
 };
 
-// Dedup result of a gather, written to pinned host memory by the chunk scan:
-// the host waits for it before it launches the rest of the gather.
+// Dedup result of a gather, written by the chunk scan twice: to pinned host
+// memory (the host reads the unique count and the error flag from it) and to a
+// per-gather device gate that the row copies read (they run on other streams
+// after the metadata kernels have reset the call counters).  In the gate,
+// n_host counts the entries of the host-fetch list.
 struct DedupResult {
   uint32_t err;
   uint32_t n_unique;
-  uint32_t pad[2];
+  uint32_t n_host;
+  uint32_t pad;
 };
 
 // Per-call scratch, every array sized for max_batch entries unless noted.
-// slot, src, ring_dst and fill_dst are read by the row copies of a gather while
-// the next gather's metadata kernels run, so the runtime keeps two of them and
-// alternates by gather parity.
+// slot, src, ring_dst, fill_dst, host_list, staging and gate are read by the
+// row copies of a gather while the next gather's metadata kernels run, so the
+// runtime keeps two of them and alternates by gather parity.
 struct Scratch {
   uint32_t *uniq;       // ascending unique IDs
   uint32_t *uset;       // set of uniq[u]
@@ -97,9 +101,12 @@ struct Scratch {
   uint64_t *this_q;     // 1 + ring sequence of u's own enqueue in this batch, or 0
   uint32_t *this_enq;   // the unique index that enqueued u in this batch
   uint64_t *src;        // row source of out row u (kSrc* code)
-  uint64_t *ring_dst;   // 1 + ring slot that receives the row u evicted, or 0
+  uint64_t *ring_dst;   // 1 + staging row that receives the row u evicted, or 0
   uint32_t *fill_dst;   // 1 + cache slot that out row u refills (the way's final fill), or 0
   uint32_t *stat_part;  // [kNumStat][kMaxGrid] per-block partial counts
+  DedupResult *gate;    // [1] unique count, error flag and host-list length of the gather
+  uint32_t *host_list;  // unique indices whose rows come from pinned host memory
+  uint8_t *staging;     // [min(max_batch, V)][R] evicted rows in ring order, for the DMA engine
 };
 
 struct DevState {
@@ -117,29 +124,37 @@ struct DevState {
   uint32_t *set_idx;     // [S]
   uint32_t *uidx;        // [N] unique index of the node in the current batch
                          //     (meaningful only where uniq[uidx[x]] == x)
+  uint64_t *tail;        // [2] ring entries ever enqueued (the FIFO tail), and
+                         //     the tail before the last gather's enqueues
   uint64_t N, R, S, V;
   uint64_t nchunks;
   uint32_t L, T;
 };
 
-enum class CopyMode { kHbmToOut, kHostToOut, kCacheToRing, kOutToCache };
+enum class CopyMode { kHbmToOut, kHostToOut, kCacheToStage, kOutToCache };
 
 // ----- launchers (gather_kernels.hip) -----
 void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, const StatGrids &grids,
-                   hipStream_t s);
-void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, const int64_t *clear_ids, uint64_t clear_n,
-                  uint32_t clear_bit, Scratch &sc, int64_t *unique_out, Counters *cn, DedupResult *dd,
-                  hipStream_t s);
+                   uint64_t *tail, hipStream_t s);
+// ann_ids/ann_n: the list announced with this gather (validated here), or NULL/0
+void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, const int64_t *ann_ids, uint64_t ann_n,
+                  const int64_t *clear_ids, uint64_t clear_n, uint32_t clear_bit, Scratch &sc, int64_t *unique_out,
+                  Counters *cn, DedupResult *dd, hipStream_t s);
 void launch_group_by_set(const DevState &d, const int64_t *ids, uint64_t n, int64_t *inverse, Scratch &sc,
                          Counters *cn, hipStream_t s);
 void launch_set_walk(const DevState &d, uint64_t n, uint32_t t, Scratch &sc, Counters *cn, StatGrids &grids,
                      hipStream_t s);
-void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t tail0, Scratch &sc, uint8_t *outcome,
-                         Counters *cn, StatGrids &grids, hipStream_t s);
-void launch_copy(CopyMode mode, const DevState &d, uint32_t n_unique, const Scratch &sc, uint8_t *out,
-                 hipStream_t s);
+void launch_ring_resolve(const DevState &d, uint64_t n, Scratch &sc, uint8_t *outcome, Counters *cn,
+                         StatGrids &grids, hipStream_t s);
+// n bounds the gather's unique count (the copies read the exact one from the gate)
+void launch_copy(CopyMode mode, const DevState &d, uint64_t n, const Scratch &sc, uint8_t *out, hipStream_t s);
 void launch_window_set(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
                        bool record, Counters *cn, hipStream_t s);
+void launch_window_rollback(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask,
+                            hipStream_t s);
+// sets the announced bits unless the gather's gate holds an error
+void launch_announce(const int64_t *ids, uint64_t n, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
+                     const Scratch &sc, hipStream_t s);
 void launch_copy_plain(const void *src, void *dst, uint64_t bytes, hipStream_t s);
 
 // host twin of the device set-index function

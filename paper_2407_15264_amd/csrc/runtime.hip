@@ -4,20 +4,37 @@
 // pinned victim ring), validates arguments before anything changes, and
 // launches the gfx950 kernels of gather_kernels.hip.
 //
-// Streams.  A gather runs on three internal streams, all at default priority:
-//   meta  - dedup, set grouping, set walk, ring resolution, counters
-//   host  - the host fetch (misses and victim hits, PCIe ingress)
-//   data  - the enqueue copy (PCIe egress), the hit copy, the fills
+// Streams.  A gather runs on three internal streams, all at default priority
+// (three, so that with the caller's stream each gets its own hardware queue
+// under HIP's default of four per process; streams that share a queue run in
+// order with each other):
+//   meta  - dedup, set grouping, set walk, ring resolution, counters, then
+//           staging of the enqueued rows and the hit copy
+//   host  - the host fetch (misses and victim hits, PCIe ingress), then the
+//           fills
+//   dma   - the staged rows to the pinned victim ring on a DMA engine (PCIe
+//           egress without compute units: a copy kernel's host-link writes
+//           would stall the memory requests of the kernels beside it)
+// The host queues all of a gather's kernels at once (every batch-dependent
+// size, and the ring tail, stay in device memory) and then waits only for the
+// dedup result, to report the unique count or reject the batch; a rejected
+// batch's kernels are already queued and do nothing.  A DMA copy needs its
+// size on the host, so gather t's ring write is queued once its counters are
+// known: by the next call's dedup wait, or by any call that synchronises.
 // The metadata of gather t+1 depends only on the metadata of gather t, so it
-// can run while gather t still moves rows.  The data kernels of a gather read
-// four per-unique arrays (slot, src, ring_dst, fill_dst) that its metadata
-// wrote; two copies of them alternate by gather parity, so gather t's
-// metadata first waits for gather t-2's data.  Other cross-gather hazards:
-//   - ring rows: gather t's host fetch waits for gather t-1's enqueue copy;
-//     gather t's enqueue copy follows gather t-1's fill on the data stream,
-//     and that fill waited for gather t-1's host fetch;
-//   - cache rows: gather t's hit and enqueue copies follow gather t-1's fill
-//     on the same stream.
+// runs while gather t's host fetch moves rows.  The data kernels of a gather
+// read per-unique arrays (slot, src, ring_dst, fill_dst, host_list), the gate
+// and the staging rows that its metadata wrote; two copies of them alternate
+// by gather parity, so gather t's metadata first waits for gather t-2's fills,
+// and its staging for gather t-2's DMA.  Other cross-gather hazards:
+//   - cache rows: gather t's staging and hit copy wait for gather t-1's fills;
+//     gather t's fills wait for its staging and hit copy;
+//   - ring rows: gather t reads ring rows only of entries enqueued by gathers
+//     up to t-2 (entries of gather t-1 are read from the backing store), so
+//     its host fetch waits for gather t-2's DMA; gather t's DMA overwrites
+//     slots that gather t-1's host fetch may read, and it waits for gather
+//     t's staging, which waited for gather t-1's fills, which follow gather
+//     t-1's host fetch on the host stream.
 // Every call first makes the meta stream wait for the work already queued on
 // the caller's stream (the IDs and the output buffers).
 #include <hip/hip_runtime.h>
@@ -59,14 +76,28 @@ struct Flight {
   Scratch sc{};                // metadata scratch (shared) + this parity's per-unique arrays
   Counters *hc = nullptr;      // pinned: counters published by the gather's last metadata kernel
   Counters *hc_dev = nullptr;
-  hipEvent_t meta_done = nullptr, finish_done = nullptr, enq_done = nullptr, host_done = nullptr,
-             data_done = nullptr;
-  hipEvent_t pe[kNumEv] = {};  // profiling
+  hipEvent_t meta_done = nullptr, finish_done = nullptr, stage_done = nullptr, data_done = nullptr,
+             dma_done = nullptr;
   bool used = false;           // events of this slot have been recorded at least once
   bool stats_pending = false;  // counters not yet added to the totals
-  bool prof_pending = false;   // profiling events not yet read
-  bool ring = false;
+  bool dma_pending = false;    // staged rows not yet queued for the ring
+  bool dma_used = false;       // dma_done has been recorded at least once
   uint64_t t = 0, requests = 0;
+  uint64_t enq_total = 0, tail_end = 0;  // enqueues of the gather, ring tail after it
+};
+
+// Timing events of one gather.  Four sets rotate by gather index: when gather
+// t is queued, gather t-4's events are complete (gather t-2's dedup, already
+// waited for, ran after gather t-4's rows had moved), so reading them never
+// blocks.
+constexpr int kPerfSets = 4;
+struct PerfSet {
+  hipEvent_t e[kNumEv] = {};
+  bool pending = false;  // events recorded for gather t and not yet read
+  bool counted = false;  // row counts of gather t copied in
+  bool ring = false;     // the ring write was timed
+  uint64_t t = 0, requests = 0;
+  uint32_t n_hbm = 0, n_host = 0, n_enq = 0, n_fill = 0;
 };
 
 }  // namespace
@@ -83,7 +114,9 @@ struct lsmgnn_cache {
   Counters *hc_adv = nullptr, *hc_adv_dev = nullptr;
   DedupResult *dd = nullptr, *dd_dev = nullptr;
   Flight fl[2];
-  hipStream_t meta = nullptr, host = nullptr, data = nullptr;
+  PerfSet ps[kPerfSets];
+  hipStream_t meta = nullptr, host = nullptr, dma = nullptr;
+  uint8_t *ring_host = nullptr;  // pinned victim ring rows, host address
   hipEvent_t ev_in = nullptr, ev_dedup = nullptr, ev_adv = nullptr;
   uint64_t t = 0;  // gathers issued
   uint64_t n_adv = 0, tail = 0;
@@ -102,15 +135,15 @@ void release(lsmgnn_cache *c) {
   c->dev_allocs.clear();
   for (void *p : c->host_allocs) (void)hipHostFree(p);
   c->host_allocs.clear();
-  for (Flight &f : c->fl) {
-    for (hipEvent_t e : {f.meta_done, f.finish_done, f.enq_done, f.host_done, f.data_done})
+  for (Flight &f : c->fl)
+    for (hipEvent_t e : {f.meta_done, f.finish_done, f.stage_done, f.data_done, f.dma_done})
       if (e) (void)hipEventDestroy(e);
-    for (hipEvent_t e : f.pe)
+  for (PerfSet &p : c->ps)
+    for (hipEvent_t e : p.e)
       if (e) (void)hipEventDestroy(e);
-  }
   for (hipEvent_t e : {c->ev_in, c->ev_dedup, c->ev_adv})
     if (e) (void)hipEventDestroy(e);
-  for (hipStream_t s : {c->meta, c->host, c->data})
+  for (hipStream_t s : {c->meta, c->host, c->dma})
     if (s) (void)hipStreamDestroy(s);
 }
 
@@ -177,62 +210,120 @@ void harvest_stats(lsmgnn_cache *c, Flight &f) {
   c->total.enqueued += st.enqueued;
   c->total.dropped += st.dropped;
   c->tail += h.enq_total;
+  f.enq_total = h.enq_total;
+  f.tail_end = c->tail;
+  f.dma_pending = c->d.V > 0 && h.enq_total > 0;
+  PerfSet &p = c->ps[f.t % kPerfSets];
+  if (p.pending && p.t == f.t) {
+    p.n_hbm = h.n_hbm;
+    p.n_host = h.n_host;
+    p.n_enq = h.n_enq_copy;
+    p.n_fill = h.n_fill;
+    p.counted = true;
+  }
   f.stats_pending = false;
 }
 
-// Read a finished gather's kernel timings (its rows must have moved).
-void harvest_profile(lsmgnn_cache *c, Flight &f) {
-  if (!f.prof_pending) return;
+// Queue a harvested gather's ring write: its E enqueues have the sequence
+// numbers [tail_end - E, tail_end), of which the last min(E, V) survive; they
+// were staged in that order and land in at most two contiguous ring pieces.
+void issue_dma(lsmgnn_cache *c, Flight &f) {
+  if (!f.dma_pending) return;
+  f.dma_pending = false;
+  const uint64_t V = c->d.V, R = c->d.R;
+  const uint64_t rows = f.enq_total < V ? f.enq_total : V;
+  const uint64_t p0 = (f.tail_end - rows) % V;
+  const uint64_t first = rows < V - p0 ? rows : V - p0;
+  PerfSet &p = c->ps[f.t % kPerfSets];
+  const bool prof = p.pending && p.t == f.t;
+  (void)hipStreamWaitEvent(c->dma, f.stage_done, 0);
+  if (prof) (void)hipEventRecord(p.e[kEvEnq0], c->dma);
+  (void)hipMemcpyAsync(c->ring_host + p0 * R, f.sc.staging, first * R, hipMemcpyDeviceToHost, c->dma);
+  if (rows > first)
+    (void)hipMemcpyAsync(c->ring_host, f.sc.staging + first * R, (rows - first) * R, hipMemcpyDeviceToHost, c->dma);
+  if (prof) {
+    (void)hipEventRecord(p.e[kEvEnq1], c->dma);
+    p.ring = true;
+  }
+  (void)hipEventRecord(f.dma_done, c->dma);
+  f.dma_used = true;
+}
+
+// Read a finished gather's kernel timings (its rows must have moved and its
+// counters must have been harvested).
+void harvest_profile(lsmgnn_cache *c, PerfSet &p) {
+  if (!p.pending || !p.counted) return;
   auto el = [&](int a, int b) {
     float v = 0;
-    return hipEventElapsedTime(&v, f.pe[a], f.pe[b]) == hipSuccess ? (double)v : 0.0;
+    return hipEventElapsedTime(&v, p.e[a], p.e[b]) == hipSuccess ? (double)v : 0.0;
   };
-  const Counters &h = *f.hc;
+  if (p.ring) (void)hipEventSynchronize(p.e[kEvEnq1]);  // queued three gathers ago: long done
   c->acc.gather_ms += el(kEvAll0, kEvAll1);
   c->acc.gathers += 1;
-  if (f.requests) {
+  if (p.requests) {
     c->acc.hbm_copy_ms += el(kEvHbm0, kEvHbm1);
     c->acc.hbm_copy_launches += 1;
-    c->acc.hbm_copy_rows += h.n_hbm;
-    if (f.ring) {
+    c->acc.hbm_copy_rows += p.n_hbm;
+    if (p.ring) {
       c->acc.enqueue_ms += el(kEvEnq0, kEvEnq1);
       c->acc.enqueue_launches += 1;
-      c->acc.enqueue_rows += h.n_enq_copy;
+      c->acc.enqueue_rows += p.n_enq;
     }
     c->acc.host_fetch_ms += el(kEvHost0, kEvHost1);
     c->acc.host_fetch_launches += 1;
-    c->acc.host_fetch_rows += h.n_host;
+    c->acc.host_fetch_rows += p.n_host;
     c->acc.fill_ms += el(kEvFill0, kEvFill1);
     c->acc.fill_launches += 1;
-    c->acc.fill_rows += h.n_fill;
+    c->acc.fill_rows += p.n_fill;
   }
   (void)hipGetLastError();
-  f.prof_pending = false;
+  p.pending = false;
 }
 
-// Wait for every queued kernel, then account everything in issue order.
+// Wait for every queued kernel and copy, then account everything in issue
+// order.
 lsmgnn_status sync_all(lsmgnn_cache *c) {
-  for (hipStream_t s : {c->meta, c->host, c->data})
-    if (hipStreamSynchronize(s) != hipSuccess) return fail_device(c);
+  if (hipStreamSynchronize(c->meta) != hipSuccess) return fail_device(c);
   Flight &older = c->fl[c->t & 1], &newer = c->fl[(c->t + 1) & 1];
   harvest_stats(c, older);
+  issue_dma(c, older);
   harvest_stats(c, newer);
-  harvest_profile(c, older);
-  harvest_profile(c, newer);
+  issue_dma(c, newer);
+  if (hipGetLastError() != hipSuccess) return fail_device(c);
+  for (hipStream_t s : {c->host, c->dma})
+    if (hipStreamSynchronize(s) != hipSuccess) return fail_device(c);
+  for (uint64_t k = kPerfSets; k > 0; --k) harvest_profile(c, c->ps[(c->t + k) % kPerfSets]);
   return LSMGNN_OK;
 }
 
-// Queue one gather.  Returns once its unique count is known; its row movement
-// may still be running on the host and data streams.
-lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t *unique_ids,
-                           int64_t *inverse, uint8_t *outcome, uint64_t *n_unique, hipStream_t s, Flight **used) {
+// The announcement made together with a gather, if any.
+struct Announce {
+  bool on = false;
+  const int64_t *ids = nullptr;
+  uint64_t n = 0;
+};
+
+// Queue one gather (and the announcement after it).  Returns once its unique
+// count is known; its metadata and row movement may still be running on the
+// three streams.  *issued receives the gather index.
+lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, const Announce &an, void *out,
+                           int64_t *unique_ids, int64_t *inverse, uint8_t *outcome, uint64_t *n_unique,
+                           hipStream_t s, uint64_t *issued) {
   DevState &d = c->d;
   const uint64_t t = c->t;
+  // the announcement is the k-th, made once t+1 gathers are done
+  const uint64_t k = c->n_adv;
+  if (an.on && k > t + 1 + d.L) return LSMGNN_E_WINDOW;
+  const bool record = an.on && k > t + 1 && d.L > 0 && an.n > 0;  // lists for k <= t+1 are never consulted
+  const int kslot = (int)(k % (d.L + 1));
   Flight &f = c->fl[t & 1];
   Flight &pf = c->fl[(t + 1) & 1];  // gather t-1
+  PerfSet &ps = c->ps[t % kPerfSets];
+  harvest_profile(c, ps);  // gather t-4's events are complete
+  issue_dma(c, f);         // gather t-2's ring write (normally queued by gather t-1's call)
   const bool prof = c->prof != 0;
   auto rec = [&](int e, hipStream_t st) {
-    if (prof) (void)hipEventRecord(f.pe[e], st);
+    if (prof) (void)hipEventRecord(ps.e[e], st);
   };
   uint8_t *outp = static_cast<uint8_t *>(out);
 
@@ -250,72 +341,82 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, void
   const uint64_t clear_n = clear ? c->win_len[slot] : 0;
 
   rec(kEvAll0, c->meta);
-  const bool dedup = n || clear_n;
+  const uint64_t ann_n = an.on ? an.n : 0;
+  const bool dedup = n || clear_n || ann_n;
   if (dedup)
-    lsm::launch_dedup(d, ids, n, clear_ids, clear_n, (uint32_t)(t & 31u), f.sc, unique_ids, c->cn, c->dd_dev,
-                      c->meta);
-  if (hipEventRecord(c->ev_dedup, c->meta) != hipSuccess || hipGetLastError() != hipSuccess ||
-      hipEventSynchronize(c->ev_dedup) != hipSuccess)
-    return fail_device(c);
-  // the meta stream is in order: gather t-1's counters are published, and
-  // gather t-2's rows have moved
-  harvest_stats(c, pf);
-  harvest_profile(c, f);
-  const uint32_t err = dedup ? c->dd->err : 0u;
-  const uint32_t U = dedup ? c->dd->n_unique : 0u;
-  if (err) {
-    // rejected: the marks are already undone; re-zero the counters (the
-    // announcement mirror receives them and nobody reads it now)
-    lsm::launch_finish(c->cn, c->hc_adv_dev, f.sc.stat_part, lsm::StatGrids{}, c->meta);
-    if (hipGetLastError() != hipSuccess || hipStreamSynchronize(c->meta) != hipSuccess) return fail_device(c);
-    return LSMGNN_E_RANGE;
-  }
-
-  f.used = true;
-  f.t = t;
-  f.requests = n;
-  f.ring = d.V > 0;
+    lsm::launch_dedup(d, ids, n, ann_n ? an.ids : nullptr, ann_n, clear_ids, clear_n, (uint32_t)(t & 31u), f.sc,
+                      unique_ids, c->cn, c->dd_dev, c->meta);
+  (void)hipEventRecord(c->ev_dedup, c->meta);
   lsm::StatGrids grids{};
   if (n) {
     lsm::launch_group_by_set(d, ids, n, inverse, f.sc, c->cn, c->meta);
     lsm::launch_set_walk(d, n, (uint32_t)t, f.sc, c->cn, grids, c->meta);
-    lsm::launch_ring_resolve(d, n, c->tail, f.sc, outcome, c->cn, grids, c->meta);
+    lsm::launch_ring_resolve(d, n, f.sc, outcome, c->cn, grids, c->meta);
   }
   (void)hipEventRecord(f.meta_done, c->meta);
-  lsm::launch_finish(c->cn, f.hc_dev, f.sc.stat_part, grids, c->meta);
+  lsm::launch_finish(c->cn, f.hc_dev, f.sc.stat_part, grids, d.tail, c->meta);
+  // the announced bits are first read by the next gather's set walk
+  if (record)
+    lsm::launch_announce(an.ids, an.n, (uint32_t)(k & 31u), d.mask, c->win_ids + (uint64_t)kslot * c->max_batch,
+                         f.sc, c->meta);
   (void)hipEventRecord(f.finish_done, c->meta);
-  f.stats_pending = true;
 
-  // host fetch (PCIe ingress) beside the enqueue copy (PCIe egress) and the
-  // hit copy; fills after both
+  // host fetch (PCIe ingress), after gather t-1's fills on the same stream
   (void)hipStreamWaitEvent(c->host, f.meta_done, 0);
-  if (pf.used) (void)hipStreamWaitEvent(c->host, pf.enq_done, 0);
+  if (f.dma_used) (void)hipStreamWaitEvent(c->host, f.dma_done, 0);
   rec(kEvHost0, c->host);
-  if (n) lsm::launch_copy(CopyMode::kHostToOut, d, U, f.sc, outp, c->host);
+  if (n) lsm::launch_copy(CopyMode::kHostToOut, d, n, f.sc, outp, c->host);
   rec(kEvHost1, c->host);
-  (void)hipEventRecord(f.host_done, c->host);
 
-  (void)hipStreamWaitEvent(c->data, f.meta_done, 0);
-  rec(kEvEnq0, c->data);
-  if (n && d.V) lsm::launch_copy(CopyMode::kCacheToRing, d, U, f.sc, outp, c->data);
-  rec(kEvEnq1, c->data);
-  (void)hipEventRecord(f.enq_done, c->data);
-  rec(kEvHbm0, c->data);
-  if (n) lsm::launch_copy(CopyMode::kHbmToOut, d, U, f.sc, outp, c->data);
-  rec(kEvHbm1, c->data);
-  (void)hipStreamWaitEvent(c->data, f.host_done, 0);
-  rec(kEvFill0, c->data);
-  if (n) lsm::launch_copy(CopyMode::kOutToCache, d, U, f.sc, outp, c->data);
-  rec(kEvFill1, c->data);
-  rec(kEvAll1, c->data);
-  (void)hipEventRecord(f.data_done, c->data);
-  f.prof_pending = prof;
+  // staging and hit copy once gather t-1's fills have landed; the ring write
+  // (PCIe egress) is queued later on the DMA stream
+  if (pf.used) (void)hipStreamWaitEvent(c->meta, pf.data_done, 0);
+  if (f.dma_used) (void)hipStreamWaitEvent(c->meta, f.dma_done, 0);
+  if (n && d.V) lsm::launch_copy(CopyMode::kCacheToStage, d, n, f.sc, outp, c->meta);
+  rec(kEvHbm0, c->meta);
+  if (n) lsm::launch_copy(CopyMode::kHbmToOut, d, n, f.sc, outp, c->meta);
+  rec(kEvHbm1, c->meta);
+  (void)hipEventRecord(f.stage_done, c->meta);
+
+  // fills after the host fetch, the staging and the hit copy
+  (void)hipStreamWaitEvent(c->host, f.stage_done, 0);
+  rec(kEvFill0, c->host);
+  if (n) lsm::launch_copy(CopyMode::kOutToCache, d, n, f.sc, outp, c->host);
+  rec(kEvFill1, c->host);
+  rec(kEvAll1, c->host);
+  (void)hipEventRecord(f.data_done, c->host);
+  f.used = true;
+  ps.pending = false;
   if (hipGetLastError() != hipSuccess) return fail_device(c);
 
+  // the GPU runs on while the host waits for the dedup result; the meta stream
+  // is in order, so gather t-1's counters are published by then
+  if (hipEventSynchronize(c->ev_dedup) != hipSuccess) return fail_device(c);
+  harvest_stats(c, pf);
+  issue_dma(c, pf);
+  const uint32_t err = dedup ? c->dd->err : 0u;
+  const uint32_t U = dedup ? c->dd->n_unique : 0u;
+  if (err) return LSMGNN_E_RANGE;  // every queued kernel of the batch is a no-op
+
+  f.stats_pending = true;
+  f.t = t;
+  f.requests = n;
+  if (prof) {
+    ps.pending = true;
+    ps.counted = false;
+    ps.t = t;
+    ps.requests = n;
+    ps.ring = false;
+  }
   if (clear) c->win_batch[slot] = -1;
+  if (record) {
+    c->win_batch[kslot] = (int64_t)k;
+    c->win_len[kslot] = an.n;
+  }
+  if (an.on) c->n_adv = k + 1;
   c->t = t + 1;
   *n_unique = U;
-  if (used) *used = &f;
+  if (issued) *issued = t;
   return LSMGNN_OK;
 }
 
@@ -418,6 +519,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
             dev_alloc(c, &d.stat, N) && dev_alloc(c, &d.present, map_bytes) &&
             dev_alloc(c, &d.chunk_sums, d.nchunks) &&
             dev_alloc(c, &d.set_count, S) && dev_alloc(c, &d.set_idx, S) && dev_alloc(c, &d.uidx, N) &&
+            dev_alloc(c, &d.tail, 2) &&
             (V == 0 || (dev_alloc(c, &d.vpos, N) && dev_alloc(c, &d.ring_tag, V))) &&
             dev_alloc(c, &c->win_ids, (uint64_t)(d.L + 1) * B) && dev_alloc(c, &c->cn, 1) &&
             dev_alloc(c, &c->cn_adv, 1) && dev_alloc(c, &sc.uniq, B) && dev_alloc(c, &sc.uset, B) &&
@@ -433,30 +535,30 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   for (Flight &f : c->fl) {
     f.sc = sc;
     ok = ok && dev_alloc(c, &f.sc.slot, B) && dev_alloc(c, &f.sc.src, B) && dev_alloc(c, &f.sc.ring_dst, B) &&
-         dev_alloc(c, &f.sc.fill_dst, B) && host_alloc(c, &f.hc, &f.hc_dev, sizeof(Counters), true);
+         dev_alloc(c, &f.sc.fill_dst, B) && dev_alloc(c, &f.sc.gate, 1) && dev_alloc(c, &f.sc.host_list, B) &&
+         (V == 0 || dev_alloc(c, &f.sc.staging, (B < V ? B : V) * R)) &&
+         host_alloc(c, &f.hc, &f.hc_dev, sizeof(Counters), true);
   }
-  if (ok && V) {
-    uint8_t *ring_host = nullptr;
-    ok = host_alloc(c, &ring_host, &d.ring_rows, V * R, false);
-  }
+  if (ok && V) ok = host_alloc(c, &c->ring_host, &d.ring_rows, V * R, false);
   if (!ok) {
     release(c);
     delete c;
     return LSMGNN_E_NOMEM;
   }
-  for (hipStream_t *s : {&c->meta, &c->host, &c->data})
+  for (hipStream_t *s : {&c->meta, &c->host, &c->dma})
     ok = ok && hipStreamCreateWithFlags(s, hipStreamNonBlocking) == hipSuccess;
   for (hipEvent_t *e : {&c->ev_in, &c->ev_dedup, &c->ev_adv})
     ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
-  for (Flight &f : c->fl) {
-    for (hipEvent_t *e : {&f.meta_done, &f.finish_done, &f.enq_done, &f.host_done, &f.data_done})
+  for (Flight &f : c->fl)
+    for (hipEvent_t *e : {&f.meta_done, &f.finish_done, &f.stage_done, &f.data_done, &f.dma_done})
       ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
-    for (hipEvent_t &e : f.pe) ok = ok && hipEventCreate(&e) == hipSuccess;
-  }
+  for (PerfSet &p : c->ps)
+    for (hipEvent_t &e : p.e) ok = ok && hipEventCreate(&e) == hipSuccess;
   // initial state: all ways empty, nothing announced, ring empty, counters zero
   ok = ok && hipMemset(d.sets, 0xff, S * sizeof(lsm::SetRec)) == hipSuccess &&
        hipMemset(d.mask, 0, N * 4) == hipSuccess && hipMemset(d.present, 0, map_bytes) == hipSuccess &&
-       hipMemset(d.set_count, 0, S * 4) == hipSuccess && hipMemset(c->cn, 0, sizeof(Counters)) == hipSuccess &&
+       hipMemset(d.set_count, 0, S * 4) == hipSuccess && hipMemset(d.tail, 0, 16) == hipSuccess &&
+       hipMemset(c->cn, 0, sizeof(Counters)) == hipSuccess &&
        hipMemset(c->cn_adv, 0, sizeof(Counters)) == hipSuccess &&
        hipMemcpy(d.stat, cfg->static_score, N * 4, hipMemcpyHostToDevice) == hipSuccess &&
        (V == 0 || (hipMemset(d.vpos, 0, N * 8) == hipSuccess && hipMemset(d.ring_tag, 0xff, V * 4) == hipSuccess)) &&
@@ -475,7 +577,8 @@ void lsmgnn_cache_destroy(lsmgnn_cache *c) {
   if (!c) return;
   {
     DeviceGuard guard(c->device);
-    for (hipStream_t s : {c->meta, c->host, c->data})
+    (void)sync_all(c);  // queues any pending ring write, then waits for everything
+    for (hipStream_t s : {c->meta, c->host, c->dma})
       if (s) (void)hipStreamSynchronize(s);
     release(c);
   }
@@ -495,14 +598,22 @@ lsmgnn_status lsmgnn_advance(lsmgnn_cache *c, const int64_t *ids, uint64_t n, vo
   const int slot = (int)(j % (c->d.L + 1));
   if (hipEventRecord(c->ev_in, s) != hipSuccess) return fail_device(c);
   (void)hipStreamWaitEvent(c->meta, c->ev_in, 0);
+  const uint32_t bit = (uint32_t)(j & 31u);
   if (n)
-    lsm::launch_window_set(ids, n, c->d.N, (uint32_t)(j & 31u), c->d.mask,
-                           c->win_ids + (uint64_t)slot * c->max_batch, record, c->cn_adv, c->meta);
-  lsm::launch_finish(c->cn_adv, c->hc_adv_dev, c->fl[0].sc.stat_part, lsm::StatGrids{}, c->meta);
+    lsm::launch_window_set(ids, n, c->d.N, bit, c->d.mask, c->win_ids + (uint64_t)slot * c->max_batch, record,
+                           c->cn_adv, c->meta);
+  lsm::launch_finish(c->cn_adv, c->hc_adv_dev, c->fl[0].sc.stat_part, lsm::StatGrids{}, nullptr, c->meta);
   if (hipEventRecord(c->ev_adv, c->meta) != hipSuccess || hipGetLastError() != hipSuccess ||
       hipEventSynchronize(c->ev_adv) != hipSuccess)
     return fail_device(c);
-  if (c->hc_adv->err) return LSMGNN_E_RANGE;
+  if (c->hc_adv->err) {
+    // the valid IDs of a recorded list had their bit set: clear it again
+    if (record) {
+      lsm::launch_window_rollback(ids, n, c->d.N, bit, c->d.mask, c->meta);
+      if (hipGetLastError() != hipSuccess || hipStreamSynchronize(c->meta) != hipSuccess) return fail_device(c);
+    }
+    return LSMGNN_E_RANGE;
+  }
   if (record) {
     c->win_batch[slot] = (int64_t)j;
     c->win_len[slot] = n;
@@ -518,30 +629,33 @@ lsmgnn_status lsmgnn_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, voi
   DeviceGuard guard(c->device);
   if (!guard.ok) return LSMGNN_E_DEVICE;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  Flight *f = nullptr;
-  st = issue_gather(c, ids, n, out, unique_ids, inverse, outcome, n_unique, s, &f);
+  uint64_t t = 0;
+  st = issue_gather(c, ids, n, Announce{}, out, unique_ids, inverse, outcome, n_unique, s, &t);
   if (st != LSMGNN_OK) return st;
-  if (hipStreamWaitEvent(s, f->data_done, 0) != hipSuccess || hipEventSynchronize(f->finish_done) != hipSuccess ||
+  Flight &f = c->fl[t & 1];
+  if (hipStreamWaitEvent(s, f.data_done, 0) != hipSuccess || hipEventSynchronize(f.finish_done) != hipSuccess ||
       hipStreamSynchronize(s) != hipSuccess)
     return fail_device(c);
-  harvest_stats(c, *f);
-  harvest_profile(c, *f);
+  harvest_stats(c, f);
+  issue_dma(c, f);  // the ring write may still run when this returns
   return LSMGNN_OK;
 }
 
-lsmgnn_status lsmgnn_gather_async(lsmgnn_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t *unique_ids,
-                                  int64_t *inverse, uint8_t *outcome, uint64_t *n_unique, uint64_t *ticket,
-                                  void *stream) {
+lsmgnn_status lsmgnn_gather_async(lsmgnn_cache *c, const int64_t *ids, uint64_t n, const int64_t *next_ids,
+                                  uint64_t next_n, void *out, int64_t *unique_ids, int64_t *inverse,
+                                  uint8_t *outcome, uint64_t *n_unique, uint64_t *ticket, void *stream) {
   lsmgnn_status st = check_gather_args(c, ids, n, out, unique_ids, inverse, n_unique);
   if (st != LSMGNN_OK) return st;
-  if (!ticket) return LSMGNN_E_INVAL;
+  if (!ticket || (!next_ids && next_n) || next_n > c->max_batch || (reinterpret_cast<uintptr_t>(next_ids) & 7u))
+    return LSMGNN_E_INVAL;
+  Announce an;
+  an.on = next_ids != nullptr;
+  an.ids = next_ids;
+  an.n = next_n;
   DeviceGuard guard(c->device);
   if (!guard.ok) return LSMGNN_E_DEVICE;
-  const uint64_t t = c->t;
-  st = issue_gather(c, ids, n, out, unique_ids, inverse, outcome, n_unique, static_cast<hipStream_t>(stream),
-                    nullptr);
-  if (st == LSMGNN_OK) *ticket = t;
-  return st;
+  return issue_gather(c, ids, n, an, out, unique_ids, inverse, outcome, n_unique,
+                      static_cast<hipStream_t>(stream), ticket);
 }
 
 lsmgnn_status lsmgnn_gather_wait(lsmgnn_cache *c, uint64_t ticket, void *stream) {

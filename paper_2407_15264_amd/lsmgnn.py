@@ -72,7 +72,8 @@ def lib():
         L.lsmgnn_gather.restype = i32
         L.lsmgnn_gather.argtypes = [vp, vp, u64, vp, vp, vp, vp, ctypes.POINTER(u64), vp]
         L.lsmgnn_gather_async.restype = i32
-        L.lsmgnn_gather_async.argtypes = [vp, vp, u64, vp, vp, vp, vp, ctypes.POINTER(u64), ctypes.POINTER(u64), vp]
+        L.lsmgnn_gather_async.argtypes = [vp, vp, u64, vp, u64, vp, vp, vp, vp, ctypes.POINTER(u64),
+                                          ctypes.POINTER(u64), vp]
         L.lsmgnn_gather_wait.restype = i32
         L.lsmgnn_gather_wait.argtypes = [vp, u64, vp]
         L.lsmgnn_sync.restype = i32
@@ -268,13 +269,23 @@ class FeatureCache:
         _check(lib().lsmgnn_gather(*args, ctypes.byref(nu), _stream_handle(stream, self.device)), "lsmgnn_gather")
         return self._result(nu.value, n, out, unique, inv_t, oc_t)
 
-    def gather_async(self, ids, out, unique, inverse=None, outcome=None, stream=None):
+    def gather_async(self, ids, out, unique, inverse=None, outcome=None, stream=None, announce=None):
         """Pipelined gather: returns (ticket, GatherResult) once the unique
-        count is known.  The buffers must be caller-owned tensors (not reused
-        until wait(ticket) and a synchronisation of the stream)."""
+        count is known.  `announce` (int64 device tensor, or None) is the next
+        minibatch to announce after this gather, as advance() would.  The
+        buffers must be caller-owned tensors (not reused until wait(ticket) and
+        a synchronisation of the stream)."""
+        import torch
         n, out, unique, inv_t, oc_t, args = self._gather_args(ids, out, unique, inverse, outcome)
+        if announce is None:
+            ann = (None, 0)
+        else:
+            an = announce.numel()
+            # any non-NULL pointer announces, even an empty list (then it is
+            # not read): the unique buffer's address serves
+            ann = (_dev_ptr(announce, torch.int64, "announce") if an else args[4], an)
         nu, tk = ctypes.c_uint64(), ctypes.c_uint64()
-        _check(lib().lsmgnn_gather_async(*args, ctypes.byref(nu), ctypes.byref(tk),
+        _check(lib().lsmgnn_gather_async(*args[:3], *ann, *args[3:], ctypes.byref(nu), ctypes.byref(tk),
                                          _stream_handle(stream, self.device)), "lsmgnn_gather_async")
         return tk.value, self._result(nu.value, n, out, unique, inv_t, oc_t)
 

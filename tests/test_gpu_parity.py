@@ -233,9 +233,11 @@ def test_provenance_hits_from_hbm_misses_from_store():
     cache.close()
 
 
-def _run_async_parity(store, static, S, V, L, batches, label):
+def _run_async_parity(store, static, S, V, L, batches, label, combined=True):
     """Pipelined gathers (two in flight) with rotating output buffers; each
-    gather's outputs are compared with the oracle once it has been waited for."""
+    gather's outputs are compared with the oracle once it has been waited for.
+    combined: announce the next minibatch within the gather call (else with a
+    separate advance call after it)."""
     dev = torch.device("cuda", 0)
     mb = max(1, max(len(b) for b in batches))
     cache = lsmgnn.FeatureCache(store.num_nodes, store.row_bytes, store.buf, static, S, V, L, mb)
@@ -264,10 +266,14 @@ def _run_async_parity(store, static, S, V, L, batches, label):
 
     for b in range(len(batches)):
         out, uq, inv, oc = bufs[b % 3]
-        ticket, r = cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc)
+        nxt = db[b + L + 1] if b + L + 1 < len(batches) else None
+        if combined:
+            ticket, r = cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc, announce=nxt)
+        else:
+            ticket, r = cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc)
+            if nxt is not None:
+                cache.advance(nxt)
         pending.append((ticket, r, b))
-        if b + L + 1 < len(batches):
-            cache.advance(db[b + L + 1])
         if len(pending) == 2:
             check(*pending.pop(0))
     for p in pending:
@@ -302,6 +308,82 @@ def test_async_pipeline_rmat20_first_60():
 @pytest.mark.parametrize("seed", range(6))
 def test_async_pipeline_random(seed):
     n, S, V, L, T, rb, stat, batches, announce = _random_case(100 + seed)
-    log(f"case: pipelined random seed {seed}: N={n} S={S} V={V} L={L}")
+    combined = seed % 2 == 0
+    log(f"case: pipelined random seed {seed}: N={n} S={S} V={V} L={L} combined={combined}")
     store = Store.random_bytes(n, rb, seed)
-    _run_async_parity(store, stat, S, V, L, batches, f"async-random{seed}")
+    _run_async_parity(store, stat, S, V, L, batches, f"async-random{seed}", combined=combined)
+
+
+def test_async_announce_errors_leave_state_unchanged():
+    """A pipelined gather whose own list or announced list holds an
+    out-of-range ID is rejected as a whole: neither the gather nor the
+    announcement happens, and the stream then continues exactly like the
+    oracle's."""
+    log("case: pipelined gather + announcement error paths")
+    n, S, V, L, mb = 300, 4, 8, 2, 64
+    store = Store.random_bytes(n, 32, 3)
+    stat = (np.arange(n, dtype=np.uint32) * 7) % 11
+    cache = lsmgnn.FeatureCache(n, 32, store.buf, stat, S, V, L, mb)
+    orc = Oracle(n, 32, stat, S, V, L, store=store.np)
+    dev = lambda a: torch.as_tensor(np.asarray(a, np.int64)).cuda()  # noqa: E731
+    rng = np.random.default_rng(9)
+    batches = [rng.integers(0, n, size=int(rng.integers(1, mb + 1))) for _ in range(12)]
+    db = [dev(b) for b in batches]
+    out, uq, inv, oc = (torch.empty(mb * 32, dtype=torch.uint8, device="cuda"),
+                        torch.empty(mb, dtype=torch.int64, device="cuda"),
+                        torch.empty(mb, dtype=torch.int64, device="cuda"),
+                        torch.empty(mb, dtype=torch.uint8, device="cuda"))
+    for j in range(L + 1):
+        cache.advance(db[j])
+        orc.advance(batches[j])
+
+    def good(b):
+        tk, r = cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc, announce=db[b + L + 1])
+        cache.wait(tk)
+        torch.cuda.current_stream().synchronize()
+        o = orc.gather(batches[b])
+        orc.advance(batches[b + L + 1])
+        assert np.array_equal(r.unique.cpu().numpy(), o["uniq"]), b
+        assert np.array_equal(r.inverse.cpu().numpy(), o["inv"]), b
+        assert np.array_equal(r.outcome.cpu().numpy(), o["outcome"]), b
+        assert np.array_equal(r.out.cpu().numpy(), o["out"]), b
+
+    good(0)
+    good(1)
+    cache.sync()
+    before = cache.export_state()
+    for bad in ([0, n], [-5, 1], [n - 1, 1 << 40]):
+        with pytest.raises(lsmgnn.LsmgnnError) as e:
+            cache.gather_async(db[2], out, uq, inverse=inv, outcome=oc, announce=dev(bad))
+        assert e.value.status == "E_RANGE"
+        with pytest.raises(lsmgnn.LsmgnnError) as e:  # a bad gather list with a good announcement
+            cache.gather_async(dev(bad), out, uq, inverse=inv, outcome=oc, announce=db[2 + L + 1])
+        assert e.value.status == "E_RANGE"
+    # the combined calls keep the window full: a separate announcement is refused
+    with pytest.raises(lsmgnn.LsmgnnError) as e:
+        cache.advance(db[2 + L + 1])
+    assert e.value.status == "E_WINDOW"
+    with pytest.raises(lsmgnn.LsmgnnError) as e:
+        cache.gather_async(db[2], out, uq, inverse=inv, outcome=oc, announce=dev(np.zeros(mb + 1)))
+    assert e.value.status == "E_INVAL"
+    cache.sync()
+    after = cache.export_state()
+    assert after["t"] == before["t"] and np.array_equal(after["tags"], before["tags"])
+    assert np.array_equal(after["ring_tags"], before["ring_tags"]) and after["ring_tail"] == before["ring_tail"]
+    # the stream continues exactly like the oracle's
+    last = len(batches) - L - 1
+    for b in range(2, last):
+        good(b)
+    compare_state(cache, orc, "after pipelined errors")
+    # an empty announcement is an announcement: the window is full after it
+    tk, r = cache.gather_async(db[last], out, uq, inverse=inv, outcome=oc, announce=dev([]))
+    cache.wait(tk)
+    torch.cuda.current_stream().synchronize()
+    o = orc.gather(batches[last])
+    orc.advance(np.zeros(0, np.int64))
+    assert np.array_equal(r.out.cpu().numpy(), o["out"])
+    with pytest.raises(lsmgnn.LsmgnnError) as e:
+        cache.advance(db[0])
+    assert e.value.status == "E_WINDOW"
+    compare_state(cache, orc, "after empty announcement")
+    cache.close()
