@@ -205,16 +205,18 @@ def main():
 
     # per-kernel rates from HIP events on the gather stream
     kern = {}
-    for name, rows_k, ms, per_row, bound in (
-            ("hbm_copy", prof["hbm_copy_rows"], prof["hbm_copy_ms"], 2 * R, "hbm"),
-            ("host_fetch", prof["host_fetch_rows"], prof["host_fetch_ms"], R, "host_link"),
-            ("enqueue", prof["enqueue_rows"], prof["enqueue_ms"], R, "host_link"),
-            ("fill", prof["fill_rows"], prof["fill_ms"], 2 * R, "hbm")):
-        launches = max(prof[name + "_launches"], 1)
+    for name, key, per_row, bound in (
+            ("hbm_copy", "hbm_copy", 2 * R, "hbm"),
+            ("host_fetch", "host_fetch", R, "host_link"),
+            ("ring_write_dma", "enqueue", R, "host_link"),
+            ("fill", "fill", 2 * R, "hbm")):
+        rows_k, ms = prof[key + "_rows"], prof[key + "_ms"]
+        launches = max(prof[key + "_launches"], 1)
         kern[name] = dict(ms_total=ms, launches=launches, rows=rows_k, avg_us=1e3 * ms / launches,
                           bytes_per_launch=rows_k * per_row / launches,
                           GBps=(rows_k * per_row / (ms / 1e3) / 1e9) if ms > 0 else 0.0, bound=bound)
-    dom = max(kern, key=lambda k: kern[k]["ms_total"])
+    kern["ring_write_dma"]["engine"] = "runtime copy (hipMemcpyAsync of the staged rows), not one of our kernels"
+    dom = max((k for k in kern if "engine" not in kern[k]), key=lambda k: kern[k]["ms_total"])
     kd = kern[dom]
     link_peak = max(ceil["dma_h2d_GBps"], ceil["zero_copy_read_GBps"])
     if kd["bound"] == "hbm":

@@ -94,20 +94,21 @@ typedef struct {
   uint64_t dropped;     /* evicted lines discarded */
 } lsmgnn_counts;
 
-/* Accumulated device time of the data-movement kernels (filled only while
-   profiling is on; see lsmgnn_set_profiling).  Bytes are algorithmic: rows
-   moved times row_bytes, per direction. */
+/* Accumulated device time of the data movement (filled only while profiling
+   is on; see lsmgnn_set_profiling).  Bytes are algorithmic: rows moved times
+   row_bytes, per direction.  The enqueue figures time the ring write (the
+   runtime copy of the staged evicted rows), not the staging kernel. */
 typedef struct {
   double hbm_copy_ms;   uint64_t hbm_copy_launches;   uint64_t hbm_copy_rows;   /* cache -> out */
   double host_fetch_ms; uint64_t host_fetch_launches; uint64_t host_fetch_rows; /* store/ring -> out */
-  double enqueue_ms;    uint64_t enqueue_launches;    uint64_t enqueue_rows;    /* cache -> ring */
+  double enqueue_ms;    uint64_t enqueue_launches;    uint64_t enqueue_rows;    /* staging -> ring */
   double fill_ms;       uint64_t fill_launches;       uint64_t fill_rows;       /* out -> cache */
   double gather_ms;     uint64_t gathers;             /* whole gather, first to last kernel */
 } lsmgnn_profile;
 
 /* Create a cache on cfg->device.  Allocates the HBM cache (S*8 rows), its
-   metadata, per-node window/static/ring-index arrays (about 16 bytes per node),
-   scratch sized for max_batch, and the pinned victim ring (V rows).  On
+   metadata, per-node arrays (about 21 bytes per node), scratch and staging
+   rows sized for max_batch, and the pinned victim ring (V rows).  On
    failure *out is NULL and nothing stays allocated. */
 lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out);
 void lsmgnn_cache_destroy(lsmgnn_cache *c);

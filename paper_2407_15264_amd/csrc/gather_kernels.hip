@@ -22,7 +22,7 @@
 //               q + V >= tail0 + (enqueues before x)  (Sec. 4.3.1)
 //   data        row copies with 128-bit loads/stores: hits HBM->out, misses
 //               and victim hits pinned host->out (a dense list, small grid),
-//               enqueued rows HBM->staging in ring order (a DMA engine then
+//               enqueued rows HBM->staging in ring order (a runtime copy then
 //               writes them to the pinned ring), then fills out->HBM for each
 //               way's final occupant
 #include "internal.h"
@@ -204,12 +204,12 @@ __global__ __launch_bounds__(kBlock) void k_chunk_popc(const uint8_t *present, u
 }
 
 __global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uint32_t nchunks, Counters *cn,
-                                                       DedupResult *dd, DedupResult *gate) {
+                                                       DedupResult *dd, Gate *gate) {
   const uint32_t err = cn->err;
   if (err) {
     if (threadIdx.x == 0) {
-      *gate = DedupResult{err, 0, 0, 0};
-      *dd = DedupResult{err, 0, 0, 0};
+      *gate = Gate{err, 0, 0, 0, 0, 0, {0, 0}};
+      *dd = DedupResult{err, 0, {0, 0}};
     }
     return;
   }
@@ -224,8 +224,8 @@ __global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uin
   }
   if (threadIdx.x == 0) {
     cn->n_unique = carry;
-    *gate = DedupResult{0, carry, 0, 0};
-    *dd = DedupResult{0, carry, 0, 0};
+    *gate = Gate{0, carry, 0, 0, 0, 0, {0, 0}};
+    *dd = DedupResult{0, carry, {0, 0}};
   }
 }
 
@@ -595,9 +595,10 @@ __global__ __launch_bounds__(kBlock) void k_scan_final(const DevState d, Scratch
   }
 }
 
-// Victim-ring probe of every fill and the row source of every unique ID; the
-// unique indices whose rows come from pinned host memory form the host-fetch
-// list (in arbitrary order).
+// Victim-ring probe of every fill and the row source of every unique ID.  Builds
+// the gather's row-copy lists (dense, in arbitrary order): the host fetch (rows
+// from pinned host memory), the hit copy (rows from cache slots) and the fills
+// (each way's final occupant).
 __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc, uint8_t *outcome, Counters *cn) {
   if (cn->err) return;
   const uint32_t U = cn->n_unique;
@@ -606,11 +607,12 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
   uint32_t c_vhit = 0, c_miss = 0, c_hbm = 0, c_host = 0;
   for (uint32_t base = blockIdx.x * kBlock; base < U; base += gridDim.x * kBlock) {
     const uint32_t u = base + threadIdx.x;
-    bool from_host = false;
+    bool from_host = false, from_hbm = false, refill = false;
+    uint64_t code = 0;
+    uint32_t fd = 0;
     if (u < U) {
       const uint8_t kind = sc.kind[u];
       uint8_t oc = 0;  // LSMGNN_HIT
-      uint64_t code;
       if (kind == kKindHit) {
         code = kSrcHbm | sc.slot[u];
         ++c_hbm;
@@ -644,7 +646,7 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
           } else if (q + d.V >= tail_end) {
             // no enqueue of this batch reuses the slot: remove the entry now.
             // An entry of the previous gather may still be on its way to the
-            // ring (its DMA runs beside this gather), so its row is taken from
+            // ring (its copy runs beside this gather), so its row is taken from
             // the backing store, which holds identical bytes.
             d.ring_tag[q % d.V] = kEmpty;
             code = q >= tail_prev ? (kSrcStore | x) : (kSrcRing | (q % d.V));
@@ -663,12 +665,27 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
           ++c_host;
         }
       }
-      sc.src[u] = code;
       from_host = (code & ~kSrcIndex) != kSrcHbm;
+      from_hbm = !from_host;
+      fd = sc.fill_dst[u];
+      refill = fd != 0;
       if (outcome) outcome[u] = oc;
     }
-    const uint32_t i = block_append(from_host, &sc.gate->n_host);
-    if (from_host) sc.host_list[i] = u;
+    const uint32_t ih = block_append(from_host, &sc.gate->n_host);
+    if (from_host) {
+      sc.host_list[ih] = u;
+      sc.host_src[ih] = code;
+    }
+    const uint32_t ib = block_append(from_hbm, &sc.gate->n_hbm);
+    if (from_hbm) {
+      sc.hbm.src[ib] = (uint32_t)(code & kSrcIndex);
+      sc.hbm.dst[ib] = u;
+    }
+    const uint32_t ifl = block_append(refill, &sc.gate->n_fill);
+    if (refill) {
+      sc.fill.src[ifl] = u;
+      sc.fill.dst[ifl] = fd - 1;
+    }
   }
   block_count(c_vhit, sc.stat_part, kStVictimHits);
   block_count(c_miss, sc.stat_part, kStMisses);
@@ -676,7 +693,7 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
   block_count(c_host, sc.stat_part, kStHost);
 }
 
-// Ring bookkeeping for this batch's enqueues; marks the row copies of the
+// Ring bookkeeping for this batch's enqueues; lists the row copies of the
 // entries that are still in the ring at the end of the batch.  Those entries
 // have the sequence numbers [q_lo, tail_end), q_lo = tail_end - min(E, V) for E
 // enqueues, and their rows are staged in that order (entries removed again in
@@ -689,9 +706,11 @@ __global__ __launch_bounds__(kBlock) void k_enq_finalize(const DevState d, Scrat
   const uint64_t tail_end = tail0 + E;
   const uint64_t q_lo = tail_end - (E < d.V ? E : d.V);
   uint32_t c_copy = 0;
-  for (uint32_t u = blockIdx.x * kBlock + threadIdx.x; u < U; u += gridDim.x * kBlock) {
-    uint64_t dst = 0;
-    if (sc.kind[u] == kKindFill && (sc.flags[u] & kFlagEnqueue)) {
+  for (uint32_t base = blockIdx.x * kBlock; base < U; base += gridDim.x * kBlock) {
+    const uint32_t u = base + threadIdx.x;
+    bool stage = false;
+    uint32_t pos = 0;
+    if (u < U && sc.kind[u] == kKindFill && (sc.flags[u] & kFlagEnqueue)) {
       const uint64_t q = tail0 + sc.enq_before[u];
       const uint32_t z = sc.evicted[u];
       d.vpos[z] = q + 1;
@@ -700,12 +719,17 @@ __global__ __launch_bounds__(kBlock) void k_enq_finalize(const DevState d, Scrat
           d.ring_tag[q % d.V] = kEmpty;
         } else {
           d.ring_tag[q % d.V] = z;
-          dst = (q - q_lo) + 1;
+          stage = true;
+          pos = (uint32_t)(q - q_lo);
           ++c_copy;
         }
       }
     }
-    sc.ring_dst[u] = dst;
+    const uint32_t i = block_append(stage, &sc.gate->n_stage);
+    if (stage) {
+      sc.stage.src[i] = sc.slot[u];
+      sc.stage.dst[i] = pos;
+    }
   }
   block_count(c_copy, sc.stat_part, kStEnqCopy);
 }
@@ -736,89 +760,83 @@ void launch_ring_resolve(const DevState &d, uint64_t n, Scratch &sc, uint8_t *ou
 // from the gather's gate; a rejected gather moves nothing.
 constexpr int kUnroll = 4;
 
-template <CopyMode M>
-__device__ __forceinline__ bool row_ends(const DevState &d, const Scratch &sc, uint8_t *out, uint32_t e,
-                                         const uint8_t *&src, uint8_t *&dst) {
-  const uint64_t R = d.R;
-  if constexpr (M == CopyMode::kHbmToOut) {
-    const uint64_t code = sc.src[e];
-    if ((code & ~kSrcIndex) != kSrcHbm) return false;
-    src = d.rows + (code & kSrcIndex) * R;
-    dst = out + (uint64_t)e * R;
-  } else if constexpr (M == CopyMode::kCacheToStage) {
-    const uint64_t rd = sc.ring_dst[e];
-    if (!rd) return false;
-    src = d.rows + (uint64_t)sc.slot[e] * R;
-    dst = sc.staging + (rd - 1) * R;
-  } else {
-    const uint32_t fd = sc.fill_dst[e];
-    if (!fd) return false;
-    src = out + (uint64_t)e * R;
-    dst = d.rows + (uint64_t)(fd - 1) * R;
-  }
-  return true;
-}
-
+// Copy of a row list: item w = (list entry i, 16-byte vector v).  The mode only
+// names the instance (hit copy, staging, fills) so that profiles tell them apart.
 template <CopyMode M, bool kPow2>
-__global__ __launch_bounds__(kBlock) void k_copy(const DevState d, Scratch sc, uint8_t *out, uint32_t nvec,
-                                                 uint32_t vshift) {
-  const DedupResult g = *sc.gate;
-  if (g.err) return;
-  const uint64_t total = (uint64_t)g.n_unique * nvec;
+__global__ __launch_bounds__(kBlock) void k_list_copy(const uint8_t *src, const uint32_t *sidx, uint8_t *dst,
+                                                      const uint32_t *didx, const Gate *gate, const uint32_t *count,
+                                                      uint64_t R, uint32_t nvec, uint32_t vshift) {
+  if (gate->err) return;
+  const uint64_t total = (uint64_t)*count * nvec;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
   for (uint64_t w0 = (uint64_t)blockIdx.x * kBlock + threadIdx.x; w0 < total; w0 += stride * kUnroll) {
     u32x4 v[kUnroll];
-    uint8_t *dst[kUnroll];
+    uint8_t *dp[kUnroll];
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k) {
       const uint64_t w = w0 + k * stride;
-      dst[k] = nullptr;
+      dp[k] = nullptr;
       if (w < total) {
-        const uint32_t e = kPow2 ? (uint32_t)(w >> vshift) : (uint32_t)(w / nvec);
-        const uint64_t byte = (w - (uint64_t)e * nvec) * 16u;
-        const uint8_t *src;
-        uint8_t *dp;
-        if (row_ends<M>(d, sc, out, e, src, dp)) {
-          v[k] = *reinterpret_cast<const u32x4 *>(src + byte);
-          dst[k] = dp + byte;
-        }
+        const uint32_t i = kPow2 ? (uint32_t)(w >> vshift) : (uint32_t)(w / nvec);
+        const uint64_t byte = (w - (uint64_t)i * nvec) * 16u;
+        v[k] = *reinterpret_cast<const u32x4 *>(src + (uint64_t)sidx[i] * R + byte);
+        dp[k] = dst + (uint64_t)didx[i] * R + byte;
       }
     }
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k)
-      if (dst[k]) *reinterpret_cast<u32x4 *>(dst[k]) = v[k];
+      if (dp[k]) *reinterpret_cast<u32x4 *>(dp[k]) = v[k];
   }
 }
 
 // Host fetch: item w = (host-list entry i, 16-byte vector v).  The list entry
-// and its source code are the same for all lanes of a row (broadcast loads).
+// is the same for all lanes of a row (broadcast loads), and the entries of the
+// next pass are loaded while this pass's host reads are in flight, so the
+// reads never wait behind a dependent HBM load.
+#ifndef LSM_HOST_UNROLL
+#define LSM_HOST_UNROLL 4
+#endif
 template <bool kPow2>
 __global__ __launch_bounds__(kBlock) void k_host_fetch(const DevState d, Scratch sc, uint8_t *out, uint32_t nvec,
                                                        uint32_t vshift) {
-  const DedupResult g = *sc.gate;
+  constexpr int kU = LSM_HOST_UNROLL;
+  const Gate g = *sc.gate;
   if (g.err) return;
   const uint64_t R = d.R;
   const uint64_t total = (uint64_t)g.n_host * nvec;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-  for (uint64_t w0 = (uint64_t)blockIdx.x * kBlock + threadIdx.x; w0 < total; w0 += stride * kUnroll) {
-    u32x4 v[kUnroll];
-    uint8_t *dst[kUnroll];
+  auto entry = [&](uint64_t w, uint32_t &e, uint64_t &code) {
+    if (w < total) {
+      const uint32_t i = kPow2 ? (uint32_t)(w >> vshift) : (uint32_t)(w / nvec);
+      e = sc.host_list[i];
+      code = sc.host_src[i];
+    }
+  };
+  uint32_t e[kU];
+  uint64_t code[kU];
+  uint64_t w0 = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k) {
+  for (int k = 0; k < kU; ++k) entry(w0 + k * stride, e[k], code[k]);
+  for (; w0 < total; w0 += stride * kU) {
+    u32x4 v[kU];
+    uint8_t *dst[kU];
+#pragma unroll
+    for (int k = 0; k < kU; ++k) {
       const uint64_t w = w0 + k * stride;
       dst[k] = nullptr;
       if (w < total) {
-        const uint32_t i = kPow2 ? (uint32_t)(w >> vshift) : (uint32_t)(w / nvec);
-        const uint64_t byte = (w - (uint64_t)i * nvec) * 16u;
-        const uint32_t e = sc.host_list[i];
-        const uint64_t code = sc.src[e];
-        const uint8_t *src = ((code & ~kSrcIndex) == kSrcRing ? d.ring_rows : d.store) + (code & kSrcIndex) * R;
+        const uint64_t byte = (kPow2 ? (w & (nvec - 1)) : (w % nvec)) * 16u;
+        const uint8_t *src =
+            ((code[k] & ~kSrcIndex) == kSrcRing ? d.ring_rows : d.store) + (code[k] & kSrcIndex) * R;
         v[k] = *reinterpret_cast<const u32x4 *>(src + byte);
-        dst[k] = out + (uint64_t)e * R + byte;
+        dst[k] = out + (uint64_t)e[k] * R + byte;
       }
     }
+    const uint64_t w1 = w0 + stride * kU;
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k)
+    for (int k = 0; k < kU; ++k) entry(w1 + k * stride, e[k], code[k]);
+#pragma unroll
+    for (int k = 0; k < kU; ++k)
       if (dst[k]) *reinterpret_cast<u32x4 *>(dst[k]) = v[k];
   }
 }
@@ -835,11 +853,23 @@ __global__ __launch_bounds__(kBlock) void k_host_fetch(const DevState d, Scratch
 #endif
 
 template <CopyMode M>
-static void launch_copy_mode(const DevState &d, uint64_t n, const Scratch &sc, uint8_t *out, hipStream_t s) {
+static void launch_list(const uint8_t *src, const RowList &l, uint8_t *dst, const Gate *gate, const uint32_t *count,
+                        uint64_t n, uint64_t R, hipStream_t s) {
+  const uint32_t nvec = (uint32_t)(R / 16);
+  const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kUnroll, LSM_HBM_GRID);
+  if ((nvec & (nvec - 1)) == 0)
+    hipLaunchKernelGGL((k_list_copy<M, true>), dim3(g), dim3(kBlock), 0, s, src, l.src, dst, l.dst, gate, count, R,
+                       nvec, (uint32_t)__builtin_ctz(nvec));
+  else
+    hipLaunchKernelGGL((k_list_copy<M, false>), dim3(g), dim3(kBlock), 0, s, src, l.src, dst, l.dst, gate, count, R,
+                       nvec, 0u);
+}
+
+void launch_copy(CopyMode mode, const DevState &d, uint64_t n, const Scratch &sc, uint8_t *out, hipStream_t s) {
   const uint32_t nvec = (uint32_t)(d.R / 16);
   const bool pow2 = (nvec & (nvec - 1)) == 0;
   const uint32_t vshift = pow2 ? (uint32_t)__builtin_ctz(nvec) : 0u;
-  if constexpr (M == CopyMode::kHostToOut) {
+  if (mode == CopyMode::kHostToOut) {
     const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kUnroll, LSM_HOST_GRID);
     if (pow2)
       hipLaunchKernelGGL((k_host_fetch<true>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift);
@@ -847,19 +877,16 @@ static void launch_copy_mode(const DevState &d, uint64_t n, const Scratch &sc, u
       hipLaunchKernelGGL((k_host_fetch<false>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift);
     return;
   }
-  const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kUnroll, LSM_HBM_GRID);
-  if (pow2)
-    hipLaunchKernelGGL((k_copy<M, true>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift);
-  else
-    hipLaunchKernelGGL((k_copy<M, false>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift);
-}
-
-void launch_copy(CopyMode mode, const DevState &d, uint64_t n, const Scratch &sc, uint8_t *out, hipStream_t s) {
   switch (mode) {
-    case CopyMode::kHbmToOut: launch_copy_mode<CopyMode::kHbmToOut>(d, n, sc, out, s); break;
-    case CopyMode::kHostToOut: launch_copy_mode<CopyMode::kHostToOut>(d, n, sc, out, s); break;
-    case CopyMode::kCacheToStage: launch_copy_mode<CopyMode::kCacheToStage>(d, n, sc, out, s); break;
-    case CopyMode::kOutToCache: launch_copy_mode<CopyMode::kOutToCache>(d, n, sc, out, s); break;
+    case CopyMode::kHbmToOut:
+      launch_list<CopyMode::kHbmToOut>(d.rows, sc.hbm, out, sc.gate, &sc.gate->n_hbm, n, d.R, s);
+      break;
+    case CopyMode::kCacheToStage:
+      launch_list<CopyMode::kCacheToStage>(d.rows, sc.stage, sc.staging, sc.gate, &sc.gate->n_stage, n, d.R, s);
+      break;
+    default:
+      launch_list<CopyMode::kOutToCache>(out, sc.fill, d.rows, sc.gate, &sc.gate->n_fill, n, d.R, s);
+      break;
   }
 }
 
@@ -943,7 +970,7 @@ void launch_window_rollback(const int64_t *ids, uint64_t n, uint64_t N, uint32_t
 // the list in its window slot and sets the minibatch's bit for every ID (only
 // that bit changes in this kernel, so a plain read-modify-write is exact).
 __global__ void k_announce(const int64_t *ids, uint32_t n, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
-                           const DedupResult *gate) {
+                           const Gate *gate) {
   if (gate->err) return;
   const uint32_t b = 1u << bit;
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {

@@ -65,22 +65,39 @@ struct Counters {
   uint32_t pad[16];
 };
 
-// Dedup result of a gather, written by the chunk scan twice: to pinned host
-// memory (the host reads the unique count and the error flag from it) and to a
-// per-gather device gate that the row copies read (they run on other streams
-// after the metadata kernels have reset the call counters).  In the gate,
-// n_host counts the entries of the host-fetch list.
+// Dedup result of a gather, written by the chunk scan to pinned host memory:
+// the host reads the unique count and the error flag from it.
 struct DedupResult {
   uint32_t err;
   uint32_t n_unique;
-  uint32_t n_host;
-  uint32_t pad;
+  uint32_t pad[2];
+};
+
+// The gather's gate in device memory: the error flag and unique count (set by
+// the chunk scan) and the lengths of the row-copy lists (appended by the
+// resolve and enqueue kernels).  The row copies run on other streams after the
+// metadata kernels have reset the call counters, so they read it from here.
+struct Gate {
+  uint32_t err;
+  uint32_t n_unique;
+  uint32_t n_host;   // host-fetch list
+  uint32_t n_hbm;    // hit-copy list
+  uint32_t n_fill;   // fill list
+  uint32_t n_stage;  // staging list
+  uint32_t pad[2];
+};
+
+// A row-copy list: entry i moves row src[i] of its source to row dst[i] of its
+// destination (dense, in arbitrary order).
+struct RowList {
+  uint32_t *src;
+  uint32_t *dst;
 };
 
 // Per-call scratch, every array sized for max_batch entries unless noted.
-// slot, src, ring_dst, fill_dst, host_list, staging and gate are read by the
-// row copies of a gather while the next gather's metadata kernels run, so the
-// runtime keeps two of them and alternates by gather parity.
+// The row-copy lists, the gate and the staging rows are read by the row copies
+// of a gather while the next gather's metadata kernels run, so the runtime
+// keeps two of them and alternates by gather parity.
 struct Scratch {
   uint32_t *uniq;       // ascending unique IDs
   uint32_t *uset;       // set of uniq[u]
@@ -100,13 +117,15 @@ struct Scratch {
   uint32_t *scan_part;  // ceil(max_batch / kScanChunk) + 2 partial sums
   uint64_t *this_q;     // 1 + ring sequence of u's own enqueue in this batch, or 0
   uint32_t *this_enq;   // the unique index that enqueued u in this batch
-  uint64_t *src;        // row source of out row u (kSrc* code)
-  uint64_t *ring_dst;   // 1 + staging row that receives the row u evicted, or 0
   uint32_t *fill_dst;   // 1 + cache slot that out row u refills (the way's final fill), or 0
   uint32_t *stat_part;  // [kNumStat][kMaxGrid] per-block partial counts
-  DedupResult *gate;    // [1] unique count, error flag and host-list length of the gather
-  uint32_t *host_list;  // unique indices whose rows come from pinned host memory
-  uint8_t *staging;     // [min(max_batch, V)][R] evicted rows in ring order, for the DMA engine
+  Gate *gate;           // [1]
+  uint32_t *host_list;  // host fetch: out rows whose rows come from pinned host memory
+  uint64_t *host_src;   //   and the source code (kSrc*) of each
+  RowList hbm;          // hits and same-batch victim hits: cache slot -> out row
+  RowList fill;         // final occupants: out row -> cache slot
+  RowList stage;        // surviving enqueues: cache slot -> staging row
+  uint8_t *staging;     // [min(max_batch, V)][R] evicted rows in ring order, for the ring write
 };
 
 struct DevState {

@@ -10,31 +10,33 @@
 // order with each other):
 //   meta  - dedup, set grouping, set walk, ring resolution, counters, then
 //           staging of the enqueued rows and the hit copy
-//   host  - the host fetch (misses and victim hits, PCIe ingress), then the
-//           fills
-//   dma   - the staged rows to the pinned victim ring on a DMA engine (PCIe
-//           egress without compute units: a copy kernel's host-link writes
-//           would stall the memory requests of the kernels beside it)
+//   host  - the host fetch (misses and victim hits, PCIe ingress), back to
+//           back from gather to gather
+//   dma   - the staged rows to the pinned victim ring as a runtime copy
+//           (hipMemcpyAsync: a DMA engine, or the runtime's own copy kernel,
+//           as the runtime decides; either stalls the kernels beside it far
+//           less than a copy kernel of ours writing over the host link), and
+//           after each ring write the fills of the next gather
 // The host queues all of a gather's kernels at once (every batch-dependent
 // size, and the ring tail, stay in device memory) and then waits only for the
 // dedup result, to report the unique count or reject the batch; a rejected
-// batch's kernels are already queued and do nothing.  A DMA copy needs its
+// batch's kernels are already queued and do nothing.  A runtime copy needs its
 // size on the host, so gather t's ring write is queued once its counters are
 // known: by the next call's dedup wait, or by any call that synchronises.
 // The metadata of gather t+1 depends only on the metadata of gather t, so it
-// runs while gather t's host fetch moves rows.  The data kernels of a gather
-// read per-unique arrays (slot, src, ring_dst, fill_dst, host_list), the gate
-// and the staging rows that its metadata wrote; two copies of them alternate
-// by gather parity, so gather t's metadata first waits for gather t-2's fills,
-// and its staging for gather t-2's DMA.  Other cross-gather hazards:
+// runs while gather t's host fetch moves rows.  The data copies of a gather
+// read the row-copy lists, the gate and the staging rows that its metadata
+// wrote; two copies of them alternate by gather parity, so gather t's metadata
+// first waits for gather t-2's fills, and its staging for gather t-2's ring
+// write.  Other cross-gather hazards:
 //   - cache rows: gather t's staging and hit copy wait for gather t-1's fills;
-//     gather t's fills wait for its staging and hit copy;
+//     gather t's fills wait for its host fetch, staging and hit copy;
 //   - ring rows: gather t reads ring rows only of entries enqueued by gathers
 //     up to t-2 (entries of gather t-1 are read from the backing store), so
-//     its host fetch waits for gather t-2's DMA; gather t's DMA overwrites
-//     slots that gather t-1's host fetch may read, and it waits for gather
-//     t's staging, which waited for gather t-1's fills, which follow gather
-//     t-1's host fetch on the host stream.
+//     its host fetch waits for gather t-2's ring write; gather t's ring write
+//     overwrites slots that gather t-1's host fetch may read, and it follows
+//     gather t's staging, which waited for gather t-1's fills, which waited
+//     for gather t-1's host fetch.
 // Every call first makes the meta stream wait for the work already queued on
 // the caller's stream (the IDs and the output buffers).
 #include <hip/hip_runtime.h>
@@ -73,11 +75,11 @@ enum { kEvHbm0, kEvHbm1, kEvEnq0, kEvEnq1, kEvHost0, kEvHost1, kEvFill0, kEvFill
 
 // One gather in flight; two of these alternate by gather parity.
 struct Flight {
-  Scratch sc{};                // metadata scratch (shared) + this parity's per-unique arrays
+  Scratch sc{};                // metadata scratch (shared) + this parity's row-copy lists and gate
   Counters *hc = nullptr;      // pinned: counters published by the gather's last metadata kernel
   Counters *hc_dev = nullptr;
-  hipEvent_t meta_done = nullptr, finish_done = nullptr, stage_done = nullptr, data_done = nullptr,
-             dma_done = nullptr;
+  hipEvent_t meta_done = nullptr, finish_done = nullptr, stage_done = nullptr, host_done = nullptr,
+             data_done = nullptr, dma_done = nullptr;
   bool used = false;           // events of this slot have been recorded at least once
   bool stats_pending = false;  // counters not yet added to the totals
   bool dma_pending = false;    // staged rows not yet queued for the ring
@@ -136,7 +138,7 @@ void release(lsmgnn_cache *c) {
   for (void *p : c->host_allocs) (void)hipHostFree(p);
   c->host_allocs.clear();
   for (Flight &f : c->fl)
-    for (hipEvent_t e : {f.meta_done, f.finish_done, f.stage_done, f.data_done, f.dma_done})
+    for (hipEvent_t e : {f.meta_done, f.finish_done, f.stage_done, f.host_done, f.data_done, f.dma_done})
       if (e) (void)hipEventDestroy(e);
   for (PerfSet &p : c->ps)
     for (hipEvent_t e : p.e)
@@ -361,15 +363,16 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
                          f.sc, c->meta);
   (void)hipEventRecord(f.finish_done, c->meta);
 
-  // host fetch (PCIe ingress), after gather t-1's fills on the same stream
+  // host fetch (PCIe ingress), right after gather t-1's on the same stream
   (void)hipStreamWaitEvent(c->host, f.meta_done, 0);
   if (f.dma_used) (void)hipStreamWaitEvent(c->host, f.dma_done, 0);
   rec(kEvHost0, c->host);
   if (n) lsm::launch_copy(CopyMode::kHostToOut, d, n, f.sc, outp, c->host);
   rec(kEvHost1, c->host);
+  (void)hipEventRecord(f.host_done, c->host);
 
   // staging and hit copy once gather t-1's fills have landed; the ring write
-  // (PCIe egress) is queued later on the DMA stream
+  // (PCIe egress) is queued later on the dma stream
   if (pf.used) (void)hipStreamWaitEvent(c->meta, pf.data_done, 0);
   if (f.dma_used) (void)hipStreamWaitEvent(c->meta, f.dma_done, 0);
   if (n && d.V) lsm::launch_copy(CopyMode::kCacheToStage, d, n, f.sc, outp, c->meta);
@@ -377,23 +380,27 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   if (n) lsm::launch_copy(CopyMode::kHbmToOut, d, n, f.sc, outp, c->meta);
   rec(kEvHbm1, c->meta);
   (void)hipEventRecord(f.stage_done, c->meta);
-
-  // fills after the host fetch, the staging and the hit copy
-  (void)hipStreamWaitEvent(c->host, f.stage_done, 0);
-  rec(kEvFill0, c->host);
-  if (n) lsm::launch_copy(CopyMode::kOutToCache, d, n, f.sc, outp, c->host);
-  rec(kEvFill1, c->host);
-  rec(kEvAll1, c->host);
-  (void)hipEventRecord(f.data_done, c->host);
   f.used = true;
   ps.pending = false;
   if (hipGetLastError() != hipSuccess) return fail_device(c);
 
   // the GPU runs on while the host waits for the dedup result; the meta stream
-  // is in order, so gather t-1's counters are published by then
+  // is in order, so gather t-1's counters are published by then and its ring
+  // write can be queued
   if (hipEventSynchronize(c->ev_dedup) != hipSuccess) return fail_device(c);
   harvest_stats(c, pf);
   issue_dma(c, pf);
+
+  // fills after the host fetch, the staging and the hit copy, queued behind
+  // gather t-1's ring write so that the next host fetch need not wait for them
+  (void)hipStreamWaitEvent(c->dma, f.host_done, 0);
+  (void)hipStreamWaitEvent(c->dma, f.stage_done, 0);
+  rec(kEvFill0, c->dma);
+  if (n) lsm::launch_copy(CopyMode::kOutToCache, d, n, f.sc, outp, c->dma);
+  rec(kEvFill1, c->dma);
+  rec(kEvAll1, c->dma);
+  (void)hipEventRecord(f.data_done, c->dma);
+  if (hipGetLastError() != hipSuccess) return fail_device(c);
   const uint32_t err = dedup ? c->dd->err : 0u;
   const uint32_t U = dedup ? c->dd->n_unique : 0u;
   if (err) return LSMGNN_E_RANGE;  // every queued kernel of the batch is a no-op
@@ -528,14 +535,15 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
             dev_alloc(c, &sc.seg_st, B) && dev_alloc(c, &sc.kind, B) && dev_alloc(c, &sc.flags, B) &&
             dev_alloc(c, &sc.dead, B) && dev_alloc(c, &sc.evicted, B) && dev_alloc(c, &sc.enq_before, B) &&
             dev_alloc(c, &sc.scan_part, B / lsm::kScanChunk + 2) && dev_alloc(c, &sc.this_q, B) &&
-            dev_alloc(c, &sc.this_enq, B) &&
+            dev_alloc(c, &sc.this_enq, B) && dev_alloc(c, &sc.slot, B) && dev_alloc(c, &sc.fill_dst, B) &&
             dev_alloc(c, &sc.stat_part, (uint64_t)lsm::kNumStat * lsm::kMaxGrid) &&
             host_alloc(c, &c->dd, &c->dd_dev, sizeof(DedupResult), true) &&
             host_alloc(c, &c->hc_adv, &c->hc_adv_dev, sizeof(Counters), true);
   for (Flight &f : c->fl) {
     f.sc = sc;
-    ok = ok && dev_alloc(c, &f.sc.slot, B) && dev_alloc(c, &f.sc.src, B) && dev_alloc(c, &f.sc.ring_dst, B) &&
-         dev_alloc(c, &f.sc.fill_dst, B) && dev_alloc(c, &f.sc.gate, 1) && dev_alloc(c, &f.sc.host_list, B) &&
+    ok = ok && dev_alloc(c, &f.sc.gate, 1) && dev_alloc(c, &f.sc.host_list, B) && dev_alloc(c, &f.sc.host_src, B) &&
+         dev_alloc(c, &f.sc.hbm.src, B) && dev_alloc(c, &f.sc.hbm.dst, B) && dev_alloc(c, &f.sc.fill.src, B) &&
+         dev_alloc(c, &f.sc.fill.dst, B) && dev_alloc(c, &f.sc.stage.src, B) && dev_alloc(c, &f.sc.stage.dst, B) &&
          (V == 0 || dev_alloc(c, &f.sc.staging, (B < V ? B : V) * R)) &&
          host_alloc(c, &f.hc, &f.hc_dev, sizeof(Counters), true);
   }
@@ -550,7 +558,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   for (hipEvent_t *e : {&c->ev_in, &c->ev_dedup, &c->ev_adv})
     ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
   for (Flight &f : c->fl)
-    for (hipEvent_t *e : {&f.meta_done, &f.finish_done, &f.stage_done, &f.data_done, &f.dma_done})
+    for (hipEvent_t *e : {&f.meta_done, &f.finish_done, &f.stage_done, &f.host_done, &f.data_done, &f.dma_done})
       ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
   for (PerfSet &p : c->ps)
     for (hipEvent_t &e : p.e) ok = ok && hipEventCreate(&e) == hipSuccess;
