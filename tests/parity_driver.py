@@ -126,6 +126,94 @@ def run_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, 
     return dict(total=tot, seconds=time.time() - t0)
 
 
+def device_store(store: Store, device=0):
+    """A device copy of the backing store, for checking gathered rows on the GPU."""
+    import torch
+    t = torch.empty((store.num_nodes, store.row_bytes), dtype=torch.uint8, device=torch.device("cuda", device))
+    lsmgnn.copy_bytes(t.data_ptr(), store.buf.ptr, store.num_nodes * store.row_bytes)
+    return t
+
+
+def run_async_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, rows="all", store_gpu=None,
+                     state_every=0, label="async", combined=True, near_threshold=0, device=0):
+    """The launch configuration of bench.py: lsmgnn_gather_async with the next
+    minibatch's announcement (combined=True; else a separate lsmgnn_advance),
+    two gathers in flight, three rotating output-buffer sets.  Each gather's
+    unique IDs, inverse, outcomes and rows are compared with the oracle once it
+    has been waited for; counters are compared as totals and the cache and ring
+    state every `state_every` gathers and at the end.  rows as in run_parity."""
+    import torch
+    dev = torch.device("cuda", device)
+    mb = max(1, max(len(b) for b in batches))
+    L = lookahead
+    cache = lsmgnn.FeatureCache(store.num_nodes, store.row_bytes, store.buf, static, num_sets, victim_rows, L, mb,
+                                near_threshold=near_threshold, device=device)
+    orc = Oracle(store.num_nodes, store.row_bytes, static, num_sets, victim_rows, L,
+                 near_threshold=near_threshold, store=store.np)
+    db = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in batches]
+    bufs = [(torch.empty(mb * store.row_bytes, dtype=torch.uint8, device=dev),
+             torch.empty(mb, dtype=torch.int64, device=dev), torch.empty(mb, dtype=torch.int64, device=dev),
+             torch.empty(mb, dtype=torch.uint8, device=dev)) for _ in range(3)]
+    for j in range(min(L + 1, len(batches))):
+        cache.advance(db[j])
+        orc.advance(batches[j])
+    pending = []
+    t0 = time.time()
+
+    def check(ticket, r, b):
+        cache.wait(ticket)
+        torch.cuda.current_stream().synchronize()
+        where = f"{label} gather {b}"
+        full_rows = rows == "all" or (isinstance(rows, int) and b % rows == 0)
+        o = orc.gather(np.asarray(batches[b], np.int64), rows=full_rows)
+        assert r.n_unique == o["uniq"].size, (where, r.n_unique, o["uniq"].size)
+        if not np.array_equal(r.unique.cpu().numpy(), o["uniq"]):
+            raise AssertionError(f"{where}: unique IDs differ")
+        if not np.array_equal(r.inverse.cpu().numpy(), o["inv"]):
+            raise AssertionError(f"{where}: inverse differs")
+        oc = r.outcome.cpu().numpy()
+        if not np.array_equal(oc, o["outcome"]):
+            bad = np.flatnonzero(oc != o["outcome"])[:5]
+            raise AssertionError(f"{where}: outcome differs at unique idx {bad.tolist()}")
+        if full_rows:
+            if not np.array_equal(r.out.cpu().numpy(), o["out"]):
+                raise AssertionError(f"{where}: gathered rows differ from the oracle's")
+        elif store_gpu is not None:
+            if not torch.equal(r.out, store_gpu.index_select(0, r.unique)):
+                raise AssertionError(f"{where}: gathered rows differ from the backing store")
+        if b + L + 1 < len(batches):
+            orc.advance(batches[b + L + 1])
+
+    for b in range(len(batches)):
+        out, uq, inv, oc = bufs[b % 3]
+        nxt = db[b + L + 1] if b + L + 1 < len(batches) else None
+        if combined:
+            ticket, r = cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc, announce=nxt)
+        else:
+            ticket, r = cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc)
+            if nxt is not None:
+                cache.advance(nxt)
+        pending.append((ticket, r, b))
+        if state_every and (b + 1) % state_every == 0:
+            # the exported state is the one after every issued gather: drain first
+            while pending:
+                check(*pending.pop(0))
+            compare_state(cache, orc, f"{label} gather {b}")
+            log(f"  {label}: {b + 1} gathers checked ({time.time() - t0:.1f} s)")
+        elif len(pending) == 2:
+            check(*pending.pop(0))
+    for p in pending:
+        check(*p)
+    tot_gpu = cache.stats()[1]
+    tot_orc = orc.stats()[1]
+    for k in COUNT_KEYS:
+        assert tot_gpu[k] == tot_orc[k], (label, k, tot_gpu[k], tot_orc[k])
+    compare_state(cache, orc, f"{label} end")
+    cache.close()
+    orc.close()
+    return dict(total=tot_gpu, seconds=time.time() - t0)
+
+
 def config_stream(cfg, batches=None):
     wl = W.Workload(cfg, batches)
     return wl, [wl.batch(b) for b in range(wl.num_batches)]

@@ -9,6 +9,8 @@ the cache, L = 0, V = 0 and 1, n = max_batch), error paths that must leave the
 state unchanged, determinism, and provenance (hits come from HBM, misses from
 the backing store).
 """
+import time
+
 import numpy as np
 import pytest
 
@@ -18,7 +20,8 @@ torch = pytest.importorskip("torch")
 
 from paper_2407_15264_amd import lsmgnn  # noqa: E402
 from paper_2407_15264_amd import workload as W  # noqa: E402
-from tests.parity_driver import Store, compare_state, config_stream, log, run_parity  # noqa: E402
+from tests.parity_driver import (Store, compare_state, config_stream, device_store, log,  # noqa: E402
+                                 run_async_parity, run_parity)
 from oracle.oracle import Oracle  # noqa: E402
 
 
@@ -53,6 +56,31 @@ def test_workload_rmat20_parity():
     tot = res["total"]
     log(f"  {cfg.name}: {tot}")
     assert tot["victim_hits"] > 0 and tot["hits"] > 0
+
+
+@pytest.mark.timeout(1500)
+def test_workload_rmat10m_full_size_pipelined_parity():
+    """The 10M-node workload at full size (41 GB pinned store, 8 GiB cache,
+    4 GiB ring, 500 minibatches of 4096 seeds) in the bench's launch
+    configuration.  Every gather: unique IDs, inverse and outcomes against the
+    oracle, rows against the backing store (a device copy); every 50th gather:
+    rows against the oracle's; every 100th and at the end: cache and ring
+    state; at the end: all counters."""
+    cfg = W.CONFIGS[3]
+    log(f"case: {cfg.name}, all {cfg.batches} gathers, pipelined, full size")
+    t0 = time.time()
+    wl, batches = config_stream(cfg)
+    log(f"  workload generated in {time.time() - t0:.1f} s (max batch {wl.max_batch})")
+    store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
+    sg = device_store(store)
+    log(f"  store filled and copied to the device ({time.time() - t0:.1f} s)")
+    res = run_async_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead,
+                           batches, rows=50, store_gpu=sg, state_every=100, label=cfg.name)
+    tot = res["total"]
+    log(f"  {cfg.name}: {tot} in {res['seconds']:.1f} s")
+    assert tot["hits"] > 0 and tot["victim_hits"] > 0 and tot["misses"] > 0
+    del sg
+    torch.cuda.empty_cache()
 
 
 def _random_case(seed):
@@ -234,56 +262,7 @@ def test_provenance_hits_from_hbm_misses_from_store():
 
 
 def _run_async_parity(store, static, S, V, L, batches, label, combined=True):
-    """Pipelined gathers (two in flight) with rotating output buffers; each
-    gather's outputs are compared with the oracle once it has been waited for.
-    combined: announce the next minibatch within the gather call (else with a
-    separate advance call after it)."""
-    dev = torch.device("cuda", 0)
-    mb = max(1, max(len(b) for b in batches))
-    cache = lsmgnn.FeatureCache(store.num_nodes, store.row_bytes, store.buf, static, S, V, L, mb)
-    orc = Oracle(store.num_nodes, store.row_bytes, static, S, V, L, store=store.np)
-    db = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in batches]
-    bufs = [(torch.empty(mb * store.row_bytes, dtype=torch.uint8, device=dev),
-             torch.empty(mb, dtype=torch.int64, device=dev), torch.empty(mb, dtype=torch.int64, device=dev),
-             torch.empty(mb, dtype=torch.uint8, device=dev)) for _ in range(3)]
-    for j in range(min(L + 1, len(batches))):
-        cache.advance(db[j])
-        orc.advance(batches[j])
-    pending = []
-
-    def check(ticket, r, b):
-        cache.wait(ticket)
-        torch.cuda.current_stream().synchronize()
-        o = orc.gather(np.asarray(batches[b], np.int64))
-        where = f"{label} async gather {b}"
-        assert r.n_unique == o["uniq"].size, where
-        assert np.array_equal(r.unique.cpu().numpy(), o["uniq"]), where
-        assert np.array_equal(r.inverse.cpu().numpy(), o["inv"]), where
-        assert np.array_equal(r.outcome.cpu().numpy(), o["outcome"]), where
-        assert np.array_equal(r.out.cpu().numpy(), o["out"]), where
-        if b + L + 1 < len(batches):
-            orc.advance(batches[b + L + 1])
-
-    for b in range(len(batches)):
-        out, uq, inv, oc = bufs[b % 3]
-        nxt = db[b + L + 1] if b + L + 1 < len(batches) else None
-        if combined:
-            ticket, r = cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc, announce=nxt)
-        else:
-            ticket, r = cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc)
-            if nxt is not None:
-                cache.advance(nxt)
-        pending.append((ticket, r, b))
-        if len(pending) == 2:
-            check(*pending.pop(0))
-    for p in pending:
-        check(*p)
-    tot_gpu = cache.stats()[1]
-    tot_orc = orc.stats()[1]
-    for k in ("batch", "requests", "unique", "hits", "victim_hits", "misses", "evictions", "enqueued", "dropped"):
-        assert tot_gpu[k] == tot_orc[k], (label, k, tot_gpu[k], tot_orc[k])
-    compare_state(cache, orc, f"{label} async end")
-    cache.close()
+    run_async_parity(store, static, S, V, L, batches, rows="all", label=label, combined=combined)
 
 
 def test_async_pipeline_rmat14():
@@ -312,6 +291,34 @@ def test_async_pipeline_random(seed):
     log(f"case: pipelined random seed {seed}: N={n} S={S} V={V} L={L} combined={combined}")
     store = Store.random_bytes(n, rb, seed)
     _run_async_parity(store, stat, S, V, L, batches, f"async-random{seed}", combined=combined)
+
+
+def _long_case(seed):
+    rng = np.random.default_rng(77 + seed)
+    n = int(rng.integers(50, 400))
+    S = int(rng.integers(2, 12))
+    V = int(rng.choice([0, 5, 40]))
+    L = int(rng.choice([4, 8, 9, 16, 31]))
+    T = int(rng.choice([0, 1, 2]))
+    stat = rng.integers(0, 50, n).astype(np.uint32)
+    batches = [rng.integers(0, n, rng.integers(10, 60)) for _ in range(90)]
+    return n, S, V, L, T, stat, batches
+
+
+@pytest.mark.parametrize("pipelined", [False, True])
+@pytest.mark.parametrize("seed", range(12))
+def test_long_streams_window_wrap(seed, pipelined):
+    """90 minibatches, so the announced-minibatch bit positions wrap around
+    their 32-bit word several times, with lookaheads up to 31."""
+    n, S, V, L, T, stat, batches = _long_case(seed)
+    log(f"case: long stream seed {seed} pipelined={pipelined}: N={n} S={S} V={V} L={L} T={T}")
+    store = Store.random_bytes(n, 32, seed)
+    if pipelined:
+        run_async_parity(store, stat, S, V, L, batches, rows="all", near_threshold=T, label=f"long{seed}",
+                         state_every=10)
+    else:
+        run_parity(store, stat, S, V, L, batches, near_threshold=T, rows="all", state_every=10,
+                   label=f"long{seed}")
 
 
 def test_async_announce_errors_leave_state_unchanged():
