@@ -13,6 +13,8 @@ Default workload: R-MAT graph with 2^20 nodes and 2^24 edges (a, b, c, d =
 0.57, 0.19, 0.19, 0.05), fp32 x 256 features (1 GiB pinned host store), GraphSAGE
 sampling of 1024 seeds per minibatch with fanout (15, 10, 5), an 8-way cache
 holding 10% of the nodes, a victim ring of 5% of the nodes, lookahead 4.
+--config picks another shape; the typed graph (4) runs one cache per node type
+and a step gathers the minibatch's IDs of every type.
 
 Prints one JSON line.  `value` is gathered feature bytes (unique rows x row
 bytes) per second over the timed steps; `roofline` rates the dominant data
@@ -94,28 +96,56 @@ def measure_ceilings(torch, lsmgnn, store_ptr, nbytes):
     return res
 
 
-def cpu_baseline(cfg, wl, store_np, budget_s):
-    """The CPU oracle (single-threaded C) on the same stream from gather 0,
-    stopped after about budget_s seconds."""
+def make_parts(W, cfg, nb):
+    """One part per cache: a homogeneous workload has one, a typed workload one
+    per node type (each with its own feature width, store, cache and ring)."""
+    if isinstance(cfg, W.HeteroConfig):
+        wl = W.HeteroWorkload(cfg, nb)
+        parts = [dict(label=f"type {t}", num_nodes=n, dim=d, elt=cfg.elt_bytes, seed=cfg.seed + 1 + t,
+                      static=wl.static[t], shape=cfg.cache_shape(t), batches=wl.type_batches(t))
+                 for t, (n, d) in enumerate(zip(cfg.type_counts(), cfg.dims))]
+        requests = float(sum(b.size for p in parts for b in p["batches"])) / nb
+    else:
+        wl = W.Workload(cfg, nb)
+        parts = [dict(label="all", num_nodes=cfg.num_nodes, dim=cfg.dim, elt=cfg.elt_bytes, seed=cfg.seed,
+                      static=wl.static, shape=cfg.cache, batches=[wl.batch(b) for b in range(nb)])]
+        requests = float(wl.ids.size) / nb
+    for p in parts:
+        p["R"] = p["dim"] * p["elt"]
+    return parts, requests
+
+
+def cpu_baseline(parts, budget_s):
+    """The CPU oracle (single-threaded C, one instance per part) on the same
+    stream from gather 0, stopped after about budget_s seconds."""
     from oracle.oracle import Oracle
-    L = cfg.cache.lookahead
-    o = Oracle(cfg.num_nodes, cfg.row_bytes, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, L,
-               store=store_np)
-    for j in range(L + 1):
-        o.advance(wl.batch(j))
+    orcs = []
+    for p in parts:
+        sh = p["shape"]
+        o = Oracle(p["num_nodes"], p["R"], p["static"], sh.num_sets, sh.victim_rows, sh.lookahead,
+                   near_threshold=sh.near_threshold, store=p["store_np"])
+        for j in range(sh.lookahead + 1):
+            o.advance(p["batches"][j])
+        orcs.append(o)
+    L = parts[0]["shape"].lookahead
+    nb = len(parts[0]["batches"])
     t0 = time.perf_counter()
-    done, rows = 0, 0
-    while done < wl.num_batches - L - 1 and time.perf_counter() - t0 < budget_s:
-        r = o.gather(wl.batch(done), rows=True)
-        o.advance(wl.batch(done + L + 1))
-        rows += r["uniq"].size
+    done, rows, nbytes = 0, 0, 0
+    while done < nb - L - 1 and time.perf_counter() - t0 < budget_s:
+        for p, o in zip(parts, orcs):
+            r = o.gather(p["batches"][done], rows=True)
+            o.advance(p["batches"][done + L + 1])
+            rows += r["uniq"].size
+            nbytes += r["uniq"].size * p["R"]
         done += 1
     dt = time.perf_counter() - t0
-    o.close()
-    return {"value": rows * cfg.row_bytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+    for o in orcs:
+        o.close()
+    return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"gathers 0..{done - 1} of the same stream ({done} minibatches, {rows} unique rows, "
                       f"{dt:.1f} s), rows copied with memcpy from the host store",
-            "rows_per_s": rows / dt, "seconds_per_minibatch": dt / max(done, 1),
+            "rows_per_s": rows / dt,
+        "parts": len(parts), "seconds_per_minibatch": dt / max(done, 1),
             "cpu": platform.processor() or platform.machine()}
 
 
@@ -124,7 +154,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=180)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", type=int, default=2, help="workload shape (1, 2, 3 or 5)")
+    ap.add_argument("--config", type=int, default=2, help="workload shape (1 to 5; 4 is the typed graph)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sync", action="store_true",
@@ -142,79 +172,96 @@ def main():
 
     lsmgnn.lib()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    cfg = W.CONFIGS[args.config]
-    L = cfg.cache.lookahead
+    cfg = {**W.CONFIGS, **W.HETERO}[args.config]
+    L = cfg.lookahead if isinstance(cfg, W.HeteroConfig) else cfg.cache.lookahead
     nb = max(cfg.batches, args.warmup + args.steps + L + 1)
     t0 = time.perf_counter()
-    wl = W.Workload(cfg, nb)
+    parts, requests = make_parts(W, cfg, nb)
     log(f"[bench] workload {cfg.name}: {nb} minibatches generated in {time.perf_counter() - t0:.1f}s "
-        f"(mean {np.diff(wl.offsets).mean():.0f} requests)")
-    store = lsmgnn.PinnedBuffer(cfg.num_nodes * cfg.row_bytes)
-    W.fill_features(store.ptr, cfg.dim, cfg.elt_bytes, 0, cfg.num_nodes, cfg.seed)
-    store_np = store.numpy(np.uint8, (cfg.num_nodes, cfg.row_bytes))
-    log(f"[bench] pinned store {cfg.num_nodes * cfg.row_bytes / 2**30:.2f} GiB filled")
+        f"(mean {requests:.0f} requests)")
+    for p in parts:
+        p["store"] = lsmgnn.PinnedBuffer(p["num_nodes"] * p["R"])
+        W.fill_features(p["store"].ptr, p["dim"], p["elt"], 0, p["num_nodes"], p["seed"])
+        p["store_np"] = p["store"].numpy(np.uint8, (p["num_nodes"], p["R"]))
+    log(f"[bench] pinned store {sum(p['num_nodes'] * p['R'] for p in parts) / 2**30:.2f} GiB filled")
 
-    ceil = measure_ceilings(torch, lsmgnn, store.ptr, cfg.num_nodes * cfg.row_bytes)
+    big = max(parts, key=lambda p: p["num_nodes"] * p["R"])
+    ceil = measure_ceilings(torch, lsmgnn, big["store"].ptr, big["num_nodes"] * big["R"])
     log(f"[bench] ceilings: {json.dumps({k: round(v, 1) for k, v in ceil.items()})}")
 
     dev = torch.device("cuda", 0)
-    batches = [torch.as_tensor(wl.batch(b)).to(dev) for b in range(nb)]
-    mb = wl.max_batch
-    cache = lsmgnn.FeatureCache(cfg.num_nodes, cfg.row_bytes, store, wl.static, cfg.cache.num_sets,
-                                cfg.cache.victim_rows, L, mb, near_threshold=cfg.cache.near_threshold)
-    # three output sets rotate: at most two gathers are in flight
-    bufs = [(torch.empty(mb * cfg.row_bytes, dtype=torch.uint8, device=dev),
-             torch.empty(mb, dtype=torch.int64, device=dev),
-             torch.empty(mb, dtype=torch.int64, device=dev)) for _ in range(3)]
-    for j in range(L + 1):
-        cache.advance(batches[j])
-    tickets = {}
+    for p in parts:
+        sh = p["shape"]
+        p["dev_batches"] = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in p["batches"]]
+        mb = max(1, max(b.size for b in p["batches"]))
+        p["cache"] = lsmgnn.FeatureCache(p["num_nodes"], p["R"], p["store"], p["static"], sh.num_sets,
+                                         sh.victim_rows, sh.lookahead, mb, near_threshold=sh.near_threshold)
+        # three output sets rotate: at most two gathers are in flight
+        p["bufs"] = [(torch.empty(mb * p["R"], dtype=torch.uint8, device=dev),
+                      torch.empty(mb, dtype=torch.int64, device=dev),
+                      torch.empty(mb, dtype=torch.int64, device=dev)) for _ in range(3)]
+        for j in range(L + 1):
+            p["cache"].advance(p["dev_batches"][j])
+        p["tickets"] = {}
 
     def step(b):
-        out, uniq, inv = bufs[b % 3]
-        if args.sync:
-            r = cache.gather(batches[b], out=out, unique=uniq, inverse=inv)
-            cache.advance(batches[b + L + 1])
-        else:  # gather minibatch b and announce minibatch b+L+1 in one call
-            tickets[b], r = cache.gather_async(batches[b], out, uniq, inverse=inv, announce=batches[b + L + 1])
-        if not args.sync and b - 1 in tickets:
-            cache.wait(tickets.pop(b - 1))  # a consumer of minibatch b-1 would run after this
-        return r.n_unique
+        nbytes = 0
+        for p in parts:
+            c, db = p["cache"], p["dev_batches"]
+            out, uniq, inv = p["bufs"][b % 3]
+            if args.sync:
+                r = c.gather(db[b], out=out, unique=uniq, inverse=inv)
+                c.advance(db[b + L + 1])
+            else:  # gather minibatch b and announce minibatch b+L+1 in one call
+                p["tickets"][b], r = c.gather_async(db[b], out, uniq, inverse=inv, announce=db[b + L + 1])
+            nbytes += r.n_unique * p["R"]
+        if not args.sync:
+            for p in parts:
+                if b - 1 in p["tickets"]:
+                    p["cache"].wait(p["tickets"].pop(b - 1))  # a consumer of minibatch b-1 would run after this
+        return nbytes
+
+    def drain():
+        for p in parts:
+            for b in list(p["tickets"]):
+                p["cache"].wait(p["tickets"].pop(b))
 
     for b in range(args.warmup):
         step(b)
-    for b in list(tickets):
-        cache.wait(tickets.pop(b))
-    _, tot0 = cache.stats()
-    cache.set_profiling(True)
+    drain()
+    tot0 = [p["cache"].stats()[1] for p in parts]
+    for p in parts:
+        p["cache"].set_profiling(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    rows = 0
+    nbytes = 0
     for b in range(args.warmup, args.warmup + args.steps):
-        rows += step(b)
-    for b in list(tickets):
-        cache.wait(tickets.pop(b))
+        nbytes += step(b)
+    drain()
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    prof = cache.profile()
-    cache.set_profiling(False)
-    _, tot1 = cache.stats()
-    d = {k: tot1[k] - tot0[k] for k in tot1}
-    R = cfg.row_bytes
-    gbps = rows * R / dt / 1e9
+    profs = [p["cache"].profile() for p in parts]
+    for p in parts:
+        p["cache"].set_profiling(False)
+    tot1 = [p["cache"].stats()[1] for p in parts]
+    d = {k: sum(t1[k] - t0_[k] for t0_, t1 in zip(tot0, tot1)) for k in tot1[0]}
+    gbps = nbytes / dt / 1e9
+    rows = d["unique"]
 
-    # per-kernel rates from HIP events on the gather stream
+    # per-kernel rates from HIP events on the gather streams, summed over the parts
     kern = {}
     for name, key, per_row, bound in (
-            ("hbm_copy", "hbm_copy", 2 * R, "hbm"),
-            ("host_fetch", "host_fetch", R, "host_link"),
-            ("ring_write_dma", "enqueue", R, "host_link"),
-            ("fill", "fill", 2 * R, "hbm")):
-        rows_k, ms = prof[key + "_rows"], prof[key + "_ms"]
-        launches = max(prof[key + "_launches"], 1)
+            ("hbm_copy", "hbm_copy", 2, "hbm"),
+            ("host_fetch", "host_fetch", 1, "host_link"),
+            ("ring_write_dma", "enqueue", 1, "host_link"),
+            ("fill", "fill", 2, "hbm")):
+        ms = sum(pr[key + "_ms"] for pr in profs)
+        rows_k = sum(pr[key + "_rows"] for pr in profs)
+        kbytes = sum(pr[key + "_rows"] * per_row * p["R"] for pr, p in zip(profs, parts))
+        launches = max(sum(pr[key + "_launches"] for pr in profs), 1)
         kern[name] = dict(ms_total=ms, launches=launches, rows=rows_k, avg_us=1e3 * ms / launches,
-                          bytes_per_launch=rows_k * per_row / launches,
-                          GBps=(rows_k * per_row / (ms / 1e3) / 1e9) if ms > 0 else 0.0, bound=bound)
+                          bytes_per_launch=kbytes / launches,
+                          GBps=(kbytes / (ms / 1e3) / 1e9) if ms > 0 else 0.0, bound=bound)
     kern["ring_write_dma"]["engine"] = "runtime copy (hipMemcpyAsync of the staged rows), not one of our kernels"
     dom = max((k for k in kern if "engine" not in kern[k]), key=lambda k: kern[k]["ms_total"])
     kd = kern[dom]
@@ -247,11 +294,13 @@ def main():
         "metric": METRIC, "value": gbps, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": 1e3 * dt / args.steps, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
-        "config": dict(cfg.describe(), feature_dtype=cfg.feature_dtype, minibatches_timed=args.steps,
+        "config": dict(cfg.describe(), feature_dtype="fp32" if cfg.elt_bytes == 4 else "fp16",
+                       minibatches_timed=args.steps,
                        first_timed_minibatch=args.warmup,
                        api=("lsmgnn_gather + lsmgnn_advance" if args.sync
                             else "lsmgnn_gather_async with announcement (two minibatches in flight)")),
         "rows_per_s": rows / dt,
+        "parts": len(parts),
         "hit_rate": d["hits"] / max(d["unique"], 1),
         "victim_hit_rate": d["victim_hits"] / max(d["unique"], 1),
         "miss_rate": d["misses"] / max(d["unique"], 1),
@@ -261,13 +310,14 @@ def main():
         "roofline_hbm": roof_hbm,
         "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}
                     for k, v in kern.items()},
-        "gather_ms_events": prof["gather_ms"] / max(prof["gathers"], 1),
+        "gather_ms_events": sum(pr["gather_ms"] for pr in profs) / max(sum(pr["gathers"] for pr in profs), 1),
         "ceilings": ceil,
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(cfg, wl, store_np, args.cpu_budget)
+        res["cpu_baseline"] = cpu_baseline(parts, args.cpu_budget)
         res["cpu_baseline"]["gpu_over_cpu"] = gbps / res["cpu_baseline"]["value"]
-    cache.close()
+    for p in parts:
+        p["cache"].close()
     print(json.dumps(res), flush=True)
 
 

@@ -63,6 +63,9 @@ typedef enum {
 /* per-unique-ID outcome codes written by lsmgnn_gather */
 enum { LSMGNN_HIT = 0, LSMGNN_VICTIM_HIT = 1, LSMGNN_MISS = 2 };
 
+/* lsmgnn_config.flags */
+#define LSMGNN_FLAG_PAGEABLE_STORE 1u /* host_store is ordinary (pageable) host memory */
+
 typedef struct {
   uint64_t num_nodes;   /* IDs are int64 in [0, num_nodes); 1 <= num_nodes <= 2^32 - 1 */
   uint64_t row_bytes;   /* bytes per feature row; a positive multiple of 16 */
@@ -72,11 +75,19 @@ typedef struct {
   uint32_t lookahead;   /* L in [0, 31]: minibatches announced ahead */
   uint32_t near_threshold; /* T; 0 selects max(1, L / 8) (one eighth of the window) */
   int32_t device;       /* HIP device ordinal */
-  uint32_t flags;       /* reserved, must be 0 */
-  /* Backing store: num_nodes * row_bytes bytes of PINNED host memory (from
-     lsmgnn_host_alloc, hipHostMalloc or a pinned torch tensor), row v at
-     offset v * row_bytes.  Borrowed: the caller keeps it alive and unchanged
-     while the cache exists; the library only reads it. */
+  uint32_t flags;       /* 0 or LSMGNN_FLAG_PAGEABLE_STORE; other bits must be 0 */
+  uint32_t host_threads; /* pageable store: host threads copying rows (0 selects 8) */
+  /* Backing store: num_nodes * row_bytes bytes of host memory, row v at offset
+     v * row_bytes.  Borrowed: the caller keeps it alive and unchanged while
+     the cache exists; the library only reads it.
+     Without flags it must be PINNED memory (from lsmgnn_host_alloc,
+     hipHostMalloc or a pinned torch tensor): the GPU reads miss rows from it
+     directly.  With LSMGNN_FLAG_PAGEABLE_STORE it may be ordinary memory, for
+     stores larger than the pinned memory a process may hold: after a
+     gather's metadata, host threads copy the rows of its misses and victim
+     hits into a pinned bounce buffer (max_batch rows per gather in flight)
+     that the GPU then reads.  Same results; lsmgnn_gather_async then returns
+     once those rows are copied. */
   const void *host_store;
   /* Static score per node (host, num_nodes entries); copied at create. */
   const uint32_t *static_score;
@@ -103,6 +114,7 @@ typedef struct {
   double host_fetch_ms; uint64_t host_fetch_launches; uint64_t host_fetch_rows; /* store/ring -> out */
   double enqueue_ms;    uint64_t enqueue_launches;    uint64_t enqueue_rows;    /* staging -> ring */
   double fill_ms;       uint64_t fill_launches;       uint64_t fill_rows;       /* out -> cache */
+  double host_copy_ms;  uint64_t host_copy_rows;      /* pageable store: host threads' row copies (wall time) */
   double gather_ms;     uint64_t gathers;             /* whole gather, first to last kernel */
 } lsmgnn_profile;
 

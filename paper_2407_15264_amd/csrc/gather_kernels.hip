@@ -792,7 +792,8 @@ __global__ __launch_bounds__(kBlock) void k_list_copy(const uint8_t *src, const 
 // Host fetch: item w = (host-list entry i, 16-byte vector v).  The list entry
 // is the same for all lanes of a row (broadcast loads), and the entries of the
 // next pass are loaded while this pass's host reads are in flight, so the
-// reads never wait behind a dependent HBM load.
+// reads never wait behind a dependent HBM load.  With a pageable store the
+// host has already copied entry i's row to bounce row i.
 #ifndef LSM_HOST_UNROLL
 #define LSM_HOST_UNROLL 4
 #endif
@@ -826,9 +827,13 @@ __global__ __launch_bounds__(kBlock) void k_host_fetch(const DevState d, Scratch
       dst[k] = nullptr;
       if (w < total) {
         const uint64_t byte = (kPow2 ? (w & (nvec - 1)) : (w % nvec)) * 16u;
-        const uint8_t *src =
-            ((code[k] & ~kSrcIndex) == kSrcRing ? d.ring_rows : d.store) + (code[k] & kSrcIndex) * R;
-        v[k] = *reinterpret_cast<const u32x4 *>(src + byte);
+        // bounce row i holds entry i: vector w is the w-th of the buffer
+        const u32x4 *sp =
+            sc.bounce ? reinterpret_cast<const u32x4 *>(sc.bounce) + w
+                      : reinterpret_cast<const u32x4 *>(
+                            ((code[k] & ~kSrcIndex) == kSrcRing ? d.ring_rows : d.store) + (code[k] & kSrcIndex) * R +
+                            byte);
+        v[k] = *sp;
         dst[k] = out + (uint64_t)e[k] * R + byte;
       }
     }

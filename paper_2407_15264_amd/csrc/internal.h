@@ -126,6 +126,7 @@ struct Scratch {
   RowList fill;         // final occupants: out row -> cache slot
   RowList stage;        // surviving enqueues: cache slot -> staging row
   uint8_t *staging;     // [min(max_batch, V)][R] evicted rows in ring order, for the ring write
+  uint8_t *bounce;      // pageable store only: [max_batch][R] pinned, the host-fetch rows in list order
 };
 
 struct DevState {

@@ -4,10 +4,13 @@
 // pinned victim ring), validates arguments before anything changes, and
 // launches the gfx950 kernels of gather_kernels.hip.
 //
-// Streams.  A gather runs on three internal streams, all at default priority
-// (three, so that with the caller's stream each gets its own hardware queue
-// under HIP's default of four per process; streams that share a queue run in
-// order with each other):
+// Streams.  A gather runs on three internal streams, all at default priority,
+// shared by every cache on the device (three in all, so that with the caller's
+// stream each gets its own hardware queue under HIP's default of four per
+// process; streams that share a queue run in order with each other, and the
+// caches of a heterogeneous graph, one per node type, would otherwise
+// multiply them).  Each cache orders its own work with its own events; on a
+// shared stream the work of different caches only interleaves:
 //   meta  - dedup, set grouping, set walk, ring resolution, counters, then
 //           staging of the enqueued rows and the hit copy
 //   host  - the host fetch (misses and victim hits, PCIe ingress), back to
@@ -41,12 +44,15 @@
 // the caller's stream (the IDs and the output buffers).
 #include <hip/hip_runtime.h>
 
+#include <chrono>
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
+#include "host_pool.h"
 #include "internal.h"
 #include "lsmgnn.h"
 
@@ -80,6 +86,9 @@ struct Flight {
   Counters *hc_dev = nullptr;
   hipEvent_t meta_done = nullptr, finish_done = nullptr, stage_done = nullptr, host_done = nullptr,
              data_done = nullptr, dma_done = nullptr;
+  uint32_t *hlist_host = nullptr;  // pageable store: host views of sc.host_list, sc.host_src, sc.bounce
+  uint64_t *hsrc_host = nullptr;
+  uint8_t *bounce_host = nullptr;
   bool used = false;           // events of this slot have been recorded at least once
   bool stats_pending = false;  // counters not yet added to the totals
   bool dma_pending = false;    // staged rows not yet queued for the ring
@@ -102,6 +111,50 @@ struct PerfSet {
   uint32_t n_hbm = 0, n_host = 0, n_enq = 0, n_fill = 0;
 };
 
+// The per-device stream triple, created with the first cache on a device and
+// destroyed with the last.
+constexpr int kMaxDevices = 64;
+struct StreamSet {
+  hipStream_t meta = nullptr, host = nullptr, dma = nullptr;
+  int refs = 0;
+};
+std::mutex g_streams_mu;
+StreamSet g_streams[kMaxDevices];
+
+// Call with the device current.
+bool acquire_streams(int dev, StreamSet &out) {
+  std::lock_guard<std::mutex> lock(g_streams_mu);
+  StreamSet &ss = g_streams[dev];
+  if (ss.refs == 0) {
+    bool ok = true;
+    for (hipStream_t *st : {&ss.meta, &ss.host, &ss.dma})
+      ok = ok && hipStreamCreateWithFlags(st, hipStreamNonBlocking) == hipSuccess;
+    if (!ok) {
+      (void)hipGetLastError();
+      for (hipStream_t *st : {&ss.meta, &ss.host, &ss.dma}) {
+        if (*st) (void)hipStreamDestroy(*st);
+        *st = nullptr;
+      }
+      return false;
+    }
+  }
+  ++ss.refs;
+  out = ss;
+  return true;
+}
+
+void release_streams(int dev) {
+  std::lock_guard<std::mutex> lock(g_streams_mu);
+  StreamSet &ss = g_streams[dev];
+  if (ss.refs <= 0) return;
+  if (--ss.refs == 0) {
+    for (hipStream_t *st : {&ss.meta, &ss.host, &ss.dma}) {
+      if (*st) (void)hipStreamDestroy(*st);
+      *st = nullptr;
+    }
+  }
+}
+
 }  // namespace
 
 struct lsmgnn_cache {
@@ -117,8 +170,12 @@ struct lsmgnn_cache {
   DedupResult *dd = nullptr, *dd_dev = nullptr;
   Flight fl[2];
   PerfSet ps[kPerfSets];
-  hipStream_t meta = nullptr, host = nullptr, dma = nullptr;
+  hipStream_t meta = nullptr, host = nullptr, dma = nullptr;  // the device's shared streams
+  bool has_streams = false;
   uint8_t *ring_host = nullptr;  // pinned victim ring rows, host address
+  bool pageable = false;         // the backing store is pageable: host threads copy its rows
+  const uint8_t *store_host = nullptr;
+  lsm::HostPool *pool = nullptr;
   hipEvent_t ev_in = nullptr, ev_dedup = nullptr, ev_adv = nullptr;
   uint64_t t = 0;  // gathers issued
   uint64_t n_adv = 0, tail = 0;
@@ -133,6 +190,8 @@ struct lsmgnn_cache {
 namespace {
 
 void release(lsmgnn_cache *c) {
+  delete c->pool;
+  c->pool = nullptr;
   for (void *p : c->dev_allocs) (void)hipFree(p);
   c->dev_allocs.clear();
   for (void *p : c->host_allocs) (void)hipHostFree(p);
@@ -145,8 +204,8 @@ void release(lsmgnn_cache *c) {
       if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : {c->ev_in, c->ev_dedup, c->ev_adv})
     if (e) (void)hipEventDestroy(e);
-  for (hipStream_t s : {c->meta, c->host, c->dma})
-    if (s) (void)hipStreamDestroy(s);
+  if (c->has_streams) release_streams(c->device);
+  c->has_streams = false;
 }
 
 template <typename T>
@@ -249,6 +308,29 @@ void issue_dma(lsmgnn_cache *c, Flight &f) {
   }
   (void)hipEventRecord(f.dma_done, c->dma);
   f.dma_used = true;
+}
+
+// Pageable store: copy the rows of the gather's host-fetch list (misses and
+// victim hits) into its pinned bounce buffer, row i for list entry i, on the
+// pool's threads.  The list and the source codes were written by the resolve
+// kernel into pinned memory.
+void copy_host_rows(lsmgnn_cache *c, Flight &f, uint64_t n, bool prof) {
+  const uint64_t R = c->d.R;
+  const uint64_t *src = f.hsrc_host;
+  uint8_t *bounce = f.bounce_host;
+  const uint8_t *store = c->store_host, *ring = c->ring_host;
+  const auto t0 = std::chrono::steady_clock::now();
+  c->pool->run(n, 256, [&](uint64_t i0, uint64_t i1) {
+    for (uint64_t i = i0; i < i1; ++i) {
+      const uint64_t code = src[i];
+      const uint8_t *s = ((code & ~lsm::kSrcIndex) == lsm::kSrcRing ? ring : store) + (code & lsm::kSrcIndex) * R;
+      std::memcpy(bounce + i * R, s, R);
+    }
+  });
+  if (prof) {
+    c->acc.host_copy_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    c->acc.host_copy_rows += n;
+  }
 }
 
 // Read a finished gather's kernel timings (its rows must have moved and its
@@ -363,13 +445,17 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
                          f.sc, c->meta);
   (void)hipEventRecord(f.finish_done, c->meta);
 
-  // host fetch (PCIe ingress), right after gather t-1's on the same stream
-  (void)hipStreamWaitEvent(c->host, f.meta_done, 0);
-  if (f.dma_used) (void)hipStreamWaitEvent(c->host, f.dma_done, 0);
-  rec(kEvHost0, c->host);
-  if (n) lsm::launch_copy(CopyMode::kHostToOut, d, n, f.sc, outp, c->host);
-  rec(kEvHost1, c->host);
-  (void)hipEventRecord(f.host_done, c->host);
+  // host fetch (PCIe ingress), right after gather t-1's on the same stream;
+  // with a pageable store it is launched once the host has copied the rows
+  auto host_fetch = [&]() {
+    (void)hipStreamWaitEvent(c->host, f.meta_done, 0);
+    if (!c->pageable && f.dma_used) (void)hipStreamWaitEvent(c->host, f.dma_done, 0);
+    rec(kEvHost0, c->host);
+    if (n) lsm::launch_copy(CopyMode::kHostToOut, d, n, f.sc, outp, c->host);
+    rec(kEvHost1, c->host);
+    (void)hipEventRecord(f.host_done, c->host);
+  };
+  if (!c->pageable) host_fetch();
 
   // staging and hit copy once gather t-1's fills have landed; the ring write
   // (PCIe egress) is queued later on the dma stream
@@ -384,12 +470,21 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   ps.pending = false;
   if (hipGetLastError() != hipSuccess) return fail_device(c);
 
-  // the GPU runs on while the host waits for the dedup result; the meta stream
-  // is in order, so gather t-1's counters are published by then and its ring
-  // write can be queued
-  if (hipEventSynchronize(c->ev_dedup) != hipSuccess) return fail_device(c);
+  // the GPU runs on while the host waits for the dedup result (with a pageable
+  // store: for the whole metadata); the meta stream is in order, so gather
+  // t-1's counters are published by then and its ring write can be queued
+  if (hipEventSynchronize(c->pageable ? f.finish_done : c->ev_dedup) != hipSuccess) return fail_device(c);
   harvest_stats(c, pf);
   issue_dma(c, pf);
+  if (c->pageable) {
+    if (n && !(dedup && c->dd->err)) {
+      // ring rows are read only for entries of gathers up to t-2, whose ring
+      // writes must have landed
+      if (f.dma_used && hipEventSynchronize(f.dma_done) != hipSuccess) return fail_device(c);
+      copy_host_rows(c, f, f.hc->n_host, prof);
+    }
+    host_fetch();
+  }
 
   // fills after the host fetch, the staging and the hit copy, queued behind
   // gather t-1's ring write so that the next host fetch need not wait for them
@@ -478,25 +573,30 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   *out = nullptr;
   if (!cfg || !cfg->host_store || !cfg->static_score) return LSMGNN_E_INVAL;
   if (reinterpret_cast<uintptr_t>(cfg->host_store) & 15u) return LSMGNN_E_INVAL;
+  const bool pageable = (cfg->flags & LSMGNN_FLAG_PAGEABLE_STORE) != 0;
   const uint64_t N = cfg->num_nodes, R = cfg->row_bytes, S = cfg->num_sets, V = cfg->victim_rows;
   if (N == 0 || N > 0xffffffffull || R == 0 || R % 16 != 0 || S == 0 || S > (0xffffffffull / lsm::kWays) ||
-      cfg->lookahead > 31 || cfg->max_batch == 0 || cfg->max_batch > (1ull << 31) || cfg->flags != 0 ||
+      cfg->lookahead > 31 || cfg->max_batch == 0 || cfg->max_batch > (1ull << 31) ||
+      (cfg->flags & ~LSMGNN_FLAG_PAGEABLE_STORE) != 0 || cfg->host_threads > 256 ||
       V > (1ull << 40))
     return LSMGNN_E_INVAL;
   // byte sizes must not overflow 64 bits
   if (R > (1ull << 40) || S * lsm::kWays > (~0ull / R) || (V && V > (~0ull / R))) return LSMGNN_E_INVAL;
 
   int ndev = 0;
-  if (hipGetDeviceCount(&ndev) != hipSuccess || cfg->device < 0 || cfg->device >= ndev) {
+  if (hipGetDeviceCount(&ndev) != hipSuccess || cfg->device < 0 || cfg->device >= ndev ||
+      cfg->device >= kMaxDevices) {
     (void)hipGetLastError();
     return LSMGNN_E_INVAL;
   }
   DeviceGuard guard(cfg->device);
   if (!guard.ok) return LSMGNN_E_DEVICE;
 
-  // the backing store must be pinned host memory the device can address
+  // without the pageable flag the backing store must be pinned host memory
+  // the device can address
   void *store_dev = nullptr;
-  if (hipHostGetDevicePointer(&store_dev, const_cast<void *>(cfg->host_store), 0) != hipSuccess || !store_dev) {
+  if (!pageable &&
+      (hipHostGetDevicePointer(&store_dev, const_cast<void *>(cfg->host_store), 0) != hipSuccess || !store_dev)) {
     (void)hipGetLastError();
     return LSMGNN_E_INVAL;
   }
@@ -516,7 +616,9 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   d.V = V;
   d.L = cfg->lookahead;
   d.T = cfg->near_threshold ? cfg->near_threshold : (cfg->lookahead / 8 > 1 ? cfg->lookahead / 8 : 1);
-  d.store = static_cast<const uint8_t *>(store_dev);
+  d.store = static_cast<const uint8_t *>(store_dev);  // null for a pageable store
+  c->pageable = pageable;
+  c->store_host = static_cast<const uint8_t *>(cfg->host_store);
   d.nchunks = (N + lsm::kChunkBytes - 1) / lsm::kChunkBytes;
   const uint64_t map_bytes = d.nchunks * lsm::kChunkBytes;
   const uint64_t B = cfg->max_batch;
@@ -541,20 +643,42 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
             host_alloc(c, &c->hc_adv, &c->hc_adv_dev, sizeof(Counters), true);
   for (Flight &f : c->fl) {
     f.sc = sc;
-    ok = ok && dev_alloc(c, &f.sc.gate, 1) && dev_alloc(c, &f.sc.host_list, B) && dev_alloc(c, &f.sc.host_src, B) &&
+    ok = ok && dev_alloc(c, &f.sc.gate, 1) &&
+         (pageable || (dev_alloc(c, &f.sc.host_list, B) && dev_alloc(c, &f.sc.host_src, B))) &&
          dev_alloc(c, &f.sc.hbm.src, B) && dev_alloc(c, &f.sc.hbm.dst, B) && dev_alloc(c, &f.sc.fill.src, B) &&
          dev_alloc(c, &f.sc.fill.dst, B) && dev_alloc(c, &f.sc.stage.src, B) && dev_alloc(c, &f.sc.stage.dst, B) &&
          (V == 0 || dev_alloc(c, &f.sc.staging, (B < V ? B : V) * R)) &&
          host_alloc(c, &f.hc, &f.hc_dev, sizeof(Counters), true);
+    if (ok && pageable) {
+      // the host reads the host-fetch list and fills the bounce rows
+      ok = host_alloc(c, &f.hlist_host, &f.sc.host_list, B * sizeof(uint32_t), false) &&
+           host_alloc(c, &f.hsrc_host, &f.sc.host_src, B * sizeof(uint64_t), false) &&
+           host_alloc(c, &f.bounce_host, &f.sc.bounce, B * R, false);
+    }
   }
   if (ok && V) ok = host_alloc(c, &c->ring_host, &d.ring_rows, V * R, false);
+  if (ok && pageable) {
+    const unsigned threads = cfg->host_threads ? cfg->host_threads : 8;
+    try {
+      c->pool = new lsm::HostPool(threads - 1);
+    } catch (...) {
+      c->pool = nullptr;
+    }
+    ok = c->pool != nullptr;
+  }
   if (!ok) {
     release(c);
     delete c;
     return LSMGNN_E_NOMEM;
   }
-  for (hipStream_t *s : {&c->meta, &c->host, &c->dma})
-    ok = ok && hipStreamCreateWithFlags(s, hipStreamNonBlocking) == hipSuccess;
+  {
+    StreamSet ss;
+    c->has_streams = acquire_streams(c->device, ss);
+    ok = ok && c->has_streams;
+    c->meta = ss.meta;
+    c->host = ss.host;
+    c->dma = ss.dma;
+  }
   for (hipEvent_t *e : {&c->ev_in, &c->ev_dedup, &c->ev_adv})
     ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
   for (Flight &f : c->fl)

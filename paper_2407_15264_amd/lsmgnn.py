@@ -33,7 +33,10 @@ class Config(ctypes.Structure):
     _fields_ = [("num_nodes", ctypes.c_uint64), ("row_bytes", ctypes.c_uint64), ("num_sets", ctypes.c_uint64),
                 ("victim_rows", ctypes.c_uint64), ("max_batch", ctypes.c_uint64), ("lookahead", ctypes.c_uint32),
                 ("near_threshold", ctypes.c_uint32), ("device", ctypes.c_int32), ("flags", ctypes.c_uint32),
-                ("host_store", ctypes.c_void_p), ("static_score", ctypes.c_void_p)]
+                ("host_threads", ctypes.c_uint32), ("host_store", ctypes.c_void_p), ("static_score", ctypes.c_void_p)]
+
+
+FLAG_PAGEABLE_STORE = 1
 
 
 class Counts(ctypes.Structure):
@@ -48,6 +51,7 @@ class Profile(ctypes.Structure):
                 ("enqueue_ms", ctypes.c_double), ("enqueue_launches", ctypes.c_uint64),
                 ("enqueue_rows", ctypes.c_uint64),
                 ("fill_ms", ctypes.c_double), ("fill_launches", ctypes.c_uint64), ("fill_rows", ctypes.c_uint64),
+                ("host_copy_ms", ctypes.c_double), ("host_copy_rows", ctypes.c_uint64),
                 ("gather_ms", ctypes.c_double), ("gathers", ctypes.c_uint64)]
 
 
@@ -186,12 +190,14 @@ class GatherResult:
 class FeatureCache:
     """GPU feature-gather cache on one device.
 
-    host_store: address of pinned host memory holding num_nodes * row_bytes
-    bytes (PinnedBuffer.ptr, or a pinned torch tensor's data_ptr()); it must
-    outlive the cache.  static_score: num_nodes unsigned scores."""
+    host_store: num_nodes * row_bytes bytes of host memory that must outlive
+    the cache: pinned (a PinnedBuffer, its ptr, or a pinned torch tensor), or
+    with pageable=True ordinary memory (a numpy array or an address), whose
+    rows the library's host threads (host_threads, 0 = 8) copy for the GPU.
+    static_score: num_nodes unsigned scores."""
 
     def __init__(self, num_nodes, row_bytes, host_store, static_score, num_sets, victim_rows, lookahead,
-                 max_batch, near_threshold=0, device=0):
+                 max_batch, near_threshold=0, device=0, pageable=False, host_threads=0):
         import torch
         self.device = torch.device("cuda", device)
         self.num_nodes, self.row_bytes = int(num_nodes), int(row_bytes)
@@ -201,10 +207,15 @@ class FeatureCache:
             host_store = host_store.ptr
         elif isinstance(host_store, torch.Tensor):
             host_store = host_store.data_ptr()
+        elif isinstance(host_store, np.ndarray):
+            if not host_store.flags.c_contiguous or host_store.nbytes < self.num_nodes * self.row_bytes:
+                raise ValueError("host_store array must be C-contiguous and hold num_nodes * row_bytes bytes")
+            self._store_ref = host_store
+            host_store = host_store.ctypes.data
         stat = np.ascontiguousarray(np.asarray(static_score), dtype=np.uint32)
         cfg = Config(self.num_nodes, self.row_bytes, self.num_sets, self.victim_rows, self.max_batch,
-                     self.lookahead, int(near_threshold), int(device), 0, ctypes.c_void_p(int(host_store)),
-                     ctypes.c_void_p(stat.ctypes.data))
+                     self.lookahead, int(near_threshold), int(device), FLAG_PAGEABLE_STORE if pageable else 0,
+                     int(host_threads), ctypes.c_void_p(int(host_store)), ctypes.c_void_p(stat.ctypes.data))
         h = ctypes.c_void_p()
         _check(lib().lsmgnn_cache_create(ctypes.byref(cfg), ctypes.byref(h)), "lsmgnn_cache_create")
         self._h = h

@@ -93,6 +93,77 @@ CONFIGS = {
 }
 
 
+@dataclasses.dataclass(frozen=True)
+class HeteroConfig:
+    """A typed graph: one homogeneous R-MAT graph over all nodes, each node given
+    a type by a seeded permutation (the first type_share[0] of the permuted
+    order is type 0, and so on; a node's local ID is its position within its
+    type), each type with its own feature width and its own cache.  The cache
+    and victim-ring budgets are split in proportion to each type's store bytes.
+    Edge types play no part in sampling."""
+    name: str
+    num_nodes: int
+    num_edges: int
+    type_share: tuple
+    dims: tuple
+    elt_bytes: int
+    batches: int
+    batch_size: int
+    fanout: tuple
+    cache_bytes: int
+    ring_bytes: int
+    lookahead: int
+    rmat: tuple = (0.57, 0.19, 0.19)
+    seed: int = 0
+
+    @property
+    def num_types(self) -> int:
+        return len(self.dims)
+
+    def type_counts(self) -> list:
+        c = [int(round(f * self.num_nodes)) for f in self.type_share[:-1]]
+        return c + [self.num_nodes - sum(c)]
+
+    def row_bytes(self, t: int) -> int:
+        return self.dims[t] * self.elt_bytes
+
+    def store_bytes(self, t: int) -> int:
+        return self.type_counts()[t] * self.row_bytes(t)
+
+    def cache_shape(self, t: int) -> CacheShape:
+        total = sum(self.store_bytes(k) for k in range(self.num_types))
+        share = self.store_bytes(t) / total
+        return CacheShape(num_sets=int(self.cache_bytes * share) // self.row_bytes(t) // 8,
+                          victim_rows=int(self.ring_bytes * share) // self.row_bytes(t),
+                          lookahead=self.lookahead)
+
+    def describe(self) -> dict:
+        return {
+            "workload": self.name,
+            "num_nodes": self.num_nodes,
+            "num_edges": self.num_edges,
+            "types": [{"nodes": n, "feature": f"fp32x{d}" if self.elt_bytes == 4 else f"fp16x{d}",
+                       "row_bytes": self.row_bytes(t), "num_sets": self.cache_shape(t).num_sets,
+                       "victim_rows": self.cache_shape(t).victim_rows}
+                      for t, (n, d) in enumerate(zip(self.type_counts(), self.dims))],
+            "batch_size": self.batch_size,
+            "fanout": list(self.fanout),
+            "ways": 8,
+            "lookahead": self.lookahead,
+        }
+
+
+# The heterogeneous workload shape: 4 node types (40/30/20/10 %), fp32 widths
+# 1024/768/256/128, caches totalling 32 GiB of HBM, rings totalling 16 GiB.
+HETERO = {
+    4: HeteroConfig("rmat-20M-e250M-4types", 20_000_000, 250_000_000, (0.4, 0.3, 0.2, 0.1), (1024, 768, 256, 128), 4,
+                    500, 8192, (10, 5, 5), 32 * GIB, 16 * GIB, 8),
+}
+
+# key offset of the node-type permutation (distinct from the seed-node permutation)
+TYPE_PERM_SEED = 0x54595045
+
+
 def build(verbose: bool = False) -> str:
     cmd = ["gcc", "-O3", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-Wall",
            os.path.join(HERE, "gen.c"), "-o", LIB_PATH + ".tmp", "-lm"]
@@ -211,6 +282,50 @@ class Workload:
         return int(np.diff(self.offsets).max()) if self.num_batches else 0
 
 
+class HeteroWorkload:
+    """Graph + request streams of a typed workload, split by node type.  The
+    raw request list of a minibatch (global IDs, as the sampler produced them)
+    is split into one list per type, in request order, of local IDs."""
+
+    def __init__(self, cfg: HeteroConfig, batches: int | None = None):
+        self.cfg = cfg
+        self.num_batches = cfg.batches if batches is None else batches
+        N = cfg.num_nodes
+        self.graph = rmat_graph(N, cfg.num_edges, cfg.rmat, cfg.seed)
+        self.seeds = seed_permutation(N, self.num_batches * cfg.batch_size, cfg.seed)
+        self.ids, self.offsets = sample_batches(self.graph, self.seeds, cfg.batch_size, cfg.fanout,
+                                                0, self.num_batches, cfg.seed)
+        perm = seed_permutation(N, N, cfg.seed + TYPE_PERM_SEED)
+        counts = cfg.type_counts()
+        self.type_offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
+        self.node_type = np.empty(N, np.uint8)
+        self.node_local = np.empty(N, np.int64)
+        self.static = []
+        for t in range(cfg.num_types):
+            nodes = perm[self.type_offsets[t]: self.type_offsets[t + 1]]
+            self.node_type[nodes] = t
+            self.node_local[nodes] = np.arange(nodes.size, dtype=np.int64)
+            self.static.append(np.ascontiguousarray(self.graph.indeg[nodes]))
+        del perm
+        self._split = {}
+
+    def batch(self, b: int, t: int) -> np.ndarray:
+        """Local IDs of type t in minibatch b, in request order."""
+        if b not in self._split:
+            g = self.ids[self.offsets[b]: self.offsets[b + 1]]
+            ty = self.node_type[g]
+            loc = self.node_local[g]
+            self._split = {b: [loc[ty == k] for k in range(self.cfg.num_types)]}
+        return self._split[b][t]
+
+    def type_batches(self, t: int) -> list:
+        out = []
+        for b in range(self.num_batches):
+            g = self.ids[self.offsets[b]: self.offsets[b + 1]]
+            out.append(self.node_local[g][self.node_type[g] == t])
+        return out
+
+
 def scaled_cache(cfg: WorkloadConfig) -> CacheShape:
     return cfg.cache
 
@@ -219,6 +334,6 @@ def near_threshold_default(lookahead: int) -> int:
     return max(1, lookahead // 8)
 
 
-__all__ = ["CONFIGS", "WorkloadConfig", "CacheShape", "Workload", "Graph", "rmat_graph",
+__all__ = ["CONFIGS", "HETERO", "HeteroConfig", "HeteroWorkload", "WorkloadConfig", "CacheShape", "Workload", "Graph", "rmat_graph",
            "seed_permutation", "sample_batches", "features", "fill_features", "build", "splitmix_at",
            "near_threshold_default", "math"]

@@ -27,24 +27,33 @@ def log(msg):
 
 
 class Store:
-    """A pinned host feature table (num_nodes x row_bytes)."""
+    """A host feature table (num_nodes x row_bytes): pinned (read by the GPU
+    directly), or with pinned=False ordinary pageable memory (rows copied by
+    the library's host threads)."""
 
-    def __init__(self, num_nodes, dim, elt_bytes=4, seed=0, fill=None):
+    def __init__(self, num_nodes, dim, elt_bytes=4, seed=0, fill=None, pinned=True):
         self.num_nodes, self.row_bytes = num_nodes, dim * elt_bytes
-        self.buf = lsmgnn.PinnedBuffer(num_nodes * self.row_bytes)
-        self.np = self.buf.numpy(np.uint8, (num_nodes, self.row_bytes))
+        self._alloc(pinned)
         if fill is None:
-            W.fill_features(self.buf.ptr, dim, elt_bytes, 0, num_nodes, seed)
+            W.fill_features(self.np.ctypes.data, dim, elt_bytes, 0, num_nodes, seed)
         else:
             self.np[:] = fill
 
+    def _alloc(self, pinned):
+        self.pinned = pinned
+        if pinned:
+            self.buf = lsmgnn.PinnedBuffer(self.num_nodes * self.row_bytes)
+            self.np = self.buf.numpy(np.uint8, (self.num_nodes, self.row_bytes))
+        else:
+            self.np = np.empty((self.num_nodes, self.row_bytes), np.uint8)
+            self.buf = self.np
+
     @classmethod
-    def random_bytes(cls, num_nodes, row_bytes, seed=0):
+    def random_bytes(cls, num_nodes, row_bytes, seed=0, pinned=True):
         rng = np.random.default_rng(seed)
         s = cls.__new__(cls)
         s.num_nodes, s.row_bytes = num_nodes, row_bytes
-        s.buf = lsmgnn.PinnedBuffer(num_nodes * row_bytes)
-        s.np = s.buf.numpy(np.uint8, (num_nodes, row_bytes))
+        s._alloc(pinned)
         s.np[:] = rng.integers(0, 256, (num_nodes, row_bytes), dtype=np.uint8)
         return s
 
@@ -74,7 +83,7 @@ def run_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, 
     mb = max_batch or max(1, max((len(b) for b in list(batches) + list(announce)), default=1))
     L = lookahead
     cache = lsmgnn.FeatureCache(store.num_nodes, store.row_bytes, store.buf, static, num_sets, victim_rows, L, mb,
-                                near_threshold=near_threshold, device=device)
+                                near_threshold=near_threshold, device=device, pageable=not store.pinned)
     orc = Oracle(store.num_nodes, store.row_bytes, static, num_sets, victim_rows, L,
                  near_threshold=near_threshold, store=store.np)
     dev_ann = [torch.as_tensor(np.asarray(a, np.int64)).to(dev) for a in announce]
@@ -129,43 +138,65 @@ def run_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, 
 def device_store(store: Store, device=0):
     """A device copy of the backing store, for checking gathered rows on the GPU."""
     import torch
-    t = torch.empty((store.num_nodes, store.row_bytes), dtype=torch.uint8, device=torch.device("cuda", device))
+    dev = torch.device("cuda", device)
+    if not store.pinned:
+        return torch.from_numpy(store.np).to(dev)
+    t = torch.empty((store.num_nodes, store.row_bytes), dtype=torch.uint8, device=dev)
     lsmgnn.copy_bytes(t.data_ptr(), store.buf.ptr, store.num_nodes * store.row_bytes)
     return t
 
 
-def run_async_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, rows="all", store_gpu=None,
-                     state_every=0, label="async", combined=True, near_threshold=0, device=0):
-    """The launch configuration of bench.py: lsmgnn_gather_async with the next
-    minibatch's announcement (combined=True; else a separate lsmgnn_advance),
-    two gathers in flight, three rotating output-buffer sets.  Each gather's
-    unique IDs, inverse, outcomes and rows are compared with the oracle once it
-    has been waited for; counters are compared as totals and the cache and ring
-    state every `state_every` gathers and at the end.  rows as in run_parity."""
-    import torch
-    dev = torch.device("cuda", device)
-    mb = max(1, max(len(b) for b in batches))
-    L = lookahead
-    cache = lsmgnn.FeatureCache(store.num_nodes, store.row_bytes, store.buf, static, num_sets, victim_rows, L, mb,
-                                near_threshold=near_threshold, device=device)
-    orc = Oracle(store.num_nodes, store.row_bytes, static, num_sets, victim_rows, L,
-                 near_threshold=near_threshold, store=store.np)
-    db = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in batches]
-    bufs = [(torch.empty(mb * store.row_bytes, dtype=torch.uint8, device=dev),
-             torch.empty(mb, dtype=torch.int64, device=dev), torch.empty(mb, dtype=torch.int64, device=dev),
-             torch.empty(mb, dtype=torch.uint8, device=dev)) for _ in range(3)]
-    for j in range(min(L + 1, len(batches))):
-        cache.advance(db[j])
-        orc.advance(batches[j])
-    pending = []
-    t0 = time.time()
+class _Lane:
+    """One cache driven in the launch configuration of bench.py
+    (lsmgnn_gather_async with the next minibatch's announcement, or a separate
+    lsmgnn_advance; two gathers in flight; three rotating output-buffer sets),
+    with its oracle beside it.  Each gather's unique IDs, inverse, outcomes and
+    rows are compared once it has been waited for."""
 
-    def check(ticket, r, b):
-        cache.wait(ticket)
+    def __init__(self, store, static, num_sets, victim_rows, lookahead, batches, rows, store_gpu, label,
+                 combined, near_threshold, device):
+        import torch
+        self.torch = torch
+        dev = torch.device("cuda", device)
+        self.mb = max(1, max(len(b) for b in batches))
+        self.L, self.batches, self.rows, self.store_gpu, self.label = lookahead, batches, rows, store_gpu, label
+        self.combined = combined
+        self.cache = lsmgnn.FeatureCache(store.num_nodes, store.row_bytes, store.buf, static, num_sets, victim_rows,
+                                         lookahead, self.mb, near_threshold=near_threshold, device=device,
+                                         pageable=not store.pinned)
+        self.orc = Oracle(store.num_nodes, store.row_bytes, static, num_sets, victim_rows, lookahead,
+                          near_threshold=near_threshold, store=store.np)
+        self.db = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in batches]
+        self.bufs = [(torch.empty(self.mb * store.row_bytes, dtype=torch.uint8, device=dev),
+                      torch.empty(self.mb, dtype=torch.int64, device=dev),
+                      torch.empty(self.mb, dtype=torch.int64, device=dev),
+                      torch.empty(self.mb, dtype=torch.uint8, device=dev)) for _ in range(3)]
+        for j in range(min(lookahead + 1, len(batches))):
+            self.cache.advance(self.db[j])
+            self.orc.advance(batches[j])
+        self.pending = []
+
+    def issue(self, b):
+        out, uq, inv, oc = self.bufs[b % 3]
+        L = self.L
+        nxt = self.db[b + L + 1] if b + L + 1 < len(self.batches) else None
+        if self.combined:
+            ticket, r = self.cache.gather_async(self.db[b], out, uq, inverse=inv, outcome=oc, announce=nxt)
+        else:
+            ticket, r = self.cache.gather_async(self.db[b], out, uq, inverse=inv, outcome=oc)
+            if nxt is not None:
+                self.cache.advance(nxt)
+        self.pending.append((ticket, r, b))
+
+    def check_oldest(self):
+        torch = self.torch
+        ticket, r, b = self.pending.pop(0)
+        self.cache.wait(ticket)
         torch.cuda.current_stream().synchronize()
-        where = f"{label} gather {b}"
+        where = f"{self.label} gather {b}"
+        rows = self.rows
         full_rows = rows == "all" or (isinstance(rows, int) and b % rows == 0)
-        o = orc.gather(np.asarray(batches[b], np.int64), rows=full_rows)
+        o = self.orc.gather(np.asarray(self.batches[b], np.int64), rows=full_rows)
         assert r.n_unique == o["uniq"].size, (where, r.n_unique, o["uniq"].size)
         if not np.array_equal(r.unique.cpu().numpy(), o["uniq"]):
             raise AssertionError(f"{where}: unique IDs differ")
@@ -178,40 +209,69 @@ def run_async_parity(store: Store, static, num_sets, victim_rows, lookahead, bat
         if full_rows:
             if not np.array_equal(r.out.cpu().numpy(), o["out"]):
                 raise AssertionError(f"{where}: gathered rows differ from the oracle's")
-        elif store_gpu is not None:
-            if not torch.equal(r.out, store_gpu.index_select(0, r.unique)):
+        elif self.store_gpu is not None:
+            if not torch.equal(r.out, self.store_gpu.index_select(0, r.unique)):
                 raise AssertionError(f"{where}: gathered rows differ from the backing store")
-        if b + L + 1 < len(batches):
-            orc.advance(batches[b + L + 1])
+        if b + self.L + 1 < len(self.batches):
+            self.orc.advance(self.batches[b + self.L + 1])
 
-    for b in range(len(batches)):
-        out, uq, inv, oc = bufs[b % 3]
-        nxt = db[b + L + 1] if b + L + 1 < len(batches) else None
-        if combined:
-            ticket, r = cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc, announce=nxt)
-        else:
-            ticket, r = cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc)
-            if nxt is not None:
-                cache.advance(nxt)
-        pending.append((ticket, r, b))
+    def drain(self):
+        while self.pending:
+            self.check_oldest()
+
+    def finish(self):
+        self.drain()
+        tot_gpu = self.cache.stats()[1]
+        tot_orc = self.orc.stats()[1]
+        for k in COUNT_KEYS:
+            assert tot_gpu[k] == tot_orc[k], (self.label, k, tot_gpu[k], tot_orc[k])
+        compare_state(self.cache, self.orc, f"{self.label} end")
+        self.cache.close()
+        self.orc.close()
+        return tot_gpu
+
+
+def _run_lanes(lanes, nb, state_every, label):
+    t0 = time.time()
+    for b in range(nb):
+        for ln in lanes:
+            ln.issue(b)
         if state_every and (b + 1) % state_every == 0:
             # the exported state is the one after every issued gather: drain first
-            while pending:
-                check(*pending.pop(0))
-            compare_state(cache, orc, f"{label} gather {b}")
+            for ln in lanes:
+                ln.drain()
+                compare_state(ln.cache, ln.orc, f"{ln.label} gather {b}")
             log(f"  {label}: {b + 1} gathers checked ({time.time() - t0:.1f} s)")
-        elif len(pending) == 2:
-            check(*pending.pop(0))
-    for p in pending:
-        check(*p)
-    tot_gpu = cache.stats()[1]
-    tot_orc = orc.stats()[1]
-    for k in COUNT_KEYS:
-        assert tot_gpu[k] == tot_orc[k], (label, k, tot_gpu[k], tot_orc[k])
-    compare_state(cache, orc, f"{label} end")
-    cache.close()
-    orc.close()
-    return dict(total=tot_gpu, seconds=time.time() - t0)
+        else:
+            for ln in lanes:
+                if len(ln.pending) == 2:
+                    ln.check_oldest()
+    totals = [ln.finish() for ln in lanes]
+    return totals, time.time() - t0
+
+
+def run_async_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, rows="all", store_gpu=None,
+                     state_every=0, label="async", combined=True, near_threshold=0, device=0):
+    """One cache in the launch configuration of bench.py, against the oracle:
+    unique IDs, inverse, outcomes and rows of every gather (rows as in
+    run_parity), counters as totals, the cache and ring state every
+    `state_every` gathers and at the end."""
+    ln = _Lane(store, static, num_sets, victim_rows, lookahead, batches, rows, store_gpu, label, combined,
+               near_threshold, device)
+    totals, seconds = _run_lanes([ln], len(batches), state_every, label)
+    return dict(total=totals[0], seconds=seconds)
+
+
+def run_typed_async_parity(stores, statics, shapes, type_batches, rows=50, stores_gpu=None, state_every=0,
+                           label="typed", device=0):
+    """A typed workload: one cache per node type, all driven together, minibatch
+    by minibatch (each type's gather of minibatch b is issued before any check
+    of minibatch b-1), each against its own oracle."""
+    lanes = [_Lane(stores[t], statics[t], shapes[t].num_sets, shapes[t].victim_rows, shapes[t].lookahead,
+                   type_batches[t], rows, None if stores_gpu is None else stores_gpu[t], f"{label} type {t}", True,
+                   shapes[t].near_threshold, device) for t in range(len(stores))]
+    totals, seconds = _run_lanes(lanes, len(type_batches[0]), state_every, label)
+    return dict(totals=totals, seconds=seconds)
 
 
 def config_stream(cfg, batches=None):

@@ -21,7 +21,7 @@ torch = pytest.importorskip("torch")
 from paper_2407_15264_amd import lsmgnn  # noqa: E402
 from paper_2407_15264_amd import workload as W  # noqa: E402
 from tests.parity_driver import (Store, compare_state, config_stream, device_store, log,  # noqa: E402
-                                 run_async_parity, run_parity)
+                                 run_async_parity, run_parity, run_typed_async_parity)
 from oracle.oracle import Oracle  # noqa: E402
 
 
@@ -79,6 +79,33 @@ def test_workload_rmat10m_full_size_pipelined_parity():
     tot = res["total"]
     log(f"  {cfg.name}: {tot} in {res['seconds']:.1f} s")
     assert tot["hits"] > 0 and tot["victim_hits"] > 0 and tot["misses"] > 0
+    del sg
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(2400)
+def test_workload_typed_20m_full_size_pipelined_parity():
+    """The typed 20M-node workload at full size: four node types with their own
+    feature widths, caches and rings (56 GB of pinned stores, 32 GiB of caches,
+    16 GiB of rings, 500 minibatches of 8192 seeds), one cache per type, all in
+    the bench's launch configuration.  Checks as for the 10M-node workload,
+    per type."""
+    cfg = W.HETERO[4]
+    log(f"case: {cfg.name}, all {cfg.batches} gathers per type, pipelined, full size")
+    t0 = time.time()
+    wl = W.HeteroWorkload(cfg)
+    type_batches = [wl.type_batches(t) for t in range(cfg.num_types)]
+    log(f"  workload generated in {time.time() - t0:.1f} s")
+    stores = [Store(n, d, cfg.elt_bytes, cfg.seed + 1 + t) for t, (n, d) in enumerate(zip(cfg.type_counts(), cfg.dims))]
+    sg = [device_store(st) for st in stores]
+    log(f"  stores filled and copied to the device ({time.time() - t0:.1f} s)")
+    shapes = [cfg.cache_shape(t) for t in range(cfg.num_types)]
+    res = run_typed_async_parity(stores, wl.static, shapes, type_batches, rows=50, stores_gpu=sg, state_every=100,
+                                 label=cfg.name)
+    for t, tot in enumerate(res["totals"]):
+        log(f"  {cfg.name} type {t}: {tot}")
+        assert tot["hits"] > 0 and tot["misses"] > 0
+    log(f"  {res['seconds']:.1f} s")
     del sg
     torch.cuda.empty_cache()
 
@@ -319,6 +346,41 @@ def test_long_streams_window_wrap(seed, pipelined):
     else:
         run_parity(store, stat, S, V, L, batches, near_threshold=T, rows="all", state_every=10,
                    label=f"long{seed}")
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_pageable_store_random(seed):
+    """The same policy with the backing store in ordinary pageable memory:
+    misses and victim hits are copied by host threads into the pinned bounce
+    buffer.  Odd seeds go through the pipelined entry point."""
+    n, S, V, L, T, rb, stat, batches, announce = _random_case(300 + seed)
+    log(f"case: pageable store, random seed {seed}: N={n} S={S} V={V} L={L} T={T}")
+    store = Store.random_bytes(n, rb, seed, pinned=False)
+    if seed % 2:
+        run_async_parity(store, stat, S, V, L, batches, rows="all", near_threshold=T, label=f"pageable{seed}")
+    else:
+        mb = max(1, max(len(b) for b in list(batches) + list(announce)))
+        run_parity(store, stat, S, V, L, batches, announce=announce, near_threshold=T, rows="all", max_batch=mb,
+                   label=f"pageable{seed}")
+
+
+def test_pageable_store_rmat14_pipelined():
+    cfg = W.CONFIGS[1]
+    log(f"case: pageable store, {cfg.name}, pipelined")
+    wl, batches = config_stream(cfg)
+    store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed, pinned=False)
+    res = run_async_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead,
+                           batches, rows="all", state_every=5, label=f"{cfg.name} pageable")
+    assert res["total"]["victim_hits"] > 0
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_pageable_store_long_streams(seed):
+    n, S, V, L, T, stat, batches = _long_case(40 + seed)
+    log(f"case: pageable store, long stream seed {seed}: N={n} S={S} V={V} L={L} T={T}")
+    store = Store.random_bytes(n, 64, seed, pinned=False)
+    run_async_parity(store, stat, S, V, L, batches, rows="all", near_threshold=T, label=f"pageable-long{seed}",
+                     state_every=10)
 
 
 def test_async_announce_errors_leave_state_unchanged():
