@@ -326,6 +326,24 @@ class HeteroWorkload:
         return out
 
 
+# Pinned host memory a process may hold is limited (64 GiB on the MI355X hosts
+# measured); the victim rings, the pinned stores and the bounce buffers of
+# pageable stores must fit together.
+PINNED_BUDGET = 52 * GIB
+
+
+def pin_plan(store_bytes, ring_bytes_total, budget=PINNED_BUDGET):
+    """Which stores to keep in pinned memory: the largest first, while the
+    rings and the pinned stores fit the budget; the rest stay pageable."""
+    pinned = [False] * len(store_bytes)
+    used = ring_bytes_total
+    for i in sorted(range(len(store_bytes)), key=lambda k: -store_bytes[k]):
+        if used + store_bytes[i] <= budget:
+            pinned[i] = True
+            used += store_bytes[i]
+    return pinned
+
+
 def scaled_cache(cfg: WorkloadConfig) -> CacheShape:
     return cfg.cache
 
@@ -336,4 +354,4 @@ def near_threshold_default(lookahead: int) -> int:
 
 __all__ = ["CONFIGS", "HETERO", "HeteroConfig", "HeteroWorkload", "WorkloadConfig", "CacheShape", "Workload", "Graph", "rmat_graph",
            "seed_permutation", "sample_batches", "features", "fill_features", "build", "splitmix_at",
-           "near_threshold_default", "math"]
+           "near_threshold_default", "pin_plan", "PINNED_BUDGET", "math"]

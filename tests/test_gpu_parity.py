@@ -96,10 +96,14 @@ def test_workload_typed_20m_full_size_pipelined_parity():
     wl = W.HeteroWorkload(cfg)
     type_batches = [wl.type_batches(t) for t in range(cfg.num_types)]
     log(f"  workload generated in {time.time() - t0:.1f} s")
-    stores = [Store(n, d, cfg.elt_bytes, cfg.seed + 1 + t) for t, (n, d) in enumerate(zip(cfg.type_counts(), cfg.dims))]
+    shapes = [cfg.cache_shape(t) for t in range(cfg.num_types)]
+    pinned = W.pin_plan([cfg.store_bytes(t) for t in range(cfg.num_types)],
+                        sum(sh.victim_rows * cfg.row_bytes(t) for t, sh in enumerate(shapes)))
+    log(f"  pinned stores: {pinned} (the others pageable)")
+    stores = [Store(n, d, cfg.elt_bytes, cfg.seed + 1 + t, pinned=pinned[t])
+              for t, (n, d) in enumerate(zip(cfg.type_counts(), cfg.dims))]
     sg = [device_store(st) for st in stores]
     log(f"  stores filled and copied to the device ({time.time() - t0:.1f} s)")
-    shapes = [cfg.cache_shape(t) for t in range(cfg.num_types)]
     res = run_typed_async_parity(stores, wl.static, shapes, type_batches, rows=50, stores_gpu=sg, state_every=100,
                                  label=cfg.name)
     for t, tot in enumerate(res["totals"]):
