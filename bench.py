@@ -176,7 +176,10 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     cfg = {**W.CONFIGS, **W.HETERO}[args.config]
     L = cfg.lookahead if isinstance(cfg, W.HeteroConfig) else cfg.cache.lookahead
-    nb = max(cfg.batches, args.warmup + args.steps + L + 1)
+    nb = args.warmup + args.steps + L + 1  # the minibatches the timed stream uses (a prefix of the configured run)
+    if nb > cfg.batches:
+        print(f"bench.py: {nb} minibatches needed, the workload has {cfg.batches}", file=sys.stderr)
+        sys.exit(2)
     t0 = time.perf_counter()
     parts, requests = make_parts(W, cfg, nb)
     log(f"[bench] workload {cfg.name}: {nb} minibatches generated in {time.perf_counter() - t0:.1f}s "

@@ -154,9 +154,11 @@ class _Lane:
     rows are compared once it has been waited for."""
 
     def __init__(self, store, static, num_sets, victim_rows, lookahead, batches, rows, store_gpu, label,
-                 combined, near_threshold, device):
+                 combined, near_threshold, device, row_sample=0):
         import torch
         self.torch = torch
+        self.store, self.row_sample = store, row_sample
+        self.rng = np.random.default_rng(12345)
         dev = torch.device("cuda", device)
         self.mb = max(1, max(len(b) for b in batches))
         self.L, self.batches, self.rows, self.store_gpu, self.label = lookahead, batches, rows, store_gpu, label
@@ -212,6 +214,13 @@ class _Lane:
         elif self.store_gpu is not None:
             if not torch.equal(r.out, self.store_gpu.index_select(0, r.unique)):
                 raise AssertionError(f"{where}: gathered rows differ from the backing store")
+        elif self.row_sample and r.n_unique:
+            # a seeded sample of the gathered rows against the host store
+            k = min(self.row_sample, r.n_unique)
+            u = np.sort(self.rng.choice(r.n_unique, size=k, replace=False))
+            got = r.out[torch.as_tensor(u, device=r.out.device)].cpu().numpy()
+            if not np.array_equal(got, self.store.np[o["uniq"][u]]):
+                raise AssertionError(f"{where}: sampled gathered rows differ from the backing store")
         if b + self.L + 1 < len(self.batches):
             self.orc.advance(self.batches[b + self.L + 1])
 
@@ -251,13 +260,13 @@ def _run_lanes(lanes, nb, state_every, label):
 
 
 def run_async_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, rows="all", store_gpu=None,
-                     state_every=0, label="async", combined=True, near_threshold=0, device=0):
+                     state_every=0, label="async", combined=True, near_threshold=0, device=0, row_sample=0):
     """One cache in the launch configuration of bench.py, against the oracle:
     unique IDs, inverse, outcomes and rows of every gather (rows as in
     run_parity), counters as totals, the cache and ring state every
     `state_every` gathers and at the end."""
     ln = _Lane(store, static, num_sets, victim_rows, lookahead, batches, rows, store_gpu, label, combined,
-               near_threshold, device)
+               near_threshold, device, row_sample)
     totals, seconds = _run_lanes([ln], len(batches), state_every, label)
     return dict(total=totals[0], seconds=seconds)
 
