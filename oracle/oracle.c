@@ -21,6 +21,12 @@
  *     oldest entry; lines in the far or near level are enqueued, others are
  *     dropped; a victim hit removes the entry and refills the line through the
  *     normal fill path; V > 0 turns on the swapped (PVP) level order.
+ * The other policies of the evaluation (Sec. 5) choose the victim among the
+ * full set's lines differently and keep everything else: static-only evicts
+ * the lowest static score; dynamic-only evicts the line whose next announced
+ * use is furthest away (no announced use first); round-robin evicts the way a
+ * per-set pointer names and then advances the pointer.  Ties go to the lowest
+ * way index in every policy.
  */
 #include "oracle.h"
 
@@ -39,7 +45,8 @@ typedef struct {
 
 struct orc_cache {
   uint64_t num_nodes, num_sets, victim_rows;
-  uint32_t row_bytes, ways, lookahead, near_thr;
+  uint32_t row_bytes, ways, lookahead, near_thr, policy;
+  uint32_t *rr;      /* [num_sets] round-robin pointer (next way to evict) */
   const unsigned char *store;
   uint32_t *stat;    /* static score per node (copied) */
   uint32_t *tag;     /* [num_sets][ways] */
@@ -87,11 +94,11 @@ static int contains(const ann_list *l, int64_t x) {
 
 int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const uint32_t *static_score,
                uint64_t num_sets, uint32_t ways, uint64_t victim_rows, uint32_t lookahead,
-               uint32_t near_threshold, orc_cache **out) {
+               uint32_t near_threshold, uint32_t policy, orc_cache **out) {
   if (!out || !static_score) return ORC_E_INVAL;
   *out = NULL;
   if (num_nodes == 0 || num_nodes > 0xffffffffULL || row_bytes == 0 || row_bytes % 16 != 0 ||
-      num_sets == 0 || num_sets > 0xffffffffULL || ways == 0 || lookahead > 31)
+      num_sets == 0 || num_sets > 0xffffffffULL || ways == 0 || lookahead > 31 || policy > ORC_POLICY_ROUND_ROBIN)
     return ORC_E_INVAL;
   orc_cache *c = (orc_cache *)calloc(1, sizeof(orc_cache));
   if (!c) return ORC_E_NOMEM;
@@ -101,6 +108,7 @@ int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const 
   c->row_bytes = row_bytes;
   c->ways = ways;
   c->lookahead = lookahead;
+  c->policy = policy;
   /* Sec. 4.2: the default threshold is one eighth of the window; at least 1 */
   c->near_thr = near_threshold ? near_threshold : (lookahead / 8 > 1 ? lookahead / 8 : 1);
   c->store = (const unsigned char *)store;
@@ -109,7 +117,8 @@ int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const 
   c->ins = (int64_t *)malloc(num_sets * ways * sizeof(int64_t));
   c->vtag = (uint32_t *)malloc((victim_rows ? victim_rows : 1) * sizeof(uint32_t));
   c->where = (int64_t *)malloc(num_nodes * sizeof(int64_t));
-  if (!c->stat || !c->tag || !c->ins || !c->vtag || !c->where) { orc_destroy(c); return ORC_E_NOMEM; }
+  c->rr = (uint32_t *)calloc(num_sets, sizeof(uint32_t));
+  if (!c->stat || !c->tag || !c->ins || !c->vtag || !c->where || !c->rr) { orc_destroy(c); return ORC_E_NOMEM; }
   memcpy(c->stat, static_score, num_nodes * sizeof(uint32_t));
   for (uint64_t i = 0; i < num_sets * ways; ++i) { c->tag[i] = EMPTY; c->ins[i] = -1; }
   for (uint64_t k = 0; k < victim_rows; ++k) c->vtag[k] = EMPTY;
@@ -122,7 +131,7 @@ void orc_destroy(orc_cache *c) {
   if (!c) return;
   for (uint64_t j = 0; j < c->n_ann; ++j) free(c->ann[j].ids);
   free(c->ann);
-  free(c->stat); free(c->tag); free(c->ins); free(c->vtag); free(c->where);
+  free(c->stat); free(c->tag); free(c->ins); free(c->vtag); free(c->where); free(c->rr);
   free(c);
 }
 
@@ -167,6 +176,17 @@ static int line_class(const orc_cache *c, uint64_t s, uint32_t w) {
       return d <= c->near_thr ? CLS_C : CLS_F;
   }
   return CLS_N;
+}
+
+/* Distance from the current gather to the next announced use of node x
+   (1..L), or 0 when none of the next L minibatches names it (Sec. 4.2, the
+   next reuse iteration). */
+static uint64_t reuse_distance(const orc_cache *c, uint32_t x) {
+  for (uint64_t d = 1; d <= c->lookahead; ++d) {
+    uint64_t j = c->t + d;
+    if (j < c->n_ann && contains(&c->ann[j], (int64_t)x)) return d;
+  }
+  return 0;
 }
 
 /* Eviction priority, lowest level evicted first.  Hybrid order (Sec. 4.2):
@@ -233,22 +253,44 @@ int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t 
         ++st.misses;
         if (outcome) outcome[u] = ORC_MISS;
       }
-      /* choose the way: an empty way first, else the lowest level, then the
-         lowest static score, then the lowest way index (Sec. 4.2) */
+      /* choose the way: an empty way first; in a full set the policy's
+         victim (Sec. 4.2 for the hybrid; Sec. 5 for the others) */
       uint32_t pick = c->ways;
       for (uint32_t w = 0; w < c->ways && pick == c->ways; ++w)
         if (tag[w] == EMPTY) pick = w;
       if (pick == c->ways) {
-        int best_lvl = 99;
-        uint32_t best_stat = 0;
-        for (uint32_t w = 0; w < c->ways; ++w) {
-          int lvl = level_of(c, line_class(c, s, w));
-          uint32_t sv = c->stat[tag[w]];
-          if (lvl < best_lvl || (lvl == best_lvl && sv < best_stat)) {
-            best_lvl = lvl;
-            best_stat = sv;
-            pick = w;
+        if (c->policy == ORC_POLICY_HYBRID) {
+          /* the lowest level, then the lowest static score, then the lowest way */
+          int best_lvl = 99;
+          uint32_t best_stat = 0;
+          for (uint32_t w = 0; w < c->ways; ++w) {
+            int lvl = level_of(c, line_class(c, s, w));
+            uint32_t sv = c->stat[tag[w]];
+            if (lvl < best_lvl || (lvl == best_lvl && sv < best_stat)) {
+              best_lvl = lvl;
+              best_stat = sv;
+              pick = w;
+            }
           }
+        } else if (c->policy == ORC_POLICY_STATIC) {
+          /* the lowest static score, then the lowest way */
+          for (uint32_t w = 0; w < c->ways; ++w)
+            if (pick == c->ways || c->stat[tag[w]] < c->stat[tag[pick]]) pick = w;
+        } else if (c->policy == ORC_POLICY_DYNAMIC) {
+          /* no announced use first, then the furthest next use, then the lowest way */
+          uint64_t best = 0;
+          for (uint32_t w = 0; w < c->ways; ++w) {
+            uint64_t d = reuse_distance(c, tag[w]);
+            uint64_t far = d ? d : c->lookahead + 1;
+            if (pick == c->ways || far > best) {
+              best = far;
+              pick = w;
+            }
+          }
+        } else {
+          /* round-robin: the way the set's pointer names; the pointer advances */
+          pick = c->rr[s];
+          c->rr[s] = (c->rr[s] + 1) % c->ways;
         }
         /* evict: a line with reuse information goes to the victim buffer,
            others are discarded (Sec. 4.3.1) */

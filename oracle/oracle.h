@@ -36,6 +36,11 @@ enum {
 /* per-unique outcome codes */
 enum { ORC_HIT = 0, ORC_VICTIM_HIT = 1, ORC_MISS = 2 };
 
+/* eviction policies compared in the paper's evaluation (Sec. 5, impact of the
+   cache eviction policy): hybrid (Sec. 4.2), static information only, dynamic
+   information only, round-robin */
+enum { ORC_POLICY_HYBRID = 0, ORC_POLICY_STATIC = 1, ORC_POLICY_DYNAMIC = 2, ORC_POLICY_ROUND_ROBIN = 3 };
+
 typedef struct orc_cache orc_cache;
 
 typedef struct {
@@ -48,7 +53,7 @@ uint64_t orc_set_of(uint64_t x, uint64_t num_sets);
 /* store may be NULL: gather then skips row copies (metadata-only runs) */
 int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const uint32_t *static_score,
                uint64_t num_sets, uint32_t ways, uint64_t victim_rows, uint32_t lookahead,
-               uint32_t near_threshold, orc_cache **out);
+               uint32_t near_threshold, uint32_t policy, orc_cache **out);
 void orc_destroy(orc_cache *c);
 int orc_advance(orc_cache *c, const int64_t *ids, uint64_t n);
 /* out (U rows), uniq (U), inv (n), outcome (U) may each be NULL */

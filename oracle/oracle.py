@@ -42,20 +42,28 @@ def build(verbose: bool = False) -> str:
     return LIB_PATH
 
 
+def stale() -> bool:
+    """True when liboracle.so is missing or older than its sources."""
+    if not os.path.exists(LIB_PATH):
+        return True
+    built = os.path.getmtime(LIB_PATH)
+    return any(os.path.getmtime(os.path.join(HERE, f)) > built for f in ("oracle.c", "oracle.h"))
+
+
 _lib = None
 
 
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
+        if stale():
             build()
         L = ctypes.CDLL(LIB_PATH)
         u64, u32, i32, vp = ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int, ctypes.c_void_p
         L.orc_set_of.restype = u64
         L.orc_set_of.argtypes = [u64, u64]
         L.orc_create.restype = i32
-        L.orc_create.argtypes = [u64, u32, vp, vp, u64, u32, u64, u32, u32, ctypes.POINTER(vp)]
+        L.orc_create.argtypes = [u64, u32, vp, vp, u64, u32, u64, u32, u32, u32, ctypes.POINTER(vp)]
         L.orc_destroy.restype = None
         L.orc_destroy.argtypes = [vp]
         L.orc_advance.restype = i32
@@ -80,12 +88,18 @@ def _ptr(a):
     return None if a is None else a.ctypes.data
 
 
+# eviction policies of the paper's evaluation (Sec. 5): hybrid (Sec. 4.2),
+# static information only, dynamic information only, round-robin
+POLICIES = {"hybrid": 0, "static": 1, "dynamic": 2, "round_robin": 3}
+
+
 class Oracle:
     """Sequential reference cache.  ``store`` is a (num_nodes, row_bytes) uint8
-    view of the backing feature table, or None for metadata-only runs."""
+    view of the backing feature table, or None for metadata-only runs.
+    ``policy`` is a name in POLICIES (or its number)."""
 
     def __init__(self, num_nodes, row_bytes, static_score, num_sets, victim_rows,
-                 lookahead, near_threshold=0, ways=8, store=None):
+                 lookahead, near_threshold=0, ways=8, store=None, policy="hybrid"):
         self.num_nodes = int(num_nodes)
         self.row_bytes = int(row_bytes)
         self.num_sets = int(num_sets)
@@ -98,7 +112,7 @@ class Oracle:
         h = ctypes.c_void_p()
         rc = lib().orc_create(self.num_nodes, self.row_bytes, _ptr(self.store), _ptr(self.static),
                               self.num_sets, self.ways, self.victim_rows, int(lookahead),
-                              int(near_threshold), ctypes.byref(h))
+                              int(near_threshold), POLICIES.get(policy, policy), ctypes.byref(h))
         if rc:
             raise OracleError(rc, "orc_create")
         self._h = h

@@ -17,10 +17,10 @@ def pytest_configure(config):
 
 @pytest.fixture(scope="session", autouse=True)
 def _host_libs():
-    """The oracle and the workload generators are plain C; build them if absent."""
+    """The oracle and the workload generators are plain C; build them if absent or stale."""
     from oracle import oracle
     from paper_2407_15264_amd import workload
-    if not os.path.exists(oracle.LIB_PATH):
+    if oracle.stale():
         oracle.build()
     if not os.path.exists(workload.LIB_PATH):
         workload.build()

@@ -15,7 +15,7 @@ NEAR, FAR, RECENT, NONE = "near", "far", "recent", "none"
 
 class NaiveCache:
     def __init__(self, num_nodes, num_sets, ways, victim_rows, lookahead, static, set_of,
-                 near_threshold=0):
+                 near_threshold=0, policy="hybrid"):
         self.N, self.S, self.W, self.V, self.L = num_nodes, num_sets, ways, victim_rows, lookahead
         self.T = near_threshold or max(1, lookahead // 8)
         self.static = list(static)
@@ -25,6 +25,8 @@ class NaiveCache:
         self.tail = 0
         self.announced = []
         self.t = 0
+        self.policy = policy
+        self.pointer = [0] * num_sets  # round-robin: next way to evict
 
     def advance(self, ids):
         if len(self.announced) > self.t + self.L:
@@ -71,9 +73,7 @@ class NaiveCache:
             if empties:
                 w = empties[0]
             else:
-                cands = sorted((self._level(self._class(e)), self.static[e[0]], w)
-                               for w, e in enumerate(ways))
-                w = cands[0][2]
+                w = self._victim(self.set_of(x), ways)
                 cls = self._class(ways[w])
                 st["evictions"] += 1
                 if self.V > 0 and cls in (FAR, NEAR):
@@ -85,6 +85,24 @@ class NaiveCache:
             ways[w] = (x, self.t)
         self.t += 1
         return "OK", dict(uniq=uniq, outcome="".join(outcome), **st)
+
+    def _next_use(self, node):
+        uses = [d for d in range(1, self.L + 1)
+                if self.t + d < len(self.announced) and node in self.announced[self.t + d]]
+        return min(uses) if uses else None
+
+    def _victim(self, s, ways):
+        if self.policy == "hybrid":
+            return sorted((self._level(self._class(e)), self.static[e[0]], w) for w, e in enumerate(ways))[0][2]
+        if self.policy == "static":
+            return sorted((self.static[e[0]], w) for w, e in enumerate(ways))[0][1]
+        if self.policy == "dynamic":
+            # no announced use counts as further than any announced one
+            far = [(self.L + 1 if self._next_use(e[0]) is None else self._next_use(e[0])) for e in ways]
+            return sorted((-f, w) for w, f in enumerate(far))[0][1]
+        w = self.pointer[s]
+        self.pointer[s] = (w + 1) % self.W
+        return w
 
     def tags(self):
         return [[-1 if e is None else e[0] for e in s] for s in self.sets]

@@ -226,9 +226,118 @@ def test_hits_never_exceed_belady(seed):
     assert sum(r["stats"]["hits"] for r in res) <= bound
 
 
+# ---------------------------------------------------- eviction policies
+# The evaluation's ablation (Sec. 5, impact of the cache eviction policy) swaps
+# only the choice of victim in a full set; these pins hold each alternative to
+# a closed form or to an exhaustive optimum.
+POLICY_NAMES = ["hybrid", "static", "dynamic", "round_robin"]
+
+
+@pytest.mark.parametrize("ways", [1, 2, 4, 8])
+@pytest.mark.parametrize("V", [0, 3])
+@pytest.mark.parametrize("one_batch", [False, True])
+def test_round_robin_closed_form(ways, V, one_batch):
+    # Round-robin ignores scores and reuse: the k-th distinct ID into a set
+    # goes to way k mod W, so way w ends up holding the largest such k.  With
+    # no window nothing has reuse information and every eviction is dropped.
+    n = 11
+    rng = np.random.default_rng(ways * 10 + V)
+    o = Oracle(n, 16, rng.integers(0, 9, n), 1, V, 0, ways=ways, policy="round_robin")
+    if one_batch:
+        res = [o.gather(rng.permutation(n), rows=False)]  # uniques are served in ascending order
+    else:
+        res = [o.gather(np.array([k]), rows=False) for k in range(n)]
+    st = o.export_state()
+    assert [int(t) for t in st["tags"][0]] == [max(k for k in range(n) if k % ways == w) for w in range(ways)]
+    assert sum(r["stats"]["evictions"] for r in res) == n - ways
+    assert sum(r["stats"]["dropped"] for r in res) == n - ways
+
+
+def test_round_robin_pointer_example():
+    # four ways, IDs 0..9 one per gather: ways hold 8, 9, 6, 7 and the next
+    # eviction (ID 10) replaces way 2
+    o = Oracle(16, 16, np.ones(16, np.uint32), 1, 0, 0, ways=4, policy="round_robin")
+    for k in range(10):
+        o.gather(np.array([k]), rows=False)
+    assert o.export_state()["tags"][0].tolist() == [8, 9, 6, 7]
+    o.gather(np.array([10]), rows=False)
+    assert o.export_state()["tags"][0].tolist() == [8, 9, 10, 7]
+
+
+@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("ways", [1, 2, 3, 5])
+def test_static_only_keeps_newest_and_best_scores(seed, ways):
+    # Static-only evicts the lowest score in the full set whatever the window
+    # says, so after distinct IDs x_1..x_m arrive one per gather the set holds
+    # x_m and the W - 1 highest-scored of x_1..x_{m-1}.
+    rng = np.random.default_rng(seed)
+    n, m, L = 30, 17, 4
+    stat = rng.permutation(n).astype(np.uint32)
+    seq = rng.permutation(n)[:m]
+    announce = [rng.integers(0, n, 5) for _ in range(m + L)]
+    o = Oracle(n, 16, stat, 1, 2, L, ways=ways, policy="static")
+    _drive(o, [np.array([x]) for x in seq], L, announce)
+    keep = {int(seq[-1])} | set(sorted(seq[:-1].tolist(), key=lambda x: -int(stat[x]))[:ways - 1])
+    assert set(o.export_state()["tags"][0].tolist()) == keep
+
+
+def _min_demand_misses(seq, ways):
+    """Fewest misses any policy that must insert every missed ID can reach on
+    one fully associative set, by exhaustive search over the evictions."""
+    import functools
+
+    @functools.lru_cache(maxsize=None)
+    def best(i, cache):
+        if i == len(seq):
+            return 0
+        x = seq[i]
+        if x in cache:
+            return best(i + 1, cache)
+        if len(cache) < ways:
+            return 1 + best(i + 1, cache | {x})
+        return 1 + min(best(i + 1, (cache - {y}) | {x}) for y in cache)
+
+    return best(0, frozenset())
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_dynamic_only_with_full_window_is_optimal(seed):
+    # With one ID per gather and a window covering the whole stream, evicting
+    # the line whose next use is furthest (unused lines first) is Belady's
+    # rule, optimal among policies that insert every miss.
+    rng = np.random.default_rng(500 + seed)
+    n, ways = int(rng.integers(3, 7)), int(rng.integers(1, 4))
+    seq = rng.integers(0, n, int(rng.integers(4, 13))).tolist()
+    L = len(seq)
+    o = Oracle(n, 16, rng.integers(0, 4, n), 1, 0, L, ways=ways, policy="dynamic")
+    res = _drive(o, [np.array([x]) for x in seq], L)
+    assert sum(r["stats"]["misses"] for r in res) == _min_demand_misses(tuple(seq), ways)
+
+
+@pytest.mark.parametrize("policy", POLICY_NAMES)
+@pytest.mark.parametrize("seed", range(3))
+def test_policies_never_exceed_belady(policy, seed):
+    rng = np.random.default_rng(seed)
+    n, S, ways_ = 40, 3, 8
+    batches = [rng.integers(0, n, rng.integers(5, 30)) for _ in range(15)]
+    o = Oracle(n, 16, rng.integers(0, 4, n), S, 0, 3, policy=policy)
+    res = _drive(o, batches, 3)
+    per_set = {s: [] for s in range(S)}
+    for ids in batches:
+        for x in np.unique(ids):
+            per_set[set_of(int(x), S)].append(int(x))
+    assert sum(r["stats"]["hits"] for r in res) <= sum(_belady_hits(q, ways_) for q in per_set.values())
+
+
+def test_policy_rejected_when_unknown():
+    with pytest.raises(OracleError) as e:
+        Oracle(10, 16, np.ones(10, np.uint32), 2, 2, 1, policy=4)
+    assert e.value.status == "E_INVAL"
+
+
 # ------------------------------------------------------- naive brute force
-def _naive_run(n, S, ways, V, L, T, stat, batches, announce):
-    m = NaiveCache(n, S, ways, V, L, stat, lambda x: set_of(x, S), T)
+def _naive_run(n, S, ways, V, L, T, stat, batches, announce, policy="hybrid"):
+    m = NaiveCache(n, S, ways, V, L, stat, lambda x: set_of(x, S), T, policy=policy)
     out = []
     for j in range(min(L + 1, len(announce))):
         assert m.advance(announce[j]) == "OK"
@@ -240,9 +349,9 @@ def _naive_run(n, S, ways, V, L, T, stat, batches, announce):
     return m, out
 
 
-def _compare(n, S, ways, V, L, T, stat, batches, announce):
-    m, exp = _naive_run(n, S, ways, V, L, T, stat, batches, announce)
-    o = Oracle(n, 16, stat, S, V, L, near_threshold=T, ways=ways)
+def _compare(n, S, ways, V, L, T, stat, batches, announce, policy="hybrid"):
+    m, exp = _naive_run(n, S, ways, V, L, T, stat, batches, announce, policy)
+    o = Oracle(n, 16, stat, S, V, L, near_threshold=T, ways=ways, policy=policy)
     got = _drive(o, batches, L, announce)
     for e, g in zip(exp, got):
         assert "".join(CODE[c] for c in g["outcome"]) == e["outcome"]
@@ -254,7 +363,8 @@ def _compare(n, S, ways, V, L, T, stat, batches, announce):
     assert st["ring_tail"] == m.tail
 
 
-def test_exhaustive_tiny_universe_against_naive_model():
+@pytest.mark.parametrize("policy", POLICY_NAMES)
+def test_exhaustive_tiny_universe_against_naive_model(policy):
     n = 3
     subsets = [np.array(c, np.int64) for r in range(n + 1) for c in itertools.combinations(range(n), r)]
     stat = np.array([2, 1, 2], np.uint32)
@@ -263,13 +373,14 @@ def test_exhaustive_tiny_universe_against_naive_model():
         for L in (1, 2):
             for seq in itertools.product(range(len(subsets)), repeat=4):
                 batches = [subsets[i] for i in seq]
-                _compare(n, 1, 2, V, L, 0, stat, batches, batches)
+                _compare(n, 1, 2, V, L, 0, stat, batches, batches, policy)
                 count += 1
     assert count == 4 * len(subsets) ** 4
 
 
-@pytest.mark.parametrize("seed", range(300))
-def test_random_small_against_naive_model(seed):
+@pytest.mark.parametrize("policy", POLICY_NAMES)
+@pytest.mark.parametrize("seed", range(150))
+def test_random_small_against_naive_model(seed, policy):
     rng = np.random.default_rng(1000 + seed)
     n = int(rng.integers(2, 14))
     S = int(rng.integers(1, 4))
@@ -285,7 +396,7 @@ def test_random_small_against_naive_model(seed):
         announce = [rng.integers(0, n, rng.integers(0, 8)) for _ in range(nb + L)]
     else:
         announce = batches
-    _compare(n, S, ways, V, L, T, stat, batches, announce)
+    _compare(n, S, ways, V, L, T, stat, batches, announce, policy)
 
 
 # ------------------------------------------------------------------- errors
