@@ -854,7 +854,7 @@ __global__ __launch_bounds__(kBlock) void k_host_fetch(const DevState d, Scratch
 #define LSM_HOST_GRID 32
 #endif
 #ifndef LSM_HBM_GRID
-#define LSM_HBM_GRID 2048
+#define LSM_HBM_GRID 4096  // the HBM-side copies: a grid sweep beside the host fetch chose it
 #endif
 
 template <CopyMode M>
