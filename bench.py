@@ -115,15 +115,16 @@ def make_parts(W, cfg, nb):
     return parts, requests
 
 
-def cpu_baseline(parts, budget_s):
+def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None):
     """The CPU oracle (single-threaded C, one instance per part) on the same
     stream from gather 0, stopped after about budget_s seconds."""
     from oracle.oracle import Oracle
     orcs = []
     for p in parts:
         sh = p["shape"]
-        o = Oracle(p["num_nodes"], p["R"], p["static"], sh.num_sets, sh.victim_rows, sh.lookahead,
-                   near_threshold=sh.near_threshold, store=p["store_np"])
+        o = Oracle(p["num_nodes"], p["R"], p["static"], sh.num_sets,
+                   sh.victim_rows if victim_rows is None else victim_rows, sh.lookahead,
+                   near_threshold=sh.near_threshold, store=p["store_np"], policy=policy)
         for j in range(sh.lookahead + 1):
             o.advance(p["batches"][j])
         orcs.append(o)
@@ -159,6 +160,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--host-threads", type=int, default=16,
                     help="host threads copying rows for a store kept in pageable memory")
+    ap.add_argument("--policy", default="hybrid", choices=["hybrid", "static", "dynamic", "round_robin"],
+                    help="eviction policy: the method's hybrid order or one of the evaluation's alternatives")
+    ap.add_argument("--no-ring", action="store_true", help="no victim ring (and so no PVP level swap)")
     ap.add_argument("--sync", action="store_true",
                     help="blocking lsmgnn_gather per minibatch instead of the pipelined lsmgnn_gather_async")
     args = ap.parse_args()
@@ -176,10 +180,13 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     cfg = {**W.CONFIGS, **W.HETERO}[args.config]
     L = cfg.lookahead if isinstance(cfg, W.HeteroConfig) else cfg.cache.lookahead
-    nb = args.warmup + args.steps + L + 1  # the minibatches the timed stream uses (a prefix of the configured run)
-    if nb > cfg.batches:
-        print(f"bench.py: {nb} minibatches needed, the workload has {cfg.batches}", file=sys.stderr)
+    if args.warmup + args.steps > cfg.batches:
+        print(f"bench.py: {args.warmup + args.steps} minibatches needed, the workload has {cfg.batches}",
+              file=sys.stderr)
         sys.exit(2)
+    # the minibatches the timed stream gathers or announces (a prefix of the
+    # configured run); near the run's end the last gathers announce nothing
+    nb = min(cfg.batches, args.warmup + args.steps + L + 1)
     t0 = time.perf_counter()
     parts, requests = make_parts(W, cfg, nb)
     log(f"[bench] workload {cfg.name}: {nb} minibatches generated in {time.perf_counter() - t0:.1f}s "
@@ -214,8 +221,9 @@ def main():
         p["dev_batches"] = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in p["batches"]]
         mb = max(1, max(b.size for b in p["batches"]))
         p["cache"] = lsmgnn.FeatureCache(p["num_nodes"], p["R"], p["store"], p["static"], sh.num_sets,
-                                         sh.victim_rows, sh.lookahead, mb, near_threshold=sh.near_threshold,
-                                         pageable=not p["pinned"], host_threads=args.host_threads)
+                                         0 if args.no_ring else sh.victim_rows, sh.lookahead, mb,
+                                         near_threshold=sh.near_threshold, pageable=not p["pinned"],
+                                         host_threads=args.host_threads, policy=args.policy)
         # three output sets rotate: at most two gathers are in flight
         p["bufs"] = [(torch.empty(mb * p["R"], dtype=torch.uint8, device=dev),
                       torch.empty(mb, dtype=torch.int64, device=dev),
@@ -231,9 +239,11 @@ def main():
             out, uniq, inv = p["bufs"][b % 3]
             if args.sync:
                 r = c.gather(db[b], out=out, unique=uniq, inverse=inv)
-                c.advance(db[b + L + 1])
+                if b + L + 1 < nb:
+                    c.advance(db[b + L + 1])
             else:  # gather minibatch b and announce minibatch b+L+1 in one call
-                p["tickets"][b], r = c.gather_async(db[b], out, uniq, inverse=inv, announce=db[b + L + 1])
+                p["tickets"][b], r = c.gather_async(db[b], out, uniq, inverse=inv,
+                                                    announce=db[b + L + 1] if b + L + 1 < nb else None)
             nbytes += r.n_unique * p["R"]
         if not args.sync:
             for p in parts:
@@ -322,7 +332,8 @@ def main():
         "warmup": args.warmup, "ms_per_step": 1e3 * dt / args.steps, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
         "config": dict(cfg.describe(), feature_dtype="fp32" if cfg.elt_bytes == 4 else "fp16",
-                       minibatches_timed=args.steps,
+                       minibatches_timed=args.steps, policy=args.policy,
+                       victim_ring="off" if args.no_ring else "on",
                        first_timed_minibatch=args.warmup,
                        api=("lsmgnn_gather + lsmgnn_advance" if args.sync
                             else "lsmgnn_gather_async with announcement (two minibatches in flight)")),
@@ -341,7 +352,7 @@ def main():
         "ceilings": ceil,
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(parts, args.cpu_budget)
+        res["cpu_baseline"] = cpu_baseline(parts, args.cpu_budget, args.policy, 0 if args.no_ring else None)
         res["cpu_baseline"]["gpu_over_cpu"] = gbps / res["cpu_baseline"]["value"]
     for p in parts:
         p["cache"].close()

@@ -66,6 +66,19 @@ enum { LSMGNN_HIT = 0, LSMGNN_VICTIM_HIT = 1, LSMGNN_MISS = 2 };
 /* lsmgnn_config.flags */
 #define LSMGNN_FLAG_PAGEABLE_STORE 1u /* host_store is ordinary (pageable) host memory */
 
+/* lsmgnn_config.policy: how a full set chooses the line to evict.  The hybrid
+   order is the method's (Sec. 4.2, with the level swap of Sec. 4.3.2 when the
+   victim ring is on); the other three are the alternatives its evaluation
+   compares against (Sec. 5, impact of the cache eviction policy).  Only the
+   choice changes: empty ways are taken first (lowest index), an evicted line
+   goes to the victim ring iff its next announced use lies within the window
+   and it was not inserted by the current gather, and ties go to the lowest
+   way index. */
+#define LSMGNN_POLICY_HYBRID 0u      /* lowest level, then lowest static score */
+#define LSMGNN_POLICY_STATIC 1u      /* lowest static score */
+#define LSMGNN_POLICY_DYNAMIC 2u     /* no announced use, else the furthest next use */
+#define LSMGNN_POLICY_ROUND_ROBIN 3u /* a per-set pointer (from way 0) that advances by one per eviction */
+
 typedef struct {
   uint64_t num_nodes;   /* IDs are int64 in [0, num_nodes); 1 <= num_nodes <= 2^32 - 1 */
   uint64_t row_bytes;   /* bytes per feature row; a positive multiple of 16 */
@@ -77,6 +90,7 @@ typedef struct {
   int32_t device;       /* HIP device ordinal */
   uint32_t flags;       /* 0 or LSMGNN_FLAG_PAGEABLE_STORE; other bits must be 0 */
   uint32_t host_threads; /* pageable store: host threads copying rows (0 selects 8) */
+  uint32_t policy;      /* LSMGNN_POLICY_*; other values are rejected */
   /* Backing store: num_nodes * row_bytes bytes of host memory, row v at offset
      v * row_bytes.  Borrowed: the caller keeps it alive and unchanged while
      the cache exists; the library only reads it.

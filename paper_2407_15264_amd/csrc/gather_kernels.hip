@@ -393,6 +393,13 @@ __device__ __forceinline__ uint32_t class_from_bits(uint32_t m, uint32_t t, uint
   return (uint32_t)__builtin_ctz(rel) + 1u <= T ? kClsNear : kClsFar;
 }
 
+// Distance from gather t to the line's next announced use (1..L), or 0 when
+// none of the next L minibatches names it.
+__device__ __forceinline__ uint32_t dist_from_bits(uint32_t m, uint32_t t, uint32_t L) {
+  const uint32_t rel = __builtin_amdgcn_alignbit(m, m, (t + 1u) & 31u) & ((1u << L) - 1u);
+  return rel ? (uint32_t)__builtin_ctz(rel) + 1u : 0u;
+}
+
 // eviction level, lowest evicted first: none < far < recent < near, or with
 // the victim ring on, far < none < recent < near
 __device__ __forceinline__ uint32_t level_of(uint32_t cls, bool ring_on) {
@@ -414,7 +421,11 @@ __device__ __forceinline__ uint64_t group_min(uint64_t v) {
 // One set per group of 8 lanes, lane w owning way w.  The group walks the
 // set's IDs in ascending order (the per-set order of the definition); each
 // step is a ballot for the tag probe, a ballot for an empty way, and on a full
-// set a 3-step shuffle minimum of (level, static score, way).
+// set the policy's victim: for the hybrid order (Sec. 4.2) a 3-step shuffle
+// minimum of (level, static score, way); for the evaluation's ablations
+// (Sec. 5) the minimum of (static score, way), of (no announced use first,
+// then the furthest next use; way), or the set's round-robin pointer.
+template <int P>
 __global__ __launch_bounds__(kBlock) void k_set_walk(const DevState d, Scratch sc, uint32_t t, Counters *cn) {
   if (cn->err) return;
   const uint32_t Tn = cn->n_touched;
@@ -432,8 +443,11 @@ __global__ __launch_bounds__(kBlock) void k_set_walk(const DevState d, Scratch s
     const uint32_t k = d.set_count[s];
     SetRec *rec = d.sets + s;
     uint32_t tag = rec->tag[w], st = rec->stat[w], ins = rec->ins[w];
-    uint32_t cls = kClsNone, lvl = 0;
-    bool known = false;  // class of this way for this gather computed
+    uint32_t cls = kClsNone, lvl = 0, dist = 0;
+    bool known = false;  // class (and next-use distance) of this way for this gather computed
+    uint32_t rr = 0;     // round-robin pointer (the record holds its complement)
+    if constexpr (P == kPolicyRoundRobin) rr = ~rec->rr_inv & (kWays - 1);
+    const uint32_t rr0 = rr;
     int32_t last = -1;   // unique index of this way's last fill
     bool dirty = false;
     uint32_t pu = 0, px = 0, ps = 0;  // entry (j & ~7) + w of the segment, loaded 8 at a time
@@ -464,12 +478,22 @@ __global__ __launch_bounds__(kBlock) void k_set_walk(const DevState d, Scratch s
         pick = (uint32_t)__builtin_ctz(emptym);
       } else {
         if (!known) {  // batch-start resident: class from its announced-use bits
-          cls = (ins == t) ? kClsRecent : class_from_bits(d.mask[tag], t, d.L, d.T);
+          const uint32_t m = d.mask[tag];
+          cls = (ins == t) ? kClsRecent : class_from_bits(m, t, d.L, d.T);
           lvl = level_of(cls, ring_on);
+          if constexpr (P == kPolicyDynamic) dist = dist_from_bits(m, t, d.L);
           known = true;
         }
-        const uint64_t key = ((uint64_t)lvl << 35) | ((uint64_t)st << 3) | w;
-        pick = (uint32_t)(group_min(key) & 7u);
+        if constexpr (P == kPolicyHybrid) {
+          pick = (uint32_t)(group_min(((uint64_t)lvl << 35) | ((uint64_t)st << 3) | w) & 7u);
+        } else if constexpr (P == kPolicyStatic) {
+          pick = (uint32_t)(group_min(((uint64_t)st << 3) | w) & 7u);
+        } else if constexpr (P == kPolicyDynamic) {
+          pick = (uint32_t)(group_min((uint64_t)((dist ? 32u - dist : 0u) << 3) | w) & 7u);
+        } else {
+          pick = rr;
+          rr = (rr + 1u) & (kWays - 1);
+        }
         z = __shfl(tag, (int)pick, kWays);
         const uint32_t pc = __shfl(cls, (int)pick, kWays);
         if (lead) {
@@ -495,6 +519,7 @@ __global__ __launch_bounds__(kBlock) void k_set_walk(const DevState d, Scratch s
         ins = t;
         cls = kClsRecent;
         lvl = recent_lvl;
+        if constexpr (P == kPolicyDynamic) dist = dist_from_bits(d.mask[x], t, d.L);
         known = true;
         last = (int32_t)u;
       }
@@ -508,6 +533,8 @@ __global__ __launch_bounds__(kBlock) void k_set_walk(const DevState d, Scratch s
       rec->stat[w] = st;
       rec->ins[w] = ins;
     }
+    if constexpr (P == kPolicyRoundRobin)
+      if (lead && rr != rr0) rec->rr_inv = ~rr;
     if (lead) d.set_count[s] = 0;
   }
   block_count(c_hit, sc.stat_part, kStHits);
@@ -521,7 +548,19 @@ __global__ __launch_bounds__(kBlock) void k_set_walk(const DevState d, Scratch s
 void launch_set_walk(const DevState &d, uint64_t n, uint32_t t, Scratch &sc, Counters *cn, StatGrids &grids,
                      hipStream_t s) {
   const unsigned g = grid_for(n * kWays, kBlock, 1024);
-  hipLaunchKernelGGL(k_set_walk, dim3(g), dim3(kBlock), 0, s, d, sc, t, cn);
+  switch (d.policy) {
+    case kPolicyStatic:
+      hipLaunchKernelGGL(k_set_walk<kPolicyStatic>, dim3(g), dim3(kBlock), 0, s, d, sc, t, cn);
+      break;
+    case kPolicyDynamic:
+      hipLaunchKernelGGL(k_set_walk<kPolicyDynamic>, dim3(g), dim3(kBlock), 0, s, d, sc, t, cn);
+      break;
+    case kPolicyRoundRobin:
+      hipLaunchKernelGGL(k_set_walk<kPolicyRoundRobin>, dim3(g), dim3(kBlock), 0, s, d, sc, t, cn);
+      break;
+    default:
+      hipLaunchKernelGGL(k_set_walk<kPolicyHybrid>, dim3(g), dim3(kBlock), 0, s, d, sc, t, cn);
+  }
   for (int st = kStHits; st <= kStFinal; ++st) grids.g[st] = g;
 }
 

@@ -29,13 +29,19 @@ constexpr uint64_t kSrcRing = 2ull << 62;   // victim-ring row (pinned host)
 constexpr uint64_t kSrcIndex = (1ull << 62) - 1;
 
 // One set = one 128-byte record (one L2 line): the 8 resident node IDs, their
-// static scores and the gather index at which each was inserted.
+// static scores, the gather index at which each was inserted, and (round-robin
+// policy only) the complement of the next way to evict, so that the all-ones
+// initial record means way 0.
 struct alignas(128) SetRec {
   uint32_t tag[kWays];
   uint32_t stat[kWays];
   uint32_t ins[kWays];
-  uint32_t pad[kWays];
+  uint32_t rr_inv;
+  uint32_t pad[kWays - 1];
 };
+
+// eviction policies (values of lsmgnn_config.policy)
+enum : uint32_t { kPolicyHybrid = 0, kPolicyStatic = 1, kPolicyDynamic = 2, kPolicyRoundRobin = 3 };
 static_assert(sizeof(SetRec) == 128, "set record must be one 128-byte line");
 
 // Per-block partial counts: each block of a counting kernel stores its sums
@@ -149,6 +155,7 @@ struct DevState {
   uint64_t N, R, S, V;
   uint64_t nchunks;
   uint32_t L, T;
+  uint32_t policy;
 };
 
 enum class CopyMode { kHbmToOut, kHostToOut, kCacheToStage, kOutToCache };

@@ -577,7 +577,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   const uint64_t N = cfg->num_nodes, R = cfg->row_bytes, S = cfg->num_sets, V = cfg->victim_rows;
   if (N == 0 || N > 0xffffffffull || R == 0 || R % 16 != 0 || S == 0 || S > (0xffffffffull / lsm::kWays) ||
       cfg->lookahead > 31 || cfg->max_batch == 0 || cfg->max_batch > (1ull << 31) ||
-      (cfg->flags & ~LSMGNN_FLAG_PAGEABLE_STORE) != 0 || cfg->host_threads > 256 ||
+      (cfg->flags & ~LSMGNN_FLAG_PAGEABLE_STORE) != 0 || cfg->host_threads > 256 || cfg->policy > LSMGNN_POLICY_ROUND_ROBIN ||
       V > (1ull << 40))
     return LSMGNN_E_INVAL;
   // byte sizes must not overflow 64 bits
@@ -616,6 +616,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   d.V = V;
   d.L = cfg->lookahead;
   d.T = cfg->near_threshold ? cfg->near_threshold : (cfg->lookahead / 8 > 1 ? cfg->lookahead / 8 : 1);
+  d.policy = cfg->policy;
   d.store = static_cast<const uint8_t *>(store_dev);  // null for a pageable store
   c->pageable = pageable;
   c->store_host = static_cast<const uint8_t *>(cfg->host_store);

@@ -460,3 +460,56 @@ def test_async_announce_errors_leave_state_unchanged():
     assert e.value.status == "E_WINDOW"
     compare_state(cache, orc, "after empty announcement")
     cache.close()
+
+
+# ---------------------------------------------- the evaluation's ablations
+POLICIES = ["static", "dynamic", "round_robin"]
+
+
+@pytest.mark.parametrize("policy", POLICIES)
+@pytest.mark.parametrize("seed", range(10))
+def test_policies_random_small_caches(seed, policy):
+    """The alternative eviction policies (static score only, next announced use
+    only, round-robin) on randomized small caches, blocking entry point."""
+    n, S, V, L, T, rb, stat, batches, announce = _random_case(700 + seed)
+    log(f"case: policy {policy} random seed {seed}: N={n} S={S} V={V} L={L} T={T} R={rb}")
+    store = Store.random_bytes(n, rb, seed)
+    run_parity(store, stat, S, V, L, batches, announce, near_threshold=T, rows="all", label=f"{policy}{seed}",
+               policy=policy)
+
+
+@pytest.mark.parametrize("policy", POLICIES)
+@pytest.mark.parametrize("seed", range(3))
+def test_policies_long_streams_pipelined(seed, policy):
+    """90 minibatches through the pipelined entry point, so the announced-use
+    bits wrap their 32-bit word (the dynamic policy's distances come from
+    them) and the round-robin pointers go round many times."""
+    n, S, V, L, T, stat, batches = _long_case(40 + seed)
+    log(f"case: policy {policy} long stream seed {seed}: N={n} S={S} V={V} L={L} T={T}")
+    store = Store.random_bytes(n, 32, seed)
+    run_async_parity(store, stat, S, V, L, batches, rows="all", near_threshold=T, label=f"{policy}-long{seed}",
+                     state_every=10, policy=policy)
+
+
+@pytest.mark.parametrize("policy", POLICIES)
+@pytest.mark.parametrize("name", ["one_set", "batch_exceeds_cache", "no_window", "big_batch"])
+def test_policies_adversarial(name, policy):
+    c = _adversarial()[name]
+    log(f"case: policy {policy} adversarial {name}: N={c['n']} S={c['S']} V={c['V']} L={c['L']}")
+    rb = 64 if c["n"] < (1 << 21) else 16
+    store = Store.random_bytes(c["n"], rb, 1)
+    stat = np.random.default_rng(3).integers(0, 5, c["n"]).astype(np.uint32)
+    mb = max(1, max(len(b) for b in c["batches"]))
+    run_parity(store, stat, c["S"], c["V"], c["L"], c["batches"], rows="all", max_batch=mb,
+               label=f"{policy}-{name}", policy=policy)
+
+
+@pytest.mark.parametrize("policy", POLICIES)
+def test_policies_workload_rmat14_pipelined(policy):
+    cfg = W.CONFIGS[1]
+    log(f"case: policy {policy} {cfg.name} pipelined")
+    wl, batches = config_stream(cfg)
+    store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
+    res = run_async_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead,
+                           batches, rows="all", state_every=25, label=f"{policy}-{cfg.name}", policy=policy)
+    log(f"  {policy}: {res['total']}")

@@ -57,16 +57,16 @@ def test_set_index_helper_matches_oracle(L):
 
 @pytest.mark.parametrize("bad", [dict(num_sets=0), dict(row_bytes=24), dict(lookahead=32), dict(max_batch=0),
                                  dict(num_nodes=0), dict(num_nodes=1 << 32), dict(flags=2), dict(flags=1 << 31),
-                                 dict(flags=1, host_threads=257)])
+                                 dict(flags=1, host_threads=257), dict(policy=4), dict(policy=1 << 31)])
 def test_bad_config_rejected_before_device(L, bad):
     stat = np.ones(16, np.uint32)
     store = np.zeros(16 * 16, np.uint8)
     kw = dict(num_nodes=16, row_bytes=16, num_sets=2, victim_rows=2, max_batch=8, lookahead=1, near_threshold=0,
-              device=0, flags=0, host_threads=0)
+              device=0, flags=0, host_threads=0, policy=0)
     kw.update(bad)
     cfg = lsmgnn.Config(kw["num_nodes"], kw["row_bytes"], kw["num_sets"], kw["victim_rows"], kw["max_batch"],
                         kw["lookahead"], kw["near_threshold"], kw["device"], kw["flags"], kw["host_threads"],
-                        ctypes.c_void_p(store.ctypes.data), ctypes.c_void_p(stat.ctypes.data))
+                        kw["policy"], ctypes.c_void_p(store.ctypes.data), ctypes.c_void_p(stat.ctypes.data))
     h = ctypes.c_void_p()
     assert L.lsmgnn_cache_create(ctypes.byref(cfg), ctypes.byref(h)) == lsmgnn.E_INVAL
     assert not h.value
@@ -78,3 +78,26 @@ def test_null_arguments(L):
     assert L.lsmgnn_gather(None, None, 0, None, None, None, None, None, None) == lsmgnn.E_INVAL
     assert L.lsmgnn_advance(None, None, 0, None) == lsmgnn.E_INVAL
     assert L.lsmgnn_stats(None, None, None) == lsmgnn.E_INVAL
+
+
+def test_struct_layouts_match_header(tmp_path):
+    # The ctypes mirrors must place every field where a C compiler does.
+    import subprocess
+    structs = {"lsmgnn_config": lsmgnn.Config, "lsmgnn_counts": lsmgnn.Counts, "lsmgnn_profile": lsmgnn.Profile}
+    lines = ["#include <stddef.h>", "#include <stdio.h>", '#include "lsmgnn.h"', "int main(void) {"]
+    for name, cls in structs.items():
+        lines.append(f'  printf("{name} %zu\\n", sizeof({name}));')
+        for f, _ in cls._fields_:
+            lines.append(f'  printf("{name}.{f} %zu\\n", offsetof({name}, {f}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    subprocess.run(["gcc", "-std=c11", "-I", inc, str(src), "-o", str(exe)], check=True)
+    got = dict(line.split() for line in subprocess.run([str(exe)], check=True, capture_output=True,
+                                                       text=True).stdout.splitlines())
+    for name, cls in structs.items():
+        assert int(got[name]) == ctypes.sizeof(cls), name
+        for f, _ in cls._fields_:
+            assert int(got[f"{name}.{f}"]) == getattr(cls, f).offset, f"{name}.{f}"
