@@ -62,6 +62,13 @@ int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t 
 int orc_stats(const orc_cache *c, orc_counts *last, orc_counts *total);
 /* tags: num_sets*ways entries, ring_tags: victim_rows entries (either may be NULL) */
 int orc_export_state(const orc_cache *c, uint32_t *tags, uint32_t *ring_tags, uint64_t *ring_tail, uint64_t *t);
+
+/* Static score (pagerank.c): K power iterations of the PageRank of the walk
+   along CSR entries (offsets[N+1], adj[offsets[N]]) with damping d, from the
+   uniform vector, dangling mass spread uniformly; rank[N] receives it.
+   orc_rank_scores: floor(rank / max rank * (2^32 - 1)). */
+int orc_pagerank(uint64_t N, const int64_t *offsets, const uint32_t *adj, double d, uint32_t K, double *rank);
+int orc_rank_scores(uint64_t N, const double *rank, uint32_t *score);
 uint32_t orc_near_threshold(const orc_cache *c);
 
 #ifdef __cplusplus

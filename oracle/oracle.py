@@ -36,7 +36,7 @@ class _Stats(ctypes.Structure):
 def build(verbose: bool = False) -> str:
     """Compile liboracle.so (plain C, -O2, single-threaded)."""
     cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Wextra",
-           os.path.join(HERE, "oracle.c"), "-o", LIB_PATH + ".tmp"]
+           os.path.join(HERE, "oracle.c"), os.path.join(HERE, "pagerank.c"), "-lm", "-o", LIB_PATH + ".tmp"]
     subprocess.run(cmd, check=True, capture_output=not verbose)
     os.replace(LIB_PATH + ".tmp", LIB_PATH)
     return LIB_PATH
@@ -47,7 +47,7 @@ def stale() -> bool:
     if not os.path.exists(LIB_PATH):
         return True
     built = os.path.getmtime(LIB_PATH)
-    return any(os.path.getmtime(os.path.join(HERE, f)) > built for f in ("oracle.c", "oracle.h"))
+    return any(os.path.getmtime(os.path.join(HERE, f)) > built for f in ("oracle.c", "pagerank.c", "oracle.h"))
 
 
 _lib = None
@@ -64,6 +64,10 @@ def lib():
         L.orc_set_of.argtypes = [u64, u64]
         L.orc_create.restype = i32
         L.orc_create.argtypes = [u64, u32, vp, vp, u64, u32, u64, u32, u32, u32, ctypes.POINTER(vp)]
+        L.orc_pagerank.restype = i32
+        L.orc_pagerank.argtypes = [u64, vp, vp, ctypes.c_double, u32, vp]
+        L.orc_rank_scores.restype = i32
+        L.orc_rank_scores.argtypes = [u64, vp, vp]
         L.orc_destroy.restype = None
         L.orc_destroy.argtypes = [vp]
         L.orc_advance.restype = i32
@@ -170,3 +174,27 @@ class Oracle:
             raise OracleError(rc, "orc_export_state")
         return dict(tags=tags.reshape(self.num_sets, self.ways),
                     ring_tags=ring[:self.victim_rows], ring_tail=tail.value, t=t.value)
+
+
+def pagerank(offsets, adj, damping=0.85, iterations=20):
+    """Reverse-PageRank ranks (float64, one per node) of a CSR graph whose node u
+    lists the neighbours it samples; see pagerank.c for the definition."""
+    offsets = np.ascontiguousarray(offsets, np.int64)
+    adj = np.ascontiguousarray(adj, np.uint32)
+    n = offsets.size - 1
+    rank = np.empty(max(n, 1), np.float64)
+    rc = lib().orc_pagerank(n, _ptr(offsets), _ptr(adj) if adj.size else None, float(damping), int(iterations),
+                            _ptr(rank))
+    if rc:
+        raise OracleError(rc, "orc_pagerank")
+    return rank[:n]
+
+
+def rank_scores(rank):
+    """32-bit static scores: floor(rank / max rank * (2^32 - 1))."""
+    rank = np.ascontiguousarray(rank, np.float64)
+    out = np.empty(max(rank.size, 1), np.uint32)
+    rc = lib().orc_rank_scores(rank.size, _ptr(rank), _ptr(out))
+    if rc:
+        raise OracleError(rc, "orc_rank_scores")
+    return out[:rank.size]
