@@ -108,7 +108,8 @@ def make_parts(W, cfg, nb):
     else:
         wl = W.Workload(cfg, nb)
         parts = [dict(label="all", num_nodes=cfg.num_nodes, dim=cfg.dim, elt=cfg.elt_bytes, seed=cfg.seed,
-                      static=wl.static, shape=cfg.cache, batches=[wl.batch(b) for b in range(nb)])]
+                      static=wl.static, shape=cfg.cache, batches=[wl.batch(b) for b in range(nb)],
+                      graph=wl.graph)]
         requests = float(wl.ids.size) / nb
     for p in parts:
         p["R"] = p["dim"] * p["elt"]
@@ -193,6 +194,8 @@ def main():
     ap.add_argument("--policy", default="hybrid", choices=["hybrid", "static", "dynamic", "round_robin"],
                     help="eviction policy: the method's hybrid order or one of the evaluation's alternatives")
     ap.add_argument("--no-ring", action="store_true", help="no victim ring (and so no PVP level swap)")
+    ap.add_argument("--static", default="indegree", choices=["indegree", "pagerank"],
+                    help="static score: the in-degree, or the reverse PageRank computed on the GPU")
     ap.add_argument("--sync", action="store_true",
                     help="blocking lsmgnn_gather per minibatch instead of the pipelined lsmgnn_gather_async")
     args = ap.parse_args()
@@ -217,6 +220,9 @@ def main():
     # the minibatches the timed stream gathers or announces (a prefix of the
     # configured run); near the run's end the last gathers announce nothing
     nb = min(cfg.batches, args.warmup + args.steps + L + 1)
+    if args.static == "pagerank" and isinstance(cfg, W.HeteroConfig):
+        print("bench.py: --static pagerank is for the homogeneous workloads", file=sys.stderr)
+        sys.exit(2)
     t0 = time.perf_counter()
     parts, requests = make_parts(W, cfg, nb)
     log(f"[bench] workload {cfg.name}: {nb} minibatches generated in {time.perf_counter() - t0:.1f}s "
@@ -246,6 +252,22 @@ def main():
     log(f"[bench] ceilings: {json.dumps({k: round(v, 1) for k, v in ceil.items()})}")
 
     dev = torch.device("cuda", 0)
+    static_info = {"kind": "in-degree"}
+    if args.static == "pagerank":
+        g = parts[0]["graph"]
+        off_t = torch.as_tensor(g.offsets).to(dev)
+        adj_t = torch.as_tensor(g.adj.view(np.int32)).to(dev)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        sc = lsmgnn.pagerank_scores(off_t, adj_t, 0.85, 20)
+        torch.cuda.synchronize()
+        static_info = {"kind": "reverse PageRank (d = 0.85, 20 iterations) on the GPU",
+                       "ms": 1e3 * (time.perf_counter() - t0)}
+        parts[0]["static"] = sc.cpu().numpy().view(np.uint32).copy()
+        del off_t, adj_t, sc
+        log(f"[bench] reverse-PageRank static scores in {static_info['ms']:.1f} ms")
+    for p in parts:
+        p.pop("graph", None)
     for p in parts:
         sh = p["shape"]
         p["dev_batches"] = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in p["batches"]]
@@ -364,7 +386,7 @@ def main():
         "warmup": args.warmup, "ms_per_step": 1e3 * dt / args.steps, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
         "config": dict(cfg.describe(), feature_dtype="fp32" if cfg.elt_bytes == 4 else "fp16",
-                       minibatches_timed=args.steps, policy=args.policy,
+                       minibatches_timed=args.steps, policy=args.policy, static_score=static_info,
                        victim_ring="off" if args.no_ring else "on",
                        first_timed_minibatch=args.warmup,
                        api=("lsmgnn_gather + lsmgnn_advance" if args.sync

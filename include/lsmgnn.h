@@ -216,6 +216,31 @@ void lsmgnn_host_free(void *ptr);
    `stream`. */
 lsmgnn_status lsmgnn_copy_bytes(void *dst, const void *src, uint64_t bytes, void *stream);
 
+/* Static score from the graph: the normalized reverse PageRank that Sec. 4.2
+   names as the hybrid policy's static information (and the evaluation's static
+   policy uses, Sec. 5), as an alternative to the in-degree.
+   offsets (num_nodes + 1 int64) and adj (offsets[num_nodes] uint32, may be
+   NULL when there are no entries): the sampling adjacency in CSR form, node u
+   listing the neighbours it samples; DEVICE memory on `device`, read only.
+   The walk moves to a uniformly chosen CSR entry of the current node with
+   probability `damping` (a repeated entry counts each time) and jumps to a
+   uniformly chosen node otherwise; a node without entries always jumps.
+   `iterations` power iterations start from the uniform vector.
+   scores (num_nodes uint32, device): floor(rank / max rank * (2^32 - 1)).
+   rank (num_nodes double, device) receives the ranks, or may be NULL.
+   Ranks agree with a sequential evaluation to rounding (the per-node sums are
+   accumulated with atomics in varying order), so a score may differ by one
+   where its rank lies within rounding of a quantization step.
+   Work memory of 4 bytes per entry plus 24 bytes per node is allocated and
+   freed inside; the call is ordered after the work queued on `stream` and
+   returns once the scores are written.
+   Errors: E_INVAL (num_nodes 0 or above 2^32 - 1, damping outside [0, 1), NULL
+   offsets/scores, or NULL adj with entries); E_RANGE (offsets not starting at 0
+   or decreasing, or an entry >= num_nodes; nothing written); E_NOMEM; E_DEVICE. */
+lsmgnn_status lsmgnn_pagerank_scores(const int64_t *offsets, const uint32_t *adj, uint64_t num_nodes,
+                                     double damping, uint32_t iterations, uint32_t *scores, double *rank,
+                                     int device, void *stream);
+
 /* Set index the cache uses for node x (host-side helper, for tests). */
 uint64_t lsmgnn_set_of(uint64_t x, uint64_t num_sets);
 

@@ -7,11 +7,12 @@ import subprocess
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB_PATH = os.path.join(PKG, "liblsmgnn.so")
-SOURCES = [os.path.join(PKG, "csrc", f) for f in ("gather_kernels.hip", "runtime.hip")]
+SOURCES = [os.path.join(PKG, "csrc", f) for f in ("gather_kernels.hip", "runtime.hip", "pagerank.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-# packed-FP32 instructions are disabled: the library does no float math, and
-# the option keeps the compiler from ever emitting them.
+# packed-FP32 instructions are disabled: the library's only float math is the
+# float64 static-score pass, and the option keeps the compiler from ever
+# emitting them.
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I" + os.path.join(ROOT, "include"), "-I" + os.path.join(PKG, "csrc")]

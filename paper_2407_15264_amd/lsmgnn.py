@@ -102,6 +102,8 @@ def lib():
         L.lsmgnn_set_of.argtypes = [u64, u64]
         L.lsmgnn_copy_bytes.restype = i32
         L.lsmgnn_copy_bytes.argtypes = [vp, vp, u64, vp]
+        L.lsmgnn_pagerank_scores.restype = i32
+        L.lsmgnn_pagerank_scores.argtypes = [vp, vp, u64, ctypes.c_double, ctypes.c_uint32, vp, vp, i32, vp]
         L.lsmgnn_strerror.restype = ctypes.c_char_p
         L.lsmgnn_strerror.argtypes = [i32]
         _lib = L
@@ -121,6 +123,25 @@ def copy_bytes(dst_ptr: int, src_ptr: int, nbytes: int, stream=None, device=0):
     """Calibration copy (device or pinned host pointers), synchronous."""
     _check(lib().lsmgnn_copy_bytes(ctypes.c_void_p(dst_ptr), ctypes.c_void_p(src_ptr), int(nbytes),
                                    _stream_handle(stream, device)), "lsmgnn_copy_bytes")
+
+
+def pagerank_scores(offsets, adj, damping=0.85, iterations=20, rank=False, device=0, stream=None):
+    """Reverse-PageRank static scores (lsmgnn_pagerank_scores) of a CSR graph
+    given as device tensors (offsets int64 [N+1], adj int32/uint32 [E]).
+    Returns a device uint32-valued int32 tensor of scores (viewed as uint32 by
+    callers through .cpu().numpy().view(np.uint32)), and the float64 ranks
+    when rank=True."""
+    import torch
+    dev = torch.device("cuda", device)
+    n = offsets.numel() - 1
+    scores = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+    rk = torch.empty(max(n, 1), dtype=torch.float64, device=dev) if rank else None
+    _check(lib().lsmgnn_pagerank_scores(ctypes.c_void_p(offsets.data_ptr()),
+                                        ctypes.c_void_p(adj.data_ptr()) if adj.numel() else None, n,
+                                        float(damping), int(iterations), ctypes.c_void_p(scores.data_ptr()),
+                                        ctypes.c_void_p(rk.data_ptr()) if rank else None, int(device),
+                                        _stream_handle(stream, device)), "lsmgnn_pagerank_scores")
+    return (scores[:n], rk[:n]) if rank else scores[:n]
 
 
 class PinnedBuffer:
