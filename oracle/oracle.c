@@ -21,6 +21,13 @@
  *     oldest entry; lines in the far or near level are enqueued, others are
  *     dropped; a victim hit removes the entry and refills the line through the
  *     normal fill path; V > 0 turns on the swapped (PVP) level order.
+ * The victim buffer may instead take the form of Sec. 4.3.1's per-iteration
+ * queues (victim_mode ORC_VICTIM_QUEUES): queue j holds lines evicted with
+ * next reuse iteration j, at most C = V / (L + 1) of them in eviction order
+ * (a line finding its queue full is dropped); while minibatch t is gathered,
+ * a requested node that queue t holds is a victim hit (its row having been
+ * prefetched, Sec. 4.3), and after the gather queue t is emptied.  Queues are
+ * kept in L + 1 slots, slot j mod (L + 1).
  * The other policies of the evaluation (Sec. 5) choose the victim among the
  * full set's lines differently and keep everything else: static-only evicts
  * the lowest static score; dynamic-only evicts the line whose next announced
@@ -45,13 +52,16 @@ typedef struct {
 
 struct orc_cache {
   uint64_t num_nodes, num_sets, victim_rows;
-  uint32_t row_bytes, ways, lookahead, near_thr, policy;
+  uint32_t row_bytes, ways, lookahead, near_thr, policy, vmode;
+  uint64_t qcap, nslots; /* queue mode: rows per queue, queue slots */
+  uint64_t *qcnt;        /* [nslots] entries in each queue */
+  uint32_t *qbits;       /* [num_nodes] bit k: the node has an entry in slot k */
   uint32_t *rr;      /* [num_sets] round-robin pointer (next way to evict) */
   const unsigned char *store;
   uint32_t *stat;    /* static score per node (copied) */
   uint32_t *tag;     /* [num_sets][ways] */
   int64_t *ins;      /* [num_sets][ways] gather index at insertion */
-  uint32_t *vtag;    /* [victim_rows] */
+  uint32_t *vtag;    /* [victim_rows] ring entries, or queue slot k's entries at k * qcap */
   int64_t *where;    /* [num_nodes] ring slot holding the node, or -1 */
   uint64_t tail;     /* total enqueues ever */
   ann_list *ann;     /* announced batches, index j */
@@ -94,12 +104,15 @@ static int contains(const ann_list *l, int64_t x) {
 
 int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const uint32_t *static_score,
                uint64_t num_sets, uint32_t ways, uint64_t victim_rows, uint32_t lookahead,
-               uint32_t near_threshold, uint32_t policy, orc_cache **out) {
+               uint32_t near_threshold, uint32_t policy, uint32_t victim_mode, orc_cache **out) {
   if (!out || !static_score) return ORC_E_INVAL;
   *out = NULL;
   if (num_nodes == 0 || num_nodes > 0xffffffffULL || row_bytes == 0 || row_bytes % 16 != 0 ||
-      num_sets == 0 || num_sets > 0xffffffffULL || ways == 0 || lookahead > 31 || policy > ORC_POLICY_ROUND_ROBIN)
+      num_sets == 0 || num_sets > 0xffffffffULL || ways == 0 || lookahead > 31 || policy > ORC_POLICY_ROUND_ROBIN ||
+      victim_mode > ORC_VICTIM_QUEUES)
     return ORC_E_INVAL;
+  /* queue mode needs room for at least one entry per queue */
+  if (victim_mode == ORC_VICTIM_QUEUES && victim_rows && victim_rows < (uint64_t)lookahead + 1) return ORC_E_INVAL;
   orc_cache *c = (orc_cache *)calloc(1, sizeof(orc_cache));
   if (!c) return ORC_E_NOMEM;
   c->num_nodes = num_nodes;
@@ -109,6 +122,9 @@ int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const 
   c->ways = ways;
   c->lookahead = lookahead;
   c->policy = policy;
+  c->vmode = victim_mode;
+  c->nslots = (uint64_t)lookahead + 1;
+  c->qcap = victim_mode == ORC_VICTIM_QUEUES ? victim_rows / c->nslots : 0;
   /* Sec. 4.2: the default threshold is one eighth of the window; at least 1 */
   c->near_thr = near_threshold ? near_threshold : (lookahead / 8 > 1 ? lookahead / 8 : 1);
   c->store = (const unsigned char *)store;
@@ -118,7 +134,12 @@ int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const 
   c->vtag = (uint32_t *)malloc((victim_rows ? victim_rows : 1) * sizeof(uint32_t));
   c->where = (int64_t *)malloc(num_nodes * sizeof(int64_t));
   c->rr = (uint32_t *)calloc(num_sets, sizeof(uint32_t));
-  if (!c->stat || !c->tag || !c->ins || !c->vtag || !c->where || !c->rr) { orc_destroy(c); return ORC_E_NOMEM; }
+  c->qcnt = (uint64_t *)calloc(c->nslots, sizeof(uint64_t));
+  c->qbits = (uint32_t *)calloc(num_nodes, sizeof(uint32_t));
+  if (!c->stat || !c->tag || !c->ins || !c->vtag || !c->where || !c->rr || !c->qcnt || !c->qbits) {
+    orc_destroy(c);
+    return ORC_E_NOMEM;
+  }
   memcpy(c->stat, static_score, num_nodes * sizeof(uint32_t));
   for (uint64_t i = 0; i < num_sets * ways; ++i) { c->tag[i] = EMPTY; c->ins[i] = -1; }
   for (uint64_t k = 0; k < victim_rows; ++k) c->vtag[k] = EMPTY;
@@ -132,6 +153,7 @@ void orc_destroy(orc_cache *c) {
   for (uint64_t j = 0; j < c->n_ann; ++j) free(c->ann[j].ids);
   free(c->ann);
   free(c->stat); free(c->tag); free(c->ins); free(c->vtag); free(c->where); free(c->rr);
+  free(c->qcnt); free(c->qbits);
   free(c);
 }
 
@@ -244,8 +266,12 @@ int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t 
       ++st.hits;
       if (outcome) outcome[u] = ORC_HIT;
     } else {
-      /* the victim buffer is probed for the line before storage (Sec. 4.3) */
-      if (c->victim_rows && c->where[x] >= 0) {
+      /* the victim buffer is probed for the line before storage (Sec. 4.3);
+         in queue mode only the current iteration's queue holds rows */
+      if (c->vmode == ORC_VICTIM_QUEUES && c->qcap && ((c->qbits[x] >> (c->t % c->nslots)) & 1u)) {
+        ++st.victim_hits;
+        if (outcome) outcome[u] = ORC_VICTIM_HIT;
+      } else if (c->vmode == ORC_VICTIM_FIFO && c->victim_rows && c->where[x] >= 0) {
         ++st.victim_hits;
         ring_put(c, (uint64_t)c->where[x], EMPTY);
         if (outcome) outcome[u] = ORC_VICTIM_HIT;
@@ -297,7 +323,19 @@ int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t 
         uint32_t z = tag[pick];
         int cls = line_class(c, s, pick);
         ++st.evictions;
-        if (c->victim_rows && (cls == CLS_F || cls == CLS_C)) {
+        if (c->vmode == ORC_VICTIM_QUEUES && c->qcap && (cls == CLS_F || cls == CLS_C)) {
+          /* the queue of the line's next reuse iteration, unless it is full */
+          uint64_t slot = (c->t + reuse_distance(c, z)) % c->nslots;
+          if (c->qcnt[slot] < c->qcap) {
+            c->vtag[slot * c->qcap + c->qcnt[slot]] = z;
+            ++c->qcnt[slot];
+            c->qbits[z] |= 1u << slot;
+            ++c->tail;
+            ++st.enqueued;
+          } else {
+            ++st.dropped;
+          }
+        } else if (c->vmode == ORC_VICTIM_FIFO && c->victim_rows && (cls == CLS_F || cls == CLS_C)) {
           ring_put(c, c->tail % c->victim_rows, z);
           ++c->tail;
           ++st.enqueued;
@@ -322,6 +360,15 @@ int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t 
   free(uniq);
   if (n_unique) *n_unique = U;
 
+  /* queue mode: the current iteration's queue has been served */
+  if (c->vmode == ORC_VICTIM_QUEUES && c->qcap) {
+    uint64_t slot = c->t % c->nslots;
+    for (uint64_t p = 0; p < c->qcnt[slot]; ++p) {
+      c->qbits[c->vtag[slot * c->qcap + p]] &= ~(1u << slot);
+      c->vtag[slot * c->qcap + p] = EMPTY;
+    }
+    c->qcnt[slot] = 0;
+  }
   /* lists of minibatches up to t are never consulted again */
   if (c->t < c->n_ann) {
     free(c->ann[c->t].ids);

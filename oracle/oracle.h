@@ -41,6 +41,10 @@ enum { ORC_HIT = 0, ORC_VICTIM_HIT = 1, ORC_MISS = 2 };
    information only, round-robin */
 enum { ORC_POLICY_HYBRID = 0, ORC_POLICY_STATIC = 1, ORC_POLICY_DYNAMIC = 2, ORC_POLICY_ROUND_ROBIN = 3 };
 
+/* victim buffer forms: one FIFO ring, or per-reuse-iteration queues with
+   prefetch (Sec. 4.3.1) */
+enum { ORC_VICTIM_FIFO = 0, ORC_VICTIM_QUEUES = 1 };
+
 typedef struct orc_cache orc_cache;
 
 typedef struct {
@@ -53,7 +57,7 @@ uint64_t orc_set_of(uint64_t x, uint64_t num_sets);
 /* store may be NULL: gather then skips row copies (metadata-only runs) */
 int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const uint32_t *static_score,
                uint64_t num_sets, uint32_t ways, uint64_t victim_rows, uint32_t lookahead,
-               uint32_t near_threshold, uint32_t policy, orc_cache **out);
+               uint32_t near_threshold, uint32_t policy, uint32_t victim_mode, orc_cache **out);
 void orc_destroy(orc_cache *c);
 int orc_advance(orc_cache *c, const int64_t *ids, uint64_t n);
 /* out (U rows), uniq (U), inv (n), outcome (U) may each be NULL */

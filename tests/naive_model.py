@@ -15,7 +15,7 @@ NEAR, FAR, RECENT, NONE = "near", "far", "recent", "none"
 
 class NaiveCache:
     def __init__(self, num_nodes, num_sets, ways, victim_rows, lookahead, static, set_of,
-                 near_threshold=0, policy="hybrid"):
+                 near_threshold=0, policy="hybrid", victim_mode="fifo"):
         self.N, self.S, self.W, self.V, self.L = num_nodes, num_sets, ways, victim_rows, lookahead
         self.T = near_threshold or max(1, lookahead // 8)
         self.static = list(static)
@@ -27,6 +27,9 @@ class NaiveCache:
         self.t = 0
         self.policy = policy
         self.pointer = [0] * num_sets  # round-robin: next way to evict
+        self.queues = victim_mode == "queues"
+        self.C = victim_rows // (lookahead + 1) if self.queues else 0
+        self.q = {}  # queue mode: reuse iteration j -> evicted nodes, in eviction order
 
     def advance(self, ids):
         if len(self.announced) > self.t + self.L:
@@ -62,7 +65,10 @@ class NaiveCache:
                 st["hits"] += 1
                 outcome.append("H")
                 continue
-            if x in self.ring:
+            if self.queues and x in self.q.get(self.t, []):
+                st["victim_hits"] += 1
+                outcome.append("V")
+            elif not self.queues and x in self.ring:
                 self.ring[self.ring.index(x)] = None
                 st["victim_hits"] += 1
                 outcome.append("V")
@@ -76,13 +82,22 @@ class NaiveCache:
                 w = self._victim(self.set_of(x), ways)
                 cls = self._class(ways[w])
                 st["evictions"] += 1
-                if self.V > 0 and cls in (FAR, NEAR):
+                if self.queues and self.C > 0 and cls in (FAR, NEAR):
+                    j = self.t + self._next_use(ways[w][0])
+                    if len(self.q.setdefault(j, [])) < self.C:
+                        self.q[j].append(ways[w][0])
+                        self.tail += 1
+                        st["enqueued"] += 1
+                    else:
+                        st["dropped"] += 1
+                elif not self.queues and self.V > 0 and cls in (FAR, NEAR):
                     self.ring[self.tail % self.V] = ways[w][0]
                     self.tail += 1
                     st["enqueued"] += 1
                 else:
                     st["dropped"] += 1
             ways[w] = (x, self.t)
+        self.q.pop(self.t, None)
         self.t += 1
         return "OK", dict(uniq=uniq, outcome="".join(outcome), **st)
 
@@ -108,4 +123,10 @@ class NaiveCache:
         return [[-1 if e is None else e[0] for e in s] for s in self.sets]
 
     def ring_tags(self):
-        return [-1 if r is None else r for r in self.ring]
+        if not self.queues:
+            return [-1 if r is None else r for r in self.ring]
+        out = [-1] * self.V
+        for j, nodes in self.q.items():
+            slot = j % (self.L + 1)
+            out[slot * self.C: slot * self.C + len(nodes)] = nodes
+        return out

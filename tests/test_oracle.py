@@ -336,8 +336,8 @@ def test_policy_rejected_when_unknown():
 
 
 # ------------------------------------------------------- naive brute force
-def _naive_run(n, S, ways, V, L, T, stat, batches, announce, policy="hybrid"):
-    m = NaiveCache(n, S, ways, V, L, stat, lambda x: set_of(x, S), T, policy=policy)
+def _naive_run(n, S, ways, V, L, T, stat, batches, announce, policy="hybrid", victim_mode="fifo"):
+    m = NaiveCache(n, S, ways, V, L, stat, lambda x: set_of(x, S), T, policy=policy, victim_mode=victim_mode)
     out = []
     for j in range(min(L + 1, len(announce))):
         assert m.advance(announce[j]) == "OK"
@@ -349,9 +349,9 @@ def _naive_run(n, S, ways, V, L, T, stat, batches, announce, policy="hybrid"):
     return m, out
 
 
-def _compare(n, S, ways, V, L, T, stat, batches, announce, policy="hybrid"):
-    m, exp = _naive_run(n, S, ways, V, L, T, stat, batches, announce, policy)
-    o = Oracle(n, 16, stat, S, V, L, near_threshold=T, ways=ways, policy=policy)
+def _compare(n, S, ways, V, L, T, stat, batches, announce, policy="hybrid", victim_mode="fifo"):
+    m, exp = _naive_run(n, S, ways, V, L, T, stat, batches, announce, policy, victim_mode)
+    o = Oracle(n, 16, stat, S, V, L, near_threshold=T, ways=ways, policy=policy, victim_mode=victim_mode)
     got = _drive(o, batches, L, announce)
     for e, g in zip(exp, got):
         assert "".join(CODE[c] for c in g["outcome"]) == e["outcome"]
@@ -434,4 +434,97 @@ def test_bad_config_rejected(kw):
     with pytest.raises(OracleError) as e:
         Oracle(args["num_nodes"], args["row_bytes"], np.ones(max(1, min(args["num_nodes"], 64)), np.uint32),
                args["num_sets"], args["victim_rows"], args["lookahead"])
+    assert e.value.status == "E_INVAL"
+
+
+# ------------------------------------------------ per-iteration victim queues
+# Sec. 4.3.1's form of the victim buffer: one queue per reuse iteration, a
+# counter giving each evicted line its position, drop when full.
+def _queue_scenario(C):
+    """Worked case in the spirit of the paper's example (a line whose next reuse
+    iteration is 4 goes to the queue of iteration 4 at the position its
+    counter names).  One 8-way set, L = 4 (so T = 1), V = 5 * C.  Gather 0
+    fills nodes 0..7; gather 1 brings 8..15 and evicts all of 0..7, whose next
+    announced use is minibatch 4 (distance 3: the far level), in ascending
+    static score (all lines are far, so the score decides)."""
+    n, L = 16, 4
+    stat = np.zeros(n, np.uint32)
+    stat[:8] = [5, 3, 4, 0, 2, 1, 7, 6]
+    batches = [np.arange(8), np.arange(8, 16), np.array([], np.int64), np.array([], np.int64), np.arange(8)]
+    o = Oracle(n, 16, stat, 1, 5 * C, L, victim_mode="queues")
+    return o, stat, batches, L
+
+
+def test_queue_positions_follow_the_counter():
+    o, stat, batches, L = _queue_scenario(C=8)
+    res = _drive(o, batches[:2], L, batches)
+    assert res[1]["stats"]["evictions"] == 8 and res[1]["stats"]["enqueued"] == 8
+    order = sorted(range(8), key=lambda x: stat[x])  # eviction order: 3, 5, 4, 1, 2, 0, 7, 6
+    ring = o.export_state()["ring_tags"].reshape(5, 8)
+    assert ring[4].tolist() == order  # queue of iteration 4, slot 4 mod 5; the 6th eviction (counter 5) at position 5
+    assert ring[4][5] == 0
+    assert (np.delete(ring, 4, axis=0) == EMPTY).all()
+
+
+def test_queue_full_drops_and_queue_serves_only_its_iteration():
+    o, stat, batches, L = _queue_scenario(C=5)
+    res = _drive(o, batches, L)
+    assert res[1]["stats"]["enqueued"] == 5 and res[1]["stats"]["dropped"] == 3  # counters 5, 6, 7 find it full
+    kept = sorted(range(8), key=lambda x: stat[x])[:5]
+    st4 = res[4]
+    assert st4["stats"]["victim_hits"] == 5 and st4["stats"]["misses"] == 3
+    assert sorted(int(x) for x in st4["uniq"][st4["outcome"] == VICTIM_HIT]) == sorted(kept)
+    assert (o.export_state()["ring_tags"] == EMPTY).all()  # the served queue is emptied
+
+
+def test_queue_entry_is_not_served_before_its_iteration():
+    # node 3 sits in the queue of iteration 4; requested (unannounced) at
+    # gather 2 it is a miss.  At gather 4 its queue entry is still there, so
+    # it is served from the cache or, if an earlier fill of that gather evicted
+    # it again, from the queue: never from storage.
+    o, stat, batches, L = _queue_scenario(C=8)
+    served = list(batches)
+    served[2] = np.array([3])
+    res = _drive(o, served, L, batches)
+    assert res[2]["stats"]["misses"] == 1 and res[2]["stats"]["victim_hits"] == 0
+    r4 = res[4]
+    assert r4["outcome"][list(r4["uniq"]).index(3)] != MISS
+    assert r4["stats"]["misses"] == 0
+
+
+@pytest.mark.parametrize("policy", POLICY_NAMES)
+def test_queues_exhaustive_tiny_universe_against_naive_model(policy):
+    n = 3
+    subsets = [np.array(c, np.int64) for r in range(n + 1) for c in itertools.combinations(range(n), r)]
+    stat = np.array([2, 1, 2], np.uint32)
+    for L in (1, 2):
+        for V in (0, L + 1, 2 * (L + 1)):
+            for seq in itertools.product(range(len(subsets)), repeat=4):
+                batches = [subsets[i] for i in seq]
+                _compare(n, 1, 2, V, L, 0, stat, batches, batches, policy, "queues")
+
+
+@pytest.mark.parametrize("policy", POLICY_NAMES)
+@pytest.mark.parametrize("seed", range(100))
+def test_queues_random_small_against_naive_model(seed, policy):
+    rng = np.random.default_rng(5000 + seed)
+    n = int(rng.integers(2, 14))
+    S = int(rng.integers(1, 4))
+    ways = int(rng.integers(1, 4))
+    L = int(rng.choice([0, 1, 2, 3, 5, 9]))
+    V = int(rng.choice([0, 1, 2, 3])) * (L + 1)
+    T = int(rng.choice([0, 0, 1, 2]))
+    stat = rng.integers(0, 4, n).astype(np.uint32)
+    nb = int(rng.integers(1, 10))
+    batches = [rng.integers(0, n, rng.integers(0, 8)) for _ in range(nb)]
+    if rng.random() < 0.5:
+        announce = [rng.integers(0, n, rng.integers(0, 8)) for _ in range(nb + L)]
+    else:
+        announce = batches
+    _compare(n, S, ways, V, L, T, stat, batches, announce, policy, "queues")
+
+
+def test_queue_mode_needs_a_row_per_queue():
+    with pytest.raises(OracleError) as e:
+        Oracle(10, 16, np.ones(10, np.uint32), 2, 3, 3, victim_mode="queues")  # V = 3 < L + 1 = 4
     assert e.value.status == "E_INVAL"
