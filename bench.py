@@ -116,7 +116,7 @@ def make_parts(W, cfg, nb):
     return parts, requests
 
 
-def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None):
+def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None, victim_mode="fifo"):
     """The CPU oracle (single-threaded C, one instance per part) on the same
     stream from gather 0, stopped after about budget_s seconds."""
     from oracle.oracle import Oracle
@@ -125,7 +125,7 @@ def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None):
         sh = p["shape"]
         o = Oracle(p["num_nodes"], p["R"], p["static"], sh.num_sets,
                    sh.victim_rows if victim_rows is None else victim_rows, sh.lookahead,
-                   near_threshold=sh.near_threshold, store=p["store_np"], policy=policy)
+                   near_threshold=sh.near_threshold, store=p["store_np"], policy=policy, victim_mode=victim_mode)
         for j in range(sh.lookahead + 1):
             o.advance(p["batches"][j])
         orcs.append(o)
@@ -193,7 +193,12 @@ def main():
                     help="host threads copying rows for a store kept in pageable memory")
     ap.add_argument("--policy", default="hybrid", choices=["hybrid", "static", "dynamic", "round_robin"],
                     help="eviction policy: the method's hybrid order or one of the evaluation's alternatives")
-    ap.add_argument("--no-ring", action="store_true", help="no victim ring (and so no PVP level swap)")
+    ap.add_argument("--no-ring", action="store_true", help="no victim buffer (and so no PVP level swap)")
+    ap.add_argument("--victim-mode", default="fifo", choices=["fifo", "queues"],
+                    help="victim buffer: one FIFO ring, or per-reuse-iteration queues prefetched into HBM")
+    ap.add_argument("--train-us", type=float, default=0.0,
+                    help="simulated training step per minibatch: a GPU wait of this length on the caller's "
+                         "stream after each minibatch's rows arrive (no memory or link traffic)")
     ap.add_argument("--static", default="indegree", choices=["indegree", "pagerank"],
                     help="static score: the in-degree, or the reverse PageRank computed on the GPU")
     ap.add_argument("--sync", action="store_true",
@@ -275,7 +280,8 @@ def main():
         p["cache"] = lsmgnn.FeatureCache(p["num_nodes"], p["R"], p["store"], p["static"], sh.num_sets,
                                          0 if args.no_ring else sh.victim_rows, sh.lookahead, mb,
                                          near_threshold=sh.near_threshold, pageable=not p["pinned"],
-                                         host_threads=args.host_threads, policy=args.policy)
+                                         host_threads=args.host_threads, policy=args.policy,
+                                         victim_mode=args.victim_mode)
         # three output sets rotate: at most two gathers are in flight
         p["bufs"] = [(torch.empty(mb * p["R"], dtype=torch.uint8, device=dev),
                       torch.empty(mb, dtype=torch.int64, device=dev),
@@ -283,6 +289,18 @@ def main():
         for j in range(L + 1):
             p["cache"].advance(p["dev_batches"][j])
         p["tickets"] = {}
+
+    sleep_cycles = 0
+    if args.train_us > 0:
+        # calibrate the device wait: cycles per microsecond of torch's spin kernel
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(1000000)
+        e0.record()
+        torch.cuda._sleep(10000000)
+        e1.record()
+        torch.cuda.synchronize()
+        sleep_cycles = int(args.train_us * 10000000 / (1e3 * e0.elapsed_time(e1)))
+        log(f"[bench] simulated training step: {args.train_us:.0f} us = {sleep_cycles} spin cycles")
 
     def step(b):
         nbytes = 0
@@ -301,6 +319,8 @@ def main():
             for p in parts:
                 if b - 1 in p["tickets"]:
                     p["cache"].wait(p["tickets"].pop(b - 1))  # a consumer of minibatch b-1 would run after this
+        if sleep_cycles:  # the training step that consumes minibatch b-1 (or b, with blocking calls)
+            torch.cuda._sleep(sleep_cycles)
         return nbytes
 
     def drain():
@@ -337,7 +357,8 @@ def main():
             ("hbm_copy", "hbm_copy", 2, "hbm"),
             ("host_fetch", "host_fetch", 1, "host_link"),
             ("ring_write_dma", "enqueue", 1, "host_link"),
-            ("fill", "fill", 2, "hbm")):
+            ("fill", "fill", 2, "hbm"),
+            ("prefetch", "prefetch", 1, "host_link")):
         ms = sum(pr[key + "_ms"] for pr in profs)
         rows_k = sum(pr[key + "_rows"] for pr in profs)
         kbytes = sum(pr[key + "_rows"] * per_row * p["R"] for pr, p in zip(profs, parts))
@@ -387,7 +408,8 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
         "config": dict(cfg.describe(), feature_dtype="fp32" if cfg.elt_bytes == 4 else "fp16",
                        minibatches_timed=args.steps, policy=args.policy, static_score=static_info,
-                       victim_ring="off" if args.no_ring else "on",
+                       victim_ring="off" if args.no_ring else "on", victim_mode=args.victim_mode,
+                       simulated_training_us=args.train_us,
                        first_timed_minibatch=args.warmup,
                        api=("lsmgnn_gather + lsmgnn_advance" if args.sync
                             else "lsmgnn_gather_async with announcement (two minibatches in flight)")),
@@ -406,7 +428,8 @@ def main():
         "ceilings": ceil,
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(parts, args.cpu_budget, args.policy, 0 if args.no_ring else None)
+        res["cpu_baseline"] = cpu_baseline(parts, args.cpu_budget, args.policy, 0 if args.no_ring else None,
+                                           args.victim_mode)
         res["cpu_baseline"]["gpu_over_cpu"] = gbps / res["cpu_baseline"]["value"]
     for p in parts:
         p["cache"].close()

@@ -79,6 +79,22 @@ enum { LSMGNN_HIT = 0, LSMGNN_VICTIM_HIT = 1, LSMGNN_MISS = 2 };
 #define LSMGNN_POLICY_DYNAMIC 2u     /* no announced use, else the furthest next use */
 #define LSMGNN_POLICY_ROUND_ROBIN 3u /* a per-set pointer (from way 0) that advances by one per eviction */
 
+/* lsmgnn_config.victim_mode: the form of the victim buffer (victim_rows > 0).
+   FIFO: one ring of victim_rows entries that overwrites its oldest; a node
+   with a live entry is a victim hit whenever it is requested, and its row
+   crosses the host link during that gather.
+   QUEUES: the per-reuse-iteration queues of Sec. 4.3.1: an evicted line whose
+   next announced use is minibatch j goes to the queue of iteration j at the
+   position its counter gives (ascending request ID within a gather), unless
+   the queue already holds C = victim_rows / (lookahead + 1) entries (then it
+   is dropped).  After gather t is queued, the library copies queue t+1 into
+   a prefetch buffer in HBM on its host-link stream (while the caller works on
+   minibatch t, Sec. 4.3); gather t+1 serves the nodes queue t+1 holds from
+   there (victim hits) and then empties it.  Requires victim_rows = 0 or
+   lookahead + 1 <= victim_rows with C < 2^31; uses 2 C extra rows of HBM. */
+#define LSMGNN_VICTIM_FIFO 0u
+#define LSMGNN_VICTIM_QUEUES 1u
+
 typedef struct {
   uint64_t num_nodes;   /* IDs are int64 in [0, num_nodes); 1 <= num_nodes <= 2^32 - 1 */
   uint64_t row_bytes;   /* bytes per feature row; a positive multiple of 16 */
@@ -91,6 +107,7 @@ typedef struct {
   uint32_t flags;       /* 0 or LSMGNN_FLAG_PAGEABLE_STORE; other bits must be 0 */
   uint32_t host_threads; /* pageable store: host threads copying rows (0 selects 8) */
   uint32_t policy;      /* LSMGNN_POLICY_*; other values are rejected */
+  uint32_t victim_mode; /* LSMGNN_VICTIM_*; other values are rejected */
   /* Backing store: num_nodes * row_bytes bytes of host memory, row v at offset
      v * row_bytes.  Borrowed: the caller keeps it alive and unchanged while
      the cache exists; the library only reads it.
@@ -129,6 +146,7 @@ typedef struct {
   double enqueue_ms;    uint64_t enqueue_launches;    uint64_t enqueue_rows;    /* staging -> ring */
   double fill_ms;       uint64_t fill_launches;       uint64_t fill_rows;       /* out -> cache */
   double host_copy_ms;  uint64_t host_copy_rows;      /* pageable store: host threads' row copies (wall time) */
+  double prefetch_ms;   uint64_t prefetch_launches;   uint64_t prefetch_rows;   /* victim queue -> HBM buffer */
   double gather_ms;     uint64_t gathers;             /* whole gather, first to last kernel */
 } lsmgnn_profile;
 

@@ -87,7 +87,7 @@ static inline unsigned grid_for(uint64_t work, uint64_t per_block, unsigned cap)
 // (keeping the previous tail) and zero the device counters for the next call
 // (they start zeroed at create).
 __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host, const uint32_t *part,
-                                                   StatGrids grids, uint64_t *tail) {
+                                                   StatGrids grids, uint64_t *tail, QueueFinish qf) {
   __shared__ uint32_t red[kNumStat][kBlock / 64];
   __shared__ uint32_t sums[kNumStat];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -127,18 +127,33 @@ __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host,
     c.n_hbm = sums[kStHbm];
     c.n_host = sums[kStHost];
     c.n_enq_copy = sums[kStEnqCopy];
+    // queue mode: candidates that found their queue full were dropped
+    c.enqueued -= c.q_overflow;
+    c.dropped += c.q_overflow;
     *host = c;
     if (tail && !c.err) {  // a rejected gather leaves both tails alone
       tail[1] = tail[0];
       tail[0] += c.enq_total;
+    }
+    if (qf.qcount && !c.err) {
+      // the served queue is empty from now on; the next gather's queue holds
+      // qcount[next] entries, the last q_placed[next] of them staged by this
+      // gather after the rows it staged for the lower slots
+      qf.qcount[qf.cur] = 0;
+      uint32_t off = 0;
+      for (uint32_t k = 0; k < qf.next; ++k) off += c.q_placed[k];
+      const uint32_t cnt = qf.qcount[qf.next];
+      qf.gate->q_count = cnt;
+      qf.gate->q_before = cnt - c.q_placed[qf.next];
+      qf.gate->q_stage_off = off;
     }
     *cn = Counters{};
   }
 }
 
 void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, const StatGrids &grids,
-                   uint64_t *tail, hipStream_t s) {
-  hipLaunchKernelGGL(k_finish, dim3(1), dim3(kBlock), 0, s, cn, host, stat_part, grids, tail);
+                   uint64_t *tail, const QueueFinish &qf, hipStream_t s) {
+  hipLaunchKernelGGL(k_finish, dim3(1), dim3(kBlock), 0, s, cn, host, stat_part, grids, tail, qf);
 }
 
 // ------------------------------------------------------------------- dedup
@@ -208,7 +223,7 @@ __global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uin
   const uint32_t err = cn->err;
   if (err) {
     if (threadIdx.x == 0) {
-      *gate = Gate{err, 0, 0, 0, 0, 0, {0, 0}};
+      *gate = Gate{err, 0, 0, 0, 0, 0, 0, 0, 0, {0, 0, 0}};
       *dd = DedupResult{err, 0, {0, 0}};
     }
     return;
@@ -224,7 +239,7 @@ __global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uin
   }
   if (threadIdx.x == 0) {
     cn->n_unique = carry;
-    *gate = Gate{0, carry, 0, 0, 0, 0, {0, 0}};
+    *gate = Gate{0, carry, 0, 0, 0, 0, 0, 0, 0, {0, 0, 0}};
     *dd = DedupResult{0, carry, {0, 0}};
   }
 }
@@ -481,7 +496,7 @@ __global__ __launch_bounds__(kBlock) void k_set_walk(const DevState d, Scratch s
           const uint32_t m = d.mask[tag];
           cls = (ins == t) ? kClsRecent : class_from_bits(m, t, d.L, d.T);
           lvl = level_of(cls, ring_on);
-          if constexpr (P == kPolicyDynamic) dist = dist_from_bits(m, t, d.L);
+          if (P == kPolicyDynamic || d.qmode) dist = dist_from_bits(m, t, d.L);
           known = true;
         }
         if constexpr (P == kPolicyHybrid) {
@@ -496,10 +511,11 @@ __global__ __launch_bounds__(kBlock) void k_set_walk(const DevState d, Scratch s
         }
         z = __shfl(tag, (int)pick, kWays);
         const uint32_t pc = __shfl(cls, (int)pick, kWays);
+        const uint32_t pd = __shfl(dist, (int)pick, kWays);
         if (lead) {
           ++c_evict;
           if (ring_on && (pc == kClsFar || pc == kClsNear)) {
-            f = kFlagEnqueue;
+            f = (uint8_t)(kFlagEnqueue | (pd << kFlagDistShift));
             ++c_enq;
           } else {
             ++c_drop;
@@ -634,11 +650,145 @@ __global__ __launch_bounds__(kBlock) void k_scan_final(const DevState d, Scratch
   }
 }
 
+// ------------------------------------------------------------ victim queues
+// Queue mode (Sec. 4.3.1): an enqueue candidate u goes to the queue of its
+// line's next reuse iteration j = t + distance (slot j mod (L+1)) at the
+// position the queue's counter gives in ascending-u order, or is dropped when
+// that position is C or more.  Per-block counts per slot, one block's scan of
+// them per slot, then each candidate's rank among its block's candidates for
+// the same slot (one ballot per slot).
+__device__ __forceinline__ bool q_candidate(const Scratch &sc, uint32_t u, uint32_t U, uint64_t t, uint32_t slots,
+                                            uint32_t &key) {
+  if (u >= U || sc.kind[u] != kKindFill) return false;
+  const uint32_t f = sc.flags[u];
+  if (!(f & kFlagEnqueue)) return false;
+  key = (uint32_t)((t + (f >> kFlagDistShift)) % slots);
+  return true;
+}
+
+__global__ __launch_bounds__(kBlock) void k_qcount(const DevState d, Scratch sc, uint64_t t, const Counters *cn) {
+  if (cn->err) return;
+  const uint32_t U = cn->n_unique;
+  const uint32_t slots = d.L + 1;
+  const uint32_t nb = (U + kBlock - 1) / kBlock;
+  __shared__ uint32_t cnt[kMaxQueues];
+  for (uint32_t b = blockIdx.x; b < nb; b += gridDim.x) {
+    if (threadIdx.x < kMaxQueues) cnt[threadIdx.x] = 0;
+    __syncthreads();
+    uint32_t key = 0;
+    if (q_candidate(sc, b * kBlock + threadIdx.x, U, t, slots, key)) atomicAdd(&cnt[key], 1u);
+    __syncthreads();
+    if (threadIdx.x < slots) sc.qpart[(uint64_t)threadIdx.x * nb + b] = cnt[threadIdx.x];
+    __syncthreads();
+  }
+}
+
+// One block: per slot, the exclusive scan of the per-block counts, then the
+// slot's placements (up to C entries in all) and the counters the finish and
+// the host read.  The queue counters advance here; the placement kernel reads
+// the values from before this gather from the call's counters.
+__global__ __launch_bounds__(kBlock) void k_qtop(const DevState d, Scratch sc, Counters *cn) {
+  if (cn->err) return;
+  const uint32_t U = cn->n_unique;
+  const uint32_t slots = d.L + 1;
+  const uint32_t nb = (U + kBlock - 1) / kBlock;
+  __shared__ uint32_t tot[kMaxQueues];
+  for (uint32_t k = 0; k < slots; ++k) {
+    uint32_t carry = 0;
+    uint32_t *row = sc.qpart + (uint64_t)k * nb;
+    for (uint32_t base = 0; base < nb; base += kBlock) {
+      const uint32_t i = base + threadIdx.x;
+      const uint32_t v = i < nb ? row[i] : 0u;
+      uint32_t blk;
+      const uint32_t ex = block_exclusive_scan(v, blk);
+      if (i < nb) row[i] = carry + ex;
+      carry += blk;
+    }
+    if (threadIdx.x == 0) tot[k] = carry;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t placed_all = 0, over = 0;
+    for (uint32_t k = 0; k < slots; ++k) {
+      const uint32_t before = d.qcount[k];
+      const uint32_t room = (uint32_t)d.C - before;
+      const uint32_t placed = tot[k] < room ? tot[k] : room;
+      cn->q_before[k] = before;
+      cn->q_placed[k] = placed;
+      d.qcount[k] = before + placed;
+      placed_all += placed;
+      over += tot[k] - placed;
+    }
+    cn->enq_total = placed_all;
+    cn->q_overflow = over;
+  }
+}
+
+// Position of every candidate: the slot's entries before this gather, the
+// candidates of lower blocks and those of lower lanes of this block.  A placed
+// entry records its tag and its node's latest entry, and lists its row for
+// staging: the gather's placements are staged slot by slot, in position order.
+// Runs after the resolve kernel, which reads the nodes' entries from before
+// this gather.
+__global__ __launch_bounds__(kBlock) void k_qplace(const DevState d, Scratch sc, uint64_t t, Counters *cn) {
+  if (cn->err) return;
+  const uint32_t U = cn->n_unique;
+  const uint32_t slots = d.L + 1;
+  const uint32_t nb = (U + kBlock - 1) / kBlock;
+  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
+  __shared__ uint32_t wcnt[kBlock / 64][kMaxQueues];
+  __shared__ uint32_t off[kMaxQueues];
+  if (threadIdx.x == 0) {
+    uint32_t o = 0;
+    for (uint32_t k = 0; k < slots; ++k) {
+      off[k] = o;
+      o += cn->q_placed[k];
+    }
+  }
+  __syncthreads();
+  uint32_t c_copy = 0;
+  for (uint32_t b = blockIdx.x; b < nb; b += gridDim.x) {
+    const uint32_t u = b * kBlock + threadIdx.x;
+    uint32_t key = 0;
+    const bool cand = q_candidate(sc, u, U, t, slots, key);
+    uint32_t rank = 0;
+    for (uint32_t k = 0; k < slots; ++k) {
+      const uint64_t m = __ballot(cand && key == k);
+      if (cand && key == k) rank = (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
+      if (lane == 0) wcnt[wid][k] = (uint32_t)__popcll(m);
+    }
+    __syncthreads();
+    bool stage = false;
+    uint32_t pos = 0;
+    if (cand) {
+      for (uint32_t w = 0; w < wid; ++w) rank += wcnt[w][key];
+      const uint32_t before = cn->q_before[key];
+      const uint64_t p = (uint64_t)before + sc.qpart[(uint64_t)key * nb + b] + rank;
+      if (p < d.C) {
+        const uint32_t z = sc.evicted[u];
+        const uint64_t j = t + (sc.flags[u] >> kFlagDistShift);
+        d.ring_tag[key * d.C + p] = z;
+        d.vpos[z] = ((j + 1) << 32) | p;
+        pos = off[key] + (uint32_t)(p - before);
+        stage = true;
+        ++c_copy;
+      }
+    }
+    const uint32_t i = block_append(stage, &sc.gate->n_stage);
+    if (stage) {
+      sc.stage.src[i] = sc.slot[u];
+      sc.stage.dst[i] = pos;
+    }
+  }
+  block_count(c_copy, sc.stat_part, kStEnqCopy);
+}
+
 // Victim-ring probe of every fill and the row source of every unique ID.  Builds
 // the gather's row-copy lists (dense, in arbitrary order): the host fetch (rows
 // from pinned host memory), the hit copy (rows from cache slots) and the fills
 // (each way's final occupant).
-__global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc, uint8_t *outcome, Counters *cn) {
+__global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc, uint64_t t, uint8_t *outcome,
+                                                    Counters *cn) {
   if (cn->err) return;
   const uint32_t U = cn->n_unique;
   const uint64_t tail0 = d.tail[0], tail_prev = d.tail[1];
@@ -655,6 +805,22 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
       if (kind == kKindHit) {
         code = kSrcHbm | sc.slot[u];
         ++c_hbm;
+      } else if (d.qmode) {
+        // queue mode: a victim hit iff the node's latest entry is in the queue
+        // of this iteration, whose rows were prefetched into buffer t & 1
+        const uint32_t x = sc.uniq[u];
+        const uint64_t vp = d.V ? d.vpos[x] : 0;
+        if ((vp >> 32) == t + 1) {
+          ++c_vhit;
+          oc = 1;  // LSMGNN_VICTIM_HIT
+          code = kSrcHbm | (d.S * kWays + (t & 1) * d.C + (vp & 0xffffffffu));
+          ++c_hbm;
+        } else {
+          ++c_miss;
+          oc = 2;  // LSMGNN_MISS
+          code = kSrcStore | x;
+          ++c_host;
+        }
       } else {
         const uint32_t x = sc.uniq[u];
         uint64_t q = 0;
@@ -773,19 +939,29 @@ __global__ __launch_bounds__(kBlock) void k_enq_finalize(const DevState d, Scrat
   block_count(c_copy, sc.stat_part, kStEnqCopy);
 }
 
-void launch_ring_resolve(const DevState &d, uint64_t n, Scratch &sc, uint8_t *outcome, Counters *cn,
+void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, uint8_t *outcome, Counters *cn,
                          StatGrids &grids, hipStream_t s) {
   const unsigned g = grid_for(n, kBlock, kMaxGrid);
   const unsigned gs = grid_for(n, kScanChunk, kMaxGrid);
-  if (d.V) {
+  const bool ring = d.V && !d.qmode;
+  const bool queues = d.V && d.qmode && d.L > 0;  // with L = 0 no line has a reuse iteration
+  if (ring) {
     hipLaunchKernelGGL(k_scan_partial, dim3(gs), dim3(kBlock), 0, s, sc.flags, sc.scan_part, cn);
     hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kBlock), 0, s, sc.scan_part, cn);
     hipLaunchKernelGGL(k_scan_final, dim3(gs), dim3(kBlock), 0, s, d, sc, cn);
   }
-  hipLaunchKernelGGL(k_resolve, dim3(g), dim3(kBlock), 0, s, d, sc, outcome, cn);
+  if (queues) {
+    hipLaunchKernelGGL(k_qcount, dim3(g), dim3(kBlock), 0, s, d, sc, t, cn);
+    hipLaunchKernelGGL(k_qtop, dim3(1), dim3(kBlock), 0, s, d, sc, cn);
+  }
+  hipLaunchKernelGGL(k_resolve, dim3(g), dim3(kBlock), 0, s, d, sc, t, outcome, cn);
   for (int st = kStVictimHits; st <= kStHost; ++st) grids.g[st] = g;
-  if (d.V) {
+  if (ring) {
     hipLaunchKernelGGL(k_enq_finalize, dim3(g), dim3(kBlock), 0, s, d, sc, cn);
+    grids.g[kStEnqCopy] = g;
+  }
+  if (queues) {
+    hipLaunchKernelGGL(k_qplace, dim3(g), dim3(kBlock), 0, s, d, sc, t, cn);
     grids.g[kStEnqCopy] = g;
   }
 }
@@ -932,6 +1108,45 @@ void launch_copy(CopyMode mode, const DevState &d, uint64_t n, const Scratch &sc
       launch_list<CopyMode::kOutToCache>(out, sc.fill, d.rows, sc.gate, &sc.gate->n_fill, n, d.R, s);
       break;
   }
+}
+
+// Queue mode: the queue of the next gather into its prefetch buffer.  Rows of
+// entries placed by earlier gathers cross the host link (a small grid, like
+// the host fetch); those placed by the gather just issued are still in its
+// staging rows in HBM.
+__global__ __launch_bounds__(kBlock) void k_prefetch(const DevState d, const Gate *gate, const uint8_t *staging,
+                                                     uint32_t slot, uint32_t par, uint32_t nvec) {
+  const uint32_t cnt = gate->q_count, before = gate->q_before, off = gate->q_stage_off;
+  const uint64_t R = d.R;
+  const uint64_t total = (uint64_t)cnt * nvec;
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  uint8_t *pf = d.rows + (d.S * kWays + (uint64_t)par * d.C) * R;
+  const uint8_t *q = d.ring_rows + (uint64_t)slot * d.C * R;
+  for (uint64_t w0 = (uint64_t)blockIdx.x * kBlock + threadIdx.x; w0 < total; w0 += stride * kUnroll) {
+    u32x4 v[kUnroll];
+    uint8_t *dp[kUnroll];
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      const uint64_t w = w0 + k * stride;
+      dp[k] = nullptr;
+      if (w < total) {
+        const uint64_t i = w / nvec;
+        const uint64_t byte = (w - i * nvec) * 16u;
+        const uint8_t *src = i < before ? q + i * R + byte : staging + (off + (i - before)) * R + byte;
+        v[k] = *reinterpret_cast<const u32x4 *>(src);
+        dp[k] = pf + i * R + byte;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k)
+      if (dp[k]) *reinterpret_cast<u32x4 *>(dp[k]) = v[k];
+  }
+}
+
+void launch_prefetch(const DevState &d, const Gate *gate, const uint8_t *staging, uint32_t slot, uint32_t par,
+                     hipStream_t s) {
+  hipLaunchKernelGGL(k_prefetch, dim3(LSM_HOST_GRID), dim3(kBlock), 0, s, d, gate, staging, slot, par,
+                     (uint32_t)(d.R / 16));
 }
 
 // ------------------------------------------------------------ calibration

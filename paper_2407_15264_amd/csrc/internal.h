@@ -15,13 +15,16 @@ constexpr int kWordsPerThread = kBytesPerThread / 4;
 constexpr int kChunkBytes = kBlock * kBytesPerThread;  // dedup map bytes per block
 constexpr int kScanPerThread = 8;    // flags per thread in the enqueue scan
 constexpr int kScanChunk = kBlock * kScanPerThread;
+constexpr int kMaxQueues = 32;       // victim-queue slots: L + 1 <= 32
 
 // dynamic classes of a resident line while a gather runs
 enum : uint32_t { kClsNone = 0, kClsFar = 1, kClsRecent = 2, kClsNear = 3 };
 // per-unique kinds from the set walk
 enum : uint8_t { kKindHit = 0, kKindFill = 1 };
-// per-unique flags
+// per-unique flags: bit 0 the evicted line goes to the victim buffer; bits 1-5
+// its next reuse distance (queue mode)
 enum : uint8_t { kFlagEnqueue = 1 };
+constexpr int kFlagDistShift = 1;
 // per-unique row source: top two bits select the place, the rest index it
 constexpr uint64_t kSrcHbm = 0ull << 62;    // cache slot in HBM
 constexpr uint64_t kSrcStore = 1ull << 62;  // backing-store row (pinned host)
@@ -39,6 +42,9 @@ struct alignas(128) SetRec {
   uint32_t rr_inv;
   uint32_t pad[kWays - 1];
 };
+
+// victim-buffer forms (values of lsmgnn_config.victim_mode)
+enum : uint32_t { kVictimFifo = 0, kVictimQueues = 1 };
 
 // eviction policies (values of lsmgnn_config.policy)
 enum : uint32_t { kPolicyHybrid = 0, kPolicyStatic = 1, kPolicyDynamic = 2, kPolicyRoundRobin = 3 };
@@ -68,7 +74,12 @@ struct Counters {
   uint32_t hits, fills, evictions, enqueued, dropped, victim_hits, misses;
   uint32_t n_hbm, n_host, n_enq_copy, n_fill;  // rows per data kernel
   uint32_t enq_total;
-  uint32_t pad[16];
+  // victim queues (queue mode): enqueue candidates that found their queue
+  // full, and per queue slot the entries before this gather and those it placed
+  uint32_t q_overflow;
+  uint32_t q_before[kMaxQueues];
+  uint32_t q_placed[kMaxQueues];
+  uint32_t pad[15];
 };
 
 // Dedup result of a gather, written by the chunk scan to pinned host memory:
@@ -90,7 +101,12 @@ struct Gate {
   uint32_t n_hbm;    // hit-copy list
   uint32_t n_fill;   // fill list
   uint32_t n_stage;  // staging list
-  uint32_t pad[2];
+  // queue mode, written by the gather's last metadata kernel for the prefetch
+  // of the next gather's queue: its entries, how many of them earlier gathers
+  // placed (their rows are in the host queue), and where this gather staged
+  // the rest
+  uint32_t q_count, q_before, q_stage_off;
+  uint32_t pad[3];
 };
 
 // A row-copy list: entry i moves row src[i] of its source to row dst[i] of its
@@ -133,6 +149,7 @@ struct Scratch {
   RowList stage;        // surviving enqueues: cache slot -> staging row
   uint8_t *staging;     // [min(max_batch, V)][R] evicted rows in ring order, for the ring write
   uint8_t *bounce;      // pageable store only: [max_batch][R] pinned, the host-fetch rows in list order
+  uint32_t *qpart;      // queue mode: [kMaxQueues][ceil(max_batch / kBlock)] per-block enqueue counts
 };
 
 struct DevState {
@@ -140,9 +157,10 @@ struct DevState {
   uint8_t *rows;         // [S*8][R] cache data
   uint32_t *mask;        // [N] announced-batch bits (bit j mod 32)
   uint32_t *stat;        // [N] static score
-  uint64_t *vpos;        // [N] 1 + sequence of the node's latest ring entry, or 0
-  uint32_t *ring_tag;    // [V]
-  uint8_t *ring_rows;    // [V][R] pinned host, device-visible address
+  uint64_t *vpos;        // [N] FIFO: 1 + sequence of the node's latest ring entry, or 0;
+                         //     queues: (1 + reuse iteration) << 32 | position of its latest entry
+  uint32_t *ring_tag;    // [V] FIFO ring entries, or queue slot k's entries at k * C
+  uint8_t *ring_rows;    // [V][R] pinned host, device-visible address (ring or queue rows)
   const uint8_t *store;  // [N][R] pinned host, device-visible address
   uint8_t *present;      // [nchunks * kChunkBytes] dedup byte map (all zero between calls)
   uint32_t *chunk_sums;  // [nchunks]
@@ -156,13 +174,27 @@ struct DevState {
   uint64_t nchunks;
   uint32_t L, T;
   uint32_t policy;
+  uint32_t qmode;        // kVictimQueues: per-reuse-iteration queues instead of the ring
+  uint64_t C;            // queue mode: rows per queue, V / (L + 1)
+  uint32_t *qcount;      // queue mode: [L + 1] entries in each queue slot
+  // queue mode: the two prefetch buffers (C rows each, by gather parity) are
+  // rows S*8 .. S*8 + 2C of `rows`, after the cache lines
 };
 
 enum class CopyMode { kHbmToOut, kHostToOut, kCacheToStage, kOutToCache };
 
+// What the last kernel of a gather does for the victim queues: empty the
+// served slot `cur` and record in the gate what the prefetch of slot `next`
+// needs.  qcount == nullptr: nothing (ring mode, announcements).
+struct QueueFinish {
+  uint32_t *qcount = nullptr;
+  Gate *gate = nullptr;
+  uint32_t cur = 0, next = 0;
+};
+
 // ----- launchers (gather_kernels.hip) -----
 void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, const StatGrids &grids,
-                   uint64_t *tail, hipStream_t s);
+                   uint64_t *tail, const QueueFinish &qf, hipStream_t s);
 // ann_ids/ann_n: the list announced with this gather (validated here), or NULL/0
 void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, const int64_t *ann_ids, uint64_t ann_n,
                   const int64_t *clear_ids, uint64_t clear_n, uint32_t clear_bit, Scratch &sc, int64_t *unique_out,
@@ -171,8 +203,14 @@ void launch_group_by_set(const DevState &d, const int64_t *ids, uint64_t n, int6
                          Counters *cn, hipStream_t s);
 void launch_set_walk(const DevState &d, uint64_t n, uint32_t t, Scratch &sc, Counters *cn, StatGrids &grids,
                      hipStream_t s);
-void launch_ring_resolve(const DevState &d, uint64_t n, Scratch &sc, uint8_t *outcome, Counters *cn,
+// t: the gather's index (queue mode serves queue t from prefetch buffer t & 1)
+void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, uint8_t *outcome, Counters *cn,
                          StatGrids &grids, hipStream_t s);
+// Queue mode: copy the queue of gather t+1 (slot `slot`) into prefetch buffer
+// `par`: entries placed by gathers up to t-1 from the pinned host queue, those
+// placed by gather t from its staging rows; sizes from gather t's gate.
+void launch_prefetch(const DevState &d, const Gate *gate, const uint8_t *staging, uint32_t slot, uint32_t par,
+                     hipStream_t s);
 // n bounds the gather's unique count (the copies read the exact one from the gate)
 void launch_copy(CopyMode mode, const DevState &d, uint64_t n, const Scratch &sc, uint8_t *out, hipStream_t s);
 void launch_window_set(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask, int64_t *slot_ids,

@@ -77,7 +77,8 @@ struct DeviceGuard {
   }
 };
 
-enum { kEvHbm0, kEvHbm1, kEvEnq0, kEvEnq1, kEvHost0, kEvHost1, kEvFill0, kEvFill1, kEvAll0, kEvAll1, kNumEv };
+enum { kEvHbm0, kEvHbm1, kEvEnq0, kEvEnq1, kEvHost0, kEvHost1, kEvFill0, kEvFill1, kEvAll0, kEvAll1, kEvPf0, kEvPf1,
+       kNumEv };
 
 // One gather in flight; two of these alternate by gather parity.
 struct Flight {
@@ -86,6 +87,8 @@ struct Flight {
   Counters *hc_dev = nullptr;
   hipEvent_t meta_done = nullptr, finish_done = nullptr, stage_done = nullptr, host_done = nullptr,
              data_done = nullptr, dma_done = nullptr;
+  hipEvent_t pf_done = nullptr;  // queue mode: this parity's prefetch buffer holds the gather's queue
+  bool pf_ready = false;         // pf_done has been recorded for the gather that uses this parity next
   uint32_t *hlist_host = nullptr;  // pageable store: host views of sc.host_list, sc.host_src, sc.bounce
   uint64_t *hsrc_host = nullptr;
   uint8_t *bounce_host = nullptr;
@@ -95,6 +98,7 @@ struct Flight {
   bool dma_used = false;       // dma_done has been recorded at least once
   uint64_t t = 0, requests = 0;
   uint64_t enq_total = 0, tail_end = 0;  // enqueues of the gather, ring tail after it
+  uint32_t q_before[lsm::kMaxQueues] = {}, q_placed[lsm::kMaxQueues] = {};  // queue mode, per slot
 };
 
 // Timing events of one gather.  Four sets rotate by gather index: when gather
@@ -107,8 +111,9 @@ struct PerfSet {
   bool pending = false;  // events recorded for gather t and not yet read
   bool counted = false;  // row counts of gather t copied in
   bool ring = false;     // the ring write was timed
+  bool pf = false;       // the prefetch this gather issued for the next one was timed
   uint64_t t = 0, requests = 0;
-  uint32_t n_hbm = 0, n_host = 0, n_enq = 0, n_fill = 0;
+  uint32_t n_hbm = 0, n_host = 0, n_enq = 0, n_fill = 0, n_pf = 0;
 };
 
 // The per-device stream triple, created with the first cache on a device and
@@ -177,6 +182,7 @@ struct lsmgnn_cache {
   const uint8_t *store_host = nullptr;
   lsm::HostPool *pool = nullptr;
   hipEvent_t ev_in = nullptr, ev_dedup = nullptr, ev_adv = nullptr;
+  hipEvent_t ev_q = nullptr;  // queue mode: the queue writes queued so far have landed
   uint64_t t = 0;  // gathers issued
   uint64_t n_adv = 0, tail = 0;
   lsmgnn_counts last{}, total{};
@@ -197,12 +203,12 @@ void release(lsmgnn_cache *c) {
   for (void *p : c->host_allocs) (void)hipHostFree(p);
   c->host_allocs.clear();
   for (Flight &f : c->fl)
-    for (hipEvent_t e : {f.meta_done, f.finish_done, f.stage_done, f.host_done, f.data_done, f.dma_done})
+    for (hipEvent_t e : {f.meta_done, f.finish_done, f.stage_done, f.host_done, f.data_done, f.dma_done, f.pf_done})
       if (e) (void)hipEventDestroy(e);
   for (PerfSet &p : c->ps)
     for (hipEvent_t e : p.e)
       if (e) (void)hipEventDestroy(e);
-  for (hipEvent_t e : {c->ev_in, c->ev_dedup, c->ev_adv})
+  for (hipEvent_t e : {c->ev_in, c->ev_dedup, c->ev_adv, c->ev_q})
     if (e) (void)hipEventDestroy(e);
   if (c->has_streams) release_streams(c->device);
   c->has_streams = false;
@@ -274,12 +280,21 @@ void harvest_stats(lsmgnn_cache *c, Flight &f) {
   f.enq_total = h.enq_total;
   f.tail_end = c->tail;
   f.dma_pending = c->d.V > 0 && h.enq_total > 0;
+  if (c->d.qmode)
+    for (int k = 0; k < lsm::kMaxQueues; ++k) {
+      f.q_before[k] = h.q_before[k];
+      f.q_placed[k] = h.q_placed[k];
+    }
   PerfSet &p = c->ps[f.t % kPerfSets];
   if (p.pending && p.t == f.t) {
     p.n_hbm = h.n_hbm;
     p.n_host = h.n_host;
     p.n_enq = h.n_enq_copy;
     p.n_fill = h.n_fill;
+    if (c->d.qmode) {  // the prefetch this gather issued moved the next queue's entries
+      const uint32_t nx = (uint32_t)((f.t + 1) % (c->d.L + 1));
+      p.n_pf = h.q_before[nx] + h.q_placed[nx];
+    }
     p.counted = true;
   }
   f.stats_pending = false;
@@ -288,20 +303,35 @@ void harvest_stats(lsmgnn_cache *c, Flight &f) {
 // Queue a harvested gather's ring write: its E enqueues have the sequence
 // numbers [tail_end - E, tail_end), of which the last min(E, V) survive; they
 // were staged in that order and land in at most two contiguous ring pieces.
+//
+// Queue mode: the placements were staged slot by slot; slot k's go to its
+// positions [q_before[k], q_before[k] + q_placed[k]).
 void issue_dma(lsmgnn_cache *c, Flight &f) {
   if (!f.dma_pending) return;
   f.dma_pending = false;
   const uint64_t V = c->d.V, R = c->d.R;
-  const uint64_t rows = f.enq_total < V ? f.enq_total : V;
-  const uint64_t p0 = (f.tail_end - rows) % V;
-  const uint64_t first = rows < V - p0 ? rows : V - p0;
   PerfSet &p = c->ps[f.t % kPerfSets];
   const bool prof = p.pending && p.t == f.t;
   (void)hipStreamWaitEvent(c->dma, f.stage_done, 0);
   if (prof) (void)hipEventRecord(p.e[kEvEnq0], c->dma);
-  (void)hipMemcpyAsync(c->ring_host + p0 * R, f.sc.staging, first * R, hipMemcpyDeviceToHost, c->dma);
-  if (rows > first)
-    (void)hipMemcpyAsync(c->ring_host, f.sc.staging + first * R, (rows - first) * R, hipMemcpyDeviceToHost, c->dma);
+  if (c->d.qmode) {
+    uint64_t off = 0;
+    for (uint32_t k = 0; k <= c->d.L; ++k) {
+      const uint64_t m = f.q_placed[k];
+      if (m)
+        (void)hipMemcpyAsync(c->ring_host + (k * c->d.C + f.q_before[k]) * R, f.sc.staging + off * R, m * R,
+                             hipMemcpyDeviceToHost, c->dma);
+      off += m;
+    }
+  } else {
+    const uint64_t rows = f.enq_total < V ? f.enq_total : V;
+    const uint64_t p0 = (f.tail_end - rows) % V;
+    const uint64_t first = rows < V - p0 ? rows : V - p0;
+    (void)hipMemcpyAsync(c->ring_host + p0 * R, f.sc.staging, first * R, hipMemcpyDeviceToHost, c->dma);
+    if (rows > first)
+      (void)hipMemcpyAsync(c->ring_host, f.sc.staging + first * R, (rows - first) * R, hipMemcpyDeviceToHost,
+                           c->dma);
+  }
   if (prof) {
     (void)hipEventRecord(p.e[kEvEnq1], c->dma);
     p.ring = true;
@@ -360,6 +390,12 @@ void harvest_profile(lsmgnn_cache *c, PerfSet &p) {
     c->acc.fill_launches += 1;
     c->acc.fill_rows += p.n_fill;
   }
+  if (p.pf) {
+    (void)hipEventSynchronize(p.e[kEvPf1]);
+    c->acc.prefetch_ms += el(kEvPf0, kEvPf1);
+    c->acc.prefetch_launches += 1;
+    c->acc.prefetch_rows += p.n_pf;
+  }
   (void)hipGetLastError();
   p.pending = false;
 }
@@ -406,6 +442,7 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   harvest_profile(c, ps);  // gather t-4's events are complete
   issue_dma(c, f);         // gather t-2's ring write (normally queued by gather t-1's call)
   const bool prof = c->prof != 0;
+  const bool queues = d.qmode && d.V && d.L > 0;  // per-iteration victim queues with prefetch
   auto rec = [&](int e, hipStream_t st) {
     if (prof) (void)hipEventRecord(ps.e[e], st);
   };
@@ -435,10 +472,17 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   if (n) {
     lsm::launch_group_by_set(d, ids, n, inverse, f.sc, c->cn, c->meta);
     lsm::launch_set_walk(d, n, (uint32_t)t, f.sc, c->cn, grids, c->meta);
-    lsm::launch_ring_resolve(d, n, f.sc, outcome, c->cn, grids, c->meta);
+    lsm::launch_ring_resolve(d, n, t, f.sc, outcome, c->cn, grids, c->meta);
   }
   (void)hipEventRecord(f.meta_done, c->meta);
-  lsm::launch_finish(c->cn, f.hc_dev, f.sc.stat_part, grids, d.tail, c->meta);
+  lsm::QueueFinish qf;
+  if (queues) {
+    qf.qcount = d.qcount;
+    qf.gate = f.sc.gate;
+    qf.cur = (uint32_t)(t % (d.L + 1));
+    qf.next = (uint32_t)((t + 1) % (d.L + 1));
+  }
+  lsm::launch_finish(c->cn, f.hc_dev, f.sc.stat_part, grids, d.tail, qf, c->meta);
   // the announced bits are first read by the next gather's set walk
   if (record)
     lsm::launch_announce(an.ids, an.n, (uint32_t)(k & 31u), d.mask, c->win_ids + (uint64_t)kslot * c->max_batch,
@@ -462,6 +506,9 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   if (pf.used) (void)hipStreamWaitEvent(c->meta, pf.data_done, 0);
   if (f.dma_used) (void)hipStreamWaitEvent(c->meta, f.dma_done, 0);
   if (n && d.V) lsm::launch_copy(CopyMode::kCacheToStage, d, n, f.sc, outp, c->meta);
+  // queue mode: the hit copy also moves the victim hits, from the prefetch
+  // buffer that the previous call filled
+  if (queues && f.pf_ready) (void)hipStreamWaitEvent(c->meta, f.pf_done, 0);
   rec(kEvHbm0, c->meta);
   if (n) lsm::launch_copy(CopyMode::kHbmToOut, d, n, f.sc, outp, c->meta);
   rec(kEvHbm1, c->meta);
@@ -476,6 +523,7 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   if (hipEventSynchronize(c->pageable ? f.finish_done : c->ev_dedup) != hipSuccess) return fail_device(c);
   harvest_stats(c, pf);
   issue_dma(c, pf);
+  if (queues) (void)hipEventRecord(c->ev_q, c->dma);  // every queue write up to gather t-1's
   if (c->pageable) {
     if (n && !(dedup && c->dd->err)) {
       // ring rows are read only for entries of gathers up to t-2, whose ring
@@ -509,6 +557,27 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
     ps.t = t;
     ps.requests = n;
     ps.ring = false;
+    ps.pf = false;
+  }
+  if (queues) {
+    // prefetch of the next gather's queue, on the host-link stream after this
+    // gather's host fetch: while the caller consumes this minibatch.  Its rows
+    // are in the host queue (written by the queue writes up to gather t-1's)
+    // or in this gather's staging rows; its buffer was last read by gather
+    // t-1's hit copy, which precedes this gather's staging.
+    Flight &nf = c->fl[(t + 1) & 1];
+    (void)hipStreamWaitEvent(c->host, f.stage_done, 0);
+    (void)hipStreamWaitEvent(c->host, c->ev_q, 0);
+    if (prof) (void)hipEventRecord(ps.e[kEvPf0], c->host);
+    lsm::launch_prefetch(d, f.sc.gate, f.sc.staging, (uint32_t)((t + 1) % (d.L + 1)), (uint32_t)((t + 1) & 1),
+                         c->host);
+    if (prof) {
+      (void)hipEventRecord(ps.e[kEvPf1], c->host);
+      ps.pf = true;
+    }
+    (void)hipEventRecord(nf.pf_done, c->host);
+    nf.pf_ready = true;
+    if (hipGetLastError() != hipSuccess) return fail_device(c);
   }
   if (clear) c->win_batch[slot] = -1;
   if (record) {
@@ -578,7 +647,11 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   if (N == 0 || N > 0xffffffffull || R == 0 || R % 16 != 0 || S == 0 || S > (0xffffffffull / lsm::kWays) ||
       cfg->lookahead > 31 || cfg->max_batch == 0 || cfg->max_batch > (1ull << 31) ||
       (cfg->flags & ~LSMGNN_FLAG_PAGEABLE_STORE) != 0 || cfg->host_threads > 256 || cfg->policy > LSMGNN_POLICY_ROUND_ROBIN ||
-      V > (1ull << 40))
+      cfg->victim_mode > LSMGNN_VICTIM_QUEUES || V > (1ull << 40))
+    return LSMGNN_E_INVAL;
+  // the queues need a row each at least
+  const bool qmode = cfg->victim_mode == LSMGNN_VICTIM_QUEUES;
+  if (qmode && V && (V < (uint64_t)cfg->lookahead + 1 || V / ((uint64_t)cfg->lookahead + 1) > 0x7fffffffull))
     return LSMGNN_E_INVAL;
   // byte sizes must not overflow 64 bits
   if (R > (1ull << 40) || S * lsm::kWays > (~0ull / R) || (V && V > (~0ull / R))) return LSMGNN_E_INVAL;
@@ -617,6 +690,9 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   d.L = cfg->lookahead;
   d.T = cfg->near_threshold ? cfg->near_threshold : (cfg->lookahead / 8 > 1 ? cfg->lookahead / 8 : 1);
   d.policy = cfg->policy;
+  d.qmode = qmode ? lsm::kVictimQueues : lsm::kVictimFifo;
+  d.C = qmode ? V / ((uint64_t)d.L + 1) : 0;
+  const bool queues = qmode && V && d.L > 0;  // queues that can hold entries, and their prefetch buffers
   d.store = static_cast<const uint8_t *>(store_dev);  // null for a pageable store
   c->pageable = pageable;
   c->store_host = static_cast<const uint8_t *>(cfg->host_store);
@@ -625,12 +701,15 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   const uint64_t B = cfg->max_batch;
   Scratch sc{};
 
-  bool ok = dev_alloc(c, &d.sets, S) && dev_alloc(c, &d.rows, S * lsm::kWays * R) && dev_alloc(c, &d.mask, N) &&
+  bool ok = dev_alloc(c, &d.sets, S) && dev_alloc(c, &d.rows, (S * lsm::kWays + (queues ? 2 * d.C : 0)) * R) &&
+            dev_alloc(c, &d.mask, N) &&
             dev_alloc(c, &d.stat, N) && dev_alloc(c, &d.present, map_bytes) &&
             dev_alloc(c, &d.chunk_sums, d.nchunks) &&
             dev_alloc(c, &d.set_count, S) && dev_alloc(c, &d.set_idx, S) && dev_alloc(c, &d.uidx, N) &&
             dev_alloc(c, &d.tail, 2) &&
             (V == 0 || (dev_alloc(c, &d.vpos, N) && dev_alloc(c, &d.ring_tag, V))) &&
+            (!queues || (dev_alloc(c, &d.qcount, (uint64_t)d.L + 1) &&
+                         dev_alloc(c, &sc.qpart, (uint64_t)lsm::kMaxQueues * (B / lsm::kBlock + 1)))) &&
             dev_alloc(c, &c->win_ids, (uint64_t)(d.L + 1) * B) && dev_alloc(c, &c->cn, 1) &&
             dev_alloc(c, &c->cn_adv, 1) && dev_alloc(c, &sc.uniq, B) && dev_alloc(c, &sc.uset, B) &&
             dev_alloc(c, &sc.arrival, B) && dev_alloc(c, &sc.touched, B) && dev_alloc(c, &sc.seg_off, B) &&
@@ -680,10 +759,11 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
     c->host = ss.host;
     c->dma = ss.dma;
   }
-  for (hipEvent_t *e : {&c->ev_in, &c->ev_dedup, &c->ev_adv})
+  for (hipEvent_t *e : {&c->ev_in, &c->ev_dedup, &c->ev_adv, &c->ev_q})
     ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
   for (Flight &f : c->fl)
-    for (hipEvent_t *e : {&f.meta_done, &f.finish_done, &f.stage_done, &f.host_done, &f.data_done, &f.dma_done})
+    for (hipEvent_t *e : {&f.meta_done, &f.finish_done, &f.stage_done, &f.host_done, &f.data_done, &f.dma_done,
+                          &f.pf_done})
       ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
   for (PerfSet &p : c->ps)
     for (hipEvent_t &e : p.e) ok = ok && hipEventCreate(&e) == hipSuccess;
@@ -695,6 +775,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
        hipMemset(c->cn_adv, 0, sizeof(Counters)) == hipSuccess &&
        hipMemcpy(d.stat, cfg->static_score, N * 4, hipMemcpyHostToDevice) == hipSuccess &&
        (V == 0 || (hipMemset(d.vpos, 0, N * 8) == hipSuccess && hipMemset(d.ring_tag, 0xff, V * 4) == hipSuccess)) &&
+       (!queues || hipMemset(d.qcount, 0, ((uint64_t)d.L + 1) * 4) == hipSuccess) &&
        hipDeviceSynchronize() == hipSuccess;
   if (!ok) {
     (void)hipGetLastError();
@@ -735,7 +816,8 @@ lsmgnn_status lsmgnn_advance(lsmgnn_cache *c, const int64_t *ids, uint64_t n, vo
   if (n)
     lsm::launch_window_set(ids, n, c->d.N, bit, c->d.mask, c->win_ids + (uint64_t)slot * c->max_batch, record,
                            c->cn_adv, c->meta);
-  lsm::launch_finish(c->cn_adv, c->hc_adv_dev, c->fl[0].sc.stat_part, lsm::StatGrids{}, nullptr, c->meta);
+  lsm::launch_finish(c->cn_adv, c->hc_adv_dev, c->fl[0].sc.stat_part, lsm::StatGrids{}, nullptr, lsm::QueueFinish{},
+                     c->meta);
   if (hipEventRecord(c->ev_adv, c->meta) != hipSuccess || hipGetLastError() != hipSuccess ||
       hipEventSynchronize(c->ev_adv) != hipSuccess)
     return fail_device(c);
@@ -842,6 +924,20 @@ lsmgnn_status lsmgnn_export_state(lsmgnn_cache *c, uint32_t *tags, uint32_t *rin
     if (hipMemcpy(ring_tags, c->d.ring_tag, c->d.V * 4, hipMemcpyDeviceToHost) != hipSuccess) {
       (void)hipGetLastError();
       return LSMGNN_E_DEVICE;
+    }
+    if (c->d.qmode) {
+      // queue slot k holds qcount[k] entries from position 0; the rest is empty
+      uint32_t cnt[lsm::kMaxQueues] = {};
+      if (c->d.qcount &&
+          hipMemcpy(cnt, c->d.qcount, ((uint64_t)c->d.L + 1) * 4, hipMemcpyDeviceToHost) != hipSuccess) {
+        (void)hipGetLastError();
+        return LSMGNN_E_DEVICE;
+      }
+      const uint64_t C = c->d.C;
+      for (uint64_t i = 0; i < c->d.V; ++i) {
+        const uint64_t k = i / C, pos = i % C;
+        if (k > c->d.L || pos >= cnt[k]) ring_tags[i] = lsm::kEmpty;
+      }
     }
   }
   if (ring_tail) *ring_tail = c->tail;

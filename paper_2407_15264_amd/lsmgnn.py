@@ -33,14 +33,17 @@ class Config(ctypes.Structure):
     _fields_ = [("num_nodes", ctypes.c_uint64), ("row_bytes", ctypes.c_uint64), ("num_sets", ctypes.c_uint64),
                 ("victim_rows", ctypes.c_uint64), ("max_batch", ctypes.c_uint64), ("lookahead", ctypes.c_uint32),
                 ("near_threshold", ctypes.c_uint32), ("device", ctypes.c_int32), ("flags", ctypes.c_uint32),
-                ("host_threads", ctypes.c_uint32), ("policy", ctypes.c_uint32), ("host_store", ctypes.c_void_p),
-                ("static_score", ctypes.c_void_p)]
+                ("host_threads", ctypes.c_uint32), ("policy", ctypes.c_uint32), ("victim_mode", ctypes.c_uint32),
+                ("host_store", ctypes.c_void_p), ("static_score", ctypes.c_void_p)]
 
 
 FLAG_PAGEABLE_STORE = 1
 # lsmgnn_config.policy values: the method's hybrid order and the evaluation's
 # alternatives (static score only, next announced use only, round-robin)
 POLICY = {"hybrid": 0, "static": 1, "dynamic": 2, "round_robin": 3}
+# lsmgnn_config.victim_mode values: one FIFO ring, or per-reuse-iteration
+# queues prefetched into HBM before their iteration
+VICTIM_MODE = {"fifo": 0, "queues": 1}
 
 
 class Counts(ctypes.Structure):
@@ -56,6 +59,8 @@ class Profile(ctypes.Structure):
                 ("enqueue_rows", ctypes.c_uint64),
                 ("fill_ms", ctypes.c_double), ("fill_launches", ctypes.c_uint64), ("fill_rows", ctypes.c_uint64),
                 ("host_copy_ms", ctypes.c_double), ("host_copy_rows", ctypes.c_uint64),
+                ("prefetch_ms", ctypes.c_double), ("prefetch_launches", ctypes.c_uint64),
+                ("prefetch_rows", ctypes.c_uint64),
                 ("gather_ms", ctypes.c_double), ("gathers", ctypes.c_uint64)]
 
 
@@ -220,10 +225,12 @@ class FeatureCache:
     with pageable=True ordinary memory (a numpy array or an address), whose
     rows the library's host threads (host_threads, 0 = 8) copy for the GPU.
     static_score: num_nodes unsigned scores.
-    policy: a name in POLICY (or its number)."""
+    policy: a name in POLICY (or its number); victim_mode: a name in
+    VICTIM_MODE (or its number)."""
 
     def __init__(self, num_nodes, row_bytes, host_store, static_score, num_sets, victim_rows, lookahead,
-                 max_batch, near_threshold=0, device=0, pageable=False, host_threads=0, policy="hybrid"):
+                 max_batch, near_threshold=0, device=0, pageable=False, host_threads=0, policy="hybrid",
+                 victim_mode="fifo"):
         import torch
         self.device = torch.device("cuda", device)
         self.num_nodes, self.row_bytes = int(num_nodes), int(row_bytes)
@@ -241,7 +248,8 @@ class FeatureCache:
         stat = np.ascontiguousarray(np.asarray(static_score), dtype=np.uint32)
         cfg = Config(self.num_nodes, self.row_bytes, self.num_sets, self.victim_rows, self.max_batch,
                      self.lookahead, int(near_threshold), int(device), FLAG_PAGEABLE_STORE if pageable else 0,
-                     int(host_threads), int(POLICY.get(policy, policy)), ctypes.c_void_p(int(host_store)),
+                     int(host_threads), int(POLICY.get(policy, policy)),
+                     int(VICTIM_MODE.get(victim_mode, victim_mode)), ctypes.c_void_p(int(host_store)),
                      ctypes.c_void_p(stat.ctypes.data))
         h = ctypes.c_void_p()
         _check(lib().lsmgnn_cache_create(ctypes.byref(cfg), ctypes.byref(h)), "lsmgnn_cache_create")

@@ -513,3 +513,134 @@ def test_policies_workload_rmat14_pipelined(policy):
     res = run_async_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead,
                            batches, rows="all", state_every=25, label=f"{policy}-{cfg.name}", policy=policy)
     log(f"  {policy}: {res['total']}")
+
+
+# ------------------------------------------- per-iteration victim queues
+QPOL = ["hybrid", "static", "dynamic", "round_robin"]
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_queues_random_small_caches(seed):
+    """The paper's victim-queue form (a queue per reuse iteration, prefetched
+    into HBM before its iteration) on randomized small caches, blocking calls;
+    the policy rotates with the seed."""
+    n, S, V, L, T, rb, stat, batches, announce = _random_case(900 + seed)
+    V = V * (L + 1)  # C = V / (L + 1) rows per queue
+    pol = QPOL[seed % 4]
+    log(f"case: queues random seed {seed} policy {pol}: N={n} S={S} V={V} L={L} T={T} R={rb}")
+    store = Store.random_bytes(n, rb, seed)
+    run_parity(store, stat, S, V, L, batches, announce, near_threshold=T, rows="all", label=f"queues{seed}",
+               policy=pol, victim_mode="queues")
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_queues_long_streams_pipelined(seed):
+    """90 minibatches through the pipelined entry point: every queue slot is
+    reused many times, and each gather's prefetch overlaps the next gather's
+    metadata."""
+    n, S, V, L, T, stat, batches = _long_case(60 + seed)
+    V = max(V, 1) * (L + 1)
+    if seed % 3 == 2:
+        V = L + 1  # one row per queue: most candidates are dropped
+    log(f"case: queues long stream seed {seed}: N={n} S={S} V={V} L={L} T={T}")
+    store = Store.random_bytes(n, 32, seed)
+    run_async_parity(store, stat, S, V, L, batches, rows="all", near_threshold=T, label=f"queues-long{seed}",
+                     state_every=10, victim_mode="queues")
+
+
+def test_queues_worked_example():
+    """Eight lines evicted at gather 1 with next use at minibatch 4 fill queue
+    4 in eviction order; with C = 5 the last three are dropped, and gather 4
+    serves five victim hits from the prefetched queue."""
+    log("case: queues worked example")
+    n, L = 16, 4
+    stat = np.zeros(n, np.uint32)
+    stat[:8] = [5, 3, 4, 0, 2, 1, 7, 6]
+    batches = [np.arange(8), np.arange(8, 16), np.array([], np.int64), np.array([], np.int64), np.arange(8)]
+    for C in (8, 5):
+        store = Store.random_bytes(n, 64, C)
+        run_parity(store, stat, 1, 5 * C, L, batches, rows="all", state_every=1, label=f"queue-example-C{C}",
+                   victim_mode="queues")
+
+
+def test_queues_workload_rmat14_pipelined():
+    cfg = W.CONFIGS[1]
+    log(f"case: queues {cfg.name} pipelined")
+    wl, batches = config_stream(cfg)
+    store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
+    run_async_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead, batches,
+                     rows="all", state_every=5, label=f"queues-{cfg.name}", victim_mode="queues")
+
+
+@pytest.mark.timeout(600)
+def test_queues_workload_rmat20_first_60_pipelined():
+    cfg = W.CONFIGS[2]
+    log(f"case: queues {cfg.name} first 60 pipelined")
+    wl, batches = config_stream(cfg, 60)
+    store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
+    res = run_async_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead,
+                           batches, rows=4, store_gpu=device_store(store), state_every=20,
+                           label=f"queues-{cfg.name}", victim_mode="queues")
+    assert res["total"]["victim_hits"] > 0
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_queues_pageable_store(seed):
+    n, S, V, L, T, rb, stat, batches, announce = _random_case(950 + seed)
+    V = max(V, 1) * (L + 1)
+    log(f"case: queues pageable seed {seed}: N={n} S={S} V={V} L={L}")
+    store = Store.random_bytes(n, rb, seed, pinned=False)
+    if seed % 2:
+        run_async_parity(store, stat, S, V, L, batches, rows="all", near_threshold=T, label=f"queues-pg{seed}",
+                         state_every=3, victim_mode="queues")
+    else:
+        run_parity(store, stat, S, V, L, batches, announce, near_threshold=T, rows="all", label=f"queues-pg{seed}",
+                   victim_mode="queues")
+
+
+@pytest.mark.parametrize("pipelined", [False, True])
+def test_queues_rejected_gathers_in_between(pipelined):
+    """A rejected gather between good ones changes nothing, also the queue
+    that the previous good gather prefetched for the next one."""
+    log(f"case: queues with rejected gathers, pipelined={pipelined}")
+    rng = np.random.default_rng(77)
+    n, S, V, L, mb = 400, 3, 3 * 5, 4, 64
+    store = Store.random_bytes(n, 32, 5)
+    stat = rng.integers(0, 9, n).astype(np.uint32)
+    batches = [rng.integers(0, n, int(rng.integers(20, mb + 1))) for _ in range(30)]
+    cache = lsmgnn.FeatureCache(n, 32, store.buf, stat, S, V, L, mb, victim_mode="queues")
+    orc = Oracle(n, 32, stat, S, V, L, store=store.np, victim_mode="queues")
+    dev = lambda a: torch.as_tensor(np.asarray(a, np.int64)).cuda()  # noqa: E731
+    db = [dev(b) for b in batches]
+    out, uq, inv, oc = (torch.empty(mb * 32, dtype=torch.uint8, device="cuda"),
+                        torch.empty(mb, dtype=torch.int64, device="cuda"),
+                        torch.empty(mb, dtype=torch.int64, device="cuda"),
+                        torch.empty(mb, dtype=torch.uint8, device="cuda"))
+    for j in range(L + 1):
+        cache.advance(db[j])
+        orc.advance(batches[j])
+    vh = 0
+    for b in range(len(batches) - L - 1):
+        if b % 3 == 1:  # a bad list first
+            with pytest.raises(lsmgnn.LsmgnnError) as e:
+                if pipelined:
+                    cache.gather_async(dev([0, n + b]), out, uq, inverse=inv, outcome=oc, announce=db[b + L + 1])
+                else:
+                    cache.gather(dev([0, n + b]), out=out, unique=uq, inverse=inv, outcome=oc)
+            assert e.value.status == "E_RANGE"
+        if pipelined:
+            tk, r = cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc, announce=db[b + L + 1])
+            cache.wait(tk)
+            torch.cuda.current_stream().synchronize()
+        else:
+            r = cache.gather(db[b], out=out, unique=uq, inverse=inv, outcome=oc)
+            cache.advance(db[b + L + 1])
+        o = orc.gather(batches[b])
+        orc.advance(batches[b + L + 1])
+        assert np.array_equal(r.outcome.cpu().numpy(), o["outcome"]), b
+        assert np.array_equal(r.out.cpu().numpy(), o["out"]), b
+        vh += int((o["outcome"] == 1).sum())
+    compare_state(cache, orc, "queues after rejected gathers")
+    assert vh > 0
+    cache.close()
+    orc.close()

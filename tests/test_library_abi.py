@@ -57,16 +57,18 @@ def test_set_index_helper_matches_oracle(L):
 
 @pytest.mark.parametrize("bad", [dict(num_sets=0), dict(row_bytes=24), dict(lookahead=32), dict(max_batch=0),
                                  dict(num_nodes=0), dict(num_nodes=1 << 32), dict(flags=2), dict(flags=1 << 31),
-                                 dict(flags=1, host_threads=257), dict(policy=4), dict(policy=1 << 31)])
+                                 dict(flags=1, host_threads=257), dict(policy=4), dict(policy=1 << 31),
+                                 dict(victim_mode=2), dict(victim_mode=1, victim_rows=1, lookahead=1)])
 def test_bad_config_rejected_before_device(L, bad):
     stat = np.ones(16, np.uint32)
     store = np.zeros(16 * 16, np.uint8)
     kw = dict(num_nodes=16, row_bytes=16, num_sets=2, victim_rows=2, max_batch=8, lookahead=1, near_threshold=0,
-              device=0, flags=0, host_threads=0, policy=0)
+              device=0, flags=0, host_threads=0, policy=0, victim_mode=0)
     kw.update(bad)
     cfg = lsmgnn.Config(kw["num_nodes"], kw["row_bytes"], kw["num_sets"], kw["victim_rows"], kw["max_batch"],
                         kw["lookahead"], kw["near_threshold"], kw["device"], kw["flags"], kw["host_threads"],
-                        kw["policy"], ctypes.c_void_p(store.ctypes.data), ctypes.c_void_p(stat.ctypes.data))
+                        kw["policy"], kw["victim_mode"], ctypes.c_void_p(store.ctypes.data),
+                        ctypes.c_void_p(stat.ctypes.data))
     h = ctypes.c_void_p()
     assert L.lsmgnn_cache_create(ctypes.byref(cfg), ctypes.byref(h)) == lsmgnn.E_INVAL
     assert not h.value
