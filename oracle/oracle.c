@@ -13,8 +13,11 @@
  *   - reuse "dynamic value" is read as the distance d from the current gather to
  *     the next announced use; d <= T is the kept "near" level, T < d <= L the
  *     "far" level; T defaults to max(1, floor(L/8));
- *   - the dynamic information is exact at every gather (refresh period 1);
- *   - "recently inserted" = inserted during the current gather;
+ *   - the dynamic information (each resident line's next reuse iteration) is
+ *     updated before every U-th gather (U = 1 by default: exact at every
+ *     gather), from the lists announced by then; a line inserted since the
+ *     last update has none ("recently inserted"), and a recorded reuse
+ *     iteration that has passed counts as recently used, the same level;
  *   - ties at equal level and equal static score go to the lowest way index,
  *     and empty ways are always filled first, lowest index first;
  *   - the victim buffer is one FIFO ring of V entries that overwrites its
@@ -52,7 +55,9 @@ typedef struct {
 
 struct orc_cache {
   uint64_t num_nodes, num_sets, victim_rows;
-  uint32_t row_bytes, ways, lookahead, near_thr, policy, vmode;
+  uint32_t row_bytes, ways, lookahead, near_thr, policy, vmode, period;
+  uint64_t t_upd;    /* gather index of the last update of the dynamic information */
+  int64_t *rl;       /* [num_sets][ways] next reuse iteration recorded at that update, or -1 */
   uint64_t qcap, nslots; /* queue mode: rows per queue, queue slots */
   uint64_t *qcnt;        /* [nslots] entries in each queue */
   uint32_t *qbits;       /* [num_nodes] bit k: the node has an entry in slot k */
@@ -104,7 +109,8 @@ static int contains(const ann_list *l, int64_t x) {
 
 int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const uint32_t *static_score,
                uint64_t num_sets, uint32_t ways, uint64_t victim_rows, uint32_t lookahead,
-               uint32_t near_threshold, uint32_t policy, uint32_t victim_mode, orc_cache **out) {
+               uint32_t near_threshold, uint32_t policy, uint32_t victim_mode, uint32_t refresh_period,
+               orc_cache **out) {
   if (!out || !static_score) return ORC_E_INVAL;
   *out = NULL;
   if (num_nodes == 0 || num_nodes > 0xffffffffULL || row_bytes == 0 || row_bytes % 16 != 0 ||
@@ -123,6 +129,7 @@ int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const 
   c->lookahead = lookahead;
   c->policy = policy;
   c->vmode = victim_mode;
+  c->period = refresh_period ? refresh_period : 1;
   c->nslots = (uint64_t)lookahead + 1;
   c->qcap = victim_mode == ORC_VICTIM_QUEUES ? victim_rows / c->nslots : 0;
   /* Sec. 4.2: the default threshold is one eighth of the window; at least 1 */
@@ -136,12 +143,13 @@ int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const 
   c->rr = (uint32_t *)calloc(num_sets, sizeof(uint32_t));
   c->qcnt = (uint64_t *)calloc(c->nslots, sizeof(uint64_t));
   c->qbits = (uint32_t *)calloc(num_nodes, sizeof(uint32_t));
-  if (!c->stat || !c->tag || !c->ins || !c->vtag || !c->where || !c->rr || !c->qcnt || !c->qbits) {
+  c->rl = (int64_t *)malloc(num_sets * ways * sizeof(int64_t));
+  if (!c->stat || !c->tag || !c->ins || !c->vtag || !c->where || !c->rr || !c->qcnt || !c->qbits || !c->rl) {
     orc_destroy(c);
     return ORC_E_NOMEM;
   }
   memcpy(c->stat, static_score, num_nodes * sizeof(uint32_t));
-  for (uint64_t i = 0; i < num_sets * ways; ++i) { c->tag[i] = EMPTY; c->ins[i] = -1; }
+  for (uint64_t i = 0; i < num_sets * ways; ++i) { c->tag[i] = EMPTY; c->ins[i] = -1; c->rl[i] = -1; }
   for (uint64_t k = 0; k < victim_rows; ++k) c->vtag[k] = EMPTY;
   for (uint64_t v = 0; v < num_nodes; ++v) c->where[v] = -1;
   *out = c;
@@ -153,7 +161,7 @@ void orc_destroy(orc_cache *c) {
   for (uint64_t j = 0; j < c->n_ann; ++j) free(c->ann[j].ids);
   free(c->ann);
   free(c->stat); free(c->tag); free(c->ins); free(c->vtag); free(c->where); free(c->rr);
-  free(c->qcnt); free(c->qbits);
+  free(c->qcnt); free(c->qbits); free(c->rl);
   free(c);
 }
 
@@ -184,22 +192,6 @@ int orc_advance(orc_cache *c, const int64_t *ids, uint64_t n) {
   return ORC_OK;
 }
 
-/* Dynamic information (Sec. 4.2): the class of the line in way w of set s while
-   gather t is served.  Lines inserted during gather t have no reuse
-   information yet ("recently inserted").  Otherwise the announced lists of the
-   next L minibatches are scanned for the line's node: none -> no reuse; the
-   nearest use at distance d <= T -> near; T < d <= L -> far. */
-static int line_class(const orc_cache *c, uint64_t s, uint32_t w) {
-  uint64_t i = s * c->ways + w;
-  if (c->ins[i] == (int64_t)c->t) return CLS_R;
-  for (uint64_t d = 1; d <= c->lookahead; ++d) {
-    uint64_t j = c->t + d;
-    if (j < c->n_ann && contains(&c->ann[j], (int64_t)c->tag[i]))
-      return d <= c->near_thr ? CLS_C : CLS_F;
-  }
-  return CLS_N;
-}
-
 /* Distance from the current gather to the next announced use of node x
    (1..L), or 0 when none of the next L minibatches names it (Sec. 4.2, the
    next reuse iteration). */
@@ -209,6 +201,39 @@ static uint64_t reuse_distance(const orc_cache *c, uint32_t x) {
     if (j < c->n_ann && contains(&c->ann[j], (int64_t)x)) return d;
   }
   return 0;
+}
+
+/* The update of the dynamic information (Sec. 4.2), run before every U-th
+   gather: the next reuse iteration of every resident line from the announced
+   lists of the next L minibatches. */
+static void update_reuse(orc_cache *c) {
+  c->t_upd = c->t;
+  for (uint64_t i = 0; i < c->num_sets * c->ways; ++i) {
+    uint64_t d = c->tag[i] == EMPTY ? 0 : reuse_distance(c, c->tag[i]);
+    c->rl[i] = d ? (int64_t)(c->t + d) : -1;
+  }
+}
+
+/* Dynamic information (Sec. 4.2): the class of the line in way w of set s while
+   gather t is served.  A line inserted since the last update has no reuse
+   information ("recently inserted"); so is treated a line whose recorded
+   reuse iteration has passed.  Otherwise, with d the distance to the recorded
+   reuse iteration: none -> no reuse; d <= T -> near; T < d -> far. */
+static int line_class(const orc_cache *c, uint64_t s, uint32_t w) {
+  uint64_t i = s * c->ways + w;
+  if (c->ins[i] >= (int64_t)c->t_upd) return CLS_R;
+  if (c->rl[i] < 0) return CLS_N;
+  if (c->rl[i] <= (int64_t)c->t) return CLS_R;
+  return (uint64_t)(c->rl[i] - (int64_t)c->t) <= c->near_thr ? CLS_C : CLS_F;
+}
+
+/* The dynamic-only policy's view (Sec. 5): the distance to the line's recorded
+   reuse iteration, or 0 (no expected reuse) when it has none, it has passed,
+   or the line was inserted since the last update. */
+static uint64_t line_distance(const orc_cache *c, uint64_t s, uint32_t w) {
+  uint64_t i = s * c->ways + w;
+  if (c->ins[i] >= (int64_t)c->t_upd || c->rl[i] <= (int64_t)c->t) return 0;
+  return (uint64_t)(c->rl[i] - (int64_t)c->t);
 }
 
 /* Eviction priority, lowest level evicted first.  Hybrid order (Sec. 4.2):
@@ -248,6 +273,7 @@ int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t 
   uint64_t U = 0;
   int64_t *uniq = sorted_unique(ids, n, &U);
   if (!uniq) return ORC_E_NOMEM;
+  if (c->t % c->period == 0) update_reuse(c);
   orc_counts st;
   memset(&st, 0, sizeof st);
   st.batch = c->t;
@@ -306,7 +332,7 @@ int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t 
           /* no announced use first, then the furthest next use, then the lowest way */
           uint64_t best = 0;
           for (uint32_t w = 0; w < c->ways; ++w) {
-            uint64_t d = reuse_distance(c, tag[w]);
+            uint64_t d = line_distance(c, s, w);
             uint64_t far = d ? d : c->lookahead + 1;
             if (pick == c->ways || far > best) {
               best = far;
@@ -325,7 +351,7 @@ int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t 
         ++st.evictions;
         if (c->vmode == ORC_VICTIM_QUEUES && c->qcap && (cls == CLS_F || cls == CLS_C)) {
           /* the queue of the line's next reuse iteration, unless it is full */
-          uint64_t slot = (c->t + reuse_distance(c, z)) % c->nslots;
+          uint64_t slot = (uint64_t)c->rl[s * c->ways + pick] % c->nslots;
           if (c->qcnt[slot] < c->qcap) {
             c->vtag[slot * c->qcap + c->qcnt[slot]] = z;
             ++c->qcnt[slot];

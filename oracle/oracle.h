@@ -57,7 +57,8 @@ uint64_t orc_set_of(uint64_t x, uint64_t num_sets);
 /* store may be NULL: gather then skips row copies (metadata-only runs) */
 int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const uint32_t *static_score,
                uint64_t num_sets, uint32_t ways, uint64_t victim_rows, uint32_t lookahead,
-               uint32_t near_threshold, uint32_t policy, uint32_t victim_mode, orc_cache **out);
+               uint32_t near_threshold, uint32_t policy, uint32_t victim_mode, uint32_t refresh_period,
+               orc_cache **out);
 void orc_destroy(orc_cache *c);
 int orc_advance(orc_cache *c, const int64_t *ids, uint64_t n);
 /* out (U rows), uniq (U), inv (n), outcome (U) may each be NULL */

@@ -63,7 +63,7 @@ def lib():
         L.orc_set_of.restype = u64
         L.orc_set_of.argtypes = [u64, u64]
         L.orc_create.restype = i32
-        L.orc_create.argtypes = [u64, u32, vp, vp, u64, u32, u64, u32, u32, u32, u32, ctypes.POINTER(vp)]
+        L.orc_create.argtypes = [u64, u32, vp, vp, u64, u32, u64, u32, u32, u32, u32, u32, ctypes.POINTER(vp)]
         L.orc_pagerank.restype = i32
         L.orc_pagerank.argtypes = [u64, vp, vp, ctypes.c_double, u32, vp]
         L.orc_rank_scores.restype = i32
@@ -105,7 +105,8 @@ class Oracle:
     ``policy`` is a name in POLICIES (or its number)."""
 
     def __init__(self, num_nodes, row_bytes, static_score, num_sets, victim_rows,
-                 lookahead, near_threshold=0, ways=8, store=None, policy="hybrid", victim_mode="fifo"):
+                 lookahead, near_threshold=0, ways=8, store=None, policy="hybrid", victim_mode="fifo",
+                 refresh_period=1):
         self.num_nodes = int(num_nodes)
         self.row_bytes = int(row_bytes)
         self.num_sets = int(num_sets)
@@ -119,7 +120,7 @@ class Oracle:
         rc = lib().orc_create(self.num_nodes, self.row_bytes, _ptr(self.store), _ptr(self.static),
                               self.num_sets, self.ways, self.victim_rows, int(lookahead),
                               int(near_threshold), POLICIES.get(policy, policy),
-                              VICTIM_MODES.get(victim_mode, victim_mode), ctypes.byref(h))
+                              VICTIM_MODES.get(victim_mode, victim_mode), int(refresh_period), ctypes.byref(h))
         if rc:
             raise OracleError(rc, "orc_create")
         self._h = h

@@ -5,8 +5,10 @@ It is written from the rules of the paper (arXiv 2407.15264, Sec. 4.2 levels and
 static tie-break, Sec. 4.3.1 victim-buffer enqueue, Sec. 4.3.2 level swap) with
 different data structures from the oracle: Python lists of (node, inserted_at)
 pairs per set, the victim ring as a plain list searched linearly, the window as
-the list of announced Python sets scanned at every class query, and victim
-selection by sorting all candidates.  The set-index function is injected.
+the list of announced Python sets scanned at every update of the dynamic
+information (a dict of recorded next uses per resident node), victim queues as
+a dict of lists keyed by iteration, and victim selection by sorting all
+candidates.  The set-index function is injected.
 """
 from __future__ import annotations
 
@@ -15,7 +17,7 @@ NEAR, FAR, RECENT, NONE = "near", "far", "recent", "none"
 
 class NaiveCache:
     def __init__(self, num_nodes, num_sets, ways, victim_rows, lookahead, static, set_of,
-                 near_threshold=0, policy="hybrid", victim_mode="fifo"):
+                 near_threshold=0, policy="hybrid", victim_mode="fifo", refresh_period=1):
         self.N, self.S, self.W, self.V, self.L = num_nodes, num_sets, ways, victim_rows, lookahead
         self.T = near_threshold or max(1, lookahead // 8)
         self.static = list(static)
@@ -30,6 +32,9 @@ class NaiveCache:
         self.queues = victim_mode == "queues"
         self.C = victim_rows // (lookahead + 1) if self.queues else 0
         self.q = {}  # queue mode: reuse iteration j -> evicted nodes, in eviction order
+        self.U = refresh_period
+        self.t_upd = 0
+        self.info = {}  # node -> next reuse iteration seen at the last update (resident nodes only)
 
     def advance(self, ids):
         if len(self.announced) > self.t + self.L:
@@ -39,15 +44,26 @@ class NaiveCache:
         self.announced.append(set(int(x) for x in ids))
         return "OK"
 
+    def _update(self):
+        self.t_upd = self.t
+        self.info = {}
+        for ways in self.sets:
+            for e in ways:
+                if e is not None:
+                    uses = [j for j in range(self.t + 1, self.t + self.L + 1)
+                            if j < len(self.announced) and e[0] in self.announced[j]]
+                    self.info[e[0]] = min(uses) if uses else None
+
     def _class(self, entry):
         node, at = entry
-        if at == self.t:
-            return RECENT
-        for d in range(1, self.L + 1):
-            j = self.t + d
-            if j < len(self.announced) and node in self.announced[j]:
-                return NEAR if d <= self.T else FAR
-        return NONE
+        if at >= self.t_upd:
+            return RECENT  # no dynamic information yet
+        r = self.info.get(node)
+        if r is None:
+            return NONE
+        if r <= self.t:
+            return RECENT  # its recorded reuse has come
+        return NEAR if r - self.t <= self.T else FAR
 
     def _level(self, cls):
         order = [FAR, NONE, RECENT, NEAR] if self.V > 0 else [NONE, FAR, RECENT, NEAR]
@@ -57,6 +73,8 @@ class NaiveCache:
         if any(not (0 <= x < self.N) for x in ids):
             return "E_RANGE", None
         uniq = sorted(set(int(x) for x in ids))
+        if self.t % self.U == 0:
+            self._update()
         st = dict(hits=0, victim_hits=0, misses=0, evictions=0, enqueued=0, dropped=0)
         outcome = []
         for x in uniq:
@@ -83,7 +101,7 @@ class NaiveCache:
                 cls = self._class(ways[w])
                 st["evictions"] += 1
                 if self.queues and self.C > 0 and cls in (FAR, NEAR):
-                    j = self.t + self._next_use(ways[w][0])
+                    j = self.info[ways[w][0]]
                     if len(self.q.setdefault(j, [])) < self.C:
                         self.q[j].append(ways[w][0])
                         self.tail += 1
@@ -101,10 +119,13 @@ class NaiveCache:
         self.t += 1
         return "OK", dict(uniq=uniq, outcome="".join(outcome), **st)
 
-    def _next_use(self, node):
-        uses = [d for d in range(1, self.L + 1)
-                if self.t + d < len(self.announced) and node in self.announced[self.t + d]]
-        return min(uses) if uses else None
+    def _next_use(self, entry):
+        """Distance to the recorded reuse, or None without usable information."""
+        node, at = entry
+        r = self.info.get(node)
+        if at >= self.t_upd or r is None or r <= self.t:
+            return None
+        return r - self.t
 
     def _victim(self, s, ways):
         if self.policy == "hybrid":
@@ -113,7 +134,7 @@ class NaiveCache:
             return sorted((self.static[e[0]], w) for w, e in enumerate(ways))[0][1]
         if self.policy == "dynamic":
             # no announced use counts as further than any announced one
-            far = [(self.L + 1 if self._next_use(e[0]) is None else self._next_use(e[0])) for e in ways]
+            far = [(self.L + 1 if self._next_use(e) is None else self._next_use(e)) for e in ways]
             return sorted((-f, w) for w, f in enumerate(far))[0][1]
         w = self.pointer[s]
         self.pointer[s] = (w + 1) % self.W

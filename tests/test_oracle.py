@@ -336,8 +336,9 @@ def test_policy_rejected_when_unknown():
 
 
 # ------------------------------------------------------- naive brute force
-def _naive_run(n, S, ways, V, L, T, stat, batches, announce, policy="hybrid", victim_mode="fifo"):
-    m = NaiveCache(n, S, ways, V, L, stat, lambda x: set_of(x, S), T, policy=policy, victim_mode=victim_mode)
+def _naive_run(n, S, ways, V, L, T, stat, batches, announce, policy="hybrid", victim_mode="fifo", U=1):
+    m = NaiveCache(n, S, ways, V, L, stat, lambda x: set_of(x, S), T, policy=policy, victim_mode=victim_mode,
+                   refresh_period=U)
     out = []
     for j in range(min(L + 1, len(announce))):
         assert m.advance(announce[j]) == "OK"
@@ -349,9 +350,10 @@ def _naive_run(n, S, ways, V, L, T, stat, batches, announce, policy="hybrid", vi
     return m, out
 
 
-def _compare(n, S, ways, V, L, T, stat, batches, announce, policy="hybrid", victim_mode="fifo"):
-    m, exp = _naive_run(n, S, ways, V, L, T, stat, batches, announce, policy, victim_mode)
-    o = Oracle(n, 16, stat, S, V, L, near_threshold=T, ways=ways, policy=policy, victim_mode=victim_mode)
+def _compare(n, S, ways, V, L, T, stat, batches, announce, policy="hybrid", victim_mode="fifo", U=1):
+    m, exp = _naive_run(n, S, ways, V, L, T, stat, batches, announce, policy, victim_mode, U)
+    o = Oracle(n, 16, stat, S, V, L, near_threshold=T, ways=ways, policy=policy, victim_mode=victim_mode,
+               refresh_period=U)
     got = _drive(o, batches, L, announce)
     for e, g in zip(exp, got):
         assert "".join(CODE[c] for c in g["outcome"]) == e["outcome"]
@@ -528,3 +530,71 @@ def test_queue_mode_needs_a_row_per_queue():
     with pytest.raises(OracleError) as e:
         Oracle(10, 16, np.ones(10, np.uint32), 2, 3, 3, victim_mode="queues")  # V = 3 < L + 1 = 4
     assert e.value.status == "E_INVAL"
+
+
+# ------------------------------------------ update period of the dynamic information
+# Sec. 4.2 updates the lines' next reuse iterations every few iterations; lines
+# inserted since the last update lack dynamic information (recently inserted).
+def test_lines_inserted_since_the_update_are_recent():
+    # A = 0 (static 5), B = 1 (static 1), C = 2; L = 2 (T = 1).  At gather 1, B's
+    # next use is gather 2 (near) and A has none.  Updating every gather, A (no
+    # reuse) is evicted for C; updating every third gather, both still count as
+    # recently inserted at gather 1 and the lower static score, B, goes.
+    stat = np.array([5, 1, 9], np.uint32)
+    batches = [np.array([0, 1]), np.array([2]), np.array([1])]
+    for U, gone in ((1, 0), (3, 1)):
+        o = Oracle(3, 16, stat, 1, 0, 2, ways=2, refresh_period=U)
+        _drive(o, batches[:2], 2, batches)
+        assert gone not in o.export_state()["tags"][0].tolist(), U
+
+
+def test_a_passed_reuse_counts_as_recent():
+    # C = 0 (static 9), X = 2 (static 1), Y = 3 (static 5); L = 2.  Updated at
+    # gather 2, X's next use is gather 3.  At gather 3 (no update with U = 2)
+    # that recorded use has come, so X ranks as recent and Y (no reuse) makes
+    # room for C: X is then a hit.  Updated at gather 3 (U = 1), X has no further
+    # use, loses on its static score, and is a miss.
+    stat = np.array([9, 0, 1, 5], np.uint32)
+    batches = [np.array([2, 3]), np.array([], np.int64), np.array([], np.int64), np.array([0, 2])]
+    for U, outcome_x in ((2, HIT), (1, MISS)):
+        o = Oracle(4, 16, stat, 1, 0, 2, ways=2, refresh_period=U)
+        r = _drive(o, batches, 2)[3]
+        assert r["outcome"][list(r["uniq"]).index(2)] == outcome_x, U
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_no_update_reduces_hybrid_to_static_order(seed):
+    # With no update after the first (empty) one, no line ever has dynamic
+    # information: the hybrid order is the static order over all lines.
+    rng = np.random.default_rng(seed)
+    n, S, L = 40, 2, 3
+    stat = rng.integers(0, 6, n).astype(np.uint32)
+    batches = [rng.integers(0, n, int(rng.integers(1, 12))) for _ in range(12)]
+    a = Oracle(n, 16, stat, S, 0, L, ways=3, refresh_period=1000)
+    b = Oracle(n, 16, stat, S, 0, L, ways=3, policy="static")
+    ra, rb = _drive(a, batches, L), _drive(b, batches, L)
+    for x, y in zip(ra, rb):
+        assert np.array_equal(x["outcome"], y["outcome"])
+    assert np.array_equal(a.export_state()["tags"], b.export_state()["tags"])
+
+
+@pytest.mark.parametrize("mode", ["fifo", "queues"])
+@pytest.mark.parametrize("policy", POLICY_NAMES)
+@pytest.mark.parametrize("seed", range(40))
+def test_update_period_random_small_against_naive_model(seed, policy, mode):
+    rng = np.random.default_rng(7000 + seed)
+    n = int(rng.integers(2, 14))
+    S = int(rng.integers(1, 4))
+    ways = int(rng.integers(1, 4))
+    L = int(rng.choice([0, 1, 2, 3, 5, 9]))
+    V = int(rng.choice([0, 1, 2, 3])) * (L + 1)
+    T = int(rng.choice([0, 0, 1, 2]))
+    U = int(rng.choice([2, 3, 4, 7]))
+    stat = rng.integers(0, 4, n).astype(np.uint32)
+    nb = int(rng.integers(1, 12))
+    batches = [rng.integers(0, n, rng.integers(0, 8)) for _ in range(nb)]
+    if rng.random() < 0.5:
+        announce = [rng.integers(0, n, rng.integers(0, 8)) for _ in range(nb + L)]
+    else:
+        announce = batches
+    _compare(n, S, ways, V, L, T, stat, batches, announce, policy, mode, U)
