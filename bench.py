@@ -116,7 +116,7 @@ def make_parts(W, cfg, nb):
     return parts, requests
 
 
-def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None, victim_mode="fifo"):
+def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None, victim_mode="fifo", refresh_period=1):
     """The CPU oracle (single-threaded C, one instance per part) on the same
     stream from gather 0, stopped after about budget_s seconds."""
     from oracle.oracle import Oracle
@@ -125,7 +125,8 @@ def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None, victim_mode
         sh = p["shape"]
         o = Oracle(p["num_nodes"], p["R"], p["static"], sh.num_sets,
                    sh.victim_rows if victim_rows is None else victim_rows, sh.lookahead,
-                   near_threshold=sh.near_threshold, store=p["store_np"], policy=policy, victim_mode=victim_mode)
+                   near_threshold=sh.near_threshold, store=p["store_np"], policy=policy, victim_mode=victim_mode,
+                   refresh_period=refresh_period)
         for j in range(sh.lookahead + 1):
             o.advance(p["batches"][j])
         orcs.append(o)
@@ -194,6 +195,8 @@ def main():
     ap.add_argument("--policy", default="hybrid", choices=["hybrid", "static", "dynamic", "round_robin"],
                     help="eviction policy: the method's hybrid order or one of the evaluation's alternatives")
     ap.add_argument("--no-ring", action="store_true", help="no victim buffer (and so no PVP level swap)")
+    ap.add_argument("--refresh-period", type=int, default=1,
+                    help="update period of the dynamic information (1: exact at every gather)")
     ap.add_argument("--victim-mode", default="fifo", choices=["fifo", "queues"],
                     help="victim buffer: one FIFO ring, or per-reuse-iteration queues prefetched into HBM")
     ap.add_argument("--train-us", type=float, default=0.0,
@@ -281,7 +284,7 @@ def main():
                                          0 if args.no_ring else sh.victim_rows, sh.lookahead, mb,
                                          near_threshold=sh.near_threshold, pageable=not p["pinned"],
                                          host_threads=args.host_threads, policy=args.policy,
-                                         victim_mode=args.victim_mode)
+                                         victim_mode=args.victim_mode, refresh_period=args.refresh_period)
         # three output sets rotate: at most two gathers are in flight
         p["bufs"] = [(torch.empty(mb * p["R"], dtype=torch.uint8, device=dev),
                       torch.empty(mb, dtype=torch.int64, device=dev),
@@ -409,6 +412,7 @@ def main():
         "config": dict(cfg.describe(), feature_dtype="fp32" if cfg.elt_bytes == 4 else "fp16",
                        minibatches_timed=args.steps, policy=args.policy, static_score=static_info,
                        victim_ring="off" if args.no_ring else "on", victim_mode=args.victim_mode,
+                       refresh_period=args.refresh_period,
                        simulated_training_us=args.train_us,
                        first_timed_minibatch=args.warmup,
                        api=("lsmgnn_gather + lsmgnn_advance" if args.sync
@@ -429,7 +433,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(parts, args.cpu_budget, args.policy, 0 if args.no_ring else None,
-                                           args.victim_mode)
+                                           args.victim_mode, args.refresh_period)
         res["cpu_baseline"]["gpu_over_cpu"] = gbps / res["cpu_baseline"]["value"]
     for p in parts:
         p["cache"].close()

@@ -108,6 +108,16 @@ typedef struct {
   uint32_t host_threads; /* pageable store: host threads copying rows (0 selects 8) */
   uint32_t policy;      /* LSMGNN_POLICY_*; other values are rejected */
   uint32_t victim_mode; /* LSMGNN_VICTIM_*; other values are rejected */
+  /* Update period U of the dynamic information (Sec. 4.2); 0 selects 1.  U = 1:
+     every gather sees each resident line's exact next use among the next
+     lookahead minibatches.  U > 1: before every U-th gather (gather index a
+     multiple of U) each resident line records its next reuse iteration from
+     the lists announced by then; until the next update, a line inserted since
+     then, or whose recorded iteration has come, ranks as recently inserted,
+     and the others by the distance to the recorded iteration.  Costs one pass
+     over the S * 8 lines per update instead of one window lookup per
+     eviction candidate. */
+  uint32_t refresh_period;
   /* Backing store: num_nodes * row_bytes bytes of host memory, row v at offset
      v * row_bytes.  Borrowed: the caller keeps it alive and unchanged while
      the cache exists; the library only reads it.

@@ -415,6 +415,47 @@ __device__ __forceinline__ uint32_t dist_from_bits(uint32_t m, uint32_t t, uint3
   return rel ? (uint32_t)__builtin_ctz(rel) + 1u : 0u;
 }
 
+// The update of the dynamic information (Sec. 4.2) with an update period U >
+// 1, before every U-th gather: each resident line records 1 + its next reuse
+// iteration from the announced-batch bits (0: none).  Skipped when the
+// gather's IDs were rejected; the retry of the same gather runs it.
+__global__ __launch_bounds__(kBlock) void k_refresh(const DevState d, uint32_t t, const Counters *cn) {
+  if (cn->err) return;
+  const uint64_t lines = d.S * kWays;
+  for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < lines; i += (uint64_t)gridDim.x * kBlock) {
+    const uint32_t tag = d.sets[i / kWays].tag[i % kWays];
+    uint32_t r = 0;
+    if (tag != kEmpty) {
+      const uint32_t dist = dist_from_bits(d.mask[tag], t, d.L);
+      r = dist ? t + dist + 1u : 0u;
+    }
+    d.lreuse[i] = r;
+  }
+}
+
+void launch_refresh(const DevState &d, uint32_t t, const Counters *cn, hipStream_t s) {
+  hipLaunchKernelGGL(k_refresh, dim3(grid_for(d.S * kWays, kBlock, kMaxGrid)), dim3(kBlock), 0, s, d, t, cn);
+}
+
+// Class and next-reuse distance of a batch-start resident from the
+// information recorded at the last update (update period U > 1): inserted at
+// or after that update, or its recorded reuse has come -> recently inserted
+// (distance 0); none recorded -> no reuse; else near or far by the distance.
+__device__ __forceinline__ void class_from_record(uint32_t rec, uint32_t ins, uint32_t t, uint32_t t_upd, uint32_t T,
+                                                  uint32_t &cls, uint32_t &dist) {
+  dist = 0;
+  if (ins >= t_upd) {
+    cls = kClsRecent;
+  } else if (rec == 0) {
+    cls = kClsNone;
+  } else if (rec - 1u <= t) {
+    cls = kClsRecent;
+  } else {
+    dist = rec - 1u - t;
+    cls = dist <= T ? kClsNear : kClsFar;
+  }
+}
+
 // eviction level, lowest evicted first: none < far < recent < near, or with
 // the victim ring on, far < none < recent < near
 __device__ __forceinline__ uint32_t level_of(uint32_t cls, bool ring_on) {
@@ -492,11 +533,15 @@ __global__ __launch_bounds__(kBlock) void k_set_walk(const DevState d, Scratch s
       if (emptym) {
         pick = (uint32_t)__builtin_ctz(emptym);
       } else {
-        if (!known) {  // batch-start resident: class from its announced-use bits
-          const uint32_t m = d.mask[tag];
-          cls = (ins == t) ? kClsRecent : class_from_bits(m, t, d.L, d.T);
+        if (!known) {  // batch-start resident
+          if (d.U > 1) {  // from the information recorded at the last update
+            class_from_record(d.lreuse[s * kWays + w], ins, t, t - t % d.U, d.T, cls, dist);
+          } else {        // exact: from its announced-use bits
+            const uint32_t m = d.mask[tag];
+            cls = (ins == t) ? kClsRecent : class_from_bits(m, t, d.L, d.T);
+            if (P == kPolicyDynamic || d.qmode) dist = dist_from_bits(m, t, d.L);
+          }
           lvl = level_of(cls, ring_on);
-          if (P == kPolicyDynamic || d.qmode) dist = dist_from_bits(m, t, d.L);
           known = true;
         }
         if constexpr (P == kPolicyHybrid) {
@@ -535,7 +580,7 @@ __global__ __launch_bounds__(kBlock) void k_set_walk(const DevState d, Scratch s
         ins = t;
         cls = kClsRecent;
         lvl = recent_lvl;
-        if constexpr (P == kPolicyDynamic) dist = dist_from_bits(d.mask[x], t, d.L);
+        dist = 0;  // a line inserted by this gather has no dynamic information yet
         known = true;
         last = (int32_t)u;
       }

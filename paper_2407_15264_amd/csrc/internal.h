@@ -177,6 +177,8 @@ struct DevState {
   uint32_t qmode;        // kVictimQueues: per-reuse-iteration queues instead of the ring
   uint64_t C;            // queue mode: rows per queue, V / (L + 1)
   uint32_t *qcount;      // queue mode: [L + 1] entries in each queue slot
+  uint32_t U;            // update period of the dynamic information (1: exact at every gather)
+  uint32_t *lreuse;      // U > 1: [S*8] 1 + next reuse iteration recorded at the last update, or 0
   // queue mode: the two prefetch buffers (C rows each, by gather parity) are
   // rows S*8 .. S*8 + 2C of `rows`, after the cache lines
 };
@@ -203,6 +205,8 @@ void launch_group_by_set(const DevState &d, const int64_t *ids, uint64_t n, int6
                          Counters *cn, hipStream_t s);
 void launch_set_walk(const DevState &d, uint64_t n, uint32_t t, Scratch &sc, Counters *cn, StatGrids &grids,
                      hipStream_t s);
+// U > 1, before every U-th gather's set walk: record every resident line's next reuse iteration
+void launch_refresh(const DevState &d, uint32_t t, const Counters *cn, hipStream_t s);
 // t: the gather's index (queue mode serves queue t from prefetch buffer t & 1)
 void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, uint8_t *outcome, Counters *cn,
                          StatGrids &grids, hipStream_t s);

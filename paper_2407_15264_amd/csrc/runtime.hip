@@ -468,6 +468,7 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
     lsm::launch_dedup(d, ids, n, ann_n ? an.ids : nullptr, ann_n, clear_ids, clear_n, (uint32_t)(t & 31u), f.sc,
                       unique_ids, c->cn, c->dd_dev, c->meta);
   (void)hipEventRecord(c->ev_dedup, c->meta);
+  if (d.U > 1 && t % d.U == 0) lsm::launch_refresh(d, (uint32_t)t, c->cn, c->meta);
   lsm::StatGrids grids{};
   if (n) {
     lsm::launch_group_by_set(d, ids, n, inverse, f.sc, c->cn, c->meta);
@@ -692,6 +693,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   d.policy = cfg->policy;
   d.qmode = qmode ? lsm::kVictimQueues : lsm::kVictimFifo;
   d.C = qmode ? V / ((uint64_t)d.L + 1) : 0;
+  d.U = cfg->refresh_period ? cfg->refresh_period : 1;
   const bool queues = qmode && V && d.L > 0;  // queues that can hold entries, and their prefetch buffers
   d.store = static_cast<const uint8_t *>(store_dev);  // null for a pageable store
   c->pageable = pageable;
@@ -708,6 +710,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
             dev_alloc(c, &d.set_count, S) && dev_alloc(c, &d.set_idx, S) && dev_alloc(c, &d.uidx, N) &&
             dev_alloc(c, &d.tail, 2) &&
             (V == 0 || (dev_alloc(c, &d.vpos, N) && dev_alloc(c, &d.ring_tag, V))) &&
+            (d.U == 1 || dev_alloc(c, &d.lreuse, S * lsm::kWays)) &&
             (!queues || (dev_alloc(c, &d.qcount, (uint64_t)d.L + 1) &&
                          dev_alloc(c, &sc.qpart, (uint64_t)lsm::kMaxQueues * (B / lsm::kBlock + 1)))) &&
             dev_alloc(c, &c->win_ids, (uint64_t)(d.L + 1) * B) && dev_alloc(c, &c->cn, 1) &&
@@ -776,6 +779,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
        hipMemcpy(d.stat, cfg->static_score, N * 4, hipMemcpyHostToDevice) == hipSuccess &&
        (V == 0 || (hipMemset(d.vpos, 0, N * 8) == hipSuccess && hipMemset(d.ring_tag, 0xff, V * 4) == hipSuccess)) &&
        (!queues || hipMemset(d.qcount, 0, ((uint64_t)d.L + 1) * 4) == hipSuccess) &&
+       (d.U == 1 || hipMemset(d.lreuse, 0, S * lsm::kWays * 4) == hipSuccess) &&
        hipDeviceSynchronize() == hipSuccess;
   if (!ok) {
     (void)hipGetLastError();

@@ -34,7 +34,8 @@ class Config(ctypes.Structure):
                 ("victim_rows", ctypes.c_uint64), ("max_batch", ctypes.c_uint64), ("lookahead", ctypes.c_uint32),
                 ("near_threshold", ctypes.c_uint32), ("device", ctypes.c_int32), ("flags", ctypes.c_uint32),
                 ("host_threads", ctypes.c_uint32), ("policy", ctypes.c_uint32), ("victim_mode", ctypes.c_uint32),
-                ("host_store", ctypes.c_void_p), ("static_score", ctypes.c_void_p)]
+                ("refresh_period", ctypes.c_uint32), ("host_store", ctypes.c_void_p),
+                ("static_score", ctypes.c_void_p)]
 
 
 FLAG_PAGEABLE_STORE = 1
@@ -226,11 +227,12 @@ class FeatureCache:
     rows the library's host threads (host_threads, 0 = 8) copy for the GPU.
     static_score: num_nodes unsigned scores.
     policy: a name in POLICY (or its number); victim_mode: a name in
-    VICTIM_MODE (or its number)."""
+    VICTIM_MODE (or its number); refresh_period: the update period of the
+    dynamic information (1 = exact at every gather)."""
 
     def __init__(self, num_nodes, row_bytes, host_store, static_score, num_sets, victim_rows, lookahead,
                  max_batch, near_threshold=0, device=0, pageable=False, host_threads=0, policy="hybrid",
-                 victim_mode="fifo"):
+                 victim_mode="fifo", refresh_period=1):
         import torch
         self.device = torch.device("cuda", device)
         self.num_nodes, self.row_bytes = int(num_nodes), int(row_bytes)
@@ -249,7 +251,8 @@ class FeatureCache:
         cfg = Config(self.num_nodes, self.row_bytes, self.num_sets, self.victim_rows, self.max_batch,
                      self.lookahead, int(near_threshold), int(device), FLAG_PAGEABLE_STORE if pageable else 0,
                      int(host_threads), int(POLICY.get(policy, policy)),
-                     int(VICTIM_MODE.get(victim_mode, victim_mode)), ctypes.c_void_p(int(host_store)),
+                     int(VICTIM_MODE.get(victim_mode, victim_mode)), int(refresh_period),
+                     ctypes.c_void_p(int(host_store)),
                      ctypes.c_void_p(stat.ctypes.data))
         h = ctypes.c_void_p()
         _check(lib().lsmgnn_cache_create(ctypes.byref(cfg), ctypes.byref(h)), "lsmgnn_cache_create")

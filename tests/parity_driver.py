@@ -73,7 +73,7 @@ def compare_state(cache, orc, where=""):
 
 def run_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, announce=None,
                near_threshold=0, rows="all", max_batch=None, device=0, state_every=0, label="parity",
-               store_gpu=None, policy="hybrid", victim_mode="fifo"):
+               store_gpu=None, policy="hybrid", victim_mode="fifo", refresh_period=1):
     """rows: 'all' -> compare every gathered row with the oracle's; an int k ->
     compare with the oracle on every k-th gather and, on every gather, with the
     backing-store rows indexed on the GPU (store_gpu, a device copy)."""
@@ -84,9 +84,10 @@ def run_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, 
     L = lookahead
     cache = lsmgnn.FeatureCache(store.num_nodes, store.row_bytes, store.buf, static, num_sets, victim_rows, L, mb,
                                 near_threshold=near_threshold, device=device, pageable=not store.pinned,
-                                policy=policy, victim_mode=victim_mode)
+                                policy=policy, victim_mode=victim_mode, refresh_period=refresh_period)
     orc = Oracle(store.num_nodes, store.row_bytes, static, num_sets, victim_rows, L,
-                 near_threshold=near_threshold, store=store.np, policy=policy, victim_mode=victim_mode)
+                 near_threshold=near_threshold, store=store.np, policy=policy, victim_mode=victim_mode,
+                 refresh_period=refresh_period)
     dev_ann = [torch.as_tensor(np.asarray(a, np.int64)).to(dev) for a in announce]
     dev_bat = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in batches]
     for j in range(min(L + 1, len(announce))):
@@ -155,7 +156,8 @@ class _Lane:
     rows are compared once it has been waited for."""
 
     def __init__(self, store, static, num_sets, victim_rows, lookahead, batches, rows, store_gpu, label,
-                 combined, near_threshold, device, row_sample=0, policy="hybrid", victim_mode="fifo"):
+                 combined, near_threshold, device, row_sample=0, policy="hybrid", victim_mode="fifo",
+                 refresh_period=1):
         import torch
         self.torch = torch
         self.store, self.row_sample = store, row_sample
@@ -166,9 +168,11 @@ class _Lane:
         self.combined = combined
         self.cache = lsmgnn.FeatureCache(store.num_nodes, store.row_bytes, store.buf, static, num_sets, victim_rows,
                                          lookahead, self.mb, near_threshold=near_threshold, device=device,
-                                         pageable=not store.pinned, policy=policy, victim_mode=victim_mode)
+                                         pageable=not store.pinned, policy=policy, victim_mode=victim_mode,
+                                         refresh_period=refresh_period)
         self.orc = Oracle(store.num_nodes, store.row_bytes, static, num_sets, victim_rows, lookahead,
-                          near_threshold=near_threshold, store=store.np, policy=policy, victim_mode=victim_mode)
+                          near_threshold=near_threshold, store=store.np, policy=policy, victim_mode=victim_mode,
+                          refresh_period=refresh_period)
         self.db = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in batches]
         self.bufs = [(torch.empty(self.mb * store.row_bytes, dtype=torch.uint8, device=dev),
                       torch.empty(self.mb, dtype=torch.int64, device=dev),
@@ -262,13 +266,13 @@ def _run_lanes(lanes, nb, state_every, label):
 
 def run_async_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, rows="all", store_gpu=None,
                      state_every=0, label="async", combined=True, near_threshold=0, device=0, row_sample=0,
-                     policy="hybrid", victim_mode="fifo"):
+                     policy="hybrid", victim_mode="fifo", refresh_period=1):
     """One cache in the launch configuration of bench.py, against the oracle:
     unique IDs, inverse, outcomes and rows of every gather (rows as in
     run_parity), counters as totals, the cache and ring state every
     `state_every` gathers and at the end."""
     ln = _Lane(store, static, num_sets, victim_rows, lookahead, batches, rows, store_gpu, label, combined,
-               near_threshold, device, row_sample, policy, victim_mode)
+               near_threshold, device, row_sample, policy, victim_mode, refresh_period)
     totals, seconds = _run_lanes([ln], len(batches), state_every, label)
     return dict(total=totals[0], seconds=seconds)
 

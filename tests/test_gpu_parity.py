@@ -644,3 +644,44 @@ def test_queues_rejected_gathers_in_between(pipelined):
     assert vh > 0
     cache.close()
     orc.close()
+
+
+# ------------------------------- update period of the dynamic information
+@pytest.mark.parametrize("seed", range(16))
+def test_update_period_random_small_caches(seed):
+    """Dynamic information updated every U-th gather (U > 1): lines inserted
+    since the update rank as recently inserted, passed reuses as recent.
+    Policy and victim-buffer form rotate with the seed."""
+    n, S, V, L, T, rb, stat, batches, announce = _random_case(1100 + seed)
+    U = [2, 3, 4, 7][seed % 4]
+    pol = QPOL[(seed // 4) % 4]
+    mode = "queues" if seed % 2 else "fifo"
+    if mode == "queues":
+        V = V * (L + 1)
+    log(f"case: update period {U} seed {seed} policy {pol} {mode}: N={n} S={S} V={V} L={L} T={T} R={rb}")
+    store = Store.random_bytes(n, rb, seed)
+    run_parity(store, stat, S, V, L, batches, announce, near_threshold=T, rows="all", label=f"upd{seed}",
+               policy=pol, victim_mode=mode, refresh_period=U)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_update_period_long_streams_pipelined(seed):
+    n, S, V, L, T, stat, batches = _long_case(80 + seed)
+    U = [2, 4, 5][seed % 3]
+    mode = "queues" if seed >= 3 else "fifo"
+    if mode == "queues":
+        V = max(V, 1) * (L + 1)
+    log(f"case: update period {U} long stream seed {seed} {mode}: N={n} S={S} V={V} L={L} T={T}")
+    store = Store.random_bytes(n, 32, seed)
+    run_async_parity(store, stat, S, V, L, batches, rows="all", near_threshold=T, label=f"upd-long{seed}",
+                     state_every=10, victim_mode=mode, refresh_period=U)
+
+
+@pytest.mark.parametrize("U", [2, 4])
+def test_update_period_workload_rmat14_pipelined(U):
+    cfg = W.CONFIGS[1]
+    log(f"case: update period {U}, {cfg.name} pipelined")
+    wl, batches = config_stream(cfg)
+    store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
+    run_async_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead, batches,
+                     rows="all", state_every=5, label=f"upd{U}-{cfg.name}", refresh_period=U)

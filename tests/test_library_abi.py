@@ -63,11 +63,11 @@ def test_bad_config_rejected_before_device(L, bad):
     stat = np.ones(16, np.uint32)
     store = np.zeros(16 * 16, np.uint8)
     kw = dict(num_nodes=16, row_bytes=16, num_sets=2, victim_rows=2, max_batch=8, lookahead=1, near_threshold=0,
-              device=0, flags=0, host_threads=0, policy=0, victim_mode=0)
+              device=0, flags=0, host_threads=0, policy=0, victim_mode=0, refresh_period=0)
     kw.update(bad)
     cfg = lsmgnn.Config(kw["num_nodes"], kw["row_bytes"], kw["num_sets"], kw["victim_rows"], kw["max_batch"],
                         kw["lookahead"], kw["near_threshold"], kw["device"], kw["flags"], kw["host_threads"],
-                        kw["policy"], kw["victim_mode"], ctypes.c_void_p(store.ctypes.data),
+                        kw["policy"], kw["victim_mode"], kw["refresh_period"], ctypes.c_void_p(store.ctypes.data),
                         ctypes.c_void_p(stat.ctypes.data))
     h = ctypes.c_void_p()
     assert L.lsmgnn_cache_create(ctypes.byref(cfg), ctypes.byref(h)) == lsmgnn.E_INVAL
