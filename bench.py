@@ -116,6 +116,17 @@ def make_parts(W, cfg, nb):
     return parts, requests
 
 
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
 def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None, victim_mode="fifo", refresh_period=1):
     """The CPU oracle (single-threaded C, one instance per part) on the same
     stream from gather 0, stopped after about budget_s seconds."""
@@ -149,7 +160,7 @@ def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None, victim_mode
                       f"{dt:.1f} s), rows copied with memcpy from the host store",
             "rows_per_s": rows / dt,
         "parts": len(parts), "seconds_per_minibatch": dt / max(done, 1),
-            "cpu": platform.processor() or platform.machine()}
+            "cpu": _cpu_model(), "host_cpus": os.cpu_count()}
 
 
 def hit_path_alone(parts, b, reps=5):
