@@ -13,8 +13,9 @@ Default workload: R-MAT graph with 2^20 nodes and 2^24 edges (a, b, c, d =
 0.57, 0.19, 0.19, 0.05), fp32 x 256 features (1 GiB pinned host store), GraphSAGE
 sampling of 1024 seeds per minibatch with fanout (15, 10, 5), an 8-way cache
 holding 10% of the nodes, a victim ring of 5% of the nodes, lookahead 4.
---config picks another shape; the typed graph (4) runs one cache per node type
-and a step gathers the minibatch's IDs of every type.
+--workload picks another shape by name; the typed graph (rmat-20M-e250M-4types)
+runs one cache per node type and a step gathers the minibatch's IDs of every
+type.
 
 Prints one JSON line.  `value` is gathered feature bytes (unique rows x row
 bytes) per second over the timed steps; `roofline` rates the dominant data
@@ -198,7 +199,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=180)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", type=int, default=2, help="workload shape (1 to 5; 4 is the typed graph)")
+    ap.add_argument("--workload", default="rmat-s20-deg16-f32x256",
+                    choices=["rmat-s14-e18-f32x128", "rmat-s20-deg16-f32x256", "rmat-10M-e120M-f32x1024",
+                             "rmat-20M-e250M-4types", "rmat-100M-e1.6B-f16x1024"],
+                    help="workload shape by name")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--host-threads", type=int, default=16,
@@ -219,7 +223,7 @@ def main():
                     help="blocking lsmgnn_gather per minibatch instead of the pipelined lsmgnn_gather_async")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on exactly one GPU: this build has no multi-GPU path (asked for --gpus "
+        print(f"bench.py runs on exactly one GPU: the library has no multi-GPU path (asked for --gpus "
               f"{args.gpus}). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
@@ -230,7 +234,7 @@ def main():
 
     lsmgnn.lib()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    cfg = {**W.CONFIGS, **W.HETERO}[args.config]
+    cfg = W.WORKLOADS[args.workload]
     L = cfg.lookahead if isinstance(cfg, W.HeteroConfig) else cfg.cache.lookahead
     if args.warmup + args.steps > cfg.batches:
         print(f"bench.py: {args.warmup + args.steps} minibatches needed, the workload has {cfg.batches}",

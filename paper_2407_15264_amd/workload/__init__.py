@@ -76,18 +76,25 @@ def _cache_lines_for(bytes_budget: int, row_bytes: int) -> int:
     return bytes_budget // row_bytes
 
 
-# The homogeneous workload shapes.  Cache/ring budgets in GiB; cache sets are
-# the budget in rows divided by the 8 ways.
+# Workload names, smallest to largest.
+RMAT14 = "rmat-s14-e18-f32x128"
+RMAT20 = "rmat-s20-deg16-f32x256"
+RMAT10M = "rmat-10M-e120M-f32x1024"
+TYPED20M = "rmat-20M-e250M-4types"
+RMAT100M = "rmat-100M-e1.6B-f16x1024"
+
+# The homogeneous workload shapes, by name.  Cache/ring budgets in GiB; cache
+# sets are the budget in rows divided by the 8 ways.
 CONFIGS = {
-    1: WorkloadConfig("rmat-s14-e18-f32x128", 1 << 14, 1 << 18, 128, 4, 20, 256, (10, 5),
+    RMAT14: WorkloadConfig(RMAT14, 1 << 14, 1 << 18, 128, 4, 20, 256, (10, 5),
                       CacheShape(num_sets=2048, victim_rows=1024, lookahead=2)),
-    2: WorkloadConfig("rmat-s20-deg16-f32x256", 1 << 20, 1 << 24, 256, 4, 200, 1024, (15, 10, 5),
+    RMAT20: WorkloadConfig(RMAT20, 1 << 20, 1 << 24, 256, 4, 200, 1024, (15, 10, 5),
                       CacheShape(num_sets=int(0.10 * (1 << 20)) // 8, victim_rows=int(0.05 * (1 << 20)),
                                  lookahead=4)),
-    3: WorkloadConfig("rmat-10M-e120M-f32x1024", 10_000_000, 120_000_000, 1024, 4, 500, 4096, (10, 5, 5),
+    RMAT10M: WorkloadConfig(RMAT10M, 10_000_000, 120_000_000, 1024, 4, 500, 4096, (10, 5, 5),
                       CacheShape(num_sets=_cache_lines_for(8 * GIB, 4096) // 8,
                                  victim_rows=_cache_lines_for(4 * GIB, 4096), lookahead=8)),
-    5: WorkloadConfig("rmat-100M-e1.6B-f16x1024", 100_000_000, 1_600_000_000, 1024, 2, 1000, 8192, (15, 10, 5),
+    RMAT100M: WorkloadConfig(RMAT100M, 100_000_000, 1_600_000_000, 1024, 2, 1000, 8192, (15, 10, 5),
                       CacheShape(num_sets=_cache_lines_for(96 * GIB, 2048) // 8,
                                  victim_rows=_cache_lines_for(32 * GIB, 2048), lookahead=16)),
 }
@@ -156,9 +163,12 @@ class HeteroConfig:
 # The heterogeneous workload shape: 4 node types (40/30/20/10 %), fp32 widths
 # 1024/768/256/128, caches totalling 32 GiB of HBM, rings totalling 16 GiB.
 HETERO = {
-    4: HeteroConfig("rmat-20M-e250M-4types", 20_000_000, 250_000_000, (0.4, 0.3, 0.2, 0.1), (1024, 768, 256, 128), 4,
+    TYPED20M: HeteroConfig(TYPED20M, 20_000_000, 250_000_000, (0.4, 0.3, 0.2, 0.1), (1024, 768, 256, 128), 4,
                     500, 8192, (10, 5, 5), 32 * GIB, 16 * GIB, 8),
 }
+
+# every workload, smallest to largest
+WORKLOADS = {n: {**CONFIGS, **HETERO}[n] for n in (RMAT14, RMAT20, RMAT10M, TYPED20M, RMAT100M)}
 
 # key offset of the node-type permutation (distinct from the seed-node permutation)
 TYPE_PERM_SEED = 0x54595045
@@ -352,6 +362,6 @@ def near_threshold_default(lookahead: int) -> int:
     return max(1, lookahead // 8)
 
 
-__all__ = ["CONFIGS", "HETERO", "HeteroConfig", "HeteroWorkload", "WorkloadConfig", "CacheShape", "Workload", "Graph", "rmat_graph",
+__all__ = ["RMAT14", "RMAT20", "RMAT10M", "TYPED20M", "RMAT100M", "WORKLOADS", "CONFIGS", "HETERO", "HeteroConfig", "HeteroWorkload", "WorkloadConfig", "CacheShape", "Workload", "Graph", "rmat_graph",
            "seed_permutation", "sample_batches", "features", "fill_features", "build", "splitmix_at",
            "near_threshold_default", "pin_plan", "PINNED_BUDGET", "math"]

@@ -83,9 +83,9 @@ def test_no_entries_at_all():
     assert np.allclose(r, 0.2, rtol=1e-15, atol=0) and (s == 4294967295).all()
 
 
-@pytest.mark.parametrize("config", [1, 2])
-def test_workload_graphs(config):
-    cfg = W.CONFIGS[config]
+@pytest.mark.parametrize("name", ["rmat-s14-e18-f32x128", "rmat-s20-deg16-f32x256"])
+def test_workload_graphs(name):
+    cfg = W.CONFIGS[name]
     log(f"case: pagerank {cfg.name}")
     g = W.rmat_graph(cfg.num_nodes, cfg.num_edges, cfg.rmat, cfg.seed)
     _check(g.offsets, g.adj, 0.85, 20, cfg.name)
@@ -111,7 +111,7 @@ def test_errors_leave_scores_unwritten():
 
 def test_cache_parity_with_pagerank_scores():
     # the GPU's scores drive both the library's cache and the oracle's
-    cfg = W.CONFIGS[1]
+    cfg = W.CONFIGS[W.RMAT14]
     log(f"case: cache parity with reverse-PageRank static scores, {cfg.name}")
     wl = W.Workload(cfg)
     off_t = torch.as_tensor(wl.graph.offsets).cuda()

@@ -33,7 +33,7 @@ def _gpu():
 
 
 def test_workload_rmat14_full_parity():
-    cfg = W.CONFIGS[1]
+    cfg = W.CONFIGS[W.RMAT14]
     log(f"case: {cfg.name}, all {cfg.batches} gathers, all rows")
     wl, batches = config_stream(cfg)
     store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
@@ -45,7 +45,7 @@ def test_workload_rmat14_full_parity():
 
 @pytest.mark.timeout(600)
 def test_workload_rmat20_parity():
-    cfg = W.CONFIGS[2]
+    cfg = W.CONFIGS[W.RMAT20]
     log(f"case: {cfg.name}, all {cfg.batches} gathers; rows vs oracle every 20th gather, "
         f"vs the backing store on the GPU for every gather")
     wl, batches = config_stream(cfg)
@@ -66,7 +66,7 @@ def test_workload_rmat10m_full_size_pipelined_parity():
     oracle, rows against the backing store (a device copy); every 50th gather:
     rows against the oracle's; every 100th and at the end: cache and ring
     state; at the end: all counters."""
-    cfg = W.CONFIGS[3]
+    cfg = W.CONFIGS[W.RMAT10M]
     log(f"case: {cfg.name}, all {cfg.batches} gathers, pipelined, full size")
     t0 = time.time()
     wl, batches = config_stream(cfg)
@@ -90,7 +90,7 @@ def test_workload_typed_20m_full_size_pipelined_parity():
     16 GiB of rings, 500 minibatches of 8192 seeds), one cache per type, all in
     the bench's launch configuration.  Checks as for the 10M-node workload,
     per type."""
-    cfg = W.HETERO[4]
+    cfg = W.HETERO[W.TYPED20M]
     log(f"case: {cfg.name}, all {cfg.batches} gathers per type, pipelined, full size")
     t0 = time.time()
     wl = W.HeteroWorkload(cfg)
@@ -241,7 +241,7 @@ def test_bad_configs_rejected():
 
 
 def test_deterministic_state():
-    cfg = W.CONFIGS[1]
+    cfg = W.CONFIGS[W.RMAT14]
     wl, batches = config_stream(cfg)
     store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes)
     states = []
@@ -297,7 +297,7 @@ def _run_async_parity(store, static, S, V, L, batches, label, combined=True):
 
 
 def test_async_pipeline_rmat14():
-    cfg = W.CONFIGS[1]
+    cfg = W.CONFIGS[W.RMAT14]
     log(f"case: pipelined gathers, {cfg.name}")
     wl, batches = config_stream(cfg)
     store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
@@ -307,7 +307,7 @@ def test_async_pipeline_rmat14():
 
 @pytest.mark.timeout(600)
 def test_async_pipeline_rmat20_first_60():
-    cfg = W.CONFIGS[2]
+    cfg = W.CONFIGS[W.RMAT20]
     log(f"case: pipelined gathers, {cfg.name}, first 60 minibatches")
     wl, batches = config_stream(cfg, 60)
     store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
@@ -369,7 +369,7 @@ def test_pageable_store_random(seed):
 
 
 def test_pageable_store_rmat14_pipelined():
-    cfg = W.CONFIGS[1]
+    cfg = W.CONFIGS[W.RMAT14]
     log(f"case: pageable store, {cfg.name}, pipelined")
     wl, batches = config_stream(cfg)
     store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed, pinned=False)
@@ -506,7 +506,7 @@ def test_policies_adversarial(name, policy):
 
 @pytest.mark.parametrize("policy", POLICIES)
 def test_policies_workload_rmat14_pipelined(policy):
-    cfg = W.CONFIGS[1]
+    cfg = W.CONFIGS[W.RMAT14]
     log(f"case: policy {policy} {cfg.name} pipelined")
     wl, batches = config_stream(cfg)
     store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
@@ -564,7 +564,7 @@ def test_queues_worked_example():
 
 
 def test_queues_workload_rmat14_pipelined():
-    cfg = W.CONFIGS[1]
+    cfg = W.CONFIGS[W.RMAT14]
     log(f"case: queues {cfg.name} pipelined")
     wl, batches = config_stream(cfg)
     store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
@@ -574,7 +574,7 @@ def test_queues_workload_rmat14_pipelined():
 
 @pytest.mark.timeout(600)
 def test_queues_workload_rmat20_first_60_pipelined():
-    cfg = W.CONFIGS[2]
+    cfg = W.CONFIGS[W.RMAT20]
     log(f"case: queues {cfg.name} first 60 pipelined")
     wl, batches = config_stream(cfg, 60)
     store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
@@ -679,7 +679,7 @@ def test_update_period_long_streams_pipelined(seed):
 
 @pytest.mark.parametrize("U", [2, 4])
 def test_update_period_workload_rmat14_pipelined(U):
-    cfg = W.CONFIGS[1]
+    cfg = W.CONFIGS[W.RMAT14]
     log(f"case: update period {U}, {cfg.name} pipelined")
     wl, batches = config_stream(cfg)
     store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)

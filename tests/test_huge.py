@@ -28,7 +28,7 @@ PREFIX = 300  # minibatches checked: the cache fills after about 75 of them
 def test_rmat100m_full_size_pipelined_prefix():
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
-    cfg = W.CONFIGS[5]
+    cfg = W.CONFIGS[W.RMAT100M]
     log(f"case: {cfg.name}, first {PREFIX} minibatches, pipelined, full size, pageable store")
     t0 = time.time()
     wl = W.Workload(cfg, PREFIX)

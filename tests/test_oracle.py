@@ -167,7 +167,7 @@ def _drive(o, batches, L, announce=None, check=None):
 
 
 def test_invariants_on_small_rmat_stream():
-    cfg = W.CONFIGS[1]
+    cfg = W.CONFIGS[W.RMAT14]
     wl = W.Workload(cfg)
     store = W.features(cfg.num_nodes, cfg.dim)
     o = Oracle(cfg.num_nodes, cfg.row_bytes, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows,
