@@ -244,6 +244,20 @@ void lsmgnn_host_free(void *ptr);
    `stream`. */
 lsmgnn_status lsmgnn_copy_bytes(void *dst, const void *src, uint64_t bytes, void *stream);
 
+/* Rows in request order: out[i] <- rows[inverse[i]] for i < n, row_bytes each
+   (a positive multiple of 16).  rows is a gather's output (one row per unique
+   ID) and inverse its inverse index; together they give every requested
+   position its feature row, as a minibatch consumer indexes them (the paper's
+   prefetched rows go to their positions in the minibatch, Sec. 4.3.2).  All
+   pointers are DEVICE memory; rows and out 16-byte aligned, inverse 8-byte
+   aligned; every inverse[i] must index a row of `rows` (a gather's inverse
+   does).  Queued on `stream` after the work already there (the gather's
+   output is ready once the caller's stream has waited for it); returns
+   without waiting.  Errors: E_INVAL (NULL pointer with n > 0, bad row_bytes
+   or alignment), E_DEVICE. */
+lsmgnn_status lsmgnn_expand(const void *rows, const int64_t *inverse, uint64_t n, uint64_t row_bytes, void *out,
+                            void *stream);
+
 /* Static score from the graph: the normalized reverse PageRank that Sec. 4.2
    names as the hybrid policy's static information (and the evaluation's static
    policy uses, Sec. 5), as an alternative to the in-degree.

@@ -215,6 +215,8 @@ void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t t, Scratch &sc,
 // placed by gather t from its staging rows; sizes from gather t's gate.
 void launch_prefetch(const DevState &d, const Gate *gate, const uint8_t *staging, uint32_t slot, uint32_t par,
                      hipStream_t s);
+// out[i] <- rows[inv[i]] for i < n (R bytes each)
+void launch_expand(const uint8_t *rows, const int64_t *inv, uint64_t n, uint64_t R, uint8_t *out, hipStream_t s);
 // n bounds the gather's unique count (the copies read the exact one from the gate)
 void launch_copy(CopyMode mode, const DevState &d, uint64_t n, const Scratch &sc, uint8_t *out, hipStream_t s);
 void launch_window_set(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask, int64_t *slot_ids,

@@ -949,6 +949,19 @@ lsmgnn_status lsmgnn_export_state(lsmgnn_cache *c, uint32_t *tags, uint32_t *rin
   return LSMGNN_OK;
 }
 
+lsmgnn_status lsmgnn_expand(const void *rows, const int64_t *inverse, uint64_t n, uint64_t row_bytes, void *out,
+                            void *stream) {
+  if (n == 0) return LSMGNN_OK;
+  if (!rows || !inverse || !out || row_bytes == 0 || row_bytes % 16 != 0 || n > (1ull << 40) ||
+      (reinterpret_cast<uintptr_t>(rows) & 15u) || (reinterpret_cast<uintptr_t>(out) & 15u) ||
+      (reinterpret_cast<uintptr_t>(inverse) & 7u))
+    return LSMGNN_E_INVAL;
+  lsm::launch_expand(static_cast<const uint8_t *>(rows), inverse, n, row_bytes, static_cast<uint8_t *>(out),
+                     static_cast<hipStream_t>(stream));
+  if (hipGetLastError() != hipSuccess) return LSMGNN_E_DEVICE;
+  return LSMGNN_OK;
+}
+
 lsmgnn_status lsmgnn_copy_bytes(void *dst, const void *src, uint64_t bytes, void *stream) {
   if (!dst || !src || bytes % 16 != 0 || (reinterpret_cast<uintptr_t>(dst) & 15u) ||
       (reinterpret_cast<uintptr_t>(src) & 15u))

@@ -110,6 +110,8 @@ def lib():
         L.lsmgnn_copy_bytes.argtypes = [vp, vp, u64, vp]
         L.lsmgnn_pagerank_scores.restype = i32
         L.lsmgnn_pagerank_scores.argtypes = [vp, vp, u64, ctypes.c_double, ctypes.c_uint32, vp, vp, i32, vp]
+        L.lsmgnn_expand.restype = i32
+        L.lsmgnn_expand.argtypes = [vp, vp, u64, u64, vp, vp]
         L.lsmgnn_strerror.restype = ctypes.c_char_p
         L.lsmgnn_strerror.argtypes = [i32]
         _lib = L
@@ -129,6 +131,21 @@ def copy_bytes(dst_ptr: int, src_ptr: int, nbytes: int, stream=None, device=0):
     """Calibration copy (device or pinned host pointers), synchronous."""
     _check(lib().lsmgnn_copy_bytes(ctypes.c_void_p(dst_ptr), ctypes.c_void_p(src_ptr), int(nbytes),
                                    _stream_handle(stream, device)), "lsmgnn_copy_bytes")
+
+
+def expand(rows, inverse, row_bytes, out=None, stream=None, device=0):
+    """Rows in request order (lsmgnn_expand): out[i] = rows[inverse[i]].  rows:
+    a gather's unique-row output (uint8 device tensor), inverse: its int64
+    inverse index (n entries).  Returns `out` (uint8, n * row_bytes), allocated
+    when not given."""
+    import torch
+    n = inverse.numel()
+    if out is None:
+        out = torch.empty(max(n, 1) * row_bytes, dtype=torch.uint8, device=inverse.device)
+    _check(lib().lsmgnn_expand(ctypes.c_void_p(rows.data_ptr()), ctypes.c_void_p(inverse.data_ptr()), n,
+                               int(row_bytes), ctypes.c_void_p(out.data_ptr()), _stream_handle(stream, device)),
+           "lsmgnn_expand")
+    return out[: n * row_bytes]
 
 
 def pagerank_scores(offsets, adj, damping=0.85, iterations=20, rank=False, device=0, stream=None):

@@ -685,3 +685,42 @@ def test_update_period_workload_rmat14_pipelined(U):
     store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
     run_async_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead, batches,
                      rows="all", state_every=5, label=f"upd{U}-{cfg.name}", refresh_period=U)
+
+
+# ------------------------------------------------- rows in request order
+@pytest.mark.parametrize("rb", [16, 48, 64, 1024])
+def test_expand_gives_every_request_its_row(rb):
+    """lsmgnn_expand after a gather: row i of the result is the stored row of
+    request i (closed form), duplicates included."""
+    log(f"case: expand R={rb}")
+    rng = np.random.default_rng(rb)
+    n_nodes, S, V, L = 5000, 16, 64, 2
+    store = Store.random_bytes(n_nodes, rb, rb)
+    stat = rng.integers(0, 9, n_nodes).astype(np.uint32)
+    batches = [rng.integers(0, n_nodes, int(rng.integers(1, 3000))) for _ in range(8)]
+    mb = max(b.size for b in batches)
+    cache = lsmgnn.FeatureCache(n_nodes, rb, store.buf, stat, S, V, L, mb)
+    for j in range(L + 1):
+        cache.advance(torch.as_tensor(batches[j]).cuda())
+    for b, ids in enumerate(batches):
+        ids_t = torch.as_tensor(ids).cuda()
+        r = cache.gather(ids_t, inverse=True)
+        rows = lsmgnn.expand(r.out, r.inverse, rb)
+        torch.cuda.synchronize()
+        got = rows.cpu().numpy().reshape(ids.size, rb)
+        assert np.array_equal(got, store.np[ids]), b
+        if b + L + 1 < len(batches):
+            cache.advance(torch.as_tensor(batches[b + L + 1]).cuda())
+    cache.close()
+
+
+def test_expand_arguments():
+    log("case: expand arguments")
+    L = lsmgnn.lib()
+    rows = torch.zeros(64, dtype=torch.uint8, device="cuda")
+    inv = torch.zeros(2, dtype=torch.int64, device="cuda")
+    out = torch.zeros(64, dtype=torch.uint8, device="cuda")
+    assert L.lsmgnn_expand(None, None, 0, 16, None, None) == lsmgnn.OK  # nothing to do
+    assert L.lsmgnn_expand(rows.data_ptr(), inv.data_ptr(), 2, 24, out.data_ptr(), None) == lsmgnn.E_INVAL
+    assert L.lsmgnn_expand(rows.data_ptr() + 8, inv.data_ptr(), 2, 16, out.data_ptr(), None) == lsmgnn.E_INVAL
+    assert L.lsmgnn_expand(rows.data_ptr(), None, 2, 16, out.data_ptr(), None) == lsmgnn.E_INVAL
