@@ -57,7 +57,9 @@ struct orc_cache {
   uint64_t num_nodes, num_sets, victim_rows;
   uint32_t row_bytes, ways, lookahead, near_thr, policy, vmode, period;
   uint64_t t_upd;    /* gather index of the last update of the dynamic information */
-  int64_t *rl;       /* [num_sets][ways] next reuse iteration recorded at that update, or -1 */
+  uint32_t upd;      /* number of updates so far */
+  uint32_t *seen;    /* [num_nodes] the update at which `first` was last written */
+  int64_t *first;    /* [num_nodes] at that update, the node's first announced use in the window */
   uint64_t qcap, nslots; /* queue mode: rows per queue, queue slots */
   uint64_t *qcnt;        /* [nslots] entries in each queue */
   uint32_t *qbits;       /* [num_nodes] bit k: the node has an entry in slot k */
@@ -103,10 +105,6 @@ static int64_t *sorted_unique(const int64_t *ids, uint64_t n, uint64_t *m) {
   return u;
 }
 
-static int contains(const ann_list *l, int64_t x) {
-  return l->n && bsearch(&x, l->ids, l->n, sizeof(int64_t), cmp_i64) != NULL;
-}
-
 int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const uint32_t *static_score,
                uint64_t num_sets, uint32_t ways, uint64_t victim_rows, uint32_t lookahead,
                uint32_t near_threshold, uint32_t policy, uint32_t victim_mode, uint32_t refresh_period,
@@ -143,13 +141,15 @@ int orc_create(uint64_t num_nodes, uint32_t row_bytes, const void *store, const 
   c->rr = (uint32_t *)calloc(num_sets, sizeof(uint32_t));
   c->qcnt = (uint64_t *)calloc(c->nslots, sizeof(uint64_t));
   c->qbits = (uint32_t *)calloc(num_nodes, sizeof(uint32_t));
-  c->rl = (int64_t *)malloc(num_sets * ways * sizeof(int64_t));
-  if (!c->stat || !c->tag || !c->ins || !c->vtag || !c->where || !c->rr || !c->qcnt || !c->qbits || !c->rl) {
+  c->seen = (uint32_t *)calloc(num_nodes, sizeof(uint32_t));
+  c->first = (int64_t *)malloc(num_nodes * sizeof(int64_t));
+  if (!c->stat || !c->tag || !c->ins || !c->vtag || !c->where || !c->rr || !c->qcnt || !c->qbits || !c->seen ||
+      !c->first) {
     orc_destroy(c);
     return ORC_E_NOMEM;
   }
   memcpy(c->stat, static_score, num_nodes * sizeof(uint32_t));
-  for (uint64_t i = 0; i < num_sets * ways; ++i) { c->tag[i] = EMPTY; c->ins[i] = -1; c->rl[i] = -1; }
+  for (uint64_t i = 0; i < num_sets * ways; ++i) { c->tag[i] = EMPTY; c->ins[i] = -1; }
   for (uint64_t k = 0; k < victim_rows; ++k) c->vtag[k] = EMPTY;
   for (uint64_t v = 0; v < num_nodes; ++v) c->where[v] = -1;
   *out = c;
@@ -161,7 +161,7 @@ void orc_destroy(orc_cache *c) {
   for (uint64_t j = 0; j < c->n_ann; ++j) free(c->ann[j].ids);
   free(c->ann);
   free(c->stat); free(c->tag); free(c->ins); free(c->vtag); free(c->where); free(c->rr);
-  free(c->qcnt); free(c->qbits); free(c->rl);
+  free(c->qcnt); free(c->qbits); free(c->seen); free(c->first);
   free(c);
 }
 
@@ -192,26 +192,30 @@ int orc_advance(orc_cache *c, const int64_t *ids, uint64_t n) {
   return ORC_OK;
 }
 
-/* Distance from the current gather to the next announced use of node x
-   (1..L), or 0 when none of the next L minibatches names it (Sec. 4.2, the
-   next reuse iteration). */
-static uint64_t reuse_distance(const orc_cache *c, uint32_t x) {
-  for (uint64_t d = 1; d <= c->lookahead; ++d) {
-    uint64_t j = c->t + d;
-    if (j < c->n_ann && contains(&c->ann[j], (int64_t)x)) return d;
-  }
-  return 0;
-}
-
 /* The update of the dynamic information (Sec. 4.2), run before every U-th
-   gather: the next reuse iteration of every resident line from the announced
-   lists of the next L minibatches. */
+   gather: every resident line's next reuse iteration from the announced lists
+   of the next L minibatches.  Kept per node (the first of those lists that
+   names it, found by walking the lists in order), which is what each resident
+   line records: a line inserted later has no record (it counts as recently
+   inserted), so a per-node value frozen at the update is all a line reads. */
 static void update_reuse(orc_cache *c) {
   c->t_upd = c->t;
-  for (uint64_t i = 0; i < c->num_sets * c->ways; ++i) {
-    uint64_t d = c->tag[i] == EMPTY ? 0 : reuse_distance(c, c->tag[i]);
-    c->rl[i] = d ? (int64_t)(c->t + d) : -1;
-  }
+  ++c->upd;
+  for (uint64_t j = c->t + 1; j <= c->t + c->lookahead && j < c->n_ann; ++j)
+    for (uint64_t k = 0; k < c->ann[j].n; ++k) {
+      uint32_t x = (uint32_t)c->ann[j].ids[k];
+      if (c->seen[x] != c->upd) {
+        c->seen[x] = c->upd;
+        c->first[x] = (int64_t)j;
+      }
+    }
+}
+
+/* The next reuse iteration recorded for the line in way w of set s at the
+   last update, or -1 (none) */
+static int64_t recorded_reuse(const orc_cache *c, uint64_t i) {
+  uint32_t x = c->tag[i];
+  return (x != EMPTY && c->seen[x] == c->upd) ? c->first[x] : -1;
 }
 
 /* Dynamic information (Sec. 4.2): the class of the line in way w of set s while
@@ -222,9 +226,10 @@ static void update_reuse(orc_cache *c) {
 static int line_class(const orc_cache *c, uint64_t s, uint32_t w) {
   uint64_t i = s * c->ways + w;
   if (c->ins[i] >= (int64_t)c->t_upd) return CLS_R;
-  if (c->rl[i] < 0) return CLS_N;
-  if (c->rl[i] <= (int64_t)c->t) return CLS_R;
-  return (uint64_t)(c->rl[i] - (int64_t)c->t) <= c->near_thr ? CLS_C : CLS_F;
+  int64_t r = recorded_reuse(c, i);
+  if (r < 0) return CLS_N;
+  if (r <= (int64_t)c->t) return CLS_R;
+  return (uint64_t)(r - (int64_t)c->t) <= c->near_thr ? CLS_C : CLS_F;
 }
 
 /* The dynamic-only policy's view (Sec. 5): the distance to the line's recorded
@@ -232,8 +237,9 @@ static int line_class(const orc_cache *c, uint64_t s, uint32_t w) {
    or the line was inserted since the last update. */
 static uint64_t line_distance(const orc_cache *c, uint64_t s, uint32_t w) {
   uint64_t i = s * c->ways + w;
-  if (c->ins[i] >= (int64_t)c->t_upd || c->rl[i] <= (int64_t)c->t) return 0;
-  return (uint64_t)(c->rl[i] - (int64_t)c->t);
+  int64_t r = recorded_reuse(c, i);
+  if (c->ins[i] >= (int64_t)c->t_upd || r <= (int64_t)c->t) return 0;
+  return (uint64_t)(r - (int64_t)c->t);
 }
 
 /* Eviction priority, lowest level evicted first.  Hybrid order (Sec. 4.2):
@@ -351,7 +357,7 @@ int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t 
         ++st.evictions;
         if (c->vmode == ORC_VICTIM_QUEUES && c->qcap && (cls == CLS_F || cls == CLS_C)) {
           /* the queue of the line's next reuse iteration, unless it is full */
-          uint64_t slot = (uint64_t)c->rl[s * c->ways + pick] % c->nslots;
+          uint64_t slot = (uint64_t)recorded_reuse(c, s * c->ways + pick) % c->nslots;
           if (c->qcnt[slot] < c->qcap) {
             c->vtag[slot * c->qcap + c->qcnt[slot]] = z;
             ++c->qcnt[slot];
