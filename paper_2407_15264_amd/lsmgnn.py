@@ -175,6 +175,7 @@ class PinnedBuffer:
         _check(lib().lsmgnn_host_alloc(int(nbytes), ctypes.byref(p)), "lsmgnn_host_alloc")
         self.ptr = p.value
         self.nbytes = int(nbytes)
+        self._free = lib().lsmgnn_host_free  # kept: module globals may be gone when the finalizer runs
 
     def numpy(self, dtype=np.uint8, shape=None) -> np.ndarray:
         raw = (ctypes.c_uint8 * self.nbytes).from_address(self.ptr)
@@ -183,7 +184,7 @@ class PinnedBuffer:
 
     def close(self):
         if getattr(self, "ptr", None):
-            lib().lsmgnn_host_free(self.ptr)
+            self._free(self.ptr)
             self.ptr = None
 
     __del__ = close
@@ -273,12 +274,13 @@ class FeatureCache:
                      ctypes.c_void_p(stat.ctypes.data))
         h = ctypes.c_void_p()
         _check(lib().lsmgnn_cache_create(ctypes.byref(cfg), ctypes.byref(h)), "lsmgnn_cache_create")
+        self._destroy = lib().lsmgnn_cache_destroy  # kept: module globals may be gone when the finalizer runs
         self._h = h
         self._scratch = {}
 
     def close(self):
         if getattr(self, "_h", None):
-            lib().lsmgnn_cache_destroy(self._h)
+            self._destroy(self._h)
             self._h = None
 
     __del__ = close
