@@ -1194,44 +1194,6 @@ void launch_prefetch(const DevState &d, const Gate *gate, const uint8_t *staging
                      (uint32_t)(d.R / 16));
 }
 
-// Per-position output: row i of `out` <- row inv[i] of `rows` (the unique-row
-// output of a gather), for the n requests in their original order.  Item w =
-// (request i, 16-byte vector v); the inverse entry is a broadcast load.
-template <bool kPow2>
-__global__ __launch_bounds__(kBlock) void k_expand(const uint8_t *rows, const int64_t *inv, uint64_t n, uint64_t R,
-                                                   uint32_t nvec, uint32_t vshift, uint8_t *out) {
-  const uint64_t total = n * nvec;
-  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-  for (uint64_t w0 = (uint64_t)blockIdx.x * kBlock + threadIdx.x; w0 < total; w0 += stride * kUnroll) {
-    u32x4 v[kUnroll];
-    uint8_t *dp[kUnroll];
-#pragma unroll
-    for (int k = 0; k < kUnroll; ++k) {
-      const uint64_t w = w0 + k * stride;
-      dp[k] = nullptr;
-      if (w < total) {
-        const uint64_t i = kPow2 ? (w >> vshift) : (w / nvec);
-        const uint64_t byte = (w - i * nvec) * 16u;
-        v[k] = *reinterpret_cast<const u32x4 *>(rows + (uint64_t)inv[i] * R + byte);
-        dp[k] = out + i * R + byte;
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < kUnroll; ++k)
-      if (dp[k]) *reinterpret_cast<u32x4 *>(dp[k]) = v[k];
-  }
-}
-
-void launch_expand(const uint8_t *rows, const int64_t *inv, uint64_t n, uint64_t R, uint8_t *out, hipStream_t s) {
-  const uint32_t nvec = (uint32_t)(R / 16);
-  const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kUnroll, LSM_HBM_GRID);
-  if ((nvec & (nvec - 1)) == 0)
-    hipLaunchKernelGGL(k_expand<true>, dim3(g), dim3(kBlock), 0, s, rows, inv, n, R, nvec,
-                       (uint32_t)__builtin_ctz(nvec), out);
-  else
-    hipLaunchKernelGGL(k_expand<false>, dim3(g), dim3(kBlock), 0, s, rows, inv, n, R, nvec, 0u, out);
-}
-
 // ------------------------------------------------------------ calibration
 // Plain contiguous copy with the same 128-bit access pattern and unrolling as
 // the row copies; used to measure the host-link and HBM ceilings and to scale
@@ -1327,6 +1289,45 @@ void launch_announce(const int64_t *ids, uint64_t n, uint32_t bit, uint32_t *mas
                      const Scratch &sc, hipStream_t s) {
   const unsigned g = grid_for(n, kBlock, kMaxGrid);
   hipLaunchKernelGGL(k_announce, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, bit, mask, slot_ids, sc.gate);
+}
+
+// ------------------------------------------------------ request order
+// Per-position output: row i of `out` <- row inv[i] of `rows` (the unique-row
+// output of a gather), for the n requests in their original order.  Item w =
+// (request i, 16-byte vector v); the inverse entry is a broadcast load.
+template <bool kPow2>
+__global__ __launch_bounds__(kBlock) void k_expand(const uint8_t *rows, const int64_t *inv, uint64_t n, uint64_t R,
+                                                   uint32_t nvec, uint32_t vshift, uint8_t *out) {
+  const uint64_t total = n * nvec;
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  for (uint64_t w0 = (uint64_t)blockIdx.x * kBlock + threadIdx.x; w0 < total; w0 += stride * kUnroll) {
+    u32x4 v[kUnroll];
+    uint8_t *dp[kUnroll];
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      const uint64_t w = w0 + k * stride;
+      dp[k] = nullptr;
+      if (w < total) {
+        const uint64_t i = kPow2 ? (w >> vshift) : (w / nvec);
+        const uint64_t byte = (w - i * nvec) * 16u;
+        v[k] = *reinterpret_cast<const u32x4 *>(rows + (uint64_t)inv[i] * R + byte);
+        dp[k] = out + i * R + byte;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k)
+      if (dp[k]) *reinterpret_cast<u32x4 *>(dp[k]) = v[k];
+  }
+}
+
+void launch_expand(const uint8_t *rows, const int64_t *inv, uint64_t n, uint64_t R, uint8_t *out, hipStream_t s) {
+  const uint32_t nvec = (uint32_t)(R / 16);
+  const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kUnroll, LSM_HBM_GRID);
+  if ((nvec & (nvec - 1)) == 0)
+    hipLaunchKernelGGL(k_expand<true>, dim3(g), dim3(kBlock), 0, s, rows, inv, n, R, nvec,
+                       (uint32_t)__builtin_ctz(nvec), out);
+  else
+    hipLaunchKernelGGL(k_expand<false>, dim3(g), dim3(kBlock), 0, s, rows, inv, n, R, nvec, 0u, out);
 }
 
 }  // namespace lsm
