@@ -437,6 +437,10 @@ def main():
         "hit_rate": d["hits"] / max(d["unique"], 1),
         "victim_hit_rate": d["victim_hits"] / max(d["unique"], 1),
         "miss_rate": d["misses"] / max(d["unique"], 1),
+        # the same outcomes per raw request (a repeated ID counts each time)
+        "request_hit_rate": d["request_hits"] / max(d["requests"], 1),
+        "request_victim_hit_rate": d["request_victim_hits"] / max(d["requests"], 1),
+        "request_miss_rate": 1.0 - (d["request_hits"] + d["request_victim_hits"]) / max(d["requests"], 1),
         "unique_per_minibatch": d["unique"] / args.steps,
         "requests_per_minibatch": d["requests"] / args.steps,
         "roofline": roof,

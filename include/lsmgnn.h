@@ -144,6 +144,10 @@ typedef struct {
   uint64_t evictions;   /* = enqueued + dropped */
   uint64_t enqueued;    /* evicted lines written to the victim ring */
   uint64_t dropped;     /* evicted lines discarded */
+  /* the outcomes counted per raw request (a repeated ID counts each time):
+     request misses = requests - request_hits - request_victim_hits */
+  uint64_t request_hits;
+  uint64_t request_victim_hits;
 } lsmgnn_counts;
 
 /* Accumulated device time of the data movement (filled only while profiling

@@ -279,6 +279,11 @@ int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t 
   uint64_t U = 0;
   int64_t *uniq = sorted_unique(ids, n, &U);
   if (!uniq) return ORC_E_NOMEM;
+  uint8_t *oc = (uint8_t *)malloc(U ? U : 1); /* each unique ID's outcome */
+  if (!oc) {
+    free(uniq);
+    return ORC_E_NOMEM;
+  }
   if (c->t % c->period == 0) update_reuse(c);
   orc_counts st;
   memset(&st, 0, sizeof st);
@@ -296,20 +301,20 @@ int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t 
       if (tag[w] == x) hit = 1;
     if (hit) {
       ++st.hits;
-      if (outcome) outcome[u] = ORC_HIT;
+      oc[u] = ORC_HIT;
     } else {
       /* the victim buffer is probed for the line before storage (Sec. 4.3);
          in queue mode only the current iteration's queue holds rows */
       if (c->vmode == ORC_VICTIM_QUEUES && c->qcap && ((c->qbits[x] >> (c->t % c->nslots)) & 1u)) {
         ++st.victim_hits;
-        if (outcome) outcome[u] = ORC_VICTIM_HIT;
+        oc[u] = ORC_VICTIM_HIT;
       } else if (c->vmode == ORC_VICTIM_FIFO && c->victim_rows && c->where[x] >= 0) {
         ++st.victim_hits;
         ring_put(c, (uint64_t)c->where[x], EMPTY);
-        if (outcome) outcome[u] = ORC_VICTIM_HIT;
+        oc[u] = ORC_VICTIM_HIT;
       } else {
         ++st.misses;
-        if (outcome) outcome[u] = ORC_MISS;
+        oc[u] = ORC_MISS;
       }
       /* choose the way: an empty way first; in a full set the policy's
          victim (Sec. 4.2 for the hybrid; Sec. 5 for the others) */
@@ -384,11 +389,15 @@ int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t 
   }
 
   if (uniq_out) memcpy(uniq_out, uniq, U * sizeof(int64_t));
-  if (inv)
-    for (uint64_t i = 0; i < n; ++i) {
-      int64_t *p = (int64_t *)bsearch(&ids[i], uniq, U, sizeof(int64_t), cmp_i64);
-      inv[i] = p - uniq;
-    }
+  if (outcome) memcpy(outcome, oc, U);
+  /* each request takes its unique ID's outcome */
+  for (uint64_t i = 0; i < n; ++i) {
+    int64_t *p = (int64_t *)bsearch(&ids[i], uniq, U, sizeof(int64_t), cmp_i64);
+    if (inv) inv[i] = p - uniq;
+    if (oc[p - uniq] == ORC_HIT) ++st.request_hits;
+    if (oc[p - uniq] == ORC_VICTIM_HIT) ++st.request_victim_hits;
+  }
+  free(oc);
   free(uniq);
   if (n_unique) *n_unique = U;
 
@@ -417,6 +426,8 @@ int orc_gather(orc_cache *c, const int64_t *ids, uint64_t n, void *out, int64_t 
   c->total.evictions += st.evictions;
   c->total.enqueued += st.enqueued;
   c->total.dropped += st.dropped;
+  c->total.request_hits += st.request_hits;
+  c->total.request_victim_hits += st.request_victim_hits;
   ++c->t;
   return ORC_OK;
 }

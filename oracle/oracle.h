@@ -49,6 +49,8 @@ typedef struct orc_cache orc_cache;
 
 typedef struct {
   uint64_t batch, requests, unique, hits, victim_hits, misses, evictions, enqueued, dropped;
+  /* the same outcomes counted per raw request (a repeated ID counts each time) */
+  uint64_t request_hits, request_victim_hits;
 } orc_counts;
 
 /* set index of node x in a cache of num_sets sets */

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(HERE, "liboracle.so")
 HIT, VICTIM_HIT, MISS = 0, 1, 2
 STATUS = {0: "OK", 1: "E_INVAL", 2: "E_RANGE", 3: "E_WINDOW", 4: "E_NOMEM"}
 STAT_FIELDS = ("batch", "requests", "unique", "hits", "victim_hits", "misses",
-               "evictions", "enqueued", "dropped")
+               "evictions", "enqueued", "dropped", "request_hits", "request_victim_hits")
 
 
 class OracleError(RuntimeError):

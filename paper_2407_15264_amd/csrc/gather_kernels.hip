@@ -127,6 +127,8 @@ __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host,
     c.n_hbm = sums[kStHbm];
     c.n_host = sums[kStHost];
     c.n_enq_copy = sums[kStEnqCopy];
+    c.req_hits = sums[kStReqHits];
+    c.req_victim_hits = sums[kStReqVictimHits];
     // queue mode: candidates that found their queue full were dropped
     c.enqueued -= c.q_overflow;
     c.dropped += c.q_overflow;
@@ -919,6 +921,7 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
       from_hbm = !from_host;
       fd = sc.fill_dst[u];
       refill = fd != 0;
+      sc.oc[u] = oc;
       if (outcome) outcome[u] = oc;
     }
     const uint32_t ih = block_append(from_host, &sc.gate->n_host);
@@ -941,6 +944,29 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
   block_count(c_miss, sc.stat_part, kStMisses);
   block_count(c_hbm, sc.stat_part, kStHbm);
   block_count(c_host, sc.stat_part, kStHost);
+}
+
+// Outcomes per raw request: each request takes its unique ID's outcome (the
+// compaction recorded every requested node's unique index).
+__global__ __launch_bounds__(kBlock) void k_request_counts(const DevState d, Scratch sc, const int64_t *ids,
+                                                           uint32_t n, const Counters *cn) {
+  if (cn->err) return;
+  uint32_t c_hit = 0, c_vhit = 0;
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
+    const uint8_t o = sc.oc[d.uidx[ids[i]]];
+    c_hit += o == 0;   // LSMGNN_HIT
+    c_vhit += o == 1;  // LSMGNN_VICTIM_HIT
+  }
+  block_count(c_hit, sc.stat_part, kStReqHits);
+  block_count(c_vhit, sc.stat_part, kStReqVictimHits);
+}
+
+void launch_request_counts(const DevState &d, const int64_t *ids, uint64_t n, Scratch &sc, Counters *cn,
+                           StatGrids &grids, hipStream_t s) {
+  const unsigned g = grid_for(n, kBlock, kMaxGrid);
+  hipLaunchKernelGGL(k_request_counts, dim3(g), dim3(kBlock), 0, s, d, sc, ids, (uint32_t)n, cn);
+  grids.g[kStReqHits] = g;
+  grids.g[kStReqVictimHits] = g;
 }
 
 // Ring bookkeeping for this batch's enqueues; lists the row copies of the

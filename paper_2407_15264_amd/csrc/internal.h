@@ -57,6 +57,7 @@ enum StatSlot : int {
   kStHits, kStFills, kStEvictions, kStEnqueued, kStDropped, kStFinal,  // set walk
   kStVictimHits, kStMisses, kStHbm, kStHost,                           // resolve
   kStEnqCopy,                                                          // enqueue finalize
+  kStReqHits, kStReqVictimHits,                                        // per-request outcomes
   kNumStat
 };
 constexpr unsigned kMaxGrid = 8192;  // grid cap of every grid-stride kernel
@@ -74,6 +75,7 @@ struct Counters {
   uint32_t hits, fills, evictions, enqueued, dropped, victim_hits, misses;
   uint32_t n_hbm, n_host, n_enq_copy, n_fill;  // rows per data kernel
   uint32_t enq_total;
+  uint32_t req_hits, req_victim_hits;  // outcomes counted per raw request
   // victim queues (queue mode): enqueue candidates that found their queue
   // full, and per queue slot the entries before this gather and those it placed
   uint32_t q_overflow;
@@ -132,6 +134,7 @@ struct Scratch {
   uint32_t *seg_st;     // static score of seg_x[.]
   uint8_t *kind;
   uint8_t *flags;
+  uint8_t *oc;          // outcome of u (LSMGNN_HIT / _VICTIM_HIT / _MISS)
   uint8_t *dead;        // enqueue entry whose line was victim-hit in the same batch
   uint32_t *slot;       // cache slot (set*8+way) hit or filled by u
   uint32_t *evicted;    // node evicted by u's fill, or kEmpty
@@ -208,6 +211,9 @@ void launch_set_walk(const DevState &d, uint64_t n, uint32_t t, Scratch &sc, Cou
 // U > 1, before every U-th gather's set walk: record every resident line's next reuse iteration
 void launch_refresh(const DevState &d, uint32_t t, const Counters *cn, hipStream_t s);
 // t: the gather's index (queue mode serves queue t from prefetch buffer t & 1)
+// per-request outcome counts (each request takes its unique ID's outcome)
+void launch_request_counts(const DevState &d, const int64_t *ids, uint64_t n, Scratch &sc, Counters *cn,
+                           StatGrids &grids, hipStream_t s);
 void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, uint8_t *outcome, Counters *cn,
                          StatGrids &grids, hipStream_t s);
 // Queue mode: copy the queue of gather t+1 (slot `slot`) into prefetch buffer

@@ -266,6 +266,8 @@ void harvest_stats(lsmgnn_cache *c, Flight &f) {
   st.evictions = h.evictions;
   st.enqueued = h.enqueued;
   st.dropped = h.dropped;
+  st.request_hits = h.req_hits;
+  st.request_victim_hits = h.req_victim_hits;
   c->last = st;
   c->total.batch = f.t + 1;
   c->total.requests += st.requests;
@@ -276,6 +278,8 @@ void harvest_stats(lsmgnn_cache *c, Flight &f) {
   c->total.evictions += st.evictions;
   c->total.enqueued += st.enqueued;
   c->total.dropped += st.dropped;
+  c->total.request_hits += st.request_hits;
+  c->total.request_victim_hits += st.request_victim_hits;
   c->tail += h.enq_total;
   f.enq_total = h.enq_total;
   f.tail_end = c->tail;
@@ -474,6 +478,7 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
     lsm::launch_group_by_set(d, ids, n, inverse, f.sc, c->cn, c->meta);
     lsm::launch_set_walk(d, n, (uint32_t)t, f.sc, c->cn, grids, c->meta);
     lsm::launch_ring_resolve(d, n, t, f.sc, outcome, c->cn, grids, c->meta);
+    lsm::launch_request_counts(d, ids, n, f.sc, c->cn, grids, c->meta);
   }
   (void)hipEventRecord(f.meta_done, c->meta);
   lsm::QueueFinish qf;
@@ -718,6 +723,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
             dev_alloc(c, &sc.arrival, B) && dev_alloc(c, &sc.touched, B) && dev_alloc(c, &sc.seg_off, B) &&
             dev_alloc(c, &sc.seg, B) && dev_alloc(c, &sc.seg_u, B) && dev_alloc(c, &sc.seg_x, B) &&
             dev_alloc(c, &sc.seg_st, B) && dev_alloc(c, &sc.kind, B) && dev_alloc(c, &sc.flags, B) &&
+            dev_alloc(c, &sc.oc, B) &&
             dev_alloc(c, &sc.dead, B) && dev_alloc(c, &sc.evicted, B) && dev_alloc(c, &sc.enq_before, B) &&
             dev_alloc(c, &sc.scan_part, B / lsm::kScanChunk + 2) && dev_alloc(c, &sc.this_q, B) &&
             dev_alloc(c, &sc.this_enq, B) && dev_alloc(c, &sc.slot, B) && dev_alloc(c, &sc.fill_dst, B) &&

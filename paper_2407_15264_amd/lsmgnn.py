@@ -18,7 +18,8 @@ STATUS_NAMES = {0: "OK", 1: "E_INVAL", 2: "E_RANGE", 3: "E_WINDOW", 4: "E_NOMEM"
 HIT, VICTIM_HIT, MISS = 0, 1, 2
 EMPTY = 0xFFFFFFFF
 COUNT_FIELDS = ("batch", "requests", "unique", "hits", "victim_hits", "misses", "evictions", "enqueued",
-                "dropped")
+                "dropped", "request_hits",
+                "request_victim_hits")
 
 
 class LsmgnnError(RuntimeError):

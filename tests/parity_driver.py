@@ -18,7 +18,8 @@ from oracle.oracle import Oracle
 from paper_2407_15264_amd import lsmgnn
 from paper_2407_15264_amd import workload as W
 
-COUNT_KEYS = ("batch", "requests", "unique", "hits", "victim_hits", "misses", "evictions", "enqueued", "dropped")
+COUNT_KEYS = ("batch", "requests", "unique", "hits", "victim_hits", "misses", "evictions", "enqueued", "dropped",
+              "request_hits", "request_victim_hits")
 
 
 def log(msg):

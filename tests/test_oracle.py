@@ -133,6 +133,9 @@ def _check_invariants(o, ids, r, store=None):
     assert st["evictions"] == st["enqueued"] + st["dropped"]
     assert np.count_nonzero(r["outcome"] == HIT) == st["hits"]
     assert np.count_nonzero(r["outcome"] == VICTIM_HIT) == st["victim_hits"]
+    per_request = r["outcome"][inv.reshape(-1)]  # each request takes its unique ID's outcome
+    assert st["request_hits"] == np.count_nonzero(per_request == HIT)
+    assert st["request_victim_hits"] == np.count_nonzero(per_request == VICTIM_HIT)
     s = o.export_state()
     tags = s["tags"]
     live = tags[tags != EMPTY]
@@ -598,3 +601,14 @@ def test_update_period_random_small_against_naive_model(seed, policy, mode):
     else:
         announce = batches
     _compare(n, S, ways, V, L, T, stat, batches, announce, policy, mode, U)
+
+
+def test_request_counts_repeat_with_the_request():
+    # a node requested k times counts k times per request and once per unique ID
+    o = Oracle(10, 16, np.ones(10, np.uint32), 1, 0, 0)
+    o.gather(np.array([3, 4]))
+    r = o.gather(np.array([3, 3, 3, 4, 5, 5]))
+    st = r["stats"]
+    assert (st["hits"], st["misses"]) == (2, 1)
+    assert (st["request_hits"], st["request_victim_hits"]) == (4, 0)
+    assert st["requests"] - st["request_hits"] - st["request_victim_hits"] == 2
