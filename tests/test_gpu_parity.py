@@ -238,6 +238,11 @@ def test_bad_configs_rejected():
     with pytest.raises(lsmgnn.LsmgnnError) as e:
         lsmgnn.FeatureCache(**dict(base, host_store=pageable.ctypes.data))
     assert e.value.status == "E_INVAL"
+    # cache rows beyond the device memory: 2^31 lines of 4 KiB (8 TiB)
+    big = Store.random_bytes(16, 4096, 0)
+    with pytest.raises(lsmgnn.LsmgnnError) as e:
+        lsmgnn.FeatureCache(**dict(base, host_store=big.buf, row_bytes=4096, num_sets=1 << 28))
+    assert e.value.status == "E_NOMEM"
 
 
 def test_deterministic_state():
