@@ -1134,10 +1134,12 @@ __global__ __launch_bounds__(kBlock) void k_host_fetch(const DevState d, Scratch
 
 // Grid caps.  Every outstanding host-link read queues in front of the memory
 // requests of the kernels that run beside it (the next gather's metadata, the
-// hit copy, the fills), so the host fetch keeps only a few hundred KB in
-// flight: enough to cover the link's latency, not more.
+// hit copy, the fills, the ring write), so the host fetch keeps only about
+// 640 KB in flight (40 blocks x 256 lanes x 4 x 16 B): enough to cover the
+// link's latency, not more.  A sweep of block counts and unroll depths on
+// the full pipeline chose it.
 #ifndef LSM_HOST_GRID
-#define LSM_HOST_GRID 32
+#define LSM_HOST_GRID 40
 #endif
 #ifndef LSM_HBM_GRID
 #define LSM_HBM_GRID 4096  // the HBM-side copies: a grid sweep beside the host fetch chose it
