@@ -260,7 +260,13 @@ def main():
         else:  # beyond the pinned-memory budget: ordinary memory, rows copied by the library's host threads
             p["store_np"] = np.empty((p["num_nodes"], p["R"]), np.uint8)
             p["store"] = p["store_np"]
-        W.fill_features(p["store_np"].ctypes.data, p["dim"], p["elt"], 0, p["num_nodes"], p["seed"])
+        # in slices of about 8 GiB, with a progress line for each of a large store
+        step = max(1, (8 << 30) // p["R"])
+        for v0 in range(0, p["num_nodes"], step):
+            v1 = min(p["num_nodes"], v0 + step)
+            W.fill_features(p["store_np"][v0:].ctypes.data, p["dim"], p["elt"], v0, v1, p["seed"])
+            if p["num_nodes"] > step:
+                log(f"[bench]   {p['label']}: store rows {v1} of {p['num_nodes']} filled")
     log(f"[bench] stores filled: {sum(p['num_nodes'] * p['R'] for p in parts) / 2**30:.2f} GiB "
         f"({'pinned' if all(pinned) else 'pinned per part: ' + str(pinned)})")
 

@@ -1137,7 +1137,8 @@ __global__ __launch_bounds__(kBlock) void k_host_fetch(const DevState d, Scratch
 // hit copy, the fills, the ring write), so the host fetch keeps only about
 // 640 KB in flight (40 blocks x 256 lanes x 4 x 16 B): enough to cover the
 // link's latency, not more.  A sweep of block counts and unroll depths on
-// the full pipeline chose it.
+// the full pipeline chose it.  The runtime may ask for fewer blocks
+// (DevState::host_grid) when more traffic shares the host or the link.
 #ifndef LSM_HOST_GRID
 #define LSM_HOST_GRID 40
 #endif
@@ -1163,7 +1164,7 @@ void launch_copy(CopyMode mode, const DevState &d, uint64_t n, const Scratch &sc
   const bool pow2 = (nvec & (nvec - 1)) == 0;
   const uint32_t vshift = pow2 ? (uint32_t)__builtin_ctz(nvec) : 0u;
   if (mode == CopyMode::kHostToOut) {
-    const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kUnroll, LSM_HOST_GRID);
+    const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kUnroll, d.host_grid ? d.host_grid : LSM_HOST_GRID);
     if (pow2)
       hipLaunchKernelGGL((k_host_fetch<true>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift);
     else

@@ -181,6 +181,7 @@ struct DevState {
   uint64_t C;            // queue mode: rows per queue, V / (L + 1)
   uint32_t *qcount;      // queue mode: [L + 1] entries in each queue slot
   uint32_t U;            // update period of the dynamic information (1: exact at every gather)
+  uint32_t host_grid;    // blocks of the host fetch (0: the default), chosen per gather by the runtime
   uint32_t *lreuse;      // U > 1: [S*8] 1 + next reuse iteration recorded at the last update, or 0
   // queue mode: the two prefetch buffers (C rows each, by gather parity) are
   // rows S*8 .. S*8 + 2C of `rows`, after the cache lines

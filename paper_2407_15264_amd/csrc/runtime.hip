@@ -148,6 +148,12 @@ bool acquire_streams(int dev, StreamSet &out) {
   return true;
 }
 
+// Caches sharing the device's streams.
+int caches_on_device(int dev) {
+  std::lock_guard<std::mutex> lock(g_streams_mu);
+  return g_streams[dev].refs;
+}
+
 void release_streams(int dev) {
   std::lock_guard<std::mutex> lock(g_streams_mu);
   StreamSet &ss = g_streams[dev];
@@ -447,6 +453,12 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   issue_dma(c, f);         // gather t-2's ring write (normally queued by gather t-1's call)
   const bool prof = c->prof != 0;
   const bool queues = d.qmode && d.V && d.L > 0;  // per-iteration victim queues with prefetch
+  // The host fetch's grid: 40 blocks when this cache has the link and the
+  // host's memory to itself; 32 when host threads also copy rows (a pageable
+  // store) or other caches' host fetches, ring writes and copies share the
+  // device (measured: one pinned cache gains 8-11 % from 40, several caches
+  // or a pageable store lose 2-5 %).
+  d.host_grid = (c->pageable || caches_on_device(c->device) > 1) ? 32u : 0u;
   auto rec = [&](int e, hipStream_t st) {
     if (prof) (void)hipEventRecord(ps.e[e], st);
   };
