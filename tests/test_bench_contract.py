@@ -1,0 +1,31 @@
+"""bench.py's command-line contract on the CPU (no GPU): one GPU only, with a
+message for more; the workload names and options it accepts."""
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _bench(*args):
+    return subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args], capture_output=True, text=True,
+                          timeout=120, cwd=ROOT)
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    r = _bench("--gpus", "2", "--steps", "5", "--warmup", "1")
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_options_and_workload_names():
+    r = _bench("--help")
+    assert r.returncode == 0
+    for opt in ("--gpus", "--steps", "--warmup", "--workload", "--policy", "--victim-mode", "--refresh-period",
+                "--static", "--train-us", "--sync", "--no-cpu-baseline"):
+        assert opt in r.stdout, opt
+    from paper_2407_15264_amd import workload as W
+    for name in W.WORKLOADS:
+        assert name in r.stdout, name
+    bad = _bench("--workload", "no-such-workload")
+    assert bad.returncode != 0
