@@ -16,7 +16,9 @@
  *     (Sec. 4.3.1, 4.3.2).
  * Storage (SSDs in the paper) is a host-resident, pinned backing feature table.
  *
- * Semantics, fixed where the paper is silent:
+ * Semantics, fixed where the paper is silent (for the default configuration;
+ * lsmgnn_config.policy, .victim_mode and .refresh_period select the
+ * alternatives the paper's evaluation compares, documented with them below):
  *   - a gather deduplicates its IDs and serves them in ascending ID order; the
  *     output holds one row per unique ID, ascending, plus an inverse index;
  *   - set(x) = ((hi32(splitmix64(x)) * num_sets) >> 32), where splitmix64(x) is
