@@ -19,7 +19,10 @@ type.
 
 Prints one JSON line.  `value` is gathered feature bytes (unique rows x row
 bytes) per second over the timed steps; `roofline` rates the dominant data
-kernel against its bound, timed with HIP events on the gather's stream.
+kernel against its bound, timed with HIP events on the gather's stream.  The
+timed steps run twice over the same minibatches, each time from fresh caches:
+first without the library's timing events (`value`), then with them (the
+per-kernel figures, and `profiled_pass`).
 """
 import argparse
 import hashlib
@@ -298,21 +301,29 @@ def main():
     for p in parts:
         p.pop("graph", None)
     for p in parts:
-        sh = p["shape"]
         p["dev_batches"] = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in p["batches"]]
         mb = max(1, max(b.size for b in p["batches"]))
-        p["cache"] = lsmgnn.FeatureCache(p["num_nodes"], p["R"], p["store"], p["static"], sh.num_sets,
-                                         0 if args.no_ring else sh.victim_rows, sh.lookahead, mb,
-                                         near_threshold=sh.near_threshold, pageable=not p["pinned"],
-                                         host_threads=args.host_threads, policy=args.policy,
-                                         victim_mode=args.victim_mode, refresh_period=args.refresh_period)
         # three output sets rotate: at most two gathers are in flight
         p["bufs"] = [(torch.empty(mb * p["R"], dtype=torch.uint8, device=dev),
                       torch.empty(mb, dtype=torch.int64, device=dev),
                       torch.empty(mb, dtype=torch.int64, device=dev)) for _ in range(3)]
-        for j in range(L + 1):
-            p["cache"].advance(p["dev_batches"][j])
-        p["tickets"] = {}
+
+    def fresh_caches():
+        """A new cache per part (the previous one closed first), its window
+        holding the first L+1 minibatches."""
+        for p in parts:
+            if "cache" in p:
+                p["cache"].close()
+            sh = p["shape"]
+            mb = p["bufs"][0][1].numel()
+            p["cache"] = lsmgnn.FeatureCache(p["num_nodes"], p["R"], p["store"], p["static"], sh.num_sets,
+                                             0 if args.no_ring else sh.victim_rows, sh.lookahead, mb,
+                                             near_threshold=sh.near_threshold, pageable=not p["pinned"],
+                                             host_threads=args.host_threads, policy=args.policy,
+                                             victim_mode=args.victim_mode, refresh_period=args.refresh_period)
+            for j in range(L + 1):
+                p["cache"].advance(p["dev_batches"][j])
+            p["tickets"] = {}
 
     sleep_cycles = 0
     if args.train_us > 0:
@@ -352,26 +363,41 @@ def main():
             for b in list(p["tickets"]):
                 p["cache"].wait(p["tickets"].pop(b))
 
-    for b in range(args.warmup):
-        step(b)
-    drain()
-    tot0 = [p["cache"].stats()[1] for p in parts]
-    for p in parts:
-        p["cache"].set_profiling(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    nbytes = 0
-    for b in range(args.warmup, args.warmup + args.steps):
-        nbytes += step(b)
-    drain()
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t0
-    profs = [p["cache"].profile() for p in parts]
-    for p in parts:
-        p["cache"].set_profiling(False)
-    tot1 = [p["cache"].stats()[1] for p in parts]
+    def run_pass(profiled):
+        """Fresh caches, W warmup minibatches, then K timed ones; with
+        `profiled` the library records HIP events around every row copy."""
+        fresh_caches()
+        for b in range(args.warmup):
+            step(b)
+        drain()
+        tot0 = [p["cache"].stats()[1] for p in parts]
+        for p in parts:
+            p["cache"].set_profiling(profiled)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        nbytes = 0
+        for b in range(args.warmup, args.warmup + args.steps):
+            nbytes += step(b)
+        drain()
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        profs = [p["cache"].profile() for p in parts] if profiled else None
+        for p in parts:
+            p["cache"].set_profiling(False)
+        tot1 = [p["cache"].stats()[1] for p in parts]
+        d = {k: sum(t1[k] - t0_[k] for t0_, t1 in zip(tot0, tot1)) for k in tot1[0]}
+        return dt, nbytes, d, profs
+
+    # The headline pass runs as a user would, without the library's timing
+    # events (each is a marker on a stream of the pipeline and costs a few
+    # percent).  A second pass over the same minibatches, from fresh caches,
+    # records the events for the per-kernel figures.
+    dt, nbytes, d, _ = run_pass(False)
+    log(f"[bench] timed pass: {args.steps} minibatches in {1e3 * dt:.1f} ms")
+    dt_p, nbytes_p, d_p, profs = run_pass(True)
+    log(f"[bench] profiled pass: {1e3 * dt_p:.1f} ms")
+    assert nbytes_p == nbytes and d_p == d, "the two passes over one stream must do identical work"
     alone = hit_path_alone(parts, args.warmup + args.steps - 1)
-    d = {k: sum(t1[k] - t0_[k] for t0_, t1 in zip(tot0, tot1)) for k in tot1[0]}
     gbps = nbytes / dt / 1e9
     rows = d["unique"]
 
@@ -455,6 +481,10 @@ def main():
                     for k, v in kern.items()},
         "gather_ms_events": sum(pr["gather_ms"] for pr in profs) / max(sum(pr["gathers"] for pr in profs), 1),
         "ceilings": ceil,
+        "profiled_pass": {"value": nbytes_p / dt_p / 1e9, "ms_per_step": 1e3 * dt_p / args.steps,
+                          "how": "the same minibatches from fresh caches with the library's HIP timing "
+                                 "events on; `kernels` and the rooflines come from this pass, `value` "
+                                 "from the pass without them"},
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(parts, args.cpu_budget, args.policy, 0 if args.no_ring else None,
