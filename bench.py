@@ -69,9 +69,58 @@ def recorded_traffic(workload, kernel):
             "source": os.path.relpath(path, ROOT)}
 
 
-def measure_ceilings(torch, lsmgnn, store_ptr, nbytes):
+def duplex_probe(nbytes=1 << 30):
+    """Both link directions at once, as in the pipeline (which sends about half
+    as many bytes out as it reads in): the runtime's copies, nbytes host to
+    device on one stream and nbytes/2 device to host on another, from and to
+    pinned memory.  Runs in a process of its own: the two extra streams would
+    otherwise take hardware queues that the library's streams need."""
+    import torch
+    dev = torch.device("cuda", 0)
+    half = nbytes // 32 * 16
+    h_in = torch.ones(nbytes, dtype=torch.uint8).pin_memory()
+    h_out = torch.empty(half, dtype=torch.uint8).pin_memory()
+    d_in = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    d_out = torch.zeros(half, dtype=torch.uint8, device=dev)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    best = None
+    for _ in range(5):
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        with torch.cuda.stream(sa):
+            ev[0].record()
+            d_in.copy_(h_in, non_blocking=True)
+            ev[1].record()
+        with torch.cuda.stream(sb):
+            ev[2].record()
+            h_out.copy_(d_out, non_blocking=True)
+            ev[3].record()
+        torch.cuda.synchronize()
+        ta, tb = ev[0].elapsed_time(ev[1]) / 1e3, ev[2].elapsed_time(ev[3]) / 1e3
+        span = max(ev[0].elapsed_time(ev[1]), ev[0].elapsed_time(ev[3])) / 1e3
+        r = {"h2d_GBps": nbytes / ta / 1e9, "d2h_GBps": half / tb / 1e9,
+             "total_GBps": (nbytes + half) / span / 1e9, "bytes_in": nbytes, "bytes_out": half,
+             "how": "runtime copies from and to pinned memory on two streams, started together"}
+        if best is None or r["total_GBps"] > best["total_GBps"]:
+            best = r
+    print(json.dumps(best), flush=True)
+
+
+def duplex_ceiling():
+    """duplex_probe() in a child process; None if it fails."""
+    import subprocess
+    try:
+        out = subprocess.run([sys.executable, os.path.abspath(__file__), "--duplex-probe"], capture_output=True,
+                             text=True, timeout=300)
+        return json.loads(out.stdout.strip().splitlines()[-1]) if out.returncode == 0 else None
+    except (subprocess.SubprocessError, ValueError, IndexError, OSError):
+        return None
+
+
+def measure_ceilings(torch, lsmgnn, store_ptr, nbytes, duplex):
     """Host-link and HBM ceilings in this run: pinned H2D DMA, zero-copy reads
-    and writes by the 128-bit copy kernel, and a device-to-device copy."""
+    and writes by the 128-bit copy kernel, a device-to-device copy; `duplex`
+    is duplex_probe()'s result, measured in a child process beforehand."""
     dev = torch.device("cuda", 0)
     nbytes = min(nbytes, 1 << 30) // 16 * 16
     d0 = torch.empty(nbytes, dtype=torch.uint8, device=dev)
@@ -95,6 +144,8 @@ def measure_ceilings(torch, lsmgnn, store_ptr, nbytes):
     res["zero_copy_write_GBps"] = nbytes / best(
         lambda: lsmgnn.copy_bytes(pinned.data_ptr(), d0.data_ptr(), nbytes)) / 1e9
     res["hbm_copy_GBps"] = 2 * nbytes / best(lambda: lsmgnn.copy_bytes(d1.data_ptr(), d0.data_ptr(), nbytes)) / 1e9
+
+    res["duplex"] = duplex
     res["bytes"] = nbytes
     del d0, d1, pinned
     return res
@@ -224,11 +275,23 @@ def main():
                     help="static score: the in-degree, or the reverse PageRank computed on the GPU")
     ap.add_argument("--sync", action="store_true",
                     help="blocking lsmgnn_gather per minibatch instead of the pipelined lsmgnn_gather_async")
+    ap.add_argument("--duplex-probe", action="store_true", help=argparse.SUPPRESS)
+    ap.add_argument("--no-duplex-probe", action="store_true",
+                    help="skip the link probe with both directions at once (a child process)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU: the library has no multi-GPU path (asked for --gpus "
               f"{args.gpus}). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+    if args.duplex_probe:
+        duplex_probe()
+        return
+    # The child process starts before this one touches the GPU.  Not under a
+    # profiler: its preloaded library would trace the child too, into the same
+    # output files.
+    profiled_run = any(k.startswith("ROCPROF") for k in os.environ)
+    duplex = None if args.no_duplex_probe or profiled_run else duplex_ceiling()
+    log(f"[bench] duplex link probe: {duplex}")
 
     import numpy as np
     import torch
@@ -280,8 +343,8 @@ def main():
     else:
         cbytes = 1 << 30
         cbuf = lsmgnn.PinnedBuffer(cbytes)
-    ceil = measure_ceilings(torch, lsmgnn, cbuf.ptr, cbytes)
-    log(f"[bench] ceilings: {json.dumps({k: round(v, 1) for k, v in ceil.items()})}")
+    ceil = measure_ceilings(torch, lsmgnn, cbuf.ptr, cbytes, duplex)
+    log(f"[bench] ceilings: {json.dumps({k: round(v, 1) if isinstance(v, float) else v for k, v in ceil.items()})}")
 
     dev = torch.device("cuda", 0)
     static_info = {"kind": "in-degree"}
@@ -437,6 +500,15 @@ def main():
                 "peak_source": "measured in this run (best of pinned DMA and zero-copy kernel)",
                 "frac_of_published_pcie5_x16": kd["GBps"] / PCIE5_X16_PEAK_GBPS}
     roof.update(kernel=dom, avg_launch_us=kd["avg_us"], bytes_per_launch=kd["bytes_per_launch"])
+    if kd["bound"] == "host_link":
+        # both link directions over the headline pass: rows in (host fetch,
+        # prefetch) and rows out (ring writes), against the duplex ceiling
+        b_in = sum((pr["host_fetch_rows"] + pr["prefetch_rows"]) * p["R"] for pr, p in zip(profs, parts))
+        b_out = sum(pr["enqueue_rows"] * p["R"] for pr, p in zip(profs, parts))
+        roof["link_both_directions"] = {
+            "in_GBps": b_in / dt / 1e9, "out_GBps": b_out / dt / 1e9, "total_GBps": (b_in + b_out) / dt / 1e9,
+            "frac_of_duplex_total": None if ceil["duplex"] is None else
+            (b_in + b_out) / dt / 1e9 / ceil["duplex"]["total_GBps"]}
     tr = recorded_traffic(cfg.name, dom)
     if tr is not None:
         # algorithmic bytes of the launch on both sides of the copy (read + write)
