@@ -96,6 +96,7 @@ struct Flight {
   bool stats_pending = false;  // counters not yet added to the totals
   bool dma_pending = false;    // staged rows not yet queued for the ring
   bool dma_used = false;       // dma_done has been recorded at least once
+  uint64_t dma_seq = 0, fill_seq = 0;  // positions of the ring write and the fill among the cache's dma submissions
   uint64_t t = 0, requests = 0;
   uint64_t enq_total = 0, tail_end = 0;  // enqueues of the gather, ring tail after it
   uint32_t q_before[lsm::kMaxQueues] = {}, q_placed[lsm::kMaxQueues] = {};  // queue mode, per slot
@@ -190,6 +191,11 @@ struct lsmgnn_cache {
   hipEvent_t ev_in = nullptr, ev_dedup = nullptr, ev_adv = nullptr;
   hipEvent_t ev_q = nullptr;  // queue mode: the queue writes queued so far have landed
   uint64_t t = 0;  // gathers issued
+  // Submissions of this cache to the in-order dma stream are numbered; the
+  // meta stream has waited for one recorded right after submission
+  // meta_dma_seen, so everything the cache submitted there up to it is done.
+  // A later wait on anything at or below it would only add a queue packet.
+  uint64_t dma_subs = 0, meta_dma_seen = 0;
   uint64_t n_adv = 0, tail = 0;
   lsmgnn_counts last{}, total{};
   bool broken = false;
@@ -310,6 +316,15 @@ void harvest_stats(lsmgnn_cache *c, Flight &f) {
   f.stats_pending = false;
 }
 
+// Make the meta stream wait for an event recorded on the dma stream right
+// after this cache's submission number `seq` there, unless it already waited
+// for a later one.
+void meta_wait_dma(lsmgnn_cache *c, hipEvent_t e, uint64_t seq) {
+  if (seq <= c->meta_dma_seen) return;
+  (void)hipStreamWaitEvent(c->meta, e, 0);
+  c->meta_dma_seen = seq;
+}
+
 // Queue a harvested gather's ring write: its E enqueues have the sequence
 // numbers [tail_end - E, tail_end), of which the last min(E, V) survive; they
 // were staged in that order and land in at most two contiguous ring pieces.
@@ -348,6 +363,7 @@ void issue_dma(lsmgnn_cache *c, Flight &f) {
   }
   (void)hipEventRecord(f.dma_done, c->dma);
   f.dma_used = true;
+  f.dma_seq = ++c->dma_subs;
 }
 
 // Pageable store: copy the rows of the gather's host-fetch list (misses and
@@ -468,7 +484,7 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   // are free once gather t-2's rows have moved
   if (hipEventRecord(c->ev_in, s) != hipSuccess) return fail_device(c);
   (void)hipStreamWaitEvent(c->meta, c->ev_in, 0);
-  if (f.used) (void)hipStreamWaitEvent(c->meta, f.data_done, 0);
+  if (f.used) meta_wait_dma(c, f.data_done, f.fill_seq);
 
   // the window list of the minibatch being gathered is never consulted again:
   // the first kernel clears its bits
@@ -521,8 +537,8 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
 
   // staging and hit copy once gather t-1's fills have landed; the ring write
   // (PCIe egress) is queued later on the dma stream
-  if (pf.used) (void)hipStreamWaitEvent(c->meta, pf.data_done, 0);
-  if (f.dma_used) (void)hipStreamWaitEvent(c->meta, f.dma_done, 0);
+  if (pf.used) meta_wait_dma(c, pf.data_done, pf.fill_seq);
+  if (f.dma_used) meta_wait_dma(c, f.dma_done, f.dma_seq);
   if (n && d.V) lsm::launch_copy(CopyMode::kCacheToStage, d, n, f.sc, outp, c->meta);
   // queue mode: the hit copy also moves the victim hits, from the prefetch
   // buffer that the previous call filled
@@ -561,6 +577,7 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   rec(kEvFill1, c->dma);
   rec(kEvAll1, c->dma);
   (void)hipEventRecord(f.data_done, c->dma);
+  f.fill_seq = ++c->dma_subs;
   if (hipGetLastError() != hipSuccess) return fail_device(c);
   const uint32_t err = dedup ? c->dd->err : 0u;
   const uint32_t U = dedup ? c->dd->n_unique : 0u;
