@@ -603,6 +603,71 @@ def test_queues_pageable_store(seed):
                    victim_mode="queues")
 
 
+@pytest.mark.parametrize("pageable", [False, True])
+def test_async_rejected_calls_while_gathers_in_flight(pageable):
+    """Rejected calls between pipelined gathers, with no wait in between: the
+    rejected call's queued kernels (no-ops) reuse a flight whose previous
+    gather's fills and ring write may still be running, and the next good call
+    reuses it again.  Every gather's rows, outcomes and the final state match
+    the oracle's."""
+    log(f"case: pipelined gathers with rejected calls in flight, pageable={pageable}")
+    rng = np.random.default_rng(4242)
+    n, R, S, V, L, mb, nb = 20000, 1024, 150, 2500, 3, 6000, 36
+    store = Store.random_bytes(n, R, 11, pinned=not pageable)
+    stat = rng.integers(0, 50, n).astype(np.uint32)
+    hot = rng.permutation(n)[:3000]
+    batches = [np.concatenate([rng.choice(hot, int(rng.integers(1000, 3000))),
+                               rng.integers(0, n, int(rng.integers(500, 3000)))]) for _ in range(nb)]
+    cache = lsmgnn.FeatureCache(n, R, store.buf, stat, S, V, L, mb, pageable=pageable)
+    orc = Oracle(n, R, stat, S, V, L, store=store.np)
+    dev = lambda a: torch.as_tensor(np.asarray(a, np.int64)).cuda()  # noqa: E731
+    db = [dev(b) for b in batches]
+    bufs = [(torch.empty(mb * R, dtype=torch.uint8, device="cuda"), torch.empty(mb, dtype=torch.int64, device="cuda"),
+             torch.empty(mb, dtype=torch.int64, device="cuda"), torch.empty(mb, dtype=torch.uint8, device="cuda"))
+            for _ in range(3)]
+    for j in range(L + 1):
+        cache.advance(db[j])
+    pending, rejected, checked = {}, 0, 0
+
+    def check(b):
+        tk, r = pending.pop(b)
+        cache.wait(tk)
+        torch.cuda.current_stream().synchronize()
+        o = orc.gather(batches[b])
+        if b + L + 1 < nb:
+            orc.advance(batches[b + L + 1])
+        assert np.array_equal(r.unique.cpu().numpy(), o["uniq"]), b
+        assert np.array_equal(r.outcome.cpu().numpy(), o["outcome"]), b
+        assert np.array_equal(r.out.cpu().numpy(), o["out"]), b
+
+    for j in range(L + 1):
+        orc.advance(batches[j])
+    for b in range(nb):
+        out, uq, inv, oc = bufs[b % 3]
+        ann = db[b + L + 1] if b + L + 1 < nb else None
+        if b % 3 == 2:  # rejected calls right before the good one, gathers b-1 and b-2 still in flight
+            bad = dev([int(batches[b][0]), n + b])
+            with pytest.raises(lsmgnn.LsmgnnError) as e:
+                cache.gather_async(bad, out, uq, inverse=inv, outcome=oc, announce=ann)
+            assert e.value.status == "E_RANGE"
+            if ann is not None:
+                with pytest.raises(lsmgnn.LsmgnnError) as e:
+                    cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc, announce=bad)
+                assert e.value.status == "E_RANGE"
+            rejected += 1
+        pending[b] = cache.gather_async(db[b], out, uq, inverse=inv, outcome=oc, announce=ann)
+        if b - 1 in pending:
+            check(b - 1)
+            checked += 1
+    check(nb - 1)
+    checked += 1
+    compare_state(cache, orc, "after the stream with rejected calls")
+    tot = cache.stats()[1]
+    log(f"  {checked} gathers checked, {rejected} rounds of rejected calls; totals {tot}")
+    assert tot["victim_hits"] > 0 and tot["evictions"] > 0
+    cache.close()
+
+
 @pytest.mark.parametrize("pipelined", [False, True])
 def test_queues_rejected_gathers_in_between(pipelined):
     """A rejected gather between good ones changes nothing, also the queue
