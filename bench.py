@@ -20,9 +20,10 @@ type.
 Prints one JSON line.  `value` is gathered feature bytes (unique rows x row
 bytes) per second over the timed steps; `roofline` rates the dominant data
 kernel against its bound, timed with HIP events on the gather's stream.  The
-timed steps run twice over the same minibatches, each time from fresh caches:
-first without the library's timing events (`value`), then with them (the
-per-kernel figures, and `profiled_pass`).
+timed steps run over the same minibatches three times, each time from fresh
+caches: without the library's timing events (`value`), with them (the
+per-kernel figures, and `profiled_pass`), and untimed with every gather's
+counts read (`per_minibatch`).
 """
 import argparse
 import hashlib
@@ -426,9 +427,11 @@ def main():
             for b in list(p["tickets"]):
                 p["cache"].wait(p["tickets"].pop(b))
 
-    def run_pass(profiled):
+    def run_pass(profiled, per_gather=False):
         """Fresh caches, W warmup minibatches, then K timed ones; with
-        `profiled` the library records HIP events around every row copy."""
+        `profiled` the library records HIP events around every row copy.  With
+        `per_gather` the counts of the latest counted gather are read after
+        every step (a call that waits for the queued work: not for timing)."""
         fresh_caches()
         for b in range(args.warmup):
             step(b)
@@ -436,31 +439,52 @@ def main():
         tot0 = [p["cache"].stats()[1] for p in parts]
         for p in parts:
             p["cache"].set_profiling(profiled)
+        per = [dict() for _ in parts]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         nbytes = 0
         for b in range(args.warmup, args.warmup + args.steps):
             nbytes += step(b)
+            if per_gather:
+                for p, pp in zip(parts, per):
+                    last = p["cache"].stats()[0]
+                    pp[last["batch"]] = last
         drain()
         torch.cuda.synchronize()
         dt = time.perf_counter() - t0
         profs = [p["cache"].profile() for p in parts] if profiled else None
-        for p in parts:
+        for p, pp in zip(parts, per):
             p["cache"].set_profiling(False)
+            if per_gather:
+                last = p["cache"].stats()[0]
+                pp[last["batch"]] = last
         tot1 = [p["cache"].stats()[1] for p in parts]
         d = {k: sum(t1[k] - t0_[k] for t0_, t1 in zip(tot0, tot1)) for k in tot1[0]}
-        return dt, nbytes, d, profs
+        return dt, nbytes, d, profs, per
 
     # The headline pass runs as a user would, without the library's timing
     # events (each is a marker on a stream of the pipeline and costs a few
     # percent).  A second pass over the same minibatches, from fresh caches,
     # records the events for the per-kernel figures.
-    dt, nbytes, d, _ = run_pass(False)
+    dt, nbytes, d, _, _ = run_pass(False)
     log(f"[bench] timed pass: {args.steps} minibatches in {1e3 * dt:.1f} ms")
-    dt_p, nbytes_p, d_p, profs = run_pass(True)
+    dt_p, nbytes_p, d_p, profs, _ = run_pass(True)
     log(f"[bench] profiled pass: {1e3 * dt_p:.1f} ms")
-    assert nbytes_p == nbytes and d_p == d, "the two passes over one stream must do identical work"
+    # a third, untimed pass reads every gather's counts
+    _, nbytes_c, d_c, _, per = run_pass(False, per_gather=True)
+    assert nbytes_p == nbytes == nbytes_c and d_p == d == d_c, "the passes over one stream must do identical work"
     alone = hit_path_alone(parts, args.warmup + args.steps - 1)
+    # per-minibatch rates over the timed gathers (all parts of a minibatch summed)
+    timed = [b for b in range(args.warmup, args.warmup + args.steps) if all(b in pp for pp in per)]
+
+    def spread(key):
+        v = sorted(sum(pp[b][key] for pp in per) / max(sum(pp[b]["unique"] for pp in per), 1) for b in timed)
+        if not v:
+            return None
+        q = lambda f: v[min(len(v) - 1, int(f * len(v)))]  # noqa: E731
+        return {"min": v[0], "p10": q(0.1), "median": q(0.5), "p90": q(0.9), "max": v[-1]}
+    per_minibatch = {"gathers": len(timed), "hit_rate": spread("hits"), "victim_hit_rate": spread("victim_hits"),
+                     "miss_rate": spread("misses")}
     gbps = nbytes / dt / 1e9
     rows = d["unique"]
 
@@ -545,6 +569,7 @@ def main():
         "request_hit_rate": d["request_hits"] / max(d["requests"], 1),
         "request_victim_hit_rate": d["request_victim_hits"] / max(d["requests"], 1),
         "request_miss_rate": 1.0 - (d["request_hits"] + d["request_victim_hits"]) / max(d["requests"], 1),
+        "per_minibatch": per_minibatch,
         "unique_per_minibatch": d["unique"] / args.steps,
         "requests_per_minibatch": d["requests"] / args.steps,
         "roofline": roof,
