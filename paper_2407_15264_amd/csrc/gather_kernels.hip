@@ -1027,6 +1027,13 @@ void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t t, Scratch &sc,
   }
   hipLaunchKernelGGL(k_resolve, dim3(g), dim3(kBlock), 0, s, d, sc, t, outcome, cn);
   for (int st = kStVictimHits; st <= kStHost; ++st) grids.g[st] = g;
+}
+
+void launch_ring_enqueue(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, Counters *cn, StatGrids &grids,
+                         hipStream_t s) {
+  const unsigned g = grid_for(n, kBlock, kMaxGrid);
+  const bool ring = d.V && !d.qmode;
+  const bool queues = d.V && d.qmode && d.L > 0;
   if (ring) {
     hipLaunchKernelGGL(k_enq_finalize, dim3(g), dim3(kBlock), 0, s, d, sc, cn);
     grids.g[kStEnqCopy] = g;

@@ -215,8 +215,13 @@ void launch_refresh(const DevState &d, uint32_t t, const Counters *cn, hipStream
 // per-request outcome counts (each request takes its unique ID's outcome)
 void launch_request_counts(const DevState &d, const int64_t *ids, uint64_t n, Scratch &sc, Counters *cn,
                            StatGrids &grids, hipStream_t s);
+// sequence numbers of the batch's enqueues, then the resolve: outcomes, the
+// hit-copy, host-fetch and fill lists
 void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, uint8_t *outcome, Counters *cn,
                          StatGrids &grids, hipStream_t s);
+// after the resolve: the enqueues' ring (or queue) entries and the staging list
+void launch_ring_enqueue(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, Counters *cn, StatGrids &grids,
+                         hipStream_t s);
 // Queue mode: copy the queue of gather t+1 (slot `slot`) into prefetch buffer
 // `par`: entries placed by gathers up to t-1 from the pinned host queue, those
 // placed by gather t from its staging rows; sizes from gather t's gate.

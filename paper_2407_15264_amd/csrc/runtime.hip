@@ -506,9 +506,14 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
     lsm::launch_group_by_set(d, ids, n, inverse, f.sc, c->cn, c->meta);
     lsm::launch_set_walk(d, n, (uint32_t)t, f.sc, c->cn, grids, c->meta);
     lsm::launch_ring_resolve(d, n, t, f.sc, outcome, c->cn, grids, c->meta);
+  }
+  // the host fetch needs only the resolve's list; the rest of the metadata
+  // runs beside it
+  (void)hipEventRecord(f.meta_done, c->meta);
+  if (n) {
+    lsm::launch_ring_enqueue(d, n, t, f.sc, c->cn, grids, c->meta);
     lsm::launch_request_counts(d, ids, n, f.sc, c->cn, grids, c->meta);
   }
-  (void)hipEventRecord(f.meta_done, c->meta);
   lsm::QueueFinish qf;
   if (queues) {
     qf.qcount = d.qcount;
