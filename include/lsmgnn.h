@@ -289,6 +289,52 @@ lsmgnn_status lsmgnn_pagerank_scores(const int64_t *offsets, const uint32_t *adj
                                      double damping, uint32_t iterations, uint32_t *scores, double *rank,
                                      int device, void *stream);
 
+/* ---------------------------------------------------------- GPU sampler
+   The raw request lists of GraphSAGE minibatches (uniform neighbour sampling
+   with a fixed fanout per hop, Sec. 2.1), produced on the GPU as the system
+   overview's GPU-side sampler does (Sec. 4), so that lsmgnn_gather_async and
+   its announcement take them straight from device memory.  For minibatch b:
+     frontier_0 = the seeds, sorted, duplicates removed;
+     hop h: each frontier node v, ascending, draws k = min(fanout[h], deg v)
+       distinct adjacency positions with Floyd's algorithm and lists them
+       ascending; its samples are adj[offsets[v] + position] in that order;
+       frontier_{h+1} = the hop's samples, sorted, duplicates removed;
+     list = seeds (in the given order) ++ hop 0's samples ++ hop 1's ++ ...
+   Draws come from counter-based SplitMix64 streams: key_b =
+   derive(derive(seed, 3), b) with derive(p, l) = output l of the stream keyed
+   by mix(p ^ 0x5851f42d4c957f2d), where output k of the stream keyed by K is
+   mix(K + (k + 1) * 0x9e3779b97f4a7c15) and mix is SplitMix64's finalizer;
+   hop h uses derive(key_b, h), node v in it derive(key_hop, v), and Floyd's
+   j-th draw for v is output j of that stream reduced to [0, m) as
+   ((r >> 32) * m) >> 32.  The list depends only on the graph, the seeds, the
+   fanouts, `seed` and b.
+
+   lsmgnn_sampler_create: offsets (num_nodes + 1 int64) and adj
+   (offsets[num_nodes] uint32) in device-accessible memory on `device` (HBM,
+   or pinned host memory through its device address), read only, borrowed:
+   they must outlive the sampler.  1 <= hops <= 8, every fanout[h] <= 64
+   (copied).  The graph is checked once (offsets from 0, non-decreasing, every
+   degree below 2^32, every entry < num_nodes).  Work memory: 9 bytes per node
+   plus 1 byte per node rounded up to 16 KiB, in HBM.
+   Errors: E_INVAL (NULL pointers, num_nodes 0 or above 2^32 - 1, hops or a
+   fanout out of range); E_RANGE (a malformed graph); E_NOMEM; E_DEVICE.
+
+   lsmgnn_sample: seeds (n_seeds int64, device) in [0, num_nodes); out
+   (out_cap int64, device) receives the list.  Ordered after the work queued
+   on `stream`; returns once *n_out (the list's length) is known, with the
+   list written.  One call at a time per sampler.
+   Errors: E_RANGE (a seed outside [0, num_nodes): *n_out is set, the list is
+   not valid); E_INVAL (NULL pointers, or a list longer than out_cap: *n_out
+   is the length needed and only the first out_cap entries were written);
+   E_DEVICE. */
+typedef struct lsmgnn_sampler lsmgnn_sampler; /* opaque, owned by the library */
+lsmgnn_status lsmgnn_sampler_create(const int64_t *offsets, const uint32_t *adj, uint64_t num_nodes,
+                                    const uint32_t *fanout, uint32_t hops, uint64_t seed, int device,
+                                    lsmgnn_sampler **out);
+void lsmgnn_sampler_destroy(lsmgnn_sampler *s);
+lsmgnn_status lsmgnn_sample(lsmgnn_sampler *s, const int64_t *seeds, uint64_t n_seeds, uint64_t batch, int64_t *out,
+                            uint64_t out_cap, uint64_t *n_out, void *stream);
+
 /* Set index the cache uses for node x (host-side helper, for tests). */
 uint64_t lsmgnn_set_of(uint64_t x, uint64_t num_sets);
 

@@ -7,7 +7,7 @@ import subprocess
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB_PATH = os.path.join(PKG, "liblsmgnn.so")
-SOURCES = [os.path.join(PKG, "csrc", f) for f in ("gather_kernels.hip", "runtime.hip", "pagerank.hip")]
+SOURCES = [os.path.join(PKG, "csrc", f) for f in ("gather_kernels.hip", "runtime.hip", "pagerank.hip", "sampler.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # packed-FP32 instructions are disabled: the library's only float math is the

@@ -1,0 +1,489 @@
+// Neighbour sampling on the GPU: the raw request lists of GraphSAGE
+// minibatches (uniform sampling of a fixed number of neighbours per hop,
+// Sec. 2.1), produced on the device, as the GPU-side sampler of the system
+// overview (Sec. 4) does, so that the cache's gather and announcement take
+// them without a host round trip.
+//
+// One minibatch, from its seed nodes and the fanouts f_0 .. f_{H-1}:
+//   frontier_0 = the seeds, sorted, duplicates removed;
+//   hop h: each frontier node v, in ascending order, draws k = min(f_h, deg v)
+//     distinct positions of its adjacency list with Floyd's algorithm (Bentley
+//     and Floyd, CACM 1987) and lists them ascending; the hop's samples are
+//     adj[off[v] + position] in that order; frontier_{h+1} = the hop's samples,
+//     sorted, duplicates removed;
+//   request list = seeds (as given) ++ samples of hop 0 ++ hop 1 ++ ...
+// Random draws come from counter-based SplitMix64 streams (Steele, Lea and
+// Flood, OOPSLA 2014): output k of the stream keyed by K is mix(K + (k+1) G).
+// Minibatch b of a sampler seeded with s uses the key
+//   key_b = derive(derive(s, 3), b),  derive(p, l) = output l of the stream
+//   keyed by mix(p ^ 0x5851f42d4c957f2d);
+// hop h of it derive(key_b, h), node v in that hop derive(key_hop, v), and
+// the j-th draw of Floyd's algorithm for v is output j of that node's stream,
+// reduced to [0, m) as ((r >> 32) * m) >> 32.
+//
+// Per hop, on the caller's stream:
+//   tiles    per tile of 2048 frontier entries, the sum of the k's
+//   top      one block: exclusive scan of the tile sums, the list length
+//   draw     per entry: Floyd's draws, a sort of at most 64 positions in
+//            registers, the samples written at their list positions, and the
+//            next frontier's byte-map marks (plain byte stores)
+//   popc / chunk scan / compact: the marked nodes in ascending order become
+//            the next frontier, and the map is cleared
+// Every count stays on the device; the host learns the list length once, at
+// the end.  The byte map holds one byte per node and is all zero between calls.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+
+#include "lsmgnn.h"
+
+namespace lsm_smp {
+
+constexpr int kBlock = 256;
+constexpr int kMapBytesPerThread = 64;                        // byte-map bytes per thread
+constexpr uint64_t kChunk = (uint64_t)kBlock * kMapBytesPerThread;  // byte-map bytes per block
+constexpr int kPerThread = 8;                                 // frontier entries per thread in a tile
+constexpr uint32_t kTile = kBlock * kPerThread;
+constexpr unsigned kMaxGrid = 4096;
+constexpr uint32_t kMaxFanout = 64;
+constexpr uint32_t kMaxHops = 8;
+constexpr uint64_t kGamma = 0x9e3779b97f4a7c15ull;
+constexpr uint64_t kLabelSample = 3;
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__host__ __device__ __forceinline__ uint64_t mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+__host__ __device__ __forceinline__ uint64_t stream_at(uint64_t key, uint64_t k) { return mix(key + (k + 1) * kGamma); }
+__host__ __device__ __forceinline__ uint64_t derive(uint64_t parent, uint64_t label) {
+  return stream_at(mix(parent ^ 0x5851f42d4c957f2dull), label);
+}
+
+// Device-side state of one call.
+struct Ctl {
+  uint32_t err;       // a seed outside [0, N)
+  uint32_t frontier;  // current frontier size
+  uint64_t len;       // request-list length so far
+  uint64_t hop_base;  // list position of the current hop's first sample
+};
+
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t &total) {
+  __shared__ uint32_t wsum[kBlock / 64];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) wsum[wid] = x;
+  __syncthreads();
+  uint32_t base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kBlock / 64; ++w) {
+    const uint32_t sw = wsum[w];
+    base += (w < wid) ? sw : 0u;
+    tot += sw;
+  }
+  __syncthreads();
+  total = tot;
+  return base + x - v;
+}
+
+// 64-bit variant for the scan over tile sums
+__device__ __forceinline__ uint64_t block_exclusive_scan64(uint64_t v, uint64_t &total) {
+  __shared__ uint64_t wsum[kBlock / 64];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  uint64_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint64_t y = __shfl_up(x, d);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) wsum[wid] = x;
+  __syncthreads();
+  uint64_t base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kBlock / 64; ++w) {
+    const uint64_t sw = wsum[w];
+    base += (w < wid) ? sw : 0ull;
+    tot += sw;
+  }
+  __syncthreads();
+  total = tot;
+  return base + x - v;
+}
+
+__global__ __launch_bounds__(kBlock) void k_validate(const int64_t *off, const uint32_t *adj, uint64_t N, uint64_t E,
+                                                     uint32_t *err) {
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  bool bad = false;
+  for (uint64_t u = (uint64_t)blockIdx.x * kBlock + threadIdx.x; u < N; u += stride) {
+    const int64_t deg = off[u + 1] - off[u];
+    bad |= deg < 0 || deg > (int64_t)0xffffffffll;
+  }
+  for (uint64_t e = (uint64_t)blockIdx.x * kBlock + threadIdx.x; e < E; e += stride) bad |= adj[e] >= N;
+  if (bad) *err = 1u;
+}
+
+__global__ void k_init(Ctl *ctl, uint64_t n_seeds) {
+  if (threadIdx.x == 0) *ctl = Ctl{0u, 0u, n_seeds, n_seeds};
+}
+
+// The seeds open the list and mark the first frontier.
+__global__ __launch_bounds__(kBlock) void k_seeds(const int64_t *seeds, uint64_t n, uint64_t N, int64_t *out,
+                                                  uint64_t cap, uint8_t *present, Ctl *ctl) {
+  bool bad = false;
+  for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (uint64_t)gridDim.x * kBlock) {
+    const int64_t x = seeds[i];
+    if (x < 0 || (uint64_t)x >= N) {
+      bad = true;
+      continue;
+    }
+    if (i < cap) out[i] = x;
+    present[x] = 1;
+  }
+  if (__ballot(bad) && __lane_id() == 0) atomicOr(&ctl->err, 1u);
+}
+
+__device__ __forceinline__ void load_map(const uint8_t *present, uint32_t (&w)[kMapBytesPerThread / 4]) {
+  const u32x4 *p = reinterpret_cast<const u32x4 *>(present + (uint64_t)blockIdx.x * kChunk +
+                                                    (uint64_t)threadIdx.x * kMapBytesPerThread);
+#pragma unroll
+  for (int k = 0; k < kMapBytesPerThread / 16; ++k) {
+    const u32x4 a = p[k];
+    w[4 * k] = a.x;
+    w[4 * k + 1] = a.y;
+    w[4 * k + 2] = a.z;
+    w[4 * k + 3] = a.w;
+  }
+}
+
+// marked bytes hold exactly 1, so a word's popcount counts them
+__global__ __launch_bounds__(kBlock) void k_popc(const uint8_t *present, uint32_t *chunk_sums) {
+  uint32_t w[kMapBytesPerThread / 4];
+  load_map(present, w);
+  uint32_t c = 0;
+#pragma unroll
+  for (int k = 0; k < kMapBytesPerThread / 4; ++k) c += __popc(w[k]);
+  uint32_t tot;
+  (void)block_exclusive_scan(c, tot);
+  if (threadIdx.x == 0) chunk_sums[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uint32_t nchunks, Ctl *ctl) {
+  uint32_t carry = 0;
+  for (uint32_t base = 0; base < nchunks; base += kBlock) {
+    const uint32_t i = base + threadIdx.x;
+    const uint32_t v = i < nchunks ? chunk_sums[i] : 0u;
+    uint32_t tot;
+    const uint32_t ex = block_exclusive_scan(v, tot);
+    if (i < nchunks) chunk_sums[i] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) ctl->frontier = carry;
+}
+
+// The marked nodes, ascending, become the frontier; the map is cleared.
+__global__ __launch_bounds__(kBlock) void k_compact(uint8_t *present, const uint32_t *chunk_off, uint32_t *frontier) {
+  uint32_t w[kMapBytesPerThread / 4];
+  load_map(present, w);
+  const uint64_t b0 = (uint64_t)blockIdx.x * kChunk + (uint64_t)threadIdx.x * kMapBytesPerThread;
+  uint32_t c = 0;
+#pragma unroll
+  for (int k = 0; k < kMapBytesPerThread / 4; ++k) c += __popc(w[k]);
+  uint32_t tot;
+  const uint32_t ex = block_exclusive_scan(c, tot);
+  if (tot == 0) return;
+  uint32_t pos = chunk_off[blockIdx.x] + ex;
+#pragma unroll
+  for (int k = 0; k < kMapBytesPerThread / 4; ++k) {
+    uint32_t word = w[k];
+    if (word) reinterpret_cast<uint32_t *>(present + b0)[k] = 0u;
+    while (word) {  // marked bytes ascending: bit 8j is set for byte j
+      frontier[pos++] = (uint32_t)(b0 + 4 * k + (__builtin_ctz(word) >> 3));
+      word &= word - 1u;
+    }
+  }
+}
+
+__device__ __forceinline__ uint32_t draws_of(const int64_t *off, uint32_t v, uint32_t fanout) {
+  const uint64_t deg = (uint64_t)(off[v + 1] - off[v]);
+  return (uint32_t)(fanout < deg ? fanout : deg);
+}
+
+// Per tile of the frontier, the number of samples it draws.
+__global__ __launch_bounds__(kBlock) void k_tiles(const uint32_t *frontier, const int64_t *off, uint32_t fanout,
+                                                  uint64_t *tile_sum, const Ctl *ctl) {
+  const uint32_t f = ctl->frontier;
+  const uint32_t ntiles = (f + kTile - 1) / kTile;
+  for (uint32_t b = blockIdx.x; b < ntiles; b += gridDim.x) {
+    const uint32_t i0 = b * kTile + threadIdx.x * kPerThread;
+    uint32_t c = 0;
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k)
+      if (i0 + k < f) c += draws_of(off, frontier[i0 + k], fanout);
+    uint32_t tot;
+    (void)block_exclusive_scan(c, tot);
+    if (threadIdx.x == 0) tile_sum[b] = tot;
+  }
+}
+
+// One block: tile sums -> tile offsets within the hop; the hop's samples take
+// list positions [len, len + total).
+__global__ __launch_bounds__(kBlock) void k_top(uint64_t *tile_sum, Ctl *ctl) {
+  const uint32_t f = ctl->frontier;
+  const uint32_t ntiles = (f + kTile - 1) / kTile;
+  uint64_t carry = 0;
+  for (uint32_t base = 0; base < ntiles; base += kBlock) {
+    const uint32_t i = base + threadIdx.x;
+    const uint64_t v = i < ntiles ? tile_sum[i] : 0ull;
+    uint64_t tot;
+    const uint64_t ex = block_exclusive_scan64(v, tot);
+    if (i < ntiles) tile_sum[i] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) {
+    ctl->hop_base = ctl->len;
+    ctl->len += carry;
+  }
+}
+
+// Floyd's algorithm for node v: k distinct positions in [0, deg), ascending.
+__device__ __forceinline__ void draw_positions(uint64_t key_v, uint64_t deg, uint32_t k, uint32_t *pos) {
+  if (k == deg) {
+    for (uint32_t j = 0; j < k; ++j) pos[j] = j;
+    return;
+  }
+  uint32_t m = 0;
+  uint64_t draw = 0;
+  for (uint64_t j = deg - k; j < deg; ++j) {
+    const uint64_t r = ((stream_at(key_v, draw++) >> 32) * (j + 1)) >> 32;
+    bool seen = false;
+    for (uint32_t q = 0; q < m; ++q) seen |= pos[q] == (uint32_t)r;
+    pos[m++] = seen ? (uint32_t)j : (uint32_t)r;
+  }
+  for (uint32_t x = 1; x < m; ++x) {  // insertion sort, ascending
+    const uint32_t y = pos[x];
+    int z = (int)x - 1;
+    while (z >= 0 && pos[z] > y) {
+      pos[z + 1] = pos[z];
+      --z;
+    }
+    pos[z + 1] = y;
+  }
+}
+
+// Each thread takes kPerThread consecutive frontier entries of a tile; their
+// samples go to consecutive list positions.  `mark`: set the next frontier's
+// byte-map bytes (not needed after the last hop).
+__global__ __launch_bounds__(kBlock) void k_draw(const uint32_t *frontier, const int64_t *off, const uint32_t *adj,
+                                                 uint32_t fanout, uint64_t key_hop, const uint64_t *tile_off,
+                                                 int64_t *out, uint64_t cap, uint8_t *present, int mark,
+                                                 const Ctl *ctl) {
+  const uint32_t f = ctl->frontier;
+  const uint64_t hop_base = ctl->hop_base;
+  const uint32_t ntiles = (f + kTile - 1) / kTile;
+  uint32_t pos[kMaxFanout];
+  for (uint32_t b = blockIdx.x; b < ntiles; b += gridDim.x) {
+    const uint32_t i0 = b * kTile + threadIdx.x * kPerThread;
+    uint32_t c = 0;
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k)
+      if (i0 + k < f) c += draws_of(off, frontier[i0 + k], fanout);
+    uint32_t tot;
+    uint64_t p = hop_base + tile_off[b] + block_exclusive_scan(c, tot);
+    for (int q = 0; q < kPerThread; ++q) {
+      if (i0 + q >= f) break;
+      const uint32_t v = frontier[i0 + q];
+      const int64_t o = off[v];
+      const uint64_t deg = (uint64_t)(off[v + 1] - o);
+      const uint32_t k = (uint32_t)(fanout < deg ? fanout : deg);
+      if (k == 0) continue;
+      draw_positions(derive(key_hop, v), deg, k, pos);
+      for (uint32_t j = 0; j < k; ++j, ++p) {
+        const uint32_t u = adj[o + pos[j]];
+        if (p < cap) out[p] = (int64_t)u;
+        if (mark) present[u] = 1;
+      }
+    }
+  }
+}
+
+static unsigned grid_for(uint64_t work, uint64_t per_block, unsigned cap) {
+  uint64_t b = (work + per_block - 1) / per_block;
+  if (b < 1) b = 1;
+  if (b > cap) b = cap;
+  return (unsigned)b;
+}
+
+}  // namespace lsm_smp
+
+struct lsmgnn_sampler {
+  int device = 0;
+  const int64_t *off = nullptr;
+  const uint32_t *adj = nullptr;
+  uint64_t N = 0, nchunks = 0, max_tiles = 0;
+  uint32_t hops = 0;
+  uint32_t fanout[lsm_smp::kMaxHops] = {};
+  uint64_t seed = 0;
+  uint8_t *present = nullptr;  // byte map, nchunks * kChunk bytes, zero between calls
+  uint32_t *chunk_sums = nullptr;
+  uint32_t *frontier[2] = {nullptr, nullptr};
+  uint64_t *tile_sum = nullptr;
+  lsm_smp::Ctl *ctl = nullptr;      // device
+  lsm_smp::Ctl *ctl_host = nullptr;  // pinned copy read at the end of a call
+};
+
+namespace {
+
+struct DeviceScope {
+  int prev = -1;
+  bool ok = false;
+  explicit DeviceScope(int dev) {
+    ok = hipGetDevice(&prev) == hipSuccess && hipSetDevice(dev) == hipSuccess;
+    if (!ok) (void)hipGetLastError();
+  }
+  ~DeviceScope() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+void sampler_free(lsmgnn_sampler *s) {
+  for (void *p : {(void *)s->present, (void *)s->chunk_sums, (void *)s->frontier[0], (void *)s->frontier[1],
+                  (void *)s->tile_sum, (void *)s->ctl})
+    if (p) (void)hipFree(p);
+  if (s->ctl_host) (void)hipHostFree(s->ctl_host);
+  (void)hipGetLastError();
+  delete s;
+}
+
+}  // namespace
+
+extern "C" {
+
+lsmgnn_status lsmgnn_sampler_create(const int64_t *offsets, const uint32_t *adj, uint64_t num_nodes,
+                                    const uint32_t *fanout, uint32_t hops, uint64_t seed, int device,
+                                    lsmgnn_sampler **out) {
+  using namespace lsm_smp;
+  if (!out) return LSMGNN_E_INVAL;
+  *out = nullptr;
+  if (!offsets || !fanout || num_nodes == 0 || num_nodes > 0xffffffffull || hops == 0 || hops > kMaxHops)
+    return LSMGNN_E_INVAL;
+  for (uint32_t h = 0; h < hops; ++h)
+    if (fanout[h] > kMaxFanout) return LSMGNN_E_INVAL;
+  DeviceScope ds(device);
+  if (!ds.ok) return LSMGNN_E_DEVICE;
+  const uint64_t N = num_nodes;
+  int64_t ends[2] = {0, 0};
+  if (hipMemcpy(&ends[0], offsets, 8, hipMemcpyDeviceToHost) != hipSuccess ||
+      hipMemcpy(&ends[1], offsets + N, 8, hipMemcpyDeviceToHost) != hipSuccess) {
+    (void)hipGetLastError();
+    return LSMGNN_E_DEVICE;
+  }
+  if (ends[0] != 0 || ends[1] < 0 || ends[1] > (int64_t)1 << 40) return LSMGNN_E_RANGE;
+  const uint64_t E = (uint64_t)ends[1];
+  if (E > 0 && !adj) return LSMGNN_E_INVAL;
+  lsmgnn_sampler *s = new (std::nothrow) lsmgnn_sampler;
+  if (!s) return LSMGNN_E_NOMEM;
+  s->device = device;
+  s->off = offsets;
+  s->adj = adj;
+  s->N = N;
+  s->hops = hops;
+  s->seed = seed;
+  for (uint32_t h = 0; h < hops; ++h) s->fanout[h] = fanout[h];
+  s->nchunks = (N + kChunk - 1) / kChunk;
+  s->max_tiles = (N + kTile - 1) / kTile;
+  uint32_t *err = nullptr;
+  bool ok = hipMalloc(&s->present, s->nchunks * kChunk) == hipSuccess &&
+            hipMalloc(&s->chunk_sums, s->nchunks * 4) == hipSuccess &&
+            hipMalloc(&s->frontier[0], N * 4) == hipSuccess && hipMalloc(&s->frontier[1], N * 4) == hipSuccess &&
+            hipMalloc(&s->tile_sum, s->max_tiles * 8) == hipSuccess &&
+            hipMalloc(&s->ctl, sizeof(Ctl)) == hipSuccess &&
+            hipHostMalloc(&s->ctl_host, sizeof(Ctl), hipHostMallocDefault) == hipSuccess &&
+            hipMalloc(&err, 4) == hipSuccess;
+  if (!ok) {
+    (void)hipGetLastError();
+    if (err) (void)hipFree(err);
+    sampler_free(s);
+    return LSMGNN_E_NOMEM;
+  }
+  // the byte map starts zero; the graph is checked once so that no later
+  // kernel reads outside it
+  uint32_t herr = 0;
+  ok = hipMemset(s->present, 0, s->nchunks * kChunk) == hipSuccess && hipMemset(err, 0, 4) == hipSuccess;
+  if (ok) {
+    hipLaunchKernelGGL(k_validate, dim3(grid_for(N > E ? N : E, kBlock, 8192)), dim3(kBlock), 0, 0, offsets, adj, N,
+                       E, err);
+    ok = hipGetLastError() == hipSuccess && hipMemcpy(&herr, err, 4, hipMemcpyDeviceToHost) == hipSuccess;
+  }
+  (void)hipFree(err);
+  if (!ok) {
+    (void)hipGetLastError();
+    sampler_free(s);
+    return LSMGNN_E_DEVICE;
+  }
+  if (herr) {
+    sampler_free(s);
+    return LSMGNN_E_RANGE;
+  }
+  *out = s;
+  return LSMGNN_OK;
+}
+
+void lsmgnn_sampler_destroy(lsmgnn_sampler *s) {
+  if (!s) return;
+  DeviceScope ds(s->device);
+  (void)hipDeviceSynchronize();
+  sampler_free(s);
+}
+
+lsmgnn_status lsmgnn_sample(lsmgnn_sampler *s, const int64_t *seeds, uint64_t n_seeds, uint64_t batch, int64_t *out,
+                            uint64_t out_cap, uint64_t *n_out, void *stream) {
+  using namespace lsm_smp;
+  if (!s || !n_out || (n_seeds && !seeds) || (out_cap && !out)) return LSMGNN_E_INVAL;
+  DeviceScope ds(s->device);
+  if (!ds.ok) return LSMGNN_E_DEVICE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const unsigned gN = grid_for(s->N, kTile, kMaxGrid);  // frontier tiles: at most N entries
+  const unsigned gc = (unsigned)s->nchunks;
+  const uint64_t key_b = derive(derive(s->seed, kLabelSample), batch);
+  hipLaunchKernelGGL(k_init, dim3(1), dim3(64), 0, st, s->ctl, n_seeds);
+  if (n_seeds)
+    hipLaunchKernelGGL(k_seeds, dim3(grid_for(n_seeds, kBlock, kMaxGrid)), dim3(kBlock), 0, st, seeds, n_seeds, s->N,
+                       out, out_cap, s->present, s->ctl);
+  hipLaunchKernelGGL(k_popc, dim3(gc), dim3(kBlock), 0, st, s->present, s->chunk_sums);
+  hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, st, s->chunk_sums, (uint32_t)s->nchunks, s->ctl);
+  hipLaunchKernelGGL(k_compact, dim3(gc), dim3(kBlock), 0, st, s->present, s->chunk_sums, s->frontier[0]);
+  // with a bad seed the frontier is still built (and the map cleared) from the
+  // valid ones; the hops run, and the call reports E_RANGE
+  for (uint32_t h = 0; h < s->hops; ++h) {
+    uint32_t *cur = s->frontier[h & 1], *nxt = s->frontier[(h + 1) & 1];
+    const int last = h + 1 == s->hops;
+    hipLaunchKernelGGL(k_tiles, dim3(gN), dim3(kBlock), 0, st, cur, s->off, s->fanout[h], s->tile_sum, s->ctl);
+    hipLaunchKernelGGL(k_top, dim3(1), dim3(kBlock), 0, st, s->tile_sum, s->ctl);
+    hipLaunchKernelGGL(k_draw, dim3(gN), dim3(kBlock), 0, st, cur, s->off, s->adj, s->fanout[h], derive(key_b, h),
+                       s->tile_sum, out, out_cap, s->present, last ? 0 : 1, s->ctl);
+    if (!last) {
+      hipLaunchKernelGGL(k_popc, dim3(gc), dim3(kBlock), 0, st, s->present, s->chunk_sums);
+      hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, st, s->chunk_sums, (uint32_t)s->nchunks, s->ctl);
+      hipLaunchKernelGGL(k_compact, dim3(gc), dim3(kBlock), 0, st, s->present, s->chunk_sums, nxt);
+    }
+  }
+  if (hipGetLastError() != hipSuccess ||
+      hipMemcpyAsync(s->ctl_host, s->ctl, sizeof(Ctl), hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess) {
+    (void)hipGetLastError();
+    return LSMGNN_E_DEVICE;
+  }
+  *n_out = s->ctl_host->len;
+  if (s->ctl_host->err) return LSMGNN_E_RANGE;
+  return s->ctl_host->len > out_cap ? LSMGNN_E_INVAL : LSMGNN_OK;
+}
+
+}  // extern "C"

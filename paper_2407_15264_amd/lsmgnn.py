@@ -113,6 +113,12 @@ def lib():
         L.lsmgnn_pagerank_scores.argtypes = [vp, vp, u64, ctypes.c_double, ctypes.c_uint32, vp, vp, i32, vp]
         L.lsmgnn_expand.restype = i32
         L.lsmgnn_expand.argtypes = [vp, vp, u64, u64, vp, vp]
+        L.lsmgnn_sampler_create.restype = i32
+        L.lsmgnn_sampler_create.argtypes = [vp, vp, u64, vp, ctypes.c_uint32, u64, i32, ctypes.POINTER(vp)]
+        L.lsmgnn_sampler_destroy.restype = None
+        L.lsmgnn_sampler_destroy.argtypes = [vp]
+        L.lsmgnn_sample.restype = i32
+        L.lsmgnn_sample.argtypes = [vp, vp, u64, u64, vp, u64, ctypes.POINTER(u64), vp]
         L.lsmgnn_strerror.restype = ctypes.c_char_p
         L.lsmgnn_strerror.argtypes = [i32]
         _lib = L
@@ -166,6 +172,43 @@ def pagerank_scores(offsets, adj, damping=0.85, iterations=20, rank=False, devic
                                         ctypes.c_void_p(rk.data_ptr()) if rank else None, int(device),
                                         _stream_handle(stream, device)), "lsmgnn_pagerank_scores")
     return (scores[:n], rk[:n]) if rank else scores[:n]
+
+
+class GpuSampler:
+    """GraphSAGE request lists sampled on the GPU (lsmgnn_sampler_create /
+    lsmgnn_sample) from a CSR graph in device memory (offsets int64 [N+1],
+    adj int32/uint32 [E]); the tensors must outlive the sampler."""
+
+    def __init__(self, offsets, adj, fanout, seed=0, device=0):
+        import torch
+        self.device = torch.device("cuda", device)
+        self._graph = (offsets, adj)  # keeps the borrowed graph alive
+        self.num_nodes = offsets.numel() - 1
+        fan = (ctypes.c_uint32 * len(fanout))(*[int(f) for f in fanout])
+        self.hops = len(fanout)
+        h = ctypes.c_void_p()
+        _check(lib().lsmgnn_sampler_create(ctypes.c_void_p(offsets.data_ptr()),
+                                           ctypes.c_void_p(adj.data_ptr()) if adj.numel() else None,
+                                           self.num_nodes, fan, self.hops, int(seed), int(device), ctypes.byref(h)),
+               "lsmgnn_sampler_create")
+        self._destroy = lib().lsmgnn_sampler_destroy  # kept: module globals may be gone when the finalizer runs
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._destroy(self._h)
+            self._h = None
+
+    __del__ = close
+
+    def sample(self, seeds, batch, out, stream=None):
+        """Request list of minibatch `batch` from its seeds (int64 device
+        tensor) into `out` (int64 device tensor); returns out[:length]."""
+        n = ctypes.c_uint64(0)
+        _check(lib().lsmgnn_sample(self._h, ctypes.c_void_p(seeds.data_ptr()) if seeds.numel() else None,
+                                   seeds.numel(), int(batch), ctypes.c_void_p(out.data_ptr()), out.numel(),
+                                   ctypes.byref(n), _stream_handle(stream, self.device.index)), "lsmgnn_sample")
+        return out[: n.value]
 
 
 class PinnedBuffer:

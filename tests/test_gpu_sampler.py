@@ -1,0 +1,145 @@
+"""GPU neighbour sampler (lsmgnn_sampler_create / lsmgnn_sample) against the
+seeded host sampler of the workload generator, needs an MI355X.
+
+Both implement one definition (uniform sampling without replacement per hop,
+Floyd's draws from counter-based SplitMix64 streams), so every request list
+must be identical, element by element, including the seeds' order, the
+frontier order and the order of each node's samples.
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from paper_2407_15264_amd import lsmgnn  # noqa: E402
+from paper_2407_15264_amd import workload as W  # noqa: E402
+from tests.parity_driver import log  # noqa: E402
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lsmgnn.lib()
+
+
+def _dev_graph(g):
+    off = torch.as_tensor(np.asarray(g.offsets, np.int64)).cuda()
+    adj = torch.as_tensor(np.asarray(g.adj, np.uint32).view(np.int32)).cuda()
+    return off, adj
+
+
+def _host_lists(g, seeds, batch_size, fanout, nb, seed):
+    ids, offs = W.sample_batches(g, np.asarray(seeds, np.int64), batch_size, fanout, 0, nb, seed)
+    return [ids[offs[b]:offs[b + 1]] for b in range(nb)]
+
+
+def _check_stream(g, seeds, batch_size, fanout, nb, seed, label, cap=None):
+    ref = _host_lists(g, seeds, batch_size, fanout, nb, seed)
+    off, adj = _dev_graph(g)
+    smp = lsmgnn.GpuSampler(off, adj, fanout, seed=seed)
+    dseeds = torch.as_tensor(np.asarray(seeds, np.int64)).cuda()
+    cap = cap or max(1, max(r.size for r in ref))
+    out = torch.empty(cap, dtype=torch.int64, device="cuda")
+    for b in range(nb):
+        got = smp.sample(dseeds[b * batch_size:(b + 1) * batch_size], b, out).cpu().numpy()
+        assert got.size == ref[b].size, (label, b, got.size, ref[b].size)
+        assert np.array_equal(got, ref[b]), (label, b, int(np.argmax(got != ref[b])))
+    log(f"  {label}: {nb} lists identical, {sum(r.size for r in ref)} requests")
+    smp.close()
+    return ref
+
+
+@pytest.mark.parametrize("fanout", [(10, 5), (15, 10, 5), (64,), (3, 3, 3, 3), (1, 64, 1)])
+def test_rmat_lists_match_host_sampler(fanout):
+    log(f"case: R-MAT 2^12 nodes, 2^15 edges, fanout {fanout}")
+    g = W.rmat_graph(1 << 12, 1 << 15, seed=5)
+    seeds = W.seed_permutation(1 << 12, 12 * 100, seed=5)
+    _check_stream(g, seeds, 100, fanout, 12, seed=5, label=f"fanout {fanout}")
+
+
+def test_duplicate_seeds_zero_degree_nodes_and_small_degrees():
+    """Repeated seeds stay in the list as given (the frontier holds each once);
+    nodes without neighbours draw nothing; nodes with fewer neighbours than
+    the fanout list all of them."""
+    log("case: duplicate seeds, zero-degree and low-degree nodes")
+    rng = np.random.default_rng(3)
+    n = 500
+    deg = rng.choice([0, 0, 1, 2, 5, 30, 80], n)
+    off = np.zeros(n + 1, np.int64)
+    np.cumsum(deg, out=off[1:])
+    adj = rng.integers(0, n, int(off[-1])).astype(np.uint32)
+    g = W.Graph(off, adj, np.zeros(n, np.uint32))
+    seeds = rng.integers(0, n, 40 * 30)
+    seeds[::7] = seeds[0]
+    _check_stream(g, seeds, 40, (6, 64, 2), 30, seed=11, label="mixed degrees")
+
+
+def test_workload_stream_matches_generated_requests():
+    """The first minibatches of the bench workload: the GPU sampler gives the
+    request lists the bench's host-generated streams hold."""
+    cfg = W.CONFIGS[W.RMAT20]
+    log(f"case: {cfg.name}, first 6 minibatches")
+    wl = W.Workload(cfg, 6)
+    off, adj = _dev_graph(wl.graph)
+    smp = lsmgnn.GpuSampler(off, adj, cfg.fanout, seed=cfg.seed)
+    seeds = torch.as_tensor(wl.seeds).cuda()
+    out = torch.empty(wl.max_batch, dtype=torch.int64, device="cuda")
+    for b in range(6):
+        got = smp.sample(seeds[b * cfg.batch_size:(b + 1) * cfg.batch_size], b, out).cpu().numpy()
+        assert np.array_equal(got, wl.batch(b)), b
+    log(f"  identical to the generated stream ({wl.ids.size} requests)")
+    smp.close()
+
+
+def test_capacity_empty_and_bad_seeds():
+    g = W.rmat_graph(1 << 10, 1 << 13, seed=2)
+    n = 1 << 10
+    ref = _host_lists(g, np.arange(64), 64, (10, 5), 1, 9)[0]
+    off, adj = _dev_graph(g)
+    smp = lsmgnn.GpuSampler(off, adj, (10, 5), seed=9)
+    seeds = torch.arange(64, dtype=torch.int64, device="cuda")
+    # a list longer than the output: E_INVAL, the length needed, the prefix written
+    small = torch.full((100,), -7, dtype=torch.int64, device="cuda")
+    with pytest.raises(lsmgnn.LsmgnnError) as e:
+        smp.sample(seeds, 0, small)
+    assert e.value.status == "E_INVAL"
+    assert np.array_equal(small.cpu().numpy(), ref[:100])
+    # no seeds: an empty list
+    out = torch.empty(ref.size, dtype=torch.int64, device="cuda")
+    assert smp.sample(torch.empty(0, dtype=torch.int64, device="cuda"), 0, out).numel() == 0
+    # a seed outside [0, N) rejects the call; the next call is unaffected
+    for bad in ([3, n], [-1, 5]):
+        with pytest.raises(lsmgnn.LsmgnnError) as e:
+            smp.sample(torch.as_tensor(bad, dtype=torch.int64).cuda(), 0, out)
+        assert e.value.status == "E_RANGE"
+        assert np.array_equal(smp.sample(seeds, 0, out).cpu().numpy(), ref)
+    smp.close()
+
+
+def test_bad_graphs_and_arguments_rejected():
+    n = 64
+    off = np.arange(n + 1, dtype=np.int64)
+    adj = np.arange(n, dtype=np.uint32)
+    good_off, good_adj = torch.as_tensor(off).cuda(), torch.as_tensor(adj.view(np.int32)).cuda()
+    for fanout in ((), (65,), (1,) * 9):
+        with pytest.raises(lsmgnn.LsmgnnError) as e:
+            lsmgnn.GpuSampler(good_off, good_adj, fanout)
+        assert e.value.status == "E_INVAL"
+    bad_adj = adj.copy()
+    bad_adj[10] = n  # an entry outside [0, N)
+    with pytest.raises(lsmgnn.LsmgnnError) as e:
+        lsmgnn.GpuSampler(good_off, torch.as_tensor(bad_adj.view(np.int32)).cuda(), (4,))
+    assert e.value.status == "E_RANGE"
+    bad_off = off.copy()
+    bad_off[5], bad_off[6] = 7, 6  # decreasing, same total
+    with pytest.raises(lsmgnn.LsmgnnError) as e:
+        lsmgnn.GpuSampler(torch.as_tensor(bad_off).cuda(), good_adj, (4,))
+    assert e.value.status == "E_RANGE"
+    shifted = off + 1  # does not start at 0; adj still holds offsets[N] entries
+    adj2 = np.zeros(n + 1, np.uint32)
+    with pytest.raises(lsmgnn.LsmgnnError) as e:
+        lsmgnn.GpuSampler(torch.as_tensor(shifted).cuda(), torch.as_tensor(adj2.view(np.int32)).cuda(), (4,))
+    assert e.value.status == "E_RANGE"
