@@ -165,7 +165,7 @@ def make_parts(W, cfg, nb):
         wl = W.Workload(cfg, nb)
         parts = [dict(label="all", num_nodes=cfg.num_nodes, dim=cfg.dim, elt=cfg.elt_bytes, seed=cfg.seed,
                       static=wl.static, shape=cfg.cache, batches=[wl.batch(b) for b in range(nb)],
-                      graph=wl.graph)]
+                      graph=wl.graph, seeds=wl.seeds)]
         requests = float(wl.ids.size) / nb
     for p in parts:
         p["R"] = p["dim"] * p["elt"]
@@ -219,6 +219,31 @@ def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None, victim_mode
             "cpu": _cpu_model(), "host_cpus": os.cpu_count()}
 
 
+def gpu_sampler_check(torch, lsmgnn, W, part, cfg, L, nb, warmup, steps, dev):
+    """The GPU sampler against the host-generated lists (every minibatch of the
+    run, element by element), and its rate alone: the timed minibatches sampled
+    back to back, against the host sampler on the same minibatches."""
+    import numpy as np
+    g = part["graph"]
+    lists = SampledLists(torch, lsmgnn, g, part["seeds"], cfg, L, max(1, max(b.size for b in part["batches"])), dev)
+    mismatched = sum(int(not np.array_equal(lists[b].cpu().numpy(), part["batches"][b])) for b in range(nb))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for b in range(warmup, warmup + steps):
+        lists[b]
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    requests = sum(int(part["batches"][b].size) for b in range(warmup, warmup + steps))
+    t0 = time.perf_counter()
+    W.sample_batches(g, part["seeds"], cfg.batch_size, cfg.fanout, warmup, warmup + steps, cfg.seed)
+    dh = time.perf_counter() - t0
+    lists.sampler.close()
+    return {"identical_to_host_lists": mismatched == 0, "minibatches_compared": nb,
+            "alone_ms_per_minibatch": 1e3 * dt / steps, "alone_requests_per_s": requests / dt,
+            "host_sampler_ms_per_minibatch": 1e3 * dh / steps,
+            "host_sampler_threads": int(os.environ.get("OMP_NUM_THREADS", os.cpu_count()))}
+
+
 def hit_path_alone(parts, b, reps=5):
     """The hit copy with no host fetch running beside it: minibatch b gathered
     again (once to make its rows resident, then `reps` timed passes that find
@@ -249,6 +274,29 @@ def hit_path_alone(parts, b, reps=5):
                    "bytes = hit rows x row bytes x 2 (read + write)"}
 
 
+class SampledLists:
+    """Request lists of a homogeneous workload sampled on the GPU on demand
+    (lsmgnn_sample), indexable like the list of resident host-generated ones.
+    A ring of L+3 buffers: the list written at step b (minibatch b+L+1) takes
+    the buffer of minibatch b-2, whose gather's metadata has finished by then
+    (the caller's stream, on which the sampler runs, has waited for its rows)."""
+
+    def __init__(self, torch, lsmgnn, graph, seeds, cfg, L, max_len, dev):
+        self.off = torch.as_tensor(graph.offsets).to(dev)
+        self.adj = torch.as_tensor(graph.adj.view("int32")).to(dev)
+        self.sampler = lsmgnn.GpuSampler(self.off, self.adj, cfg.fanout, seed=cfg.seed)
+        self.seeds = torch.as_tensor(seeds).to(dev)
+        self.B = cfg.batch_size
+        self.ring = [torch.empty(max_len, dtype=torch.int64, device=dev) for _ in range(L + 3)]
+        self.held = [None] * (L + 3)  # (minibatch, view) in each buffer
+
+    def __getitem__(self, b):
+        k = b % len(self.ring)
+        if self.held[k] is None or self.held[k][0] != b:
+            self.held[k] = (b, self.sampler.sample(self.seeds[b * self.B:(b + 1) * self.B], b, self.ring[k]))
+        return self.held[k][1]
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -276,6 +324,9 @@ def main():
                     help="static score: the in-degree, or the reverse PageRank computed on the GPU")
     ap.add_argument("--sync", action="store_true",
                     help="blocking lsmgnn_gather per minibatch instead of the pipelined lsmgnn_gather_async")
+    ap.add_argument("--gpu-sampler", action="store_true",
+                    help="sample each minibatch's request list on the GPU inside the timed region (lsmgnn_sample; "
+                         "homogeneous workloads) instead of taking the resident host-generated lists")
     ap.add_argument("--duplex-probe", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--no-duplex-probe", action="store_true",
                     help="skip the link probe with both directions at once (a child process)")
@@ -310,6 +361,9 @@ def main():
     # the minibatches the timed stream gathers or announces (a prefix of the
     # configured run); near the run's end the last gathers announce nothing
     nb = min(cfg.batches, args.warmup + args.steps + L + 1)
+    if args.gpu_sampler and isinstance(cfg, W.HeteroConfig):
+        print("bench.py: --gpu-sampler is for the homogeneous workloads", file=sys.stderr)
+        sys.exit(2)
     if args.static == "pagerank" and isinstance(cfg, W.HeteroConfig):
         print("bench.py: --static pagerank is for the homogeneous workloads", file=sys.stderr)
         sys.exit(2)
@@ -362,10 +416,17 @@ def main():
         parts[0]["static"] = sc.cpu().numpy().view(np.uint32).copy()
         del off_t, adj_t, sc
         log(f"[bench] reverse-PageRank static scores in {static_info['ms']:.1f} ms")
+    sampler_info = None
+    if args.gpu_sampler:
+        sampler_info = gpu_sampler_check(torch, lsmgnn, W, parts[0], cfg, L, nb, args.warmup, args.steps, dev)
+        log(f"[bench] GPU sampler: {sampler_info}")
     for p in parts:
+        if args.gpu_sampler:
+            p["dev_batches"] = SampledLists(torch, lsmgnn, p["graph"], p["seeds"], cfg, L,
+                                            max(1, max(b.size for b in p["batches"])), dev)
+        else:
+            p["dev_batches"] = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in p["batches"]]
         p.pop("graph", None)
-    for p in parts:
-        p["dev_batches"] = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in p["batches"]]
         mb = max(1, max(b.size for b in p["batches"]))
         # three output sets rotate: at most two gathers are in flight
         p["bufs"] = [(torch.empty(mb * p["R"], dtype=torch.uint8, device=dev),
@@ -557,6 +618,8 @@ def main():
                        victim_ring="off" if args.no_ring else "on", victim_mode=args.victim_mode,
                        refresh_period=args.refresh_period,
                        simulated_training_us=args.train_us,
+                       requests=("sampled on the GPU inside the timed region (lsmgnn_sample)" if args.gpu_sampler
+                                 else "host-generated, resident in HBM before the timed region"),
                        first_timed_minibatch=args.warmup,
                        api=("lsmgnn_gather + lsmgnn_advance" if args.sync
                             else "lsmgnn_gather_async with announcement (two minibatches in flight)")),
@@ -578,6 +641,7 @@ def main():
                     for k, v in kern.items()},
         "gather_ms_events": sum(pr["gather_ms"] for pr in profs) / max(sum(pr["gathers"] for pr in profs), 1),
         "ceilings": ceil,
+        "gpu_sampler": sampler_info,
         "profiled_pass": {"value": nbytes_p / dt_p / 1e9, "ms_per_step": 1e3 * dt_p / args.steps,
                           "how": "the same minibatches from fresh caches with the library's HIP timing "
                                  "events on; `kernels` and the rooflines come from this pass, `value` "
