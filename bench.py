@@ -38,6 +38,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "gathered feature GB/s per minibatch stream (% HBM/host-link roofline) + hit rate"
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
+SAMPLE_AHEAD = 2                # --gpu-sampler: minibatches sampled before their announcement
 PCIE5_X16_PEAK_GBPS = 64.0      # host link, published per direction
 
 
@@ -274,27 +275,64 @@ def hit_path_alone(parts, b, reps=5):
                    "bytes = hit rows x row bytes x 2 (read + write)"}
 
 
+def side_stream(torch):
+    """One more HIP stream, at default priority, from the runtime PyTorch
+    loaded (a torch.cuda.Stream would instantiate PyTorch's whole stream pool)."""
+    import ctypes
+    hip = ctypes.CDLL(os.path.join(os.path.dirname(torch.__file__), "lib", "libamdhip64.so"))
+    s = ctypes.c_void_p()
+    rc = hip.hipStreamCreateWithFlags(ctypes.byref(s), ctypes.c_uint(1))  # hipStreamNonBlocking
+    if rc != 0:
+        raise RuntimeError(f"hipStreamCreateWithFlags failed ({rc})")
+    return torch.cuda.ExternalStream(s.value)
+
+
 class SampledLists:
     """Request lists of a homogeneous workload sampled on the GPU on demand
-    (lsmgnn_sample), indexable like the list of resident host-generated ones.
-    A ring of L+3 buffers: the list written at step b (minibatch b+L+1) takes
-    the buffer of minibatch b-2, whose gather's metadata has finished by then
-    (the caller's stream, on which the sampler runs, has waited for its rows)."""
+    (lsmgnn_sample_async), indexable like the list of resident host-generated
+    ones.  The sampler runs on `stream` (a training loop's data-loading
+    stream); prefetch(b) queues minibatch b's list without waiting, and
+    indexing waits only for that list.  Ring of L+3+ahead buffers: the list
+    prefetched at step b (minibatch b+L+1+ahead) takes the buffer of minibatch
+    b-2, whose gather's metadata has finished by then (the host has seen
+    gather b-1's unique count, and the metadata stream is in order)."""
 
-    def __init__(self, torch, lsmgnn, graph, seeds, cfg, L, max_len, dev):
+    def __init__(self, torch, lsmgnn, graph, seeds, cfg, L, max_len, dev, stream=None, ahead=0):
+        import numpy as np
+        self.torch = torch
         self.off = torch.as_tensor(graph.offsets).to(dev)
         self.adj = torch.as_tensor(graph.adj.view("int32")).to(dev)
         self.sampler = lsmgnn.GpuSampler(self.off, self.adj, cfg.fanout, seed=cfg.seed)
         self.seeds = torch.as_tensor(seeds).to(dev)
         self.B = cfg.batch_size
-        self.ring = [torch.empty(max_len, dtype=torch.int64, device=dev) for _ in range(L + 3)]
-        self.held = [None] * (L + 3)  # (minibatch, view) in each buffer
+        K = L + 3 + ahead
+        self.ring = [torch.empty(max_len, dtype=torch.int64, device=dev) for _ in range(K)]
+        self.res = lsmgnn.PinnedBuffer(16 * K)  # (length, status) per buffer
+        self.res_np = self.res.numpy(np.uint64, (K, 2))
+        self.events = [torch.cuda.Event() for _ in range(K)]
+        self.issued = [None] * K  # minibatch queued into each buffer
+        self.ready = [None] * K   # its list, once waited for
+        self.stream = stream
+
+    def prefetch(self, b):
+        k = b % len(self.ring)
+        if self.issued[k] == b:
+            return
+        self.sampler.sample_async(self.seeds[b * self.B:(b + 1) * self.B], b, self.ring[k], self.res.ptr + 16 * k,
+                                  stream=self.stream)
+        self.events[k].record(self.stream if self.stream is not None else self.torch.cuda.current_stream())
+        self.issued[k], self.ready[k] = b, None
 
     def __getitem__(self, b):
         k = b % len(self.ring)
-        if self.held[k] is None or self.held[k][0] != b:
-            self.held[k] = (b, self.sampler.sample(self.seeds[b * self.B:(b + 1) * self.B], b, self.ring[k]))
-        return self.held[k][1]
+        self.prefetch(b)
+        if self.ready[k] is None:
+            self.events[k].synchronize()
+            n, status = int(self.res_np[k, 0]), int(self.res_np[k, 1])
+            if status != 0:
+                raise RuntimeError(f"lsmgnn_sample_async of minibatch {b}: status {status}")
+            self.ready[k] = self.ring[k][:n]
+        return self.ready[k]
 
 
 def main():
@@ -338,6 +376,10 @@ def main():
     if args.duplex_probe:
         duplex_probe()
         return
+    if args.gpu_sampler:
+        # the sampler's stream is a fifth stream beside the caller's and the
+        # library's three: give each its own hardware queue (HIP's default is 4)
+        os.environ["GPU_MAX_HW_QUEUES"] = "8"
     # The child process starts before this one touches the GPU.  Not under a
     # profiler: its preloaded library would trace the child too, into the same
     # output files.
@@ -423,7 +465,8 @@ def main():
     for p in parts:
         if args.gpu_sampler:
             p["dev_batches"] = SampledLists(torch, lsmgnn, p["graph"], p["seeds"], cfg, L,
-                                            max(1, max(b.size for b in p["batches"])), dev)
+                                            max(1, max(b.size for b in p["batches"])), dev, side_stream(torch),
+                                            ahead=SAMPLE_AHEAD)
         else:
             p["dev_batches"] = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in p["batches"]]
         p.pop("graph", None)
@@ -466,6 +509,8 @@ def main():
         nbytes = 0
         for p in parts:
             c, db = p["cache"], p["dev_batches"]
+            if args.gpu_sampler and b + L + 1 + SAMPLE_AHEAD < nb:
+                db.prefetch(b + L + 1 + SAMPLE_AHEAD)  # sampled ahead on its own stream
             out, uniq, inv = p["bufs"][b % 3]
             if args.sync:
                 r = c.gather(db[b], out=out, unique=uniq, inverse=inv)
@@ -618,7 +663,9 @@ def main():
                        victim_ring="off" if args.no_ring else "on", victim_mode=args.victim_mode,
                        refresh_period=args.refresh_period,
                        simulated_training_us=args.train_us,
-                       requests=("sampled on the GPU inside the timed region (lsmgnn_sample)" if args.gpu_sampler
+                       requests=(f"sampled on the GPU inside the timed region (lsmgnn_sample_async on a stream "
+                                 f"of its own, {SAMPLE_AHEAD} minibatches before their announcement)"
+                                 if args.gpu_sampler
                                  else "host-generated, resident in HBM before the timed region"),
                        first_timed_minibatch=args.warmup,
                        api=("lsmgnn_gather + lsmgnn_advance" if args.sync

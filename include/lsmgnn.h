@@ -322,7 +322,8 @@ lsmgnn_status lsmgnn_pagerank_scores(const int64_t *offsets, const uint32_t *adj
    lsmgnn_sample: seeds (n_seeds int64, device) in [0, num_nodes); out
    (out_cap int64, device) receives the list.  Ordered after the work queued
    on `stream`; returns once *n_out (the list's length) is known, with the
-   list written.  One call at a time per sampler.
+   list written.  Calls of one sampler share its work memory: one at a time,
+   or queued on one stream.
    Errors: E_RANGE (a seed outside [0, num_nodes): *n_out is set, the list is
    not valid); E_INVAL (NULL pointers, or a list longer than out_cap: *n_out
    is the length needed and only the first out_cap entries were written);
@@ -334,6 +335,17 @@ lsmgnn_status lsmgnn_sampler_create(const int64_t *offsets, const uint32_t *adj,
 void lsmgnn_sampler_destroy(lsmgnn_sampler *s);
 lsmgnn_status lsmgnn_sample(lsmgnn_sampler *s, const int64_t *seeds, uint64_t n_seeds, uint64_t batch, int64_t *out,
                             uint64_t out_cap, uint64_t *n_out, void *stream);
+/* lsmgnn_sample_async: the same sampling, queued on `stream` without waiting
+   for it (a data-loading stream can then sample minibatches ahead of the
+   gathers).  When the stream has run the call, result_host[0] holds the
+   list's length and result_host[1] its status (LSMGNN_OK, LSMGNN_E_RANGE for a
+   seed outside [0, num_nodes), LSMGNN_E_INVAL for a list longer than
+   out_cap); result_host is two uint64 in pinned host memory (lsmgnn_host_alloc),
+   to be read after the caller has synchronized with the stream.  Calls of one
+   sampler share its work memory: queue them on one stream.  Returns E_INVAL
+   for NULL pointers, E_DEVICE if queueing failed, else LSMGNN_OK. */
+lsmgnn_status lsmgnn_sample_async(lsmgnn_sampler *s, const int64_t *seeds, uint64_t n_seeds, uint64_t batch,
+                                  int64_t *out, uint64_t out_cap, uint64_t *result_host, void *stream);
 
 /* Set index the cache uses for node x (host-side helper, for tests). */
 uint64_t lsmgnn_set_of(uint64_t x, uint64_t num_sets);

@@ -314,6 +314,15 @@ __global__ __launch_bounds__(kBlock) void k_draw(const uint32_t *frontier, const
   }
 }
 
+// (list length, status) of the call: LSMGNN_OK, E_RANGE for a bad seed, or
+// E_INVAL for a list longer than the output
+__global__ void k_result(const Ctl *ctl, uint64_t cap, uint64_t *res) {
+  if (threadIdx.x == 0) {
+    res[0] = ctl->len;
+    res[1] = ctl->err ? (uint64_t)LSMGNN_E_RANGE : ctl->len > cap ? (uint64_t)LSMGNN_E_INVAL : (uint64_t)LSMGNN_OK;
+  }
+}
+
 static unsigned grid_for(uint64_t work, uint64_t per_block, unsigned cap) {
   uint64_t b = (work + per_block - 1) / per_block;
   if (b < 1) b = 1;
@@ -335,8 +344,9 @@ struct lsmgnn_sampler {
   uint32_t *chunk_sums = nullptr;
   uint32_t *frontier[2] = {nullptr, nullptr};
   uint64_t *tile_sum = nullptr;
-  lsm_smp::Ctl *ctl = nullptr;      // device
-  lsm_smp::Ctl *ctl_host = nullptr;  // pinned copy read at the end of a call
+  lsm_smp::Ctl *ctl = nullptr;     // device
+  uint64_t *res = nullptr;          // device: (list length, status) of the last call queued
+  uint64_t *res_host = nullptr;     // pinned: the same, read by the blocking call
 };
 
 namespace {
@@ -355,11 +365,45 @@ struct DeviceScope {
 
 void sampler_free(lsmgnn_sampler *s) {
   for (void *p : {(void *)s->present, (void *)s->chunk_sums, (void *)s->frontier[0], (void *)s->frontier[1],
-                  (void *)s->tile_sum, (void *)s->ctl})
+                  (void *)s->tile_sum, (void *)s->ctl, (void *)s->res})
     if (p) (void)hipFree(p);
-  if (s->ctl_host) (void)hipHostFree(s->ctl_host);
+  if (s->res_host) (void)hipHostFree(s->res_host);
   (void)hipGetLastError();
   delete s;
+}
+
+// Queue one minibatch's sampling on `st`; the last kernel leaves (list
+// length, status) in s->res.
+bool queue_sample(lsmgnn_sampler *s, const int64_t *seeds, uint64_t n_seeds, uint64_t batch, int64_t *out,
+                  uint64_t out_cap, hipStream_t st) {
+  using namespace lsm_smp;
+  const unsigned gN = grid_for(s->N, kTile, kMaxGrid);  // frontier tiles: at most N entries
+  const unsigned gc = (unsigned)s->nchunks;
+  const uint64_t key_b = derive(derive(s->seed, kLabelSample), batch);
+  hipLaunchKernelGGL(k_init, dim3(1), dim3(64), 0, st, s->ctl, n_seeds);
+  if (n_seeds)
+    hipLaunchKernelGGL(k_seeds, dim3(grid_for(n_seeds, kBlock, kMaxGrid)), dim3(kBlock), 0, st, seeds, n_seeds, s->N,
+                       out, out_cap, s->present, s->ctl);
+  hipLaunchKernelGGL(k_popc, dim3(gc), dim3(kBlock), 0, st, s->present, s->chunk_sums);
+  hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, st, s->chunk_sums, (uint32_t)s->nchunks, s->ctl);
+  hipLaunchKernelGGL(k_compact, dim3(gc), dim3(kBlock), 0, st, s->present, s->chunk_sums, s->frontier[0]);
+  // with a bad seed the frontier is still built (and the map cleared) from the
+  // valid ones; the hops run, and the call reports E_RANGE
+  for (uint32_t h = 0; h < s->hops; ++h) {
+    uint32_t *cur = s->frontier[h & 1], *nxt = s->frontier[(h + 1) & 1];
+    const int last = h + 1 == s->hops;
+    hipLaunchKernelGGL(k_tiles, dim3(gN), dim3(kBlock), 0, st, cur, s->off, s->fanout[h], s->tile_sum, s->ctl);
+    hipLaunchKernelGGL(k_top, dim3(1), dim3(kBlock), 0, st, s->tile_sum, s->ctl);
+    hipLaunchKernelGGL(k_draw, dim3(gN), dim3(kBlock), 0, st, cur, s->off, s->adj, s->fanout[h], derive(key_b, h),
+                       s->tile_sum, out, out_cap, s->present, last ? 0 : 1, s->ctl);
+    if (!last) {
+      hipLaunchKernelGGL(k_popc, dim3(gc), dim3(kBlock), 0, st, s->present, s->chunk_sums);
+      hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, st, s->chunk_sums, (uint32_t)s->nchunks, s->ctl);
+      hipLaunchKernelGGL(k_compact, dim3(gc), dim3(kBlock), 0, st, s->present, s->chunk_sums, nxt);
+    }
+  }
+  hipLaunchKernelGGL(k_result, dim3(1), dim3(64), 0, st, s->ctl, out_cap, s->res);
+  return hipGetLastError() == hipSuccess;
 }
 
 }  // namespace
@@ -404,8 +448,8 @@ lsmgnn_status lsmgnn_sampler_create(const int64_t *offsets, const uint32_t *adj,
             hipMalloc(&s->chunk_sums, s->nchunks * 4) == hipSuccess &&
             hipMalloc(&s->frontier[0], N * 4) == hipSuccess && hipMalloc(&s->frontier[1], N * 4) == hipSuccess &&
             hipMalloc(&s->tile_sum, s->max_tiles * 8) == hipSuccess &&
-            hipMalloc(&s->ctl, sizeof(Ctl)) == hipSuccess &&
-            hipHostMalloc(&s->ctl_host, sizeof(Ctl), hipHostMallocDefault) == hipSuccess &&
+            hipMalloc(&s->ctl, sizeof(Ctl)) == hipSuccess && hipMalloc(&s->res, 16) == hipSuccess &&
+            hipHostMalloc(&s->res_host, 16, hipHostMallocDefault) == hipSuccess &&
             hipMalloc(&err, 4) == hipSuccess;
   if (!ok) {
     (void)hipGetLastError();
@@ -445,45 +489,32 @@ void lsmgnn_sampler_destroy(lsmgnn_sampler *s) {
 
 lsmgnn_status lsmgnn_sample(lsmgnn_sampler *s, const int64_t *seeds, uint64_t n_seeds, uint64_t batch, int64_t *out,
                             uint64_t out_cap, uint64_t *n_out, void *stream) {
-  using namespace lsm_smp;
   if (!s || !n_out || (n_seeds && !seeds) || (out_cap && !out)) return LSMGNN_E_INVAL;
   DeviceScope ds(s->device);
   if (!ds.ok) return LSMGNN_E_DEVICE;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const unsigned gN = grid_for(s->N, kTile, kMaxGrid);  // frontier tiles: at most N entries
-  const unsigned gc = (unsigned)s->nchunks;
-  const uint64_t key_b = derive(derive(s->seed, kLabelSample), batch);
-  hipLaunchKernelGGL(k_init, dim3(1), dim3(64), 0, st, s->ctl, n_seeds);
-  if (n_seeds)
-    hipLaunchKernelGGL(k_seeds, dim3(grid_for(n_seeds, kBlock, kMaxGrid)), dim3(kBlock), 0, st, seeds, n_seeds, s->N,
-                       out, out_cap, s->present, s->ctl);
-  hipLaunchKernelGGL(k_popc, dim3(gc), dim3(kBlock), 0, st, s->present, s->chunk_sums);
-  hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, st, s->chunk_sums, (uint32_t)s->nchunks, s->ctl);
-  hipLaunchKernelGGL(k_compact, dim3(gc), dim3(kBlock), 0, st, s->present, s->chunk_sums, s->frontier[0]);
-  // with a bad seed the frontier is still built (and the map cleared) from the
-  // valid ones; the hops run, and the call reports E_RANGE
-  for (uint32_t h = 0; h < s->hops; ++h) {
-    uint32_t *cur = s->frontier[h & 1], *nxt = s->frontier[(h + 1) & 1];
-    const int last = h + 1 == s->hops;
-    hipLaunchKernelGGL(k_tiles, dim3(gN), dim3(kBlock), 0, st, cur, s->off, s->fanout[h], s->tile_sum, s->ctl);
-    hipLaunchKernelGGL(k_top, dim3(1), dim3(kBlock), 0, st, s->tile_sum, s->ctl);
-    hipLaunchKernelGGL(k_draw, dim3(gN), dim3(kBlock), 0, st, cur, s->off, s->adj, s->fanout[h], derive(key_b, h),
-                       s->tile_sum, out, out_cap, s->present, last ? 0 : 1, s->ctl);
-    if (!last) {
-      hipLaunchKernelGGL(k_popc, dim3(gc), dim3(kBlock), 0, st, s->present, s->chunk_sums);
-      hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, st, s->chunk_sums, (uint32_t)s->nchunks, s->ctl);
-      hipLaunchKernelGGL(k_compact, dim3(gc), dim3(kBlock), 0, st, s->present, s->chunk_sums, nxt);
-    }
-  }
-  if (hipGetLastError() != hipSuccess ||
-      hipMemcpyAsync(s->ctl_host, s->ctl, sizeof(Ctl), hipMemcpyDeviceToHost, st) != hipSuccess ||
+  if (!queue_sample(s, seeds, n_seeds, batch, out, out_cap, st) ||
+      hipMemcpyAsync(s->res_host, s->res, 16, hipMemcpyDeviceToHost, st) != hipSuccess ||
       hipStreamSynchronize(st) != hipSuccess) {
     (void)hipGetLastError();
     return LSMGNN_E_DEVICE;
   }
-  *n_out = s->ctl_host->len;
-  if (s->ctl_host->err) return LSMGNN_E_RANGE;
-  return s->ctl_host->len > out_cap ? LSMGNN_E_INVAL : LSMGNN_OK;
+  *n_out = s->res_host[0];
+  return static_cast<lsmgnn_status>(s->res_host[1]);
+}
+
+lsmgnn_status lsmgnn_sample_async(lsmgnn_sampler *s, const int64_t *seeds, uint64_t n_seeds, uint64_t batch,
+                                  int64_t *out, uint64_t out_cap, uint64_t *result_host, void *stream) {
+  if (!s || !result_host || (n_seeds && !seeds) || (out_cap && !out)) return LSMGNN_E_INVAL;
+  DeviceScope ds(s->device);
+  if (!ds.ok) return LSMGNN_E_DEVICE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (!queue_sample(s, seeds, n_seeds, batch, out, out_cap, st) ||
+      hipMemcpyAsync(result_host, s->res, 16, hipMemcpyDeviceToHost, st) != hipSuccess) {
+    (void)hipGetLastError();
+    return LSMGNN_E_DEVICE;
+  }
+  return LSMGNN_OK;
 }
 
 }  // extern "C"

@@ -119,6 +119,8 @@ def lib():
         L.lsmgnn_sampler_destroy.argtypes = [vp]
         L.lsmgnn_sample.restype = i32
         L.lsmgnn_sample.argtypes = [vp, vp, u64, u64, vp, u64, ctypes.POINTER(u64), vp]
+        L.lsmgnn_sample_async.restype = i32
+        L.lsmgnn_sample_async.argtypes = [vp, vp, u64, u64, vp, u64, vp, vp]
         L.lsmgnn_strerror.restype = ctypes.c_char_p
         L.lsmgnn_strerror.argtypes = [i32]
         _lib = L
@@ -209,6 +211,15 @@ class GpuSampler:
                                    seeds.numel(), int(batch), ctypes.c_void_p(out.data_ptr()), out.numel(),
                                    ctypes.byref(n), _stream_handle(stream, self.device.index)), "lsmgnn_sample")
         return out[: n.value]
+
+    def sample_async(self, seeds, batch, out, result_ptr, stream=None):
+        """Queue the sampling of minibatch `batch` into `out`; once `stream`
+        has run it, the two uint64 at result_ptr (pinned host memory) hold
+        the list's length and its status code."""
+        _check(lib().lsmgnn_sample_async(self._h, ctypes.c_void_p(seeds.data_ptr()) if seeds.numel() else None,
+                                         seeds.numel(), int(batch), ctypes.c_void_p(out.data_ptr()), out.numel(),
+                                         ctypes.c_void_p(result_ptr), _stream_handle(stream, self.device.index)),
+               "lsmgnn_sample_async")
 
 
 class PinnedBuffer:

@@ -143,3 +143,36 @@ def test_bad_graphs_and_arguments_rejected():
     with pytest.raises(lsmgnn.LsmgnnError) as e:
         lsmgnn.GpuSampler(torch.as_tensor(shifted).cuda(), torch.as_tensor(adj2.view(np.int32)).cuda(), (4,))
     assert e.value.status == "E_RANGE"
+
+
+def test_async_calls_queue_several_minibatches():
+    """lsmgnn_sample_async: several minibatches queued back to back on one
+    stream, each into its own output, give the blocking call's lists; the
+    status word reports a bad seed and a short output."""
+    g = W.rmat_graph(1 << 11, 1 << 14, seed=8)
+    fanout = (12, 6)
+    nb, B = 6, 50
+    seeds = W.seed_permutation(1 << 11, nb * B, seed=8)
+    ref = _host_lists(g, seeds, B, fanout, nb, 8)
+    off, adj = _dev_graph(g)
+    smp = lsmgnn.GpuSampler(off, adj, fanout, seed=8)
+    dseeds = torch.as_tensor(seeds).cuda()
+    res = lsmgnn.PinnedBuffer(16 * (nb + 2))
+    r = res.numpy(np.uint64, (nb + 2, 2))
+    outs = [torch.full((max(x.size for x in ref),), -1, dtype=torch.int64, device="cuda") for _ in range(nb)]
+    for b in range(nb):
+        smp.sample_async(dseeds[b * B:(b + 1) * B], b, outs[b], res.ptr + 16 * b)
+    short = torch.empty(10, dtype=torch.int64, device="cuda")
+    smp.sample_async(dseeds[:B], 0, short, res.ptr + 16 * nb)
+    bad_seeds = torch.as_tensor([1, 1 << 11], dtype=torch.int64).cuda()  # kept alive until the stream has run
+    bad_out = torch.empty(5, dtype=torch.int64, device="cuda")
+    smp.sample_async(bad_seeds, 0, bad_out, res.ptr + 16 * (nb + 1))
+    torch.cuda.current_stream().synchronize()
+    for b in range(nb):
+        assert int(r[b, 1]) == 0 and int(r[b, 0]) == ref[b].size, b
+        assert np.array_equal(outs[b][: ref[b].size].cpu().numpy(), ref[b]), b
+    assert int(r[nb, 0]) == ref[0].size and int(r[nb, 1]) == 1  # LSMGNN_E_INVAL: longer than the output
+    assert np.array_equal(short.cpu().numpy(), ref[0][:10])
+    assert int(r[nb + 1, 1]) == 2  # LSMGNN_E_RANGE: a seed outside [0, N)
+    smp.close()
+    res.close()
