@@ -52,7 +52,7 @@ def _check_stream(g, seeds, batch_size, fanout, nb, seed, label, cap=None):
     return ref
 
 
-@pytest.mark.parametrize("fanout", [(10, 5), (15, 10, 5), (64,), (3, 3, 3, 3), (1, 64, 1)])
+@pytest.mark.parametrize("fanout", [(10, 5), (15, 10, 5), (64,), (3, 3, 3, 3), (1, 64, 1), (0, 5), (4, 0, 3)])
 def test_rmat_lists_match_host_sampler(fanout):
     log(f"case: R-MAT 2^12 nodes, 2^15 edges, fanout {fanout}")
     g = W.rmat_graph(1 << 12, 1 << 15, seed=5)
