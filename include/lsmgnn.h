@@ -314,8 +314,9 @@ lsmgnn_status lsmgnn_pagerank_scores(const int64_t *offsets, const uint32_t *adj
    or pinned host memory through its device address), read only, borrowed:
    they must outlive the sampler.  1 <= hops <= 8, every fanout[h] <= 64
    (copied).  The graph is checked once (offsets from 0, non-decreasing, every
-   degree below 2^32, every entry < num_nodes).  Work memory: 9 bytes per node
-   plus 1 byte per node rounded up to 16 KiB, in HBM.
+   degree below 2^32, every entry < num_nodes).  Work memory in HBM: about 9
+   bytes per node (two frontier arrays, a byte map rounded up to 16 KiB, the
+   per-tile sums).
    Errors: E_INVAL (NULL pointers, num_nodes 0 or above 2^32 - 1, hops or a
    fanout out of range); E_RANGE (a malformed graph); E_NOMEM; E_DEVICE.
 
