@@ -81,6 +81,20 @@ def test_workload_rmat10m_full_size_pipelined_parity():
     assert tot["hits"] > 0 and tot["victim_hits"] > 0 and tot["misses"] > 0
     del sg
     torch.cuda.empty_cache()
+    # the GPU sampler on the full-size graph gives the same request lists
+    off = torch.as_tensor(wl.graph.offsets).cuda()
+    adj = torch.as_tensor(wl.graph.adj.view(np.int32)).cuda()
+    smp = lsmgnn.GpuSampler(off, adj, cfg.fanout, seed=cfg.seed)
+    seeds = torch.as_tensor(wl.seeds).cuda()
+    out = torch.empty(wl.max_batch, dtype=torch.int64, device="cuda")
+    B = cfg.batch_size
+    for b in list(range(8)) + [cfg.batches - 1]:
+        got = smp.sample(seeds[b * B:(b + 1) * B], b, out).cpu().numpy()
+        assert np.array_equal(got, batches[b]), f"GPU sampler, minibatch {b}"
+    log(f"  GPU sampler: minibatches 0-7 and {cfg.batches - 1} identical to the generated lists")
+    smp.close()
+    del off, adj, seeds, out
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.timeout(2400)
