@@ -348,6 +348,27 @@ lsmgnn_status lsmgnn_sample(lsmgnn_sampler *s, const int64_t *seeds, uint64_t n_
 lsmgnn_status lsmgnn_sample_async(lsmgnn_sampler *s, const int64_t *seeds, uint64_t n_seeds, uint64_t batch,
                                   int64_t *out, uint64_t out_cap, uint64_t *result_host, void *stream);
 
+/* Typed graphs (the heterogeneous workloads: one cache per node type): a
+   request list of global node IDs split into one list per type, in request
+   order, each ID replaced by its index within its type.
+   ids (n int64, device); node_type (num_nodes uint8, device, each < num_types);
+   local (num_nodes uint32, device): each node's index within its type;
+   outs: num_types device pointers (host array), each to out_cap int64;
+   work: device memory of at least lsmgnn_split_work_bytes(n, num_types) bytes,
+   the caller's (no allocation inside); result_host: num_types + 1 uint64 in
+   pinned host memory.  Queued on `stream`, returns at once; once the stream
+   has run it, result_host[t] is type t's list length and result_host[num_types]
+   the status (LSMGNN_OK; LSMGNN_E_RANGE for an ID outside [0, num_nodes) or a
+   type >= num_types; LSMGNN_E_INVAL for a list longer than out_cap, of which
+   the first out_cap entries were written).  1 <= num_types <= 16.
+   Returns E_INVAL for bad arguments (work too small included), E_DEVICE if
+   queueing failed, else LSMGNN_OK. */
+uint64_t lsmgnn_split_work_bytes(uint64_t n, uint32_t num_types);
+lsmgnn_status lsmgnn_split_by_type_async(const int64_t *ids, uint64_t n, uint64_t num_nodes, const uint8_t *node_type,
+                                         const uint32_t *local, uint32_t num_types, int64_t *const *outs,
+                                         uint64_t out_cap, void *work, uint64_t work_bytes, uint64_t *result_host,
+                                         void *stream);
+
 /* Set index the cache uses for node x (host-side helper, for tests). */
 uint64_t lsmgnn_set_of(uint64_t x, uint64_t num_sets);
 

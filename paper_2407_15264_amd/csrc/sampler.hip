@@ -323,6 +323,112 @@ __global__ void k_result(const Ctl *ctl, uint64_t cap, uint64_t *res) {
   }
 }
 
+// ------------------------------------------------------------ typed graphs
+// A request list of global IDs split by node type, in request order, each ID
+// replaced by its index within its type.  Tiles of 256 requests: per-tile
+// counts per type, one block's scan of them per type, then each request's
+// rank among its tile's requests of the same type (one ballot per type and
+// wave).  result[t] = length of type t's list; result[T] = status.
+constexpr uint32_t kMaxTypes = 16;
+
+struct TypeOuts {
+  int64_t *p[kMaxTypes];
+};
+
+__global__ __launch_bounds__(kBlock) void k_type_count(const int64_t *ids, uint64_t n, uint64_t N,
+                                                       const uint8_t *node_type, uint32_t T, uint32_t *tile_cnt,
+                                                       uint64_t *result) {
+  __shared__ uint32_t cnt[kMaxTypes];
+  const uint64_t ntiles = (n + kBlock - 1) / kBlock;
+  for (uint64_t b = blockIdx.x; b < ntiles; b += gridDim.x) {
+    if (threadIdx.x < kMaxTypes) cnt[threadIdx.x] = 0;
+    __syncthreads();
+    const uint64_t i = b * kBlock + threadIdx.x;
+    bool bad = false;
+    if (i < n) {
+      const int64_t x = ids[i];
+      if (x < 0 || (uint64_t)x >= N) {
+        bad = true;
+      } else {
+        const uint32_t t = node_type[x];
+        if (t >= T)
+          bad = true;
+        else
+          atomicAdd(&cnt[t], 1u);
+      }
+    }
+    if (__ballot(bad) && __lane_id() == 0) atomicOr((unsigned long long *)&result[T], 1ull);
+    __syncthreads();
+    if (threadIdx.x < T) tile_cnt[b * T + threadIdx.x] = cnt[threadIdx.x];
+    __syncthreads();
+  }
+}
+
+// One block: per type, the exclusive scan of the tile counts (in place) and
+// the type's list length.
+__global__ __launch_bounds__(kBlock) void k_type_scan(uint32_t *tile_cnt, uint64_t ntiles, uint32_t T,
+                                                      uint64_t *result) {
+  for (uint32_t t = 0; t < T; ++t) {
+    uint32_t carry = 0;
+    for (uint64_t base = 0; base < ntiles; base += kBlock) {
+      const uint64_t i = base + threadIdx.x;
+      const uint32_t v = i < ntiles ? tile_cnt[i * T + t] : 0u;
+      uint32_t tot;
+      const uint32_t ex = block_exclusive_scan(v, tot);
+      if (i < ntiles) tile_cnt[i * T + t] = carry + ex;
+      carry += tot;
+    }
+    if (threadIdx.x == 0) result[t] = carry;
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_type_scatter(const int64_t *ids, uint64_t n, uint64_t N,
+                                                         const uint8_t *node_type, const uint32_t *local, uint32_t T,
+                                                         const uint32_t *tile_off, TypeOuts outs, uint64_t cap) {
+  __shared__ uint32_t wcnt[kBlock / 64][kMaxTypes];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;  // lanes below this one
+  const uint64_t ntiles = (n + kBlock - 1) / kBlock;
+  for (uint64_t b = blockIdx.x; b < ntiles; b += gridDim.x) {
+    const uint64_t i = b * kBlock + threadIdx.x;
+    uint32_t t = kMaxTypes, loc = 0;  // kMaxTypes: no request, or an invalid one
+    if (i < n) {
+      const int64_t x = ids[i];
+      if (x >= 0 && (uint64_t)x < N && node_type[x] < T) {
+        t = node_type[x];
+        loc = local[x];
+      }
+    }
+    uint32_t rank = 0;
+    for (uint32_t k = 0; k < T; ++k) {
+      const uint64_t m = __ballot(t == k);
+      if (t == k) rank = (uint32_t)__popcll(m & lt);
+      if (lane == 0) wcnt[wid][k] = (uint32_t)__popcll(m);
+    }
+    __syncthreads();
+    if (t < T) {
+      uint64_t off = tile_off[b * T + t] + rank;
+      for (int w = 0; w < wid; ++w) off += wcnt[w][t];
+      if (off < cap) outs.p[t][off] = (int64_t)loc;
+    }
+    __syncthreads();
+  }
+}
+
+__global__ void k_type_init(uint64_t *result, uint32_t T) {
+  if (threadIdx.x <= T) result[threadIdx.x] = 0;
+}
+
+// status word: an invalid ID or type (set by the count kernel as 1) becomes
+// E_RANGE; otherwise E_INVAL when a list is longer than the outputs, else OK
+__global__ void k_type_status(uint64_t *result, uint32_t T, uint64_t cap) {
+  if (threadIdx.x == 0) {
+    bool over = false;
+    for (uint32_t t = 0; t < T; ++t) over |= result[t] > cap;
+    result[T] = result[T] ? (uint64_t)LSMGNN_E_RANGE : over ? (uint64_t)LSMGNN_E_INVAL : (uint64_t)LSMGNN_OK;
+  }
+}
+
 static unsigned grid_for(uint64_t work, uint64_t per_block, unsigned cap) {
   uint64_t b = (work + per_block - 1) / per_block;
   if (b < 1) b = 1;
@@ -511,6 +617,46 @@ lsmgnn_status lsmgnn_sample_async(lsmgnn_sampler *s, const int64_t *seeds, uint6
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (!queue_sample(s, seeds, n_seeds, batch, out, out_cap, st) ||
       hipMemcpyAsync(result_host, s->res, 16, hipMemcpyDeviceToHost, st) != hipSuccess) {
+    (void)hipGetLastError();
+    return LSMGNN_E_DEVICE;
+  }
+  return LSMGNN_OK;
+}
+
+uint64_t lsmgnn_split_work_bytes(uint64_t n, uint32_t num_types) {
+  return ((n + lsm_smp::kBlock - 1) / lsm_smp::kBlock) * (uint64_t)num_types * 4 + 256;
+}
+
+lsmgnn_status lsmgnn_split_by_type_async(const int64_t *ids, uint64_t n, uint64_t num_nodes, const uint8_t *node_type,
+                                         const uint32_t *local, uint32_t num_types, int64_t *const *outs,
+                                         uint64_t out_cap, void *work, uint64_t work_bytes, uint64_t *result_host,
+                                         void *stream) {
+  using namespace lsm_smp;
+  if (!result_host || !outs || !node_type || !local || num_types == 0 || num_types > kMaxTypes ||
+      (n && !ids) || !work || work_bytes < lsmgnn_split_work_bytes(n, num_types))
+    return LSMGNN_E_INVAL;
+  TypeOuts to{};
+  for (uint32_t t = 0; t < num_types; ++t) {
+    if (out_cap && !outs[t]) return LSMGNN_E_INVAL;
+    to.p[t] = outs[t];
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  // work: the device result (num_types lengths + status, 8 B each), then the tile counts
+  uint64_t *res = static_cast<uint64_t *>(work);
+  uint32_t *tile_cnt = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(work) + 256);
+  const uint64_t ntiles = (n + kBlock - 1) / kBlock;
+  const unsigned g = grid_for(ntiles, 1, kMaxGrid);
+  hipLaunchKernelGGL(k_type_init, dim3(1), dim3(64), 0, st, res, num_types);
+  if (n) {
+    hipLaunchKernelGGL(k_type_count, dim3(g), dim3(kBlock), 0, st, ids, n, num_nodes, node_type, num_types, tile_cnt,
+                       res);
+    hipLaunchKernelGGL(k_type_scan, dim3(1), dim3(kBlock), 0, st, tile_cnt, ntiles, num_types, res);
+    hipLaunchKernelGGL(k_type_scatter, dim3(g), dim3(kBlock), 0, st, ids, n, num_nodes, node_type, local, num_types,
+                       tile_cnt, to, out_cap);
+  }
+  hipLaunchKernelGGL(k_type_status, dim3(1), dim3(64), 0, st, res, num_types, out_cap);
+  if (hipGetLastError() != hipSuccess ||
+      hipMemcpyAsync(result_host, res, (num_types + 1) * 8, hipMemcpyDeviceToHost, st) != hipSuccess) {
     (void)hipGetLastError();
     return LSMGNN_E_DEVICE;
   }

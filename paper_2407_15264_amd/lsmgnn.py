@@ -121,6 +121,11 @@ def lib():
         L.lsmgnn_sample.argtypes = [vp, vp, u64, u64, vp, u64, ctypes.POINTER(u64), vp]
         L.lsmgnn_sample_async.restype = i32
         L.lsmgnn_sample_async.argtypes = [vp, vp, u64, u64, vp, u64, vp, vp]
+        L.lsmgnn_split_work_bytes.restype = u64
+        L.lsmgnn_split_work_bytes.argtypes = [u64, ctypes.c_uint32]
+        L.lsmgnn_split_by_type_async.restype = i32
+        L.lsmgnn_split_by_type_async.argtypes = [vp, u64, u64, vp, vp, ctypes.c_uint32, ctypes.POINTER(vp), u64,
+                                                 vp, u64, vp, vp]
         L.lsmgnn_strerror.restype = ctypes.c_char_p
         L.lsmgnn_strerror.argtypes = [i32]
         _lib = L
@@ -220,6 +225,28 @@ class GpuSampler:
                                          seeds.numel(), int(batch), ctypes.c_void_p(out.data_ptr()), out.numel(),
                                          ctypes.c_void_p(result_ptr), _stream_handle(stream, self.device.index)),
                "lsmgnn_sample_async")
+
+
+def split_work_bytes(n, num_types):
+    """Device work memory split_by_type_async needs for n requests."""
+    return int(lib().lsmgnn_split_work_bytes(int(n), int(num_types)))
+
+
+def split_by_type_async(ids, node_type, local, outs, work, result_ptr, stream=None, device=0):
+    """Queue the split of a global request list (int64 device tensor) into one
+    list of within-type indices per node type (lsmgnn_split_by_type_async):
+    node_type (uint8 device tensor), local (int32/uint32 device tensor), outs
+    (int64 device tensors of equal length, one per type), work (a device
+    tensor of at least split_work_bytes bytes); result_ptr: pinned host
+    memory for the len(outs) lengths and the status."""
+    T = len(outs)
+    ptrs = (ctypes.c_void_p * T)(*[o.data_ptr() for o in outs])
+    _check(lib().lsmgnn_split_by_type_async(ctypes.c_void_p(ids.data_ptr()) if ids.numel() else None, ids.numel(),
+                                            node_type.numel(), ctypes.c_void_p(node_type.data_ptr()),
+                                            ctypes.c_void_p(local.data_ptr()), T, ptrs, outs[0].numel(),
+                                            ctypes.c_void_p(work.data_ptr()), work.numel() * work.element_size(),
+                                            ctypes.c_void_p(result_ptr), _stream_handle(stream, device)),
+           "lsmgnn_split_by_type_async")
 
 
 class PinnedBuffer:

@@ -126,6 +126,31 @@ def test_workload_typed_20m_full_size_pipelined_parity():
     log(f"  {res['seconds']:.1f} s")
     del sg
     torch.cuda.empty_cache()
+    # the GPU sampler and the split by type give the per-type lists
+    off = torch.as_tensor(wl.graph.offsets).cuda()
+    adj = torch.as_tensor(wl.graph.adj.view(np.int32)).cuda()
+    smp = lsmgnn.GpuSampler(off, adj, cfg.fanout, seed=cfg.seed)
+    seeds = torch.as_tensor(wl.seeds).cuda()
+    node_type = torch.as_tensor(wl.node_type).cuda()
+    local = torch.as_tensor(wl.node_local.astype(np.int32)).cuda()
+    mb = int(np.diff(wl.offsets).max())
+    glob = torch.empty(mb, dtype=torch.int64, device="cuda")
+    outs = [torch.empty(mb, dtype=torch.int64, device="cuda") for _ in range(cfg.num_types)]
+    work = torch.empty(lsmgnn.split_work_bytes(mb, cfg.num_types), dtype=torch.uint8, device="cuda")
+    res_h = lsmgnn.PinnedBuffer(8 * (cfg.num_types + 1))
+    r = res_h.numpy(np.uint64, (cfg.num_types + 1,))
+    B = cfg.batch_size
+    for b in list(range(4)) + [cfg.batches - 1]:
+        lst = smp.sample(seeds[b * B:(b + 1) * B], b, glob)
+        lsmgnn.split_by_type_async(lst, node_type, local, outs, work, res_h.ptr)
+        torch.cuda.current_stream().synchronize()
+        assert int(r[cfg.num_types]) == 0, b
+        for t in range(cfg.num_types):
+            got = outs[t][: int(r[t])].cpu().numpy()
+            assert np.array_equal(got, type_batches[t][b]), f"minibatch {b}, type {t}"
+    log(f"  GPU sampler + split by type: minibatches 0-3 and {cfg.batches - 1} identical per type")
+    smp.close()
+    res_h.close()
 
 
 def _random_case(seed):

@@ -176,3 +176,59 @@ def test_async_calls_queue_several_minibatches():
     assert int(r[nb + 1, 1]) == 2  # LSMGNN_E_RANGE: a seed outside [0, N)
     smp.close()
     res.close()
+
+
+def test_split_by_type_matches_a_stable_partition():
+    """lsmgnn_split_by_type_async against numpy: per type, the requests of
+    that type in request order, as within-type indices; status words for a
+    bad ID, a bad type and a short output; an empty list."""
+    rng = np.random.default_rng(21)
+    N, T = 5000, 5
+    node_type = rng.integers(0, T, N).astype(np.uint8)
+    local = np.empty(N, np.uint32)
+    for t in range(T):
+        idx = np.flatnonzero(node_type == t)
+        local[idx] = rng.permutation(idx.size)  # any index within the type
+    d_type = torch.as_tensor(node_type).cuda()
+    d_local = torch.as_tensor(local.view(np.int32)).cuda()
+    cap = 30000
+    outs = [torch.full((cap,), -1, dtype=torch.int64, device="cuda") for _ in range(T)]
+    work = torch.empty(lsmgnn.split_work_bytes(cap, T), dtype=torch.uint8, device="cuda")
+    res = lsmgnn.PinnedBuffer(8 * (T + 1))
+    r = res.numpy(np.uint64, (T + 1,))
+    for n in (0, 1, 255, 256, 257, 12345, 30000):
+        ids = rng.integers(0, N, n)
+        ids[::3] = ids[0] if n else 0
+        d_ids = torch.as_tensor(ids.astype(np.int64)).cuda()
+        lsmgnn.split_by_type_async(d_ids, d_type, d_local, outs, work, res.ptr)
+        torch.cuda.current_stream().synchronize()
+        assert int(r[T]) == 0, n
+        for t in range(T):
+            want = local[ids[node_type[ids] == t]].astype(np.int64)
+            assert int(r[t]) == want.size and np.array_equal(outs[t][: want.size].cpu().numpy(), want), (n, t)
+    # a short output: E_INVAL, the full lengths, the prefixes written
+    ids = rng.integers(0, N, 4000)
+    short = [torch.full((50,), -1, dtype=torch.int64, device="cuda") for _ in range(T)]
+    d_ids = torch.as_tensor(ids.astype(np.int64)).cuda()
+    lsmgnn.split_by_type_async(d_ids, d_type, d_local, short, work, res.ptr)
+    torch.cuda.current_stream().synchronize()
+    assert int(r[T]) == 1
+    for t in range(T):
+        want = local[ids[node_type[ids] == t]].astype(np.int64)
+        assert int(r[t]) == want.size and np.array_equal(short[t].cpu().numpy(), want[:50]), t
+    # an ID outside [0, N), or a node whose type is >= T: E_RANGE
+    bad_ids = torch.as_tensor([1, 2, N], dtype=torch.int64).cuda()
+    lsmgnn.split_by_type_async(bad_ids, d_type, d_local, outs, work, res.ptr)
+    torch.cuda.current_stream().synchronize()
+    assert int(r[T]) == 2
+    bad_type = d_type.clone()
+    bad_type[7] = T
+    seven = torch.as_tensor([3, 7], dtype=torch.int64).cuda()
+    lsmgnn.split_by_type_async(seven, bad_type, d_local, outs, work, res.ptr)
+    torch.cuda.current_stream().synchronize()
+    assert int(r[T]) == 2
+    # work memory too small: rejected before anything is queued
+    with pytest.raises(lsmgnn.LsmgnnError) as e:
+        lsmgnn.split_by_type_async(d_ids, d_type, d_local, outs, work[:64], res.ptr)
+    assert e.value.status == "E_INVAL"
+    res.close()
