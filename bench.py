@@ -156,11 +156,15 @@ def measure_ceilings(torch, lsmgnn, store_ptr, nbytes, duplex):
 def make_parts(W, cfg, nb):
     """One part per cache: a homogeneous workload has one, a typed workload one
     per node type (each with its own feature width, store, cache and ring)."""
+    import numpy as np
     if isinstance(cfg, W.HeteroConfig):
         wl = W.HeteroWorkload(cfg, nb)
         parts = [dict(label=f"type {t}", num_nodes=n, dim=d, elt=cfg.elt_bytes, seed=cfg.seed + 1 + t,
                       static=wl.static[t], shape=cfg.cache_shape(t), batches=wl.type_batches(t))
                  for t, (n, d) in enumerate(zip(cfg.type_counts(), cfg.dims))]
+        # what a GPU sampler needs: the global graph and seeds, each node's type and index within it
+        parts[0].update(graph=wl.graph, seeds=wl.seeds, node_type=wl.node_type, node_local=wl.node_local,
+                        global_max=int(np.diff(wl.offsets).max()))
         requests = float(sum(b.size for p in parts for b in p["batches"])) / nb
     else:
         wl = W.Workload(cfg, nb)
@@ -220,27 +224,31 @@ def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None, victim_mode
             "cpu": _cpu_model(), "host_cpus": os.cpu_count()}
 
 
-def gpu_sampler_check(torch, lsmgnn, W, part, cfg, L, nb, warmup, steps, dev):
-    """The GPU sampler against the host-generated lists (every minibatch of the
-    run, element by element), and its rate alone: the timed minibatches sampled
-    back to back, against the host sampler on the same minibatches."""
+def gpu_sampler_check(torch, lsmgnn, W, parts, cfg, L, nb, warmup, steps, dev):
+    """The GPU lists against the host-generated ones (every minibatch of the
+    run and every part, element by element), and their rate alone: the timed
+    minibatches sampled (and split) back to back, against the host sampler on
+    the same minibatches."""
     import numpy as np
-    g = part["graph"]
-    lists = SampledLists(torch, lsmgnn, g, part["seeds"], cfg, L, max(1, max(b.size for b in part["batches"])), dev)
-    mismatched = sum(int(not np.array_equal(lists[b].cpu().numpy(), part["batches"][b])) for b in range(nb))
+    first, typed = parts[0], len(parts) > 1
+    max_len = max(1, max(b.size for p in parts for b in p["batches"]))
+    lists = GpuLists(torch, lsmgnn, first, cfg, L, max_len, dev, typed=typed)
+    mismatched = sum(int(not np.array_equal(lists.get(b, t).cpu().numpy(), p["batches"][b]))
+                     for b in range(nb) for t, p in enumerate(parts))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for b in range(warmup, warmup + steps):
-        lists[b]
+        lists.get(b, 0)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    requests = sum(int(part["batches"][b].size) for b in range(warmup, warmup + steps))
+    requests = sum(int(p["batches"][b].size) for p in parts for b in range(warmup, warmup + steps))
     t0 = time.perf_counter()
-    W.sample_batches(g, part["seeds"], cfg.batch_size, cfg.fanout, warmup, warmup + steps, cfg.seed)
+    W.sample_batches(first["graph"], first["seeds"], cfg.batch_size, cfg.fanout, warmup, warmup + steps, cfg.seed)
     dh = time.perf_counter() - t0
-    lists.sampler.close()
-    return {"identical_to_host_lists": mismatched == 0, "minibatches_compared": nb,
+    lists.close()
+    return {"identical_to_host_lists": mismatched == 0, "minibatches_compared": nb, "parts": len(parts),
             "alone_ms_per_minibatch": 1e3 * dt / steps, "alone_requests_per_s": requests / dt,
+            "split_by_type": typed,
             "host_sampler_ms_per_minibatch": 1e3 * dh / steps,
             "host_sampler_threads": int(os.environ.get("OMP_NUM_THREADS", os.cpu_count()))}
 
@@ -287,52 +295,101 @@ def side_stream(torch):
     return torch.cuda.ExternalStream(s.value)
 
 
-class SampledLists:
-    """Request lists of a homogeneous workload sampled on the GPU on demand
-    (lsmgnn_sample_async), indexable like the list of resident host-generated
-    ones.  The sampler runs on `stream` (a training loop's data-loading
-    stream); prefetch(b) queues minibatch b's list without waiting, and
-    indexing waits only for that list.  Ring of L+3+ahead buffers: the list
-    prefetched at step b (minibatch b+L+1+ahead) takes the buffer of minibatch
-    b-2, whose gather's metadata has finished by then (the host has seen
-    gather b-1's unique count, and the metadata stream is in order)."""
+class GpuLists:
+    """Request lists sampled on the GPU on demand (lsmgnn_sample_async, then
+    for a typed workload lsmgnn_split_by_type_async), for parts that index
+    them like the resident host-generated lists (part_view).  The sampler runs
+    on `stream` (a training loop's data-loading stream); prefetch(b) queues
+    minibatch b's lists, and indexing waits only for them.  A ring of
+    L+3+ahead buffers: the lists prefetched at step b (minibatch b+L+1+ahead)
+    take the buffers of minibatch b-2, whose gathers' metadata has finished by
+    then (the host has seen gather b-1's unique counts, and the metadata
+    stream is in order)."""
 
-    def __init__(self, torch, lsmgnn, graph, seeds, cfg, L, max_len, dev, stream=None, ahead=0):
+    def __init__(self, torch, lsmgnn, first, cfg, L, max_len, dev, stream=None, ahead=0, typed=False):
         import numpy as np
-        self.torch = torch
-        self.off = torch.as_tensor(graph.offsets).to(dev)
-        self.adj = torch.as_tensor(graph.adj.view("int32")).to(dev)
+        self.torch, self.lsmgnn, self.np = torch, lsmgnn, np
+        g = first["graph"]
+        self.off = torch.as_tensor(g.offsets).to(dev)
+        self.adj = torch.as_tensor(g.adj.view("int32")).to(dev)
         self.sampler = lsmgnn.GpuSampler(self.off, self.adj, cfg.fanout, seed=cfg.seed)
-        self.seeds = torch.as_tensor(seeds).to(dev)
+        self.seeds = torch.as_tensor(first["seeds"]).to(dev)
         self.B = cfg.batch_size
+        self.stream = stream
         K = L + 3 + ahead
-        self.ring = [torch.empty(max_len, dtype=torch.int64, device=dev) for _ in range(K)]
-        self.res = lsmgnn.PinnedBuffer(16 * K)  # (length, status) per buffer
+        self.T = cfg.num_types if typed else 0
+        gmax = first.get("global_max", max_len)
+        self.glob = [torch.empty(gmax, dtype=torch.int64, device=dev) for _ in range(K)]
+        self.res = lsmgnn.PinnedBuffer(16 * K)  # sampler: (length, status) per buffer
         self.res_np = self.res.numpy(np.uint64, (K, 2))
+        if self.T:
+            self.node_type = torch.as_tensor(first["node_type"]).to(dev)
+            self.local = torch.as_tensor(first["node_local"].astype(np.int32)).to(dev)
+            self.outs = [[torch.empty(max_len, dtype=torch.int64, device=dev) for _ in range(self.T)]
+                         for _ in range(K)]
+            self.work = torch.empty(lsmgnn.split_work_bytes(gmax, self.T), dtype=torch.uint8, device=dev)
+            self.tres = lsmgnn.PinnedBuffer(8 * (self.T + 1) * K)  # split: lengths + status per buffer
+            self.tres_np = self.tres.numpy(np.uint64, (K, self.T + 1))
         self.events = [torch.cuda.Event() for _ in range(K)]
         self.issued = [None] * K  # minibatch queued into each buffer
-        self.ready = [None] * K   # its list, once waited for
-        self.stream = stream
+        self.ready = [None] * K   # its lists, once waited for
+
+    def _record(self, k):
+        self.events[k].record(self.stream if self.stream is not None else self.torch.cuda.current_stream())
 
     def prefetch(self, b):
-        k = b % len(self.ring)
+        k = b % len(self.glob)
         if self.issued[k] == b:
             return
-        self.sampler.sample_async(self.seeds[b * self.B:(b + 1) * self.B], b, self.ring[k], self.res.ptr + 16 * k,
+        self.sampler.sample_async(self.seeds[b * self.B:(b + 1) * self.B], b, self.glob[k], self.res.ptr + 16 * k,
                                   stream=self.stream)
-        self.events[k].record(self.stream if self.stream is not None else self.torch.cuda.current_stream())
-        self.issued[k], self.ready[k] = b, None
-
-    def __getitem__(self, b):
-        k = b % len(self.ring)
-        self.prefetch(b)
-        if self.ready[k] is None:
+        self._record(k)
+        if self.T:
+            # the split needs the list's length on the host: wait for this sampling only
             self.events[k].synchronize()
             n, status = int(self.res_np[k, 0]), int(self.res_np[k, 1])
             if status != 0:
                 raise RuntimeError(f"lsmgnn_sample_async of minibatch {b}: status {status}")
-            self.ready[k] = self.ring[k][:n]
-        return self.ready[k]
+            self.lsmgnn.split_by_type_async(self.glob[k][:n], self.node_type, self.local, self.outs[k], self.work,
+                                            self.tres.ptr + 8 * (self.T + 1) * k, stream=self.stream)
+            self._record(k)
+        self.issued[k], self.ready[k] = b, None
+
+    def get(self, b, t):
+        k = b % len(self.glob)
+        self.prefetch(b)
+        if self.ready[k] is None:
+            self.events[k].synchronize()
+            if self.T:
+                status = int(self.tres_np[k, self.T])
+                if status != 0:
+                    raise RuntimeError(f"lsmgnn_split_by_type_async of minibatch {b}: status {status}")
+                self.ready[k] = [self.outs[k][u][: int(self.tres_np[k, u])] for u in range(self.T)]
+            else:
+                n, status = int(self.res_np[k, 0]), int(self.res_np[k, 1])
+                if status != 0:
+                    raise RuntimeError(f"lsmgnn_sample_async of minibatch {b}: status {status}")
+                self.ready[k] = [self.glob[k][:n]]
+        return self.ready[k][t]
+
+    def part_view(self, t):
+        return _PartLists(self, t)
+
+    def close(self):
+        self.sampler.close()
+
+
+class _PartLists:
+    """One part's lists of a GpuLists producer (the type's, or the only one)."""
+
+    def __init__(self, prod, t):
+        self.prod, self.t = prod, t
+
+    def prefetch(self, b):
+        self.prod.prefetch(b)
+
+    def __getitem__(self, b):
+        return self.prod.get(b, self.t)
 
 
 def main():
@@ -403,9 +460,6 @@ def main():
     # the minibatches the timed stream gathers or announces (a prefix of the
     # configured run); near the run's end the last gathers announce nothing
     nb = min(cfg.batches, args.warmup + args.steps + L + 1)
-    if args.gpu_sampler and isinstance(cfg, W.HeteroConfig):
-        print("bench.py: --gpu-sampler is for the homogeneous workloads", file=sys.stderr)
-        sys.exit(2)
     if args.static == "pagerank" and isinstance(cfg, W.HeteroConfig):
         print("bench.py: --static pagerank is for the homogeneous workloads", file=sys.stderr)
         sys.exit(2)
@@ -460,13 +514,13 @@ def main():
         log(f"[bench] reverse-PageRank static scores in {static_info['ms']:.1f} ms")
     sampler_info = None
     if args.gpu_sampler:
-        sampler_info = gpu_sampler_check(torch, lsmgnn, W, parts[0], cfg, L, nb, args.warmup, args.steps, dev)
+        sampler_info = gpu_sampler_check(torch, lsmgnn, W, parts, cfg, L, nb, args.warmup, args.steps, dev)
         log(f"[bench] GPU sampler: {sampler_info}")
-    for p in parts:
+        producer = GpuLists(torch, lsmgnn, parts[0], cfg, L, max(1, max(b.size for p in parts for b in p["batches"])),
+                            dev, side_stream(torch), ahead=SAMPLE_AHEAD, typed=len(parts) > 1)
+    for t, p in enumerate(parts):
         if args.gpu_sampler:
-            p["dev_batches"] = SampledLists(torch, lsmgnn, p["graph"], p["seeds"], cfg, L,
-                                            max(1, max(b.size for b in p["batches"])), dev, side_stream(torch),
-                                            ahead=SAMPLE_AHEAD)
+            p["dev_batches"] = producer.part_view(t)
         else:
             p["dev_batches"] = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in p["batches"]]
         p.pop("graph", None)
