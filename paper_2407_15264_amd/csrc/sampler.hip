@@ -24,13 +24,18 @@
 // Per hop, on the caller's stream:
 //   tiles    per tile of 256 frontier entries, the sum of the k's
 //   top      one block: exclusive scan of the tile sums, the list length
-//   draw     per entry: Floyd's draws, a sort of at most 64 positions in
-//            registers, the samples written at their list positions, and the
-//            next frontier's byte-map marks (plain byte stores)
+//   draw     per entry: Floyd's draws, an insertion sort of at most 64
+//            positions in private memory, the samples written at their list
+//            positions, and the next frontier's byte-map marks (plain byte
+//            stores)
 //   popc / chunk scan / compact: the marked nodes in ascending order become
 //            the next frontier, and the map is cleared
 // Every count stays on the device; the host learns the list length once, at
 // the end.  The byte map holds one byte per node and is all zero between calls.
+//
+// Typed graphs: the list split by node type (per tile of 256 requests a count
+// per type, one block's scan per type, then a ballot rank per type and wave),
+// each ID replaced by its index within its type.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
