@@ -333,6 +333,7 @@ typedef struct lsmgnn_sampler lsmgnn_sampler; /* opaque, owned by the library */
 lsmgnn_status lsmgnn_sampler_create(const int64_t *offsets, const uint32_t *adj, uint64_t num_nodes,
                                     const uint32_t *fanout, uint32_t hops, uint64_t seed, int device,
                                     lsmgnn_sampler **out);
+/* Waits for all work queued on the sampler's device, then frees it. */
 void lsmgnn_sampler_destroy(lsmgnn_sampler *s);
 lsmgnn_status lsmgnn_sample(lsmgnn_sampler *s, const int64_t *seeds, uint64_t n_seeds, uint64_t batch, int64_t *out,
                             uint64_t out_cap, uint64_t *n_out, void *stream);
