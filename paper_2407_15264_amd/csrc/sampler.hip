@@ -22,12 +22,13 @@
 // reduced to [0, m) as ((r >> 32) * m) >> 32.
 //
 // Per hop, on the caller's stream:
-//   tiles    per tile of 256 frontier entries, the sum of the k's
+//   tiles    per tile of 256 frontier entries: each entry's k, its offset
+//            within the tile, and the tile's sum
 //   top      one block: exclusive scan of the tile sums, the list length
-//   draw     per entry: Floyd's draws, an insertion sort of at most 64
-//            positions in private memory, the samples written at their list
-//            positions, and the next frontier's byte-map marks (plain byte
-//            stores)
+//   draw     one wave per frontier node: lane j makes Floyd's j-th draw, the
+//            k steps are resolved in order with one ballot each, and each
+//            lane's rank among the k positions places its sample in the
+//            list; the next frontier's byte-map marks are plain byte stores
 //   popc / chunk scan / compact: the marked nodes in ascending order become
 //            the next frontier, and the map is cleared
 // Every count stays on the device; the host learns the list length once, at
@@ -48,10 +49,9 @@ namespace lsm_smp {
 constexpr int kBlock = 256;
 constexpr int kMapBytesPerThread = 64;                        // byte-map bytes per thread
 constexpr uint64_t kChunk = (uint64_t)kBlock * kMapBytesPerThread;  // byte-map bytes per block
-constexpr int kPerThread = 1;  // frontier entries per thread in a tile (1: 4x faster than 8, more blocks in flight)
-constexpr uint32_t kTile = kBlock * kPerThread;
+constexpr uint32_t kTile = kBlock;  // frontier entries per tile (one per thread)
 constexpr unsigned kMaxGrid = 4096;
-constexpr uint32_t kMaxFanout = 64;
+constexpr uint32_t kMaxFanout = 64;  // one wave's lanes
 constexpr uint32_t kMaxHops = 8;
 constexpr uint64_t kGamma = 0x9e3779b97f4a7c15ull;
 constexpr uint64_t kLabelSample = 3;
@@ -223,17 +223,15 @@ __device__ __forceinline__ uint32_t draws_of(const int64_t *off, uint32_t v, uin
 
 // Per tile of the frontier, the number of samples it draws.
 __global__ __launch_bounds__(kBlock) void k_tiles(const uint32_t *frontier, const int64_t *off, uint32_t fanout,
-                                                  uint64_t *tile_sum, const Ctl *ctl) {
+                                                  uint64_t *tile_sum, uint32_t *node_off, const Ctl *ctl) {
   const uint32_t f = ctl->frontier;
   const uint32_t ntiles = (f + kTile - 1) / kTile;
   for (uint32_t b = blockIdx.x; b < ntiles; b += gridDim.x) {
-    const uint32_t i0 = b * kTile + threadIdx.x * kPerThread;
-    uint32_t c = 0;
-#pragma unroll
-    for (int k = 0; k < kPerThread; ++k)
-      if (i0 + k < f) c += draws_of(off, frontier[i0 + k], fanout);
+    const uint32_t i = b * kTile + threadIdx.x;
+    const uint32_t c = i < f ? draws_of(off, frontier[i], fanout) : 0u;
     uint32_t tot;
-    (void)block_exclusive_scan(c, tot);
+    const uint32_t ex = block_exclusive_scan(c, tot);
+    if (i < f) node_off[i] = ex;
     if (threadIdx.x == 0) tile_sum[b] = tot;
   }
 }
@@ -258,73 +256,53 @@ __global__ __launch_bounds__(kBlock) void k_top(uint64_t *tile_sum, Ctl *ctl) {
   }
 }
 
-// Floyd's algorithm for node v: k distinct positions in [0, deg), ascending.
-__device__ __forceinline__ void draw_positions(uint64_t key_v, uint64_t deg, uint32_t k, uint32_t *pos) {
-  if (k == deg) {
-    for (uint32_t j = 0; j < k; ++j) pos[j] = j;
-    return;
-  }
-  uint32_t m = 0;
-  uint64_t draw = 0;
-  for (uint64_t j = deg - k; j < deg; ++j) {
-    const uint64_t r = ((stream_at(key_v, draw++) >> 32) * (j + 1)) >> 32;
-    bool seen = false;
-    for (uint32_t q = 0; q < m; ++q) seen |= pos[q] == (uint32_t)r;
-    pos[m++] = seen ? (uint32_t)j : (uint32_t)r;
-  }
-  for (uint32_t x = 1; x < m; ++x) {  // insertion sort, ascending
-    const uint32_t y = pos[x];
-    int z = (int)x - 1;
-    while (z >= 0 && pos[z] > y) {
-      pos[z + 1] = pos[z];
-      --z;
-    }
-    pos[z + 1] = y;
-  }
-}
-
-// Each thread takes kPerThread consecutive frontier entries of a tile; their
-// samples go to consecutive list positions.  `mark`: set the next frontier's
-// byte-map bytes (not needed after the last hop).
-__global__ __launch_bounds__(kBlock) void k_draw(const uint32_t *frontier, const int64_t *off, const uint32_t *adj,
-                                                 uint32_t fanout, uint64_t key_hop, const uint64_t *tile_off,
-                                                 int64_t *out, uint64_t cap, uint8_t *present, int mark,
-                                                 const Ctl *ctl) {
-  const uint32_t f = ctl->frontier;
-  const uint64_t hop_base = ctl->hop_base;
-  const uint32_t ntiles = (f + kTile - 1) / kTile;
-  uint32_t pos[kMaxFanout];
-  for (uint32_t b = blockIdx.x; b < ntiles; b += gridDim.x) {
-    const uint32_t i0 = b * kTile + threadIdx.x * kPerThread;
-    uint32_t c = 0;
-#pragma unroll
-    for (int k = 0; k < kPerThread; ++k)
-      if (i0 + k < f) c += draws_of(off, frontier[i0 + k], fanout);
-    uint32_t tot;
-    uint64_t p = hop_base + tile_off[b] + block_exclusive_scan(c, tot);
-    for (int q = 0; q < kPerThread; ++q) {
-      if (i0 + q >= f) break;
-      const uint32_t v = frontier[i0 + q];
-      const int64_t o = off[v];
-      const uint64_t deg = (uint64_t)(off[v + 1] - o);
-      const uint32_t k = (uint32_t)(fanout < deg ? fanout : deg);
-      if (k == 0) continue;
-      draw_positions(derive(key_hop, v), deg, k, pos);
-      for (uint32_t j = 0; j < k; ++j, ++p) {
-        const uint32_t u = adj[o + pos[j]];
-        if (p < cap) out[p] = (int64_t)u;
-        if (mark) present[u] = 1;
-      }
-    }
-  }
-}
-
 // (list length, status) of the call: LSMGNN_OK, E_RANGE for a bad seed, or
 // E_INVAL for a list longer than the output
 __global__ void k_result(const Ctl *ctl, uint64_t cap, uint64_t *res) {
   if (threadIdx.x == 0) {
     res[0] = ctl->len;
     res[1] = ctl->err ? (uint64_t)LSMGNN_E_RANGE : ctl->len > cap ? (uint64_t)LSMGNN_E_INVAL : (uint64_t)LSMGNN_OK;
+  }
+}
+
+// One wave per frontier node: lane j makes Floyd's j-th draw; the k steps are
+// then resolved in order with one ballot each (a draw already taken yields
+// the step's own bound instead), and each lane's rank among the k positions
+// gives its place in the ascending list.
+__global__ __launch_bounds__(kBlock) void k_draw_wave(const uint32_t *frontier, const int64_t *off,
+                                                      const uint32_t *adj, uint32_t fanout, uint64_t key_hop,
+                                                      const uint64_t *tile_off, const uint32_t *node_off,
+                                                      int64_t *out, uint64_t cap, uint8_t *present, int mark,
+                                                      const Ctl *ctl) {
+  const uint32_t f = ctl->frontier;
+  const uint64_t hop_base = ctl->hop_base;
+  const int lane = threadIdx.x & 63;
+  const uint32_t waves = gridDim.x * (kBlock / 64);
+  for (uint32_t i = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6); i < f; i += waves) {
+    const uint32_t v = frontier[i];
+    const int64_t o = off[v];
+    const uint64_t deg = (uint64_t)(off[v + 1] - o);
+    const uint32_t k = (uint32_t)(fanout < deg ? fanout : deg);
+    if (k == 0) continue;
+    uint32_t pos = (uint32_t)lane, rank = (uint32_t)lane;  // k == deg: every position, in order
+    if (k < deg) {
+      const uint64_t jj = deg - k + (uint64_t)lane;  // this lane's step bound
+      uint32_t r = 0;
+      if (lane < (int)k) r = (uint32_t)(((stream_at(derive(key_hop, v), (uint64_t)lane) >> 32) * (jj + 1)) >> 32);
+      for (uint32_t q = 0; q < k; ++q) {
+        const uint32_t rq = __shfl(r, (int)q);
+        const bool taken = __ballot(lane < (int)q && pos == rq) != 0ull;
+        if (lane == (int)q) pos = taken ? (uint32_t)jj : r;
+      }
+      rank = 0;  // the positions are distinct
+      for (uint32_t q = 0; q < k; ++q) rank += __shfl(pos, (int)q) < pos ? 1u : 0u;
+    }
+    if (lane < (int)k) {
+      const uint64_t p = hop_base + tile_off[i / kTile] + node_off[i] + rank;
+      const uint32_t u = adj[o + pos];
+      if (p < cap) out[p] = (int64_t)u;
+      if (mark) present[u] = 1;
+    }
   }
 }
 
@@ -503,10 +481,10 @@ bool queue_sample(lsmgnn_sampler *s, const int64_t *seeds, uint64_t n_seeds, uin
   for (uint32_t h = 0; h < s->hops; ++h) {
     uint32_t *cur = s->frontier[h & 1], *nxt = s->frontier[(h + 1) & 1];
     const int last = h + 1 == s->hops;
-    hipLaunchKernelGGL(k_tiles, dim3(gN), dim3(kBlock), 0, st, cur, s->off, s->fanout[h], s->tile_sum, s->ctl);
+    hipLaunchKernelGGL(k_tiles, dim3(gN), dim3(kBlock), 0, st, cur, s->off, s->fanout[h], s->tile_sum, nxt, s->ctl);
     hipLaunchKernelGGL(k_top, dim3(1), dim3(kBlock), 0, st, s->tile_sum, s->ctl);
-    hipLaunchKernelGGL(k_draw, dim3(gN), dim3(kBlock), 0, st, cur, s->off, s->adj, s->fanout[h], derive(key_b, h),
-                       s->tile_sum, out, out_cap, s->present, last ? 0 : 1, s->ctl);
+    hipLaunchKernelGGL(k_draw_wave, dim3(gN), dim3(kBlock), 0, st, cur, s->off, s->adj, s->fanout[h],
+                       derive(key_b, h), s->tile_sum, nxt, out, out_cap, s->present, last ? 0 : 1, s->ctl);
     if (!last) {
       hipLaunchKernelGGL(k_popc, dim3(gc), dim3(kBlock), 0, st, s->present, s->chunk_sums);
       hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, st, s->chunk_sums, (uint32_t)s->nchunks, s->ctl);
