@@ -86,7 +86,7 @@ def duplex_probe(nbytes=1 << 30):
     d_out = torch.zeros(half, dtype=torch.uint8, device=dev)
     sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
     best = None
-    for _ in range(5):
+    for it in range(9):  # the first three warm the link and the copy path up, untimed
         torch.cuda.synchronize()
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
         with torch.cuda.stream(sa):
@@ -102,8 +102,9 @@ def duplex_probe(nbytes=1 << 30):
         span = max(ev[0].elapsed_time(ev[1]), ev[0].elapsed_time(ev[3])) / 1e3
         r = {"h2d_GBps": nbytes / ta / 1e9, "d2h_GBps": half / tb / 1e9,
              "total_GBps": (nbytes + half) / span / 1e9, "bytes_in": nbytes, "bytes_out": half,
-             "how": "runtime copies from and to pinned memory on two streams, started together"}
-        if best is None or r["total_GBps"] > best["total_GBps"]:
+             "how": "runtime copies from and to pinned memory on two streams, started together; best of 6 "
+                    "after 3 untimed"}
+        if it >= 3 and (best is None or r["total_GBps"] > best["total_GBps"]):
             best = r
     print(json.dumps(best), flush=True)
 
