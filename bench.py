@@ -40,6 +40,7 @@ METRIC = "gathered feature GB/s per minibatch stream (% HBM/host-link roofline) 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
 SAMPLE_AHEAD = 2                # --gpu-sampler: minibatches sampled before their announcement
 PCIE5_X16_PEAK_GBPS = 64.0      # host link, published per direction
+HIT_PATH_TARGET_FRAC = 0.70     # hit-path goal: this fraction of the HBM peak
 
 
 def log(msg):
@@ -146,11 +147,24 @@ def measure_ceilings(torch, lsmgnn, store_ptr, nbytes, duplex):
     res["zero_copy_read_GBps"] = nbytes / best(lambda: lsmgnn.copy_bytes(d0.data_ptr(), store_ptr, nbytes)) / 1e9
     res["zero_copy_write_GBps"] = nbytes / best(
         lambda: lsmgnn.copy_bytes(pinned.data_ptr(), d0.data_ptr(), nbytes)) / 1e9
-    res["hbm_copy_GBps"] = 2 * nbytes / best(lambda: lsmgnn.copy_bytes(d1.data_ptr(), d0.data_ptr(), nbytes)) / 1e9
-
+    del d0, d1, pinned
+    # HBM: the best device-to-device copy over sizes and copy engines (the
+    # library's 128-bit copy kernel, and the runtime's copy behind torch's
+    # copy_), read + write bytes per second
+    hbm = {}
+    for size in (256 << 20, 1 << 30, 4 << 30):
+        a = torch.empty(size, dtype=torch.uint8, device=dev)
+        b = torch.empty(size, dtype=torch.uint8, device=dev)
+        a.fill_(1)
+        hbm[f"copy_kernel_{size >> 20}MiB"] = 2 * size / best(
+            lambda: lsmgnn.copy_bytes(b.data_ptr(), a.data_ptr(), size), reps=7) / 1e9
+        hbm[f"runtime_copy_{size >> 20}MiB"] = 2 * size / best(lambda: b.copy_(a), reps=7) / 1e9
+        del a, b
+    torch.cuda.empty_cache()
+    res["hbm_copy_GBps"] = max(hbm.values())
+    res["hbm_copy_detail"] = {k: round(v, 1) for k, v in hbm.items()}
     res["duplex"] = duplex
     res["bytes"] = nbytes
-    del d0, d1, pinned
     return res
 
 
@@ -189,9 +203,18 @@ def _cpu_model():
     return platform.processor() or platform.machine()
 
 
-def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None, victim_mode="fifo", refresh_period=1):
+def steady_start(cfg, L):
+    """First minibatch of the steady state: after max(L+1, 10 %) of the
+    configured run, once the cold cache has filled (before it nearly every
+    request misses)."""
+    return max(L + 1, -(-cfg.batches // 10))
+
+
+def cpu_baseline(parts, budget_s, first, policy="hybrid", victim_rows=None, victim_mode="fifo", refresh_period=1):
     """The CPU oracle (single-threaded C, one instance per part) on the same
-    stream from gather 0, stopped after about budget_s seconds."""
+    stream: gathers 0 .. first-1 untimed without rows (the cold-start fill),
+    then the timed minibatches from `first` with rows, stopped after about
+    budget_s seconds."""
     from oracle.oracle import Oracle
     orcs = []
     for p in parts:
@@ -205,8 +228,12 @@ def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None, victim_mode
         orcs.append(o)
     L = parts[0]["shape"].lookahead
     nb = len(parts[0]["batches"])
+    for b in range(first):
+        for p, o in zip(parts, orcs):
+            o.gather(p["batches"][b], rows=False)
+            o.advance(p["batches"][b + L + 1])
     t0 = time.perf_counter()
-    done, rows, nbytes = 0, 0, 0
+    done, rows, nbytes = first, 0, 0
     while done < nb - L - 1 and time.perf_counter() - t0 < budget_s:
         for p, o in zip(parts, orcs):
             r = o.gather(p["batches"][done], rows=True)
@@ -218,10 +245,11 @@ def cpu_baseline(parts, budget_s, policy="hybrid", victim_rows=None, victim_mode
     for o in orcs:
         o.close()
     return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"gathers 0..{done - 1} of the same stream ({done} minibatches, {rows} unique rows, "
-                      f"{dt:.1f} s), rows copied with memcpy from the host store",
+            "sample": f"gathers {first}..{done - 1} of the same stream ({done - first} minibatches from the first "
+                      f"timed one, {rows} unique rows, {dt:.1f} s; gathers 0..{first - 1} run before, untimed), "
+                      "rows copied with memcpy from the host store",
             "rows_per_s": rows / dt,
-        "parts": len(parts), "seconds_per_minibatch": dt / max(done, 1),
+            "parts": len(parts), "seconds_per_minibatch": dt / max(done - first, 1),
             "cpu": _cpu_model(), "host_cpus": os.cpu_count()}
 
 
@@ -398,10 +426,13 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=180)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="rmat-s20-deg16-f32x256",
+    ap.add_argument("--workload", default="rmat-100M-e1.6B-f16x1024",
                     choices=["rmat-s14-e18-f32x128", "rmat-s20-deg16-f32x256", "rmat-10M-e120M-f32x1024",
                              "rmat-20M-e250M-4types", "rmat-100M-e1.6B-f16x1024"],
                     help="workload shape by name")
+    ap.add_argument("--first-timed", type=int, default=None,
+                    help="first timed minibatch (default: the steady state, max(L+1, 10%% of the configured "
+                         "minibatches); the minibatches before the warmup ones fill the cold cache, untimed)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--host-threads", type=int, default=16,
@@ -454,13 +485,18 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     cfg = W.WORKLOADS[args.workload]
     L = cfg.lookahead if isinstance(cfg, W.HeteroConfig) else cfg.cache.lookahead
-    if args.warmup + args.steps > cfg.batches:
-        print(f"bench.py: {args.warmup + args.steps} minibatches needed, the workload has {cfg.batches}",
+    # The timed minibatches start at the steady state: every pass gathers
+    # minibatches 0 .. first-1 untimed from fresh caches (the cold-start fill,
+    # then the W warmup steps), then times K steps.
+    first = steady_start(cfg, L) if args.first_timed is None else args.first_timed
+    first = max(first, args.warmup)
+    if first + args.steps > cfg.batches:
+        print(f"bench.py: minibatches {first}..{first + args.steps - 1} needed, the workload has {cfg.batches}",
               file=sys.stderr)
         sys.exit(2)
     # the minibatches the timed stream gathers or announces (a prefix of the
     # configured run); near the run's end the last gathers announce nothing
-    nb = min(cfg.batches, args.warmup + args.steps + L + 1)
+    nb = min(cfg.batches, first + args.steps + L + 1)
     if args.static == "pagerank" and isinstance(cfg, W.HeteroConfig):
         print("bench.py: --static pagerank is for the homogeneous workloads", file=sys.stderr)
         sys.exit(2)
@@ -515,7 +551,7 @@ def main():
         log(f"[bench] reverse-PageRank static scores in {static_info['ms']:.1f} ms")
     sampler_info = None
     if args.gpu_sampler:
-        sampler_info = gpu_sampler_check(torch, lsmgnn, W, parts, cfg, L, nb, args.warmup, args.steps, dev)
+        sampler_info = gpu_sampler_check(torch, lsmgnn, W, parts, cfg, L, nb, first, args.steps, dev)
         log(f"[bench] GPU sampler: {sampler_info}")
         producer = GpuLists(torch, lsmgnn, parts[0], cfg, L, max(1, max(b.size for p in parts for b in p["batches"])),
                             dev, side_stream(torch), ahead=SAMPLE_AHEAD, typed=len(parts) > 1)
@@ -589,12 +625,13 @@ def main():
                 p["cache"].wait(p["tickets"].pop(b))
 
     def run_pass(profiled, per_gather=False):
-        """Fresh caches, W warmup minibatches, then K timed ones; with
-        `profiled` the library records HIP events around every row copy.  With
-        `per_gather` the counts of the latest counted gather are read after
-        every step (a call that waits for the queued work: not for timing)."""
+        """Fresh caches, the cold-start fill and the W warmup minibatches, then
+        K timed ones; with `profiled` the library records HIP events around
+        every row copy.  With `per_gather` the counts of the latest counted
+        gather are read after every step (a call that waits for the queued
+        work: not for timing)."""
         fresh_caches()
-        for b in range(args.warmup):
+        for b in range(first):
             step(b)
         drain()
         tot0 = [p["cache"].stats()[1] for p in parts]
@@ -604,7 +641,7 @@ def main():
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         nbytes = 0
-        for b in range(args.warmup, args.warmup + args.steps):
+        for b in range(first, first + args.steps):
             nbytes += step(b)
             if per_gather:
                 for p, pp in zip(parts, per):
@@ -634,9 +671,9 @@ def main():
     # a third, untimed pass reads every gather's counts
     _, nbytes_c, d_c, _, per = run_pass(False, per_gather=True)
     assert nbytes_p == nbytes == nbytes_c and d_p == d == d_c, "the passes over one stream must do identical work"
-    alone = hit_path_alone(parts, args.warmup + args.steps - 1)
+    alone = hit_path_alone(parts, first + args.steps - 1)
     # per-minibatch rates over the timed gathers (all parts of a minibatch summed)
-    timed = [b for b in range(args.warmup, args.warmup + args.steps) if all(b in pp for pp in per)]
+    timed = [b for b in range(first, first + args.steps) if all(b in pp for pp in per)]
 
     def spread(key):
         v = sorted(sum(pp[b][key] for pp in per) / max(sum(pp[b]["unique"] for pp in per), 1) for b in timed)
@@ -707,7 +744,9 @@ def main():
                 "frac_of_measured_d2d": hb["GBps"] / ceil["hbm_copy_GBps"], "avg_launch_us": hb["avg_us"],
                 "bytes_per_launch": hb["bytes_per_launch"],
                 "traffic": None if trh is None else trh["bytes"],
-                "alone": alone}
+                "target_frac": HIT_PATH_TARGET_FRAC,
+                "gap_to_target": HIT_PATH_TARGET_FRAC - hb["GBps"] / HBM_PEAK_GBPS,
+                "alone": dict(alone, frac_of_measured_d2d=alone["achieved"] / ceil["hbm_copy_GBps"])}
 
     res = {
         "metric": METRIC, "value": gbps, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
@@ -722,7 +761,8 @@ def main():
                                  f"of its own, {SAMPLE_AHEAD} minibatches before their announcement)"
                                  if args.gpu_sampler
                                  else "host-generated, resident in HBM before the timed region"),
-                       first_timed_minibatch=args.warmup,
+                       first_timed_minibatch=first,
+                       cold_start_fill_minibatches=first - args.warmup,
                        api=("lsmgnn_gather + lsmgnn_advance" if args.sync
                             else "lsmgnn_gather_async with announcement (two minibatches in flight)")),
         "rows_per_s": rows / dt,
@@ -734,6 +774,12 @@ def main():
         "request_hit_rate": d["request_hits"] / max(d["requests"], 1),
         "request_victim_hit_rate": d["request_victim_hits"] / max(d["requests"], 1),
         "request_miss_rate": 1.0 - (d["request_hits"] + d["request_victim_hits"]) / max(d["requests"], 1),
+        # where the victim hits' rows were read (all from the victim buffer):
+        # the pinned ring over the link, the previous gather's staged rows in
+        # HBM, the cache row of a line evicted earlier in the same gather, or
+        # (queues) the HBM prefetch buffer
+        "victim_hit_rows": {k[len("victim_rows_"):]: d[k] for k in ("victim_rows_ring", "victim_rows_staged",
+                                                                  "victim_rows_cache", "victim_rows_prefetched")},
         "per_minibatch": per_minibatch,
         "unique_per_minibatch": d["unique"] / args.steps,
         "requests_per_minibatch": d["requests"] / args.steps,
@@ -750,8 +796,8 @@ def main():
                                  "from the pass without them"},
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(parts, args.cpu_budget, args.policy, 0 if args.no_ring else None,
-                                           args.victim_mode, args.refresh_period)
+        res["cpu_baseline"] = cpu_baseline(parts, args.cpu_budget, first, args.policy,
+                                           0 if args.no_ring else None, args.victim_mode, args.refresh_period)
         res["cpu_baseline"]["gpu_over_cpu"] = gbps / res["cpu_baseline"]["value"]
     for p in parts:
         p["cache"].close()

@@ -83,8 +83,11 @@ enum { LSMGNN_HIT = 0, LSMGNN_VICTIM_HIT = 1, LSMGNN_MISS = 2 };
 
 /* lsmgnn_config.victim_mode: the form of the victim buffer (victim_rows > 0).
    FIFO: one ring of victim_rows entries that overwrites its oldest; a node
-   with a live entry is a victim hit whenever it is requested, and its row
-   crosses the host link during that gather.
+   with a live entry is a victim hit whenever it is requested, and its row is
+   read from the victim buffer during that gather: over the host link from the
+   pinned ring, or, for an entry the previous gather made, from the evicted
+   rows that gather staged in HBM for its ring write (lsmgnn_counts
+   victim_rows_*).
    QUEUES: the per-reuse-iteration queues of Sec. 4.3.1: an evicted line whose
    next announced use is minibatch j goes to the queue of iteration j at the
    position its counter gives (ascending request ID within a gather), unless
@@ -150,6 +153,18 @@ typedef struct {
      request misses = requests - request_hits - request_victim_hits */
   uint64_t request_hits;
   uint64_t request_victim_hits;
+  /* where the victim hits' rows were read (they sum to victim_hits); all come
+     from the victim buffer, none from the backing store:
+       ring       FIFO: the pinned host ring (entries of gathers up to t-2);
+       staged     FIFO: entries of the previous gather, from its evicted rows
+                  staged in HBM for the ring write (which may still be running);
+       cache      FIFO: lines evicted earlier in the same gather, from the
+                  cache row the evicting fill took (not yet overwritten);
+       prefetched queues: the HBM buffer the queue was prefetched into. */
+  uint64_t victim_rows_ring;
+  uint64_t victim_rows_staged;
+  uint64_t victim_rows_cache;
+  uint64_t victim_rows_prefetched;
 } lsmgnn_counts;
 
 /* Accumulated device time of the data movement (filled only while profiling

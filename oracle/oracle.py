@@ -142,16 +142,23 @@ class Oracle:
         if rc:
             raise OracleError(rc, "orc_advance")
 
-    def gather(self, ids, rows: bool = True):
-        """Returns dict(uniq, inv, outcome, out, stats)."""
+    def gather(self, ids, rows: bool = True, out=None):
+        """Returns dict(uniq, inv, outcome, out, stats).  `out`: optional
+        caller buffer for the rows (a C-contiguous uint8 array of at least
+        len(ids) * row_bytes bytes), used instead of a new array."""
         ids = np.ascontiguousarray(ids, dtype=np.int64)
         n = ids.size
         uniq = np.empty(max(n, 1), np.int64)
         inv = np.empty(max(n, 1), np.int64)
         outcome = np.empty(max(n, 1), np.uint8)
-        out = None
-        if rows and self.store is not None:
+        if not (rows and self.store is not None):
+            out = None
+        elif out is None:
             out = np.empty((max(n, 1), self.row_bytes), np.uint8)
+        else:
+            if out.dtype != np.uint8 or not out.flags.c_contiguous or out.size < n * self.row_bytes:
+                raise ValueError("out must be a C-contiguous uint8 array of at least n * row_bytes bytes")
+            out = out.reshape(-1)[: max(n, 1) * self.row_bytes].reshape(max(n, 1), self.row_bytes)
         nu = ctypes.c_uint64()
         rc = lib().orc_gather(self._h, _ptr(ids), n, _ptr(out), _ptr(uniq), _ptr(inv),
                               _ptr(outcome), ctypes.byref(nu))

@@ -129,6 +129,9 @@ __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host,
     c.n_enq_copy = sums[kStEnqCopy];
     c.req_hits = sums[kStReqHits];
     c.req_victim_hits = sums[kStReqVictimHits];
+    c.vh_ring = sums[kStVhRing];
+    c.vh_staged = sums[kStVhStaged];
+    c.vh_same = sums[kStVhSame];
     // queue mode: candidates that found their queue full were dropped
     c.enqueued -= c.q_overflow;
     c.dropped += c.q_overflow;
@@ -840,7 +843,11 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
   const uint32_t U = cn->n_unique;
   const uint64_t tail0 = d.tail[0], tail_prev = d.tail[1];
   const uint64_t tail_end = tail0 + cn->enq_total;
-  uint32_t c_vhit = 0, c_miss = 0, c_hbm = 0, c_host = 0;
+  // the previous gather's surviving entries, [q_lo_prev, tail0), were staged
+  // in that order in its staging buffer
+  const uint64_t q_lo_prev = tail0 - ((tail0 - tail_prev) < d.V ? (tail0 - tail_prev) : d.V);
+  const uint64_t stage_prev = d.stage_row0 + ((t + 1u) & 1u) * d.stage_rows;
+  uint32_t c_vhit = 0, c_miss = 0, c_hbm = 0, c_host = 0, c_vring = 0, c_vstaged = 0, c_vsame = 0;
   for (uint32_t base = blockIdx.x * kBlock; base < U; base += gridDim.x * kBlock) {
     const uint32_t u = base + threadIdx.x;
     bool from_host = false, from_hbm = false, refill = false;
@@ -895,20 +902,25 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
             code = kSrcHbm | sc.slot[e];
             sc.dead[e] = 1;
             ++c_hbm;
-          } else if (q + d.V >= tail_end) {
-            // no enqueue of this batch reuses the slot: remove the entry now.
-            // An entry of the previous gather may still be on its way to the
-            // ring (its copy runs beside this gather), so its row is taken from
-            // the backing store, which holds identical bytes.
-            d.ring_tag[q % d.V] = kEmpty;
-            code = q >= tail_prev ? (kSrcStore | x) : (kSrcRing | (q % d.V));
-            ++c_host;
+            ++c_vsame;
           } else {
-            // the slot is rewritten by an enqueue of this batch, which runs
-            // concurrently with the host fetch: take the identical bytes from
-            // the backing store instead
-            code = kSrcStore | x;
-            ++c_host;
+            // The entry leaves the ring: removed now, unless an enqueue of this
+            // batch takes its slot anyway.  Its row is the victim buffer's:
+            //  - an entry of the previous gather is read from that gather's
+            //    staging rows in HBM (its ring write may still be running);
+            //  - an older one from the pinned ring.  The ring rows it is read
+            //    from are overwritten only by this gather's ring write, which
+            //    the runtime queues after this gather's host fetch.
+            if (q + d.V >= tail_end) d.ring_tag[q % d.V] = kEmpty;
+            if (q >= tail_prev) {
+              code = kSrcHbm | (stage_prev + (q - q_lo_prev));
+              ++c_hbm;
+              ++c_vstaged;
+            } else {
+              code = kSrcRing | (q % d.V);
+              ++c_host;
+              ++c_vring;
+            }
           }
         } else {
           ++c_miss;
@@ -944,6 +956,9 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
   block_count(c_miss, sc.stat_part, kStMisses);
   block_count(c_hbm, sc.stat_part, kStHbm);
   block_count(c_host, sc.stat_part, kStHost);
+  block_count(c_vring, sc.stat_part, kStVhRing);
+  block_count(c_vstaged, sc.stat_part, kStVhStaged);
+  block_count(c_vsame, sc.stat_part, kStVhSame);
 }
 
 // Outcomes per raw request: each request takes its unique ID's outcome (the
@@ -1027,6 +1042,7 @@ void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t t, Scratch &sc,
   }
   hipLaunchKernelGGL(k_resolve, dim3(g), dim3(kBlock), 0, s, d, sc, t, outcome, cn);
   for (int st = kStVictimHits; st <= kStHost; ++st) grids.g[st] = g;
+  for (int st = kStVhRing; st <= kStVhSame; ++st) grids.g[st] = g;
 }
 
 void launch_ring_enqueue(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, Counters *cn, StatGrids &grids,

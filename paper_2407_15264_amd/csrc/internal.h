@@ -58,6 +58,7 @@ enum StatSlot : int {
   kStVictimHits, kStMisses, kStHbm, kStHost,                           // resolve
   kStEnqCopy,                                                          // enqueue finalize
   kStReqHits, kStReqVictimHits,                                        // per-request outcomes
+  kStVhRing, kStVhStaged, kStVhSame,                                   // victim hits by row source
   kNumStat
 };
 constexpr unsigned kMaxGrid = 8192;  // grid cap of every grid-stride kernel
@@ -76,12 +77,16 @@ struct Counters {
   uint32_t n_hbm, n_host, n_enq_copy, n_fill;  // rows per data kernel
   uint32_t enq_total;
   uint32_t req_hits, req_victim_hits;  // outcomes counted per raw request
+  // FIFO victim hits by where their rows were read: the pinned ring, the
+  // previous gather's staged evicted rows (HBM), the cache row of a line
+  // evicted earlier in the same gather
+  uint32_t vh_ring, vh_staged, vh_same;
   // victim queues (queue mode): enqueue candidates that found their queue
   // full, and per queue slot the entries before this gather and those it placed
   uint32_t q_overflow;
   uint32_t q_before[kMaxQueues];
   uint32_t q_placed[kMaxQueues];
-  uint32_t pad[15];
+  uint32_t pad[12];
 };
 
 // Dedup result of a gather, written by the chunk scan to pinned host memory:
@@ -150,7 +155,7 @@ struct Scratch {
   RowList hbm;          // hits and same-batch victim hits: cache slot -> out row
   RowList fill;         // final occupants: out row -> cache slot
   RowList stage;        // surviving enqueues: cache slot -> staging row
-  uint8_t *staging;     // [min(max_batch, V)][R] evicted rows in ring order, for the ring write
+  uint8_t *staging;     // [min(max_batch, V)][R] evicted rows in ring order, for the ring write (in DevState::rows)
   uint8_t *bounce;      // pageable store only: [max_batch][R] pinned, the host-fetch rows in list order
   uint32_t *qpart;      // queue mode: [kMaxQueues][ceil(max_batch / kBlock)] per-block enqueue counts
 };
@@ -183,8 +188,13 @@ struct DevState {
   uint32_t U;            // update period of the dynamic information (1: exact at every gather)
   uint32_t host_grid;    // blocks of the host fetch (0: the default), chosen per gather by the runtime
   uint32_t *lreuse;      // U > 1: [S*8] 1 + next reuse iteration recorded at the last update, or 0
-  // queue mode: the two prefetch buffers (C rows each, by gather parity) are
-  // rows S*8 .. S*8 + 2C of `rows`, after the cache lines
+  // Rows of `rows` after the S*8 cache lines: in queue mode the two prefetch
+  // buffers (C rows each, by gather parity); then, with a victim buffer, the
+  // two staging buffers (stage_rows each, by gather parity) holding each
+  // gather's evicted rows in ring (or queue) order until they are written to
+  // pinned host memory.  The hit copy reads both through row indices.
+  uint64_t stage_row0;   // row index of parity 0's staging buffer
+  uint64_t stage_rows;   // rows per staging buffer: min(max_batch, V)
 };
 
 enum class CopyMode { kHbmToOut, kHostToOut, kCacheToStage, kOutToCache };

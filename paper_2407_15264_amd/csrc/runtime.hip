@@ -35,11 +35,13 @@
 //   - cache rows: gather t's staging and hit copy wait for gather t-1's fills;
 //     gather t's fills wait for its host fetch, staging and hit copy;
 //   - ring rows: gather t reads ring rows only of entries enqueued by gathers
-//     up to t-2 (entries of gather t-1 are read from the backing store), so
-//     its host fetch waits for gather t-2's ring write; gather t's ring write
-//     overwrites slots that gather t-1's host fetch may read, and it follows
-//     gather t's staging, which waited for gather t-1's fills, which waited
-//     for gather t-1's host fetch.
+//     up to t-2 (entries of gather t-1 are read by the hit copy from gather
+//     t-1's staging rows, which gather t+1's staging overwrites after gather
+//     t's hit copy on the in-order meta stream), so its host fetch waits for
+//     gather t-2's ring write; gather t's ring write overwrites slots that
+//     gathers t-1 and t may read: it is queued on the dma stream behind gather
+//     t's fills, which wait for gather t's host fetch (and gather t-1's), and
+//     with a pageable store only after the host threads copied gather t's rows.
 // Every call first makes the meta stream wait for the work already queued on
 // the caller's stream (the IDs and the output buffers).
 #include <hip/hip_runtime.h>
@@ -280,6 +282,10 @@ void harvest_stats(lsmgnn_cache *c, Flight &f) {
   st.dropped = h.dropped;
   st.request_hits = h.req_hits;
   st.request_victim_hits = h.req_victim_hits;
+  st.victim_rows_ring = h.vh_ring;
+  st.victim_rows_staged = h.vh_staged;
+  st.victim_rows_cache = h.vh_same;
+  st.victim_rows_prefetched = c->d.qmode ? h.victim_hits : 0;
   c->last = st;
   c->total.batch = f.t + 1;
   c->total.requests += st.requests;
@@ -292,6 +298,10 @@ void harvest_stats(lsmgnn_cache *c, Flight &f) {
   c->total.dropped += st.dropped;
   c->total.request_hits += st.request_hits;
   c->total.request_victim_hits += st.request_victim_hits;
+  c->total.victim_rows_ring += st.victim_rows_ring;
+  c->total.victim_rows_staged += st.victim_rows_staged;
+  c->total.victim_rows_cache += st.victim_rows_cache;
+  c->total.victim_rows_prefetched += st.victim_rows_prefetched;
   c->tail += h.enq_total;
   f.enq_total = h.enq_total;
   f.tail_end = c->tail;
@@ -742,7 +752,17 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   const uint64_t B = cfg->max_batch;
   Scratch sc{};
 
-  bool ok = dev_alloc(c, &d.sets, S) && dev_alloc(c, &d.rows, (S * lsm::kWays + (queues ? 2 * d.C : 0)) * R) &&
+  // rows: the cache lines, then (queue mode) the two prefetch buffers, then
+  // (with a victim buffer) the two staging buffers
+  d.stage_row0 = S * lsm::kWays + (queues ? 2 * d.C : 0);
+  d.stage_rows = V ? (B < V ? B : V) : 0;
+  const uint64_t total_rows = d.stage_row0 + 2 * d.stage_rows;
+  // the row copies index these rows with 32 bits
+  if (total_rows > 0xffffffffull || total_rows > ~0ull / R) {
+    delete c;
+    return LSMGNN_E_INVAL;
+  }
+  bool ok = dev_alloc(c, &d.sets, S) && dev_alloc(c, &d.rows, total_rows * R) &&
             dev_alloc(c, &d.mask, N) &&
             dev_alloc(c, &d.stat, N) && dev_alloc(c, &d.present, map_bytes) &&
             dev_alloc(c, &d.chunk_sums, d.nchunks) &&
@@ -770,8 +790,8 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
          (pageable || (dev_alloc(c, &f.sc.host_list, B) && dev_alloc(c, &f.sc.host_src, B))) &&
          dev_alloc(c, &f.sc.hbm.src, B) && dev_alloc(c, &f.sc.hbm.dst, B) && dev_alloc(c, &f.sc.fill.src, B) &&
          dev_alloc(c, &f.sc.fill.dst, B) && dev_alloc(c, &f.sc.stage.src, B) && dev_alloc(c, &f.sc.stage.dst, B) &&
-         (V == 0 || dev_alloc(c, &f.sc.staging, (B < V ? B : V) * R)) &&
          host_alloc(c, &f.hc, &f.hc_dev, sizeof(Counters), true);
+    if (ok && V) f.sc.staging = d.rows + (d.stage_row0 + (uint64_t)(&f - c->fl) * d.stage_rows) * R;
     if (ok && pageable) {
       // the host reads the host-fetch list and fills the bounce rows
       ok = host_alloc(c, &f.hlist_host, &f.sc.host_list, B * sizeof(uint32_t), false) &&

@@ -6,8 +6,10 @@ is no CPU fallback: if the library is missing this module raises.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
+import weakref
 
 import numpy as np
 
@@ -18,8 +20,8 @@ STATUS_NAMES = {0: "OK", 1: "E_INVAL", 2: "E_RANGE", 3: "E_WINDOW", 4: "E_NOMEM"
 HIT, VICTIM_HIT, MISS = 0, 1, 2
 EMPTY = 0xFFFFFFFF
 COUNT_FIELDS = ("batch", "requests", "unique", "hits", "victim_hits", "misses", "evictions", "enqueued",
-                "dropped", "request_hits",
-                "request_victim_hits")
+                "dropped", "request_hits", "request_victim_hits", "victim_rows_ring", "victim_rows_staged",
+                "victim_rows_cache", "victim_rows_prefetched")
 
 
 class LsmgnnError(RuntimeError):
@@ -67,6 +69,21 @@ class Profile(ctypes.Structure):
 
 
 _lib = None
+
+# Library objects still open, closed at interpreter exit before module
+# teardown begins: caches first (their host threads read the stores and their
+# streams may still move rows), then samplers, then pinned buffers.  A
+# finalizer that ran during teardown would find the module's globals gone.
+_LIVE = {"cache": weakref.WeakSet(), "sampler": weakref.WeakSet(), "pinned": weakref.WeakSet()}
+
+
+def _close_all():
+    for kind in ("cache", "sampler", "pinned"):
+        for obj in list(_LIVE[kind]):
+            obj.close()
+
+
+atexit.register(_close_all)
 
 
 def lib():
@@ -189,17 +206,18 @@ class GpuSampler:
     def __init__(self, offsets, adj, fanout, seed=0, device=0):
         import torch
         self.device = torch.device("cuda", device)
+        off_p = _dev_ptr(offsets, torch.int64, "offsets")
+        adj_p = _dev_ptr(adj, (torch.int32, torch.uint32), "adj") if adj.numel() else None
         self._graph = (offsets, adj)  # keeps the borrowed graph alive
         self.num_nodes = offsets.numel() - 1
         fan = (ctypes.c_uint32 * len(fanout))(*[int(f) for f in fanout])
         self.hops = len(fanout)
         h = ctypes.c_void_p()
-        _check(lib().lsmgnn_sampler_create(ctypes.c_void_p(offsets.data_ptr()),
-                                           ctypes.c_void_p(adj.data_ptr()) if adj.numel() else None,
-                                           self.num_nodes, fan, self.hops, int(seed), int(device), ctypes.byref(h)),
-               "lsmgnn_sampler_create")
+        _check(lib().lsmgnn_sampler_create(off_p, adj_p, self.num_nodes, fan, self.hops, int(seed), int(device),
+                                           ctypes.byref(h)), "lsmgnn_sampler_create")
         self._destroy = lib().lsmgnn_sampler_destroy  # kept: module globals may be gone when the finalizer runs
         self._h = h
+        _LIVE["sampler"].add(self)
 
     def close(self):
         if getattr(self, "_h", None):
@@ -211,18 +229,22 @@ class GpuSampler:
     def sample(self, seeds, batch, out, stream=None):
         """Request list of minibatch `batch` from its seeds (int64 device
         tensor) into `out` (int64 device tensor); returns out[:length]."""
+        import torch
+        sp = _dev_ptr(seeds, torch.int64, "seeds") if seeds.numel() else None
+        op = _dev_ptr(out, torch.int64, "out")
         n = ctypes.c_uint64(0)
-        _check(lib().lsmgnn_sample(self._h, ctypes.c_void_p(seeds.data_ptr()) if seeds.numel() else None,
-                                   seeds.numel(), int(batch), ctypes.c_void_p(out.data_ptr()), out.numel(),
-                                   ctypes.byref(n), _stream_handle(stream, self.device.index)), "lsmgnn_sample")
+        _check(lib().lsmgnn_sample(self._h, sp, seeds.numel(), int(batch), op, out.numel(), ctypes.byref(n),
+                                   _stream_handle(stream, self.device.index)), "lsmgnn_sample")
         return out[: n.value]
 
     def sample_async(self, seeds, batch, out, result_ptr, stream=None):
         """Queue the sampling of minibatch `batch` into `out`; once `stream`
         has run it, the two uint64 at result_ptr (pinned host memory) hold
         the list's length and its status code."""
-        _check(lib().lsmgnn_sample_async(self._h, ctypes.c_void_p(seeds.data_ptr()) if seeds.numel() else None,
-                                         seeds.numel(), int(batch), ctypes.c_void_p(out.data_ptr()), out.numel(),
+        import torch
+        sp = _dev_ptr(seeds, torch.int64, "seeds") if seeds.numel() else None
+        op = _dev_ptr(out, torch.int64, "out")
+        _check(lib().lsmgnn_sample_async(self._h, sp, seeds.numel(), int(batch), op, out.numel(),
                                          ctypes.c_void_p(result_ptr), _stream_handle(stream, self.device.index)),
                "lsmgnn_sample_async")
 
@@ -239,12 +261,20 @@ def split_by_type_async(ids, node_type, local, outs, work, result_ptr, stream=No
     (int64 device tensors of equal length, one per type), work (a device
     tensor of at least split_work_bytes bytes); result_ptr: pinned host
     memory for the len(outs) lengths and the status."""
+    import torch
     T = len(outs)
-    ptrs = (ctypes.c_void_p * T)(*[o.data_ptr() for o in outs])
-    _check(lib().lsmgnn_split_by_type_async(ctypes.c_void_p(ids.data_ptr()) if ids.numel() else None, ids.numel(),
-                                            node_type.numel(), ctypes.c_void_p(node_type.data_ptr()),
-                                            ctypes.c_void_p(local.data_ptr()), T, ptrs, outs[0].numel(),
-                                            ctypes.c_void_p(work.data_ptr()), work.numel() * work.element_size(),
+    if T == 0:
+        raise ValueError("outs must hold one tensor per node type")
+    ids_p = _dev_ptr(ids, torch.int64, "ids") if ids.numel() else None
+    type_p = _dev_ptr(node_type, torch.uint8, "node_type")
+    local_p = _dev_ptr(local, (torch.int32, torch.uint32), "local")
+    if local.numel() != node_type.numel():
+        raise ValueError("local and node_type must have one entry per node")
+    ptrs = (ctypes.c_void_p * T)(*[_dev_ptr(o, torch.int64, f"outs[{t}]").value for t, o in enumerate(outs)])
+    cap = min(o.numel() for o in outs)  # every list may be written up to the capacity
+    work_p = _dev_ptr(work, work.dtype, "work")
+    _check(lib().lsmgnn_split_by_type_async(ids_p, ids.numel(), node_type.numel(), type_p, local_p, T, ptrs, cap,
+                                            work_p, work.numel() * work.element_size(),
                                             ctypes.c_void_p(result_ptr), _stream_handle(stream, device)),
            "lsmgnn_split_by_type_async")
 
@@ -258,6 +288,7 @@ class PinnedBuffer:
         self.ptr = p.value
         self.nbytes = int(nbytes)
         self._free = lib().lsmgnn_host_free  # kept: module globals may be gone when the finalizer runs
+        _LIVE["pinned"].add(self)
 
     def numpy(self, dtype=np.uint8, shape=None) -> np.ndarray:
         raw = (ctypes.c_uint8 * self.nbytes).from_address(self.ptr)
@@ -279,10 +310,13 @@ def _stream_handle(stream, device):
 
 
 def _dev_ptr(t, dtype, name):
+    """Device address of a contiguous tensor of `dtype` (or one of a tuple of
+    dtypes); raises TypeError for anything else."""
     import torch
     if not isinstance(t, torch.Tensor) or not t.is_cuda:
         raise TypeError(f"{name} must be a CUDA (HIP) tensor")
-    if t.dtype != dtype or not t.is_contiguous():
+    ok = t.dtype in dtype if isinstance(dtype, tuple) else t.dtype == dtype
+    if not ok or not t.is_contiguous():
         raise TypeError(f"{name} must be a contiguous {dtype} tensor")
     return ctypes.c_void_p(t.data_ptr())
 
@@ -359,6 +393,7 @@ class FeatureCache:
         self._destroy = lib().lsmgnn_cache_destroy  # kept: module globals may be gone when the finalizer runs
         self._h = h
         self._scratch = {}
+        _LIVE["cache"].add(self)
 
     def close(self):
         if getattr(self, "_h", None):

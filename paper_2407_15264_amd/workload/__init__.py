@@ -175,7 +175,7 @@ TYPE_PERM_SEED = 0x54595045
 
 
 def build(verbose: bool = False) -> str:
-    cmd = ["gcc", "-O3", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-Wall",
+    cmd = ["gcc", "-O3", "-std=c11", "-ffp-contract=off", "-fno-math-errno", "-fopenmp", "-fPIC", "-shared", "-Wall",
            os.path.join(HERE, "gen.c"), "-o", LIB_PATH + ".tmp", "-lm"]
     subprocess.run(cmd, check=True, capture_output=not verbose)
     os.replace(LIB_PATH + ".tmp", LIB_PATH)

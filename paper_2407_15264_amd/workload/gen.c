@@ -26,10 +26,17 @@
  *   (raw, with duplicates).  Seeds are consecutive chunks of a seeded
  *   Fisher-Yates permutation of [0, N).
  *
- *   Features: x[v][k] = sqrt(-2 ln u1) cos(2 pi u2) (Box-Muller) with u1, u2
- *   from the stream keyed by the feature seed at counters 2(v*dim+k) and
- *   2(v*dim+k)+1; rounded to fp32, and for fp16 further rounded from fp32 to
- *   binary16 with round-to-nearest-even.
+ *   Features: Box-Muller (Box and Muller, Ann. Math. Statist. 1958) in binary32,
+ *   both outputs of each pair used.  Row v, pair j (elements 2j and 2j+1) takes
+ *   draw r = output (v * ceil(dim/2) + j) of the stream keyed by the feature
+ *   seed; its top 24 bits give u1 = (hi24 + 1) / 2^24 in (0, 1], the next 24
+ *   bits an angle w / 2^24 of a full turn; the pair is (rho cos theta, rho sin
+ *   theta) with rho = sqrt(-2 ln u1).  The logarithm and the circular
+ *   functions are this file's own polynomials (see nrm_pair): any
+ *   approximation serves a synthetic input as long as it is fixed, and these
+ *   vectorize, which the library calls do not (a 200 GB table is filled in
+ *   seconds per core-minute instead of hours).  fp16 rows are the fp32 values
+ *   rounded to binary16 with round-to-nearest-even.
  */
 #include <math.h>
 #include <stdint.h>
@@ -92,16 +99,22 @@ int wl_rmat_csr(uint64_t n, uint64_t e, double a, double b, double c, uint64_t s
   uint32_t *dst = (uint32_t *)malloc(e * sizeof(uint32_t));
   if (!src || !dst) { free(src); free(dst); return -1; }
 
+  /* Rounds of NCH chunks of CH consecutive attempts: each chunk keeps its
+     accepted edges in attempt order, then they are placed after those of the
+     earlier chunks until e edges are accepted. */
   const uint64_t CH = 1ULL << 16;  /* attempts per chunk */
   const int NCH = 256;             /* chunks per round */
   uint64_t *cnt = (uint64_t *)malloc(NCH * sizeof(uint64_t));
+  uint32_t *kept = (uint32_t *)malloc((uint64_t)NCH * CH * 2 * sizeof(uint32_t));
+  if (!cnt || !kept) { free(cnt); free(kept); free(src); free(dst); return -1; }
   uint64_t got = 0, base = 0;
   while (got < e) {
 #pragma omp parallel for schedule(dynamic, 1)
     for (int ci = 0; ci < NCH; ++ci) {
       uint64_t k0 = base + (uint64_t)ci * CH, m = 0;
-      uint32_t s, d;
-      for (uint64_t k = k0; k < k0 + CH; ++k) m += (uint64_t)rmat_attempt(key, k, scale, a, ab, abc, n, &s, &d);
+      uint32_t *kc = kept + (uint64_t)ci * CH * 2;
+      for (uint64_t k = k0; k < k0 + CH; ++k)
+        m += (uint64_t)rmat_attempt(key, k, scale, a, ab, abc, n, &kc[2 * m], &kc[2 * m + 1]);
       cnt[ci] = m;
     }
     uint64_t pos[256];
@@ -109,16 +122,13 @@ int wl_rmat_csr(uint64_t n, uint64_t e, double a, double b, double c, uint64_t s
     for (int ci = 0; ci < NCH; ++ci) { pos[ci] = acc; acc += cnt[ci]; }
 #pragma omp parallel for schedule(dynamic, 1)
     for (int ci = 0; ci < NCH; ++ci) {
-      uint64_t p = pos[ci];
-      if (p >= e) continue;
-      uint64_t k0 = base + (uint64_t)ci * CH;
-      uint32_t s, d;
-      for (uint64_t k = k0; k < k0 + CH && p < e; ++k)
-        if (rmat_attempt(key, k, scale, a, ab, abc, n, &s, &d)) { src[p] = s; dst[p] = d; ++p; }
+      const uint32_t *kc = kept + (uint64_t)ci * CH * 2;
+      for (uint64_t i = 0, p = pos[ci]; i < cnt[ci] && p < e; ++i, ++p) { src[p] = kc[2 * i]; dst[p] = kc[2 * i + 1]; }
     }
     got = acc < e ? acc : e;
     base += (uint64_t)NCH * CH;
   }
+  free(kept);
   free(cnt);
 
   /* CSR by source: count, exclusive prefix, place, then sort each list */
@@ -278,44 +288,86 @@ int wl_sample(const int64_t *off, const uint32_t *adj, const int64_t *perm, uint
 }
 
 /* --------------------------------------------------------------- features */
+static inline float f_of(uint32_t b) { float f; memcpy(&f, &b, 4); return f; }
+static inline uint32_t b_of(float f) { uint32_t b; memcpy(&b, &f, 4); return b; }
+
+/* binary32 -> binary16, round to nearest even, for finite |f| < 65504 (the
+   features stay far below it).  Below 2^-14 the result is subnormal: adding
+   0.5 (whose unit in the last place is 2^-24, fp16's subnormal step) rounds
+   |f| to a multiple of 2^-24 in the float adder, and the sum's low mantissa
+   bits are the subnormal's.  Otherwise the exponent is rebiased by 15 - 127
+   and the 13 dropped mantissa bits are rounded half to even by adding
+   0xfff plus the lowest kept bit before the shift (a carry into the exponent
+   is the correct result).  Branch-free, so loops over rows vectorize. */
 static inline uint16_t f32_to_f16_rne(float f) {
-  uint32_t x;
-  memcpy(&x, &f, 4);
-  uint32_t sign = (x >> 16) & 0x8000u;
-  uint32_t ex = (x >> 23) & 0xffu;
-  uint32_t man = x & 0x7fffffu;
-  if (ex == 0xffu) return (uint16_t)(sign | 0x7c00u | (man ? 0x200u : 0));
-  int32_t e = (int32_t)ex - 127 + 15;
-  if (e >= 31) return (uint16_t)(sign | 0x7c00u);
-  if (e <= 0) {
-    if (e < -10) return (uint16_t)sign;
-    man |= 0x800000u;
-    uint32_t shift = (uint32_t)(14 - e);
-    uint32_t h = man >> shift;
-    uint32_t rem = man & ((1u << shift) - 1), half = 1u << (shift - 1);
-    if (rem > half || (rem == half && (h & 1u))) ++h;
-    return (uint16_t)(sign | h);
-  }
-  uint32_t h = ((uint32_t)e << 10) | (man >> 13);
-  uint32_t rem = man & 0x1fffu;
-  if (rem > 0x1000u || (rem == 0x1000u && (h & 1u))) ++h;
-  return (uint16_t)(sign | h);
+  const uint32_t x = b_of(f), sign = (x >> 16) & 0x8000u, ax = x & 0x7fffffffu;
+  const uint32_t sub = b_of(f_of(ax) + 0.5f) - 0x3f000000u;
+  const uint32_t nrm = (ax + 0xc8000fffu + ((ax >> 13) & 1u)) >> 13; /* 0xc8000000 = (15 - 127) << 23 */
+  const uint32_t is_sub = 0u - (uint32_t)(ax < 0x38800000u);
+  return (uint16_t)(sign | (sub & is_sub) | (nrm & ~is_sub));
+}
+
+/* One Box-Muller pair from a 64-bit draw r, in binary32 throughout.
+     ln u1:  u1 = m * 2^e with m in [sqrt(1/2), sqrt(2)); ln m = 2 atanh(s),
+             s = (m - 1)/(m + 1) (|s| <= 0.172), by its odd series to s^9.
+     angle:  w in [0, 2^24) is a fraction w / 2^24 of a turn; q = w / 2^22
+             rounded to the nearest integer names the quadrant and
+             phi = (w - q 2^22) (pi/2) / 2^22 in [-pi/4, pi/4] the rest;
+             sin phi and cos phi by their Taylor series to phi^9 and phi^10,
+             then rotated by q quarter turns.
+   Truncation errors are below 2e-9, under the binary32 rounding. */
+static inline void nrm_pair(uint64_t r, float *x0, float *x1) {
+  const float u1 = (float)((uint32_t)(r >> 40) + 1u) * (1.0f / 16777216.0f);
+  uint32_t ub = b_of(u1);
+  int32_t e = (int32_t)(ub >> 23) - 127;
+  uint32_t mb = (ub & 0x007fffffu) | 0x3f800000u;   /* mantissa in [1, 2) */
+  const uint32_t big = mb > 0x3fb504f3u;             /* above sqrt(2): halve it */
+  mb -= big << 23;
+  e += (int32_t)big;
+  const float m = f_of(mb), s = (m - 1.0f) / (m + 1.0f), s2 = s * s;
+  const float lnm = 2.0f * s * (1.0f + s2 * (1.0f / 3.0f + s2 * (1.0f / 5.0f + s2 * (1.0f / 7.0f + s2 * (1.0f / 9.0f)))));
+  const float ln_u1 = (float)e * 0.69314718055994531f + lnm;
+  const float rho = sqrtf(-2.0f * ln_u1);
+
+  const int32_t w = (int32_t)((r >> 16) & 0xffffffu);
+  const int32_t q = (w + (1 << 21)) >> 22;           /* 0..4 */
+  const float phi = (float)(w - (q << 22)) * (1.5707963267948966f / 4194304.0f);
+  const float p2 = phi * phi;
+  const float sn = phi * (1.0f + p2 * (-1.0f / 6.0f + p2 * (1.0f / 120.0f + p2 * (-1.0f / 5040.0f +
+                                                                                 p2 * (1.0f / 362880.0f)))));
+  const float cs = 1.0f + p2 * (-0.5f + p2 * (1.0f / 24.0f + p2 * (-1.0f / 720.0f + p2 * (1.0f / 40320.0f +
+                                                                                      p2 * (-1.0f / 3628800.0f)))));
+  const int32_t qq = q & 3;
+  const float c = qq == 0 ? cs : qq == 1 ? -sn : qq == 2 ? -cs : sn;
+  const float sv = qq == 0 ? sn : qq == 1 ? cs : qq == 2 ? -sn : -cs;
+  *x0 = rho * c;
+  *x1 = rho * sv;
 }
 
 /* Fill rows [v0, v1) of a feature table; elt_bytes is 4 (fp32) or 2 (fp16).
-   `out` points at row v0. */
+   `out` points at row v0.  Every row depends only on (seed, v, dim). */
 void wl_features(uint64_t dim, int elt_bytes, uint64_t seed, uint64_t v0, uint64_t v1, void *out) {
-  uint64_t key = sm_key(seed, LABEL_FEAT);
-  const double two_pi = 6.283185307179586476925286766559;
-#pragma omp parallel for schedule(static)
-  for (uint64_t v = v0; v < v1; ++v) {
-    for (uint64_t k = 0; k < dim; ++k) {
-      uint64_t c = 2 * (v * dim + k);
-      double u1 = u01(sm_at(key, c)) + (1.0 / 9007199254740992.0); /* (0, 1] */
-      double u2 = u01(sm_at(key, c + 1));
-      float x = (float)(sqrt(-2.0 * log(u1)) * cos(two_pi * u2));
-      if (elt_bytes == 4) ((float *)out)[(v - v0) * dim + k] = x;
-      else ((uint16_t *)out)[(v - v0) * dim + k] = f32_to_f16_rne(x);
+  const uint64_t key = sm_key(seed, LABEL_FEAT);
+  const uint64_t pairs = (dim + 1) / 2;
+#pragma omp parallel
+  {
+    float *tmp = (float *)malloc(2 * pairs * sizeof(float));
+#pragma omp for schedule(static)
+    for (uint64_t v = v0; v < v1; ++v) {
+      const uint64_t c0 = v * pairs;
+      for (uint64_t j = 0; j < pairs; ++j) nrm_pair(sm_at(key, c0 + j), &tmp[2 * j], &tmp[2 * j + 1]);
+      if (elt_bytes == 4) {
+        memcpy((float *)out + (v - v0) * dim, tmp, dim * sizeof(float));
+      } else {
+        uint16_t *o = (uint16_t *)out + (v - v0) * dim;
+        for (uint64_t k = 0; k < dim; ++k) o[k] = f32_to_f16_rne(tmp[k]);
+      }
     }
+    free(tmp);
   }
+}
+
+/* exported for the generator's own tests: the binary16 rounding */
+void wl_f32_to_f16(const float *in, uint16_t *out, uint64_t n) {
+  for (uint64_t i = 0; i < n; ++i) out[i] = f32_to_f16_rne(in[i]);
 }

@@ -11,8 +11,6 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: long CPU test")
-    config.addinivalue_line("markers", "huge: full-size GPU run needing about 250 GiB of host memory; "
-                                       "not part of -m gpu (run with -m huge)")
 
 
 @pytest.fixture(scope="session", autouse=True)

@@ -175,6 +175,13 @@ class _Lane:
                           near_threshold=near_threshold, store=store.np, policy=policy, victim_mode=victim_mode,
                           refresh_period=refresh_period)
         self.db = [torch.as_tensor(np.asarray(b, np.int64)).to(dev) for b in batches]
+        if rows is not None and rows != 0:
+            # the oracle writes its rows into pinned memory; they are compared
+            # with the gathered rows on the GPU
+            nbytes = self.mb * store.row_bytes
+            self.ref_host = torch.empty(nbytes, dtype=torch.uint8).pin_memory()
+            self.ref_np = self.ref_host.numpy()
+            self.ref_dev = torch.empty(nbytes, dtype=torch.uint8, device=dev)
         self.bufs = [(torch.empty(self.mb * store.row_bytes, dtype=torch.uint8, device=dev),
                       torch.empty(self.mb, dtype=torch.int64, device=dev),
                       torch.empty(self.mb, dtype=torch.int64, device=dev),
@@ -204,7 +211,8 @@ class _Lane:
         where = f"{self.label} gather {b}"
         rows = self.rows
         full_rows = rows == "all" or (isinstance(rows, int) and b % rows == 0)
-        o = self.orc.gather(np.asarray(self.batches[b], np.int64), rows=full_rows)
+        o = self.orc.gather(np.asarray(self.batches[b], np.int64), rows=full_rows,
+                            out=self.ref_np if full_rows else None)
         assert r.n_unique == o["uniq"].size, (where, r.n_unique, o["uniq"].size)
         if not np.array_equal(r.unique.cpu().numpy(), o["uniq"]):
             raise AssertionError(f"{where}: unique IDs differ")
@@ -215,8 +223,14 @@ class _Lane:
             bad = np.flatnonzero(oc != o["outcome"])[:5]
             raise AssertionError(f"{where}: outcome differs at unique idx {bad.tolist()}")
         if full_rows:
-            if not np.array_equal(r.out.cpu().numpy(), o["out"]):
-                raise AssertionError(f"{where}: gathered rows differ from the oracle's")
+            nb = r.n_unique * self.store.row_bytes
+            ref = self.ref_dev[:nb]
+            ref.copy_(self.ref_host[:nb], non_blocking=True)
+            got = r.out.reshape(-1)
+            if not torch.equal(got, ref):
+                bad = torch.nonzero((got != ref).view(r.n_unique, -1).any(dim=1)).flatten()[:5].tolist()
+                raise AssertionError(f"{where}: gathered rows differ from the oracle's at unique idx {bad} "
+                                     f"(outcomes {oc[bad].tolist()})")
         elif self.store_gpu is not None:
             if not torch.equal(r.out, self.store_gpu.index_select(0, r.unique)):
                 raise AssertionError(f"{where}: gathered rows differ from the backing store")

@@ -29,3 +29,15 @@ def test_options_and_workload_names():
         assert name in r.stdout, name
     bad = _bench("--workload", "no-such-workload")
     assert bad.returncode != 0
+
+
+def test_steady_state_start():
+    """The timed minibatches start after max(L+1, 10 %) of the configured run."""
+    sys.path.insert(0, ROOT)
+    import bench
+    from paper_2407_15264_amd import workload as W
+    want = {W.RMAT14: 3, W.RMAT20: 20, W.RMAT10M: 50, W.TYPED20M: 50, W.RMAT100M: 100}
+    for name, first in want.items():
+        cfg = W.WORKLOADS[name]
+        L = cfg.lookahead if isinstance(cfg, W.HeteroConfig) else cfg.cache.lookahead
+        assert bench.steady_start(cfg, L) == first, name

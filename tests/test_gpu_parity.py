@@ -336,6 +336,112 @@ def test_provenance_hits_from_hbm_misses_from_store():
     cache.close()
 
 
+def _victim_stream(seed, n, nb, size):
+    """Minibatches drawn from a skewed popularity (hot nodes reappear within
+    the window, so lines evicted with an announced reuse return as victim
+    hits)."""
+    rng = np.random.default_rng(seed)
+    p = 1.0 / np.arange(1, n + 1) ** 0.6
+    p /= p.sum()
+    perm = rng.permutation(n)
+    return [perm[rng.choice(n, size=size, p=p)].astype(np.int64) for _ in range(nb)]
+
+
+@pytest.mark.parametrize("policy", ["hybrid", "round_robin"])
+@pytest.mark.parametrize("pageable", [False, True])
+@pytest.mark.parametrize("pipelined", [False, True])
+def test_victim_rows_come_from_the_victim_buffer(pipelined, pageable, policy):
+    """Row provenance of the victim buffer (Sec. 4.3, 4.3.1).  After a warm-up,
+    the backing-store row of every node that is not resident in the cache is
+    overwritten with a sentinel.  From then on a row's bytes travel with its
+    line: a hit or a victim hit must return the bytes the line was loaded with
+    (the original ones, unless the node missed since the overwrite and so was
+    loaded with the sentinel), and only a miss may read the store.  A victim
+    hit served from the backing store would return the sentinel for a line
+    loaded before the overwrite.  Victim rows must come from the pinned ring,
+    and with the round-robin policy (which evicts lines whose next use is the
+    very next minibatch, the hybrid order keeps those) also from the previous
+    gather's staged rows."""
+    log(f"case: victim-row provenance, pipelined={pipelined}, pageable={pageable}, policy={policy}")
+    n, rb, S, V, L = 6000, 64, 32, 300, 4  # the ring wraps every few gathers
+    batches = _victim_stream(7, n, 44, 1200)
+    store = Store.random_bytes(n, rb, 21, pinned=not pageable)
+    expect = store.np.copy()  # the bytes each node's line carries
+    stat = np.random.default_rng(3).integers(0, 50, n).astype(np.uint32)
+    mb = max(b.size for b in batches)
+    cache = lsmgnn.FeatureCache(n, rb, store.buf, stat, S, V, L, mb, pageable=pageable, policy=policy)
+    dev = [torch.as_tensor(b).cuda() for b in batches]
+    for j in range(L + 1):
+        cache.advance(dev[j])
+    bufs = [(torch.empty(mb * rb, dtype=torch.uint8, device="cuda"), torch.empty(mb, dtype=torch.int64, device="cuda"),
+             torch.empty(mb, dtype=torch.int64, device="cuda"), torch.empty(mb, dtype=torch.uint8, device="cuda"))
+            for _ in range(3)]
+    POISON, warm = 0xEE, 14
+    checked = {"vhit_loaded_before": 0, "gathers": 0}
+
+    def check(r, b):
+        uq = r.unique.cpu().numpy()
+        oc = r.outcome.cpu().numpy()
+        rows = r.out.cpu().numpy()
+        if b < warm:
+            return
+        served = oc != lsmgnn.MISS
+        want = np.where(served[:, None], expect[uq], store.np[uq])
+        bad = np.flatnonzero((rows != want).any(axis=1))
+        assert bad.size == 0, (f"gather {b}: rows of unique idx {bad[:5].tolist()} (outcomes "
+                               f"{oc[bad[:5]].tolist()}) are not the bytes their lines carry")
+        vh = oc == lsmgnn.VICTIM_HIT
+        checked["vhit_loaded_before"] += int((vh & (expect[uq] != POISON).any(axis=1)
+                                              & (store.np[uq] == POISON).all(axis=1)).sum())
+        checked["gathers"] += 1
+        miss = uq[oc == lsmgnn.MISS]
+        expect[miss] = store.np[miss]
+
+    pending = []
+    for b in range(len(batches)):
+        if b == warm:
+            # drain, then overwrite the store rows of every non-resident node
+            for tk, r, bb in pending:
+                cache.wait(tk)
+                torch.cuda.current_stream().synchronize()
+                check(r, bb)
+            pending = []
+            cache.sync()
+            tags = cache.export_state()["tags"]
+            resident = np.unique(tags[tags != lsmgnn.EMPTY]).astype(np.int64)
+            poison = np.setdiff1d(np.arange(n), resident)
+            store.np[poison] = POISON
+        out, uq, inv, oc = bufs[b % 3]
+        nxt = dev[b + L + 1] if b + L + 1 < len(batches) else None
+        if pipelined:
+            tk, r = cache.gather_async(dev[b], out, uq, inverse=inv, outcome=oc, announce=nxt)
+            pending.append((tk, r, b))
+            if len(pending) == 2:
+                tk0, r0, b0 = pending.pop(0)
+                cache.wait(tk0)
+                torch.cuda.current_stream().synchronize()
+                check(r0, b0)
+        else:
+            r = cache.gather(dev[b], out=out, unique=uq, inverse=inv, outcome=oc)
+            if nxt is not None:
+                cache.advance(nxt)
+            check(r, b)
+    for tk, r, bb in pending:
+        cache.wait(tk)
+        torch.cuda.current_stream().synchronize()
+        check(r, bb)
+    tot = cache.stats()[1]
+    cache.close()
+    log(f"  totals {tot}; victim hits on lines loaded before the overwrite: {checked['vhit_loaded_before']}")
+    assert checked["gathers"] == len(batches) - warm
+    assert checked["vhit_loaded_before"] > 0
+    assert tot["victim_rows_ring"] > 0
+    if policy == "round_robin":
+        assert tot["victim_rows_staged"] > 0
+    assert (tot["victim_rows_ring"] + tot["victim_rows_staged"] + tot["victim_rows_cache"]
+            + tot["victim_rows_prefetched"] == tot["victim_hits"])
+
+
 def _run_async_parity(store, static, S, V, L, batches, label, combined=True):
     run_async_parity(store, static, S, V, L, batches, rows="all", label=label, combined=combined)
 

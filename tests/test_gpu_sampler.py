@@ -232,3 +232,47 @@ def test_split_by_type_matches_a_stable_partition():
         lsmgnn.split_by_type_async(d_ids, d_type, d_local, outs, work[:64], res.ptr)
     assert e.value.status == "E_INVAL"
     res.close()
+
+
+def test_binding_checks_dtypes_and_takes_the_smallest_capacity():
+    """The Python binding passes only contiguous device tensors of the right
+    element type, and gives the split the smallest output length as its
+    capacity (a longer list is then reported, not written past a short one)."""
+    g = W.rmat_graph(2000, 20000, seed=4)
+    off, adj = _dev_graph(g)
+    with pytest.raises(TypeError):
+        lsmgnn.GpuSampler(off.to(torch.int32), adj, (5, 3))
+    smp = lsmgnn.GpuSampler(off, adj, (5, 3), seed=1)
+    out = torch.empty(4096, dtype=torch.int64, device="cuda")
+    with pytest.raises(TypeError):
+        smp.sample(torch.arange(10, dtype=torch.int32, device="cuda"), 0, out)
+    with pytest.raises(TypeError):
+        smp.sample(torch.arange(10, dtype=torch.int64, device="cuda"), 0, out.to(torch.int32))
+    with pytest.raises(TypeError):
+        smp.sample(torch.arange(20, dtype=torch.int64, device="cuda")[::2], 0, out)
+    smp.close()
+    N, T = 300, 3
+    node_type = torch.as_tensor(np.arange(N) % T, dtype=torch.uint8).cuda()
+    local = torch.as_tensor(np.arange(N) // T, dtype=torch.int32).cuda()
+    ids = torch.arange(N, dtype=torch.int64, device="cuda")
+    work = torch.empty(lsmgnn.split_work_bytes(N, T), dtype=torch.uint8, device="cuda")
+    res = lsmgnn.PinnedBuffer(8 * (T + 1))
+    r = res.numpy(np.uint64, (T + 1,))
+    with pytest.raises(TypeError):
+        lsmgnn.split_by_type_async(ids.to(torch.int32), node_type, local, [out[:N]] * T, work, res.ptr)
+    with pytest.raises(TypeError):
+        lsmgnn.split_by_type_async(ids, node_type.to(torch.int32), local, [out[:N]] * T, work, res.ptr)
+    with pytest.raises(TypeError):
+        lsmgnn.split_by_type_async(ids, node_type, local.to(torch.int64), [out[:N]] * T, work, res.ptr)
+    # unequal outputs: each type has 100 requests, the second output holds 40
+    outs = [torch.full((128,), -1, dtype=torch.int64, device="cuda"),
+            torch.full((40,), -1, dtype=torch.int64, device="cuda"),
+            torch.full((128,), -1, dtype=torch.int64, device="cuda")]
+    guard = torch.full((64,), -7, dtype=torch.int64, device="cuda")  # allocated after the short output
+    lsmgnn.split_by_type_async(ids, node_type, local, outs, work, res.ptr)
+    torch.cuda.current_stream().synchronize()
+    assert int(r[T]) == lsmgnn.E_INVAL and [int(v) for v in r[:T]] == [100, 100, 100]
+    for t in range(T):
+        assert np.array_equal(outs[t][:40].cpu().numpy(), np.arange(40)), t
+    assert (outs[0][40:].cpu().numpy() == -1).all() and (guard.cpu().numpy() == -7).all()
+    res.close()

@@ -103,3 +103,20 @@ def test_struct_layouts_match_header(tmp_path):
         assert int(got[name]) == ctypes.sizeof(cls), name
         for f, _ in cls._fields_:
             assert int(got[f"{name}.{f}"]) == getattr(cls, f).offset, f"{name}.{f}"
+
+
+def test_binding_rejects_host_tensors_before_calling_the_library(L):
+    """Device pointers come only from device tensors: host tensors are refused
+    in the binding, before anything reaches the library."""
+    torch = pytest.importorskip("torch")
+    off = torch.zeros(11, dtype=torch.int64)
+    adj = torch.zeros(4, dtype=torch.int32)
+    with pytest.raises(TypeError):
+        lsmgnn.GpuSampler(off, adj, (3,))
+    ids = torch.zeros(4, dtype=torch.int64)
+    with pytest.raises(TypeError):
+        lsmgnn.split_by_type_async(ids, torch.zeros(10, dtype=torch.uint8), torch.zeros(10, dtype=torch.int32),
+                                   [torch.zeros(4, dtype=torch.int64)], torch.zeros(64, dtype=torch.uint8), 0)
+    with pytest.raises(ValueError):
+        lsmgnn.split_by_type_async(ids, torch.zeros(10, dtype=torch.uint8), torch.zeros(10, dtype=torch.int32),
+                                   [], torch.zeros(64, dtype=torch.uint8), 0)

@@ -2,9 +2,11 @@
 R-MAT quadrant probabilities and CSR form, seed permutations (and the prefix
 property the benchmark relies on), the GraphSAGE request-list structure
 (seeds, then per hop distinct CSR entries of each frontier node in ascending
-position order, the next frontier being the sorted unique samples), fp16
-features as the round-to-nearest-even of the fp32 ones (numpy's conversion),
-node typing, and the pinned-memory plan.
+position order, the next frontier being the sorted unique samples), the
+features against a float64 Box-Muller evaluation of the same draws and fp16
+features as the round-to-nearest-even of the fp32 ones (numpy's conversion,
+also over wide sweeps of float bit patterns), node typing, and the
+pinned-memory plan.
 """
 import numpy as np
 import pytest
@@ -84,6 +86,57 @@ def test_fp16_features_round_the_fp32_ones_to_nearest_even():
     part = np.empty((100, 64), np.float32)
     W.fill_features(part.ctypes.data, 64, 4, 100, 200, seed=9)  # any row range gives the same rows
     assert np.array_equal(part, f32[100:200])
+
+
+def _np_mix(z):
+    z = (z ^ (z >> np.uint64(30))) * np.uint64(0xbf58476d1ce4e5b9)
+    z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94d049bb133111eb)
+    return z ^ (z >> np.uint64(31))
+
+
+def _np_at(key, k):
+    with np.errstate(over="ignore"):
+        return _np_mix(np.uint64(key) + (np.asarray(k, np.uint64) + np.uint64(1)) * np.uint64(0x9e3779b97f4a7c15))
+
+
+def test_features_are_box_muller_pairs_of_the_documented_draws():
+    """Pair j of row v is (rho cos theta, rho sin theta) from draw v*dim/2 + j:
+    u1 = (top 24 bits + 1) / 2^24, theta = 2 pi (next 24 bits) / 2^24.  The
+    generator's binary32 polynomials must agree with float64 numpy to a few
+    float roundings."""
+    dim, n, seed = 96, 2000, 5
+    with np.errstate(over="ignore"):
+        key = int(_np_at(int(_np_mix(np.uint64(seed) ^ np.uint64(0x5851f42d4c957f2d))), 4))  # LABEL_FEAT = 4
+    r = _np_at(key, np.arange(n * dim // 2, dtype=np.uint64))
+    u1 = ((r >> np.uint64(40)).astype(np.float64) + 1) / 2 ** 24
+    th = 2 * np.pi * ((r >> np.uint64(16)) & np.uint64(0xffffff)).astype(np.float64) / 2 ** 24
+    rho = np.sqrt(-2 * np.log(u1))
+    want = np.stack([rho * np.cos(th), rho * np.sin(th)], axis=1).reshape(n, dim)
+    got = W.features(n, dim, 4, seed=seed).astype(np.float64)
+    err = np.abs(got - want)
+    assert err.max() < 4e-6 * max(1.0, np.abs(want).max()), err.max()
+    # the bulk is within two float ulps of the value
+    assert np.mean(err <= 2 * np.spacing(np.abs(want).astype(np.float32)).astype(np.float64) + 1e-12) > 0.99
+
+
+def test_fp16_rounding_matches_numpy_over_float_bit_sweeps():
+    import ctypes
+    lib = W.lib()
+    lib.wl_f32_to_f16.restype = None
+    lib.wl_f32_to_f16.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64]
+    # every 61st pattern of the finite fp16 range (|x| <= 65504 = 0x477fe000 in
+    # binary32), every 7th across the subnormal boundary, all around the
+    # rounding ties of the smallest normals, with both signs
+    bits = np.concatenate([np.arange(0, 0x477fe001, 61, dtype=np.uint64),
+                           np.arange(0x33000000, 0x38800000 + 4096, 7, dtype=np.uint64),
+                           np.arange(0x387fe000, 0x38802000, dtype=np.uint64)]).astype(np.uint32)
+    bits = np.concatenate([bits, bits | np.uint32(0x80000000)])
+    f = bits.view(np.float32)
+    out = np.empty(f.size, np.uint16)
+    lib.wl_f32_to_f16(f.ctypes.data, out.ctypes.data, f.size)
+    want = f.astype(np.float16).view(np.uint16)
+    bad = np.flatnonzero(out != want)
+    assert bad.size == 0, (hex(int(bits[bad[0]])), hex(int(out[bad[0]])), hex(int(want[bad[0]])))
 
 
 def test_typed_workload_split():
