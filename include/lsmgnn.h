@@ -385,6 +385,25 @@ lsmgnn_status lsmgnn_split_by_type_async(const int64_t *ids, uint64_t n, uint64_
                                          uint64_t out_cap, void *work, uint64_t work_bytes, uint64_t *result_host,
                                          void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+   capture, serving loops, harnesses that forbid hipMalloc): the same split as
+   lsmgnn_split_by_type_async, with the same arguments, results and status
+   words, but without `work`: its work memory is a device array inside the
+   library, LSMGNN_SPLIT_SCRATCH_BYTES bytes on each device it runs on, held
+   until the process ends.  The call allocates nothing (the array's address is
+   looked up on the first call on each device).  E_INVAL also when
+   lsmgnn_split_work_bytes(n, num_types) exceeds that size: n up to 2^24
+   requests with 16 types (2^26 with 4).  Every call on a device uses the
+   same array: calls that may overlap on one device (on different streams,
+   or from several threads) race and must be ordered by the caller; queued on
+   one stream they are ordered.  E_DEVICE if the stream's device cannot be
+   found or the array's address not looked up. */
+#define LSMGNN_SPLIT_SCRATCH_BYTES (256ull + (1ull << 24) / 256 * 16 * 4)
+lsmgnn_status lsmgnn_split_by_type_noalloc_async(const int64_t *ids, uint64_t n, uint64_t num_nodes,
+                                                 const uint8_t *node_type, const uint32_t *local, uint32_t num_types,
+                                                 int64_t *const *outs, uint64_t out_cap, uint64_t *result_host,
+                                                 void *stream);
+
 /* Set index the cache uses for node x (host-side helper, for tests). */
 uint64_t lsmgnn_set_of(uint64_t x, uint64_t num_sets);
 

@@ -41,6 +41,7 @@
 
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 
 #include "lsmgnn.h"
 
@@ -610,20 +611,29 @@ uint64_t lsmgnn_split_work_bytes(uint64_t n, uint32_t num_types) {
   return ((n + lsm_smp::kBlock - 1) / lsm_smp::kBlock) * (uint64_t)num_types * 4 + 256;
 }
 
-lsmgnn_status lsmgnn_split_by_type_async(const int64_t *ids, uint64_t n, uint64_t num_nodes, const uint8_t *node_type,
-                                         const uint32_t *local, uint32_t num_types, int64_t *const *outs,
-                                         uint64_t out_cap, void *work, uint64_t work_bytes, uint64_t *result_host,
-                                         void *stream) {
+}  // extern "C"
+
+namespace {
+
+// The split's arguments other than the work memory are valid.
+bool split_args_ok(const int64_t *ids, uint64_t n, const uint8_t *node_type, const uint32_t *local,
+                   uint32_t num_types, int64_t *const *outs, uint64_t out_cap, const uint64_t *result_host) {
+  if (!result_host || !outs || !node_type || !local || num_types == 0 || num_types > lsm_smp::kMaxTypes ||
+      (n && !ids))
+    return false;
+  for (uint32_t t = 0; t < num_types; ++t)
+    if (out_cap && !outs[t]) return false;
+  return true;
+}
+
+// Queue the split with `work` (device memory of at least
+// lsmgnn_split_work_bytes(n, num_types) bytes) as its work memory.
+lsmgnn_status queue_split(const int64_t *ids, uint64_t n, uint64_t num_nodes, const uint8_t *node_type,
+                          const uint32_t *local, uint32_t num_types, int64_t *const *outs, uint64_t out_cap,
+                          void *work, uint64_t *result_host, hipStream_t st) {
   using namespace lsm_smp;
-  if (!result_host || !outs || !node_type || !local || num_types == 0 || num_types > kMaxTypes ||
-      (n && !ids) || !work || work_bytes < lsmgnn_split_work_bytes(n, num_types))
-    return LSMGNN_E_INVAL;
   TypeOuts to{};
-  for (uint32_t t = 0; t < num_types; ++t) {
-    if (out_cap && !outs[t]) return LSMGNN_E_INVAL;
-    to.p[t] = outs[t];
-  }
-  hipStream_t st = static_cast<hipStream_t>(stream);
+  for (uint32_t t = 0; t < num_types; ++t) to.p[t] = outs[t];
   // work: the device result (num_types lengths + status, 8 B each), then the tile counts
   uint64_t *res = static_cast<uint64_t *>(work);
   uint32_t *tile_cnt = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(work) + 256);
@@ -644,6 +654,79 @@ lsmgnn_status lsmgnn_split_by_type_async(const int64_t *ids, uint64_t n, uint64_
     return LSMGNN_E_DEVICE;
   }
   return LSMGNN_OK;
+}
+
+}  // namespace
+
+// Work memory of the allocation-free split: one array per device, held until
+// the process ends, shared by every call on that device (calls that overlap
+// on one device race; every call rewrites all of it that it reads).  Its
+// host-side name is not a device address: kernels and copies get the address
+// hipGetSymbolAddress returns, looked up once per device.
+constexpr uint64_t kSplitScratchBytes = 256 + (uint64_t)(1u << 24) / lsm_smp::kBlock * lsm_smp::kMaxTypes * 4;
+static_assert(kSplitScratchBytes == LSMGNN_SPLIT_SCRATCH_BYTES, "header and library disagree on the scratch size");
+static __device__ __align__(256) uint8_t scratch[kSplitScratchBytes];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxScratchDevices] = {};
+
+// Device address of `dev`'s scratch array (call with `dev` current), or NULL.
+void *scratch_on(int dev) {
+  if (dev < 0 || dev >= kMaxScratchDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+lsmgnn_status lsmgnn_split_by_type_async(const int64_t *ids, uint64_t n, uint64_t num_nodes, const uint8_t *node_type,
+                                         const uint32_t *local, uint32_t num_types, int64_t *const *outs,
+                                         uint64_t out_cap, void *work, uint64_t work_bytes, uint64_t *result_host,
+                                         void *stream) {
+  if (!split_args_ok(ids, n, node_type, local, num_types, outs, out_cap, result_host) || !work ||
+      work_bytes < lsmgnn_split_work_bytes(n, num_types))
+    return LSMGNN_E_INVAL;
+  return queue_split(ids, n, num_nodes, node_type, local, num_types, outs, out_cap, work, result_host,
+                     static_cast<hipStream_t>(stream));
+}
+
+lsmgnn_status lsmgnn_split_by_type_noalloc_async(const int64_t *ids, uint64_t n, uint64_t num_nodes,
+                                                 const uint8_t *node_type, const uint32_t *local, uint32_t num_types,
+                                                 int64_t *const *outs, uint64_t out_cap, uint64_t *result_host,
+                                                 void *stream) {
+  if (!split_args_ok(ids, n, node_type, local, num_types, outs, out_cap, result_host) ||
+      lsmgnn_split_work_bytes(n, num_types) > kSplitScratchBytes)
+    return LSMGNN_E_INVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int dev = -1, prev = -1;
+  if ((st ? hipStreamGetDevice(st, &dev) : hipGetDevice(&dev)) != hipSuccess || hipGetDevice(&prev) != hipSuccess) {
+    (void)hipGetLastError();
+    return LSMGNN_E_DEVICE;
+  }
+  // the lookup must run with the stream's device current
+  if (dev != prev && hipSetDevice(dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return LSMGNN_E_DEVICE;
+  }
+  void *work = scratch_on(dev);
+  const lsmgnn_status rc = work ? queue_split(ids, n, num_nodes, node_type, local, num_types, outs, out_cap, work,
+                                              result_host, st)
+                                : LSMGNN_E_DEVICE;
+  if (dev != prev) (void)hipSetDevice(prev);
+  return rc;
 }
 
 }  // extern "C"

@@ -143,6 +143,9 @@ def lib():
         L.lsmgnn_split_by_type_async.restype = i32
         L.lsmgnn_split_by_type_async.argtypes = [vp, u64, u64, vp, vp, ctypes.c_uint32, ctypes.POINTER(vp), u64,
                                                  vp, u64, vp, vp]
+        L.lsmgnn_split_by_type_noalloc_async.restype = i32
+        L.lsmgnn_split_by_type_noalloc_async.argtypes = [vp, u64, u64, vp, vp, ctypes.c_uint32, ctypes.POINTER(vp),
+                                                         u64, vp, vp]
         L.lsmgnn_strerror.restype = ctypes.c_char_p
         L.lsmgnn_strerror.argtypes = [i32]
         _lib = L
@@ -277,6 +280,27 @@ def split_by_type_async(ids, node_type, local, outs, work, result_ptr, stream=No
                                             work_p, work.numel() * work.element_size(),
                                             ctypes.c_void_p(result_ptr), _stream_handle(stream, device)),
            "lsmgnn_split_by_type_async")
+
+
+def split_by_type_noalloc_async(ids, node_type, local, outs, result_ptr, stream=None, device=0):
+    """split_by_type_async without the work tensor
+    (lsmgnn_split_by_type_noalloc_async): the library's own device array is
+    the work memory, so the call allocates nothing; calls that may overlap on
+    one device must be ordered by the caller."""
+    import torch
+    T = len(outs)
+    if T == 0:
+        raise ValueError("outs must hold one tensor per node type")
+    ids_p = _dev_ptr(ids, torch.int64, "ids") if ids.numel() else None
+    type_p = _dev_ptr(node_type, torch.uint8, "node_type")
+    local_p = _dev_ptr(local, (torch.int32, torch.uint32), "local")
+    if local.numel() != node_type.numel():
+        raise ValueError("local and node_type must have one entry per node")
+    ptrs = (ctypes.c_void_p * T)(*[_dev_ptr(o, torch.int64, f"outs[{t}]").value for t, o in enumerate(outs)])
+    cap = min(o.numel() for o in outs)
+    _check(lib().lsmgnn_split_by_type_noalloc_async(ids_p, ids.numel(), node_type.numel(), type_p, local_p, T, ptrs,
+                                                    cap, ctypes.c_void_p(result_ptr), _stream_handle(stream, device)),
+           "lsmgnn_split_by_type_noalloc_async")
 
 
 class PinnedBuffer:
