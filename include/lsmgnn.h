@@ -259,8 +259,10 @@ lsmgnn_status lsmgnn_host_alloc(uint64_t bytes, void **ptr);
 void lsmgnn_host_free(void *ptr);
 
 /* Calibration copy: bytes (a multiple of 16) from src to dst, both 16-byte
-   aligned, each either device memory or pinned host memory, with the same
-   128-bit access pattern as the gather's row copies.  Used to measure the
+   aligned, each either device memory or pinned host memory, with the 128-bit
+   access pattern of the gather's row copies (device to device: the HBM-side
+   copies' tiles with the non-temporal hint; across the link: the host
+   fetch's grid-strided vectors).  Used to measure the
    host-link and HBM ceilings the gather is compared against.  Synchronises
    `stream`. */
 lsmgnn_status lsmgnn_copy_bytes(void *dst, const void *src, uint64_t bytes, void *stream);

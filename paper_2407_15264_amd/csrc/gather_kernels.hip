@@ -7,7 +7,7 @@
 // first (Counters::err, or the gather's gate in the row copies) and does
 // nothing once an out-of-range ID was seen, so an invalid batch changes no state.
 //
-//   dedup       byte map over node IDs marked with plain stores, per-chunk
+//   dedup       bitmap over node IDs (one bit per node), per-chunk
 //               popcount, chunk scan, ascending compaction that records each
 //               node's unique index; the inverse index is one lookup
 //   group       per-set counts with atomics, segment allocation, placement and
@@ -86,8 +86,29 @@ static inline unsigned grid_for(uint64_t work, uint64_t per_block, unsigned cap)
 // counters to pinned host memory, advance the ring tail by the call's enqueues
 // (keeping the previous tail) and zero the device counters for the next call
 // (they start zeroed at create).
+//
+// With an announcement (ann.ids != NULL) the launch has more blocks, which all
+// also set the announced minibatch's bit for each of its IDs and record its
+// list, unless the gather's gate holds an error: the announced bits are first
+// read by the next gather's set walk.  Only that bit of a node's window word
+// changes in this kernel (duplicates write the same value), so a plain
+// read-modify-write is exact.
+__device__ __forceinline__ void announce(const AnnounceArgs &a) {
+  if (a.gate->err) return;
+  const uint32_t b = 1u << a.bit;
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < a.n; i += gridDim.x * kBlock) {
+    const int64_t x = a.ids[i];
+    a.slot_ids[i] = x;
+    const uint32_t m = a.mask[x];
+    if (!(m & b)) a.mask[x] = m | b;
+  }
+}
+
 __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host, const uint32_t *part,
-                                                   StatGrids grids, uint64_t *tail, QueueFinish qf) {
+                                                   StatGrids grids, uint64_t *tail, QueueFinish qf,
+                                                   AnnounceArgs ann) {
+  if (ann.ids) announce(ann);
+  if (blockIdx.x != 0) return;
   __shared__ uint32_t red[kNumStat][kBlock / 64];
   __shared__ uint32_t sums[kNumStat];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -157,15 +178,16 @@ __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host,
 }
 
 void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, const StatGrids &grids,
-                   uint64_t *tail, const QueueFinish &qf, hipStream_t s) {
-  hipLaunchKernelGGL(k_finish, dim3(1), dim3(kBlock), 0, s, cn, host, stat_part, grids, tail, qf);
+                   uint64_t *tail, const QueueFinish &qf, const AnnounceArgs &ann, hipStream_t s) {
+  const unsigned g = ann.ids ? grid_for(ann.n, kBlock, kMaxGrid) : 1u;
+  hipLaunchKernelGGL(k_finish, dim3(g), dim3(kBlock), 0, s, cn, host, stat_part, grids, tail, qf, ann);
 }
 
 // ------------------------------------------------------------------- dedup
-// A byte per node marks the batch's requests.  Plain byte stores need no
-// atomics: every writer of a byte writes the same value, and bytes of
-// different nodes never interfere.  (Device-scope atomics serialize on hot
-// addresses and queue behind host-link traffic on this GPU.)
+// A bitmap marks the batch's requests: bit x & 31 of word x >> 5 for node x.
+// Marks are atomic ORs, skipped when the bit is already visible (repeated IDs
+// of hub nodes would otherwise queue on one word); the two popcount/compact
+// passes then read N/8 bytes instead of a byte per node.
 //
 // Validate and mark.  Out-of-range IDs set Counters::err; valid ones are still
 // marked, and the compaction kernel then clears the map instead of compacting
@@ -176,15 +198,19 @@ void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, cons
 // succeeds.  Only that bit of a node's window word changes in this kernel, so a
 // plain read-modify-write is exact.
 __global__ void k_mark(const int64_t *ids, uint32_t n, const int64_t *ann_ids, uint32_t ann_n, uint64_t N,
-                       uint8_t *present, const int64_t *clear_ids, uint32_t clear_n, uint32_t clear_bit,
+                       uint32_t *present, const int64_t *clear_ids, uint32_t clear_n, uint32_t clear_bit,
                        uint32_t *mask, Counters *cn) {
   bool bad = false;
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
     const int64_t x = ids[i];
-    if (x < 0 || (uint64_t)x >= N)
+    if (x < 0 || (uint64_t)x >= N) {
       bad = true;
-    else
-      present[x] = 1;
+    } else {
+      const uint32_t b = 1u << (x & 31);
+      uint32_t *w = present + (x >> 5);
+      if (!(__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & b))
+        __hip_atomic_fetch_or(w, b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ann_n; i += gridDim.x * kBlock) {
     const int64_t x = ann_ids[i];
@@ -199,11 +225,11 @@ __global__ void k_mark(const int64_t *ids, uint32_t n, const int64_t *ann_ids, u
   }
 }
 
-// Each thread owns kBytesPerThread consecutive bytes of the map (four 128-bit
-// loads); marked bytes hold exactly 1, so a popcount of a word counts them.
-__device__ __forceinline__ void load_bytes(const uint8_t *present, uint32_t (&w)[kWordsPerThread]) {
-  const u32x4 *p = reinterpret_cast<const u32x4 *>(present + (size_t)blockIdx.x * kChunkBytes +
-                                                    threadIdx.x * kBytesPerThread);
+// Each thread owns kWordsPerThread consecutive words of the bitmap (four
+// 128-bit loads).
+__device__ __forceinline__ void load_words(const uint32_t *present, uint32_t (&w)[kWordsPerThread]) {
+  const u32x4 *p = reinterpret_cast<const u32x4 *>(present + ((size_t)blockIdx.x * kBlock + threadIdx.x) *
+                                                                 kWordsPerThread);
 #pragma unroll
   for (int k = 0; k < kWordsPerThread / 4; ++k) {
     const u32x4 a = p[k];
@@ -211,11 +237,11 @@ __device__ __forceinline__ void load_bytes(const uint8_t *present, uint32_t (&w)
   }
 }
 
-__global__ __launch_bounds__(kBlock) void k_chunk_popc(const uint8_t *present, uint32_t *chunk_sums,
+__global__ __launch_bounds__(kBlock) void k_chunk_popc(const uint32_t *present, uint32_t *chunk_sums,
                                                        const Counters *cn) {
   if (cn->err) return;
   uint32_t w[kWordsPerThread];
-  load_bytes(present, w);
+  load_words(present, w);
   uint32_t c = 0;
 #pragma unroll
   for (int k = 0; k < kWordsPerThread; ++k) c += __popc(w[k]);
@@ -249,15 +275,27 @@ __global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uin
   }
 }
 
-__global__ __launch_bounds__(kBlock) void k_compact(uint8_t *present, const uint32_t *chunk_off, uint32_t *uidx,
-                                                    uint32_t *uniq, int64_t *uniq_out, const Counters *cn) {
+// The compaction: each node of the chunk with its bit set, ascending, gets the
+// next unique index.  kFused: the chunk's first index is the sum of the
+// earlier chunks' counts, added up by the block itself (few chunks: this
+// saves the separate one-block scan), and the last chunk's block publishes
+// the unique count; otherwise chunk_off holds the scanned offsets.
+template <bool kFused>
+__global__ __launch_bounds__(kBlock) void k_compact(uint32_t *present, const uint32_t *chunk_off, uint32_t *uidx,
+                                                    uint32_t *uniq, int64_t *uniq_out, Counters *cn,
+                                                    uint32_t nchunks, DedupResult *dd, Gate *gate) {
   uint32_t w[kWordsPerThread];
-  load_bytes(present, w);
-  const size_t b0 = (size_t)blockIdx.x * kChunkBytes + threadIdx.x * kBytesPerThread;
-  if (cn->err) {  // rejected batch: undo the marks
+  load_words(present, w);
+  const size_t w0 = ((size_t)blockIdx.x * kBlock + threadIdx.x) * kWordsPerThread;  // first word of this thread
+  const uint32_t err = cn->err;
+  if (err) {  // rejected batch: undo the marks
 #pragma unroll
     for (int k = 0; k < kWordsPerThread; ++k)
-      if (w[k]) reinterpret_cast<uint32_t *>(present + b0)[k] = 0;
+      if (w[k]) present[w0 + k] = 0;
+    if (kFused && blockIdx.x == 0 && threadIdx.x == 0) {
+      *gate = Gate{err, 0, 0, 0, 0, 0, 0, 0, 0, {0, 0, 0}};
+      *dd = DedupResult{err, 0, {0, 0}};
+    }
     return;
   }
   uint32_t c = 0;
@@ -265,13 +303,27 @@ __global__ __launch_bounds__(kBlock) void k_compact(uint8_t *present, const uint
   for (int k = 0; k < kWordsPerThread; ++k) c += __popc(w[k]);
   uint32_t tot;
   const uint32_t ex = block_exclusive_scan(c, tot);
+  uint32_t first;
+  if constexpr (kFused) {
+    uint32_t v = 0;
+    for (uint32_t j = threadIdx.x; j < blockIdx.x; j += kBlock) v += chunk_off[j];
+    first = block_sum(v);
+    if (blockIdx.x == nchunks - 1 && threadIdx.x == 0) {
+      const uint32_t total = first + tot;
+      cn->n_unique = total;
+      *gate = Gate{0, total, 0, 0, 0, 0, 0, 0, 0, {0, 0, 0}};
+      *dd = DedupResult{0, total, {0, 0}};
+    }
+  } else {
+    first = chunk_off[blockIdx.x];
+  }
   if (tot == 0) return;
-  uint32_t pos = chunk_off[blockIdx.x] + ex;
+  uint32_t pos = first + ex;
 #pragma unroll
   for (int k = 0; k < kWordsPerThread; ++k) {
     uint32_t word = w[k];
-    while (word) {  // marked bytes ascending: bit 8*j is set for byte j
-      const uint32_t x = (uint32_t)(b0 + 4 * k + (__builtin_ctz(word) >> 3));
+    while (word) {  // marked nodes ascending: bit j of word k is node 32 (w0 + k) + j
+      const uint32_t x = (uint32_t)(32 * (w0 + k) + __builtin_ctz(word));
       uniq[pos] = x;
       uniq_out[pos] = (int64_t)x;
       uidx[x] = pos;
@@ -280,6 +332,8 @@ __global__ __launch_bounds__(kBlock) void k_compact(uint8_t *present, const uint
     }
   }
 }
+
+constexpr uint32_t kFusedScanMax = 2048;  // at most this many partial sums are added up by each block
 
 void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, const int64_t *ann_ids, uint64_t ann_n,
                   const int64_t *clear_ids, uint64_t clear_n, uint32_t clear_bit, Scratch &sc, int64_t *unique_out,
@@ -290,10 +344,15 @@ void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, const int64
   hipLaunchKernelGGL(k_mark, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, ann_ids, (uint32_t)ann_n, d.N,
                      d.present, clear_ids, (uint32_t)clear_n, clear_bit, d.mask, cn);
   hipLaunchKernelGGL(k_chunk_popc, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.present, d.chunk_sums, cn);
-  hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, s, d.chunk_sums, (uint32_t)d.nchunks, cn, dd,
-                     sc.gate);
-  hipLaunchKernelGGL(k_compact, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.present, d.chunk_sums, d.uidx,
-                     sc.uniq, unique_out, cn);
+  if (d.nchunks <= kFusedScanMax) {
+    hipLaunchKernelGGL(k_compact<true>, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.present, d.chunk_sums,
+                       d.uidx, sc.uniq, unique_out, cn, (uint32_t)d.nchunks, dd, sc.gate);
+  } else {
+    hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, s, d.chunk_sums, (uint32_t)d.nchunks, cn, dd,
+                       sc.gate);
+    hipLaunchKernelGGL(k_compact<false>, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.present, d.chunk_sums,
+                       d.uidx, sc.uniq, unique_out, cn, (uint32_t)d.nchunks, dd, sc.gate);
+  }
 }
 
 // ------------------------------------------------------------ group by set
@@ -342,7 +401,7 @@ __global__ __launch_bounds__(kBlock) void k_inverse_claim(const DevState d, Scra
       sc.dead[u] = 0;
       sc.this_q[u] = 0;
       sc.fill_dst[u] = 0;
-      d.present[x] = 0;  // the map's last reader (the compaction) is done
+      d.present[x >> 5] = 0;  // the map's last reader (the compaction) is done; every writer stores 0
     }
     const uint32_t i = block_append(claim, &cn->n_touched);
     if (claim) {
@@ -365,6 +424,10 @@ __global__ __launch_bounds__(kBlock) void k_seg_alloc(const DevState d, Scratch 
     __syncthreads();
     if (i < T) sc.seg_off[i] = boff + ex;
     __syncthreads();
+    // sets with more than kSmallSet IDs are ordered by k_big_sort
+    const bool big = c > kSmallSet;
+    const uint32_t j = block_append(big, &cn->n_big);
+    if (big) sc.big[j] = i;
   }
 }
 
@@ -375,7 +438,8 @@ __global__ void k_place(const DevState d, Scratch sc, const Counters *cn) {
     sc.seg[sc.seg_off[d.set_idx[sc.uset[u]]] + sc.arrival[u]] = u;
 }
 
-// Rank of u among the IDs of its set (all smaller unique indices come first);
+// Rank of u among the IDs of its set (all smaller unique indices come first)
+// in a set of at most kSmallSet IDs, by counting (at most kSmallSet loads);
 // lays out (u, ID, static score) contiguously per set for the walk.
 __global__ void k_rank(const DevState d, Scratch sc, const Counters *cn) {
   if (cn->err) return;
@@ -384,6 +448,7 @@ __global__ void k_rank(const DevState d, Scratch sc, const Counters *cn) {
     const uint32_t s = sc.uset[u];
     const uint32_t off = sc.seg_off[d.set_idx[s]];
     const uint32_t k = d.set_count[s];
+    if (k > kSmallSet) continue;
     uint32_t r = 0;
     if (k > 1)
       for (uint32_t j = 0; j < k; ++j) r += sc.seg[off + j] < u ? 1u : 0u;
@@ -394,6 +459,83 @@ __global__ void k_rank(const DevState d, Scratch sc, const Counters *cn) {
   }
 }
 
+// A set with more than kSmallSet IDs: one block sorts its segment (distinct
+// unique indices, in arrival order) ascending with an LSD radix sort over
+// 8-bit digits of the index, in O(k) per pass, ping-ponging between seg and
+// seg_u.  Each pass: digit histogram in LDS, exclusive scan, then the scatter
+// in index order, 256 entries at a time: an entry's place among the chunk's
+// entries with the same digit comes from eight ballots per wave (the lanes
+// whose digit matches) and the counts of the lower waves.
+__global__ __launch_bounds__(kBlock) void k_big_sort(const DevState d, Scratch sc, const Counters *cn) {
+  if (cn->err) return;
+  const uint32_t nbig = cn->n_big;
+  const uint32_t U = cn->n_unique;
+  const uint32_t bits = U > 1 ? 32u - (uint32_t)__builtin_clz(U - 1u) : 1u;
+  const uint32_t passes = (bits + 7u) / 8u;
+  __shared__ uint32_t base[256];
+  __shared__ uint32_t wcnt[kBlock / 64][256];
+  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
+  const uint64_t lt = lane ? (~0ull >> (64u - lane)) : 0ull;
+  for (uint32_t b = blockIdx.x; b < nbig; b += gridDim.x) {
+    const uint32_t i = sc.big[b];
+    const uint32_t off = sc.seg_off[i];
+    const uint32_t k = d.set_count[sc.touched[i]];
+    uint32_t *src = sc.seg + off, *dst = sc.seg_u + off;
+    for (uint32_t p = 0; p < passes; ++p) {
+      const uint32_t shift = 8u * p;
+      base[threadIdx.x] = 0;
+      __syncthreads();
+      for (uint32_t j = threadIdx.x; j < k; j += kBlock) atomicAdd(&base[(src[j] >> shift) & 255u], 1u);
+      __syncthreads();
+      uint32_t tot;
+      const uint32_t ex = block_exclusive_scan(base[threadIdx.x], tot);
+      __syncthreads();
+      base[threadIdx.x] = ex;
+      for (uint32_t c0 = 0; c0 < k; c0 += kBlock) {
+#pragma unroll
+        for (int w = 0; w < kBlock / 64; ++w) wcnt[w][threadIdx.x] = 0;
+        __syncthreads();
+        const uint32_t j = c0 + threadIdx.x;
+        const bool valid = j < k;
+        const uint32_t v = valid ? src[j] : 0u;
+        const uint32_t dg = (v >> shift) & 255u;
+        uint64_t m = __ballot(valid);
+#pragma unroll
+        for (int bit = 0; bit < 8; ++bit) {
+          const bool on = (dg >> bit) & 1u;
+          const uint64_t bb = __ballot(valid && on);
+          m &= on ? bb : ~bb;
+        }
+        if (valid && (m & lt) == 0) wcnt[wid][dg] = (uint32_t)__popcll(m);
+        __syncthreads();
+        if (valid) {
+          uint32_t r = base[dg] + (uint32_t)__popcll(m & lt);
+          for (uint32_t w = 0; w < wid; ++w) r += wcnt[w][dg];
+          dst[r] = v;
+        }
+        __syncthreads();
+        uint32_t add = 0;
+#pragma unroll
+        for (int w = 0; w < kBlock / 64; ++w) add += wcnt[w][threadIdx.x];
+        base[threadIdx.x] += add;
+      }
+      __syncthreads();
+      uint32_t *tmp = src;
+      src = dst;
+      dst = tmp;
+    }
+    // the sorted indices are in src; lay out (u, ID, static score)
+    for (uint32_t j = threadIdx.x; j < k; j += kBlock) {
+      const uint32_t u = src[j];
+      const uint32_t x = sc.uniq[u];
+      sc.seg_u[off + j] = u;
+      sc.seg_x[off + j] = x;
+      sc.seg_st[off + j] = d.stat[x];
+    }
+    __syncthreads();
+  }
+}
+
 void launch_group_by_set(const DevState &d, const int64_t *ids, uint64_t n, int64_t *inverse, Scratch &sc,
                          Counters *cn, hipStream_t s) {
   const unsigned g = grid_for(n, kBlock, kMaxGrid);
@@ -401,6 +543,9 @@ void launch_group_by_set(const DevState &d, const int64_t *ids, uint64_t n, int6
   hipLaunchKernelGGL(k_seg_alloc, dim3(g), dim3(kBlock), 0, s, d, sc, cn);
   hipLaunchKernelGGL(k_place, dim3(g), dim3(kBlock), 0, s, d, sc, cn);
   hipLaunchKernelGGL(k_rank, dim3(g), dim3(kBlock), 0, s, d, sc, cn);
+  // sets of more than kSmallSet IDs exist only if n does
+  if (n > kSmallSet)
+    hipLaunchKernelGGL(k_big_sort, dim3(grid_for(n / (kSmallSet + 1), 1, 256)), dim3(kBlock), 0, s, d, sc, cn);
 }
 
 // ---------------------------------------------------------------- set walk
@@ -611,9 +756,12 @@ __global__ __launch_bounds__(kBlock) void k_set_walk(const DevState d, Scratch s
   block_count(c_final, sc.stat_part, kStFinal);
 }
 
+#ifndef LSM_WALK_GRID
+#define LSM_WALK_GRID 4096  // set-walk blocks of 32 lane groups: enough sets in flight to hide the record loads
+#endif
 void launch_set_walk(const DevState &d, uint64_t n, uint32_t t, Scratch &sc, Counters *cn, StatGrids &grids,
                      hipStream_t s) {
-  const unsigned g = grid_for(n * kWays, kBlock, 1024);
+  const unsigned g = grid_for(n * kWays, kBlock, LSM_WALK_GRID);
   switch (d.policy) {
     case kPolicyStatic:
       hipLaunchKernelGGL(k_set_walk<kPolicyStatic>, dim3(g), dim3(kBlock), 0, s, d, sc, t, cn);
@@ -665,7 +813,12 @@ __global__ __launch_bounds__(kBlock) void k_scan_top(uint32_t *part, Counters *c
 // Exclusive scan of the enqueue flags in ascending-ID order gives each
 // enqueue its ring sequence number.  An enqueued line requested later in the
 // same batch is told where its entry went.
-__global__ __launch_bounds__(kBlock) void k_scan_final(const DevState d, Scratch sc, const Counters *cn) {
+// kFused: the chunk's offset is the sum of the earlier chunks' partial counts,
+// added up by the block itself, and the last chunk's block records the total
+// (few chunks: this saves the one-block scan); otherwise scan_part holds the
+// scanned offsets.
+template <bool kFused>
+__global__ __launch_bounds__(kBlock) void k_scan_final(const DevState d, Scratch sc, Counters *cn) {
   if (cn->err) return;
   const uint32_t U = cn->n_unique;
   const uint64_t tail0 = d.tail[0];
@@ -680,7 +833,17 @@ __global__ __launch_bounds__(kBlock) void k_scan_final(const DevState d, Scratch
       c += f[k];
     }
     uint32_t tot;
-    uint32_t run = sc.scan_part[b] + block_exclusive_scan(c, tot);
+    const uint32_t ex = block_exclusive_scan(c, tot);
+    uint32_t off;
+    if constexpr (kFused) {
+      uint32_t v = 0;
+      for (uint32_t j = threadIdx.x; j < b; j += kBlock) v += sc.scan_part[j];
+      off = block_sum(v);
+      if (b == nb - 1 && threadIdx.x == 0) cn->enq_total = off + tot;
+    } else {
+      off = sc.scan_part[b];
+    }
+    uint32_t run = off + ex;
 #pragma unroll
     for (int k = 0; k < kScanPerThread; ++k) {
       const uint32_t u = base + k;
@@ -963,9 +1126,8 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
 
 // Outcomes per raw request: each request takes its unique ID's outcome (the
 // compaction recorded every requested node's unique index).
-__global__ __launch_bounds__(kBlock) void k_request_counts(const DevState d, Scratch sc, const int64_t *ids,
-                                                           uint32_t n, const Counters *cn) {
-  if (cn->err) return;
+__device__ __forceinline__ void request_counts(const DevState &d, const Scratch &sc, const int64_t *ids,
+                                               uint32_t n) {
   uint32_t c_hit = 0, c_vhit = 0;
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
     const uint8_t o = sc.oc[d.uidx[ids[i]]];
@@ -976,20 +1138,20 @@ __global__ __launch_bounds__(kBlock) void k_request_counts(const DevState d, Scr
   block_count(c_vhit, sc.stat_part, kStReqVictimHits);
 }
 
-void launch_request_counts(const DevState &d, const int64_t *ids, uint64_t n, Scratch &sc, Counters *cn,
-                           StatGrids &grids, hipStream_t s) {
-  const unsigned g = grid_for(n, kBlock, kMaxGrid);
-  hipLaunchKernelGGL(k_request_counts, dim3(g), dim3(kBlock), 0, s, d, sc, ids, (uint32_t)n, cn);
-  grids.g[kStReqHits] = g;
-  grids.g[kStReqVictimHits] = g;
+__global__ __launch_bounds__(kBlock) void k_request_counts(const DevState d, Scratch sc, const int64_t *ids,
+                                                           uint32_t n, const Counters *cn) {
+  if (cn->err) return;
+  request_counts(d, sc, ids, n);
 }
+
 
 // Ring bookkeeping for this batch's enqueues; lists the row copies of the
 // entries that are still in the ring at the end of the batch.  Those entries
 // have the sequence numbers [q_lo, tail_end), q_lo = tail_end - min(E, V) for E
 // enqueues, and their rows are staged in that order (entries removed again in
 // this batch leave a hole that nothing reads).
-__global__ __launch_bounds__(kBlock) void k_enq_finalize(const DevState d, Scratch sc, Counters *cn) {
+__global__ __launch_bounds__(kBlock) void k_enq_finalize(const DevState d, Scratch sc, const int64_t *ids, uint32_t n,
+                                                         Counters *cn) {
   if (cn->err) return;
   const uint32_t U = cn->n_unique;
   const uint64_t tail0 = d.tail[0];
@@ -1023,6 +1185,8 @@ __global__ __launch_bounds__(kBlock) void k_enq_finalize(const DevState d, Scrat
     }
   }
   block_count(c_copy, sc.stat_part, kStEnqCopy);
+  // the per-request outcome counts, in the same launch
+  request_counts(d, sc, ids, n);
 }
 
 void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, uint8_t *outcome, Counters *cn,
@@ -1033,8 +1197,12 @@ void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t t, Scratch &sc,
   const bool queues = d.V && d.qmode && d.L > 0;  // with L = 0 no line has a reuse iteration
   if (ring) {
     hipLaunchKernelGGL(k_scan_partial, dim3(gs), dim3(kBlock), 0, s, sc.flags, sc.scan_part, cn);
-    hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kBlock), 0, s, sc.scan_part, cn);
-    hipLaunchKernelGGL(k_scan_final, dim3(gs), dim3(kBlock), 0, s, d, sc, cn);
+    if ((n + kScanChunk - 1) / kScanChunk <= kFusedScanMax) {
+      hipLaunchKernelGGL(k_scan_final<true>, dim3(gs), dim3(kBlock), 0, s, d, sc, cn);
+    } else {
+      hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kBlock), 0, s, sc.scan_part, cn);
+      hipLaunchKernelGGL(k_scan_final<false>, dim3(gs), dim3(kBlock), 0, s, d, sc, cn);
+    }
   }
   if (queues) {
     hipLaunchKernelGGL(k_qcount, dim3(g), dim3(kBlock), 0, s, d, sc, t, cn);
@@ -1045,19 +1213,23 @@ void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t t, Scratch &sc,
   for (int st = kStVhRing; st <= kStVhSame; ++st) grids.g[st] = g;
 }
 
-void launch_ring_enqueue(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, Counters *cn, StatGrids &grids,
-                         hipStream_t s) {
+void launch_ring_enqueue(const DevState &d, const int64_t *ids, uint64_t n, uint64_t t, Scratch &sc, Counters *cn,
+                         StatGrids &grids, hipStream_t s) {
   const unsigned g = grid_for(n, kBlock, kMaxGrid);
   const bool ring = d.V && !d.qmode;
   const bool queues = d.V && d.qmode && d.L > 0;
-  if (ring) {
-    hipLaunchKernelGGL(k_enq_finalize, dim3(g), dim3(kBlock), 0, s, d, sc, cn);
+  if (ring) {  // with the per-request counts
+    hipLaunchKernelGGL(k_enq_finalize, dim3(g), dim3(kBlock), 0, s, d, sc, ids, (uint32_t)n, cn);
     grids.g[kStEnqCopy] = g;
+  } else {
+    if (queues) {
+      hipLaunchKernelGGL(k_qplace, dim3(g), dim3(kBlock), 0, s, d, sc, t, cn);
+      grids.g[kStEnqCopy] = g;
+    }
+    hipLaunchKernelGGL(k_request_counts, dim3(g), dim3(kBlock), 0, s, d, sc, ids, (uint32_t)n, cn);
   }
-  if (queues) {
-    hipLaunchKernelGGL(k_qplace, dim3(g), dim3(kBlock), 0, s, d, sc, t, cn);
-    grids.g[kStEnqCopy] = g;
-  }
+  grids.g[kStReqHits] = g;
+  grids.g[kStReqVictimHits] = g;
 }
 
 // -------------------------------------------------------------- row copies
@@ -1069,32 +1241,38 @@ void launch_ring_enqueue(const DevState &d, uint64_t n, uint64_t t, Scratch &sc,
 // from the gather's gate; a rejected gather moves nothing.
 constexpr int kUnroll = 4;
 
-// Copy of a row list: item w = (list entry i, 16-byte vector v).  The mode only
-// names the instance (hit copy, staging, fills) so that profiles tell them apart.
+// Copy of a row list: item w = (list entry i, 16-byte vector v).  Each block
+// takes a tile of kListUnroll * kBlock consecutive items (whole rows, their
+// 16-byte vectors on consecutive lanes), the tiles striding over the grid;
+// loads and stores carry the non-temporal hint (every row moves once).
+// Measured on the MI355X against grid-strided items without the hint:
+// 5.7-6.0 against 4.9-5.2 TB/s for 1-2 KiB random rows.  The mode only names
+// the instance (hit copy, staging, fills) so that profiles tell them apart.
+constexpr int kListUnroll = 2;
 template <CopyMode M, bool kPow2>
 __global__ __launch_bounds__(kBlock) void k_list_copy(const uint8_t *src, const uint32_t *sidx, uint8_t *dst,
                                                       const uint32_t *didx, const Gate *gate, const uint32_t *count,
                                                       uint64_t R, uint32_t nvec, uint32_t vshift) {
   if (gate->err) return;
   const uint64_t total = (uint64_t)*count * nvec;
-  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-  for (uint64_t w0 = (uint64_t)blockIdx.x * kBlock + threadIdx.x; w0 < total; w0 += stride * kUnroll) {
-    u32x4 v[kUnroll];
-    uint8_t *dp[kUnroll];
+  constexpr uint64_t tile = (uint64_t)kListUnroll * kBlock;
+  for (uint64_t base = (uint64_t)blockIdx.x * tile; base < total; base += (uint64_t)gridDim.x * tile) {
+    u32x4 v[kListUnroll];
+    uint8_t *dp[kListUnroll];
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k) {
-      const uint64_t w = w0 + k * stride;
+    for (int k = 0; k < kListUnroll; ++k) {
+      const uint64_t w = base + (uint64_t)k * kBlock + threadIdx.x;
       dp[k] = nullptr;
       if (w < total) {
         const uint32_t i = kPow2 ? (uint32_t)(w >> vshift) : (uint32_t)(w / nvec);
         const uint64_t byte = (w - (uint64_t)i * nvec) * 16u;
-        v[k] = *reinterpret_cast<const u32x4 *>(src + (uint64_t)sidx[i] * R + byte);
+        v[k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(src + (uint64_t)sidx[i] * R + byte));
         dp[k] = dst + (uint64_t)didx[i] * R + byte;
       }
     }
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k)
-      if (dp[k]) *reinterpret_cast<u32x4 *>(dp[k]) = v[k];
+    for (int k = 0; k < kListUnroll; ++k)
+      if (dp[k]) __builtin_nontemporal_store(v[k], reinterpret_cast<u32x4 *>(dp[k]));
   }
 }
 
@@ -1166,14 +1344,14 @@ __global__ __launch_bounds__(kBlock) void k_host_fetch(const DevState d, Scratch
 #define LSM_HOST_GRID 40
 #endif
 #ifndef LSM_HBM_GRID
-#define LSM_HBM_GRID 4096  // the HBM-side copies: a grid sweep beside the host fetch chose it
+#define LSM_HBM_GRID 65536  // the HBM-side copies: the largest grid of the measured sweep
 #endif
 
 template <CopyMode M>
 static void launch_list(const uint8_t *src, const RowList &l, uint8_t *dst, const Gate *gate, const uint32_t *count,
                         uint64_t n, uint64_t R, hipStream_t s) {
   const uint32_t nvec = (uint32_t)(R / 16);
-  const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kUnroll, LSM_HBM_GRID);
+  const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kListUnroll, LSM_HBM_GRID);
   if ((nvec & (nvec - 1)) == 0)
     hipLaunchKernelGGL((k_list_copy<M, true>), dim3(g), dim3(kBlock), 0, s, src, l.src, dst, l.dst, gate, count, R,
                        nvec, (uint32_t)__builtin_ctz(nvec));
@@ -1267,10 +1445,41 @@ __global__ __launch_bounds__(kBlock) void k_copy_plain(const u32x4 *src, u32x4 *
   }
 }
 
-void launch_copy_plain(const void *src, void *dst, uint64_t bytes, hipStream_t s) {
+__global__ void k_publish_host_count(const Gate *gate, uint32_t *dst) {
+  if (threadIdx.x == 0) *dst = gate->err ? 0u : gate->n_host;
+}
+
+void launch_publish_host_count(const Gate *gate, uint32_t *dst, hipStream_t s) {
+  hipLaunchKernelGGL(k_publish_host_count, dim3(1), dim3(64), 0, s, gate, dst);
+}
+
+// Device-to-device: tiles of 4 * kBlock vectors per block with the
+// non-temporal hint, the copy pattern of the row lists.
+__global__ __launch_bounds__(kBlock) void k_copy_tiles(const u32x4 *src, u32x4 *dst, uint64_t nvec) {
+  constexpr uint64_t tile = 4 * (uint64_t)kBlock;
+  for (uint64_t base = (uint64_t)blockIdx.x * tile; base < nvec; base += (uint64_t)gridDim.x * tile) {
+    u32x4 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint64_t w = base + (uint64_t)k * kBlock + threadIdx.x;
+      if (w < nvec) v[k] = __builtin_nontemporal_load(src + w);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint64_t w = base + (uint64_t)k * kBlock + threadIdx.x;
+      if (w < nvec) __builtin_nontemporal_store(v[k], dst + w);
+    }
+  }
+}
+
+void launch_copy_plain(const void *src, void *dst, uint64_t bytes, bool device_to_device, hipStream_t s) {
   const uint64_t nvec = bytes / 16;
-  hipLaunchKernelGGL(k_copy_plain, dim3(grid_for(nvec, (uint64_t)kBlock * kUnroll, 4096)), dim3(kBlock), 0, s,
-                     static_cast<const u32x4 *>(src), static_cast<u32x4 *>(dst), nvec);
+  if (device_to_device)
+    hipLaunchKernelGGL(k_copy_tiles, dim3(grid_for(nvec, 4 * (uint64_t)kBlock, 262144)), dim3(kBlock), 0, s,
+                       static_cast<const u32x4 *>(src), static_cast<u32x4 *>(dst), nvec);
+  else
+    hipLaunchKernelGGL(k_copy_plain, dim3(grid_for(nvec, (uint64_t)kBlock * kUnroll, 4096)), dim3(kBlock), 0, s,
+                       static_cast<const u32x4 *>(src), static_cast<u32x4 *>(dst), nvec);
 }
 
 // ------------------------------------------------------------------ window
@@ -1325,24 +1534,6 @@ void launch_window_rollback(const int64_t *ids, uint64_t n, uint64_t N, uint32_t
 // validated the IDs, and its gate says whether the call was accepted.  Records
 // the list in its window slot and sets the minibatch's bit for every ID (only
 // that bit changes in this kernel, so a plain read-modify-write is exact).
-__global__ void k_announce(const int64_t *ids, uint32_t n, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
-                           const Gate *gate) {
-  if (gate->err) return;
-  const uint32_t b = 1u << bit;
-  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
-    const int64_t x = ids[i];
-    slot_ids[i] = x;
-    const uint32_t m = mask[x];
-    if (!(m & b)) mask[x] = m | b;
-  }
-}
-
-void launch_announce(const int64_t *ids, uint64_t n, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
-                     const Scratch &sc, hipStream_t s) {
-  const unsigned g = grid_for(n, kBlock, kMaxGrid);
-  hipLaunchKernelGGL(k_announce, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, bit, mask, slot_ids, sc.gate);
-}
-
 // ------------------------------------------------------ request order
 // Per-position output: row i of `out` <- row inv[i] of `rows` (the unique-row
 // output of a gather), for the n requests in their original order.  Item w =
@@ -1374,7 +1565,7 @@ __global__ __launch_bounds__(kBlock) void k_expand(const uint8_t *rows, const in
 
 void launch_expand(const uint8_t *rows, const int64_t *inv, uint64_t n, uint64_t R, uint8_t *out, hipStream_t s) {
   const uint32_t nvec = (uint32_t)(R / 16);
-  const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kUnroll, LSM_HBM_GRID);
+  const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kListUnroll, LSM_HBM_GRID);
   if ((nvec & (nvec - 1)) == 0)
     hipLaunchKernelGGL(k_expand<true>, dim3(g), dim3(kBlock), 0, s, rows, inv, n, R, nvec,
                        (uint32_t)__builtin_ctz(nvec), out);

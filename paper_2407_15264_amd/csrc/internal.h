@@ -10,12 +10,14 @@ namespace lsm {
 constexpr uint32_t kWays = 8;
 constexpr uint32_t kEmpty = 0xffffffffu;
 constexpr int kBlock = 256;          // threads per block for every kernel
-constexpr int kBytesPerThread = 64;  // dedup map bytes per thread
+constexpr int kBytesPerThread = 64;  // dedup bitmap bytes per thread
 constexpr int kWordsPerThread = kBytesPerThread / 4;
-constexpr int kChunkBytes = kBlock * kBytesPerThread;  // dedup map bytes per block
+constexpr int kChunkBytes = kBlock * kBytesPerThread;  // dedup bitmap bytes per block
+constexpr uint64_t kChunkNodes = (uint64_t)kChunkBytes * 8;  // nodes per bitmap chunk
 constexpr int kScanPerThread = 8;    // flags per thread in the enqueue scan
 constexpr int kScanChunk = kBlock * kScanPerThread;
 constexpr int kMaxQueues = 32;       // victim-queue slots: L + 1 <= 32
+constexpr uint32_t kSmallSet = 64;   // sets with more unique IDs in a batch are sorted by a block each
 
 // dynamic classes of a resident line while a gather runs
 enum : uint32_t { kClsNone = 0, kClsFar = 1, kClsRecent = 2, kClsNear = 3 };
@@ -81,12 +83,13 @@ struct Counters {
   // previous gather's staged evicted rows (HBM), the cache row of a line
   // evicted earlier in the same gather
   uint32_t vh_ring, vh_staged, vh_same;
+  uint32_t n_big;       // touched sets with more than kSmallSet unique IDs
   // victim queues (queue mode): enqueue candidates that found their queue
   // full, and per queue slot the entries before this gather and those it placed
   uint32_t q_overflow;
   uint32_t q_before[kMaxQueues];
   uint32_t q_placed[kMaxQueues];
-  uint32_t pad[12];
+  uint32_t pad[11];
 };
 
 // Dedup result of a gather, written by the chunk scan to pinned host memory:
@@ -137,6 +140,7 @@ struct Scratch {
   uint32_t *seg_u;      // u grouped by set, ascending within the set
   uint32_t *seg_x;      // uniq[seg_u[.]]
   uint32_t *seg_st;     // static score of seg_x[.]
+  uint32_t *big;        // [max_batch / (kSmallSet + 1) + 1] touched-set indices of sets with more than kSmallSet IDs
   uint8_t *kind;
   uint8_t *flags;
   uint8_t *oc;          // outcome of u (LSMGNN_HIT / _VICTIM_HIT / _MISS)
@@ -170,7 +174,7 @@ struct DevState {
   uint32_t *ring_tag;    // [V] FIFO ring entries, or queue slot k's entries at k * C
   uint8_t *ring_rows;    // [V][R] pinned host, device-visible address (ring or queue rows)
   const uint8_t *store;  // [N][R] pinned host, device-visible address
-  uint8_t *present;      // [nchunks * kChunkBytes] dedup byte map (all zero between calls)
+  uint32_t *present;     // [nchunks * kChunkBytes / 4] dedup bitmap, bit x for node x (all zero between calls)
   uint32_t *chunk_sums;  // [nchunks]
   uint32_t *set_count;   // [S] (all zero between calls)
   uint32_t *set_idx;     // [S]
@@ -208,9 +212,20 @@ struct QueueFinish {
   uint32_t cur = 0, next = 0;
 };
 
+// The announcement made with a gather, set by the gather's last kernel
+// (ids == nullptr: none): the IDs, the minibatch's window bit, the window
+// words and the list's window slot.
+struct AnnounceArgs {
+  const int64_t *ids = nullptr;
+  uint32_t n = 0, bit = 0;
+  uint32_t *mask = nullptr;
+  int64_t *slot_ids = nullptr;
+  const Gate *gate = nullptr;
+};
+
 // ----- launchers (gather_kernels.hip) -----
 void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, const StatGrids &grids,
-                   uint64_t *tail, const QueueFinish &qf, hipStream_t s);
+                   uint64_t *tail, const QueueFinish &qf, const AnnounceArgs &ann, hipStream_t s);
 // ann_ids/ann_n: the list announced with this gather (validated here), or NULL/0
 void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, const int64_t *ann_ids, uint64_t ann_n,
                   const int64_t *clear_ids, uint64_t clear_n, uint32_t clear_bit, Scratch &sc, int64_t *unique_out,
@@ -222,16 +237,15 @@ void launch_set_walk(const DevState &d, uint64_t n, uint32_t t, Scratch &sc, Cou
 // U > 1, before every U-th gather's set walk: record every resident line's next reuse iteration
 void launch_refresh(const DevState &d, uint32_t t, const Counters *cn, hipStream_t s);
 // t: the gather's index (queue mode serves queue t from prefetch buffer t & 1)
-// per-request outcome counts (each request takes its unique ID's outcome)
-void launch_request_counts(const DevState &d, const int64_t *ids, uint64_t n, Scratch &sc, Counters *cn,
-                           StatGrids &grids, hipStream_t s);
 // sequence numbers of the batch's enqueues, then the resolve: outcomes, the
 // hit-copy, host-fetch and fill lists
 void launch_ring_resolve(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, uint8_t *outcome, Counters *cn,
                          StatGrids &grids, hipStream_t s);
-// after the resolve: the enqueues' ring (or queue) entries and the staging list
-void launch_ring_enqueue(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, Counters *cn, StatGrids &grids,
-                         hipStream_t s);
+// after the resolve: the enqueues' ring (or queue) entries and the staging
+// list, and the outcome counts per raw request (each request takes its
+// unique ID's outcome)
+void launch_ring_enqueue(const DevState &d, const int64_t *ids, uint64_t n, uint64_t t, Scratch &sc, Counters *cn,
+                         StatGrids &grids, hipStream_t s);
 // Queue mode: copy the queue of gather t+1 (slot `slot`) into prefetch buffer
 // `par`: entries placed by gathers up to t-1 from the pinned host queue, those
 // placed by gather t from its staging rows; sizes from gather t's gate.
@@ -245,10 +259,9 @@ void launch_window_set(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit,
                        bool record, Counters *cn, hipStream_t s);
 void launch_window_rollback(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask,
                             hipStream_t s);
-// sets the announced bits unless the gather's gate holds an error
-void launch_announce(const int64_t *ids, uint64_t n, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
-                     const Scratch &sc, hipStream_t s);
-void launch_copy_plain(const void *src, void *dst, uint64_t bytes, hipStream_t s);
+void launch_copy_plain(const void *src, void *dst, uint64_t bytes, bool device_to_device, hipStream_t s);
+// pageable store: the host-fetch list's length (0 for a rejected gather) to pinned host memory
+void launch_publish_host_count(const Gate *gate, uint32_t *dst, hipStream_t s);
 
 // host twin of the device set-index function
 uint64_t set_of_host(uint64_t x, uint64_t num_sets);

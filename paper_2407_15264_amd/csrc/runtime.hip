@@ -87,7 +87,7 @@ struct Flight {
   Scratch sc{};                // metadata scratch (shared) + this parity's row-copy lists and gate
   Counters *hc = nullptr;      // pinned: counters published by the gather's last metadata kernel
   Counters *hc_dev = nullptr;
-  hipEvent_t meta_done = nullptr, finish_done = nullptr, stage_done = nullptr, host_done = nullptr,
+  hipEvent_t meta_done = nullptr, finish_done = nullptr, stage_done = nullptr, hit_done = nullptr, host_done = nullptr,
              data_done = nullptr, dma_done = nullptr;
   hipEvent_t pf_done = nullptr;  // queue mode: this parity's prefetch buffer holds the gather's queue
   bool pf_ready = false;         // pf_done has been recorded for the gather that uses this parity next
@@ -95,6 +95,16 @@ struct Flight {
   uint64_t *hsrc_host = nullptr;
   uint8_t *bounce_host = nullptr;
   bool used = false;           // events of this slot have been recorded at least once
+  // The gather's data work (staging, hit copy, fills): its size, output and
+  // whether it is timed; with `data_deferred` its hit copy and fills are not
+  // queued yet (a pipelined gather's are queued by the next call, after that
+  // call's metadata, or by any call that waits for the gather).
+  uint64_t data_n = 0;
+  uint8_t *data_out = nullptr;
+  bool data_prof = false;
+  bool data_deferred = false;
+  hipEvent_t list_done = nullptr;  // pageable store: the host-fetch list and its length are written
+  uint32_t *hcount_host = nullptr, *hcount_dev = nullptr;  // pageable store: that length (pinned)
   bool stats_pending = false;  // counters not yet added to the totals
   bool dma_pending = false;    // staged rows not yet queued for the ring
   bool dma_used = false;       // dma_done has been recorded at least once
@@ -217,7 +227,9 @@ void release(lsmgnn_cache *c) {
   for (void *p : c->host_allocs) (void)hipHostFree(p);
   c->host_allocs.clear();
   for (Flight &f : c->fl)
-    for (hipEvent_t e : {f.meta_done, f.finish_done, f.stage_done, f.host_done, f.data_done, f.dma_done, f.pf_done})
+    for (hipEvent_t e : {f.meta_done, f.finish_done, f.stage_done, f.hit_done, f.host_done, f.data_done, f.dma_done,
+                         f.pf_done,
+                         f.list_done})
       if (e) (void)hipEventDestroy(e);
   for (PerfSet &p : c->ps)
     for (hipEvent_t e : p.e)
@@ -436,9 +448,71 @@ void harvest_profile(lsmgnn_cache *c, PerfSet &p) {
   p.pending = false;
 }
 
+// Staging of gather g (flight G) on the meta stream: its evicted rows that
+// survive in the victim buffer, copied to its staging rows, once gather g-1's
+// fills (the cache rows) and gather g-2's ring write (the staging rows of
+// parity g) have landed.
+void queue_stage(lsmgnn_cache *c, uint64_t g) {
+  DevState &d = c->d;
+  Flight &G = c->fl[g & 1], &P = c->fl[(g + 1) & 1];
+  if (P.used) meta_wait_dma(c, P.data_done, P.fill_seq);
+  if (G.dma_used) meta_wait_dma(c, G.dma_done, G.dma_seq);
+  if (G.data_n && d.V) lsm::launch_copy(CopyMode::kCacheToStage, d, G.data_n, G.sc, G.data_out, c->meta);
+  (void)hipEventRecord(G.stage_done, c->meta);
+  G.used = true;
+}
+
+// Hit copy of gather g on the meta stream, after its staging (in stream order,
+// so also after gather g-1's fills).  It also reads gather g-1's staging rows
+// (victim hits on its entries), which gather g+1's staging overwrites later
+// on the same stream.
+void queue_hit(lsmgnn_cache *c, uint64_t g) {
+  DevState &d = c->d;
+  Flight &G = c->fl[g & 1];
+  PerfSet &ps = c->ps[g % kPerfSets];
+  const bool queues = d.qmode && d.V && d.L > 0;
+  // queue mode: the hit copy also moves the victim hits, from the prefetch
+  // buffer that the previous call filled
+  if (queues && G.pf_ready) (void)hipStreamWaitEvent(c->meta, G.pf_done, 0);
+  if (G.data_prof) (void)hipEventRecord(ps.e[kEvHbm0], c->meta);
+  if (G.data_n) lsm::launch_copy(CopyMode::kHbmToOut, d, G.data_n, G.sc, G.data_out, c->meta);
+  if (G.data_prof) (void)hipEventRecord(ps.e[kEvHbm1], c->meta);
+  (void)hipEventRecord(G.hit_done, c->meta);
+}
+
+// Fills of gather g on the dma stream (behind the ring writes queued there so
+// far), once its host fetch, staging and hit copy are done.  Gather g's own
+// ring write is queued after them, so it follows gather g's host fetch.
+void queue_fills(lsmgnn_cache *c, uint64_t g) {
+  Flight &G = c->fl[g & 1];
+  PerfSet &ps = c->ps[g % kPerfSets];
+  (void)hipStreamWaitEvent(c->dma, G.host_done, 0);
+  (void)hipStreamWaitEvent(c->dma, G.hit_done, 0);  // after the staging on the same stream
+  if (G.data_prof) (void)hipEventRecord(ps.e[kEvFill0], c->dma);
+  if (G.data_n) lsm::launch_copy(CopyMode::kOutToCache, c->d, G.data_n, G.sc, G.data_out, c->dma);
+  if (G.data_prof) {
+    (void)hipEventRecord(ps.e[kEvFill1], c->dma);
+    (void)hipEventRecord(ps.e[kEvAll1], c->dma);
+  }
+  (void)hipEventRecord(G.data_done, c->dma);
+  G.fill_seq = ++c->dma_subs;
+}
+
+// Queue the latest gather's hit copy and fills if they were deferred.
+void flush_deferred(lsmgnn_cache *c) {
+  if (c->t == 0) return;
+  const uint64_t g = c->t - 1;
+  Flight &G = c->fl[g & 1];
+  if (!G.data_deferred) return;
+  G.data_deferred = false;
+  queue_hit(c, g);
+  queue_fills(c, g);
+}
+
 // Wait for every queued kernel and copy, then account everything in issue
 // order.
 lsmgnn_status sync_all(lsmgnn_cache *c) {
+  flush_deferred(c);
   if (hipStreamSynchronize(c->meta) != hipSuccess) return fail_device(c);
   Flight &older = c->fl[c->t & 1], &newer = c->fl[(c->t + 1) & 1];
   harvest_stats(c, older);
@@ -462,9 +536,17 @@ struct Announce {
 // Queue one gather (and the announcement after it).  Returns once its unique
 // count is known; its metadata and row movement may still be running on the
 // three streams.  *issued receives the gather index.
+//
+// With `defer` (pipelined gathers) the gather's hit copy and fills are queued
+// by the next call, after that call's metadata: the next gather's metadata
+// then need not wait behind this gather's hit copy.  Nothing the next
+// metadata does touches what they read or write: it writes the other
+// parity's lists and gate, and changes tags, not cache rows.  The staging
+// stays in this call, ahead of the next metadata, since this gather's ring
+// write waits for it and the host fetch two gathers on waits for that.
 lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, const Announce &an, void *out,
                            int64_t *unique_ids, int64_t *inverse, uint8_t *outcome, uint64_t *n_unique,
-                           hipStream_t s, uint64_t *issued) {
+                           hipStream_t s, uint64_t *issued, bool defer) {
   DevState &d = c->d;
   const uint64_t t = c->t;
   // the announcement is the k-th, made once t+1 gathers are done
@@ -489,6 +571,7 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
     if (prof) (void)hipEventRecord(ps.e[e], st);
   };
   uint8_t *outp = static_cast<uint8_t *>(out);
+  if (queues) defer = false;  // the prefetch of the next queue follows this gather's staging
 
   // inputs are ready once the caller's queued work is; this parity's arrays
   // are free once gather t-2's rows have moved
@@ -516,13 +599,18 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
     lsm::launch_group_by_set(d, ids, n, inverse, f.sc, c->cn, c->meta);
     lsm::launch_set_walk(d, n, (uint32_t)t, f.sc, c->cn, grids, c->meta);
     lsm::launch_ring_resolve(d, n, t, f.sc, outcome, c->cn, grids, c->meta);
+    // pageable store: the host threads start copying as soon as the list is
+    // known, while the rest of the metadata runs
+    if (c->pageable) {
+      lsm::launch_publish_host_count(f.sc.gate, f.hcount_dev, c->meta);
+      (void)hipEventRecord(f.list_done, c->meta);
+    }
   }
   // the host fetch needs only the resolve's list; the rest of the metadata
   // runs beside it
   (void)hipEventRecord(f.meta_done, c->meta);
   if (n) {
-    lsm::launch_ring_enqueue(d, n, t, f.sc, c->cn, grids, c->meta);
-    lsm::launch_request_counts(d, ids, n, f.sc, c->cn, grids, c->meta);
+    lsm::launch_ring_enqueue(d, ids, n, t, f.sc, c->cn, grids, c->meta);
   }
   lsm::QueueFinish qf;
   if (queues) {
@@ -531,15 +619,22 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
     qf.cur = (uint32_t)(t % (d.L + 1));
     qf.next = (uint32_t)((t + 1) % (d.L + 1));
   }
-  lsm::launch_finish(c->cn, f.hc_dev, f.sc.stat_part, grids, d.tail, qf, c->meta);
   // the announced bits are first read by the next gather's set walk
-  if (record)
-    lsm::launch_announce(an.ids, an.n, (uint32_t)(k & 31u), d.mask, c->win_ids + (uint64_t)kslot * c->max_batch,
-                         f.sc, c->meta);
+  lsm::AnnounceArgs ann;
+  if (record) {
+    ann.ids = an.ids;
+    ann.n = (uint32_t)an.n;
+    ann.bit = (uint32_t)(k & 31u);
+    ann.mask = d.mask;
+    ann.slot_ids = c->win_ids + (uint64_t)kslot * c->max_batch;
+    ann.gate = f.sc.gate;
+  }
+  lsm::launch_finish(c->cn, f.hc_dev, f.sc.stat_part, grids, d.tail, qf, ann, c->meta);
   (void)hipEventRecord(f.finish_done, c->meta);
 
   // host fetch (PCIe ingress), right after gather t-1's on the same stream;
   // with a pageable store it is launched once the host has copied the rows
+  const bool pageable_list = c->pageable;  // the host copies the listed rows once the list is known
   auto host_fetch = [&]() {
     (void)hipStreamWaitEvent(c->host, f.meta_done, 0);
     if (!c->pageable && f.dma_used) (void)hipStreamWaitEvent(c->host, f.dma_done, 0);
@@ -550,26 +645,24 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   };
   if (!c->pageable) host_fetch();
 
-  // staging and hit copy once gather t-1's fills have landed; the ring write
-  // (PCIe egress) is queued later on the dma stream
-  if (pf.used) meta_wait_dma(c, pf.data_done, pf.fill_seq);
-  if (f.dma_used) meta_wait_dma(c, f.dma_done, f.dma_seq);
-  if (n && d.V) lsm::launch_copy(CopyMode::kCacheToStage, d, n, f.sc, outp, c->meta);
-  // queue mode: the hit copy also moves the victim hits, from the prefetch
-  // buffer that the previous call filled
-  if (queues && f.pf_ready) (void)hipStreamWaitEvent(c->meta, f.pf_done, 0);
-  rec(kEvHbm0, c->meta);
-  if (n) lsm::launch_copy(CopyMode::kHbmToOut, d, n, f.sc, outp, c->meta);
-  rec(kEvHbm1, c->meta);
-  (void)hipEventRecord(f.stage_done, c->meta);
-  f.used = true;
+  // gather t-1's deferred hit copy and fills, now behind this gather's
+  // metadata
+  flush_deferred(c);
+  // this gather's data work: its size and output (the lists are in f.sc)
+  f.data_n = n;
+  f.data_out = outp;
+  f.data_prof = prof;
+  // staging (and unless deferred the hit copy) once gather t-1's fills have
+  // landed; the ring write (PCIe egress) is queued later on the dma stream
+  queue_stage(c, t);
+  if (!defer) queue_hit(c, t);
   ps.pending = false;
   if (hipGetLastError() != hipSuccess) return fail_device(c);
 
   // the GPU runs on while the host waits for the dedup result (with a pageable
-  // store: for the whole metadata); the meta stream is in order, so gather
+  // store: for the host-fetch list); the meta stream is in order, so gather
   // t-1's counters are published by then and its ring write can be queued
-  if (hipEventSynchronize(c->pageable ? f.finish_done : c->ev_dedup) != hipSuccess) return fail_device(c);
+  if (hipEventSynchronize(pageable_list && n ? f.list_done : c->ev_dedup) != hipSuccess) return fail_device(c);
   harvest_stats(c, pf);
   issue_dma(c, pf);
   if (queues) (void)hipEventRecord(c->ev_q, c->dma);  // every queue write up to gather t-1's
@@ -578,25 +671,19 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
       // ring rows are read only for entries of gathers up to t-2, whose ring
       // writes must have landed
       if (f.dma_used && hipEventSynchronize(f.dma_done) != hipSuccess) return fail_device(c);
-      copy_host_rows(c, f, f.hc->n_host, prof);
+      copy_host_rows(c, f, *f.hcount_host, prof);
     }
     host_fetch();
   }
 
   // fills after the host fetch, the staging and the hit copy, queued behind
   // gather t-1's ring write so that the next host fetch need not wait for them
-  (void)hipStreamWaitEvent(c->dma, f.host_done, 0);
-  (void)hipStreamWaitEvent(c->dma, f.stage_done, 0);
-  rec(kEvFill0, c->dma);
-  if (n) lsm::launch_copy(CopyMode::kOutToCache, d, n, f.sc, outp, c->dma);
-  rec(kEvFill1, c->dma);
-  rec(kEvAll1, c->dma);
-  (void)hipEventRecord(f.data_done, c->dma);
-  f.fill_seq = ++c->dma_subs;
+  if (!defer) queue_fills(c, t);
   if (hipGetLastError() != hipSuccess) return fail_device(c);
   const uint32_t err = dedup ? c->dd->err : 0u;
   const uint32_t U = dedup ? c->dd->n_unique : 0u;
   if (err) return LSMGNN_E_RANGE;  // every queued kernel of the batch is a no-op
+  f.data_deferred = defer;
 
   f.stats_pending = true;
   f.t = t;
@@ -747,7 +834,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   d.store = static_cast<const uint8_t *>(store_dev);  // null for a pageable store
   c->pageable = pageable;
   c->store_host = static_cast<const uint8_t *>(cfg->host_store);
-  d.nchunks = (N + lsm::kChunkBytes - 1) / lsm::kChunkBytes;
+  d.nchunks = (N + lsm::kChunkNodes - 1) / lsm::kChunkNodes;
   const uint64_t map_bytes = d.nchunks * lsm::kChunkBytes;
   const uint64_t B = cfg->max_batch;
   Scratch sc{};
@@ -764,7 +851,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   }
   bool ok = dev_alloc(c, &d.sets, S) && dev_alloc(c, &d.rows, total_rows * R) &&
             dev_alloc(c, &d.mask, N) &&
-            dev_alloc(c, &d.stat, N) && dev_alloc(c, &d.present, map_bytes) &&
+            dev_alloc(c, &d.stat, N) && dev_alloc(c, &d.present, map_bytes / 4) &&
             dev_alloc(c, &d.chunk_sums, d.nchunks) &&
             dev_alloc(c, &d.set_count, S) && dev_alloc(c, &d.set_idx, S) && dev_alloc(c, &d.uidx, N) &&
             dev_alloc(c, &d.tail, 2) &&
@@ -776,7 +863,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
             dev_alloc(c, &c->cn_adv, 1) && dev_alloc(c, &sc.uniq, B) && dev_alloc(c, &sc.uset, B) &&
             dev_alloc(c, &sc.arrival, B) && dev_alloc(c, &sc.touched, B) && dev_alloc(c, &sc.seg_off, B) &&
             dev_alloc(c, &sc.seg, B) && dev_alloc(c, &sc.seg_u, B) && dev_alloc(c, &sc.seg_x, B) &&
-            dev_alloc(c, &sc.seg_st, B) && dev_alloc(c, &sc.kind, B) && dev_alloc(c, &sc.flags, B) &&
+            dev_alloc(c, &sc.seg_st, B) && dev_alloc(c, &sc.big, B / (lsm::kSmallSet + 1) + 1) && dev_alloc(c, &sc.kind, B) && dev_alloc(c, &sc.flags, B) &&
             dev_alloc(c, &sc.oc, B) &&
             dev_alloc(c, &sc.dead, B) && dev_alloc(c, &sc.evicted, B) && dev_alloc(c, &sc.enq_before, B) &&
             dev_alloc(c, &sc.scan_part, B / lsm::kScanChunk + 2) && dev_alloc(c, &sc.this_q, B) &&
@@ -794,7 +881,8 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
     if (ok && V) f.sc.staging = d.rows + (d.stage_row0 + (uint64_t)(&f - c->fl) * d.stage_rows) * R;
     if (ok && pageable) {
       // the host reads the host-fetch list and fills the bounce rows
-      ok = host_alloc(c, &f.hlist_host, &f.sc.host_list, B * sizeof(uint32_t), false) &&
+      ok = host_alloc(c, &f.hcount_host, &f.hcount_dev, sizeof(uint32_t), true) &&
+           host_alloc(c, &f.hlist_host, &f.sc.host_list, B * sizeof(uint32_t), false) &&
            host_alloc(c, &f.hsrc_host, &f.sc.host_src, B * sizeof(uint64_t), false) &&
            host_alloc(c, &f.bounce_host, &f.sc.bounce, B * R, false);
     }
@@ -825,8 +913,9 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   for (hipEvent_t *e : {&c->ev_in, &c->ev_dedup, &c->ev_adv, &c->ev_q})
     ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
   for (Flight &f : c->fl)
-    for (hipEvent_t *e : {&f.meta_done, &f.finish_done, &f.stage_done, &f.host_done, &f.data_done, &f.dma_done,
-                          &f.pf_done})
+    for (hipEvent_t *e : {&f.meta_done, &f.finish_done, &f.stage_done, &f.hit_done, &f.host_done, &f.data_done,
+                          &f.dma_done,
+                          &f.pf_done, &f.list_done})
       ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
   for (PerfSet &p : c->ps)
     for (hipEvent_t &e : p.e) ok = ok && hipEventCreate(&e) == hipSuccess;
@@ -881,6 +970,7 @@ lsmgnn_status lsmgnn_advance(lsmgnn_cache *c, const int64_t *ids, uint64_t n, vo
     lsm::launch_window_set(ids, n, c->d.N, bit, c->d.mask, c->win_ids + (uint64_t)slot * c->max_batch, record,
                            c->cn_adv, c->meta);
   lsm::launch_finish(c->cn_adv, c->hc_adv_dev, c->fl[0].sc.stat_part, lsm::StatGrids{}, nullptr, lsm::QueueFinish{},
+                     lsm::AnnounceArgs{},
                      c->meta);
   if (hipEventRecord(c->ev_adv, c->meta) != hipSuccess || hipGetLastError() != hipSuccess ||
       hipEventSynchronize(c->ev_adv) != hipSuccess)
@@ -909,7 +999,7 @@ lsmgnn_status lsmgnn_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, voi
   if (!guard.ok) return LSMGNN_E_DEVICE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   uint64_t t = 0;
-  st = issue_gather(c, ids, n, Announce{}, out, unique_ids, inverse, outcome, n_unique, s, &t);
+  st = issue_gather(c, ids, n, Announce{}, out, unique_ids, inverse, outcome, n_unique, s, &t, false);
   if (st != LSMGNN_OK) return st;
   Flight &f = c->fl[t & 1];
   if (hipStreamWaitEvent(s, f.data_done, 0) != hipSuccess || hipEventSynchronize(f.finish_done) != hipSuccess ||
@@ -934,7 +1024,7 @@ lsmgnn_status lsmgnn_gather_async(lsmgnn_cache *c, const int64_t *ids, uint64_t 
   DeviceGuard guard(c->device);
   if (!guard.ok) return LSMGNN_E_DEVICE;
   return issue_gather(c, ids, n, an, out, unique_ids, inverse, outcome, n_unique,
-                      static_cast<hipStream_t>(stream), ticket);
+                      static_cast<hipStream_t>(stream), ticket, true);
 }
 
 lsmgnn_status lsmgnn_gather_wait(lsmgnn_cache *c, uint64_t ticket, void *stream) {
@@ -943,6 +1033,7 @@ lsmgnn_status lsmgnn_gather_wait(lsmgnn_cache *c, uint64_t ticket, void *stream)
   if (ticket >= c->t) return LSMGNN_E_INVAL;
   DeviceGuard guard(c->device);
   if (!guard.ok) return LSMGNN_E_DEVICE;
+  flush_deferred(c);  // the latest gather's data work may not be queued yet
   // the slot may hold a later gather by now: waiting for that one is conservative
   if (hipStreamWaitEvent(static_cast<hipStream_t>(stream), c->fl[ticket & 1].data_done, 0) != hipSuccess)
     return fail_device(c);
@@ -1028,7 +1119,8 @@ lsmgnn_status lsmgnn_copy_bytes(void *dst, const void *src, uint64_t bytes, void
     return LSMGNN_E_INVAL;
   if (bytes == 0) return LSMGNN_OK;
   // pinned host memory is addressed through its device mapping
-  auto dev_view = [](const void *p) -> const void * {
+  int on_device = 0;
+  auto dev_view = [&on_device](const void *p) -> const void * {
     hipPointerAttribute_t a{};
     if (hipPointerGetAttributes(&a, p) != hipSuccess) {
       (void)hipGetLastError();
@@ -1042,13 +1134,14 @@ lsmgnn_status lsmgnn_copy_bytes(void *dst, const void *src, uint64_t bytes, void
       }
       return dp;
     }
+    on_device += a.type == hipMemoryTypeDevice;
     return (a.type == hipMemoryTypeDevice) ? p : nullptr;
   };
   const void *s_dev = dev_view(src);
   void *d_dev = const_cast<void *>(dev_view(dst));
   if (!s_dev || !d_dev) return LSMGNN_E_INVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  lsm::launch_copy_plain(s_dev, d_dev, bytes, s);
+  lsm::launch_copy_plain(s_dev, d_dev, bytes, on_device == 2, s);
   if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) {
     (void)hipGetLastError();
     return LSMGNN_E_DEVICE;

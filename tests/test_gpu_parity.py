@@ -205,6 +205,13 @@ def _adversarial():
     cases["single_node"] = dict(n=1, S=1, V=1, L=1, batches=[np.zeros(5, np.int64), np.zeros(1, np.int64)] * 3)
     cases["big_batch"] = dict(n=1 << 22, S=4096, V=20000, L=4,
                               batches=[rng.integers(0, 1 << 22, 1 << 20) for _ in range(3)])
+    # one set receiving about 10^5 unique IDs per gather (its segment is
+    # ordered by a block's radix sort, linear in the set's size)
+    cases["one_set_large"] = dict(n=300000, S=1, V=5000, L=2,
+                                  batches=[rng.integers(0, 300000, 150000) for _ in range(3)])
+    # sets on both sides of the size at which a set's segment is sorted by a block
+    cases["sets_near_sort_threshold"] = dict(n=50000, S=200, V=2000, L=3,
+                                             batches=[rng.integers(0, 50000, 13000) for _ in range(4)])
     return cases
 
 
