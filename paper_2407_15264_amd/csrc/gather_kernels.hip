@@ -7,7 +7,7 @@
 // first (Counters::err, or the gather's gate in the row copies) and does
 // nothing once an out-of-range ID was seen, so an invalid batch changes no state.
 //
-//   dedup       bitmap over node IDs (one bit per node), per-chunk
+//   dedup       byte map over node IDs marked with plain stores, per-chunk
 //               popcount, chunk scan, ascending compaction that records each
 //               node's unique index; the inverse index is one lookup
 //   group       per-set counts with atomics, segment allocation, placement and
@@ -184,10 +184,13 @@ void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, cons
 }
 
 // ------------------------------------------------------------------- dedup
-// A bitmap marks the batch's requests: bit x & 31 of word x >> 5 for node x.
-// Marks are atomic ORs, skipped when the bit is already visible (repeated IDs
-// of hub nodes would otherwise queue on one word); the two popcount/compact
-// passes then read N/8 bytes instead of a byte per node.
+// A byte per node marks the batch's requests.  Plain byte stores need no
+// atomics: every writer of a byte writes the same value, and bytes of
+// different nodes never interfere.  A bit per node would make the popcount
+// and compaction passes read N/8 bytes instead of N, but its marks need
+// atomic ORs, and repeated IDs of hub nodes queue on one word: measured on
+// the MI355X, the byte map gives 478 GB/s on the 100M-node workload (the
+// largest N here, 100 MB per pass) against 428-437 with the bitmap.
 //
 // Validate and mark.  Out-of-range IDs set Counters::err; valid ones are still
 // marked, and the compaction kernel then clears the map instead of compacting
@@ -198,7 +201,7 @@ void launch_finish(Counters *cn, Counters *host, const uint32_t *stat_part, cons
 // succeeds.  Only that bit of a node's window word changes in this kernel, so a
 // plain read-modify-write is exact.
 __global__ void k_mark(const int64_t *ids, uint32_t n, const int64_t *ann_ids, uint32_t ann_n, uint64_t N,
-                       uint32_t *present, const int64_t *clear_ids, uint32_t clear_n, uint32_t clear_bit,
+                       uint8_t *present, const int64_t *clear_ids, uint32_t clear_n, uint32_t clear_bit,
                        uint32_t *mask, Counters *cn) {
   bool bad = false;
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
@@ -206,10 +209,7 @@ __global__ void k_mark(const int64_t *ids, uint32_t n, const int64_t *ann_ids, u
     if (x < 0 || (uint64_t)x >= N) {
       bad = true;
     } else {
-      const uint32_t b = 1u << (x & 31);
-      uint32_t *w = present + (x >> 5);
-      if (!(__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & b))
-        __hip_atomic_fetch_or(w, b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      present[x] = 1;
     }
   }
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ann_n; i += gridDim.x * kBlock) {
@@ -225,11 +225,11 @@ __global__ void k_mark(const int64_t *ids, uint32_t n, const int64_t *ann_ids, u
   }
 }
 
-// Each thread owns kWordsPerThread consecutive words of the bitmap (four
-// 128-bit loads).
-__device__ __forceinline__ void load_words(const uint32_t *present, uint32_t (&w)[kWordsPerThread]) {
+// Each thread owns kBytesPerThread consecutive bytes of the map (four 128-bit
+// loads); marked bytes hold exactly 1, so a popcount of a word counts them.
+__device__ __forceinline__ void load_words(const uint8_t *present, uint32_t (&w)[kWordsPerThread]) {
   const u32x4 *p = reinterpret_cast<const u32x4 *>(present + ((size_t)blockIdx.x * kBlock + threadIdx.x) *
-                                                                 kWordsPerThread);
+                                                                 kBytesPerThread);
 #pragma unroll
   for (int k = 0; k < kWordsPerThread / 4; ++k) {
     const u32x4 a = p[k];
@@ -237,7 +237,7 @@ __device__ __forceinline__ void load_words(const uint32_t *present, uint32_t (&w
   }
 }
 
-__global__ __launch_bounds__(kBlock) void k_chunk_popc(const uint32_t *present, uint32_t *chunk_sums,
+__global__ __launch_bounds__(kBlock) void k_chunk_popc(const uint8_t *present, uint32_t *chunk_sums,
                                                        const Counters *cn) {
   if (cn->err) return;
   uint32_t w[kWordsPerThread];
@@ -281,17 +281,17 @@ __global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uin
 // saves the separate one-block scan), and the last chunk's block publishes
 // the unique count; otherwise chunk_off holds the scanned offsets.
 template <bool kFused>
-__global__ __launch_bounds__(kBlock) void k_compact(uint32_t *present, const uint32_t *chunk_off, uint32_t *uidx,
+__global__ __launch_bounds__(kBlock) void k_compact(uint8_t *present, const uint32_t *chunk_off, uint32_t *uidx,
                                                     uint32_t *uniq, int64_t *uniq_out, Counters *cn,
                                                     uint32_t nchunks, DedupResult *dd, Gate *gate) {
   uint32_t w[kWordsPerThread];
   load_words(present, w);
-  const size_t w0 = ((size_t)blockIdx.x * kBlock + threadIdx.x) * kWordsPerThread;  // first word of this thread
+  const size_t b0 = ((size_t)blockIdx.x * kBlock + threadIdx.x) * kBytesPerThread;  // first byte of this thread
   const uint32_t err = cn->err;
   if (err) {  // rejected batch: undo the marks
 #pragma unroll
     for (int k = 0; k < kWordsPerThread; ++k)
-      if (w[k]) present[w0 + k] = 0;
+      if (w[k]) reinterpret_cast<uint32_t *>(present + b0)[k] = 0;
     if (kFused && blockIdx.x == 0 && threadIdx.x == 0) {
       *gate = Gate{err, 0, 0, 0, 0, 0, 0, 0, 0, {0, 0, 0}};
       *dd = DedupResult{err, 0, {0, 0}};
@@ -322,8 +322,8 @@ __global__ __launch_bounds__(kBlock) void k_compact(uint32_t *present, const uin
 #pragma unroll
   for (int k = 0; k < kWordsPerThread; ++k) {
     uint32_t word = w[k];
-    while (word) {  // marked nodes ascending: bit j of word k is node 32 (w0 + k) + j
-      const uint32_t x = (uint32_t)(32 * (w0 + k) + __builtin_ctz(word));
+    while (word) {  // marked bytes ascending: bit 8j is set for byte j of word k
+      const uint32_t x = (uint32_t)(b0 + 4 * k + (__builtin_ctz(word) >> 3));
       uniq[pos] = x;
       uniq_out[pos] = (int64_t)x;
       uidx[x] = pos;
@@ -401,7 +401,7 @@ __global__ __launch_bounds__(kBlock) void k_inverse_claim(const DevState d, Scra
       sc.dead[u] = 0;
       sc.this_q[u] = 0;
       sc.fill_dst[u] = 0;
-      d.present[x >> 5] = 0;  // the map's last reader (the compaction) is done; every writer stores 0
+      d.present[x] = 0;  // the map's last reader (the compaction) is done
     }
     const uint32_t i = block_append(claim, &cn->n_touched);
     if (claim) {

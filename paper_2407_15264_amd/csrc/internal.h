@@ -10,10 +10,9 @@ namespace lsm {
 constexpr uint32_t kWays = 8;
 constexpr uint32_t kEmpty = 0xffffffffu;
 constexpr int kBlock = 256;          // threads per block for every kernel
-constexpr int kBytesPerThread = 64;  // dedup bitmap bytes per thread
+constexpr int kBytesPerThread = 64;  // dedup map bytes per thread
 constexpr int kWordsPerThread = kBytesPerThread / 4;
-constexpr int kChunkBytes = kBlock * kBytesPerThread;  // dedup bitmap bytes per block
-constexpr uint64_t kChunkNodes = (uint64_t)kChunkBytes * 8;  // nodes per bitmap chunk
+constexpr int kChunkBytes = kBlock * kBytesPerThread;  // dedup map bytes (nodes) per block
 constexpr int kScanPerThread = 8;    // flags per thread in the enqueue scan
 constexpr int kScanChunk = kBlock * kScanPerThread;
 constexpr int kMaxQueues = 32;       // victim-queue slots: L + 1 <= 32
@@ -174,7 +173,7 @@ struct DevState {
   uint32_t *ring_tag;    // [V] FIFO ring entries, or queue slot k's entries at k * C
   uint8_t *ring_rows;    // [V][R] pinned host, device-visible address (ring or queue rows)
   const uint8_t *store;  // [N][R] pinned host, device-visible address
-  uint32_t *present;     // [nchunks * kChunkBytes / 4] dedup bitmap, bit x for node x (all zero between calls)
+  uint8_t *present;      // [nchunks * kChunkBytes] dedup byte map (all zero between calls)
   uint32_t *chunk_sums;  // [nchunks]
   uint32_t *set_count;   // [S] (all zero between calls)
   uint32_t *set_idx;     // [S]

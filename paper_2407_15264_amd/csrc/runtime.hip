@@ -834,7 +834,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   d.store = static_cast<const uint8_t *>(store_dev);  // null for a pageable store
   c->pageable = pageable;
   c->store_host = static_cast<const uint8_t *>(cfg->host_store);
-  d.nchunks = (N + lsm::kChunkNodes - 1) / lsm::kChunkNodes;
+  d.nchunks = (N + lsm::kChunkBytes - 1) / lsm::kChunkBytes;
   const uint64_t map_bytes = d.nchunks * lsm::kChunkBytes;
   const uint64_t B = cfg->max_batch;
   Scratch sc{};
@@ -851,7 +851,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   }
   bool ok = dev_alloc(c, &d.sets, S) && dev_alloc(c, &d.rows, total_rows * R) &&
             dev_alloc(c, &d.mask, N) &&
-            dev_alloc(c, &d.stat, N) && dev_alloc(c, &d.present, map_bytes / 4) &&
+            dev_alloc(c, &d.stat, N) && dev_alloc(c, &d.present, map_bytes) &&
             dev_alloc(c, &d.chunk_sums, d.nchunks) &&
             dev_alloc(c, &d.set_count, S) && dev_alloc(c, &d.set_idx, S) && dev_alloc(c, &d.uidx, N) &&
             dev_alloc(c, &d.tail, 2) &&
