@@ -110,21 +110,23 @@ def duplex_probe(nbytes=1 << 30):
     print(json.dumps(best), flush=True)
 
 
-def duplex_ceiling():
-    """duplex_probe() in a child process; None if it fails."""
+def child_probe(flag):
+    """A probe (--duplex-probe, --hbm-probe) in a child process: its JSON
+    result, or None if it fails."""
     import subprocess
     try:
-        out = subprocess.run([sys.executable, os.path.abspath(__file__), "--duplex-probe"], capture_output=True,
+        out = subprocess.run([sys.executable, os.path.abspath(__file__), flag], capture_output=True,
                              text=True, timeout=300)
         return json.loads(out.stdout.strip().splitlines()[-1]) if out.returncode == 0 else None
     except (subprocess.SubprocessError, ValueError, IndexError, OSError):
         return None
 
 
-def measure_ceilings(torch, lsmgnn, store_ptr, nbytes, duplex):
+def measure_ceilings(torch, lsmgnn, store_ptr, nbytes, duplex, hbm):
     """Host-link and HBM ceilings in this run: pinned H2D DMA, zero-copy reads
-    and writes by the 128-bit copy kernel, a device-to-device copy; `duplex`
-    is duplex_probe()'s result, measured in a child process beforehand."""
+    and writes by the 128-bit copy kernel; `duplex` and `hbm` are
+    duplex_probe()'s and hbm_probe()'s results, measured in child processes
+    beforehand."""
     dev = torch.device("cuda", 0)
     nbytes = min(nbytes, 1 << 30) // 16 * 16
     d0 = torch.empty(nbytes, dtype=torch.uint8, device=dev)
@@ -148,24 +150,44 @@ def measure_ceilings(torch, lsmgnn, store_ptr, nbytes, duplex):
     res["zero_copy_write_GBps"] = nbytes / best(
         lambda: lsmgnn.copy_bytes(pinned.data_ptr(), d0.data_ptr(), nbytes)) / 1e9
     del d0, d1, pinned
-    # HBM: the best device-to-device copy over sizes and copy engines (the
-    # library's 128-bit copy kernel, and the runtime's copy behind torch's
-    # copy_), read + write bytes per second
+    res["hbm_copy_GBps"] = max(hbm.values()) if hbm else None
+    res["hbm_copy_detail"] = hbm
+    res["duplex"] = duplex
+    res["bytes"] = nbytes
+    return res
+
+
+def hbm_probe():
+    """The HBM ceiling: the best device-to-device copy over sizes and copy
+    engines (the library's 128-bit copy kernel, and the runtime's copy behind
+    torch's copy_), read + write bytes per second.  Runs in a process of its
+    own: in the bench process, the runtime's device-to-device copies and the
+    8 GiB of buffers left the ring writes of the gathers measured afterwards
+    about a quarter slower."""
+    import torch
+    from paper_2407_15264_amd import lsmgnn
+    dev = torch.device("cuda", 0)
+
+    def best(fn, reps=7):
+        ts = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            ts.append(time.perf_counter() - t0)
+        return min(ts)
+
     hbm = {}
     for size in (256 << 20, 1 << 30, 4 << 30):
         a = torch.empty(size, dtype=torch.uint8, device=dev)
         b = torch.empty(size, dtype=torch.uint8, device=dev)
         a.fill_(1)
-        hbm[f"copy_kernel_{size >> 20}MiB"] = 2 * size / best(
-            lambda: lsmgnn.copy_bytes(b.data_ptr(), a.data_ptr(), size), reps=7) / 1e9
-        hbm[f"runtime_copy_{size >> 20}MiB"] = 2 * size / best(lambda: b.copy_(a), reps=7) / 1e9
+        hbm[f"copy_kernel_{size >> 20}MiB"] = round(
+            2 * size / best(lambda: lsmgnn.copy_bytes(b.data_ptr(), a.data_ptr(), size)) / 1e9, 1)
+        hbm[f"runtime_copy_{size >> 20}MiB"] = round(2 * size / best(lambda: b.copy_(a)) / 1e9, 1)
         del a, b
-    torch.cuda.empty_cache()
-    res["hbm_copy_GBps"] = max(hbm.values())
-    res["hbm_copy_detail"] = {k: round(v, 1) for k, v in hbm.items()}
-    res["duplex"] = duplex
-    res["bytes"] = nbytes
-    return res
+    print(json.dumps(hbm), flush=True)
 
 
 def make_parts(W, cfg, nb):
@@ -455,6 +477,7 @@ def main():
                     help="sample each minibatch's request list on the GPU inside the timed region (lsmgnn_sample; "
                          "homogeneous workloads) instead of taking the resident host-generated lists")
     ap.add_argument("--duplex-probe", action="store_true", help=argparse.SUPPRESS)
+    ap.add_argument("--hbm-probe", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--no-duplex-probe", action="store_true",
                     help="skip the link probe with both directions at once (a child process)")
     args = ap.parse_args()
@@ -465,6 +488,9 @@ def main():
     if args.duplex_probe:
         duplex_probe()
         return
+    if args.hbm_probe:
+        hbm_probe()
+        return
     if args.gpu_sampler:
         # the sampler's stream is a fifth stream beside the caller's and the
         # library's three: give each its own hardware queue (HIP's default is 4)
@@ -473,8 +499,10 @@ def main():
     # profiler: its preloaded library would trace the child too, into the same
     # output files.
     profiled_run = any(k.startswith("ROCPROF") for k in os.environ)
-    duplex = None if args.no_duplex_probe or profiled_run else duplex_ceiling()
+    duplex = None if args.no_duplex_probe or profiled_run else child_probe("--duplex-probe")
     log(f"[bench] duplex link probe: {duplex}")
+    hbm = None if profiled_run else child_probe("--hbm-probe")
+    log(f"[bench] HBM copy probe: {hbm}")
 
     import numpy as np
     import torch
@@ -531,7 +559,7 @@ def main():
     else:
         cbytes = 1 << 30
         cbuf = lsmgnn.PinnedBuffer(cbytes)
-    ceil = measure_ceilings(torch, lsmgnn, cbuf.ptr, cbytes, duplex)
+    ceil = measure_ceilings(torch, lsmgnn, cbuf.ptr, cbytes, duplex, hbm)
     log(f"[bench] ceilings: {json.dumps({k: round(v, 1) if isinstance(v, float) else v for k, v in ceil.items()})}")
 
     dev = torch.device("cuda", 0)
@@ -741,12 +769,14 @@ def main():
     trh = recorded_traffic(cfg.name, "hbm_copy")
     roof_hbm = {"bound": "hbm", "kernel": "hbm_copy (hit rows cache->out)", "achieved": hb["GBps"],
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": hb["GBps"] / HBM_PEAK_GBPS,
-                "frac_of_measured_d2d": hb["GBps"] / ceil["hbm_copy_GBps"], "avg_launch_us": hb["avg_us"],
+                "frac_of_measured_d2d": hb["GBps"] / ceil["hbm_copy_GBps"] if ceil["hbm_copy_GBps"] else None,
+                "avg_launch_us": hb["avg_us"],
                 "bytes_per_launch": hb["bytes_per_launch"],
                 "traffic": None if trh is None else trh["bytes"],
                 "target_frac": HIT_PATH_TARGET_FRAC,
                 "gap_to_target": HIT_PATH_TARGET_FRAC - hb["GBps"] / HBM_PEAK_GBPS,
-                "alone": dict(alone, frac_of_measured_d2d=alone["achieved"] / ceil["hbm_copy_GBps"])}
+                "alone": dict(alone, frac_of_measured_d2d=alone["achieved"] / ceil["hbm_copy_GBps"]
+                              if ceil["hbm_copy_GBps"] else None)}
 
     res = {
         "metric": METRIC, "value": gbps, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
