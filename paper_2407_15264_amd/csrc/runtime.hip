@@ -353,13 +353,20 @@ void meta_wait_dma(lsmgnn_cache *c, hipEvent_t e, uint64_t seq) {
 //
 // Queue mode: the placements were staged slot by slot; slot k's go to its
 // positions [q_before[k], q_before[k] + q_placed[k]).
-void issue_dma(lsmgnn_cache *c, Flight &f) {
+//
+// `after` (optional): an event the write also waits for.  The write that the
+// next gather's call queues waits for that gather's metadata up to its
+// host-fetch list: the write's host-link traffic then runs beside that
+// gather's host fetch (the link's other direction) instead of slowing the
+// metadata kernels, whose memory requests queue behind it.
+void issue_dma(lsmgnn_cache *c, Flight &f, hipEvent_t after = nullptr) {
   if (!f.dma_pending) return;
   f.dma_pending = false;
   const uint64_t V = c->d.V, R = c->d.R;
   PerfSet &p = c->ps[f.t % kPerfSets];
   const bool prof = p.pending && p.t == f.t;
   (void)hipStreamWaitEvent(c->dma, f.stage_done, 0);
+  if (after) (void)hipStreamWaitEvent(c->dma, after, 0);
   if (prof) (void)hipEventRecord(p.e[kEvEnq0], c->dma);
   if (c->d.qmode) {
     uint64_t off = 0;
@@ -664,7 +671,7 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   // t-1's counters are published by then and its ring write can be queued
   if (hipEventSynchronize(pageable_list && n ? f.list_done : c->ev_dedup) != hipSuccess) return fail_device(c);
   harvest_stats(c, pf);
-  issue_dma(c, pf);
+  issue_dma(c, pf, n ? f.meta_done : nullptr);
   if (queues) (void)hipEventRecord(c->ev_q, c->dma);  // every queue write up to gather t-1's
   if (c->pageable) {
     if (n && !(dedup && c->dd->err)) {
@@ -1005,8 +1012,7 @@ lsmgnn_status lsmgnn_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, voi
   if (hipStreamWaitEvent(s, f.data_done, 0) != hipSuccess || hipEventSynchronize(f.finish_done) != hipSuccess ||
       hipStreamSynchronize(s) != hipSuccess)
     return fail_device(c);
-  harvest_stats(c, f);
-  issue_dma(c, f);  // the ring write may still run when this returns
+  harvest_stats(c, f);  // its ring write is queued by the next call (after that gather's metadata) or a sync
   return LSMGNN_OK;
 }
 
