@@ -74,6 +74,15 @@ __device__ __forceinline__ uint32_t block_sum(uint32_t v) {
   return tot;
 }
 
+// A gather's gate as the dedup leaves it: the error flag and the unique count,
+// every list empty.
+__device__ __forceinline__ Gate gate_with(uint32_t err, uint32_t n_unique) {
+  Gate g{};
+  g.err = err;
+  g.n_unique = n_unique;
+  return g;
+}
+
 static inline unsigned grid_for(uint64_t work, uint64_t per_block, unsigned cap) {
   uint64_t b = (work + per_block - 1) / per_block;
   if (b < 1) b = 1;
@@ -146,7 +155,7 @@ __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host,
     c.victim_hits = sums[kStVictimHits];
     c.misses = sums[kStMisses];
     c.n_hbm = sums[kStHbm];
-    c.n_host = sums[kStHost];
+    c.n_host = sums[kStHost] + sums[kStEarly];  // both parts of the host-fetch list
     c.n_enq_copy = sums[kStEnqCopy];
     c.req_hits = sums[kStReqHits];
     c.req_victim_hits = sums[kStReqVictimHits];
@@ -254,7 +263,7 @@ __global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uin
   const uint32_t err = cn->err;
   if (err) {
     if (threadIdx.x == 0) {
-      *gate = Gate{err, 0, 0, 0, 0, 0, 0, 0, 0, {0, 0, 0}};
+      *gate = gate_with(err, 0);
       *dd = DedupResult{err, 0, {0, 0}};
     }
     return;
@@ -270,7 +279,7 @@ __global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uin
   }
   if (threadIdx.x == 0) {
     cn->n_unique = carry;
-    *gate = Gate{0, carry, 0, 0, 0, 0, 0, 0, 0, {0, 0, 0}};
+    *gate = gate_with(0, carry);
     *dd = DedupResult{0, carry, {0, 0}};
   }
 }
@@ -293,7 +302,7 @@ __global__ __launch_bounds__(kBlock) void k_compact(uint8_t *present, const uint
     for (int k = 0; k < kWordsPerThread; ++k)
       if (w[k]) reinterpret_cast<uint32_t *>(present + b0)[k] = 0;
     if (kFused && blockIdx.x == 0 && threadIdx.x == 0) {
-      *gate = Gate{err, 0, 0, 0, 0, 0, 0, 0, 0, {0, 0, 0}};
+      *gate = gate_with(err, 0);
       *dd = DedupResult{err, 0, {0, 0}};
     }
     return;
@@ -311,7 +320,7 @@ __global__ __launch_bounds__(kBlock) void k_compact(uint8_t *present, const uint
     if (blockIdx.x == nchunks - 1 && threadIdx.x == 0) {
       const uint32_t total = first + tot;
       cn->n_unique = total;
-      *gate = Gate{0, total, 0, 0, 0, 0, 0, 0, 0, {0, 0, 0}};
+      *gate = gate_with(0, total);
       *dd = DedupResult{0, total, {0, 0}};
     }
   } else {
@@ -996,6 +1005,57 @@ __global__ __launch_bounds__(kBlock) void k_qplace(const DevState d, Scratch sc,
   block_count(c_copy, sc.stat_part, kStEnqCopy);
 }
 
+// Misses known from the batch-start state, listed right after the dedup so
+// that their rows start crossing the link while the rest of the metadata
+// runs: a unique ID x that no way of its set holds at batch start is filled
+// at its turn (only x itself inserts x), and with no entry for it in the
+// victim buffer (FIFO: no ring entry naming x; queues: no entry in the queue
+// of this iteration) the fill is a miss, whatever the walk decides.  The
+// resolve, which finds the same outcome, leaves these out of its list.
+__global__ __launch_bounds__(kBlock) void k_early(const DevState d, Scratch sc, uint64_t t, const Counters *cn) {
+  if (cn->err) return;
+  const uint32_t U = cn->n_unique;
+  uint32_t c_early = 0;
+  for (uint32_t base = blockIdx.x * kBlock; base < U; base += gridDim.x * kBlock) {
+    const uint32_t u = base + threadIdx.x;
+    bool early = false;
+    uint32_t x = 0;
+    if (u < U) {
+      x = sc.uniq[u];
+      const u32x4 *tp = reinterpret_cast<const u32x4 *>(d.sets[set_index(x, d.S)].tag);
+      const u32x4 a = tp[0], b = tp[1];
+      const bool resident = a.x == x || a.y == x || a.z == x || a.w == x || b.x == x || b.y == x || b.z == x ||
+                            b.w == x;
+      if (!resident) {
+        bool entry = false;
+        if (d.V) {
+          const uint64_t vp = d.vpos[x];
+          if (d.qmode)
+            entry = (vp >> 32) == t + 1;
+          else if (vp)
+            entry = d.ring_tag[(vp - 1) % d.V] == x;
+        }
+        early = !entry;
+      }
+      sc.early[u] = early ? 1 : 0;
+      c_early += early;
+    }
+    const uint32_t i = block_append(early, &sc.gate->n_early);
+    if (early) {
+      sc.host_list[i] = u;
+      sc.host_src[i] = kSrcStore | x;
+    }
+  }
+  block_count(c_early, sc.stat_part, kStEarly);
+}
+
+void launch_early(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, Counters *cn, StatGrids &grids,
+                  hipStream_t s) {
+  const unsigned g = grid_for(n, kBlock, kMaxGrid);
+  hipLaunchKernelGGL(k_early, dim3(g), dim3(kBlock), 0, s, d, sc, t, cn);
+  grids.g[kStEarly] = g;
+}
+
 // Victim-ring probe of every fill and the row source of every unique ID.  Builds
 // the gather's row-copy lists (dense, in arbitrary order): the host fetch (rows
 // from pinned host memory), the hit copy (rows from cache slots) and the fills
@@ -1010,6 +1070,7 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
   // in that order in its staging buffer
   const uint64_t q_lo_prev = tail0 - ((tail0 - tail_prev) < d.V ? (tail0 - tail_prev) : d.V);
   const uint64_t stage_prev = d.stage_row0 + ((t + 1u) & 1u) * d.stage_rows;
+  const uint32_t n_early = sc.gate->n_early;  // the list's first entries, written by k_early
   uint32_t c_vhit = 0, c_miss = 0, c_hbm = 0, c_host = 0, c_vring = 0, c_vstaged = 0, c_vsame = 0;
   for (uint32_t base = blockIdx.x * kBlock; base < U; base += gridDim.x * kBlock) {
     const uint32_t u = base + threadIdx.x;
@@ -1022,6 +1083,10 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
       if (kind == kKindHit) {
         code = kSrcHbm | sc.slot[u];
         ++c_hbm;
+      } else if (sc.early[u]) {  // a miss already listed (its row is on its way)
+        ++c_miss;
+        oc = 2;  // LSMGNN_MISS
+        code = kSrcStore;
       } else if (d.qmode) {
         // queue mode: a victim hit iff the node's latest entry is in the queue
         // of this iteration, whose rows were prefetched into buffer t & 1
@@ -1092,14 +1157,14 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
           ++c_host;
         }
       }
-      from_host = (code & ~kSrcIndex) != kSrcHbm;
-      from_hbm = !from_host;
+      from_host = (code & ~kSrcIndex) != kSrcHbm && !sc.early[u];
+      from_hbm = (code & ~kSrcIndex) == kSrcHbm;
       fd = sc.fill_dst[u];
       refill = fd != 0;
       sc.oc[u] = oc;
       if (outcome) outcome[u] = oc;
     }
-    const uint32_t ih = block_append(from_host, &sc.gate->n_host);
+    const uint32_t ih = n_early + block_append(from_host, &sc.gate->n_host);
     if (from_host) {
       sc.host_list[ih] = u;
       sc.host_src[ih] = code;
@@ -1284,20 +1349,28 @@ __global__ __launch_bounds__(kBlock) void k_list_copy(const uint8_t *src, const 
 #ifndef LSM_HOST_UNROLL
 #define LSM_HOST_UNROLL 4
 #endif
+//
+// The list has two parts: its first n_early entries (misses known at batch
+// start, `late` false) and the n_host entries after them (the resolve's,
+// `late` true); each launch moves one part.
 template <bool kPow2>
 __global__ __launch_bounds__(kBlock) void k_host_fetch(const DevState d, Scratch sc, uint8_t *out, uint32_t nvec,
-                                                       uint32_t vshift) {
+                                                       uint32_t vshift, int late) {
   constexpr int kU = LSM_HOST_UNROLL;
   const Gate g = *sc.gate;
   if (g.err) return;
   const uint64_t R = d.R;
-  const uint64_t total = (uint64_t)g.n_host * nvec;
+  const uint32_t first = late ? g.n_early : 0u;
+  const uint64_t total = (uint64_t)(late ? g.n_host : g.n_early) * nvec;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  const uint32_t *list = sc.host_list + first;
+  const uint64_t *src = sc.host_src + first;
+  const u32x4 *bounce = sc.bounce ? reinterpret_cast<const u32x4 *>(sc.bounce) + (uint64_t)first * nvec : nullptr;
   auto entry = [&](uint64_t w, uint32_t &e, uint64_t &code) {
     if (w < total) {
       const uint32_t i = kPow2 ? (uint32_t)(w >> vshift) : (uint32_t)(w / nvec);
-      e = sc.host_list[i];
-      code = sc.host_src[i];
+      e = list[i];
+      code = src[i];
     }
   };
   uint32_t e[kU];
@@ -1316,8 +1389,8 @@ __global__ __launch_bounds__(kBlock) void k_host_fetch(const DevState d, Scratch
         const uint64_t byte = (kPow2 ? (w & (nvec - 1)) : (w % nvec)) * 16u;
         // bounce row i holds entry i: vector w is the w-th of the buffer
         const u32x4 *sp =
-            sc.bounce ? reinterpret_cast<const u32x4 *>(sc.bounce) + w
-                      : reinterpret_cast<const u32x4 *>(
+            bounce ? bounce + w
+                   : reinterpret_cast<const u32x4 *>(
                             ((code[k] & ~kSrcIndex) == kSrcRing ? d.ring_rows : d.store) + (code[k] & kSrcIndex) * R +
                             byte);
         v[k] = *sp;
@@ -1364,12 +1437,13 @@ void launch_copy(CopyMode mode, const DevState &d, uint64_t n, const Scratch &sc
   const uint32_t nvec = (uint32_t)(d.R / 16);
   const bool pow2 = (nvec & (nvec - 1)) == 0;
   const uint32_t vshift = pow2 ? (uint32_t)__builtin_ctz(nvec) : 0u;
-  if (mode == CopyMode::kHostToOut) {
+  if (mode == CopyMode::kHostToOut || mode == CopyMode::kHostEarly) {
     const unsigned g = grid_for(n * nvec, (uint64_t)kBlock * kUnroll, d.host_grid ? d.host_grid : LSM_HOST_GRID);
+    const int late = mode == CopyMode::kHostToOut;
     if (pow2)
-      hipLaunchKernelGGL((k_host_fetch<true>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift);
+      hipLaunchKernelGGL((k_host_fetch<true>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift, late);
     else
-      hipLaunchKernelGGL((k_host_fetch<false>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift);
+      hipLaunchKernelGGL((k_host_fetch<false>), dim3(g), dim3(kBlock), 0, s, d, sc, out, nvec, vshift, late);
     return;
   }
   switch (mode) {
@@ -1445,12 +1519,12 @@ __global__ __launch_bounds__(kBlock) void k_copy_plain(const u32x4 *src, u32x4 *
   }
 }
 
-__global__ void k_publish_host_count(const Gate *gate, uint32_t *dst) {
-  if (threadIdx.x == 0) *dst = gate->err ? 0u : gate->n_host;
+__global__ void k_publish_count(const Gate *gate, const uint32_t *count, uint32_t *dst) {
+  if (threadIdx.x == 0) *dst = gate->err ? 0u : *count;
 }
 
-void launch_publish_host_count(const Gate *gate, uint32_t *dst, hipStream_t s) {
-  hipLaunchKernelGGL(k_publish_host_count, dim3(1), dim3(64), 0, s, gate, dst);
+void launch_publish_count(const Gate *gate, const uint32_t *count, uint32_t *dst, hipStream_t s) {
+  hipLaunchKernelGGL(k_publish_count, dim3(1), dim3(64), 0, s, gate, count, dst);
 }
 
 // Device-to-device: tiles of 4 * kBlock vectors per block with the

@@ -60,6 +60,7 @@ enum StatSlot : int {
   kStEnqCopy,                                                          // enqueue finalize
   kStReqHits, kStReqVictimHits,                                        // per-request outcomes
   kStVhRing, kStVhStaged, kStVhSame,                                   // victim hits by row source
+  kStEarly,                                                            // misses listed before the walk
   kNumStat
 };
 constexpr unsigned kMaxGrid = 8192;  // grid cap of every grid-stride kernel
@@ -106,7 +107,7 @@ struct DedupResult {
 struct Gate {
   uint32_t err;
   uint32_t n_unique;
-  uint32_t n_host;   // host-fetch list
+  uint32_t n_host;   // host-fetch list: entries after the first n_early (appended by the resolve)
   uint32_t n_hbm;    // hit-copy list
   uint32_t n_fill;   // fill list
   uint32_t n_stage;  // staging list
@@ -115,7 +116,10 @@ struct Gate {
   // placed (their rows are in the host queue), and where this gather staged
   // the rest
   uint32_t q_count, q_before, q_stage_off;
-  uint32_t pad[3];
+  // host-fetch list entries [0, n_early): misses known from the batch-start
+  // state, listed right after the dedup and fetched before the set walk ends
+  uint32_t n_early;
+  uint32_t pad[2];
 };
 
 // A row-copy list: entry i moves row src[i] of its source to row dst[i] of its
@@ -144,6 +148,7 @@ struct Scratch {
   uint8_t *flags;
   uint8_t *oc;          // outcome of u (LSMGNN_HIT / _VICTIM_HIT / _MISS)
   uint8_t *dead;        // enqueue entry whose line was victim-hit in the same batch
+  uint8_t *early;       // 1: u's row is fetched by the early host fetch (a miss known at batch start)
   uint32_t *slot;       // cache slot (set*8+way) hit or filled by u
   uint32_t *evicted;    // node evicted by u's fill, or kEmpty
   uint32_t *enq_before; // enqueues by unique IDs below u in this batch
@@ -200,7 +205,9 @@ struct DevState {
   uint64_t stage_rows;   // rows per staging buffer: min(max_batch, V)
 };
 
-enum class CopyMode { kHbmToOut, kHostToOut, kCacheToStage, kOutToCache };
+// kHostEarly / kHostToOut: the host fetch of the host-fetch list's first
+// n_early entries, and of the rest
+enum class CopyMode { kHbmToOut, kHostToOut, kCacheToStage, kOutToCache, kHostEarly };
 
 // What the last kernel of a gather does for the victim queues: empty the
 // served slot `cur` and record in the gate what the prefetch of slot `next`
@@ -259,8 +266,13 @@ void launch_window_set(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit,
 void launch_window_rollback(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask,
                             hipStream_t s);
 void launch_copy_plain(const void *src, void *dst, uint64_t bytes, bool device_to_device, hipStream_t s);
-// pageable store: the host-fetch list's length (0 for a rejected gather) to pinned host memory
-void launch_publish_host_count(const Gate *gate, uint32_t *dst, hipStream_t s);
+// pageable store: a host-fetch list length in the gate (0 for a rejected gather) to pinned host memory
+void launch_publish_count(const Gate *gate, const uint32_t *count, uint32_t *dst, hipStream_t s);
+// right after the dedup: list the misses known from the batch-start state
+// (no way of the set holds the ID and the victim buffer has no entry for it)
+// as the first entries of the host-fetch list
+void launch_early(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, Counters *cn, StatGrids &grids,
+                  hipStream_t s);
 
 // host twin of the device set-index function
 uint64_t set_of_host(uint64_t x, uint64_t num_sets);

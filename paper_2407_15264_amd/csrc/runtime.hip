@@ -103,12 +103,14 @@ struct Flight {
   uint8_t *data_out = nullptr;
   bool data_prof = false;
   bool data_deferred = false;
-  hipEvent_t list_done = nullptr;  // pageable store: the host-fetch list and its length are written
-  uint32_t *hcount_host = nullptr, *hcount_dev = nullptr;  // pageable store: that length (pinned)
+  hipEvent_t early_done = nullptr;  // the host-fetch list's early part (misses known at batch start) is written
+  hipEvent_t list_done = nullptr;   // pageable store: the host-fetch list's rest is written
+  uint32_t *hcount_host = nullptr, *hcount_dev = nullptr;  // pageable store: the two parts' lengths (pinned)
   bool stats_pending = false;  // counters not yet added to the totals
   bool dma_pending = false;    // staged rows not yet queued for the ring
   bool dma_used = false;       // dma_done has been recorded at least once
   uint64_t dma_seq = 0, fill_seq = 0;  // positions of the ring write and the fill among the cache's dma submissions
+  bool fill_host = false;              // the fills ran on the host-link stream (blocking gather), not the dma one
   uint64_t t = 0, requests = 0;
   uint64_t enq_total = 0, tail_end = 0;  // enqueues of the gather, ring tail after it
   uint32_t q_before[lsm::kMaxQueues] = {}, q_placed[lsm::kMaxQueues] = {};  // queue mode, per slot
@@ -228,8 +230,7 @@ void release(lsmgnn_cache *c) {
   c->host_allocs.clear();
   for (Flight &f : c->fl)
     for (hipEvent_t e : {f.meta_done, f.finish_done, f.stage_done, f.hit_done, f.host_done, f.data_done, f.dma_done,
-                         f.pf_done,
-                         f.list_done})
+                         f.pf_done, f.early_done, f.list_done})
       if (e) (void)hipEventDestroy(e);
   for (PerfSet &p : c->ps)
     for (hipEvent_t e : p.e)
@@ -347,6 +348,14 @@ void meta_wait_dma(lsmgnn_cache *c, hipEvent_t e, uint64_t seq) {
   c->meta_dma_seen = seq;
 }
 
+// Make the meta stream wait for gather G's fills.
+void meta_wait_fills(lsmgnn_cache *c, const Flight &G) {
+  if (G.fill_host)
+    (void)hipStreamWaitEvent(c->meta, G.data_done, 0);
+  else
+    meta_wait_dma(c, G.data_done, G.fill_seq);
+}
+
 // Queue a harvested gather's ring write: its E enqueues have the sequence
 // numbers [tail_end - E, tail_end), of which the last min(E, V) survive; they
 // were staged in that order and land in at most two contiguous ring pieces.
@@ -366,6 +375,9 @@ void issue_dma(lsmgnn_cache *c, Flight &f, hipEvent_t after = nullptr) {
   PerfSet &p = c->ps[f.t % kPerfSets];
   const bool prof = p.pending && p.t == f.t;
   (void)hipStreamWaitEvent(c->dma, f.stage_done, 0);
+  // the gather's own host fetch may read ring rows this write overwrites
+  // (victim hits on older entries in slots its enqueues take)
+  (void)hipStreamWaitEvent(c->dma, f.host_done, 0);
   if (after) (void)hipStreamWaitEvent(c->dma, after, 0);
   if (prof) (void)hipEventRecord(p.e[kEvEnq0], c->dma);
   if (c->d.qmode) {
@@ -395,14 +407,14 @@ void issue_dma(lsmgnn_cache *c, Flight &f, hipEvent_t after = nullptr) {
   f.dma_seq = ++c->dma_subs;
 }
 
-// Pageable store: copy the rows of the gather's host-fetch list (misses and
-// victim hits) into its pinned bounce buffer, row i for list entry i, on the
-// pool's threads.  The list and the source codes were written by the resolve
-// kernel into pinned memory.
-void copy_host_rows(lsmgnn_cache *c, Flight &f, uint64_t n, bool prof) {
+// Pageable store: copy the rows of the gather's host-fetch list entries
+// [first, first + n) (misses and victim hits) into its pinned bounce buffer,
+// row i for list entry i, on the pool's threads.  The list and the source
+// codes were written by the early-miss and resolve kernels into pinned memory.
+void copy_host_rows(lsmgnn_cache *c, Flight &f, uint64_t first, uint64_t n, bool prof) {
   const uint64_t R = c->d.R;
-  const uint64_t *src = f.hsrc_host;
-  uint8_t *bounce = f.bounce_host;
+  const uint64_t *src = f.hsrc_host + first;
+  uint8_t *bounce = f.bounce_host + first * R;
   const uint8_t *store = c->store_host, *ring = c->ring_host;
   const auto t0 = std::chrono::steady_clock::now();
   c->pool->run(n, 256, [&](uint64_t i0, uint64_t i1) {
@@ -462,7 +474,7 @@ void harvest_profile(lsmgnn_cache *c, PerfSet &p) {
 void queue_stage(lsmgnn_cache *c, uint64_t g) {
   DevState &d = c->d;
   Flight &G = c->fl[g & 1], &P = c->fl[(g + 1) & 1];
-  if (P.used) meta_wait_dma(c, P.data_done, P.fill_seq);
+  if (P.used) meta_wait_fills(c, P);
   if (G.dma_used) meta_wait_dma(c, G.dma_done, G.dma_seq);
   if (G.data_n && d.V) lsm::launch_copy(CopyMode::kCacheToStage, d, G.data_n, G.sc, G.data_out, c->meta);
   (void)hipEventRecord(G.stage_done, c->meta);
@@ -487,22 +499,28 @@ void queue_hit(lsmgnn_cache *c, uint64_t g) {
   (void)hipEventRecord(G.hit_done, c->meta);
 }
 
-// Fills of gather g on the dma stream (behind the ring writes queued there so
-// far), once its host fetch, staging and hit copy are done.  Gather g's own
-// ring write is queued after them, so it follows gather g's host fetch.
-void queue_fills(lsmgnn_cache *c, uint64_t g) {
+// Fills of gather g, once its host fetch, staging and hit copy are done.
+// Pipelined gathers queue them on the dma stream, behind the ring writes
+// queued there so far, so that the next host fetch need not wait for them.
+// A blocking gather (`on_host`) queues them on the host-link stream right
+// behind its own host fetch: its caller waits for them, and on the dma stream
+// they would wait for the previous gather's ring write, which runs beside the
+// host fetch and often ends after it.
+void queue_fills(lsmgnn_cache *c, uint64_t g, bool on_host) {
   Flight &G = c->fl[g & 1];
   PerfSet &ps = c->ps[g % kPerfSets];
-  (void)hipStreamWaitEvent(c->dma, G.host_done, 0);
-  (void)hipStreamWaitEvent(c->dma, G.hit_done, 0);  // after the staging on the same stream
-  if (G.data_prof) (void)hipEventRecord(ps.e[kEvFill0], c->dma);
-  if (G.data_n) lsm::launch_copy(CopyMode::kOutToCache, c->d, G.data_n, G.sc, G.data_out, c->dma);
+  const hipStream_t st = on_host ? c->host : c->dma;
+  if (!on_host) (void)hipStreamWaitEvent(st, G.host_done, 0);
+  (void)hipStreamWaitEvent(st, G.hit_done, 0);  // after the staging on the meta stream
+  if (G.data_prof) (void)hipEventRecord(ps.e[kEvFill0], st);
+  if (G.data_n) lsm::launch_copy(CopyMode::kOutToCache, c->d, G.data_n, G.sc, G.data_out, st);
   if (G.data_prof) {
-    (void)hipEventRecord(ps.e[kEvFill1], c->dma);
-    (void)hipEventRecord(ps.e[kEvAll1], c->dma);
+    (void)hipEventRecord(ps.e[kEvFill1], st);
+    (void)hipEventRecord(ps.e[kEvAll1], st);
   }
-  (void)hipEventRecord(G.data_done, c->dma);
-  G.fill_seq = ++c->dma_subs;
+  (void)hipEventRecord(G.data_done, st);
+  G.fill_host = on_host;
+  G.fill_seq = on_host ? 0 : ++c->dma_subs;
 }
 
 // Queue the latest gather's hit copy and fills if they were deferred.
@@ -513,7 +531,7 @@ void flush_deferred(lsmgnn_cache *c) {
   if (!G.data_deferred) return;
   G.data_deferred = false;
   queue_hit(c, g);
-  queue_fills(c, g);
+  queue_fills(c, g, false);
 }
 
 // Wait for every queued kernel and copy, then account everything in issue
@@ -578,13 +596,14 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
     if (prof) (void)hipEventRecord(ps.e[e], st);
   };
   uint8_t *outp = static_cast<uint8_t *>(out);
+  const bool blocking = !defer;  // the caller waits for this gather's rows
   if (queues) defer = false;  // the prefetch of the next queue follows this gather's staging
 
   // inputs are ready once the caller's queued work is; this parity's arrays
   // are free once gather t-2's rows have moved
   if (hipEventRecord(c->ev_in, s) != hipSuccess) return fail_device(c);
   (void)hipStreamWaitEvent(c->meta, c->ev_in, 0);
-  if (f.used) meta_wait_dma(c, f.data_done, f.fill_seq);
+  if (f.used) meta_wait_fills(c, f);
 
   // the window list of the minibatch being gathered is never consulted again:
   // the first kernel clears its bits
@@ -603,13 +622,17 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   if (d.U > 1 && t % d.U == 0) lsm::launch_refresh(d, (uint32_t)t, c->cn, c->meta);
   lsm::StatGrids grids{};
   if (n) {
+    // the misses known at batch start first: their rows cross the link while
+    // the rest of the metadata runs (pageable store: the host threads copy
+    // them meanwhile)
+    lsm::launch_early(d, n, t, f.sc, c->cn, grids, c->meta);
+    if (c->pageable) lsm::launch_publish_count(f.sc.gate, &f.sc.gate->n_early, f.hcount_dev, c->meta);
+    (void)hipEventRecord(f.early_done, c->meta);
     lsm::launch_group_by_set(d, ids, n, inverse, f.sc, c->cn, c->meta);
     lsm::launch_set_walk(d, n, (uint32_t)t, f.sc, c->cn, grids, c->meta);
     lsm::launch_ring_resolve(d, n, t, f.sc, outcome, c->cn, grids, c->meta);
-    // pageable store: the host threads start copying as soon as the list is
-    // known, while the rest of the metadata runs
     if (c->pageable) {
-      lsm::launch_publish_host_count(f.sc.gate, f.hcount_dev, c->meta);
+      lsm::launch_publish_count(f.sc.gate, &f.sc.gate->n_host, f.hcount_dev + 1, c->meta);
       (void)hipEventRecord(f.list_done, c->meta);
     }
   }
@@ -639,18 +662,27 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   lsm::launch_finish(c->cn, f.hc_dev, f.sc.stat_part, grids, d.tail, qf, ann, c->meta);
   (void)hipEventRecord(f.finish_done, c->meta);
 
-  // host fetch (PCIe ingress), right after gather t-1's on the same stream;
-  // with a pageable store it is launched once the host has copied the rows
-  const bool pageable_list = c->pageable;  // the host copies the listed rows once the list is known
-  auto host_fetch = [&]() {
+  // host fetch (PCIe ingress), right after gather t-1's on the same stream,
+  // in two parts: the misses known at batch start once they are listed, the
+  // rest once the resolve has listed it (and the ring write of gather t-2,
+  // whose rows the victim hits may read, has landed); with a pageable store
+  // each part is launched once the host has copied its rows
+  auto host_fetch_early = [&]() {
+    if (n) (void)hipStreamWaitEvent(c->host, f.early_done, 0);
+    rec(kEvHost0, c->host);
+    if (n) lsm::launch_copy(CopyMode::kHostEarly, d, n, f.sc, outp, c->host);
+  };
+  auto host_fetch_late = [&]() {
     (void)hipStreamWaitEvent(c->host, f.meta_done, 0);
     if (!c->pageable && f.dma_used) (void)hipStreamWaitEvent(c->host, f.dma_done, 0);
-    rec(kEvHost0, c->host);
     if (n) lsm::launch_copy(CopyMode::kHostToOut, d, n, f.sc, outp, c->host);
     rec(kEvHost1, c->host);
     (void)hipEventRecord(f.host_done, c->host);
   };
-  if (!c->pageable) host_fetch();
+  if (!c->pageable) {
+    host_fetch_early();
+    host_fetch_late();
+  }
 
   // gather t-1's deferred hit copy and fills, now behind this gather's
   // metadata
@@ -667,25 +699,31 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   if (hipGetLastError() != hipSuccess) return fail_device(c);
 
   // the GPU runs on while the host waits for the dedup result (with a pageable
-  // store: for the host-fetch list); the meta stream is in order, so gather
-  // t-1's counters are published by then and its ring write can be queued
-  if (hipEventSynchronize(pageable_list && n ? f.list_done : c->ev_dedup) != hipSuccess) return fail_device(c);
+  // store: for the early part of the host-fetch list); the meta stream is in
+  // order, so gather t-1's counters are published by then and its ring write
+  // can be queued
+  const bool pageable_lists = c->pageable && n;
+  if (hipEventSynchronize(pageable_lists ? f.early_done : c->ev_dedup) != hipSuccess) return fail_device(c);
   harvest_stats(c, pf);
   issue_dma(c, pf, n ? f.meta_done : nullptr);
   if (queues) (void)hipEventRecord(c->ev_q, c->dma);  // every queue write up to gather t-1's
   if (c->pageable) {
-    if (n && !(dedup && c->dd->err)) {
+    const bool rows = n && !(dedup && c->dd->err);
+    const uint64_t n_early = rows ? f.hcount_host[0] : 0;
+    if (rows) copy_host_rows(c, f, 0, n_early, prof);  // store rows only
+    host_fetch_early();
+    if (rows) {
+      if (hipEventSynchronize(f.list_done) != hipSuccess) return fail_device(c);
       // ring rows are read only for entries of gathers up to t-2, whose ring
       // writes must have landed
       if (f.dma_used && hipEventSynchronize(f.dma_done) != hipSuccess) return fail_device(c);
-      copy_host_rows(c, f, *f.hcount_host, prof);
+      copy_host_rows(c, f, n_early, f.hcount_host[1], prof);
     }
-    host_fetch();
+    host_fetch_late();
   }
 
-  // fills after the host fetch, the staging and the hit copy, queued behind
-  // gather t-1's ring write so that the next host fetch need not wait for them
-  if (!defer) queue_fills(c, t);
+  // fills after the host fetch, the staging and the hit copy
+  if (!defer) queue_fills(c, t, blocking);
   if (hipGetLastError() != hipSuccess) return fail_device(c);
   const uint32_t err = dedup ? c->dd->err : 0u;
   const uint32_t U = dedup ? c->dd->n_unique : 0u;
@@ -872,7 +910,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
             dev_alloc(c, &sc.seg, B) && dev_alloc(c, &sc.seg_u, B) && dev_alloc(c, &sc.seg_x, B) &&
             dev_alloc(c, &sc.seg_st, B) && dev_alloc(c, &sc.big, B / (lsm::kSmallSet + 1) + 1) && dev_alloc(c, &sc.kind, B) && dev_alloc(c, &sc.flags, B) &&
             dev_alloc(c, &sc.oc, B) &&
-            dev_alloc(c, &sc.dead, B) && dev_alloc(c, &sc.evicted, B) && dev_alloc(c, &sc.enq_before, B) &&
+            dev_alloc(c, &sc.dead, B) && dev_alloc(c, &sc.early, B) && dev_alloc(c, &sc.evicted, B) && dev_alloc(c, &sc.enq_before, B) &&
             dev_alloc(c, &sc.scan_part, B / lsm::kScanChunk + 2) && dev_alloc(c, &sc.this_q, B) &&
             dev_alloc(c, &sc.this_enq, B) && dev_alloc(c, &sc.slot, B) && dev_alloc(c, &sc.fill_dst, B) &&
             dev_alloc(c, &sc.stat_part, (uint64_t)lsm::kNumStat * lsm::kMaxGrid) &&
@@ -888,7 +926,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
     if (ok && V) f.sc.staging = d.rows + (d.stage_row0 + (uint64_t)(&f - c->fl) * d.stage_rows) * R;
     if (ok && pageable) {
       // the host reads the host-fetch list and fills the bounce rows
-      ok = host_alloc(c, &f.hcount_host, &f.hcount_dev, sizeof(uint32_t), true) &&
+      ok = host_alloc(c, &f.hcount_host, &f.hcount_dev, 2 * sizeof(uint32_t), true) &&
            host_alloc(c, &f.hlist_host, &f.sc.host_list, B * sizeof(uint32_t), false) &&
            host_alloc(c, &f.hsrc_host, &f.sc.host_src, B * sizeof(uint64_t), false) &&
            host_alloc(c, &f.bounce_host, &f.sc.bounce, B * R, false);
@@ -922,7 +960,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   for (Flight &f : c->fl)
     for (hipEvent_t *e : {&f.meta_done, &f.finish_done, &f.stage_done, &f.hit_done, &f.host_done, &f.data_done,
                           &f.dma_done,
-                          &f.pf_done, &f.list_done})
+                          &f.pf_done, &f.early_done, &f.list_done})
       ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
   for (PerfSet &p : c->ps)
     for (hipEvent_t &e : p.e) ok = ok && hipEventCreate(&e) == hipSuccess;

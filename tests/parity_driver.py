@@ -74,10 +74,15 @@ def compare_state(cache, orc, where=""):
 
 def run_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, announce=None,
                near_threshold=0, rows="all", max_batch=None, device=0, state_every=0, label="parity",
-               store_gpu=None, policy="hybrid", victim_mode="fifo", refresh_period=1):
+               store_gpu=None, policy="hybrid", victim_mode="fifo", refresh_period=1, per_gather_stats=True):
     """rows: 'all' -> compare every gathered row with the oracle's; an int k ->
     compare with the oracle on every k-th gather and, on every gather, with the
-    backing-store rows indexed on the GPU (store_gpu, a device copy)."""
+    backing-store rows indexed on the GPU (store_gpu, a device copy).
+
+    per_gather_stats=False: the counters are compared only as totals at the
+    end, so no call waits for the library's internal streams between gathers
+    (a blocking gather waits only for its own rows); the rows, unique IDs,
+    inverse and outcomes are still compared after every gather."""
     import torch
     dev = torch.device("cuda", device)
     announce = batches if announce is None else announce
@@ -95,6 +100,7 @@ def run_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, 
         cache.advance(dev_ann[j])
         orc.advance(announce[j])
     t0 = time.time()
+    o_tot = {k: 0 for k in COUNT_KEYS}
     for b, ids in enumerate(batches):
         where = f"{label} gather {b}"
         r = cache.gather(dev_bat[b], inverse=True, outcome=True)
@@ -113,10 +119,15 @@ def run_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, 
             raise AssertionError(f"{where}: outcome differs at unique idx {bad.tolist()} "
                                  f"(ids {o['uniq'][bad].tolist()}): gpu {oc[bad].tolist()} "
                                  f"oracle {o['outcome'][bad].tolist()}")
-        last, _ = cache.stats()
-        for k in COUNT_KEYS:
-            if last[k] != o["stats"][k]:
-                raise AssertionError(f"{where}: counter {k}: gpu {last[k]} oracle {o['stats'][k]}")
+        if per_gather_stats:
+            last, _ = cache.stats()
+            for k in COUNT_KEYS:
+                if last[k] != o["stats"][k]:
+                    raise AssertionError(f"{where}: counter {k}: gpu {last[k]} oracle {o['stats'][k]}")
+        else:
+            for k in COUNT_KEYS:
+                if k != "batch":
+                    o_tot[k] += o["stats"][k]
         if full_rows:
             if not np.array_equal(r.out.cpu().numpy(), o["out"]):
                 bad = np.flatnonzero((r.out.cpu().numpy() != o["out"]).any(axis=1))[:5]
@@ -133,6 +144,10 @@ def run_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, 
             orc.advance(announce[b + L + 1])
     compare_state(cache, orc, f"{label} end")
     tot = cache.stats()[1]
+    if not per_gather_stats:
+        for k, v in o_tot.items():
+            if k != "batch" and tot[k] != v:
+                raise AssertionError(f"{label}: total {k}: gpu {tot[k]} oracle {v}")
     cache.close()
     orc.close()
     return dict(total=tot, seconds=time.time() - t0)

@@ -509,6 +509,34 @@ def test_long_streams_window_wrap(seed, pipelined):
                    label=f"long{seed}")
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_blocking_gathers_back_to_back(seed):
+    """Blocking gathers with no call in between that waits for the library's
+    internal streams (counters are compared as totals at the end): each
+    gather's fills, the ring writes and the next gather's staging are ordered
+    by the library's events alone.  Rows, unique IDs, inverse and outcomes
+    after every gather; the final cache and ring state.  Odd seeds use a
+    pageable store, every fourth the victim queues."""
+    n, S, V, L, T, stat, batches = _long_case(200 + seed)
+    mode = "queues" if seed % 4 == 3 else "fifo"
+    if mode == "queues":
+        V = max(V, 1) * (L + 1)
+    log(f"case: blocking back to back seed {seed} {mode}: N={n} S={S} V={V} L={L} T={T}")
+    store = Store.random_bytes(n, 32, seed, pinned=seed % 2 == 0)
+    run_parity(store, stat, S, V, L, batches, near_threshold=T, rows="all", label=f"blocking{seed}",
+               victim_mode=mode, per_gather_stats=False)
+
+
+def test_blocking_gathers_back_to_back_rmat14():
+    cfg = W.CONFIGS[W.RMAT14]
+    log(f"case: {cfg.name}, blocking gathers back to back")
+    wl, batches = config_stream(cfg)
+    store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
+    res = run_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead, batches,
+                     rows="all", label=f"{cfg.name}-blocking", per_gather_stats=False)
+    assert res["total"]["victim_hits"] > 0
+
+
 @pytest.mark.parametrize("seed", range(12))
 def test_pageable_store_random(seed):
     """The same policy with the backing store in ordinary pageable memory:
