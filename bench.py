@@ -728,7 +728,11 @@ def main():
         launches = max(sum(pr[key + "_launches"] for pr in profs), 1)
         kern[name] = dict(ms_total=ms, launches=launches, rows=rows_k, avg_us=1e3 * ms / launches,
                           bytes_per_launch=kbytes / launches,
-                          GBps=(kbytes / (ms / 1e3) / 1e9) if ms > 0 else 0.0, bound=bound)
+                          GBps=(kbytes / (ms / 1e3) / 1e9) if ms > 0 else 0.0, bound=bound,
+                          launches_per_minibatch=launches / args.steps,
+                          us_per_minibatch=1e3 * ms / args.steps,
+                          # busy time per minibatch over the profiled pass's own step time
+                          share_of_step=ms / (1e3 * dt_p))
     kern["ring_write_dma"]["engine"] = "runtime copy (hipMemcpyAsync of the staged rows), not one of our kernels"
     hc_ms = sum(pr["host_copy_ms"] for pr in profs)
     if hc_ms > 0:
@@ -749,7 +753,9 @@ def main():
                 "frac": kd["GBps"] / peak, "traffic": None,
                 "peak_source": "measured in this run (best of pinned DMA and zero-copy kernel)",
                 "frac_of_published_pcie5_x16": kd["GBps"] / PCIE5_X16_PEAK_GBPS}
-    roof.update(kernel=dom, avg_launch_us=kd["avg_us"], bytes_per_launch=kd["bytes_per_launch"])
+    roof.update(kernel=dom, avg_launch_us=kd["avg_us"], bytes_per_launch=kd["bytes_per_launch"],
+                launches_per_minibatch=kd["launches_per_minibatch"], us_per_minibatch=kd["us_per_minibatch"],
+                share_of_step=kd["share_of_step"])
     if kd["bound"] == "host_link":
         # both link directions over the headline pass: rows in (host fetch,
         # prefetch) and rows out (ring writes), against the duplex ceiling

@@ -170,7 +170,10 @@ typedef struct {
 /* Accumulated device time of the data movement (filled only while profiling
    is on; see lsmgnn_set_profiling).  Bytes are algorithmic: rows moved times
    row_bytes, per direction.  The enqueue figures time the ring write (the
-   runtime copy of the staged evicted rows), not the staging kernel. */
+   runtime copy of the staged evicted rows), not the staging kernel.  A
+   gather's host fetch is two launches (the misses known at batch start, then
+   the remaining host rows), both counted; its time excludes the wait between
+   them. */
 typedef struct {
   double hbm_copy_ms;   uint64_t hbm_copy_launches;   uint64_t hbm_copy_rows;   /* cache -> out */
   double host_fetch_ms; uint64_t host_fetch_launches; uint64_t host_fetch_rows; /* store/ring -> out */

@@ -79,8 +79,10 @@ struct DeviceGuard {
   }
 };
 
-enum { kEvHbm0, kEvHbm1, kEvEnq0, kEvEnq1, kEvHost0, kEvHost1, kEvFill0, kEvFill1, kEvAll0, kEvAll1, kEvPf0, kEvPf1,
-       kNumEv };
+// The host fetch is two launches: kEvHost0..kEvHostMid brackets the first
+// (the misses known at batch start), kEvHostLate..kEvHost1 the second.
+enum { kEvHbm0, kEvHbm1, kEvEnq0, kEvEnq1, kEvHost0, kEvHostMid, kEvHostLate, kEvHost1, kEvFill0, kEvFill1, kEvAll0,
+       kEvAll1, kEvPf0, kEvPf1, kNumEv };
 
 // One gather in flight; two of these alternate by gather parity.
 struct Flight {
@@ -348,6 +350,18 @@ void meta_wait_dma(lsmgnn_cache *c, hipEvent_t e, uint64_t seq) {
   c->meta_dma_seen = seq;
 }
 
+// Order the meta stream after the work queued so far on the caller's stream
+// s.  If that work is already complete there is nothing to wait for, and the
+// first kernel need not wait for a marker on another queue.
+bool after_caller(lsmgnn_cache *c, hipStream_t s) {
+  if (hipGetLastError() != hipSuccess) return false;  // an earlier call failed
+  const hipError_t q = hipStreamQuery(s);
+  if (q == hipSuccess) return true;
+  (void)hipGetLastError();  // the query's hipErrorNotReady is no failure
+  if (q != hipErrorNotReady) return false;
+  return hipEventRecord(c->ev_in, s) == hipSuccess && hipStreamWaitEvent(c->meta, c->ev_in, 0) == hipSuccess;
+}
+
 // Make the meta stream wait for gather G's fills.
 void meta_wait_fills(lsmgnn_cache *c, const Flight &G) {
   if (G.fill_host)
@@ -450,8 +464,8 @@ void harvest_profile(lsmgnn_cache *c, PerfSet &p) {
       c->acc.enqueue_launches += 1;
       c->acc.enqueue_rows += p.n_enq;
     }
-    c->acc.host_fetch_ms += el(kEvHost0, kEvHost1);
-    c->acc.host_fetch_launches += 1;
+    c->acc.host_fetch_ms += el(kEvHost0, kEvHostMid) + el(kEvHostLate, kEvHost1);  // not the wait between them
+    c->acc.host_fetch_launches += 2;
     c->acc.host_fetch_rows += p.n_host;
     c->acc.fill_ms += el(kEvFill0, kEvFill1);
     c->acc.fill_launches += 1;
@@ -601,8 +615,7 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
 
   // inputs are ready once the caller's queued work is; this parity's arrays
   // are free once gather t-2's rows have moved
-  if (hipEventRecord(c->ev_in, s) != hipSuccess) return fail_device(c);
-  (void)hipStreamWaitEvent(c->meta, c->ev_in, 0);
+  if (!after_caller(c, s)) return fail_device(c);
   if (f.used) meta_wait_fills(c, f);
 
   // the window list of the minibatch being gathered is never consulted again:
@@ -611,6 +624,28 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   const bool clear = d.L > 0 && c->win_batch[slot] == (int64_t)t;
   const int64_t *clear_ids = clear ? c->win_ids + (uint64_t)slot * c->max_batch : nullptr;
   const uint64_t clear_n = clear ? c->win_len[slot] : 0;
+
+  // host fetch (PCIe ingress), right after gather t-1's on the same stream,
+  // in two parts: the misses known at batch start once they are listed, the
+  // rest once the resolve has listed it (and the ring write of gather t-2,
+  // whose rows the victim hits may read, has landed).  Each part is queued as
+  // soon as the event it waits for is, so that the host's submission of the
+  // metadata kernels does not hold it back; with a pageable store each part is
+  // queued once the host has copied its rows.
+  auto host_fetch_early = [&]() {
+    if (n) (void)hipStreamWaitEvent(c->host, f.early_done, 0);
+    rec(kEvHost0, c->host);
+    if (n) lsm::launch_copy(CopyMode::kHostEarly, d, n, f.sc, outp, c->host);
+    rec(kEvHostMid, c->host);
+  };
+  auto host_fetch_late = [&]() {
+    (void)hipStreamWaitEvent(c->host, f.meta_done, 0);
+    if (!c->pageable && f.dma_used) (void)hipStreamWaitEvent(c->host, f.dma_done, 0);
+    rec(kEvHostLate, c->host);
+    if (n) lsm::launch_copy(CopyMode::kHostToOut, d, n, f.sc, outp, c->host);
+    rec(kEvHost1, c->host);
+    (void)hipEventRecord(f.host_done, c->host);
+  };
 
   rec(kEvAll0, c->meta);
   const uint64_t ann_n = an.on ? an.n : 0;
@@ -628,6 +663,7 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
     lsm::launch_early(d, n, t, f.sc, c->cn, grids, c->meta);
     if (c->pageable) lsm::launch_publish_count(f.sc.gate, &f.sc.gate->n_early, f.hcount_dev, c->meta);
     (void)hipEventRecord(f.early_done, c->meta);
+    if (!c->pageable) host_fetch_early();
     lsm::launch_group_by_set(d, ids, n, inverse, f.sc, c->cn, c->meta);
     lsm::launch_set_walk(d, n, (uint32_t)t, f.sc, c->cn, grids, c->meta);
     lsm::launch_ring_resolve(d, n, t, f.sc, outcome, c->cn, grids, c->meta);
@@ -639,6 +675,10 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   // the host fetch needs only the resolve's list; the rest of the metadata
   // runs beside it
   (void)hipEventRecord(f.meta_done, c->meta);
+  if (!c->pageable) {
+    if (!n) host_fetch_early();  // no rows: only its events
+    host_fetch_late();
+  }
   if (n) {
     lsm::launch_ring_enqueue(d, ids, n, t, f.sc, c->cn, grids, c->meta);
   }
@@ -661,28 +701,6 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   }
   lsm::launch_finish(c->cn, f.hc_dev, f.sc.stat_part, grids, d.tail, qf, ann, c->meta);
   (void)hipEventRecord(f.finish_done, c->meta);
-
-  // host fetch (PCIe ingress), right after gather t-1's on the same stream,
-  // in two parts: the misses known at batch start once they are listed, the
-  // rest once the resolve has listed it (and the ring write of gather t-2,
-  // whose rows the victim hits may read, has landed); with a pageable store
-  // each part is launched once the host has copied its rows
-  auto host_fetch_early = [&]() {
-    if (n) (void)hipStreamWaitEvent(c->host, f.early_done, 0);
-    rec(kEvHost0, c->host);
-    if (n) lsm::launch_copy(CopyMode::kHostEarly, d, n, f.sc, outp, c->host);
-  };
-  auto host_fetch_late = [&]() {
-    (void)hipStreamWaitEvent(c->host, f.meta_done, 0);
-    if (!c->pageable && f.dma_used) (void)hipStreamWaitEvent(c->host, f.dma_done, 0);
-    if (n) lsm::launch_copy(CopyMode::kHostToOut, d, n, f.sc, outp, c->host);
-    rec(kEvHost1, c->host);
-    (void)hipEventRecord(f.host_done, c->host);
-  };
-  if (!c->pageable) {
-    host_fetch_early();
-    host_fetch_late();
-  }
 
   // gather t-1's deferred hit copy and fills, now behind this gather's
   // metadata
@@ -1008,8 +1026,7 @@ lsmgnn_status lsmgnn_advance(lsmgnn_cache *c, const int64_t *ids, uint64_t n, vo
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool record = j > c->t && c->d.L > 0 && n > 0;  // lists for j <= t are never consulted
   const int slot = (int)(j % (c->d.L + 1));
-  if (hipEventRecord(c->ev_in, s) != hipSuccess) return fail_device(c);
-  (void)hipStreamWaitEvent(c->meta, c->ev_in, 0);
+  if (!after_caller(c, s)) return fail_device(c);
   const uint32_t bit = (uint32_t)(j & 31u);
   if (n)
     lsm::launch_window_set(ids, n, c->d.N, bit, c->d.mask, c->win_ids + (uint64_t)slot * c->max_batch, record,
@@ -1047,8 +1064,11 @@ lsmgnn_status lsmgnn_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, voi
   st = issue_gather(c, ids, n, Announce{}, out, unique_ids, inverse, outcome, n_unique, s, &t, false);
   if (st != LSMGNN_OK) return st;
   Flight &f = c->fl[t & 1];
-  if (hipStreamWaitEvent(s, f.data_done, 0) != hipSuccess || hipEventSynchronize(f.finish_done) != hipSuccess ||
-      hipStreamSynchronize(s) != hipSuccess)
+  // every output is written once the fills are done (they follow the host
+  // fetch, the hit copy and, on the meta stream, all the metadata); later work
+  // on the caller's stream is ordered after them
+  if (hipEventSynchronize(f.data_done) != hipSuccess || hipEventSynchronize(f.finish_done) != hipSuccess ||
+      hipStreamWaitEvent(s, f.data_done, 0) != hipSuccess)
     return fail_device(c);
   harvest_stats(c, f);  // its ring write is queued by the next call (after that gather's metadata) or a sync
   return LSMGNN_OK;
