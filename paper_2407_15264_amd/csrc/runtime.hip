@@ -44,7 +44,9 @@
 //     with a pageable store only after the host threads copied gather t's rows.
 // Every call first makes the meta stream wait for the work already queued on
 // the caller's stream (the IDs and the output buffers).
+#include <emmintrin.h>
 #include <hip/hip_runtime.h>
+#include <xmmintrin.h>
 
 #include <chrono>
 #include <cstdint>
@@ -425,18 +427,37 @@ void issue_dma(lsmgnn_cache *c, Flight &f, hipEvent_t after = nullptr) {
 // [first, first + n) (misses and victim hits) into its pinned bounce buffer,
 // row i for list entry i, on the pool's threads.  The list and the source
 // codes were written by the early-miss and resolve kernels into pinned memory.
+//
+// Each thread reads the source rows a few entries ahead (software prefetch:
+// the rows are scattered over the store, and one row at a time per thread
+// leaves the memory system mostly idle) and writes the bounce rows with
+// non-temporal stores: the GPU reads them over the link, so the CPU caches
+// need not hold them, and a streaming store does not first read the line.
+// Bounce rows are 16-byte aligned (row_bytes is a multiple of 16).
 void copy_host_rows(lsmgnn_cache *c, Flight &f, uint64_t first, uint64_t n, bool prof) {
   const uint64_t R = c->d.R;
   const uint64_t *src = f.hsrc_host + first;
   uint8_t *bounce = f.bounce_host + first * R;
   const uint8_t *store = c->store_host, *ring = c->ring_host;
   const auto t0 = std::chrono::steady_clock::now();
+  constexpr uint64_t kAhead = 16;  // rows in flight per thread (measured: 16 > 8 > 4)
   c->pool->run(n, 256, [&](uint64_t i0, uint64_t i1) {
-    for (uint64_t i = i0; i < i1; ++i) {
+    auto row = [&](uint64_t i) {
       const uint64_t code = src[i];
-      const uint8_t *s = ((code & ~lsm::kSrcIndex) == lsm::kSrcRing ? ring : store) + (code & lsm::kSrcIndex) * R;
-      std::memcpy(bounce + i * R, s, R);
+      return ((code & ~lsm::kSrcIndex) == lsm::kSrcRing ? ring : store) + (code & lsm::kSrcIndex) * R;
+    };
+    auto prefetch = [&](uint64_t i) {
+      const char *p = reinterpret_cast<const char *>(row(i));
+      for (uint64_t off = 0; off < R; off += 64) _mm_prefetch(p + off, _MM_HINT_T0);
+    };
+    for (uint64_t i = i0; i < i1 && i < i0 + kAhead; ++i) prefetch(i);
+    for (uint64_t i = i0; i < i1; ++i) {
+      if (i + kAhead < i1) prefetch(i + kAhead);
+      const __m128i *s = reinterpret_cast<const __m128i *>(row(i));
+      __m128i *d = reinterpret_cast<__m128i *>(bounce + i * R);
+      for (uint64_t k = 0; k < R / 16; ++k) _mm_stream_si128(d + k, _mm_loadu_si128(s + k));
     }
+    _mm_sfence();  // the streaming stores are visible before the chunk counts as done
   });
   if (prof) {
     c->acc.host_copy_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
