@@ -675,7 +675,10 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
     lsm::launch_dedup(d, ids, n, ann_n ? an.ids : nullptr, ann_n, clear_ids, clear_n, (uint32_t)(t & 31u), f.sc,
                       unique_ids, c->cn, c->dd_dev, c->meta);
   (void)hipEventRecord(c->ev_dedup, c->meta);
-  if (d.U > 1 && t % d.U == 0) lsm::launch_refresh(d, (uint32_t)t, c->cn, c->meta);
+  // the update of the dynamic information (every U-th gather) reads the window
+  // bits the dedup updated; the early-miss list neither reads what it writes
+  // nor needs it, so it runs after that list
+  const bool refresh = d.U > 1 && t % d.U == 0;
   lsm::StatGrids grids{};
   if (n) {
     // the misses known at batch start first: their rows cross the link while
@@ -685,6 +688,7 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
     if (c->pageable) lsm::launch_publish_count(f.sc.gate, &f.sc.gate->n_early, f.hcount_dev, c->meta);
     (void)hipEventRecord(f.early_done, c->meta);
     if (!c->pageable) host_fetch_early();
+    if (refresh) lsm::launch_refresh(d, (uint32_t)t, c->cn, c->meta);
     lsm::launch_group_by_set(d, ids, n, inverse, f.sc, c->cn, c->meta);
     lsm::launch_set_walk(d, n, (uint32_t)t, f.sc, c->cn, grids, c->meta);
     lsm::launch_ring_resolve(d, n, t, f.sc, outcome, c->cn, grids, c->meta);
@@ -692,6 +696,8 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
       lsm::launch_publish_count(f.sc.gate, &f.sc.gate->n_host, f.hcount_dev + 1, c->meta);
       (void)hipEventRecord(f.list_done, c->meta);
     }
+  } else if (refresh) {
+    lsm::launch_refresh(d, (uint32_t)t, c->cn, c->meta);
   }
   // the host fetch needs only the resolve's list; the rest of the metadata
   // runs beside it
