@@ -121,22 +121,37 @@ __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host,
   __shared__ uint32_t red[kNumStat][kBlock / 64];
   __shared__ uint32_t sums[kNumStat];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  // Each pass loads one partial of every slot before adding any: the loads
+  // are independent, so a pass costs one memory round trip (several µs while
+  // host-link reads are in flight beside this kernel) instead of one per slot.
+  uint32_t gmax = 0;
+#pragma unroll
+  for (int st = 0; st < kNumStat; ++st) gmax = grids.g[st] > gmax ? grids.g[st] : gmax;
+  uint32_t v[kNumStat];
+#pragma unroll
+  for (int st = 0; st < kNumStat; ++st) v[st] = 0;
+  for (uint32_t b = threadIdx.x; b < gmax; b += kBlock) {
+    uint32_t a[kNumStat];
+#pragma unroll
+    for (int st = 0; st < kNumStat; ++st) a[st] = b < grids.g[st] ? part[st * kMaxGrid + b] : 0u;
+#pragma unroll
+    for (int st = 0; st < kNumStat; ++st) v[st] += a[st];
+  }
 #pragma unroll
   for (int st = 0; st < kNumStat; ++st) {
-    uint32_t v = 0;
-    // four independent loads per pass keep the partials' reads in flight
-    for (uint32_t b = threadIdx.x; b < grids.g[st]; b += 4 * kBlock) {
-      uint32_t a0 = part[st * kMaxGrid + b];
-      uint32_t a1 = b + kBlock < grids.g[st] ? part[st * kMaxGrid + b + kBlock] : 0u;
-      uint32_t a2 = b + 2 * kBlock < grids.g[st] ? part[st * kMaxGrid + b + 2 * kBlock] : 0u;
-      uint32_t a3 = b + 3 * kBlock < grids.g[st] ? part[st * kMaxGrid + b + 3 * kBlock] : 0u;
-      v += a0 + a1 + a2 + a3;
-    }
+    uint32_t x = v[st];
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    if (lane == 0) red[st][wid] = v;
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+    if (lane == 0) red[st][wid] = x;
   }
   __syncthreads();
+  // the counters are staged in LDS and copied word by word by the whole block
+  // (a private copy would live in scratch memory: its queue arrays are indexed
+  // at run time)
+  constexpr uint32_t kWords = sizeof(Counters) / 4;
+  static_assert(sizeof(Counters) % 4 == 0 && kWords <= kBlock, "counters are copied one word per thread");
+  __shared__ Counters c;
+  if (threadIdx.x < kWords) reinterpret_cast<uint32_t *>(&c)[threadIdx.x] = reinterpret_cast<const uint32_t *>(cn)[threadIdx.x];
   if (threadIdx.x < kNumStat) {
     uint32_t v = 0;
 #pragma unroll
@@ -145,7 +160,6 @@ __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host,
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    Counters c = *cn;
     c.hits = sums[kStHits];
     c.fills = sums[kStFills];
     c.evictions = sums[kStEvictions];
@@ -165,7 +179,6 @@ __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host,
     // queue mode: candidates that found their queue full were dropped
     c.enqueued -= c.q_overflow;
     c.dropped += c.q_overflow;
-    *host = c;
     if (tail && !c.err) {  // a rejected gather leaves both tails alone
       tail[1] = tail[0];
       tail[0] += c.enq_total;
@@ -182,7 +195,11 @@ __global__ __launch_bounds__(kBlock) void k_finish(Counters *cn, Counters *host,
       qf.gate->q_before = cnt - c.q_placed[qf.next];
       qf.gate->q_stage_off = off;
     }
-    *cn = Counters{};
+  }
+  __syncthreads();
+  if (threadIdx.x < kWords) {
+    reinterpret_cast<uint32_t *>(host)[threadIdx.x] = reinterpret_cast<const uint32_t *>(&c)[threadIdx.x];
+    reinterpret_cast<uint32_t *>(cn)[threadIdx.x] = 0u;
   }
 }
 
