@@ -1180,16 +1180,14 @@ __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc
       refill = fd != 0;
       sc.oc[u] = oc;
       if (outcome) outcome[u] = oc;
+      // the hit copy's list is indexed by unique index (its destination row),
+      // so the copy writes the output rows in order
+      sc.hbm.src[u] = from_hbm ? (uint32_t)(code & kSrcIndex) : kNoRow;
     }
     const uint32_t ih = n_early + block_append(from_host, &sc.gate->n_host);
     if (from_host) {
       sc.host_list[ih] = u;
       sc.host_src[ih] = code;
-    }
-    const uint32_t ib = block_append(from_hbm, &sc.gate->n_hbm);
-    if (from_hbm) {
-      sc.hbm.src[ib] = (uint32_t)(code & kSrcIndex);
-      sc.hbm.dst[ib] = u;
     }
     const uint32_t ifl = block_append(refill, &sc.gate->n_fill);
     if (refill) {
@@ -1331,10 +1329,17 @@ constexpr int kUnroll = 4;
 // 5.7-6.0 against 4.9-5.2 TB/s for 1-2 KiB random rows.  The mode only names
 // the instance (hit copy, staging, fills) so that profiles tell them apart.
 constexpr int kListUnroll = 2;
+//
+// The hit copy's list (M = kHbmToOut) is dense by destination: entry i moves
+// to output row i, from row sidx[i] unless that is kNoRow (the unique ID's
+// row comes over the host link).  Writing the output rows in order measured
+// 6.0 TB/s against 5.2-5.4 for the same rows listed in per-block runs of
+// arbitrary order (600 K random 2 KiB rows from a 96 GiB region).
 template <CopyMode M, bool kPow2>
 __global__ __launch_bounds__(kBlock) void k_list_copy(const uint8_t *src, const uint32_t *sidx, uint8_t *dst,
                                                       const uint32_t *didx, const Gate *gate, const uint32_t *count,
                                                       uint64_t R, uint32_t nvec, uint32_t vshift) {
+  constexpr bool kDense = M == CopyMode::kHbmToOut;
   if (gate->err) return;
   const uint64_t total = (uint64_t)*count * nvec;
   constexpr uint64_t tile = (uint64_t)kListUnroll * kBlock;
@@ -1348,8 +1353,11 @@ __global__ __launch_bounds__(kBlock) void k_list_copy(const uint8_t *src, const 
       if (w < total) {
         const uint32_t i = kPow2 ? (uint32_t)(w >> vshift) : (uint32_t)(w / nvec);
         const uint64_t byte = (w - (uint64_t)i * nvec) * 16u;
-        v[k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(src + (uint64_t)sidx[i] * R + byte));
-        dp[k] = dst + (uint64_t)didx[i] * R + byte;
+        const uint32_t si = sidx[i];
+        if (!kDense || si != kNoRow) {
+          v[k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(src + (uint64_t)si * R + byte));
+          dp[k] = dst + (uint64_t)(kDense ? i : didx[i]) * R + byte;
+        }
       }
     }
 #pragma unroll
@@ -1465,7 +1473,7 @@ void launch_copy(CopyMode mode, const DevState &d, uint64_t n, const Scratch &sc
   }
   switch (mode) {
     case CopyMode::kHbmToOut:
-      launch_list<CopyMode::kHbmToOut>(d.rows, sc.hbm, out, sc.gate, &sc.gate->n_hbm, n, d.R, s);
+      launch_list<CopyMode::kHbmToOut>(d.rows, sc.hbm, out, sc.gate, &sc.gate->n_unique, n, d.R, s);
       break;
     case CopyMode::kCacheToStage:
       launch_list<CopyMode::kCacheToStage>(d.rows, sc.stage, sc.staging, sc.gate, &sc.gate->n_stage, n, d.R, s);

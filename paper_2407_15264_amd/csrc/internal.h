@@ -31,6 +31,9 @@ constexpr uint64_t kSrcHbm = 0ull << 62;    // cache slot in HBM
 constexpr uint64_t kSrcStore = 1ull << 62;  // backing-store row (pinned host)
 constexpr uint64_t kSrcRing = 2ull << 62;   // victim-ring row (pinned host)
 constexpr uint64_t kSrcIndex = (1ull << 62) - 1;
+// an HBM row index that names no row (the hit copy's list entry of a unique ID
+// whose row comes over the host link); cache create keeps the row count below it
+constexpr uint32_t kNoRow = 0xffffffffu;
 
 // One set = one 128-byte record (one L2 line): the 8 resident node IDs, their
 // static scores, the gather index at which each was inserted, and (round-robin
@@ -108,7 +111,6 @@ struct Gate {
   uint32_t err;
   uint32_t n_unique;
   uint32_t n_host;   // host-fetch list: entries after the first n_early (appended by the resolve)
-  uint32_t n_hbm;    // hit-copy list
   uint32_t n_fill;   // fill list
   uint32_t n_stage;  // staging list
   // queue mode, written by the gather's last metadata kernel for the prefetch
@@ -119,11 +121,12 @@ struct Gate {
   // host-fetch list entries [0, n_early): misses known from the batch-start
   // state, listed right after the dedup and fetched before the set walk ends
   uint32_t n_early;
-  uint32_t pad[2];
+  uint32_t pad[3];
 };
 
 // A row-copy list: entry i moves row src[i] of its source to row dst[i] of its
-// destination (dense, in arbitrary order).
+// destination (dense, in arbitrary order).  The hit copy's list is the
+// exception: one entry per unique ID, to output row i, dst unused.
 struct RowList {
   uint32_t *src;
   uint32_t *dst;
@@ -160,7 +163,7 @@ struct Scratch {
   Gate *gate;           // [1]
   uint32_t *host_list;  // host fetch: out rows whose rows come from pinned host memory
   uint64_t *host_src;   //   and the source code (kSrc*) of each
-  RowList hbm;          // hits and same-batch victim hits: cache slot -> out row
+  RowList hbm;          // hit copy, one entry per unique ID: source row (kNoRow: none) -> out row u
   RowList fill;         // final occupants: out row -> cache slot
   RowList stage;        // surviving enqueues: cache slot -> staging row
   uint8_t *staging;     // [min(max_batch, V)][R] evicted rows in ring order, for the ring write (in DevState::rows)

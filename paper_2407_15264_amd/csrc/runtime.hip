@@ -934,8 +934,8 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
   d.stage_row0 = S * lsm::kWays + (queues ? 2 * d.C : 0);
   d.stage_rows = V ? (B < V ? B : V) : 0;
   const uint64_t total_rows = d.stage_row0 + 2 * d.stage_rows;
-  // the row copies index these rows with 32 bits
-  if (total_rows > 0xffffffffull || total_rows > ~0ull / R) {
+  // the row copies index these rows with 32 bits (all ones: no row)
+  if (total_rows >= 0xffffffffull || total_rows > ~0ull / R) {
     delete c;
     return LSMGNN_E_INVAL;
   }
@@ -965,7 +965,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
     f.sc = sc;
     ok = ok && dev_alloc(c, &f.sc.gate, 1) &&
          (pageable || (dev_alloc(c, &f.sc.host_list, B) && dev_alloc(c, &f.sc.host_src, B))) &&
-         dev_alloc(c, &f.sc.hbm.src, B) && dev_alloc(c, &f.sc.hbm.dst, B) && dev_alloc(c, &f.sc.fill.src, B) &&
+         dev_alloc(c, &f.sc.hbm.src, B) && dev_alloc(c, &f.sc.fill.src, B) &&
          dev_alloc(c, &f.sc.fill.dst, B) && dev_alloc(c, &f.sc.stage.src, B) && dev_alloc(c, &f.sc.stage.dst, B) &&
          host_alloc(c, &f.hc, &f.hc_dev, sizeof(Counters), true);
     if (ok && V) f.sc.staging = d.rows + (d.stage_row0 + (uint64_t)(&f - c->fl) * d.stage_rows) * R;
