@@ -622,11 +622,14 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
   const bool prof = c->prof != 0;
   const bool queues = d.qmode && d.V && d.L > 0;  // per-iteration victim queues with prefetch
   // The host fetch's grid: 40 blocks when this cache has the link and the
-  // host's memory to itself; 32 when host threads also copy rows (a pageable
-  // store) or other caches' host fetches, ring writes and copies share the
-  // device (measured: one pinned cache gains 8-11 % from 40, several caches
-  // or a pageable store lose 2-5 %).
-  d.host_grid = (c->pageable || caches_on_device(c->device) > 1) ? 32u : 0u;
+  // host's memory to itself; 48 when its store is pageable (the GPU then reads
+  // contiguous bounce rows); 32 when other caches' host fetches, ring writes
+  // and copies share the device.  Measured: one pinned cache gains 8-11 % from
+  // 40 blocks over 32; several caches lose 2-5 % with 40; a pageable store on
+  // the 100M-node workload gives 487 GB/s with 32 blocks, 494 with 40, 498-500
+  // with 48, 502 with 56 and 444 with 64 (more reads in flight stall the hit
+  // copy beside them: 0.71 of the HBM peak with 32 blocks, 0.66 with 48).
+  d.host_grid = caches_on_device(c->device) > 1 ? 32u : c->pageable ? 48u : 0u;
   auto rec = [&](int e, hipStream_t st) {
     if (prof) (void)hipEventRecord(ps.e[e], st);
   };
