@@ -173,11 +173,14 @@ class _Lane:
 
     def __init__(self, store, static, num_sets, victim_rows, lookahead, batches, rows, store_gpu, label,
                  combined, near_threshold, device, row_sample=0, policy="hybrid", victim_mode="fifo",
-                 refresh_period=1):
+                 refresh_period=1, mixed_seed=None):
         import torch
         self.torch = torch
         self.store, self.row_sample = store, row_sample
         self.rng = np.random.default_rng(12345)
+        # mixed_seed: each gather goes through the blocking call (then a
+        # separate advance) or the pipelined one, by a seeded coin
+        self.mixed = None if mixed_seed is None else np.random.default_rng(mixed_seed)
         dev = torch.device("cuda", device)
         self.mb = max(1, max(len(b) for b in batches))
         self.L, self.batches, self.rows, self.store_gpu, self.label = lookahead, batches, rows, store_gpu, label
@@ -210,6 +213,12 @@ class _Lane:
         out, uq, inv, oc = self.bufs[b % 3]
         L = self.L
         nxt = self.db[b + L + 1] if b + L + 1 < len(self.batches) else None
+        if self.mixed is not None and self.mixed.random() < 0.5:
+            r = self.cache.gather(self.db[b], out=out, unique=uq, inverse=inv, outcome=oc)
+            if nxt is not None:
+                self.cache.advance(nxt)
+            self.pending.append((None, r, b))
+            return
         if self.combined:
             ticket, r = self.cache.gather_async(self.db[b], out, uq, inverse=inv, outcome=oc, announce=nxt)
         else:
@@ -221,7 +230,8 @@ class _Lane:
     def check_oldest(self):
         torch = self.torch
         ticket, r, b = self.pending.pop(0)
-        self.cache.wait(ticket)
+        if ticket is not None:  # a blocking gather has completed already
+            self.cache.wait(ticket)
         torch.cuda.current_stream().synchronize()
         where = f"{self.label} gather {b}"
         rows = self.rows
@@ -303,6 +313,19 @@ def run_async_parity(store: Store, static, num_sets, victim_rows, lookahead, bat
     `state_every` gathers and at the end."""
     ln = _Lane(store, static, num_sets, victim_rows, lookahead, batches, rows, store_gpu, label, combined,
                near_threshold, device, row_sample, policy, victim_mode, refresh_period)
+    totals, seconds = _run_lanes([ln], len(batches), state_every, label)
+    return dict(total=totals[0], seconds=seconds)
+
+
+def run_mixed_parity(store: Store, static, num_sets, victim_rows, lookahead, batches, seed, state_every=0,
+                     label="mixed", near_threshold=0, policy="hybrid", victim_mode="fifo", refresh_period=1):
+    """Blocking and pipelined gathers interleaved on one cache (a seeded coin
+    per gather), with no call in between that waits for the library's
+    streams except the checks' own waits: every gather's unique IDs, inverse,
+    outcomes and rows, the counters as totals, the state every `state_every`
+    gathers and at the end."""
+    ln = _Lane(store, static, num_sets, victim_rows, lookahead, batches, "all", None, label, True, near_threshold,
+               0, 0, policy, victim_mode, refresh_period, mixed_seed=seed)
     totals, seconds = _run_lanes([ln], len(batches), state_every, label)
     return dict(total=totals[0], seconds=seconds)
 

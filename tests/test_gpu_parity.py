@@ -21,7 +21,7 @@ torch = pytest.importorskip("torch")
 from paper_2407_15264_amd import lsmgnn  # noqa: E402
 from paper_2407_15264_amd import workload as W  # noqa: E402
 from tests.parity_driver import (Store, compare_state, config_stream, device_store, log,  # noqa: E402
-                                 run_async_parity, run_parity, run_typed_async_parity)
+                                 run_async_parity, run_mixed_parity, run_parity, run_typed_async_parity)
 from oracle.oracle import Oracle  # noqa: E402
 
 
@@ -525,6 +525,34 @@ def test_blocking_gathers_back_to_back(seed):
     store = Store.random_bytes(n, 32, seed, pinned=seed % 2 == 0)
     run_parity(store, stat, S, V, L, batches, near_threshold=T, rows="all", label=f"blocking{seed}",
                victim_mode=mode, per_gather_stats=False)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_blocking_and_pipelined_gathers_interleaved(seed):
+    """The two entry points alternate by a seeded coin on one cache: a blocking
+    gather's fills run on the host-link stream, a pipelined gather's on the
+    dma stream, and each gather's ring write must still follow its own host
+    fetch.  Odd seeds use a pageable store, every fourth the victim queues,
+    every third an update period of 2."""
+    n, S, V, L, T, stat, batches = _long_case(300 + seed)
+    mode = "queues" if seed % 4 == 3 else "fifo"
+    if mode == "queues":
+        V = max(V, 1) * (L + 1)
+    U = 2 if seed % 3 == 2 else 1
+    log(f"case: interleaved seed {seed} {mode} U={U}: N={n} S={S} V={V} L={L} T={T}")
+    store = Store.random_bytes(n, 32, seed, pinned=seed % 2 == 0)
+    run_mixed_parity(store, stat, S, V, L, batches, seed, state_every=15, label=f"interleaved{seed}",
+                     near_threshold=T, victim_mode=mode, refresh_period=U)
+
+
+def test_blocking_and_pipelined_gathers_interleaved_rmat14():
+    cfg = W.CONFIGS[W.RMAT14]
+    log(f"case: {cfg.name}, blocking and pipelined gathers interleaved")
+    wl, batches = config_stream(cfg)
+    store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed)
+    res = run_mixed_parity(store, wl.static, cfg.cache.num_sets, cfg.cache.victim_rows, cfg.cache.lookahead,
+                           batches, 14, state_every=5, label=f"{cfg.name}-interleaved")
+    assert res["total"]["victim_hits"] > 0
 
 
 def test_blocking_gathers_back_to_back_rmat14():
