@@ -1587,7 +1587,7 @@ void launch_copy_plain(const void *src, void *dst, uint64_t bytes, bool device_t
 // node's window word changes in this kernel (duplicates write the same value),
 // so a plain read-modify-write is exact.
 __global__ void k_window_set(const int64_t *ids, uint32_t n, uint64_t N, uint32_t bit, uint32_t *mask,
-                             int64_t *slot_ids, int record, Counters *cn) {
+                             int64_t *slot_ids, int record, uint32_t *err) {
   bool bad = false;
   const uint32_t b = 1u << bit;
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
@@ -1600,7 +1600,7 @@ __global__ void k_window_set(const int64_t *ids, uint32_t n, uint64_t N, uint32_
       if (!(m & b)) mask[x] = m | b;
     }
   }
-  if (__ballot(bad) && __lane_id() == 0) atomicOr(&cn->err, 1u);
+  if (__ballot(bad) && __lane_id() == 0) *err = 1u;  // every writer stores the same value
 }
 
 // After a rejected announcement (the host launches it only then): clear the
@@ -1617,10 +1617,10 @@ __global__ void k_window_rollback(const int64_t *ids, uint32_t n, uint64_t N, ui
 }
 
 void launch_window_set(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
-                       bool record, Counters *cn, hipStream_t s) {
+                       bool record, uint32_t *err, hipStream_t s) {
   const unsigned g = grid_for(n, kBlock, kMaxGrid);
   hipLaunchKernelGGL(k_window_set, dim3(g), dim3(kBlock), 0, s, ids, (uint32_t)n, N, bit, mask, slot_ids,
-                     record ? 1 : 0, cn);
+                     record ? 1 : 0, err);
 }
 
 void launch_window_rollback(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask,

@@ -265,7 +265,7 @@ void launch_expand(const uint8_t *rows, const int64_t *inv, uint64_t n, uint64_t
 // n bounds the gather's unique count (the copies read the exact one from the gate)
 void launch_copy(CopyMode mode, const DevState &d, uint64_t n, const Scratch &sc, uint8_t *out, hipStream_t s);
 void launch_window_set(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask, int64_t *slot_ids,
-                       bool record, Counters *cn, hipStream_t s);
+                       bool record, uint32_t *err, hipStream_t s);
 void launch_window_rollback(const int64_t *ids, uint64_t n, uint64_t N, uint32_t bit, uint32_t *mask,
                             hipStream_t s);
 void launch_copy_plain(const void *src, void *dst, uint64_t bytes, bool device_to_device, hipStream_t s);

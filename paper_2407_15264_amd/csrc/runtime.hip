@@ -195,8 +195,8 @@ struct lsmgnn_cache {
   int64_t win_batch[kMaxSlots];
   uint64_t win_len[kMaxSlots];
   Counters *cn = nullptr;      // counters of the metadata kernels (meta stream only)
-  Counters *cn_adv = nullptr;  // counters of announcements
-  Counters *hc_adv = nullptr, *hc_adv_dev = nullptr;
+  // a separate announcement's error flag (pinned), set by the window kernel
+  uint32_t *adv_err = nullptr, *adv_err_dev = nullptr;
   DedupResult *dd = nullptr, *dd_dev = nullptr;
   Flight fl[2];
   PerfSet ps[kPerfSets];
@@ -953,7 +953,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
             (!queues || (dev_alloc(c, &d.qcount, (uint64_t)d.L + 1) &&
                          dev_alloc(c, &sc.qpart, (uint64_t)lsm::kMaxQueues * (B / lsm::kBlock + 1)))) &&
             dev_alloc(c, &c->win_ids, (uint64_t)(d.L + 1) * B) && dev_alloc(c, &c->cn, 1) &&
-            dev_alloc(c, &c->cn_adv, 1) && dev_alloc(c, &sc.uniq, B) && dev_alloc(c, &sc.uset, B) &&
+            dev_alloc(c, &sc.uniq, B) && dev_alloc(c, &sc.uset, B) &&
             dev_alloc(c, &sc.arrival, B) && dev_alloc(c, &sc.touched, B) && dev_alloc(c, &sc.seg_off, B) &&
             dev_alloc(c, &sc.seg, B) && dev_alloc(c, &sc.seg_u, B) && dev_alloc(c, &sc.seg_x, B) &&
             dev_alloc(c, &sc.seg_st, B) && dev_alloc(c, &sc.big, B / (lsm::kSmallSet + 1) + 1) && dev_alloc(c, &sc.kind, B) && dev_alloc(c, &sc.flags, B) &&
@@ -963,7 +963,7 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
             dev_alloc(c, &sc.this_enq, B) && dev_alloc(c, &sc.slot, B) && dev_alloc(c, &sc.fill_dst, B) &&
             dev_alloc(c, &sc.stat_part, (uint64_t)lsm::kNumStat * lsm::kMaxGrid) &&
             host_alloc(c, &c->dd, &c->dd_dev, sizeof(DedupResult), true) &&
-            host_alloc(c, &c->hc_adv, &c->hc_adv_dev, sizeof(Counters), true);
+            host_alloc(c, &c->adv_err, &c->adv_err_dev, sizeof(uint32_t), true);
   for (Flight &f : c->fl) {
     f.sc = sc;
     ok = ok && dev_alloc(c, &f.sc.gate, 1) &&
@@ -1017,7 +1017,6 @@ lsmgnn_status lsmgnn_cache_create(const lsmgnn_config *cfg, lsmgnn_cache **out) 
        hipMemset(d.mask, 0, N * 4) == hipSuccess && hipMemset(d.present, 0, map_bytes) == hipSuccess &&
        hipMemset(d.set_count, 0, S * 4) == hipSuccess && hipMemset(d.tail, 0, 16) == hipSuccess &&
        hipMemset(c->cn, 0, sizeof(Counters)) == hipSuccess &&
-       hipMemset(c->cn_adv, 0, sizeof(Counters)) == hipSuccess &&
        hipMemcpy(d.stat, cfg->static_score, N * 4, hipMemcpyHostToDevice) == hipSuccess &&
        (V == 0 || (hipMemset(d.vpos, 0, N * 8) == hipSuccess && hipMemset(d.ring_tag, 0xff, V * 4) == hipSuccess)) &&
        (!queues || hipMemset(d.qcount, 0, ((uint64_t)d.L + 1) * 4) == hipSuccess) &&
@@ -1058,16 +1057,15 @@ lsmgnn_status lsmgnn_advance(lsmgnn_cache *c, const int64_t *ids, uint64_t n, vo
   const int slot = (int)(j % (c->d.L + 1));
   if (!after_caller(c, s)) return fail_device(c);
   const uint32_t bit = (uint32_t)(j & 31u);
+  volatile uint32_t *err = c->adv_err;  // the window kernel sets it on an out-of-range ID
+  *err = 0u;
   if (n)
     lsm::launch_window_set(ids, n, c->d.N, bit, c->d.mask, c->win_ids + (uint64_t)slot * c->max_batch, record,
-                           c->cn_adv, c->meta);
-  lsm::launch_finish(c->cn_adv, c->hc_adv_dev, c->fl[0].sc.stat_part, lsm::StatGrids{}, nullptr, lsm::QueueFinish{},
-                     lsm::AnnounceArgs{},
-                     c->meta);
+                           c->adv_err_dev, c->meta);
   if (hipEventRecord(c->ev_adv, c->meta) != hipSuccess || hipGetLastError() != hipSuccess ||
       hipEventSynchronize(c->ev_adv) != hipSuccess)
     return fail_device(c);
-  if (c->hc_adv->err) {
+  if (*err) {
     // the valid IDs of a recorded list had their bit set: clear it again
     if (record) {
       lsm::launch_window_rollback(ids, n, c->d.N, bit, c->d.mask, c->meta);
