@@ -1074,9 +1074,10 @@ void launch_early(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, Counte
 }
 
 // Victim-ring probe of every fill and the row source of every unique ID.  Builds
-// the gather's row-copy lists (dense, in arbitrary order): the host fetch (rows
-// from pinned host memory), the hit copy (rows from cache slots) and the fills
-// (each way's final occupant).
+// the gather's row-copy lists: the rest of the host fetch's (rows from pinned
+// host memory, after the early misses; dense, in arbitrary order), the hit
+// copy's (one entry per unique ID: its HBM row, or none) and the fills' (each
+// way's final occupant; dense, in arbitrary order).
 __global__ __launch_bounds__(kBlock) void k_resolve(const DevState d, Scratch sc, uint64_t t, uint8_t *outcome,
                                                     Counters *cn) {
   if (cn->err) return;
