@@ -305,11 +305,12 @@ __global__ __launch_bounds__(kBlock) void k_chunk_scan(uint32_t *chunk_sums, uin
 // next unique index.  kFused: the chunk's first index is the sum of the
 // earlier chunks' counts, added up by the block itself (few chunks: this
 // saves the separate one-block scan), and the last chunk's block publishes
-// the unique count; otherwise chunk_off holds the scanned offsets.
+// the unique count; otherwise chunk_off holds the scanned offsets.  Each
+// node's own unique index is written later (k_unique_index).
 template <bool kFused>
-__global__ __launch_bounds__(kBlock) void k_compact(uint8_t *present, const uint32_t *chunk_off, uint32_t *uidx,
-                                                    uint32_t *uniq, int64_t *uniq_out, Counters *cn,
-                                                    uint32_t nchunks, DedupResult *dd, Gate *gate) {
+__global__ __launch_bounds__(kBlock) void k_compact(uint8_t *present, const uint32_t *chunk_off, uint32_t *uniq,
+                                                    int64_t *uniq_out, Counters *cn, uint32_t nchunks,
+                                                    DedupResult *dd, Gate *gate) {
   uint32_t w[kWordsPerThread];
   load_words(present, w);
   const size_t b0 = ((size_t)blockIdx.x * kBlock + threadIdx.x) * kBytesPerThread;  // first byte of this thread
@@ -352,7 +353,6 @@ __global__ __launch_bounds__(kBlock) void k_compact(uint8_t *present, const uint
       const uint32_t x = (uint32_t)(b0 + 4 * k + (__builtin_ctz(word) >> 3));
       uniq[pos] = x;
       uniq_out[pos] = (int64_t)x;
-      uidx[x] = pos;
       ++pos;
       word &= word - 1u;
     }
@@ -372,13 +372,28 @@ void launch_dedup(const DevState &d, const int64_t *ids, uint64_t n, const int64
   hipLaunchKernelGGL(k_chunk_popc, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.present, d.chunk_sums, cn);
   if (d.nchunks <= kFusedScanMax) {
     hipLaunchKernelGGL(k_compact<true>, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.present, d.chunk_sums,
-                       d.uidx, sc.uniq, unique_out, cn, (uint32_t)d.nchunks, dd, sc.gate);
+                       sc.uniq, unique_out, cn, (uint32_t)d.nchunks, dd, sc.gate);
   } else {
     hipLaunchKernelGGL(k_chunk_scan, dim3(1), dim3(kBlock), 0, s, d.chunk_sums, (uint32_t)d.nchunks, cn, dd,
                        sc.gate);
     hipLaunchKernelGGL(k_compact<false>, dim3((unsigned)d.nchunks), dim3(kBlock), 0, s, d.present, d.chunk_sums,
-                       d.uidx, sc.uniq, unique_out, cn, (uint32_t)d.nchunks, dd, sc.gate);
+                       sc.uniq, unique_out, cn, (uint32_t)d.nchunks, dd, sc.gate);
   }
+}
+
+// Each unique ID's index, uidx[uniq[u]] = u, read by the inverse index and the
+// per-request counts.  Kept out of the compaction: these scattered 4-byte
+// writes (one per unique ID over an N-entry array) cost the compaction most
+// of its time beside the host-link reads, and the early-miss list, which
+// needs only the unique list, need not wait for them.
+__global__ __launch_bounds__(kBlock) void k_unique_index(const uint32_t *uniq, uint32_t *uidx, const Counters *cn) {
+  if (cn->err) return;
+  const uint32_t U = cn->n_unique;
+  for (uint32_t u = blockIdx.x * kBlock + threadIdx.x; u < U; u += gridDim.x * kBlock) uidx[uniq[u]] = u;
+}
+
+void launch_unique_index(const DevState &d, uint64_t n, const Scratch &sc, const Counters *cn, hipStream_t s) {
+  hipLaunchKernelGGL(k_unique_index, dim3(grid_for(n, kBlock, kMaxGrid)), dim3(kBlock), 0, s, sc.uniq, d.uidx, cn);
 }
 
 // ------------------------------------------------------------ group by set

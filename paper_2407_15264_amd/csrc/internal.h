@@ -276,6 +276,8 @@ void launch_publish_count(const Gate *gate, const uint32_t *count, uint32_t *dst
 // as the first entries of the host-fetch list
 void launch_early(const DevState &d, uint64_t n, uint64_t t, Scratch &sc, Counters *cn, StatGrids &grids,
                   hipStream_t s);
+// uidx[uniq[u]] = u for the gather's unique IDs (n bounds their count)
+void launch_unique_index(const DevState &d, uint64_t n, const Scratch &sc, const Counters *cn, hipStream_t s);
 
 // host twin of the device set-index function
 uint64_t set_of_host(uint64_t x, uint64_t num_sets);

@@ -691,6 +691,7 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
     if (c->pageable) lsm::launch_publish_count(f.sc.gate, &f.sc.gate->n_early, f.hcount_dev, c->meta);
     (void)hipEventRecord(f.early_done, c->meta);
     if (!c->pageable) host_fetch_early();
+    lsm::launch_unique_index(d, n, f.sc, c->cn, c->meta);
     if (refresh) lsm::launch_refresh(d, (uint32_t)t, c->cn, c->meta);
     lsm::launch_group_by_set(d, ids, n, inverse, f.sc, c->cn, c->meta);
     lsm::launch_set_walk(d, n, (uint32_t)t, f.sc, c->cn, grids, c->meta);
