@@ -1456,8 +1456,10 @@ __global__ __launch_bounds__(kBlock) void k_host_fetch(const DevState d, Scratch
 // hit copy, the fills, the ring write), so the host fetch keeps only about
 // 640 KB in flight (40 blocks x 256 lanes x 4 x 16 B): enough to cover the
 // link's latency, not more.  A sweep of block counts and unroll depths on
-// the full pipeline chose it.  The runtime may ask for fewer blocks
-// (DevState::host_grid) when more traffic shares the host or the link.
+// the full pipeline chose it.  The runtime picks another grid per gather
+// (DevState::host_grid): fewer blocks when more traffic shares the host or
+// the link, more when the fetch reads a pageable store's contiguous bounce
+// rows.
 #ifndef LSM_HOST_GRID
 #define LSM_HOST_GRID 40
 #endif
