@@ -25,18 +25,20 @@ torch = pytest.importorskip("torch")
 
 from paper_2407_15264_amd import lsmgnn  # noqa: E402
 from paper_2407_15264_amd import workload as W  # noqa: E402
-from tests.parity_driver import Store, log, run_async_parity  # noqa: E402
+from tests.parity_driver import Store, log, run_async_parity, run_mixed_parity  # noqa: E402
 
 PREFIX = 150
+MIXED = 100  # minibatches of the interleaved case
 
 
-@pytest.mark.timeout(900)
-def test_rmat100m_full_size_pipelined_prefix():
+@pytest.fixture(scope="module")
+def rmat100m():
+    """The workload's first PREFIX minibatches, its static scores and its store
+    (built once for both cases)."""
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     lsmgnn.lib()
     cfg = W.CONFIGS[W.RMAT100M]
-    log(f"case: {cfg.name}, first {PREFIX} minibatches, pipelined, full size, pageable store, all rows")
     t0 = time.time()
     wl = W.Workload(cfg, PREFIX)
     static = wl.static
@@ -45,9 +47,32 @@ def test_rmat100m_full_size_pipelined_prefix():
     log(f"  workload generated in {time.time() - t0:.1f} s (max batch {max(b.size for b in batches)})")
     store = Store(cfg.num_nodes, cfg.dim, cfg.elt_bytes, cfg.seed, pinned=False)
     log(f"  store filled ({time.time() - t0:.1f} s)")
+    return cfg, static, batches, store
+
+
+@pytest.mark.timeout(900)
+def test_rmat100m_full_size_pipelined_prefix(rmat100m):
+    cfg, static, batches, store = rmat100m
+    log(f"case: {cfg.name}, first {PREFIX} minibatches, pipelined, full size, pageable store, all rows")
     sh = cfg.cache
     res = run_async_parity(store, static, sh.num_sets, sh.victim_rows, sh.lookahead, batches, rows="all",
                            state_every=25, label=cfg.name)
     tot = res["total"]
     log(f"  {cfg.name}: {tot} in {res['seconds']:.1f} s")
     assert tot["hits"] > 0 and tot["victim_hits"] > 0 and tot["misses"] > 0
+
+
+@pytest.mark.timeout(900)
+def test_rmat100m_full_size_interleaved_prefix(rmat100m):
+    """The same shape with blocking and pipelined gathers interleaved by a
+    seeded coin over the first MIXED minibatches: a blocking gather's fills
+    follow its own host fetch on the host-link stream, a pipelined gather's
+    the previous ring write on the dma stream."""
+    cfg, static, batches, store = rmat100m
+    log(f"case: {cfg.name}, first {MIXED} minibatches, blocking and pipelined interleaved, full size, all rows")
+    sh = cfg.cache
+    res = run_mixed_parity(store, static, sh.num_sets, sh.victim_rows, sh.lookahead, batches[:MIXED], 100,
+                           state_every=25, label=f"{cfg.name}-interleaved")
+    tot = res["total"]
+    log(f"  {cfg.name} interleaved: {tot} in {res['seconds']:.1f} s")
+    assert tot["hits"] > 0 and tot["misses"] > 0
