@@ -9,11 +9,14 @@ rows of misses and victim hits into its pinned bounce buffers; everything else
 is the configured shape.
 
 The first PREFIX minibatches of the stream run in the benchmark's launch
-configuration (pipelined gathers with the announcement, two in flight).  The
-cold cache fills after about 75 of them, so the prefix covers the steady state
-too.  Every gather: unique IDs, inverse, per-ID outcomes and every gathered row
-against the oracle (bit-exact); every 25 gathers and at the end: every cache
-tag, every ring tag, the ring tail; at the end: all counters.
+configuration (pipelined gathers with the announcement, two in flight): the
+cold start, then evictions, victim-buffer entries and victim hits (the 96 GiB
+cache keeps filling for hundreds of minibatches; set conflicts evict from the
+first ones on).  Every gather: unique IDs, inverse, per-ID outcomes and every
+gathered row against the oracle (bit-exact); every 25 gathers and at the end:
+every cache tag, every ring tag, the ring tail; at the end: all counters.  A
+second case interleaves the blocking and the pipelined entry points over the
+first MIXED minibatches.
 """
 import time
 
