@@ -244,9 +244,10 @@ def _cpu_model():
 
 
 def steady_start(cfg, L):
-    """First minibatch of the steady state: after max(L+1, 10 %) of the
-    configured run, once the cold cache has filled (before it nearly every
-    request misses)."""
+    """First timed minibatch: after max(L+1, 10 %) of the configured run, past
+    the cold start (at first nearly every request misses).  A cache much
+    larger than a minibatch keeps filling after that, and its hit rate keeps
+    rising over the run."""
     return max(L + 1, -(-cfg.batches // 10))
 
 
