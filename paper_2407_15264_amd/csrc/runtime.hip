@@ -392,8 +392,9 @@ void issue_dma(lsmgnn_cache *c, Flight &f, hipEvent_t after = nullptr) {
   const bool prof = p.pending && p.t == f.t;
   (void)hipStreamWaitEvent(c->dma, f.stage_done, 0);
   // the gather's own host fetch may read ring rows this write overwrites
-  // (victim hits on older entries in slots its enqueues take)
-  (void)hipStreamWaitEvent(c->dma, f.host_done, 0);
+  // (victim hits on older entries in slots its enqueues take); a blocking
+  // gather's fills follow its host fetch on the host-link stream
+  (void)hipStreamWaitEvent(c->dma, f.fill_host ? f.data_done : f.host_done, 0);
   if (after) (void)hipStreamWaitEvent(c->dma, after, 0);
   if (prof) (void)hipEventRecord(p.e[kEvEnq0], c->dma);
   if (c->d.qmode) {
@@ -668,7 +669,9 @@ lsmgnn_status issue_gather(lsmgnn_cache *c, const int64_t *ids, uint64_t n, cons
     rec(kEvHostLate, c->host);
     if (n) lsm::launch_copy(CopyMode::kHostToOut, d, n, f.sc, outp, c->host);
     rec(kEvHost1, c->host);
-    (void)hipEventRecord(f.host_done, c->host);
+    // a blocking gather's fills follow on this stream, and its ring write
+    // waits for them instead: one packet fewer between the fetch and the fills
+    if (!blocking) (void)hipEventRecord(f.host_done, c->host);
   };
 
   rec(kEvAll0, c->meta);
